@@ -1,0 +1,438 @@
+"""Pins of the fp64 oracle against things other than itself (CPU only).
+
+Each test names the passage of the paper it checks.  The pins are chosen so a
+plausible slip in the oracle -- a wrong sign in the propagation shift, a
+dropped jump or direction, rows and columns swapped, the random-search window
+centred on the wrong point, a wrong distance schedule, a reversed tie rule,
+a window clamped instead of cropped, a missing scale -- fails at least one.
+"""
+import json
+import math
+import os
+import subprocess
+import tempfile
+
+import numpy as np
+import pytest
+from scipy import stats
+
+import oracle
+import oracle.dense as dense
+import scram_inputs as si
+from scram_inputs.synth import resized
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+ROCRAND_INC = "/opt/rocm/include"
+
+
+# --------------------------------------------------------------------------
+# helpers
+# --------------------------------------------------------------------------
+def unit_keys(rng, S, H, W, d):
+    k = rng.standard_normal((S, H, W, d))
+    return k / np.linalg.norm(k, axis=3, keepdims=True)
+
+
+def dilate(hits, H, W):
+    """One step of S_t = (S_{t-1} + M) within the grid, M = {0, +-j e_row, +-j e_col : j in 8,4,2,1}."""
+    out = hits.copy()
+    for j in (8, 4, 2, 1):
+        out[j:, :] |= hits[:-j, :] if j < H else False
+        out[:-j, :] |= hits[j:, :] if j < H else False
+        out[:, j:] |= hits[:, :-j] if j < W else False
+        out[:, :-j] |= hits[:, j:] if j < W else False
+    return out
+
+
+@pytest.fixture(scope="module")
+def rocrand_philox(tmp_path_factory):
+    """rocRAND's Philox4x32-10 block function, built for the host with g++."""
+    hdr = os.path.join(ROCRAND_INC, "rocrand", "rocrand_philox4x32_10.h")
+    if not os.path.exists(hdr):
+        pytest.skip("rocRAND headers not present")
+    d = tmp_path_factory.mktemp("rocrand")
+    src = d / "p.cpp"
+    src.write_text(
+        "#include <rocrand/rocrand_philox4x32_10.h>\n#include <cstdio>\n"
+        "struct P : rocrand_device::philox4x32_10_engine { uint4 f(uint4 c, uint2 k){ return ten_rounds(c,k);} };\n"
+        "int main(){ P e; unsigned a,b,c,dd,k0,k1; while(scanf(\"%u %u %u %u %u %u\",&a,&b,&c,&dd,&k0,&k1)==6){"
+        " uint4 r=e.f(uint4{a,b,c,dd}, uint2{k0,k1}); printf(\"%u %u %u %u\\n\",r.x,r.y,r.z,r.w);} }\n")
+    exe = d / "p"
+    subprocess.run(["g++", "-O1", "-I" + ROCRAND_INC, "-D__HIP_PLATFORM_AMD__", str(src), "-o", str(exe)],
+                   check=True, capture_output=True)
+
+    def run(rows):
+        inp = "\n".join(" ".join(str(int(x)) for x in r) for r in rows) + "\n"
+        out = subprocess.run([str(exe)], input=inp, capture_output=True, text=True, check=True).stdout
+        return np.array([[int(x) for x in line.split()] for line in out.strip().splitlines()], dtype=np.uint64)
+
+    return run
+
+
+# --------------------------------------------------------------------------
+# random numbers: Philox4x32-10 against a library implementation
+# --------------------------------------------------------------------------
+def test_philox_matches_library(rocrand_philox):
+    rng = np.random.default_rng(7)
+    rows = [[0, 0, 0, 0, 0, 0], [0xFFFFFFFF] * 6, [1, 2, 3, 4, 5, 6]]
+    rows += rng.integers(0, 2 ** 32, size=(61, 6), dtype=np.uint64).tolist()
+    ref = rocrand_philox(rows)
+    mine = np.array([oracle.philox4x32_10(r[:4], r[4:]) for r in rows], dtype=np.uint64)
+    np.testing.assert_array_equal(mine, ref)
+
+
+def test_init_is_the_stated_map_of_library_words(rocrand_philox):
+    """Alg. 1 initialisation: u, v uniform over the key grid from counter (g, 0, 0, 0)."""
+    S, Hq, Wq, Hk, Wk, d = 2, 5, 7, 11, 13, 4
+    rng = np.random.default_rng(1)
+    Q = rng.standard_normal((S, Hq, Wq, d))
+    K = rng.standard_normal((S, Hk, Wk, d))
+    seed = 0x1234567890ABCDEF
+    J0, s0 = oracle.pm_init(Q, K, seed)
+    n = S * Hq * Wq
+    words = rocrand_philox([[g, 0, 0, 0, seed & 0xFFFFFFFF, seed >> 32] for g in range(n)])
+    u = (words[:, 0] * np.uint64(Hk)) >> np.uint64(32)
+    v = (words[:, 1] * np.uint64(Wk)) >> np.uint64(32)
+    np.testing.assert_array_equal(J0.reshape(-1), (u * np.uint64(Wk) + v).astype(np.int64))
+    kf = K.reshape(S, Hk * Wk, d)
+    exp = np.einsum("sid,sid->si", Q.reshape(S, -1, d), kf[np.arange(S)[:, None], J0.reshape(S, -1)])
+    np.testing.assert_allclose(s0.reshape(S, -1), exp, rtol=1e-13, atol=1e-13)
+
+
+def test_random_search_draws_are_the_stated_map_of_library_words(rocrand_philox):
+    """Random search step k of iteration t: counter (g, t, k div 2, 0), words 2(k mod 2), 2(k mod 2)+1."""
+    rng = np.random.default_rng(3)
+    S, H, W, d = 1, 9, 12, 3
+    Q = rng.standard_normal((S, H, W, d))
+    K = rng.standard_normal((S, H, W, d))
+    J = rng.integers(0, H * W, (S, H, W)).astype(np.int32)
+    seed, t = 99, 3
+    for g in (0, 17, 50, 107):
+        idx, kind, win, _ = oracle.pm_trace(Q, K, J, t, seed, g, flags=oracle.NO_PROPAGATION)
+        rs = kind >= 100
+        for (c, k, w) in zip(idx[rs], kind[rs] - 100, win[rs]):
+            wd = rocrand_philox([[g, t, k // 2, 0, seed, 0]])[0]
+            wr, wc = int(wd[2 * (k % 2)]), int(wd[2 * (k % 2) + 1])
+            lo_r, hi_r, lo_c, hi_c = (int(x) for x in w)
+            r = lo_r + ((wr * (hi_r - lo_r + 1)) >> 32)
+            cc = lo_c + ((wc * (hi_c - lo_c + 1)) >> 32)
+            assert c == r * W + cc
+
+
+def test_init_uniform_over_key_grid():
+    """Initialisation draws (u, v) uniformly with 0 <= u < Hk, 0 <= v < Wk (non-square key grid)."""
+    S, Hq, Wq, Hk, Wk = 64, 16, 16, 5, 7
+    Q = np.zeros((S, Hq, Wq, 1))
+    K = np.zeros((S, Hk, Wk, 1))
+    J0, _ = oracle.pm_init(Q, K, 2024)
+    assert J0.min() >= 0 and J0.max() < Hk * Wk
+    u, v = J0 // Wk, J0 % Wk
+    for vals, m in ((u, Hk), (v, Wk)):
+        counts = np.bincount(vals.reshape(-1), minlength=m)
+        assert stats.chisquare(counts).pvalue > 1e-3
+    counts = np.bincount(J0.reshape(-1), minlength=Hk * Wk)
+    assert stats.chisquare(counts).pvalue > 1e-3
+    # different seeds give different fields
+    J1, _ = oracle.pm_init(Q, K, 2025)
+    assert (J0 != J1).mean() > 0.9
+
+
+# --------------------------------------------------------------------------
+# propagation: closed form and a hand-worked example
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("H,W,seed_px", [(24, 20, (3, 17)), (24, 20, (12, 9)), (1, 40, (0, 5)), (40, 1, (30, 0))])
+def test_propagation_closed_form(H, W, seed_px):
+    """Identity field Q = K: an exact hit spreads to p - o for every offset o = jump * delta per sweep.
+
+    J0 = p + tau' (mod grid) everywhere except one seed pixel with J0 = itself,
+    random search off.  The exact-hit set after t Jacobi sweeps is the seed
+    dilated t times by {0, +-8, +-4, +-2, +-1 along each axis} (Alg. 1,
+    propagation step; Section 4.1 assumption (1)).
+    """
+    rng = np.random.default_rng(11)
+    d = 16
+    K = unit_keys(rng, 1, H, W, d)
+    Q = K.copy()
+    xs, ys = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    J = (((xs + 5) % H) * W + (ys + 3) % W).astype(np.int32)
+    if H == 1:
+        J = (xs * W + (ys + 3) % W).astype(np.int32)
+    if W == 1:
+        J = (((xs + 5) % H) * W + ys).astype(np.int32)
+    sx, sy = seed_px
+    J[sx, sy] = sx * W + sy
+    ident = (xs * W + ys)
+    hits = (J == ident)
+    assert hits.sum() == 1
+    Jt = J[None].copy()
+    for t in range(1, 5):
+        Jt, _, _, _ = oracle.pm_iteration(Q, K, Jt, t, seed=5, flags=oracle.NO_RANDOM_SEARCH)
+        hits = dilate(hits, H, W)
+        np.testing.assert_array_equal(Jt[0] == ident, hits)
+
+
+def test_propagation_hand_example():
+    g = json.load(open(os.path.join(GOLDEN, "propagation_hand.json")))
+    K = np.array(g["k"], np.float64).reshape(1, g["Hk"], g["Wk"], g["d"])
+    Q = K.copy()
+    J = np.array(g["J0"], np.int32).reshape(1, g["Hq"], g["Wq"])
+    for t in (1, 2):
+        J, _, _, _ = oracle.pm_iteration(Q, K, J, t, seed=0, flags=oracle.NO_RANDOM_SEARCH)
+        assert J.reshape(-1).tolist() == g["expected"][str(t)]
+
+
+# --------------------------------------------------------------------------
+# random search: geometry, uniformity, convergence to the exact argmax
+# --------------------------------------------------------------------------
+def test_random_search_window_schedule_and_centre():
+    """Distances R, R/2, ..., 1 (integer halving); each window is clipped and centred on the running best."""
+    rng = np.random.default_rng(5)
+    S, Hq, Wq, Hk, Wk, d = 1, 12, 10, 23, 37, 8    # R = 37: 37, 18, 9, 4, 2, 1
+    Q = rng.standard_normal((S, Hq, Wq, d))
+    K = rng.standard_normal((S, Hk, Wk, d))
+    J = rng.integers(0, Hk * Wk, (S, Hq, Wq)).astype(np.int32)
+    Kf = K.reshape(-1, d)
+    for g in range(0, Hq * Wq, 7):
+        idx, kind, win, final = oracle.pm_trace(Q, K, J, 2, 77, g, flags=oracle.NO_PROPAGATION)
+        assert kind.tolist() == [100 + k for k in range(6)]
+        q = Q.reshape(-1, d)[g]
+        cur = int(J.reshape(-1)[g])
+        best = q @ Kf[cur]
+        for k, (c, w) in enumerate(zip(idx, win)):
+            D = [37, 18, 9, 4, 2, 1][k]
+            u, v = divmod(cur, Wk)
+            assert tuple(w) == (max(0, u - D), min(Hk - 1, u + D), max(0, v - D), min(Wk - 1, v + D))
+            r, cc = divmod(int(c), Wk)
+            assert w[0] <= r <= w[1] and w[2] <= cc <= w[3]
+            sc = q @ Kf[c]
+            if sc > best or (sc == best and c < cur):
+                cur, best = int(c), sc
+        assert final == cur
+
+
+def test_random_search_uniform_in_window():
+    """The first draw (D = R covers the grid) is uniform over the whole key grid."""
+    S, Hq, Wq, Hk, Wk = 8, 32, 32, 6, 9
+    Q = np.ones((S, Hq, Wq, 1))
+    K = np.ones((S, Hk, Wk, 1))
+    J = np.zeros((S, Hq, Wq), np.int32)
+    first = []
+    for g in range(0, S * Hq * Wq, 3):
+        idx, kind, _, _ = oracle.pm_trace(Q, K, J, 1, 31, g, flags=oracle.NO_PROPAGATION)
+        first.append(idx[0])
+    counts = np.bincount(np.array(first), minlength=Hk * Wk)
+    assert stats.chisquare(counts).pvalue > 1e-3
+
+
+def test_random_search_alone_finds_exact_argmax():
+    """With enough sweeps, random search over a 4x5 key grid reaches the brute-force argmax (Eq. 7, kappa = 1)."""
+    rng = np.random.default_rng(9)
+    Q = rng.standard_normal((6, 4, 5, 8))
+    K = rng.standard_normal((6, 4, 5, 8))
+    J, s, _, _ = oracle.patchmatch(Q, K, 200, seed=3, flags=oracle.NO_PROPAGATION)
+    Jb, sb = dense.brute_argmax(Q, K)
+    np.testing.assert_array_equal(J, Jb)
+
+
+def test_ties_go_to_lowest_index():
+    """All keys equal: every score ties, so the kept key must end at flat index 0."""
+    Q = np.ones((2, 6, 6, 3))
+    K = np.ones((2, 4, 4, 3))
+    J, _, ties, _ = oracle.patchmatch(Q, K, 60, seed=8)
+    assert (J == 0).all()
+    assert ties.any()      # exact ties between different keys are flagged as near-ties
+
+
+# --------------------------------------------------------------------------
+# whole PatchMatch: invariants and the exact argmax
+# --------------------------------------------------------------------------
+@pytest.fixture(scope="module")
+def tiny():
+    cfg = si.get(0)
+    a = si.make_arrays(cfg)
+    return cfg, a
+
+
+def test_scores_monotone_and_bounded(tiny):
+    """The incumbent is only replaced by a strictly better key: s_t >= s_{t-1}; s_t <= exact max."""
+    cfg, a = tiny
+    Q, K = a["Q"], a["K"]
+    Jb, sb = dense.brute_argmax(Q, K)
+    J, s = oracle.pm_init(Q, K, cfg.pm_seed)
+    hit_prev = J == Jb
+    for t in range(1, 9):
+        Jn, sn, _, _ = oracle.pm_iteration(Q, K, J, t, cfg.pm_seed, s_prev=s)
+        assert (sn >= s).all()
+        assert (sn <= sb + 1e-12).all()
+        hit = Jn == Jb
+        assert (hit | ~hit_prev).all()     # once the argmax is found it is kept
+        J, s, hit_prev = Jn, sn, hit
+
+
+def test_recall_against_brute_force(tiny):
+    """PatchMatch approaches the exact argmax (Section 3.3): recall grows with T on the 32x32 workload."""
+    cfg, a = tiny
+    Jb, _ = dense.brute_argmax(a["Q"], a["K"])
+    rec = []
+    for T in (1, 2, 4, 8, 16):
+        J, _, _, _ = oracle.patchmatch(a["Q"], a["K"], T, cfg.pm_seed)
+        rec.append((J == Jb).mean())
+    assert all(b >= a_ - 0.01 for a_, b in zip(rec, rec[1:]))
+    assert rec[2] > 0.85 and rec[-1] > 0.99
+
+
+def test_small_grid_exact():
+    """8x8 grid, 64 sweeps: every query ends on its exact argmax."""
+    cfg = resized(si.get(0), Hq=8, Wq=8, Hk=8, Wk=8, sigma=1.0, F=3)
+    a = si.make_arrays(cfg, seed=4)
+    J, _, _, _ = oracle.patchmatch(a["Q"], a["K"], 64, seed=1)
+    Jb, _ = dense.brute_argmax(a["Q"], a["K"])
+    np.testing.assert_array_equal(J, Jb)
+
+
+def test_identity_field_recovered():
+    """Q = K with distinct unit keys: the exact argmax is the identity, and PatchMatch finds it."""
+    rng = np.random.default_rng(2)
+    K = unit_keys(rng, 2, 32, 32, 16)
+    J, _, _, _ = oracle.patchmatch(K, K, 8, seed=6)
+    ident = np.arange(32 * 32).reshape(1, 32, 32)
+    assert (J == ident).mean() > 0.99
+
+
+def test_power_of_two_scale_invariance(tiny):
+    """Scaling Q by 2 scales every score exactly, so the map (and its tie flags) cannot change."""
+    cfg, a = tiny
+    J1, s1, t1, _ = oracle.patchmatch(a["Q"], a["K"], 4, cfg.pm_seed)
+    J2, s2, t2, _ = oracle.patchmatch(2.0 * a["Q"], a["K"], 4, cfg.pm_seed)
+    np.testing.assert_array_equal(J1, J2)
+    np.testing.assert_array_equal(s2, 2.0 * s1)
+    np.testing.assert_array_equal(t1, t2)
+
+
+def test_resume_equals_uninterrupted(tiny):
+    cfg, a = tiny
+    J, s, _, n_full = oracle.patchmatch(a["Q"], a["K"], 5, cfg.pm_seed)
+    Ja, _, _, n_a = oracle.patchmatch(a["Q"], a["K"], 2, cfg.pm_seed)
+    Jb, sb, _, n_b = oracle.patchmatch(a["Q"], a["K"], 3, cfg.pm_seed, init=Ja, t0=3)
+    np.testing.assert_array_equal(J, Jb)
+    np.testing.assert_array_equal(s, sb)
+    assert n_full == n_a + n_b
+
+
+def test_iteration_is_order_free(tiny):
+    """The parallel foreach reads only the previous field: any query subset/order gives the same rows."""
+    cfg, a = tiny
+    J0, _ = oracle.pm_init(a["Q"], a["K"], cfg.pm_seed)
+    Jf, sf, tf, _ = oracle.pm_iteration(a["Q"], a["K"], J0, 1, cfg.pm_seed)
+    ids = np.random.default_rng(0).permutation(J0.size)[:300]
+    Js, ss, ts, _ = oracle.pm_iteration(a["Q"], a["K"], J0, 1, cfg.pm_seed, query_ids=ids)
+    np.testing.assert_array_equal(Js, Jf.reshape(-1)[ids])
+    np.testing.assert_array_equal(ss, sf.reshape(-1)[ids])
+    np.testing.assert_array_equal(ts, tf.reshape(-1)[ids])
+
+
+def test_one_dimensional_grid():
+    """A 128x1 grid with d_k = 4 (the shape of the paper's Figure 2 maps): PatchMatch reaches the argmax."""
+    cfg = resized(si.get(0), Hq=128, Wq=1, Hk=128, Wk=1, d=4, sigma=2.0, F=6)
+    a = si.make_arrays(cfg, seed=12)
+    J, _, _, _ = oracle.patchmatch(a["Q"], a["K"], 24, seed=2)
+    Jb, _ = dense.brute_argmax(a["Q"], a["K"])
+    assert (J == Jb).mean() > 0.97
+
+
+def test_cross_grid_bounds():
+    """Cross non-local mean (Eq. 4): query grid 12x10, key grid 17x9 -- every index stays in the key grid."""
+    cfg = resized(si.get(4), batch=1, heads=2, Hq=12, Wq=10, Hk=17, Wk=9, F=3)
+    a = si.make_arrays(cfg, seed=3)
+    J, s, _, _ = oracle.patchmatch(a["Q"], a["K"], 30, seed=4)
+    assert J.min() >= 0 and J.max() < 17 * 9
+    Jb, sb = dense.brute_argmax(a["Q"], a["K"])
+    assert (J == Jb).mean() > 0.95
+
+
+# --------------------------------------------------------------------------
+# sparse attend (Algorithm 2, Eq. 8-9)
+# --------------------------------------------------------------------------
+def test_attend_hand_cases():
+    g = json.load(open(os.path.join(GOLDEN, "attend_hand.json")))
+    for c in g["cases"]:
+        d = len(c["q"])
+        dv = len(c["v"][0])
+        Q = np.array(c["q"], np.float64).reshape(1, c["Hq"], c["Wq"], d)
+        K = np.array(c["k"], np.float64).reshape(1, c["Hk"], c["Wk"], d)
+        V = np.array(c["v"], np.float64).reshape(1, c["Hk"], c["Wk"], dv)
+        J = np.array(c["J"], np.int32).reshape(1, c["Hq"], c["Wq"])
+        out = oracle.sparse_attend(Q, K, V, J, c["window"], c["scale"])
+        np.testing.assert_allclose(out.reshape(-1, dv), np.array(c["expected"]), rtol=g["tolerance"],
+                                   err_msg=c["note"])
+
+
+def test_attend_b0_is_value_of_match(tiny):
+    """b = 0, kappa = 1: the output is v at the argmax (Section 4.2)."""
+    cfg, a = tiny
+    J, _, _, _ = oracle.patchmatch(a["Q"], a["K"], 4, cfg.pm_seed)
+    out = oracle.sparse_attend(a["Q"], a["K"], a["V"], J, 1, cfg.scale)
+    Vf = a["V"].reshape(1, -1, cfg.dv).astype(np.float64)
+    np.testing.assert_array_equal(out.reshape(1, -1, cfg.dv), Vf[:, J.reshape(-1)])
+
+
+@pytest.mark.parametrize("H,W", [(9, 7), (1, 16), (6, 6)])
+def test_attend_full_window_is_dense_attention(H, W):
+    """A window of side >= 2 max(H, W) - 1 covers every key from any centre: Eq. 8 becomes Eq. 2."""
+    import torch
+
+    rng = np.random.default_rng(H * 100 + W)
+    S, d, dv = 2, 8, 5
+    Q = rng.standard_normal((S, 4, 3, d))
+    K = rng.standard_normal((S, H, W, d))
+    V = rng.standard_normal((S, H, W, dv))
+    J = rng.integers(0, H * W, (S, 4, 3)).astype(np.int32)
+    win = 2 * max(H, W) - 1
+    scale = 1 / math.sqrt(d)
+    out = oracle.sparse_attend(Q, K, V, J, win, scale)
+    ref = dense.dense_attend(Q, K, V, scale)
+    np.testing.assert_allclose(out, ref, rtol=1e-12, atol=1e-12)
+    tq = torch.from_numpy(Q.reshape(S, 1, -1, d))
+    tk = torch.from_numpy(K.reshape(S, 1, -1, d))
+    tv = torch.from_numpy(V.reshape(S, 1, -1, dv))
+    lib = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, scale=scale)
+    np.testing.assert_allclose(out.reshape(S, -1, dv), lib.numpy().reshape(S, -1, dv), rtol=1e-11, atol=1e-12)
+
+
+def test_attend_constant_values_unbiased(tiny):
+    """If v is constant over j the sparse estimate is exact (discussion of Eq. 10)."""
+    cfg, a = tiny
+    J, _, _, _ = oracle.patchmatch(a["Q"], a["K"], 2, cfg.pm_seed)
+    V = np.full_like(a["V"], 0.375)
+    out = oracle.sparse_attend(a["Q"], a["K"], V, J, 5, cfg.scale)
+    np.testing.assert_allclose(out, 0.375, rtol=1e-14)
+
+
+def test_attend_subset_matches_full(tiny):
+    cfg, a = tiny
+    J, _, _, _ = oracle.patchmatch(a["Q"], a["K"], 3, cfg.pm_seed)
+    full = oracle.sparse_attend(a["Q"], a["K"], a["V"], J, 3, cfg.scale)
+    ids = np.array([0, 5, 1023, 512, 31])
+    sub = oracle.sparse_attend(a["Q"], a["K"], a["V"], J, 3, cfg.scale, query_ids=ids)
+    np.testing.assert_array_equal(sub, full.reshape(-1, cfg.dv)[ids])
+
+
+# --------------------------------------------------------------------------
+# the plain definitions themselves
+# --------------------------------------------------------------------------
+def test_brute_argmax_by_loops():
+    rng = np.random.default_rng(0)
+    Q = rng.standard_normal((2, 3, 4, 5))
+    K = rng.standard_normal((2, 2, 5, 5))
+    K[1] /= np.linalg.norm(K[1], axis=2, keepdims=True)
+    K[1, 1, 3] = K[1, 0, 2]      # a duplicated unit key: the lower flat index (2, not 8) must win
+    Q[1, 0, 0] = K[1, 0, 2]
+    J, best = dense.brute_argmax(Q, K)
+    for s in range(2):
+        for x in range(3):
+            for y in range(4):
+                sc = [float(Q[s, x, y] @ K[s, r, c]) for r in range(2) for c in range(5)]
+                m = max(sc)
+                assert J[s, x, y] == sc.index(m)
+                assert best[s, x, y] == pytest.approx(m, rel=1e-14)
+    assert J[1, 0, 0] == 2
