@@ -1,0 +1,232 @@
+"""Throughput of the SCRAM hot path on one MI355X.
+
+A step is one pass of the whole path over one batch of resident synthetic
+input: PatchMatch (random init + T Jacobi sweeps) then the sparse window
+attention, on the 256x256, d=64, bf16, 4-slice workload by default.  The step
+is issued as the library calls it is made of -- one init launch, T
+single-sweep calls, one attend call (identical to a single T-sweep call, see
+test_gpu_fullsize) -- so HIP events on the launch stream can time every
+kernel inside the timed region.
+
+Prints one JSON line.  ``--gpus N`` with N > 1 exits: this path runs on one
+GPU (independent slices would shard across GPUs with no communication).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "queries/sec (PatchMatch argmax + sparse attend), 256×256 grid d=64; HBM GB/s"
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, public spec
+KERNEL_SRC = os.path.join(ROOT, "paper_1905_10308_amd", "csrc", "scram_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pm_iter_traffic.json")
+
+
+def pm_bytes_per_query_sweep(cfg) -> int:
+    """Algorithmic bytes of one query in one sweep: its q row, C candidate key
+    rows, and 4 B each for the previous index and score read and the new index
+    and score written."""
+    row = cfg.d * cfg.elem_bytes
+    return row * (1 + cfg.candidates) + 16
+
+
+def attend_bytes_per_query(cfg) -> int:
+    """q row, w^2 key rows, w^2 value rows, the 4 B index, the output row."""
+    row = cfg.d * cfg.elem_bytes
+    return row * (2 + 2 * cfg.window ** 2) + 4
+
+
+def init_bytes_per_query(cfg) -> int:
+    return 2 * cfg.d * cfg.elem_bytes + 8
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def load_traffic(cfg):
+    """Measured HBM bytes per sweep launch, if taken on the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256_16") != kernel_source_hash() or t.get("workload") != cfg.name:
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(cfg, arrays, min_s: float):
+    """The fp64 oracle on the host cores, on whole slices of the same workload.
+
+    Slices are run in turn (wrapping around) until at least ``min_s`` seconds
+    of oracle work have been timed, so the rate is stable but the run bounded.
+    """
+    import numpy as np
+
+    import oracle
+
+    threads = oracle.num_threads()
+    Q, K, V = (arrays[k].astype(np.float64) for k in ("Q", "K", "V"))
+    done_q, elapsed, runs = 0, 0.0, 0
+    per_slice = cfg.Hq * cfg.Wq
+    while elapsed < min_s and runs < 64 * cfg.S:
+        s = runs % cfg.S
+        t0 = time.perf_counter()
+        J, _, _, _ = oracle.patchmatch(Q[s:s + 1], K[s:s + 1], cfg.iters, cfg.pm_seed)
+        oracle.sparse_attend(Q[s:s + 1], K[s:s + 1], V[s:s + 1], J, cfg.window, cfg.scale)
+        elapsed += time.perf_counter() - t0
+        done_q += per_slice
+        runs += 1
+    return {
+        "value": done_q / elapsed,
+        "unit": "queries/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"{runs} slice passes over the {cfg.S}-slice workload ({done_q} queries; {cfg.iters} sweeps + "
+                  f"{cfg.window}x{cfg.window} attend each), fp64, {elapsed:.1f} s",
+    }
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=None, help="workload index (default: the 256x256 bf16 one)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="seconds of oracle work for the CPU baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1:
+        print(f"bench.py: this path runs on one GPU; --gpus {args.gpus} is not supported "
+              "(slices are independent and would shard across GPUs without communication)", file=sys.stderr)
+        return 2
+    if int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: launched with WORLD_SIZE > 1; this path runs on one GPU", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_1905_10308_amd as scram
+    import scram_inputs as si
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        return 1
+    scram.lib()
+    ci = si.HEADLINE if args.config is None else args.config
+    cfg = si.get(ci)
+    data = si.make(cfg, device="cuda")
+    Q, K, V = data["Q"], data["K"], data["V"]
+    S, Hq, Wq = cfg.S, cfg.Hq, cfg.Wq
+    dev = Q.device
+    stream = torch.cuda.current_stream(dev)
+
+    J = [torch.empty((S, Hq, Wq), dtype=torch.int32, device=dev) for _ in range(2)]
+    sc = [torch.empty((S, Hq, Wq), dtype=torch.float32, device=dev) for _ in range(2)]
+    ws = torch.empty(scram.patchmatch_workspace_bytes(S, Hq, Wq), dtype=torch.uint8, device=dev)
+    out = torch.empty((S, Hq, Wq, cfg.dv), dtype=Q.dtype, device=dev)
+    T = cfg.iters
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        scram.patchmatch(Q, K, 0, cfg.pm_seed, out=J[0], score_out=sc[0], workspace=ws)
+        if ev is not None:
+            ev[1].record(stream)
+        cur = 0
+        for t in range(1, T + 1):
+            nxt = 1 - cur
+            scram.patchmatch(Q, K, 1, cfg.pm_seed, init=J[cur], init_score=sc[cur], t0=t, out=J[nxt],
+                             score_out=sc[nxt], workspace=ws)
+            if ev is not None:
+                ev[1 + t].record(stream)
+            cur = nxt
+        scram.sparse_attend(Q, K, V, J[cur], cfg.window, cfg.scale, out=out)
+        if ev is not None:
+            ev[2 + T].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(T + 3)] for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    start.record(stream)
+    for k in range(args.steps):
+        step(events[k])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+
+    ms_step = start.elapsed_time(stop) / args.steps
+    init_ms = sum(ev[0].elapsed_time(ev[1]) for ev in events) / args.steps
+    iter_ms = sum(ev[t].elapsed_time(ev[t + 1]) for ev in events for t in range(1, T + 1)) / (args.steps * T)
+    att_ms = sum(ev[T + 1].elapsed_time(ev[T + 2]) for ev in events) / args.steps
+
+    nq = cfg.nq
+    pm_launch_bytes = nq * pm_bytes_per_query_sweep(cfg)
+    att_bytes = nq * attend_bytes_per_query(cfg)
+    achieved = pm_launch_bytes / (iter_ms * 1e-3) / 1e9
+    traffic = load_traffic(cfg)
+
+    res = {
+        "metric": METRIC,
+        "value": nq / (ms_step * 1e-3),
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": cfg.name,
+            "grid": f"{Hq}x{Wq}" + ("" if (Hq, Wq) == (cfg.Hk, cfg.Wk) else f"->{cfg.Hk}x{cfg.Wk}"),
+            "slices": S,
+            "batch": cfg.batch,
+            "heads": cfg.heads,
+            "d": cfg.d,
+            "storage": cfg.dtype,
+            "iters": T,
+            "window": cfg.window,
+            "queries_per_step": nq,
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "pm_iter",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": traffic,
+        },
+        "kernels_ms": {"pm_init": init_ms, "pm_iter": iter_ms, "attend": att_ms},
+        "attend_GBps": att_bytes / (att_ms * 1e-3) / 1e9,
+        "candidate_evals_per_s_nominal": nq * T * cfg.candidates / (ms_step * 1e-3),
+        "wall_ms_per_step": wall * 1e3 / args.steps,
+        "device": torch.cuda.get_device_name(dev),
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(cfg, data["np"], args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

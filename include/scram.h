@@ -1,0 +1,165 @@
+/*
+ * scram.h -- C ABI of the SCRAM hot path on AMD Instinct MI355X (gfx950).
+ *
+ * SCRAM ("Spatially Coherent Randomized Attention Maps", Calian et al. 2019)
+ * approximates one attention / non-local-mean layer over an image in two
+ * steps, both exported here:
+ *
+ *   1. scram_patchmatch -- PatchMatch (Algorithm 1, run once: kappa = 1)
+ *      estimates for every query pixel the key pixel with the largest q.k
+ *      (Equation 7 at kappa = 1): random initialisation, then T synchronous
+ *      sweeps of propagation from neighbours at distances 8, 4, 2, 1 and
+ *      random search at distances R, R/2, ..., 1.
+ *   2. scram_sparse_attend -- the sparse non-local mean (Algorithm 2,
+ *      Equations 8-9): a softmax of scale * q.k over the (2b+1) x (2b+1)
+ *      window of keys around each query's match, then the weighted sum of
+ *      the values of those keys.
+ *
+ * Conventions shared by every entry point
+ * ----------------------------------------
+ * - Data layout: row-major, channels innermost.  Q is [S, Hq, Wq, d], K is
+ *   [S, Hk, Wk, d], V is [S, Hk, Wk, dv], the output of the attend step is
+ *   [S, Hq, Wq, dv]; S counts independent slices (batch x heads).  Index maps
+ *   are int32 [S, Hq, Wq] holding the flat key index u * Wk + v of key pixel
+ *   (u, v) inside the query's own slice.  Query (s, x, y) has the global id
+ *   g = (s * Hq + x) * Wq + y.  Self-attention is the case Hq = Hk, Wq = Wk;
+ *   different grids give a general non-local mean (Equation 4).
+ * - Element types: SCRAM_F32 (fp32) or SCRAM_BF16 (bfloat16) storage for Q,
+ *   K, V and the attend output; all arithmetic accumulates in fp32.
+ * - Supported sizes: d in {16, 32, 64, 128}; dv == d; S*Hq*Wq < 2^31 and
+ *   Hk*Wk < 2^31.
+ * - Pointers are device pointers (HIP) owned by the caller.  Q, K, V and the
+ *   attend output must be 16-byte aligned; index and score buffers 4-byte
+ *   aligned; the workspace 256-byte aligned.  The library allocates no memory
+ *   and keeps no state between calls; calls are re-entrant.
+ * - Every call only enqueues work on `stream` (0 = the null stream) and
+ *   returns without synchronising.  Arguments are validated on the host
+ *   before any HIP call; a non-zero status means nothing was enqueued
+ *   (SCRAM_ERR_HIP: a launch failed; work enqueued before it by the same call
+ *   may still run).  Device faults surface at the caller's next
+ *   synchronisation.  Nothing else crosses the ABI: no exceptions, no abort.
+ * - Index values read from device memory (init, argmax) are clamped into
+ *   [0, Hk*Wk) before use, so an out-of-range entry gives an unspecified
+ *   result but never an out-of-bounds access.
+ */
+#ifndef SCRAM_H
+#define SCRAM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* storage type of Q, K, V and the attend output */
+typedef enum { SCRAM_F32 = 0, SCRAM_BF16 = 1 } scram_dtype;
+
+/* status codes */
+enum {
+    SCRAM_OK = 0,
+    SCRAM_ERR_NULL = -1,        /* a required pointer is NULL */
+    SCRAM_ERR_SHAPE = -2,       /* a size or count is out of range */
+    SCRAM_ERR_UNSUPPORTED = -3, /* dtype, d or dv not supported, unknown flag */
+    SCRAM_ERR_ALIGN = -4,       /* a pointer is not aligned as required */
+    SCRAM_ERR_ALIAS = -5,       /* an output overlaps an input or another output */
+    SCRAM_ERR_HIP = -6,         /* a HIP call failed */
+    SCRAM_ERR_WORKSPACE = -7    /* workspace missing or smaller than required */
+};
+
+/* flags of scram_patchmatch: switch one step of an iteration off (tests) */
+enum { SCRAM_PM_NO_PROPAGATION = 1u, SCRAM_PM_NO_RANDOM_SEARCH = 2u };
+
+/*
+ * Bytes of workspace scram_patchmatch needs for S*Hq*Wq queries: one int32
+ * index map and two fp32 score maps, each rounded up to 256 bytes.
+ */
+size_t scram_patchmatch_workspace_bytes(int S, int Hq, int Wq);
+
+/*
+ * PatchMatch argmax (Algorithm 1 with kappa = 1, so is_index_valid reduces to
+ * "inside the key grid"; the attend window size b is not used here).
+ *
+ * Initialisation (Algorithm 1, first loop): when `init` is NULL, query g
+ * draws J0[g] = u * Wk + v with u = floor(w0 * Hk / 2^32),
+ * v = floor(w1 * Wk / 2^32), where (w0, w1, ., .) is the Philox4x32-10 block
+ * (Salmon et al., SC 2011) of counter (g, 0, 0, 0) and key
+ * (seed mod 2^32, seed div 2^32).  When `init` is given it is J0 (not
+ * modified; entries clamped into the key grid).  The incumbent scores s0 are
+ * the fp32 dot products q_g . k_J0[g], or `init_score` when given (which
+ * must then hold exactly what this library computed for that map, e.g. a
+ * previous call's score_out).
+ *
+ * Iterations t = t0, ..., t0 + iters - 1 (the "parallel foreach" over query
+ * pixels), each reading only the previous iteration's map (a Jacobi sweep):
+ *   - propagation: for jump in 8, 4, 2, 1 and each axis direction delta, the
+ *     neighbour p' = p + jump * delta (skipped outside the query grid)
+ *     offers its match shifted back by jump * delta (skipped outside the key
+ *     grid) -- a shift in query is an equal shift in key (Section 4.1);
+ *   - random search: with D = R = max(Hk, Wk), halved (integer) down to 1,
+ *     a key drawn uniformly from the square of half-side D around the
+ *     running best, clipped to the key grid; step k uses the Philox block of
+ *     counter (g, t, k div 2, 0), words 2(k mod 2) and 2(k mod 2) + 1 mapped
+ *     like the initial draw onto the clipped rows and columns;
+ *   - a candidate replaces the incumbent iff its unscaled fp32 score q.k is
+ *     larger, or equal with a lower flat key index.
+ *
+ * Arguments:
+ *   Q, K        inputs, layouts above, element type `dtype`
+ *   S, Hq, Wq   slices and query grid; Hk, Wk key grid; d channels
+ *   iters       T >= 0 sweeps (0 returns the initial map)
+ *   seed        64-bit Philox key
+ *   init        nullable int32 [S, Hq, Wq] initial map
+ *   init_score  nullable fp32 [S, Hq, Wq] scores of `init` (ignored when
+ *               init is NULL)
+ *   t0          index of the first sweep, >= 1 (1 for a fresh run; a run
+ *               split as (T1 sweeps) then (init = its map, t0 = T1 + 1)
+ *               equals the unsplit run bit for bit)
+ *   flags       0, or SCRAM_PM_NO_PROPAGATION / SCRAM_PM_NO_RANDOM_SEARCH
+ *   argmax_out  int32 [S, Hq, Wq] final map J_T (written)
+ *   score_out   nullable fp32 [S, Hq, Wq] final scores q . k_{J_T} (unscaled)
+ *   workspace   >= scram_patchmatch_workspace_bytes(S, Hq, Wq) bytes of
+ *               device memory, contents ignored and overwritten
+ * Outputs must not overlap each other, the inputs or the workspace
+ * (SCRAM_ERR_ALIAS).  Returns a status code.
+ */
+int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int Wq, int Hk, int Wk,
+                     int d, int iters, uint64_t seed, const int32_t* init, const float* init_score,
+                     int t0, uint32_t flags, int32_t* argmax_out, float* score_out, void* workspace,
+                     size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Sparse attention around the argmax (Algorithm 2 with kappa = 1,
+ * Equations 8-9).  For query g with match (u, v) = divmod(argmax[g], Wk):
+ * the window W_g = {(u + a, v + c) : |a|, |c| <= b} with b = (window - 1)/2,
+ * keys outside the key grid dropped (the match itself is always inside);
+ * out[g] = sum_{j in W_g} softmax_j(scale * q_g . k_j) v_j, computed with an
+ * fp32 online softmax and written in `dtype`.
+ *
+ * Arguments:
+ *   Q, K, V   inputs, layouts above; V has dv channels (dv == d)
+ *   argmax    int32 [S, Hq, Wq] flat key indices (e.g. scram_patchmatch's)
+ *   window    odd side 2b + 1 >= 1 of the square window (<= 32767)
+ *   scale     softmax temperature, 1/sqrt(d_k) for Equation 1; finite
+ *   out       [S, Hq, Wq, dv] in `dtype` (written; must not overlap inputs)
+ * Returns a status code.
+ */
+int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype,
+                        const int32_t* argmax, int S, int Hq, int Wq, int Hk, int Wk, int d, int dv,
+                        int window, float scale, void* out, hipStream_t stream);
+
+/* Static, NUL-terminated description of a status code. */
+const char* scram_status_string(int status);
+
+/* ABI version of this header: (major << 16) | minor. */
+int scram_abi_version(void);
+
+#define SCRAM_ABI_VERSION ((1 << 16) | 0)
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SCRAM_H */

@@ -1,0 +1,18 @@
+"""SCRAM hot path on MI355X: PatchMatch argmax + sparse window attention.
+
+The computation lives in the HIP library ``_lib/libscram.so`` (C ABI:
+``include/scram.h``); this package only marshals torch tensors into it.
+Importing the package does not load the library; the first call does, and
+raises if it is missing.
+"""
+from .binding import (  # noqa: F401
+    NO_PROPAGATION,
+    NO_RANDOM_SEARCH,
+    ScramError,
+    forward,
+    lib,
+    patchmatch,
+    patchmatch_workspace_bytes,
+    sparse_attend,
+    status_string,
+)

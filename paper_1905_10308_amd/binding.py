@@ -1,0 +1,182 @@
+"""Thin ctypes binding of ``libscram.so`` (the C ABI in ``include/scram.h``).
+
+Argument marshalling only: torch tensors provide device memory and the
+current HIP stream; every step of the computation runs in the library's HIP
+kernels.  There is no fallback -- if the library is missing or a call fails,
+these functions raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "_lib", "libscram.so")
+
+SCRAM_F32 = 0
+SCRAM_BF16 = 1
+NO_PROPAGATION = 1
+NO_RANDOM_SEARCH = 2
+
+STATUS = {
+    0: "SCRAM_OK",
+    -1: "SCRAM_ERR_NULL",
+    -2: "SCRAM_ERR_SHAPE",
+    -3: "SCRAM_ERR_UNSUPPORTED",
+    -4: "SCRAM_ERR_ALIGN",
+    -5: "SCRAM_ERR_ALIAS",
+    -6: "SCRAM_ERR_HIP",
+    -7: "SCRAM_ERR_WORKSPACE",
+}
+
+_lib = None
+
+
+class ScramError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS.get(status, status)} ({status_string(status)})")
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"SCRAM HIP library not found at {LIB_PATH}; build it with "
+                           "`python -m paper_1905_10308_amd.build` (or __graft_entry__.build())")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I, U32, U64, SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_size_t
+    L.scram_patchmatch_workspace_bytes.argtypes = [I, I, I]
+    L.scram_patchmatch_workspace_bytes.restype = SZ
+    L.scram_patchmatch.argtypes = [P, P, I, I, I, I, I, I, I, I, U64, P, P, I, U32, P, P, P, SZ, P]
+    L.scram_patchmatch.restype = I
+    L.scram_sparse_attend.argtypes = [P, P, P, I, P, I, I, I, I, I, I, I, I, ctypes.c_float, P, P]
+    L.scram_sparse_attend.restype = I
+    L.scram_status_string.argtypes = [I]
+    L.scram_status_string.restype = ctypes.c_char_p
+    L.scram_abi_version.argtypes = []
+    L.scram_abi_version.restype = I
+    _lib = L
+    return L
+
+
+def status_string(status: int) -> str:
+    return lib().scram_status_string(int(status)).decode()
+
+
+def patchmatch_workspace_bytes(S: int, Hq: int, Wq: int) -> int:
+    return int(lib().scram_patchmatch_workspace_bytes(S, Hq, Wq))
+
+
+# --------------------------------------------------------------------------
+# torch marshalling
+# --------------------------------------------------------------------------
+def _torch():
+    import torch
+
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return SCRAM_F32
+    if t.dtype == torch.bfloat16:
+        return SCRAM_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}; expected float32 or bfloat16")
+
+
+def _dev_tensor(t, name, ndim=None):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device (HIP) tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got {tuple(t.shape)}")
+    return t
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device):
+    return ctypes.c_void_p(_torch().cuda.current_stream(device).cuda_stream)
+
+
+def patchmatch(Q, K, iters: int, seed: int, *, init=None, init_score=None, t0: int = 1, flags: int = 0,
+               out=None, score_out=None, workspace=None, return_score: bool = False):
+    """PatchMatch argmax map (``scram_patchmatch``).
+
+    Q ``[S, Hq, Wq, d]``, K ``[S, Hk, Wk, d]`` (float32 or bfloat16, same dtype).
+    Returns int32 ``[S, Hq, Wq]`` flat key indices (and fp32 scores if
+    ``return_score``).  ``init``/``init_score``/``t0`` resume a run.
+    """
+    torch = _torch()
+    _dev_tensor(Q, "Q", 4)
+    _dev_tensor(K, "K", 4)
+    if K.dtype != Q.dtype:
+        raise TypeError("Q and K must share a dtype")
+    S, Hq, Wq, d = Q.shape
+    Sk, Hk, Wk, dk = K.shape
+    if Sk != S or dk != d:
+        raise ValueError(f"Q {tuple(Q.shape)} and K {tuple(K.shape)} disagree on slices or channels")
+    dev = Q.device
+    if out is None:
+        out = torch.empty((S, Hq, Wq), dtype=torch.int32, device=dev)
+    if return_score and score_out is None:
+        score_out = torch.empty((S, Hq, Wq), dtype=torch.float32, device=dev)
+    for name, t, dt in (("init", init, torch.int32), ("init_score", init_score, torch.float32),
+                        ("out", out, torch.int32), ("score_out", score_out, torch.float32)):
+        if t is not None:
+            _dev_tensor(t, name)
+            if t.dtype != dt or tuple(t.shape) != (S, Hq, Wq):
+                raise ValueError(f"{name} must be {dt} of shape {(S, Hq, Wq)}")
+    need = patchmatch_workspace_bytes(S, Hq, Wq)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    rc = lib().scram_patchmatch(_ptr(Q), _ptr(K), _dtype_code(Q), S, Hq, Wq, Hk, Wk, d, int(iters),
+                                ctypes.c_uint64(int(seed) & 0xFFFFFFFFFFFFFFFF), _ptr(init), _ptr(init_score),
+                                int(t0), int(flags), _ptr(out), _ptr(score_out), _ptr(workspace),
+                                workspace.numel() * workspace.element_size(), _stream(dev))
+    if rc != 0:
+        raise ScramError(rc, "scram_patchmatch")
+    return (out, score_out) if return_score else out
+
+
+def sparse_attend(Q, K, V, argmax, window: int, scale: float | None = None, *, out=None):
+    """Window softmax + value gather around ``argmax`` (``scram_sparse_attend``).
+
+    Returns ``[S, Hq, Wq, dv]`` in Q's dtype.  ``scale`` defaults to 1/sqrt(d).
+    """
+    torch = _torch()
+    for name, t in (("Q", Q), ("K", K), ("V", V)):
+        _dev_tensor(t, name, 4)
+        if t.dtype != Q.dtype:
+            raise TypeError("Q, K, V must share a dtype")
+    _dev_tensor(argmax, "argmax", 3)
+    S, Hq, Wq, d = Q.shape
+    _, Hk, Wk, _ = K.shape
+    dv = V.shape[3]
+    if tuple(K.shape[:3]) != tuple(V.shape[:3]) or K.shape[0] != S or K.shape[3] != d:
+        raise ValueError("K and V must share the key grid; K must match Q's slices and channels")
+    if argmax.dtype != torch.int32 or tuple(argmax.shape) != (S, Hq, Wq):
+        raise ValueError("argmax must be int32 [S, Hq, Wq]")
+    if scale is None:
+        scale = d ** -0.5
+    if out is None:
+        out = torch.empty((S, Hq, Wq, dv), dtype=Q.dtype, device=Q.device)
+    _dev_tensor(out, "out", 4)
+    rc = lib().scram_sparse_attend(_ptr(Q), _ptr(K), _ptr(V), _dtype_code(Q), _ptr(argmax), S, Hq, Wq, Hk, Wk,
+                                   d, dv, int(window), float(scale), _ptr(out), _stream(Q.device))
+    if rc != 0:
+        raise ScramError(rc, "scram_sparse_attend")
+    return out
+
+
+def forward(Q, K, V, iters: int, seed: int, window: int, scale: float | None = None):
+    """The whole hot path: argmax map, then the sparse attention output."""
+    J = patchmatch(Q, K, iters, seed)
+    return sparse_attend(Q, K, V, J, window, scale), J

@@ -1,0 +1,187 @@
+// C-ABI front end of the SCRAM library: argument validation (host only, no
+// HIP call before every check has passed), ping-pong buffer planning for the
+// Jacobi sweeps, and the launches.  The contract is documented in scram.h.
+
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <hip/hip_runtime.h>
+
+#include "scram.h"
+#include "scram_launch.h"
+
+namespace {
+
+constexpr int64_t kMaxSide = int64_t(1) << 30;
+constexpr int64_t kMaxCount = int64_t(1) << 31;
+
+size_t round256(size_t b) { return (b + 255) & ~size_t(255); }
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+struct Range {
+    uintptr_t lo, hi;  // [lo, hi)
+};
+
+Range range(const void* p, size_t bytes)
+{
+    const uintptr_t a = reinterpret_cast<uintptr_t>(p);
+    return Range{a, a + bytes};
+}
+
+bool overlap(const Range& a, const Range& b)
+{
+    return a.lo != a.hi && b.lo != b.hi && a.lo < b.hi && b.lo < a.hi;
+}
+
+bool supported_width(int d) { return d == 16 || d == 32 || d == 64 || d == 128; }
+
+size_t elem_bytes(int dtype) { return dtype == SCRAM_BF16 ? 2 : 4; }
+
+int check_grid(int S, int Hq, int Wq, int Hk, int Wk)
+{
+    if (S <= 0 || Hq <= 0 || Wq <= 0 || Hk <= 0 || Wk <= 0) return SCRAM_ERR_SHAPE;
+    if (Hq > kMaxSide || Wq > kMaxSide || Hk > kMaxSide || Wk > kMaxSide) return SCRAM_ERR_SHAPE;
+    if (int64_t(S) * Hq * Wq >= kMaxCount || int64_t(Hk) * Wk >= kMaxCount) return SCRAM_ERR_SHAPE;
+    return SCRAM_OK;
+}
+
+int check_type(int dtype, int d)
+{
+    if (dtype != SCRAM_F32 && dtype != SCRAM_BF16) return SCRAM_ERR_UNSUPPORTED;
+    if (!supported_width(d)) return SCRAM_ERR_UNSUPPORTED;
+    return SCRAM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t scram_patchmatch_workspace_bytes(int S, int Hq, int Wq)
+{
+    if (S <= 0 || Hq <= 0 || Wq <= 0) return 0;
+    const size_t n = size_t(S) * size_t(Hq) * size_t(Wq);
+    return 3 * round256(4 * n);
+}
+
+int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int Wq, int Hk, int Wk,
+                     int d, int iters, uint64_t seed, const int32_t* init, const float* init_score,
+                     int t0, uint32_t flags, int32_t* argmax_out, float* score_out, void* workspace,
+                     size_t workspace_bytes, hipStream_t stream)
+{
+    // ---- validation (no HIP call above this line) ----
+    if (!Q || !K || !argmax_out) return SCRAM_ERR_NULL;
+    if (!workspace) return SCRAM_ERR_WORKSPACE;
+    int rc = check_grid(S, Hq, Wq, Hk, Wk);
+    if (rc) return rc;
+    if (iters < 0 || t0 < 1 || int64_t(t0) + iters > int64_t(0xFFFFFFFFu)) return SCRAM_ERR_SHAPE;
+    if ((rc = check_type(dtype, d))) return rc;
+    if (flags & ~uint32_t(SCRAM_PM_NO_PROPAGATION | SCRAM_PM_NO_RANDOM_SEARCH)) return SCRAM_ERR_UNSUPPORTED;
+    if (!init) init_score = nullptr;
+    if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(argmax_out, 4) || !aligned(workspace, 256) ||
+        (score_out && !aligned(score_out, 4)) || (init && !aligned(init, 4)) ||
+        (init_score && !aligned(init_score, 4)))
+        return SCRAM_ERR_ALIGN;
+    const size_t n = size_t(S) * Hq * Wq;
+    const size_t need = scram_patchmatch_workspace_bytes(S, Hq, Wq);
+    if (workspace_bytes < need) return SCRAM_ERR_WORKSPACE;
+
+    const size_t eb = elem_bytes(dtype);
+    const Range rQ = range(Q, n * d * eb), rK = range(K, size_t(S) * Hk * Wk * d * eb);
+    const Range rJ = range(argmax_out, 4 * n), rW = range(workspace, need);
+    const Range rS = score_out ? range(score_out, 4 * n) : Range{0, 0};
+    const Range rI = init ? range(init, 4 * n) : Range{0, 0};
+    const Range rIS = init_score ? range(init_score, 4 * n) : Range{0, 0};
+    for (const Range& out : {rJ, rS, rW}) {
+        for (const Range& other : {rQ, rK, rI, rIS}) {
+            if (overlap(out, other)) return SCRAM_ERR_ALIAS;
+        }
+    }
+    if (overlap(rJ, rS) || overlap(rJ, rW) || overlap(rS, rW)) return SCRAM_ERR_ALIAS;
+
+    // ---- plan the ping-pong buffers ----
+    // The map after sweep k (k = 0 is the initial map) lives in buffer
+    // (iters - k) % 2, so the last sweep writes buffer 0 = the caller's
+    // outputs and no sweep reads the buffer it writes.
+    char* ws = static_cast<char*>(workspace);
+    int32_t* Jbuf[2] = {argmax_out, reinterpret_cast<int32_t*>(ws)};
+    float* s_ws0 = reinterpret_cast<float*>(ws + round256(4 * n));
+    float* s_ws1 = reinterpret_cast<float*>(ws + 2 * round256(4 * n));
+    float* sbuf[2] = {score_out ? score_out : s_ws0, s_ws1};
+    const scram::Grid grid{S, Hq, Wq, Hk, Wk, d};
+
+    const int p0 = iters % 2;
+    const int32_t* Jcur;
+    const float* scur;
+    hipError_t e = hipSuccess;
+    if (init) {
+        Jcur = init;
+        if (init_score) {
+            scur = init_score;
+        } else {
+            e = scram::launch_pm_init(dtype, Q, K, grid, seed, init, nullptr, sbuf[p0], stream);
+            scur = sbuf[p0];
+        }
+        if (e == hipSuccess && iters == 0) {
+            e = hipMemcpyAsync(argmax_out, init, 4 * n, hipMemcpyDeviceToDevice, stream);
+            if (e == hipSuccess && score_out && init_score)
+                e = hipMemcpyAsync(score_out, init_score, 4 * n, hipMemcpyDeviceToDevice, stream);
+        }
+    } else {
+        e = scram::launch_pm_init(dtype, Q, K, grid, seed, nullptr, Jbuf[p0], sbuf[p0], stream);
+        Jcur = Jbuf[p0];
+        scur = sbuf[p0];
+    }
+    for (int k = 1; k <= iters && e == hipSuccess; ++k) {
+        const int pk = (iters - k) % 2;
+        e = scram::launch_pm_iter(dtype, Q, K, grid, seed, uint32_t(t0 + k - 1), flags, Jcur, scur, Jbuf[pk],
+                                  sbuf[pk], stream);
+        Jcur = Jbuf[pk];
+        scur = sbuf[pk];
+    }
+    return e == hipSuccess ? SCRAM_OK : SCRAM_ERR_HIP;
+}
+
+int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype,
+                        const int32_t* argmax, int S, int Hq, int Wq, int Hk, int Wk, int d, int dv,
+                        int window, float scale, void* out, hipStream_t stream)
+{
+    if (!Q || !K || !V || !argmax || !out) return SCRAM_ERR_NULL;
+    int rc = check_grid(S, Hq, Wq, Hk, Wk);
+    if (rc) return rc;
+    if (window < 1 || window % 2 == 0 || window > 32767) return SCRAM_ERR_SHAPE;
+    if (!isfinite(scale)) return SCRAM_ERR_SHAPE;
+    if ((rc = check_type(dtype, d))) return rc;
+    if (dv != d) return SCRAM_ERR_UNSUPPORTED;
+    if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(out, 16) || !aligned(argmax, 4))
+        return SCRAM_ERR_ALIGN;
+    const size_t n = size_t(S) * Hq * Wq, eb = elem_bytes(dtype);
+    const Range rO = range(out, n * dv * eb);
+    for (const Range& other : {range(Q, n * d * eb), range(K, size_t(S) * Hk * Wk * d * eb),
+                               range(V, size_t(S) * Hk * Wk * dv * eb), range(argmax, 4 * n)}) {
+        if (overlap(rO, other)) return SCRAM_ERR_ALIAS;
+    }
+    const scram::Grid grid{S, Hq, Wq, Hk, Wk, d};
+    const hipError_t e = scram::launch_attend(dtype, Q, K, V, argmax, grid, window, scale, out, stream);
+    return e == hipSuccess ? SCRAM_OK : SCRAM_ERR_HIP;
+}
+
+const char* scram_status_string(int status)
+{
+    switch (status) {
+        case SCRAM_OK: return "ok";
+        case SCRAM_ERR_NULL: return "a required pointer is NULL";
+        case SCRAM_ERR_SHAPE: return "a size or count is out of range";
+        case SCRAM_ERR_UNSUPPORTED: return "unsupported dtype, channel count or flag";
+        case SCRAM_ERR_ALIGN: return "a pointer is not aligned as required";
+        case SCRAM_ERR_ALIAS: return "an output overlaps an input or another output";
+        case SCRAM_ERR_HIP: return "a HIP launch or copy failed";
+        case SCRAM_ERR_WORKSPACE: return "workspace missing or too small";
+        default: return "unknown status";
+    }
+}
+
+int scram_abi_version(void) { return SCRAM_ABI_VERSION; }
+
+}  // extern "C"

@@ -1,0 +1,142 @@
+"""The C-ABI library: it loads, exports every declared entry point, and rejects
+bad arguments on the host before any HIP call (so these run without a GPU).
+
+Every call below has at least one invalid argument; none reaches a launch.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "scram.h")
+
+OK, ENULL, ESHAPE, EUNSUP, EALIGN, EALIAS, EHIP, EWS = 0, -1, -2, -3, -4, -5, -6, -7
+F32, BF16 = 0, 1
+
+# fake, well-aligned, non-overlapping "device" addresses (never dereferenced)
+A_Q, A_K, A_V, A_J, A_S, A_W, A_I, A_IS, A_O = (0x10000000 * (i + 1) for i in range(9))
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_1905_10308_amd import binding
+
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_1905_10308_amd import build
+
+        build.build()
+    return binding.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = "\n".join(ln for ln in text.splitlines() if not ln.lstrip().startswith("#"))
+    return sorted(set(re.findall(r"\b(scram_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_entry_points():
+    names = declared_functions()
+    for n in ("scram_patchmatch", "scram_sparse_attend", "scram_patchmatch_workspace_bytes",
+              "scram_status_string", "scram_abi_version"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(L):
+    for name in declared_functions():
+        assert hasattr(L, name), f"{name} declared in scram.h but not exported"
+
+
+def test_abi_version(L):
+    assert L.scram_abi_version() == (1 << 16)
+
+
+def test_status_strings(L):
+    seen = set()
+    for code in (OK, ENULL, ESHAPE, EUNSUP, EALIGN, EALIAS, EHIP, EWS):
+        s = L.scram_status_string(code).decode()
+        assert s and s != "unknown status"
+        seen.add(s)
+    assert len(seen) == 8
+    assert L.scram_status_string(12345).decode() == "unknown status"
+
+
+def test_workspace_formula(L):
+    def r256(b):
+        return (b + 255) // 256 * 256
+
+    for S, H, W in ((1, 1, 1), (4, 256, 256), (3, 7, 5), (32, 64, 64)):
+        assert L.scram_patchmatch_workspace_bytes(S, H, W) == 3 * r256(4 * S * H * W)
+    assert L.scram_patchmatch_workspace_bytes(0, 4, 4) == 0
+
+
+def pm(L, **kw):
+    a = dict(Q=A_Q, K=A_K, dtype=F32, S=2, Hq=8, Wq=8, Hk=8, Wk=8, d=16, iters=2, seed=1, init=None,
+             init_score=None, t0=1, flags=0, out=A_J, score=A_S, ws=A_W, ws_bytes=1 << 20)
+    a.update(kw)
+    return L.scram_patchmatch(a["Q"], a["K"], a["dtype"], a["S"], a["Hq"], a["Wq"], a["Hk"], a["Wk"], a["d"],
+                              a["iters"], a["seed"], a["init"], a["init_score"], a["t0"], a["flags"], a["out"],
+                              a["score"], a["ws"], a["ws_bytes"], None)
+
+
+def at(L, **kw):
+    a = dict(Q=A_Q, K=A_K, V=A_V, dtype=F32, J=A_J, S=2, Hq=8, Wq=8, Hk=8, Wk=8, d=16, dv=16, window=3,
+             scale=0.25, out=A_O)
+    a.update(kw)
+    return L.scram_sparse_attend(a["Q"], a["K"], a["V"], a["dtype"], a["J"], a["S"], a["Hq"], a["Wq"], a["Hk"],
+                                 a["Wk"], a["d"], a["dv"], a["window"], a["scale"], a["out"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(Q=None), ENULL), (dict(K=None), ENULL), (dict(out=None), ENULL), (dict(ws=None), EWS),
+    (dict(S=0), ESHAPE), (dict(Hq=-1), ESHAPE), (dict(Wk=0), ESHAPE), (dict(iters=-1), ESHAPE),
+    (dict(t0=0), ESHAPE), (dict(S=1 << 16, Hq=1 << 8, Wq=1 << 7), ESHAPE),
+    (dict(Hk=1 << 16, Wk=1 << 15), ESHAPE), (dict(Hq=(1 << 30) + 1, S=1, Wq=1), ESHAPE),
+    (dict(t0=-5), ESHAPE),
+    (dict(d=48), EUNSUP), (dict(d=8), EUNSUP), (dict(dtype=7), EUNSUP), (dict(flags=4), EUNSUP),
+    (dict(Q=A_Q + 8), EALIGN), (dict(K=A_K + 4), EALIGN), (dict(out=A_J + 2), EALIGN),
+    (dict(ws=A_W + 16), EALIGN), (dict(score=A_S + 1), EALIGN), (dict(init=A_I + 2), EALIGN),
+    (dict(ws_bytes=100), EWS),
+    (dict(out=A_Q), EALIAS), (dict(score=A_K + 256), EALIAS), (dict(init=A_J), EALIAS),
+    (dict(ws=A_J), EALIAS), (dict(score=A_J + 64), EALIAS), (dict(init=A_I, init_score=A_S), EALIAS),
+    (dict(ws=A_S - 256), EALIAS),
+])
+def test_patchmatch_rejects(L, kw, code):
+    assert pm(L, **kw) == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(Q=None), ENULL), (dict(V=None), ENULL), (dict(J=None), ENULL), (dict(out=None), ENULL),
+    (dict(window=4), ESHAPE), (dict(window=0), ESHAPE), (dict(window=40001), ESHAPE),
+    (dict(scale=float("inf")), ESHAPE), (dict(scale=float("nan")), ESHAPE), (dict(S=0), ESHAPE),
+    (dict(d=24), EUNSUP), (dict(dv=32), EUNSUP), (dict(dtype=2), EUNSUP),
+    (dict(V=A_V + 8), EALIGN), (dict(out=A_O + 4), EALIGN), (dict(J=A_J + 1), EALIGN),
+    (dict(out=A_Q), EALIAS), (dict(out=A_V + 64), EALIAS), (dict(out=A_J - 16), EALIAS),
+])
+def test_sparse_attend_rejects(L, kw, code):
+    assert at(L, **kw) == code
+
+
+def test_python_binding_refuses_host_tensors():
+    import torch
+
+    import paper_1905_10308_amd as scram
+
+    Q = torch.zeros(1, 4, 4, 16)
+    with pytest.raises(ValueError):
+        scram.patchmatch(Q, Q, 1, 0)
+    with pytest.raises(ValueError):
+        scram.sparse_attend(Q, Q, Q, torch.zeros(1, 4, 4, dtype=torch.int32), 3)
+
+
+def test_product_package_does_not_reference_the_oracle():
+    """The product path never imports, links or calls the CPU oracle."""
+    pkg = os.path.join(ROOT, "paper_1905_10308_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".cpp", ".h")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "import oracle" not in text and "from oracle" not in text, f
+                assert "liboracle" not in text and "scram_oracle" not in text, f

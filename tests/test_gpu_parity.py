@@ -1,0 +1,299 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle.
+
+Argmax maps are integers: they must match the oracle exactly, except where
+the oracle itself records a near tie (two different keys whose fp64 scores
+differ by at most 1e-5 of sum_e |q_e k_e|, far wider than the fp32 rounding of
+either score) -- and, after several sweeps, except inside the region a
+near tie can reach by propagation (offsets 1, 2, 4, 8 along an axis per
+sweep).  Attention outputs must be within 1e-5 (fp32 storage) or 1e-2 (bf16
+storage) of the oracle, relative to the row's largest magnitude.
+"""
+import dataclasses
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import oracle.dense as dense
+import scram_inputs as si
+from scram_inputs.synth import resized
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+TOL = {"f32": 1e-5, "bf16": 1e-2}
+
+
+@pytest.fixture(scope="module")
+def scram():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1905_10308_amd as scram
+
+    scram.lib()  # raises if the HIP library is missing: no fallback
+    return scram
+
+
+def log(*a):
+    print(*a, flush=True)
+
+
+def dilate(mask):
+    """mask + M for M = {0, +-1, +-2, +-4, +-8 along each axis}, per slice."""
+    out = mask.copy()
+    H, W = mask.shape[-2:]
+    for j in (8, 4, 2, 1):
+        if j < H:
+            out[..., j:, :] |= mask[..., :-j, :]
+            out[..., :-j, :] |= mask[..., j:, :]
+        if j < W:
+            out[..., :, j:] |= mask[..., :, :-j]
+            out[..., :, :-j] |= mask[..., :, j:]
+    return out
+
+
+def reach_of_ties(ties):
+    """Queries a near tie in sweep t can influence by the last sweep."""
+    A = np.zeros(ties.shape[1:], bool)
+    for t in range(ties.shape[0]):
+        A = dilate(A) | ties[t]
+    return A
+
+
+def to_dev(arr, dtype):
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    return torch.from_numpy(np.ascontiguousarray(arr, np.float32)).to(tdt).contiguous().cuda()
+
+
+def row_rel_err(got, ref):
+    got = np.asarray(got, np.float64).reshape(-1, ref.shape[-1])
+    ref = np.asarray(ref, np.float64).reshape(-1, ref.shape[-1])
+    return np.abs(got - ref).max(axis=1) / np.maximum(np.abs(ref).max(axis=1), 1e-6)
+
+
+# small versions of the five workloads: several blocks and a ragged tail
+SMALL = [
+    si.get(0),
+    resized(si.get(1), batch=1, heads=3, Hq=40, Wq=36, Hk=40, Wk=36),
+    resized(si.get(2), batch=1, heads=2, Hq=48, Wq=50, Hk=48, Wk=50, F=12),
+    resized(si.get(3), batch=1, heads=1, Hq=72, Wq=64, Hk=72, Wk=64, F=16),
+    resized(si.get(4), batch=1, heads=2, Hq=30, Wq=26, Hk=45, Wk=39, F=8),
+]
+IDS = [c.name for c in SMALL]
+
+
+@pytest.fixture(scope="module", params=range(len(SMALL)), ids=IDS)
+def work(request, scram):
+    cfg = SMALL[request.param]
+    a = si.make_arrays(cfg)
+    dev = {k: to_dev(a[k], cfg.dtype) for k in ("Q", "K", "V")}
+    return cfg, a, dev
+
+
+def test_init_bit_exact(scram, work):
+    cfg, a, dev = work
+    J, s = scram.patchmatch(dev["Q"], dev["K"], 0, cfg.pm_seed, return_score=True)
+    J0, s0 = oracle.pm_init(a["Q"], a["K"], cfg.pm_seed)
+    np.testing.assert_array_equal(J.cpu().numpy(), J0)
+    _, sabs = oracle.pm_scores(a["Q"], a["K"], J0)
+    assert (np.abs(s.cpu().numpy() - s0) <= 1e-6 * sabs).all()
+
+
+def test_teacher_forced_sweeps(scram, work):
+    """Each sweep t, fed the oracle's map J_{t-1}, gives the oracle's J_t (up to recorded near ties)."""
+    cfg, a, dev = work
+    J, s = oracle.pm_init(a["Q"], a["K"], cfg.pm_seed)
+    total_ties = total_mism = 0
+    for t in range(1, cfg.iters + 1):
+        Jn, sn, tie, _ = oracle.pm_iteration(a["Q"], a["K"], J, t, cfg.pm_seed, s_prev=s)
+        Jg = scram.patchmatch(dev["Q"], dev["K"], 1, cfg.pm_seed, init=torch.from_numpy(J).cuda(), t0=t)
+        Jg = Jg.cpu().numpy()
+        mism = Jg != Jn
+        assert not (mism & ~tie).any(), f"sweep {t}: {int((mism & ~tie).sum())} mismatches outside near ties"
+        total_ties += int(tie.sum())
+        total_mism += int(mism.sum())
+        J, s = Jn, sn
+    log(f"{cfg.name}: teacher-forced near ties {total_ties}, mismatches at them {total_mism}")
+
+
+@pytest.mark.parametrize("flags", [1, 2], ids=["no_propagation", "no_random_search"])
+def test_teacher_forced_single_step(scram, work, flags):
+    cfg, a, dev = work
+    J, s = oracle.pm_init(a["Q"], a["K"], cfg.pm_seed)
+    for t in (1, 2):
+        Jn, sn, tie, _ = oracle.pm_iteration(a["Q"], a["K"], J, t, cfg.pm_seed, flags=flags, s_prev=s)
+        Jg = scram.patchmatch(dev["Q"], dev["K"], 1, cfg.pm_seed, init=torch.from_numpy(J).cuda(), t0=t,
+                              flags=flags).cpu().numpy()
+        assert not ((Jg != Jn) & ~tie).any()
+        J, s = Jn, sn
+
+
+def test_end_to_end_map(scram, work):
+    cfg, a, dev = work
+    Jg, sg = scram.patchmatch(dev["Q"], dev["K"], cfg.iters, cfg.pm_seed, return_score=True)
+    Jg, sg = Jg.cpu().numpy(), sg.cpu().numpy()
+    Jo, so, ties, nc = oracle.patchmatch(a["Q"], a["K"], cfg.iters, cfg.pm_seed)
+    mism = Jg != Jo
+    allowed = reach_of_ties(ties)
+    assert not (mism & ~allowed).any(), f"{int((mism & ~allowed).sum())} mismatches outside near-tie reach"
+    # the fp32 scores are the scores of the returned keys
+    s_of_g, sabs = oracle.pm_scores(a["Q"], a["K"], Jg)
+    assert (np.abs(sg - s_of_g) <= 1e-6 * sabs).all()
+    Jb, sb = dense.brute_argmax(a["Q"], a["K"]) if cfg.nq <= 8192 else (None, None)
+    rec = float((Jg == Jb).mean()) if Jb is not None else float("nan")
+    log(f"{cfg.name}: end-to-end mismatches {int(mism.sum())} / {mism.size}, near ties {int(ties.sum())}, "
+        f"candidates {nc}, recall vs brute force {rec:.4f}")
+
+
+def test_resume_bit_exact(scram, work):
+    cfg, a, dev = work
+    full, sfull = scram.patchmatch(dev["Q"], dev["K"], cfg.iters, cfg.pm_seed, return_score=True)
+    k = cfg.iters // 2
+    part, spart = scram.patchmatch(dev["Q"], dev["K"], k, cfg.pm_seed, return_score=True)
+    rest, srest = scram.patchmatch(dev["Q"], dev["K"], cfg.iters - k, cfg.pm_seed, init=part,
+                                   init_score=spart, t0=k + 1, return_score=True)
+    rest2 = scram.patchmatch(dev["Q"], dev["K"], cfg.iters - k, cfg.pm_seed, init=part, t0=k + 1)
+    assert torch.equal(full, rest) and torch.equal(full, rest2)
+    assert torch.equal(sfull, srest)
+
+
+def test_repeatable(scram, work):
+    cfg, a, dev = work
+    r1 = scram.patchmatch(dev["Q"], dev["K"], cfg.iters, cfg.pm_seed)
+    r2 = scram.patchmatch(dev["Q"], dev["K"], cfg.iters, cfg.pm_seed)
+    assert torch.equal(r1, r2)
+
+
+def test_attend_parity(scram, work):
+    cfg, a, dev = work
+    J = scram.patchmatch(dev["Q"], dev["K"], cfg.iters, cfg.pm_seed)
+    out = scram.sparse_attend(dev["Q"], dev["K"], dev["V"], J, cfg.window, cfg.scale)
+    ref = oracle.sparse_attend(a["Q"], a["K"], a["V"], J.cpu().numpy(), cfg.window, cfg.scale)
+    err = row_rel_err(out.float().cpu().numpy(), ref)
+    log(f"{cfg.name}: attend max rel err {err.max():.3e}, p99.9 {np.quantile(err, 0.999):.3e}")
+    assert err.max() <= TOL[cfg.dtype]
+
+
+def test_attend_window_one_is_value_gather(scram, work):
+    """b = 0: the output is exactly v at the match."""
+    cfg, a, dev = work
+    J = scram.patchmatch(dev["Q"], dev["K"], 1, cfg.pm_seed)
+    out = scram.sparse_attend(dev["Q"], dev["K"], dev["V"], J, 1, cfg.scale)
+    Vf = dev["V"].reshape(cfg.S, -1, cfg.dv)
+    exp = torch.gather(Vf, 1, J.reshape(cfg.S, -1, 1).long().expand(-1, -1, cfg.dv))
+    assert torch.equal(out.reshape(cfg.S, -1, cfg.dv), exp)
+
+
+# --------------------------------------------------------------------------
+# hand-worked fixtures and closed forms on the GPU
+# --------------------------------------------------------------------------
+def pad(x, d):
+    """Zero-pad the channel axis to d: dot products and value sums are unchanged."""
+    out = np.zeros(x.shape[:-1] + (d,), np.float32)
+    out[..., : x.shape[-1]] = x
+    return out
+
+
+def test_attend_hand_cases(scram):
+    g = json.load(open(os.path.join(GOLDEN, "attend_hand.json")))
+    for c in g["cases"]:
+        d = len(c["q"])
+        dv = len(c["v"][0])
+        Q = pad(np.array(c["q"], np.float32).reshape(1, c["Hq"], c["Wq"], d), 16)
+        K = pad(np.array(c["k"], np.float32).reshape(1, c["Hk"], c["Wk"], d), 16)
+        V = pad(np.array(c["v"], np.float32).reshape(1, c["Hk"], c["Wk"], dv), 16)
+        J = torch.tensor(c["J"], dtype=torch.int32).reshape(1, c["Hq"], c["Wq"]).cuda()
+        out = scram.sparse_attend(to_dev(Q, "f32"), to_dev(K, "f32"), to_dev(V, "f32"), J, c["window"], c["scale"])
+        got = out.cpu().numpy().reshape(-1, 16)[:, :dv]
+        np.testing.assert_allclose(got, np.array(c["expected"]), rtol=1e-5, err_msg=c["note"])
+
+
+def test_propagation_hand_example(scram):
+    g = json.load(open(os.path.join(GOLDEN, "propagation_hand.json")))
+    K = pad(np.array(g["k"], np.float32).reshape(1, g["Hk"], g["Wk"], g["d"]), 16)
+    Kd = to_dev(K, "f32")
+    J = torch.tensor(g["J0"], dtype=torch.int32).reshape(1, g["Hq"], g["Wq"]).cuda()
+    for t in (1, 2):
+        J = scram.patchmatch(Kd, Kd, 1, 0, init=J, t0=t, flags=scram.NO_RANDOM_SEARCH)
+        assert J.cpu().numpy().reshape(-1).tolist() == g["expected"][str(t)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_propagation_closed_form(scram, dtype):
+    """Identity field: the exact-hit set grows by the jump cross each sweep."""
+    rng = np.random.default_rng(11)
+    H, W, d = 37, 29, 32
+    K = rng.standard_normal((1, H, W, d)).astype(np.float32)
+    K /= np.linalg.norm(K, axis=3, keepdims=True)
+    Kd = to_dev(K, dtype)
+    xs, ys = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    J = (((xs + 5) % H) * W + (ys + 3) % W).astype(np.int32)
+    J[20, 7] = 20 * W + 7
+    ident = xs * W + ys
+    hits = J == ident
+    Jd = torch.from_numpy(J[None]).cuda()
+    for t in range(1, 5):
+        Jd = scram.patchmatch(Kd, Kd, 1, 5, init=Jd, t0=t, flags=scram.NO_RANDOM_SEARCH)
+        hits = dilate(hits)
+        np.testing.assert_array_equal(Jd.cpu().numpy()[0] == ident, hits)
+
+
+def test_attend_full_window_is_dense(scram):
+    rng = np.random.default_rng(4)
+    S, Hq, Wq, H, W, d = 2, 5, 6, 9, 7, 32
+    Q = rng.standard_normal((S, Hq, Wq, d)).astype(np.float32)
+    K = rng.standard_normal((S, H, W, d)).astype(np.float32)
+    V = rng.standard_normal((S, H, W, d)).astype(np.float32)
+    J = rng.integers(0, H * W, (S, Hq, Wq)).astype(np.int32)
+    scale = 1 / math.sqrt(d)
+    out = scram.sparse_attend(to_dev(Q, "f32"), to_dev(K, "f32"), to_dev(V, "f32"), torch.from_numpy(J).cuda(),
+                              2 * max(H, W) - 1, scale)
+    ref = dense.dense_attend(Q, K, V, scale)
+    assert row_rel_err(out.cpu().numpy(), ref).max() <= 1e-5
+
+
+# --------------------------------------------------------------------------
+# shapes: every supported width and type, degenerate and ragged grids
+# --------------------------------------------------------------------------
+SHAPES = [
+    # (S, Hq, Wq, Hk, Wk, d, dtype)
+    (1, 1, 1, 1, 1, 16, "f32"),
+    (2, 1, 1, 3, 5, 32, "bf16"),
+    (1, 1, 23, 1, 23, 64, "f32"),
+    (1, 19, 1, 19, 1, 128, "bf16"),
+    (3, 9, 11, 13, 7, 128, "f32"),
+    (2, 17, 13, 17, 13, 16, "bf16"),
+    (1, 33, 31, 20, 50, 64, "bf16"),
+    (5, 7, 9, 7, 9, 32, "f32"),
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s[:-1])) + s[-1])
+def test_shapes(scram, shape):
+    S, Hq, Wq, Hk, Wk, d, dtype = shape
+    base = si.get(0)
+    cfg = dataclasses.replace(base, batch=S, heads=1, Hq=Hq, Wq=Wq, Hk=Hk, Wk=Wk, d=d, dtype=dtype,
+                              sigma=1.0, F=3.0, grid_scale=1.0)
+    a = si.make_arrays(cfg, seed=sum(shape[:-1]))
+    dev = {k: to_dev(a[k], dtype) for k in ("Q", "K", "V")}
+    T = 3
+    Jg = scram.patchmatch(dev["Q"], dev["K"], T, 77).cpu().numpy()
+    Jo, _, ties, _ = oracle.patchmatch(a["Q"], a["K"], T, 77)
+    assert not ((Jg != Jo) & ~reach_of_ties(ties)).any()
+    for window in (1, 3, 7):
+        out = scram.sparse_attend(dev["Q"], dev["K"], dev["V"], torch.from_numpy(Jg).cuda(), window, d ** -0.5)
+        ref = oracle.sparse_attend(a["Q"], a["K"], a["V"], Jg, window, d ** -0.5)
+        assert row_rel_err(out.float().cpu().numpy(), ref).max() <= TOL[dtype]
+
+
+def test_bad_arguments_raise(scram):
+    Q = torch.zeros(1, 4, 4, 24, device="cuda")
+    with pytest.raises(scram.ScramError):
+        scram.patchmatch(Q, Q, 1, 0)
+    Q = torch.zeros(1, 4, 4, 16, device="cuda")
+    with pytest.raises(scram.ScramError):
+        scram.sparse_attend(Q, Q, Q, torch.zeros(1, 4, 4, dtype=torch.int32, device="cuda"), 2)
