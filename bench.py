@@ -105,6 +105,9 @@ def main(argv=None) -> int:
     ap.add_argument("--config", type=int, default=None, help="workload index (default: the 256x256 bf16 one)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="seconds of oracle work for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="before timing, run one plain device copy of this many MiB (a known-size "
+                         "reference kernel for hardware byte counters)")
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
@@ -124,6 +127,15 @@ def main(argv=None) -> int:
         print("bench.py: no GPU visible", file=sys.stderr)
         return 1
     scram.lib()
+    if args.copy_calibration > 0:
+        # an elementwise kernel that reads and writes exactly MIB MiB each (a
+        # same-dtype copy_ would go to the runtime's blit path instead)
+        src = torch.ones(args.copy_calibration << 18, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
     ci = si.HEADLINE if args.config is None else args.config
     cfg = si.get(ci)
     data = si.make(cfg, device="cuda")
