@@ -10,22 +10,24 @@
 //                       fused with the gather of the values
 //
 // Work decomposition.  Every kernel gives one query pixel to a "lane group"
-// of G = row_bytes / 16 lanes of a 64-wide wavefront: each lane owns one
-// 16-byte slice of the query row (4 fp32 or 8 bf16 channels) in registers, so
-// gathering a candidate key row is one coalesced 16-byte load per lane (a
-// 128-byte bf16 d=64 row is 8 lanes x 16 B) and the dot product is a per-lane
-// fp32 FMA chain followed by a fixed butterfly across the group (DPP row
-// permutes).  Every lane of the group ends with the bit-identical sum, so the
-// argmax decisions are taken redundantly in registers with no extra traffic,
-// and the same reduction order is used by the init and the sweep kernels: a
-// score never depends on which kernel computed it.
+// of G lanes of a 64-wide wavefront.  A feature row (d channels) is split
+// into 16-byte chunks; lane l of the group owns chunks l, l+G, l+2G, ... so
+// each load instruction of the group reads one contiguous G*16-byte span of
+// the row (fully coalesced), and q stays in registers in its storage format.
+// A dot product is a per-lane chain in a fixed order -- v_dot2_f32_bf16 on
+// packed bf16 pairs, or fp32 FMAs -- then a fixed butterfly across the group
+// (DPP row permutes).  Every lane of the group ends with the bit-identical
+// sum, so decisions are taken redundantly in registers, and the init and
+// sweep kernels use the same order: a score never depends on which kernel
+// computed it.
 //
-// Candidate gathers are not a dense contraction, so there is no MFMA here;
-// the sweeps are bound by the memory system (HBM / Infinity Cache / L2).
+// Candidate gathers are not a dense contraction, so there is no MFMA here.
 // Blocks are remapped so that consecutive query ranges land on the same XCD
 // and share its L2.
 
 #include <stdint.h>
+
+#include <type_traits>
 
 #include <hip/hip_runtime.h>
 
@@ -100,75 +102,72 @@ __device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_
 }
 
 // ---------------------------------------------------------------------------
-// element / row helpers
+// rows: storage type T (float, or bfloat16 held as uint16_t), D channels,
+// G lanes per query
 // ---------------------------------------------------------------------------
-template <typename T>
-struct Elem;
-template <>
-struct Elem<float> {
-    static constexpr int kPer16 = 4;
-};
-template <>
-struct Elem<uint16_t> {  // bfloat16 storage
-    static constexpr int kPer16 = 8;
-};
-
-template <typename T, int D>
-struct Layout {
-    static constexpr int kEpl = Elem<T>::kPer16;  // channels per lane
-    static constexpr int kG = D / kEpl;           // lanes per query
-    static constexpr int kQpb = kBlock / kG;      // queries per block
-    static_assert(kG >= 2 && kG <= 32 && (kG & (kG - 1)) == 0, "lane group must be 2..32 lanes");
+template <typename T, int D, int G>
+struct Row {
+    static constexpr int kBytes = D * static_cast<int>(sizeof(T));
+    static constexpr int kCh = kBytes / (16 * G);  // 16-byte chunks per lane
+    static constexpr int kEpc = 16 / static_cast<int>(sizeof(T));  // channels per chunk
+    static constexpr int kQpb = kBlock / G;        // queries per block
+    static_assert(G >= 1 && G <= 32 && (G & (G - 1)) == 0, "lane group must be 1..32 lanes");
+    static_assert(kCh >= 1 && kCh * 16 * G == kBytes, "row must split into whole chunks per lane");
 };
 
-template <typename T>
-__device__ __forceinline__ void unpack(const uint4& r, float* f);
-
-template <>
-__device__ __forceinline__ void unpack<float>(const uint4& r, float* f)
+// The lane's chunks of row `row` of a [rows, D] array.
+template <typename T, int D, int G>
+__device__ __forceinline__ void load_row(const T* base, uint32_t row, int lane, uint4 (&v)[Row<T, D, G>::kCh])
 {
-    f[0] = __uint_as_float(r.x);
-    f[1] = __uint_as_float(r.y);
-    f[2] = __uint_as_float(r.z);
-    f[3] = __uint_as_float(r.w);
-}
-
-// bf16 -> fp32 is exact: the bf16 bits are the upper half of the fp32 bits.
-template <>
-__device__ __forceinline__ void unpack<uint16_t>(const uint4& r, float* f)
-{
-    const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+    const uint4* p = reinterpret_cast<const uint4*>(base + static_cast<size_t>(row) * D) + lane;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        f[2 * i] = __uint_as_float(w[i] << 16);
-        f[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
-    }
+    for (int c = 0; c < Row<T, D, G>::kCh; ++c) v[c] = p[c * G];
 }
 
-// One lane's 16-byte slice of row `row` of a [rows, D] array.
-template <typename T, int D>
-__device__ __forceinline__ uint4 load_slice(const T* base, uint32_t row, int lane)
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c)
 {
-    return reinterpret_cast<const uint4*>(base + static_cast<size_t>(row) * D)[lane];
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), c,
+                                           false);
 }
 
 // Per-lane partial dot product in a fixed order.
-template <typename T>
-__device__ __forceinline__ float slice_dot(const float* q, const uint4& raw)
+template <typename T, int CH>
+__device__ __forceinline__ float lane_dot(const uint4 (&q)[CH], const uint4 (&k)[CH])
 {
-    constexpr int E = Elem<T>::kPer16;
-    float k[E];
-    unpack<T>(raw, k);
-    float acc = q[0] * k[0];
+    if constexpr (std::is_same<T, uint16_t>::value) {
+        float acc = 0.f;
 #pragma unroll
-    for (int e = 1; e < E; ++e) acc = fmaf(q[e], k[e], acc);
-    return acc;
+        for (int c = 0; c < CH; ++c) {
+            acc = dot2_bf16(q[c].x, k[c].x, acc);
+            acc = dot2_bf16(q[c].y, k[c].y, acc);
+            acc = dot2_bf16(q[c].z, k[c].z, acc);
+            acc = dot2_bf16(q[c].w, k[c].w, acc);
+        }
+        return acc;
+    } else {
+        float acc = __uint_as_float(q[0].x) * __uint_as_float(k[0].x);
+        acc = fmaf(__uint_as_float(q[0].y), __uint_as_float(k[0].y), acc);
+        acc = fmaf(__uint_as_float(q[0].z), __uint_as_float(k[0].z), acc);
+        acc = fmaf(__uint_as_float(q[0].w), __uint_as_float(k[0].w), acc);
+#pragma unroll
+        for (int c = 1; c < CH; ++c) {
+            acc = fmaf(__uint_as_float(q[c].x), __uint_as_float(k[c].x), acc);
+            acc = fmaf(__uint_as_float(q[c].y), __uint_as_float(k[c].y), acc);
+            acc = fmaf(__uint_as_float(q[c].z), __uint_as_float(k[c].z), acc);
+            acc = fmaf(__uint_as_float(q[c].w), __uint_as_float(k[c].w), acc);
+        }
+        return acc;
+    }
 }
 
+// Value of a partner lane inside the row (every pattern used here stays
+// inside the group, so bound_ctrl never applies).
 template <int CTRL>
 __device__ __forceinline__ float dpp(float x)
 {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, true));
 }
 
 // Sum over an aligned group of G lanes.  Each step adds the value of a
@@ -186,6 +185,12 @@ __device__ __forceinline__ float group_sum(float x)
     return x;
 }
 
+template <typename T, int D, int G>
+__device__ __forceinline__ float row_score(const uint4 (&q)[Row<T, D, G>::kCh], const uint4 (&k)[Row<T, D, G>::kCh])
+{
+    return group_sum<G>(lane_dot<T, Row<T, D, G>::kCh>(q, k));
+}
+
 // Higher score wins; equal scores go to the lower flat key index.
 __device__ __forceinline__ bool better(float s, int32_t i, float bs, int32_t bi)
 {
@@ -198,6 +203,30 @@ __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f)
     u += 0x7FFFu + ((u >> 16) & 1u);
     return u >> 16;
 }
+
+// Lanes per query: a row is split so that each lane holds kLaneBytes of it
+// (one lane per query when the row is shorter).  Fewer lanes per query means
+// fewer per-query instructions replicated across the group; more lanes means
+// fewer distinct cache lines per load instruction.
+#ifndef SCRAM_PM_LANE_BYTES
+#define SCRAM_PM_LANE_BYTES 32
+#endif
+#ifndef SCRAM_ATTEND_LANE_BYTES
+#define SCRAM_ATTEND_LANE_BYTES 32
+#endif
+
+template <typename T, int D, int LANE_BYTES>
+struct LanesFor {
+    static constexpr int kBytes = D * static_cast<int>(sizeof(T));
+    static constexpr int kG0 = kBytes > LANE_BYTES ? kBytes / LANE_BYTES : 1;
+    static constexpr int kG = kG0 > 32 ? 32 : kG0;
+};
+
+template <typename T, int D>
+struct Lanes {
+    static constexpr int kPm = LanesFor<T, D, SCRAM_PM_LANE_BYTES>::kG;
+    static constexpr int kAttend = LanesFor<T, D, SCRAM_ATTEND_LANE_BYTES>::kG;
+};
 
 // ---------------------------------------------------------------------------
 // kernel parameters
@@ -238,12 +267,12 @@ struct AttParams {
 // ---------------------------------------------------------------------------
 // K1: initial field and its scores
 // ---------------------------------------------------------------------------
-template <typename T, int D>
+template <typename T, int D, int G>
 __global__ __launch_bounds__(kBlock) void pm_init_kernel(PmParams p)
 {
-    using L = Layout<T, D>;
-    const int lane = threadIdx.x & (L::kG - 1);
-    const uint32_t g = blockIdx.x * L::kQpb + threadIdx.x / L::kG;
+    using RW = Row<T, D, G>;
+    const int lane = threadIdx.x & (G - 1);
+    const uint32_t g = blockIdx.x * RW::kQpb + threadIdx.x / G;
     if (g >= p.n) return;  // whole lane groups leave together
     uint32_t s, rem;
     divmod(g, p.div_plane, s, rem);
@@ -258,9 +287,10 @@ __global__ __launch_bounds__(kBlock) void pm_init_kernel(PmParams p)
         idx = static_cast<int32_t>(u * p.Wk + v);
     }
     const T* Ks = static_cast<const T*>(p.K) + static_cast<size_t>(s) * p.nkeys * D;
-    float q[L::kEpl];
-    unpack<T>(load_slice<T, D>(static_cast<const T*>(p.Q), g, lane), q);
-    const float sc = group_sum<L::kG>(slice_dot<T>(q, load_slice<T, D>(Ks, idx, lane)));
+    uint4 q[RW::kCh], k[RW::kCh];
+    load_row<T, D, G>(static_cast<const T*>(p.Q), g, lane, q);
+    load_row<T, D, G>(Ks, idx, lane, k);
+    const float sc = row_score<T, D, G>(q, k);
     if (lane == 0) {
         if (p.Jn) p.Jn[g] = idx;
         p.sn[g] = sc;
@@ -270,23 +300,30 @@ __global__ __launch_bounds__(kBlock) void pm_init_kernel(PmParams p)
 // ---------------------------------------------------------------------------
 // K2: one Jacobi sweep (propagation + random search), (Jp, sp) -> (Jn, sn)
 // ---------------------------------------------------------------------------
-template <typename T, int D, bool PROP, bool RS>
+template <typename T, int D, int G, bool PROP, bool RS>
 __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
 {
-    using L = Layout<T, D>;
-    constexpr int G = L::kG;
+    using RW = Row<T, D, G>;
+    constexpr int CH = RW::kCh;
+    constexpr int kNb = 4;  // propagation candidates gathered per batch
+    __shared__ int32_t s_list[PROP ? RW::kQpb * 16 : 1];
+
     const int lane = threadIdx.x & (G - 1);
+    const int qslot = threadIdx.x / G;
     const int gbase = (threadIdx.x & 63) - lane;  // wave lane of the group's first lane
     const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
-    const uint32_t g = blk * L::kQpb + threadIdx.x / G;
-    if (g >= p.n) return;  // whole lane groups leave together
+    const uint32_t g_raw = blk * RW::kQpb + qslot;
+    const bool live = g_raw < p.n;
+    // groups past the end work on the last query and write nothing, so every
+    // lane reaches the block barrier below
+    const uint32_t g = live ? g_raw : p.n - 1;
 
     uint32_t s, rem, x, y;
     divmod(g, p.div_plane, s, rem);
     divmod(rem, p.div_wq, x, y);
     const T* Ks = static_cast<const T*>(p.K) + static_cast<size_t>(s) * p.nkeys * D;
-    float q[L::kEpl];
-    unpack<T>(load_slice<T, D>(static_cast<const T*>(p.Q), g, lane), q);
+    uint4 q[CH];
+    load_row<T, D, G>(static_cast<const T*>(p.Q), g, lane, q);
     int32_t cur = clamp_index(p.Jp[g], p.nkeys);
     float best = p.sp[g];
 
@@ -294,9 +331,13 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
         // Lane l of the group forms candidates l, l + G, ... of the 16
         // (jump index i/4 over 8,4,2,1; direction i%4 over row-1, row+1,
         // col-1, col+1): the neighbour's match shifted back by the offset.
+        // Candidates outside the grids, or equal to the incumbent (which
+        // cannot win), are dropped; the rest are compacted into this
+        // query's list in shared memory.
         constexpr int kSlots = (16 + G - 1) / G;
         const int32_t* Jps = p.Jp + static_cast<size_t>(s) * p.plane_q;
-        int32_t cand[kSlots];
+        const int32_t cur0 = cur;
+        int count = 0;
 #pragma unroll
         for (int m = 0; m < kSlots; ++m) {
             const int i = lane + m * G;
@@ -315,30 +356,39 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
                     if (r >= 0 && r < p.Hk && cc >= 0 && cc < p.Wk) c = r * p.Wk + cc;
                 }
             }
-            cand[m] = c;
+            const bool keep = c >= 0 && c != cur0;
+            const uint64_t bal = __ballot(keep);
+            const uint32_t grp = static_cast<uint32_t>(bal >> gbase) & (G == 32 ? 0xFFFFFFFFu : ((1u << G) - 1u));
+            if (keep) s_list[qslot * 16 + count + __popc(grp & ((1u << lane) - 1u))] = c;
+            count += __popc(grp);
         }
-        // The 16 candidates do not depend on each other: gather them four at
-        // a time with all loads in flight before the first dot product.  A
-        // candidate equal to the incumbent cannot win and is not gathered.
-        const int32_t cur0 = cur;
+        __syncthreads();
+
+        // Gather the surviving candidates kNb at a time: all loads in
+        // flight, then the dot products (independent chains), then the
+        // comparisons in list order.  Slots past the end of a query's list
+        // keep stale data whose score is never used.
+        uint4 raw[kNb][CH];
 #pragma unroll
-        for (int i0 = 0; i0 < 16; i0 += 4) {
-            int32_t c[4];
-            uint4 raw[4];
+        for (int j = 0; j < kNb; ++j)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int i = i0 + j;
-                c[j] = __shfl(cand[i / G], gbase + (i % G));
-                if (c[j] >= 0 && c[j] != cur0) raw[j] = load_slice<T, D>(Ks, c[j], lane);
+            for (int c = 0; c < CH; ++c) raw[j][c] = make_uint4(0u, 0u, 0u, 0u);
+        for (int k0 = 0; __any(k0 < count); k0 += kNb) {
+            int32_t idx[kNb];
+#pragma unroll
+            for (int j = 0; j < kNb; ++j) {
+                const int kk = k0 + j;
+                idx[j] = kk < count ? s_list[qslot * 16 + (kk & 15)] : cur0;
+                if (kk < count) load_row<T, D, G>(Ks, idx[j], lane, raw[j]);
             }
+            float sc[kNb];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                if (c[j] >= 0 && c[j] != cur0) {
-                    const float sc = group_sum<G>(slice_dot<T>(q, raw[j]));
-                    if (better(sc, c[j], best, cur)) {
-                        best = sc;
-                        cur = c[j];
-                    }
+            for (int j = 0; j < kNb; ++j) sc[j] = row_score<T, D, G>(q, raw[j]);
+#pragma unroll
+            for (int j = 0; j < kNb; ++j) {
+                if (k0 + j < count && better(sc[j], idx[j], best, cur)) {
+                    best = sc[j];
+                    cur = idx[j];
                 }
             }
         }
@@ -372,7 +422,9 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
                         const uint32_t c = lo_c + __umulhi(wc, static_cast<uint32_t>(hi_c - lo_c + 1));
                         const int32_t idx = static_cast<int32_t>(r * p.Wk + c);
                         if (idx != cur) {
-                            const float sc = group_sum<G>(slice_dot<T>(q, load_slice<T, D>(Ks, idx, lane)));
+                            uint4 kr[CH];
+                            load_row<T, D, G>(Ks, idx, lane, kr);
+                            const float sc = row_score<T, D, G>(q, kr);
                             if (better(sc, idx, best, cur)) {
                                 best = sc;
                                 cur = idx;
@@ -386,25 +438,73 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
         }
     }
 
-    if (lane == 0) {
+    if (live && lane == 0) {
         p.Jn[g] = cur;
         p.sn[g] = best;
     }
 }
 
 // ---------------------------------------------------------------------------
-// K4: window softmax + value gather (online softmax, one window row of up to
-// kNb keys per step; all key and value loads of a step issued together)
+// K4: window softmax + value gather
 // ---------------------------------------------------------------------------
-template <typename T, int D>
-__global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
+
+// acc[e] += pj * v[e] over the lane's channels of one value row.
+template <typename T, int CH>
+__device__ __forceinline__ void accumulate_row(float* acc, float pj, const uint4 (&vr)[CH])
 {
-    using L = Layout<T, D>;
-    constexpr int E = L::kEpl;
-    constexpr int kNb = 8;
-    const int lane = threadIdx.x & (L::kG - 1);
+#pragma unroll
+    for (int cc = 0; cc < CH; ++cc) {
+        const uint32_t w[4] = {vr[cc].x, vr[cc].y, vr[cc].z, vr[cc].w};
+        if constexpr (std::is_same<T, uint16_t>::value) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                acc[cc * 8 + 2 * i] = fmaf(pj, __uint_as_float(w[i] << 16), acc[cc * 8 + 2 * i]);
+                acc[cc * 8 + 2 * i + 1] = fmaf(pj, __uint_as_float(w[i] & 0xFFFF0000u), acc[cc * 8 + 2 * i + 1]);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[cc * 4 + i] = fmaf(pj, __uint_as_float(w[i]), acc[cc * 4 + i]);
+        }
+    }
+}
+
+// out row slice = acc * inv in the storage type.
+template <typename T, int D, int G>
+__device__ __forceinline__ void store_row(void* out, uint32_t g, int lane, const float* acc, float inv)
+{
+    constexpr int CH = Row<T, D, G>::kCh;
+    uint4* o = reinterpret_cast<uint4*>(static_cast<T*>(out) + static_cast<size_t>(g) * D) + lane;
+#pragma unroll
+    for (int cc = 0; cc < CH; ++cc) {
+        if constexpr (std::is_same<T, uint16_t>::value) {
+            uint32_t w[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                w[i] = f32_to_bf16_rne(acc[cc * 8 + 2 * i] * inv) |
+                       (f32_to_bf16_rne(acc[cc * 8 + 2 * i + 1] * inv) << 16);
+            o[cc * G] = make_uint4(w[0], w[1], w[2], w[3]);
+        } else {
+            o[cc * G] = make_uint4(__float_as_uint(acc[cc * 4] * inv), __float_as_uint(acc[cc * 4 + 1] * inv),
+                                   __float_as_uint(acc[cc * 4 + 2] * inv), __float_as_uint(acc[cc * 4 + 3] * inv));
+        }
+    }
+}
+
+// Fixed window side W (odd), one window row per step: the W key rows and W
+// value rows of a window row are gathered together (2W loads in flight),
+// then the W scores (base-2 domain), one online-softmax rescale, and the
+// value accumulation.  Keys outside the grid read a clamped (valid) row and
+// get weight 0; window rows entirely outside the grid are skipped.
+template <typename T, int D, int G, int W>
+__global__ __launch_bounds__(kBlock) void attend_window_kernel(AttParams p)
+{
+    using RW = Row<T, D, G>;
+    constexpr int CH = RW::kCh;
+    constexpr int E = CH * RW::kEpc;  // channels per lane
+    constexpr int B = W / 2;
+    const int lane = threadIdx.x & (G - 1);
     const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
-    const uint32_t g = blk * L::kQpb + threadIdx.x / L::kG;
+    const uint32_t g = blk * RW::kQpb + threadIdx.x / G;
     if (g >= p.n) return;
 
     uint32_t s, rem;
@@ -412,71 +512,129 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
     const size_t slice = static_cast<size_t>(s) * p.nkeys * D;
     const T* Ks = static_cast<const T*>(p.K) + slice;
     const T* Vs = static_cast<const T*>(p.V) + slice;
-    float q[E];
-    unpack<T>(load_slice<T, D>(static_cast<const T*>(p.Q), g, lane), q);
+    uint4 q[CH];
+    load_row<T, D, G>(static_cast<const T*>(p.Q), g, lane, q);
     uint32_t u, v;
     divmod(static_cast<uint32_t>(clamp_index(p.J[g], p.nkeys)), p.div_wk, u, v);
-    const int r0 = max(static_cast<int>(u) - p.b, 0), r1 = min(static_cast<int>(u) + p.b, p.Hk - 1);
-    const int c0 = max(static_cast<int>(v) - p.b, 0), c1 = min(static_cast<int>(v) + p.b, p.Wk - 1);
+
+    // column of each window column, clamped, and whether it is inside
+    int cols[W];
+    bool col_ok[W];
+#pragma unroll
+    for (int c = 0; c < W; ++c) {
+        const int col = static_cast<int>(v) + c - B;
+        col_ok[c] = col >= 0 && col < p.Wk;
+        cols[c] = min(max(col, 0), p.Wk - 1);
+    }
 
     float m = -INFINITY, l = 0.f;
     float acc[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[e] = 0.f;
 
-    for (int r = r0; r <= r1; ++r) {
-        for (int cb = c0; cb <= c1; cb += kNb) {
-            const int nk = min(kNb, c1 - cb + 1);
-            const uint32_t row0 = static_cast<uint32_t>(r * p.Wk + cb);
-            uint4 kr[kNb], vr[kNb];
+    for (int a = 0; a < W; ++a) {
+        const int r = static_cast<int>(u) + a - B;
+        if (r < 0 || r >= p.Hk) continue;
+        const uint32_t row0 = static_cast<uint32_t>(r * p.Wk);
+        uint4 kr[W][CH], vr[W][CH];
 #pragma unroll
-            for (int j = 0; j < kNb; ++j) {
-                if (j < nk) {
-                    kr[j] = load_slice<T, D>(Ks, row0 + j, lane);
-                    vr[j] = load_slice<T, D>(Vs, row0 + j, lane);
-                }
-            }
-            float sc[kNb];
-            float mb = m;
-#pragma unroll
-            for (int j = 0; j < kNb; ++j) {
-                if (j < nk) {
-                    sc[j] = group_sum<L::kG>(slice_dot<T>(q, kr[j])) * p.scale_log2e;
-                    mb = fmaxf(mb, sc[j]);
-                }
-            }
-            const float alpha = __builtin_amdgcn_exp2f(m - mb);
-            l *= alpha;
-#pragma unroll
-            for (int e = 0; e < E; ++e) acc[e] *= alpha;
-#pragma unroll
-            for (int j = 0; j < kNb; ++j) {
-                if (j < nk) {
-                    const float pj = __builtin_amdgcn_exp2f(sc[j] - mb);
-                    l += pj;
-                    float vv[E];
-                    unpack<T>(vr[j], vv);
-#pragma unroll
-                    for (int e = 0; e < E; ++e) acc[e] = fmaf(pj, vv[e], acc[e]);
-                }
-            }
-            m = mb;
+        for (int c = 0; c < W; ++c) {
+            load_row<T, D, G>(Ks, row0 + cols[c], lane, kr[c]);
+            load_row<T, D, G>(Vs, row0 + cols[c], lane, vr[c]);
         }
-    }
-
-    const float inv = 1.f / l;
-    uint4 o;
-    if constexpr (E == 4) {
-        o = make_uint4(__float_as_uint(acc[0] * inv), __float_as_uint(acc[1] * inv),
-                       __float_as_uint(acc[2] * inv), __float_as_uint(acc[3] * inv));
-    } else {
-        uint32_t w[4];
+        float sc[W];
+        float mb = m;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            w[i] = f32_to_bf16_rne(acc[2 * i] * inv) | (f32_to_bf16_rne(acc[2 * i + 1] * inv) << 16);
-        o = make_uint4(w[0], w[1], w[2], w[3]);
+        for (int c = 0; c < W; ++c) {
+            sc[c] = col_ok[c] ? row_score<T, D, G>(q, kr[c]) * p.scale_log2e : -INFINITY;
+            mb = fmaxf(mb, sc[c]);
+        }
+        const float alpha = __builtin_amdgcn_exp2f(m - mb);  // 0 on the first row
+        l *= alpha;
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] *= alpha;
+#pragma unroll
+        for (int c = 0; c < W; ++c) {
+            const float pj = __builtin_amdgcn_exp2f(sc[c] - mb);  // exp2(-inf) = 0
+            l += pj;
+            accumulate_row<T, CH>(acc, pj, vr[c]);
+        }
+        m = mb;
     }
-    reinterpret_cast<uint4*>(static_cast<T*>(p.out) + static_cast<size_t>(g) * D)[lane] = o;
+    store_row<T, D, G>(p.out, g, lane, acc, 1.f / l);
+}
+
+// Any window side: the clipped window is visited in row order, kNb keys at a
+// time with their key and value loads in flight together; an online softmax
+// keeps (running max m, running sum l, accumulator) in the base-2 domain.
+template <typename T, int D, int G>
+__global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
+{
+    using RW = Row<T, D, G>;
+    constexpr int CH = RW::kCh;
+    constexpr int E = CH * RW::kEpc;
+    constexpr int kNb = CH >= 2 ? 4 : 8;
+    const int lane = threadIdx.x & (G - 1);
+    const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+    const uint32_t g = blk * RW::kQpb + threadIdx.x / G;
+    if (g >= p.n) return;
+
+    uint32_t s, rem;
+    divmod(g, p.div_plane, s, rem);
+    const size_t slice = static_cast<size_t>(s) * p.nkeys * D;
+    const T* Ks = static_cast<const T*>(p.K) + slice;
+    const T* Vs = static_cast<const T*>(p.V) + slice;
+    uint4 q[CH];
+    load_row<T, D, G>(static_cast<const T*>(p.Q), g, lane, q);
+    uint32_t u, v;
+    divmod(static_cast<uint32_t>(clamp_index(p.J[g], p.nkeys)), p.div_wk, u, v);
+    const int r0 = max(static_cast<int>(u) - p.b, 0), r1 = min(static_cast<int>(u) + p.b, p.Hk - 1);
+    const int c0 = max(static_cast<int>(v) - p.b, 0), c1 = min(static_cast<int>(v) + p.b, p.Wk - 1);
+    const int nwin = (r1 - r0 + 1) * (c1 - c0 + 1);
+    const uint32_t centre = u * p.Wk + v;
+
+    float m = -INFINITY, l = 0.f;
+    float acc[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = 0.f;
+
+    // (r, c) walks the clipped window in row order; slots past its end read
+    // the centre row and get weight 0
+    int r = r0, c = c0;
+    for (int k0 = 0; k0 < nwin; k0 += kNb) {
+        uint4 kr[kNb][CH], vr[kNb][CH];
+        bool ok[kNb];
+#pragma unroll
+        for (int j = 0; j < kNb; ++j) {
+            ok[j] = k0 + j < nwin;
+            const uint32_t row = ok[j] ? static_cast<uint32_t>(r * p.Wk + c) : centre;
+            load_row<T, D, G>(Ks, row, lane, kr[j]);
+            load_row<T, D, G>(Vs, row, lane, vr[j]);
+            if (ok[j] && ++c > c1) {
+                c = c0;
+                ++r;
+            }
+        }
+        float sc[kNb];
+        float mb = m;
+#pragma unroll
+        for (int j = 0; j < kNb; ++j) {
+            sc[j] = ok[j] ? row_score<T, D, G>(q, kr[j]) * p.scale_log2e : -INFINITY;
+            mb = fmaxf(mb, sc[j]);
+        }
+        const float alpha = __builtin_amdgcn_exp2f(m - mb);
+        l *= alpha;
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] *= alpha;
+#pragma unroll
+        for (int j = 0; j < kNb; ++j) {
+            const float pj = __builtin_amdgcn_exp2f(sc[j] - mb);
+            l += pj;
+            accumulate_row<T, CH>(acc, pj, vr[j]);
+        }
+        m = mb;
+    }
+    store_row<T, D, G>(p.out, g, lane, acc, 1.f / l);
 }
 
 // ---------------------------------------------------------------------------
@@ -509,36 +667,42 @@ PmParams make_pm_params(const void* Q, const void* K, const Grid& gr, uint64_t s
 template <typename T, int D>
 hipError_t run_init(const PmParams& p, hipStream_t st)
 {
-    using L = Layout<T, D>;
-    const uint32_t blocks = (p.n + L::kQpb - 1) / L::kQpb;
-    hipLaunchKernelGGL((pm_init_kernel<T, D>), dim3(blocks), dim3(kBlock), 0, st, p);
+    constexpr int G = Lanes<T, D>::kPm;
+    const uint32_t blocks = (p.n + Row<T, D, G>::kQpb - 1) / Row<T, D, G>::kQpb;
+    hipLaunchKernelGGL((pm_init_kernel<T, D, G>), dim3(blocks), dim3(kBlock), 0, st, p);
     return hipGetLastError();
 }
 
 template <typename T, int D>
 hipError_t run_iter(const PmParams& p, uint32_t flags, hipStream_t st)
 {
-    using L = Layout<T, D>;
-    const uint32_t blocks = (p.n + L::kQpb - 1) / L::kQpb;
+    constexpr int G = Lanes<T, D>::kPm;
+    const uint32_t blocks = (p.n + Row<T, D, G>::kQpb - 1) / Row<T, D, G>::kQpb;
     const bool prop = !(flags & SCRAM_PM_NO_PROPAGATION);
     const bool rs = !(flags & SCRAM_PM_NO_RANDOM_SEARCH);
     if (prop && rs)
-        hipLaunchKernelGGL((pm_iter_kernel<T, D, true, true>), dim3(blocks), dim3(kBlock), 0, st, p);
+        hipLaunchKernelGGL((pm_iter_kernel<T, D, G, true, true>), dim3(blocks), dim3(kBlock), 0, st, p);
     else if (prop)
-        hipLaunchKernelGGL((pm_iter_kernel<T, D, true, false>), dim3(blocks), dim3(kBlock), 0, st, p);
+        hipLaunchKernelGGL((pm_iter_kernel<T, D, G, true, false>), dim3(blocks), dim3(kBlock), 0, st, p);
     else if (rs)
-        hipLaunchKernelGGL((pm_iter_kernel<T, D, false, true>), dim3(blocks), dim3(kBlock), 0, st, p);
+        hipLaunchKernelGGL((pm_iter_kernel<T, D, G, false, true>), dim3(blocks), dim3(kBlock), 0, st, p);
     else
-        hipLaunchKernelGGL((pm_iter_kernel<T, D, false, false>), dim3(blocks), dim3(kBlock), 0, st, p);
+        hipLaunchKernelGGL((pm_iter_kernel<T, D, G, false, false>), dim3(blocks), dim3(kBlock), 0, st, p);
     return hipGetLastError();
 }
 
 template <typename T, int D>
-hipError_t run_attend(const AttParams& p, hipStream_t st)
+hipError_t run_attend(const AttParams& p, int window, hipStream_t st)
 {
-    using L = Layout<T, D>;
-    const uint32_t blocks = (p.n + L::kQpb - 1) / L::kQpb;
-    hipLaunchKernelGGL((attend_kernel<T, D>), dim3(blocks), dim3(kBlock), 0, st, p);
+    constexpr int G = Lanes<T, D>::kAttend;
+    const uint32_t blocks = (p.n + Row<T, D, G>::kQpb - 1) / Row<T, D, G>::kQpb;
+    switch (window) {
+        case 1: hipLaunchKernelGGL((attend_window_kernel<T, D, G, 1>), dim3(blocks), dim3(kBlock), 0, st, p); break;
+        case 3: hipLaunchKernelGGL((attend_window_kernel<T, D, G, 3>), dim3(blocks), dim3(kBlock), 0, st, p); break;
+        case 5: hipLaunchKernelGGL((attend_window_kernel<T, D, G, 5>), dim3(blocks), dim3(kBlock), 0, st, p); break;
+        case 7: hipLaunchKernelGGL((attend_window_kernel<T, D, G, 7>), dim3(blocks), dim3(kBlock), 0, st, p); break;
+        default: hipLaunchKernelGGL((attend_kernel<T, D, G>), dim3(blocks), dim3(kBlock), 0, st, p); break;
+    }
     return hipGetLastError();
 }
 
@@ -611,7 +775,7 @@ hipError_t launch_attend(int dtype, const void* Q, const void* K, const void* V,
     p.b = window / 2;
     p.scale_log2e = scale * 1.4426950408889634f;
     return dispatch(dtype, g.d, [&](auto ty, auto d) {
-        return run_attend<decltype(ty), decltype(d)::value>(p, stream);
+        return run_attend<decltype(ty), decltype(d)::value>(p, window, stream);
     });
 }
 

@@ -26,6 +26,9 @@ pytestmark = pytest.mark.gpu
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 TOL = {"f32": 1e-5, "bf16": 1e-2}
+# fp32 score vs fp64: at most (roundings on the longest summation path) * 2^-24 * sum|q_e k_e|;
+# every lane split built here has at most 40 roundings on that path
+SCORE_TOL = 40 * 2.0 ** -24
 
 
 @pytest.fixture(scope="module")
@@ -100,7 +103,7 @@ def test_init_bit_exact(scram, work):
     J0, s0 = oracle.pm_init(a["Q"], a["K"], cfg.pm_seed)
     np.testing.assert_array_equal(J.cpu().numpy(), J0)
     _, sabs = oracle.pm_scores(a["Q"], a["K"], J0)
-    assert (np.abs(s.cpu().numpy() - s0) <= 1e-6 * sabs).all()
+    assert (np.abs(s.cpu().numpy() - s0) <= SCORE_TOL * sabs).all()
 
 
 def test_teacher_forced_sweeps(scram, work):
@@ -142,7 +145,7 @@ def test_end_to_end_map(scram, work):
     assert not (mism & ~allowed).any(), f"{int((mism & ~allowed).sum())} mismatches outside near-tie reach"
     # the fp32 scores are the scores of the returned keys
     s_of_g, sabs = oracle.pm_scores(a["Q"], a["K"], Jg)
-    assert (np.abs(sg - s_of_g) <= 1e-6 * sabs).all()
+    assert (np.abs(sg - s_of_g) <= SCORE_TOL * sabs).all()
     Jb, sb = dense.brute_argmax(a["Q"], a["K"]) if cfg.nq <= 8192 else (None, None)
     rec = float((Jg == Jb).mean()) if Jb is not None else float("nan")
     log(f"{cfg.name}: end-to-end mismatches {int(mism.sum())} / {mism.size}, near ties {int(ties.sum())}, "
@@ -284,7 +287,7 @@ def test_shapes(scram, shape):
     Jg = scram.patchmatch(dev["Q"], dev["K"], T, 77).cpu().numpy()
     Jo, _, ties, _ = oracle.patchmatch(a["Q"], a["K"], T, 77)
     assert not ((Jg != Jo) & ~reach_of_ties(ties)).any()
-    for window in (1, 3, 7):
+    for window in (1, 3, 7, 9):
         out = scram.sparse_attend(dev["Q"], dev["K"], dev["V"], torch.from_numpy(Jg).cuda(), window, d ** -0.5)
         ref = oracle.sparse_attend(a["Q"], a["K"], a["V"], Jg, window, d ** -0.5)
         assert row_rel_err(out.float().cpu().numpy(), ref).max() <= TOL[dtype]
