@@ -122,13 +122,21 @@ size_t scram_patchmatch_workspace_bytes(int S, int Hq, int Wq);
  *   score_out   nullable fp32 [S, Hq, Wq] final scores q . k_{J_T} (unscaled)
  *   workspace   >= scram_patchmatch_workspace_bytes(S, Hq, Wq) bytes of
  *               device memory, contents ignored and overwritten
+ *   events      nullable array of 2 * (iters + 1) caller-created HIP
+ *               events, for timing the kernels: the dispatch of launch k
+ *               stamps events[2k] with its start and events[2k + 1] with its
+ *               end (k = 0: the initial map or its scores; k = 1..iters:
+ *               sweep k).  When init and init_score are both given nothing
+ *               is launched for k = 0 and events[0], events[1] are recorded
+ *               back to back.  The library does not create, wait on or
+ *               destroy them.
  * Outputs must not overlap each other, the inputs or the workspace
  * (SCRAM_ERR_ALIAS).  Returns a status code.
  */
 int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int Wq, int Hk, int Wk,
                      int d, int iters, uint64_t seed, const int32_t* init, const float* init_score,
                      int t0, uint32_t flags, int32_t* argmax_out, float* score_out, void* workspace,
-                     size_t workspace_bytes, hipStream_t stream);
+                     size_t workspace_bytes, hipEvent_t* events, hipStream_t stream);
 
 /*
  * Sparse attention around the argmax (Algorithm 2 with kappa = 1,
@@ -144,11 +152,13 @@ int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int
  *   window    odd side 2b + 1 >= 1 of the square window (<= 32767)
  *   scale     softmax temperature, 1/sqrt(d_k) for Equation 1; finite
  *   out       [S, Hq, Wq, dv] in `dtype` (written; must not overlap inputs)
+ *   events    nullable array of 2 caller-created HIP events stamped with the
+ *             kernel's start and end (as in scram_patchmatch)
  * Returns a status code.
  */
 int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype,
                         const int32_t* argmax, int S, int Hq, int Wq, int Hk, int Wk, int d, int dv,
-                        int window, float scale, void* out, hipStream_t stream);
+                        int window, float scale, void* out, hipEvent_t* events, hipStream_t stream);
 
 /* Static, NUL-terminated description of a status code. */
 const char* scram_status_string(int status);

@@ -50,9 +50,9 @@ def lib() -> ctypes.CDLL:
     P, I, U32, U64, SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_size_t
     L.scram_patchmatch_workspace_bytes.argtypes = [I, I, I]
     L.scram_patchmatch_workspace_bytes.restype = SZ
-    L.scram_patchmatch.argtypes = [P, P, I, I, I, I, I, I, I, I, U64, P, P, I, U32, P, P, P, SZ, P]
+    L.scram_patchmatch.argtypes = [P, P, I, I, I, I, I, I, I, I, U64, P, P, I, U32, P, P, P, SZ, P, P]
     L.scram_patchmatch.restype = I
-    L.scram_sparse_attend.argtypes = [P, P, P, I, P, I, I, I, I, I, I, I, I, ctypes.c_float, P, P]
+    L.scram_sparse_attend.argtypes = [P, P, P, I, P, I, I, I, I, I, I, I, I, ctypes.c_float, P, P, P]
     L.scram_sparse_attend.restype = I
     L.scram_status_string.argtypes = [I]
     L.scram_status_string.restype = ctypes.c_char_p
@@ -106,13 +106,29 @@ def _stream(device):
     return ctypes.c_void_p(_torch().cuda.current_stream(device).cuda_stream)
 
 
+def _event_array(events, n):
+    """ctypes array of the raw handles of ``n`` torch.cuda.Event objects (already recorded once)."""
+    if len(events) != n:
+        raise ValueError(f"need {n} events, got {len(events)}")
+    handles = []
+    for ev in events:
+        h = int(getattr(ev, "cuda_event", 0) or 0)
+        if not h:
+            raise ValueError("events must be created (recorded once) before they are passed in")
+        handles.append(h)
+    return (ctypes.c_void_p * n)(*handles)
+
+
 def patchmatch(Q, K, iters: int, seed: int, *, init=None, init_score=None, t0: int = 1, flags: int = 0,
-               out=None, score_out=None, workspace=None, return_score: bool = False):
+               out=None, score_out=None, workspace=None, return_score: bool = False, events=None):
     """PatchMatch argmax map (``scram_patchmatch``).
 
     Q ``[S, Hq, Wq, d]``, K ``[S, Hk, Wk, d]`` (float32 or bfloat16, same dtype).
     Returns int32 ``[S, Hq, Wq]`` flat key indices (and fp32 scores if
     ``return_score``).  ``init``/``init_score``/``t0`` resume a run.
+    ``events``: optional ``2 * (iters + 1)`` timing-enabled torch.cuda.Event
+    objects, stamped with the start and end of each launch (init, then each
+    sweep).
     """
     torch = _torch()
     _dev_tensor(Q, "Q", 4)
@@ -137,19 +153,22 @@ def patchmatch(Q, K, iters: int, seed: int, *, init=None, init_score=None, t0: i
     need = patchmatch_workspace_bytes(S, Hq, Wq)
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    ev = None if events is None else _event_array(events, 2 * (int(iters) + 1))
     rc = lib().scram_patchmatch(_ptr(Q), _ptr(K), _dtype_code(Q), S, Hq, Wq, Hk, Wk, d, int(iters),
                                 ctypes.c_uint64(int(seed) & 0xFFFFFFFFFFFFFFFF), _ptr(init), _ptr(init_score),
                                 int(t0), int(flags), _ptr(out), _ptr(score_out), _ptr(workspace),
-                                workspace.numel() * workspace.element_size(), _stream(dev))
+                                workspace.numel() * workspace.element_size(), ev, _stream(dev))
     if rc != 0:
         raise ScramError(rc, "scram_patchmatch")
     return (out, score_out) if return_score else out
 
 
-def sparse_attend(Q, K, V, argmax, window: int, scale: float | None = None, *, out=None):
+def sparse_attend(Q, K, V, argmax, window: int, scale: float | None = None, *, out=None, events=None):
     """Window softmax + value gather around ``argmax`` (``scram_sparse_attend``).
 
     Returns ``[S, Hq, Wq, dv]`` in Q's dtype.  ``scale`` defaults to 1/sqrt(d).
+    ``events``: optional 2 timing-enabled torch.cuda.Event objects stamped with
+    the kernel's start and end.
     """
     torch = _torch()
     for name, t in (("Q", Q), ("K", K), ("V", V)):
@@ -169,8 +188,9 @@ def sparse_attend(Q, K, V, argmax, window: int, scale: float | None = None, *, o
     if out is None:
         out = torch.empty((S, Hq, Wq, dv), dtype=Q.dtype, device=Q.device)
     _dev_tensor(out, "out", 4)
+    ev = None if events is None else _event_array(events, 2)
     rc = lib().scram_sparse_attend(_ptr(Q), _ptr(K), _ptr(V), _dtype_code(Q), _ptr(argmax), S, Hq, Wq, Hk, Wk,
-                                   d, dv, int(window), float(scale), _ptr(out), _stream(Q.device))
+                                   d, dv, int(window), float(scale), _ptr(out), ev, _stream(Q.device))
     if rc != 0:
         raise ScramError(rc, "scram_sparse_attend")
     return out

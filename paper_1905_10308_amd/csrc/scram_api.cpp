@@ -68,7 +68,7 @@ size_t scram_patchmatch_workspace_bytes(int S, int Hq, int Wq)
 int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int Wq, int Hk, int Wk,
                      int d, int iters, uint64_t seed, const int32_t* init, const float* init_score,
                      int t0, uint32_t flags, int32_t* argmax_out, float* score_out, void* workspace,
-                     size_t workspace_bytes, hipStream_t stream)
+                     size_t workspace_bytes, hipEvent_t* events, hipStream_t stream)
 {
     // ---- validation (no HIP call above this line) ----
     if (!Q || !K || !argmax_out) return SCRAM_ERR_NULL;
@@ -114,13 +114,19 @@ int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int
     const int p0 = iters % 2;
     const int32_t* Jcur;
     const float* scur;
+    hipEvent_t* ev = events;  // 2 per launch: start, stop
     hipError_t e = hipSuccess;
     if (init) {
         Jcur = init;
         if (init_score) {
             scur = init_score;
+            if (ev) {  // nothing to launch: the first pair brackets no work
+                e = hipEventRecord(ev[0], stream);
+                if (e == hipSuccess) e = hipEventRecord(ev[1], stream);
+            }
         } else {
-            e = scram::launch_pm_init(dtype, Q, K, grid, seed, init, nullptr, sbuf[p0], stream);
+            e = scram::launch_pm_init(dtype, Q, K, grid, seed, init, nullptr, sbuf[p0], stream, ev ? ev[0] : nullptr,
+                                      ev ? ev[1] : nullptr);
             scur = sbuf[p0];
         }
         if (e == hipSuccess && iters == 0) {
@@ -129,14 +135,15 @@ int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int
                 e = hipMemcpyAsync(score_out, init_score, 4 * n, hipMemcpyDeviceToDevice, stream);
         }
     } else {
-        e = scram::launch_pm_init(dtype, Q, K, grid, seed, nullptr, Jbuf[p0], sbuf[p0], stream);
+        e = scram::launch_pm_init(dtype, Q, K, grid, seed, nullptr, Jbuf[p0], sbuf[p0], stream, ev ? ev[0] : nullptr,
+                                  ev ? ev[1] : nullptr);
         Jcur = Jbuf[p0];
         scur = sbuf[p0];
     }
     for (int k = 1; k <= iters && e == hipSuccess; ++k) {
         const int pk = (iters - k) % 2;
         e = scram::launch_pm_iter(dtype, Q, K, grid, seed, uint32_t(t0 + k - 1), flags, Jcur, scur, Jbuf[pk],
-                                  sbuf[pk], stream);
+                                  sbuf[pk], stream, ev ? ev[2 * k] : nullptr, ev ? ev[2 * k + 1] : nullptr);
         Jcur = Jbuf[pk];
         scur = sbuf[pk];
     }
@@ -145,7 +152,7 @@ int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int
 
 int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype,
                         const int32_t* argmax, int S, int Hq, int Wq, int Hk, int Wk, int d, int dv,
-                        int window, float scale, void* out, hipStream_t stream)
+                        int window, float scale, void* out, hipEvent_t* events, hipStream_t stream)
 {
     if (!Q || !K || !V || !argmax || !out) return SCRAM_ERR_NULL;
     int rc = check_grid(S, Hq, Wq, Hk, Wk);
@@ -163,7 +170,8 @@ int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype,
         if (overlap(rO, other)) return SCRAM_ERR_ALIAS;
     }
     const scram::Grid grid{S, Hq, Wq, Hk, Wk, d};
-    const hipError_t e = scram::launch_attend(dtype, Q, K, V, argmax, grid, window, scale, out, stream);
+    const hipError_t e = scram::launch_attend(dtype, Q, K, V, argmax, grid, window, scale, out, stream,
+                                              events ? events[0] : nullptr, events ? events[1] : nullptr);
     return e == hipSuccess ? SCRAM_OK : SCRAM_ERR_HIP;
 }
 

@@ -29,6 +29,7 @@
 
 #include <type_traits>
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "scram.h"
@@ -299,148 +300,215 @@ __global__ __launch_bounds__(kBlock) void pm_init_kernel(PmParams p)
 
 // ---------------------------------------------------------------------------
 // K2: one Jacobi sweep (propagation + random search), (Jp, sp) -> (Jn, sn)
+//
+// Each lane group carries QPG queries whose gathers are interleaved, so a
+// wave keeps several independent loads in flight.  A sweep has two stages:
+//   1. a batch of candidates that do not depend on each other: the 16
+//      propagation candidates and random-search step 0 -- at distance R the
+//      clipped search window is the whole key grid, so that draw does not
+//      depend on the running best.  Candidates outside the grids or equal to
+//      the incumbent (which cannot win) are dropped, the rest compacted per
+//      query in shared memory via wave ballots and gathered kNb at a time.
+//   2. random-search steps 1, 2, ...: each window is centred on the running
+//      best, so they form a dependent chain (interleaved across the QPG
+//      queries).
+// Because "better" is a strict total order, visiting the candidates of
+// stage 1 in any order gives the same result as the order of Algorithm 1.
 // ---------------------------------------------------------------------------
-template <typename T, int D, int G, bool PROP, bool RS>
+template <typename T, int D, int G, int QPG, int kNb, bool PROP, bool RS>
 __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
 {
     using RW = Row<T, D, G>;
     constexpr int CH = RW::kCh;
-    constexpr int kNb = 4;  // propagation candidates gathered per batch
-    __shared__ int32_t s_list[PROP ? RW::kQpb * 16 : 1];
+    constexpr int kGroups = RW::kQpb;           // lane groups per block
+    constexpr int kQpb = kGroups * QPG;         // queries per block
+    constexpr int kList = 17;                   // 16 propagation candidates + random-search step 0
+    constexpr int kSlots = (kList + G - 1) / G; // candidate slots per lane
+    static_assert(16 % G == 0, "step 0's Philox block and its candidate slot must share lane 0");
+    __shared__ int32_t s_list[kGroups * QPG * kList];
 
     const int lane = threadIdx.x & (G - 1);
     const int qslot = threadIdx.x / G;
     const int gbase = (threadIdx.x & 63) - lane;  // wave lane of the group's first lane
     const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
-    const uint32_t g_raw = blk * RW::kQpb + qslot;
-    const bool live = g_raw < p.n;
-    // groups past the end work on the last query and write nothing, so every
-    // lane reaches the block barrier below
-    const uint32_t g = live ? g_raw : p.n - 1;
 
-    uint32_t s, rem, x, y;
-    divmod(g, p.div_plane, s, rem);
-    divmod(rem, p.div_wq, x, y);
-    const T* Ks = static_cast<const T*>(p.K) + static_cast<size_t>(s) * p.nkeys * D;
-    uint4 q[CH];
-    load_row<T, D, G>(static_cast<const T*>(p.Q), g, lane, q);
-    int32_t cur = clamp_index(p.Jp[g], p.nkeys);
-    float best = p.sp[g];
+    uint32_t g[QPG], s[QPG], x[QPG], y[QPG];
+    bool live[QPG];
+    const T* Ks[QPG];
+    uint4 q[QPG][CH];
+    int32_t cur[QPG], cur0[QPG];
+    float best[QPG];
+#pragma unroll
+    for (int j = 0; j < QPG; ++j) {
+        const uint32_t gr = blk * kQpb + j * kGroups + qslot;
+        live[j] = gr < p.n;
+        // groups past the end work on the last query and write nothing, so
+        // every lane reaches the block barrier below
+        g[j] = live[j] ? gr : p.n - 1;
+        uint32_t rem;
+        divmod(g[j], p.div_plane, s[j], rem);
+        divmod(rem, p.div_wq, x[j], y[j]);
+        Ks[j] = static_cast<const T*>(p.K) + static_cast<size_t>(s[j]) * p.nkeys * D;
+        load_row<T, D, G>(static_cast<const T*>(p.Q), g[j], lane, q[j]);
+        cur[j] = clamp_index(p.Jp[g[j]], p.nkeys);
+        cur0[j] = cur[j];
+        best[j] = p.sp[g[j]];
+    }
 
-    if constexpr (PROP) {
-        // Lane l of the group forms candidates l, l + G, ... of the 16
-        // (jump index i/4 over 8,4,2,1; direction i%4 over row-1, row+1,
-        // col-1, col+1): the neighbour's match shifted back by the offset.
-        // Candidates outside the grids, or equal to the incumbent (which
-        // cannot win), are dropped; the rest are compacted into this
-        // query's list in shared memory.
-        constexpr int kSlots = (16 + G - 1) / G;
-        const int32_t* Jps = p.Jp + static_cast<size_t>(s) * p.plane_q;
-        const int32_t cur0 = cur;
-        int count = 0;
+    // Philox blocks of this sweep: block m serves random-search steps 2m and
+    // 2m+1; lane l draws block l (the first round; later rounds below).
+    const int nblk = RS ? (p.rs_steps + 1) >> 1 : 0;
+    uint4 w0[QPG];
+#pragma unroll
+    for (int j = 0; j < QPG; ++j) {
+        w0[j] = make_uint4(0u, 0u, 0u, 0u);
+        if (lane < nblk) w0[j] = philox4x32_10(g[j], p.t, static_cast<uint32_t>(lane), 0u, p.key0, p.key1);
+    }
+
+    // ---- stage 1 ----
+    int count[QPG];
+    const int32_t* Jp = p.Jp;
+#pragma unroll
+    for (int j = 0; j < QPG; ++j) {
+        count[j] = 0;
+        int32_t* list = s_list + (j * kGroups + qslot) * kList;
 #pragma unroll
         for (int m = 0; m < kSlots; ++m) {
             const int i = lane + m * G;
             int32_t c = -1;
-            if (i < 16) {
+            if (PROP && i < 16) {
+                // jump index i/4 over 8,4,2,1; direction i%4 over row-1, row+1,
+                // col-1, col+1: the neighbour's match shifted back by the offset
                 const int jump = 8 >> (i >> 2);
                 const int dir = i & 3;
                 const int ox = dir == 0 ? -jump : (dir == 1 ? jump : 0);
                 const int oy = dir == 2 ? -jump : (dir == 3 ? jump : 0);
-                const int nx = static_cast<int>(x) + ox, ny = static_cast<int>(y) + oy;
+                const int nx = static_cast<int>(x[j]) + ox, ny = static_cast<int>(y[j]) + oy;
                 if (nx >= 0 && nx < p.Hq && ny >= 0 && ny < p.Wq) {
-                    const uint32_t nb = clamp_index(Jps[nx * p.Wq + ny], p.nkeys);
+                    const uint32_t nb = clamp_index(Jp[(static_cast<size_t>(s[j]) * p.Hq + nx) * p.Wq + ny], p.nkeys);
                     uint32_t nu, nv;
                     divmod(nb, p.div_wk, nu, nv);
                     const int r = static_cast<int>(nu) - ox, cc = static_cast<int>(nv) - oy;
                     if (r >= 0 && r < p.Hk && cc >= 0 && cc < p.Wk) c = r * p.Wk + cc;
                 }
+            } else if (RS && i == 16) {
+                // random-search step 0: uniform over the whole key grid
+                const uint32_t r = __umulhi(w0[j].x, static_cast<uint32_t>(p.Hk));
+                const uint32_t cc = __umulhi(w0[j].y, static_cast<uint32_t>(p.Wk));
+                c = static_cast<int32_t>(r * p.Wk + cc);
             }
-            const bool keep = c >= 0 && c != cur0;
+            const bool keep = c >= 0 && c != cur0[j];
             const uint64_t bal = __ballot(keep);
             const uint32_t grp = static_cast<uint32_t>(bal >> gbase) & (G == 32 ? 0xFFFFFFFFu : ((1u << G) - 1u));
-            if (keep) s_list[qslot * 16 + count + __popc(grp & ((1u << lane) - 1u))] = c;
-            count += __popc(grp);
+            if (keep) list[count[j] + __popc(grp & ((1u << lane) - 1u))] = c;
+            count[j] += __popc(grp);
         }
-        __syncthreads();
+    }
+    __syncthreads();
 
-        // Gather the surviving candidates kNb at a time: all loads in
+    {
+        // gather kNb list entries of every query per batch: all loads in
         // flight, then the dot products (independent chains), then the
-        // comparisons in list order.  Slots past the end of a query's list
-        // keep stale data whose score is never used.
-        uint4 raw[kNb][CH];
+        // comparisons.  Slots past the end of a list keep stale data whose
+        // score is never used.
+        uint4 raw[QPG][kNb][CH];
 #pragma unroll
-        for (int j = 0; j < kNb; ++j)
+        for (int j = 0; j < QPG; ++j)
 #pragma unroll
-            for (int c = 0; c < CH; ++c) raw[j][c] = make_uint4(0u, 0u, 0u, 0u);
-        for (int k0 = 0; __any(k0 < count); k0 += kNb) {
-            int32_t idx[kNb];
+            for (int e = 0; e < kNb; ++e)
 #pragma unroll
-            for (int j = 0; j < kNb; ++j) {
-                const int kk = k0 + j;
-                idx[j] = kk < count ? s_list[qslot * 16 + (kk & 15)] : cur0;
-                if (kk < count) load_row<T, D, G>(Ks, idx[j], lane, raw[j]);
-            }
-            float sc[kNb];
+                for (int c = 0; c < CH; ++c) raw[j][e][c] = make_uint4(0u, 0u, 0u, 0u);
+        int most = count[0];
 #pragma unroll
-            for (int j = 0; j < kNb; ++j) sc[j] = row_score<T, D, G>(q, raw[j]);
+        for (int j = 1; j < QPG; ++j) most = max(most, count[j]);
+        for (int k0 = 0; __any(k0 < most); k0 += kNb) {
+            int32_t idx[QPG][kNb];
 #pragma unroll
-            for (int j = 0; j < kNb; ++j) {
-                if (k0 + j < count && better(sc[j], idx[j], best, cur)) {
-                    best = sc[j];
-                    cur = idx[j];
+            for (int j = 0; j < QPG; ++j) {
+                const int32_t* list = s_list + (j * kGroups + qslot) * kList;
+#pragma unroll
+                for (int e = 0; e < kNb; ++e) {
+                    const int kk = k0 + e;
+                    const int32_t entry = list[min(kk, kList - 1)];  // in bounds; stale past the end
+                    idx[j][e] = kk < count[j] ? entry : cur0[j];
+                    if (kk < count[j]) load_row<T, D, G>(Ks[j], idx[j][e], lane, raw[j][e]);
                 }
             }
+            float sc[QPG][kNb];
+#pragma unroll
+            for (int j = 0; j < QPG; ++j)
+#pragma unroll
+                for (int e = 0; e < kNb; ++e) sc[j][e] = row_score<T, D, G>(q[j], raw[j][e]);
+#pragma unroll
+            for (int j = 0; j < QPG; ++j)
+#pragma unroll
+                for (int e = 0; e < kNb; ++e) {
+                    const bool take = (k0 + e < count[j]) & better(sc[j][e], idx[j][e], best[j], cur[j]);
+                    best[j] = take ? sc[j][e] : best[j];
+                    cur[j] = take ? idx[j][e] : cur[j];
+                }
         }
     }
 
+    // ---- stage 2: random-search steps 1, 2, ... around the running best ----
+    // Step k uses words 2(k mod 2), 2(k mod 2)+1 of Philox block k/2, held by
+    // lane (k/2) mod G of the group; a new round of blocks is drawn every 2G
+    // steps.  A draw equal to the incumbent scores bit-identically and is not
+    // "better", so it needs no special case.
     if constexpr (RS) {
-        uint32_t cu, cv;
-        divmod(static_cast<uint32_t>(cur), p.div_wk, cu, cv);
-        // Philox block m serves steps 2m and 2m+1.  The blocks do not depend
-        // on the running best, so lane l of the group draws block b0 + l and
-        // the steps fetch their words from it.
-        const int nblk = (p.rs_steps + 1) >> 1;
-        for (int b0 = 0; b0 < nblk; b0 += G) {
-            uint4 w = make_uint4(0u, 0u, 0u, 0u);
-            if (b0 + lane < nblk) w = philox4x32_10(g, p.t, static_cast<uint32_t>(b0 + lane), 0u, p.key0, p.key1);
-            const int here = min(G, nblk - b0);
-            for (int j = 0; j < here; ++j) {
-                const uint32_t w0 = __shfl(w.x, gbase + j), w1 = __shfl(w.y, gbase + j);
-                const uint32_t w2 = __shfl(w.z, gbase + j), w3 = __shfl(w.w, gbase + j);
+        uint32_t cu[QPG], cv[QPG];
+        uint4 w[QPG];
 #pragma unroll
-                for (int half = 0; half < 2; ++half) {
-                    const int k = 2 * (b0 + j) + half;
-                    if (k < p.rs_steps) {
-                        const int dk = p.R >> k;
-                        const uint32_t wr = half ? w2 : w0, wc = half ? w3 : w1;
-                        const int lo_r = max(static_cast<int>(cu) - dk, 0);
-                        const int hi_r = min(static_cast<int>(cu) + dk, p.Hk - 1);
-                        const int lo_c = max(static_cast<int>(cv) - dk, 0);
-                        const int hi_c = min(static_cast<int>(cv) + dk, p.Wk - 1);
-                        const uint32_t r = lo_r + __umulhi(wr, static_cast<uint32_t>(hi_r - lo_r + 1));
-                        const uint32_t c = lo_c + __umulhi(wc, static_cast<uint32_t>(hi_c - lo_c + 1));
-                        const int32_t idx = static_cast<int32_t>(r * p.Wk + c);
-                        if (idx != cur) {
-                            uint4 kr[CH];
-                            load_row<T, D, G>(Ks, idx, lane, kr);
-                            const float sc = row_score<T, D, G>(q, kr);
-                            if (better(sc, idx, best, cur)) {
-                                best = sc;
-                                cur = idx;
-                                cu = r;
-                                cv = c;
-                            }
-                        }
-                    }
+        for (int j = 0; j < QPG; ++j) {
+            divmod(static_cast<uint32_t>(cur[j]), p.div_wk, cu[j], cv[j]);
+            w[j] = w0[j];
+        }
+        for (int k = 1; k < p.rs_steps; ++k) {
+            const int m = k >> 1;
+            if ((k & 1) == 0 && m % G == 0) {
+#pragma unroll
+                for (int j = 0; j < QPG; ++j) {
+                    w[j] = make_uint4(0u, 0u, 0u, 0u);
+                    if (m + lane < nblk)
+                        w[j] = philox4x32_10(g[j], p.t, static_cast<uint32_t>(m + lane), 0u, p.key0, p.key1);
                 }
+            }
+            const int src = gbase + m % G;
+            const int dk = p.R >> k;
+            int32_t idx[QPG];
+            uint32_t rr[QPG], rc[QPG];
+            uint4 kr[QPG][CH];
+#pragma unroll
+            for (int j = 0; j < QPG; ++j) {
+                const uint32_t wr = __shfl((k & 1) ? w[j].z : w[j].x, src);
+                const uint32_t wc = __shfl((k & 1) ? w[j].w : w[j].y, src);
+                const int lo_r = max(static_cast<int>(cu[j]) - dk, 0);
+                const int hi_r = min(static_cast<int>(cu[j]) + dk, p.Hk - 1);
+                const int lo_c = max(static_cast<int>(cv[j]) - dk, 0);
+                const int hi_c = min(static_cast<int>(cv[j]) + dk, p.Wk - 1);
+                rr[j] = lo_r + __umulhi(wr, static_cast<uint32_t>(hi_r - lo_r + 1));
+                rc[j] = lo_c + __umulhi(wc, static_cast<uint32_t>(hi_c - lo_c + 1));
+                idx[j] = static_cast<int32_t>(rr[j] * p.Wk + rc[j]);
+                load_row<T, D, G>(Ks[j], idx[j], lane, kr[j]);
+            }
+#pragma unroll
+            for (int j = 0; j < QPG; ++j) {
+                const float sc = row_score<T, D, G>(q[j], kr[j]);
+                const bool take = better(sc, idx[j], best[j], cur[j]);
+                best[j] = take ? sc : best[j];
+                cur[j] = take ? idx[j] : cur[j];
+                cu[j] = take ? rr[j] : cu[j];
+                cv[j] = take ? rc[j] : cv[j];
             }
         }
     }
 
-    if (live && lane == 0) {
-        p.Jn[g] = cur;
-        p.sn[g] = best;
+#pragma unroll
+    for (int j = 0; j < QPG; ++j) {
+        if (live[j] && lane == 0) {
+            p.Jn[g[j]] = cur[j];
+            p.sn[g[j]] = best[j];
+        }
     }
 }
 
@@ -640,6 +708,18 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
 // ---------------------------------------------------------------------------
 // host-side launch helpers
 // ---------------------------------------------------------------------------
+// Launch with the dispatch stamping optional start/stop events.
+template <typename P>
+hipError_t launch(void (*kernel)(P), uint32_t blocks, hipStream_t st, hipEvent_t start, hipEvent_t stop,
+                  const P& p)
+{
+    if (start || stop)
+        hipExtLaunchKernelGGL(kernel, dim3(blocks), dim3(kBlock), 0, st, start, stop, 0, p);
+    else
+        hipLaunchKernelGGL(kernel, dim3(blocks), dim3(kBlock), 0, st, p);
+    return hipGetLastError();
+}
+
 PmParams make_pm_params(const void* Q, const void* K, const Grid& gr, uint64_t seed)
 {
     PmParams p{};
@@ -665,45 +745,48 @@ PmParams make_pm_params(const void* Q, const void* K, const Grid& gr, uint64_t s
 }
 
 template <typename T, int D>
-hipError_t run_init(const PmParams& p, hipStream_t st)
+hipError_t run_init(const PmParams& p, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
 {
     constexpr int G = Lanes<T, D>::kPm;
     const uint32_t blocks = (p.n + Row<T, D, G>::kQpb - 1) / Row<T, D, G>::kQpb;
-    hipLaunchKernelGGL((pm_init_kernel<T, D, G>), dim3(blocks), dim3(kBlock), 0, st, p);
-    return hipGetLastError();
+    return launch(pm_init_kernel<T, D, G>, blocks, st, e0, e1, p);
 }
 
+#ifndef SCRAM_PM_QPG
+#define SCRAM_PM_QPG 1
+#endif
+#ifndef SCRAM_PM_BATCH
+#define SCRAM_PM_BATCH 4
+#endif
+
 template <typename T, int D>
-hipError_t run_iter(const PmParams& p, uint32_t flags, hipStream_t st)
+hipError_t run_iter(const PmParams& p, uint32_t flags, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
 {
     constexpr int G = Lanes<T, D>::kPm;
-    const uint32_t blocks = (p.n + Row<T, D, G>::kQpb - 1) / Row<T, D, G>::kQpb;
+    constexpr int QPG = SCRAM_PM_QPG;
+    constexpr int NB = SCRAM_PM_BATCH;
+    constexpr int kQpb = Row<T, D, G>::kQpb * QPG;
+    const uint32_t blocks = (p.n + kQpb - 1) / kQpb;
     const bool prop = !(flags & SCRAM_PM_NO_PROPAGATION);
     const bool rs = !(flags & SCRAM_PM_NO_RANDOM_SEARCH);
-    if (prop && rs)
-        hipLaunchKernelGGL((pm_iter_kernel<T, D, G, true, true>), dim3(blocks), dim3(kBlock), 0, st, p);
-    else if (prop)
-        hipLaunchKernelGGL((pm_iter_kernel<T, D, G, true, false>), dim3(blocks), dim3(kBlock), 0, st, p);
-    else if (rs)
-        hipLaunchKernelGGL((pm_iter_kernel<T, D, G, false, true>), dim3(blocks), dim3(kBlock), 0, st, p);
-    else
-        hipLaunchKernelGGL((pm_iter_kernel<T, D, G, false, false>), dim3(blocks), dim3(kBlock), 0, st, p);
-    return hipGetLastError();
+    if (prop && rs) return launch(pm_iter_kernel<T, D, G, QPG, NB, true, true>, blocks, st, e0, e1, p);
+    if (prop) return launch(pm_iter_kernel<T, D, G, QPG, NB, true, false>, blocks, st, e0, e1, p);
+    if (rs) return launch(pm_iter_kernel<T, D, G, QPG, NB, false, true>, blocks, st, e0, e1, p);
+    return launch(pm_iter_kernel<T, D, G, QPG, NB, false, false>, blocks, st, e0, e1, p);
 }
 
 template <typename T, int D>
-hipError_t run_attend(const AttParams& p, int window, hipStream_t st)
+hipError_t run_attend(const AttParams& p, int window, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
 {
     constexpr int G = Lanes<T, D>::kAttend;
     const uint32_t blocks = (p.n + Row<T, D, G>::kQpb - 1) / Row<T, D, G>::kQpb;
     switch (window) {
-        case 1: hipLaunchKernelGGL((attend_window_kernel<T, D, G, 1>), dim3(blocks), dim3(kBlock), 0, st, p); break;
-        case 3: hipLaunchKernelGGL((attend_window_kernel<T, D, G, 3>), dim3(blocks), dim3(kBlock), 0, st, p); break;
-        case 5: hipLaunchKernelGGL((attend_window_kernel<T, D, G, 5>), dim3(blocks), dim3(kBlock), 0, st, p); break;
-        case 7: hipLaunchKernelGGL((attend_window_kernel<T, D, G, 7>), dim3(blocks), dim3(kBlock), 0, st, p); break;
-        default: hipLaunchKernelGGL((attend_kernel<T, D, G>), dim3(blocks), dim3(kBlock), 0, st, p); break;
+        case 1: return launch(attend_window_kernel<T, D, G, 1>, blocks, st, e0, e1, p);
+        case 3: return launch(attend_window_kernel<T, D, G, 3>, blocks, st, e0, e1, p);
+        case 5: return launch(attend_window_kernel<T, D, G, 5>, blocks, st, e0, e1, p);
+        case 7: return launch(attend_window_kernel<T, D, G, 7>, blocks, st, e0, e1, p);
+        default: return launch(attend_kernel<T, D, G>, blocks, st, e0, e1, p);
     }
-    return hipGetLastError();
 }
 
 // (dtype, d) -> instantiation
@@ -731,20 +814,21 @@ hipError_t dispatch(int dtype, int d, F&& f)
 }  // namespace
 
 hipError_t launch_pm_init(int dtype, const void* Q, const void* K, const Grid& g, uint64_t seed,
-                          const int32_t* init, int32_t* J, float* s, hipStream_t stream)
+                          const int32_t* init, int32_t* J, float* s, hipStream_t stream, hipEvent_t start,
+                          hipEvent_t stop)
 {
     PmParams p = make_pm_params(Q, K, g, seed);
     p.init = init;
     p.Jn = J;
     p.sn = s;
     return dispatch(dtype, g.d, [&](auto t, auto d) {
-        return run_init<decltype(t), decltype(d)::value>(p, stream);
+        return run_init<decltype(t), decltype(d)::value>(p, stream, start, stop);
     });
 }
 
 hipError_t launch_pm_iter(int dtype, const void* Q, const void* K, const Grid& g, uint64_t seed,
                           uint32_t t, uint32_t flags, const int32_t* Jp, const float* sp, int32_t* Jn,
-                          float* sn, hipStream_t stream)
+                          float* sn, hipStream_t stream, hipEvent_t start, hipEvent_t stop)
 {
     PmParams p = make_pm_params(Q, K, g, seed);
     p.t = t;
@@ -753,12 +837,13 @@ hipError_t launch_pm_iter(int dtype, const void* Q, const void* K, const Grid& g
     p.Jn = Jn;
     p.sn = sn;
     return dispatch(dtype, g.d, [&](auto ty, auto d) {
-        return run_iter<decltype(ty), decltype(d)::value>(p, flags, stream);
+        return run_iter<decltype(ty), decltype(d)::value>(p, flags, stream, start, stop);
     });
 }
 
 hipError_t launch_attend(int dtype, const void* Q, const void* K, const void* V, const int32_t* J,
-                         const Grid& g, int window, float scale, void* out, hipStream_t stream)
+                         const Grid& g, int window, float scale, void* out, hipStream_t stream,
+                         hipEvent_t start, hipEvent_t stop)
 {
     AttParams p{};
     p.Q = Q;
@@ -775,7 +860,7 @@ hipError_t launch_attend(int dtype, const void* Q, const void* K, const void* V,
     p.b = window / 2;
     p.scale_log2e = scale * 1.4426950408889634f;
     return dispatch(dtype, g.d, [&](auto ty, auto d) {
-        return run_attend<decltype(ty), decltype(d)::value>(p, window, stream);
+        return run_attend<decltype(ty), decltype(d)::value>(p, window, stream, start, stop);
     });
 }
 

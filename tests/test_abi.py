@@ -78,7 +78,7 @@ def pm(L, **kw):
     a.update(kw)
     return L.scram_patchmatch(a["Q"], a["K"], a["dtype"], a["S"], a["Hq"], a["Wq"], a["Hk"], a["Wk"], a["d"],
                               a["iters"], a["seed"], a["init"], a["init_score"], a["t0"], a["flags"], a["out"],
-                              a["score"], a["ws"], a["ws_bytes"], None)
+                              a["score"], a["ws"], a["ws_bytes"], None, None)
 
 
 def at(L, **kw):
@@ -86,7 +86,7 @@ def at(L, **kw):
              scale=0.25, out=A_O)
     a.update(kw)
     return L.scram_sparse_attend(a["Q"], a["K"], a["V"], a["dtype"], a["J"], a["S"], a["Hq"], a["Wq"], a["Hk"],
-                                 a["Wk"], a["d"], a["dv"], a["window"], a["scale"], a["out"], None)
+                                 a["Wk"], a["d"], a["dv"], a["window"], a["scale"], a["out"], None, None)
 
 
 @pytest.mark.parametrize("kw,code", [

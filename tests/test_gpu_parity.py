@@ -164,6 +164,23 @@ def test_resume_bit_exact(scram, work):
     assert torch.equal(sfull, srest)
 
 
+def test_timing_events_leave_results_unchanged(scram, work):
+    cfg, a, dev = work
+    ref = scram.patchmatch(dev["Q"], dev["K"], cfg.iters, cfg.pm_seed)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(2 * (cfg.iters + 1) + 2)]
+    for e in evs:
+        e.record()
+    got = scram.patchmatch(dev["Q"], dev["K"], cfg.iters, cfg.pm_seed, events=evs[:-2])
+    out_ref = scram.sparse_attend(dev["Q"], dev["K"], dev["V"], ref, cfg.window, cfg.scale)
+    out = scram.sparse_attend(dev["Q"], dev["K"], dev["V"], got, cfg.window, cfg.scale, events=evs[-2:])
+    torch.cuda.synchronize()
+    assert torch.equal(ref, got) and torch.equal(out_ref, out)
+    times = [evs[2 * k].elapsed_time(evs[2 * k + 1]) for k in range(cfg.iters + 2)]
+    assert all(t > 0 for t in times)
+    with pytest.raises(ValueError):
+        scram.patchmatch(dev["Q"], dev["K"], cfg.iters, cfg.pm_seed, events=evs[:-3])
+
+
 def test_repeatable(scram, work):
     cfg, a, dev = work
     r1 = scram.patchmatch(dev["Q"], dev["K"], cfg.iters, cfg.pm_seed)
