@@ -55,7 +55,8 @@ def kernel_source_hash() -> str:
 
 
 def load_traffic(cfg):
-    """Measured HBM bytes per sweep launch, if taken on the current kernel source."""
+    """Measured bytes past L2 per sweep launch (copy-calibrated FETCH_SIZE + WRITE_SIZE), if
+    they were taken on the current kernel source and this workload; else None."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
@@ -194,7 +195,8 @@ def main(argv=None) -> int:
     pm_launch_bytes = nq * pm_bytes_per_query_sweep(cfg)
     att_bytes = nq * attend_bytes_per_query(cfg)
     achieved = pm_launch_bytes / (iter_ms * 1e-3) / 1e9
-    traffic = load_traffic(cfg)
+    traffic_bytes = load_traffic(cfg)
+    traffic = None if traffic_bytes is None else traffic_bytes / (iter_ms * 1e-3) / 1e9
 
     res = {
         "metric": METRIC,
@@ -229,6 +231,8 @@ def main(argv=None) -> int:
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
             "traffic": traffic,
+            "traffic_bytes_per_launch": traffic_bytes,
+            "algorithmic_bytes_per_launch": pm_launch_bytes,
         },
         "kernels_ms": {"pm_init": init_ms, "pm_iter": iter_ms, "attend": att_ms},
         "kernels_ms_source": "dispatch-stamped HIP events, timed region B",
