@@ -31,6 +31,7 @@ _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 
 NO_PROPAGATION = 1
 NO_RANDOM_SEARCH = 2
+CAUSAL = 4
 #: relative width of a "near tie" between two dot products, measured against
 #: sum_e |q_e k_e| (the forward-error scale of a dot product).
 TIE_REL = 1e-5
@@ -61,17 +62,19 @@ def _load():
     i64 = ctypes.c_int64
     lib.oracle_philox4x32_10.argtypes = [P, P, P]
     lib.oracle_philox4x32_10.restype = None
-    lib.oracle_pm_init.argtypes = [P, P, i64, i64, i64, i64, i64, ctypes.c_int, ctypes.c_uint64, P, P]
+    lib.oracle_pm_init.argtypes = [P, P, i64, i64, i64, i64, i64, ctypes.c_int, ctypes.c_uint64, ctypes.c_uint32,
+                                   i64, P, P]
     lib.oracle_pm_scores.argtypes = [P, P, i64, i64, i64, i64, i64, ctypes.c_int, P, P, P]
     lib.oracle_pm_iteration.argtypes = [P, P, i64, i64, i64, i64, i64, ctypes.c_int, ctypes.c_uint64,
-                                        i64, ctypes.c_uint32, ctypes.c_double, P, P, P, i64, P, P, P, P]
+                                        i64, ctypes.c_uint32, ctypes.c_double, P, i64, i64, P, P, P, i64, P, P,
+                                        P, P]
     lib.oracle_pm_trace.argtypes = [P, P, i64, i64, i64, i64, i64, ctypes.c_int, ctypes.c_uint64,
-                                    i64, ctypes.c_uint32, P, P, i64, i64, P, P, P, P]
+                                    i64, ctypes.c_uint32, P, i64, i64, P, P, i64, i64, P, P, P, P]
     lib.oracle_pm_trace.restype = i64
     lib.oracle_patchmatch.argtypes = [P, P, i64, i64, i64, i64, i64, ctypes.c_int, i64, ctypes.c_uint64,
-                                      P, i64, ctypes.c_uint32, ctypes.c_double, P, P, P, P]
-    lib.oracle_sparse_attend.argtypes = [P, P, P, P, i64, i64, i64, i64, i64, ctypes.c_int,
-                                         ctypes.c_int, ctypes.c_int, ctypes.c_double, P, i64, P]
+                                      P, i64, ctypes.c_uint32, ctypes.c_double, P, i64, i64, P, P, P, P]
+    lib.oracle_sparse_attend.argtypes = [P, P, P, P, i64, i64, i64, i64, i64, i64, ctypes.c_int,
+                                         ctypes.c_int, ctypes.c_int, ctypes.c_double, ctypes.c_uint32, P, i64, P]
     lib.oracle_num_threads.restype = ctypes.c_int
     lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
     _lib = lib
@@ -120,13 +123,21 @@ def philox4x32_10(ctr, key):
     return out
 
 
-def pm_init(Q, K, seed):
-    """Random initialisation (Algorithm 1, first loop) -> (J0 int32, s0 float64)."""
+def _prev(prev, S, Hq, Wq):
+    """Previous runs' maps as contiguous int32 [C, S, Hq, Wq] (None -> C = 0)."""
+    if prev is None:
+        return None, 0
+    prev = _i32(prev).reshape(-1, S, Hq, Wq)
+    return prev, prev.shape[0]
+
+
+def pm_init(Q, K, seed, flags=0, n_prev=0):
+    """Random initialisation (Algorithm 1, first loop) of run ``n_prev`` -> (J0 int32, s0 float64)."""
     Q, K = _f64(Q), _f64(K)
     S, Hq, Wq, Hk, Wk, d = _dims(Q, K)
     J = np.empty((S, Hq, Wq), np.int32)
     s = np.empty((S, Hq, Wq), np.float64)
-    _check(_load().oracle_pm_init(_ptr(Q), _ptr(K), S, Hq, Wq, Hk, Wk, d, seed, _ptr(J), _ptr(s)),
+    _check(_load().oracle_pm_init(_ptr(Q), _ptr(K), S, Hq, Wq, Hk, Wk, d, seed, flags, n_prev, _ptr(J), _ptr(s)),
            "pm_init")
     return J, s
 
@@ -142,14 +153,15 @@ def pm_scores(Q, K, J):
     return s, a
 
 
-def pm_iteration(Q, K, J_prev, t, seed, flags=0, query_ids=None, s_prev=None, tie_rel=TIE_REL):
-    """One Jacobi iteration t >= 1 of Algorithm 1.
+def pm_iteration(Q, K, J_prev, t, seed, flags=0, query_ids=None, s_prev=None, tie_rel=TIE_REL, prev=None, sep=1):
+    """One Jacobi iteration t >= 1 of Algorithm 1 (run C = len(prev), separation ``sep``).
 
     Returns ``(J, s, tie, ncand)``; with ``query_ids`` the arrays are compact
     (entry i is query ``query_ids[i]`` in flat order), otherwise ``[S, Hq, Wq]``.
     """
     Q, K, J_prev = _f64(Q), _f64(K), _i32(J_prev)
     S, Hq, Wq, Hk, Wk, d = _dims(Q, K)
+    prev, n_prev = _prev(prev, S, Hq, Wq)
     if s_prev is None:
         s_prev, _ = pm_scores(Q, K, J_prev)
     s_prev = _f64(s_prev)
@@ -163,12 +175,12 @@ def pm_iteration(Q, K, J_prev, t, seed, flags=0, query_ids=None, s_prev=None, ti
     tie = np.zeros(shape, np.uint8)
     nc = ctypes.c_int64(0)
     _check(_load().oracle_pm_iteration(_ptr(Q), _ptr(K), S, Hq, Wq, Hk, Wk, d, seed, t, flags, tie_rel,
-                                       _ptr(J_prev), _ptr(s_prev), _ptr(ids), nq, _ptr(J), _ptr(s),
-                                       _ptr(tie), ctypes.byref(nc)), "pm_iteration")
+                                       _ptr(prev), n_prev, sep, _ptr(J_prev), _ptr(s_prev), _ptr(ids), nq,
+                                       _ptr(J), _ptr(s), _ptr(tie), ctypes.byref(nc)), "pm_iteration")
     return J, s, tie.astype(bool), int(nc.value)
 
 
-def pm_trace(Q, K, J_prev, t, seed, g, flags=0, cap=256):
+def pm_trace(Q, K, J_prev, t, seed, g, flags=0, cap=256, prev=None, sep=1):
     """Every candidate scored by query ``g`` in iteration ``t``.
 
     Returns ``(idx[n], kind[n], window[n, 4], final)``; kind is
@@ -178,37 +190,60 @@ def pm_trace(Q, K, J_prev, t, seed, g, flags=0, cap=256):
     """
     Q, K, J_prev = _f64(Q), _f64(K), _i32(J_prev)
     S, Hq, Wq, Hk, Wk, d = _dims(Q, K)
+    prev, n_prev = _prev(prev, S, Hq, Wq)
     s_prev, _ = pm_scores(Q, K, J_prev)
     idx = np.zeros(cap, np.int64)
     kind = np.zeros(cap, np.int32)
     win = np.zeros((cap, 4), np.float64)
     fin = ctypes.c_int32(0)
-    n = _load().oracle_pm_trace(_ptr(Q), _ptr(K), S, Hq, Wq, Hk, Wk, d, seed, t, flags, _ptr(J_prev),
-                                _ptr(s_prev), g, cap, _ptr(idx), _ptr(kind), _ptr(win), ctypes.byref(fin))
+    n = _load().oracle_pm_trace(_ptr(Q), _ptr(K), S, Hq, Wq, Hk, Wk, d, seed, t, flags, _ptr(prev), n_prev, sep,
+                                _ptr(J_prev), _ptr(s_prev), g, cap, _ptr(idx), _ptr(kind), _ptr(win),
+                                ctypes.byref(fin))
     if n < 0:
         raise ValueError("pm_trace: bad arguments")
     return idx[:n], kind[:n], win[:n].astype(np.int64), int(fin.value)
 
 
-def patchmatch(Q, K, iters, seed, init=None, t0=1, flags=0, tie_rel=TIE_REL):
-    """Whole Algorithm 1 run -> ``(J int32, s float64, ties bool[iters,S,Hq,Wq], ncand)``."""
+def patchmatch(Q, K, iters, seed, init=None, t0=1, flags=0, tie_rel=TIE_REL, prev=None, sep=1):
+    """Whole Algorithm 1 run number C = len(prev) -> ``(J int32, s float64, ties bool[iters,S,Hq,Wq], ncand)``."""
     Q, K = _f64(Q), _f64(K)
     S, Hq, Wq, Hk, Wk, d = _dims(Q, K)
+    prev, n_prev = _prev(prev, S, Hq, Wq)
     init = None if init is None else _i32(init)
     J = np.empty((S, Hq, Wq), np.int32)
     s = np.empty((S, Hq, Wq), np.float64)
     ties = np.zeros((max(iters, 0), S, Hq, Wq), np.uint8)
     nc = ctypes.c_int64(0)
     _check(_load().oracle_patchmatch(_ptr(Q), _ptr(K), S, Hq, Wq, Hk, Wk, d, iters, seed, _ptr(init), t0,
-                                     flags, tie_rel, _ptr(J), _ptr(s), _ptr(ties), ctypes.byref(nc)),
-           "patchmatch")
+                                     flags, tie_rel, _ptr(prev), n_prev, sep, _ptr(J), _ptr(s), _ptr(ties),
+                                     ctypes.byref(nc)), "patchmatch")
     return J, s, ties.astype(bool), int(nc.value)
 
 
-def sparse_attend(Q, K, V, J, window, scale, query_ids=None):
-    """Algorithm 2 at kappa = 1 -> float64 ``[S, Hq, Wq, dv]`` (or ``[nq, dv]``)."""
+def patchmatch_kappa(Q, K, kappa, iters, seed, sep=1, flags=0, tie_rel=TIE_REL):
+    """kappa runs of Algorithm 1, run c constrained by runs 0..c-1 (Algorithm 2, first step).
+
+    Returns ``(J int32 [kappa,S,Hq,Wq], s float64 [kappa,...], ties bool [kappa,iters,...])``.
+    """
+    Js, ss, ts = [], [], []
+    for c in range(kappa):
+        prev = np.stack(Js) if Js else None
+        J, s, ties, _ = patchmatch(Q, K, iters, seed, flags=flags, tie_rel=tie_rel, prev=prev, sep=sep)
+        Js.append(J)
+        ss.append(s)
+        ts.append(ties)
+    return np.stack(Js), np.stack(ss), np.stack(ts)
+
+
+def sparse_attend(Q, K, V, J, window, scale, query_ids=None, flags=0):
+    """Algorithm 2 -> float64 ``[S, Hq, Wq, dv]`` (or ``[nq, dv]``).
+
+    ``J`` is one map ``[S, Hq, Wq]`` or kappa maps ``[kappa, S, Hq, Wq]`` (union of windows).
+    """
     Q, K, V, J = _f64(Q), _f64(K), _f64(V), _i32(J)
     S, Hq, Wq, Hk, Wk, d = _dims(Q, K)
+    J = J.reshape(-1, S, Hq, Wq)
+    kappa = J.shape[0]
     if V.shape[:3] != K.shape[:3]:
         raise ValueError("V must share K's grid")
     dv = V.shape[3]
@@ -218,6 +253,6 @@ def sparse_attend(Q, K, V, J, window, scale, query_ids=None):
         ids = np.ascontiguousarray(query_ids, dtype=np.int64)
         nq, shape = ids.size, (ids.size, dv)
     out = np.empty(shape, np.float64)
-    _check(_load().oracle_sparse_attend(_ptr(Q), _ptr(K), _ptr(V), _ptr(J), S, Hq, Wq, Hk, Wk, d, dv,
-                                        window, scale, _ptr(ids), nq, _ptr(out)), "sparse_attend")
+    _check(_load().oracle_sparse_attend(_ptr(Q), _ptr(K), _ptr(V), _ptr(J), kappa, S, Hq, Wq, Hk, Wk, d, dv,
+                                        window, scale, flags, _ptr(ids), nq, _ptr(out)), "sparse_attend")
     return out

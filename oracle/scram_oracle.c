@@ -41,6 +41,21 @@
  *     depend on a positive scale); the attend step uses the caller's scale;
  *   - attend window keys outside the key grid are dropped and the softmax is
  *     normalised over the keys that remain (Alg. 2, Eq. 8).
+ *
+ * Several matches per query (kappa > 1, Section 4.2 and Algorithm 2's first
+ * step): run c of PatchMatch receives the C = c maps of the previous runs and
+ * is_index_valid rejects a key closer than L to any of them in Chebyshev
+ * distance (max(|du|, |dv|) < L); L = 1 keeps only distinct keys (the
+ * top-kappa-max variant), L > 1 keeps the matches apart (top-kappa-mode).  An
+ * incumbent that is not valid counts as minus infinity, so the first valid
+ * candidate replaces it.  Run c draws its random numbers with counter word 3
+ * equal to c.  Algorithm 2 then attends over the union of the kappa windows,
+ * every key once.
+ *
+ * Causal masking (Section 4.2.1), for a query grid equal to the key grid: a
+ * key is valid for query i only if its raster index is at most i.  The
+ * initial match is drawn uniformly from the valid keys, and the attend
+ * window drops keys after the query.
  */
 #include <math.h>
 #include <stdint.h>
@@ -49,6 +64,7 @@
 
 #define OR_NO_PROPAGATION 1u
 #define OR_NO_RANDOM_SEARCH 2u
+#define OR_CAUSAL 4u
 
 /* ------------------------------------------------------------------------ */
 /* Philox4x32-10, from its published description: ten rounds; each round   */
@@ -132,7 +148,25 @@ typedef struct {
     uint32_t key[2];
     uint32_t flags;
     double tie_rel;
+    const int32_t* prev; /* [n_prev, S, Hq, Wq] maps of previous runs, or NULL */
+    int64_t n_prev;
+    int64_t sep;         /* minimum Chebyshev distance to every previous match */
 } pm_problem;
+
+/* is_index_valid: key idx for query g (Algorithm 1, propagation and random search). */
+static int index_valid(const pm_problem* P, int64_t g, int64_t idx)
+{
+    const int64_t plane = P->Hq * P->Wq;
+    if ((P->flags & OR_CAUSAL) && idx > g % plane) return 0;
+    const int64_t u = idx / P->Wk, v = idx % P->Wk;
+    for (int64_t c = 0; c < P->n_prev; ++c) {
+        const int64_t pj = P->prev[c * P->S * plane + g];
+        const int64_t du = llabs(u - pj / P->Wk), dv = llabs(v - pj % P->Wk);
+        const int64_t cheb = du > dv ? du : dv;
+        if (cheb < P->sep) return 0;
+    }
+    return 1;
+}
 
 /* running state of one query inside one iteration */
 typedef struct {
@@ -150,14 +184,15 @@ typedef struct {
     int64_t trace_cap, trace_len;
 } pm_state;
 
-static void consider(const pm_problem* P, pm_state* st, int64_t r, int64_t c, int kind,
+static void consider(const pm_problem* P, pm_state* st, int64_t g, int64_t r, int64_t c, int kind,
                      const int64_t window[4])
 {
     int64_t idx = r * P->Wk + c;
+    if (!index_valid(P, g, idx)) return;
     const double* k = st->Ks + idx * P->d;
     double sc = dot(st->q, k, P->d);
     st->ncand += 1;
-    if (idx != st->cur) {
+    if (idx != st->cur && st->best != -INFINITY) {
         double a = absdot(st->q, k, P->d);
         double scale = a > st->best_abs ? a : st->best_abs;
         if (fabs(sc - st->best) <= P->tie_rel * scale) st->tie = 1;
@@ -190,7 +225,7 @@ static void pm_query_iteration(const pm_problem* P, int64_t g, int64_t t,
     st->q = P->Q + g * P->d;
     st->Ks = P->K + s * P->Hk * P->Wk * P->d;
     st->cur = J_prev[g];
-    st->best = s_prev[g];
+    st->best = index_valid(P, g, st->cur) ? s_prev[g] : -INFINITY;
     st->best_abs = absdot(st->q, st->Ks + st->cur * P->d, P->d);
 
     if (!(P->flags & OR_NO_PROPAGATION)) {
@@ -206,7 +241,7 @@ static void pm_query_iteration(const pm_problem* P, int64_t g, int64_t t,
                 int64_t r = nb / P->Wk - ox;
                 int64_t c = nb % P->Wk - oy;
                 if (r < 0 || r >= P->Hk || c < 0 || c >= P->Wk) continue;
-                consider(P, st, r, c, 1 + 4 * jj + dd, NULL);
+                consider(P, st, g, r, c, 1 + 4 * jj + dd, NULL);
             }
         }
     }
@@ -214,7 +249,7 @@ static void pm_query_iteration(const pm_problem* P, int64_t g, int64_t t,
     if (!(P->flags & OR_NO_RANDOM_SEARCH)) {
         int64_t D = P->Hk > P->Wk ? P->Hk : P->Wk;
         for (int64_t k = 0;; ++k) {
-            uint32_t ctr[4] = {(uint32_t)g, (uint32_t)t, (uint32_t)(k / 2), 0u};
+            uint32_t ctr[4] = {(uint32_t)g, (uint32_t)t, (uint32_t)(k / 2), (uint32_t)P->n_prev};
             uint32_t w[4];
             philox4x32_10(ctr, P->key, w);
             uint32_t w_row = w[2 * (k % 2)], w_col = w[2 * (k % 2) + 1];
@@ -226,7 +261,7 @@ static void pm_query_iteration(const pm_problem* P, int64_t g, int64_t t,
             int64_t window[4] = {lo_r, hi_r, lo_c, hi_c};
             int64_t r = pick_in_range(w_row, lo_r, hi_r);
             int64_t c = pick_in_range(w_col, lo_c, hi_c);
-            consider(P, st, r, c, 100 + (int)k, window);
+            consider(P, st, g, r, c, 100 + (int)k, window);
             if (D == 1) break;
             D /= 2;
         }
@@ -241,27 +276,37 @@ static int check_dims(int64_t S, int64_t Hq, int64_t Wq, int64_t Hk, int64_t Wk,
 }
 
 /*
- * Random initialisation of the nearest-neighbour field (Alg. 1, first loop):
- * J0[g] = u*Wk + v with u uniform in [0, Hk), v uniform in [0, Wk), and the
- * fp64 score s0[g] = q_g . k_J0[g].
+ * Random initialisation of the nearest-neighbour field (Alg. 1, first loop)
+ * for run n_prev: counter (g, 0, 0, n_prev).  J0[g] = u*Wk + v with u uniform
+ * in [0, Hk), v uniform in [0, Wk) (words 0, 1) -- or, with OR_CAUSAL, the
+ * flat index uniform over the keys up to the query's own raster index
+ * (word 0) -- and the fp64 score s0[g] = q_g . k_J0[g].
  */
 int oracle_pm_init(const double* Q, const double* K, int64_t S, int64_t Hq, int64_t Wq,
-                   int64_t Hk, int64_t Wk, int d, uint64_t seed, int32_t* J0, double* s0)
+                   int64_t Hk, int64_t Wk, int d, uint64_t seed, uint32_t flags, int64_t n_prev,
+                   int32_t* J0, double* s0)
 {
-    if (check_dims(S, Hq, Wq, Hk, Wk, d)) return -2;
+    if (check_dims(S, Hq, Wq, Hk, Wk, d) || n_prev < 0) return -2;
+    if ((flags & OR_CAUSAL) && (Hq != Hk || Wq != Wk)) return -2;
     uint32_t key[2];
     seed_key(seed, key);
     const int64_t n = S * Hq * Wq, plane = Hq * Wq;
 #pragma omp parallel for schedule(static)
     for (int64_t g = 0; g < n; ++g) {
-        uint32_t ctr[4] = {(uint32_t)g, 0u, 0u, 0u};
+        uint32_t ctr[4] = {(uint32_t)g, 0u, 0u, (uint32_t)n_prev};
         uint32_t w[4];
         philox4x32_10(ctr, key, w);
-        int64_t u = pick_in_range(w[0], 0, Hk - 1);
-        int64_t v = pick_in_range(w[1], 0, Wk - 1);
-        J0[g] = (int32_t)(u * Wk + v);
+        int64_t idx;
+        if (flags & OR_CAUSAL) {
+            idx = pick_in_range(w[0], 0, g % plane);
+        } else {
+            int64_t u = pick_in_range(w[0], 0, Hk - 1);
+            int64_t v = pick_in_range(w[1], 0, Wk - 1);
+            idx = u * Wk + v;
+        }
+        J0[g] = (int32_t)idx;
         const double* Ks = K + (g / plane) * Hk * Wk * d;
-        s0[g] = dot(Q + g * d, Ks + (u * Wk + v) * d, d);
+        s0[g] = dot(Q + g * d, Ks + idx * d, d);
     }
     return 0;
 }
@@ -285,7 +330,8 @@ int oracle_pm_scores(const double* Q, const double* K, int64_t S, int64_t Hq, in
 }
 
 /*
- * One Jacobi iteration t (t >= 1) over the queries listed in query_ids (all
+ * One Jacobi iteration t (t >= 1) of run n_prev (with the maps of the n_prev
+ * previous runs in prev) over the queries listed in query_ids (all
  * queries when query_ids is NULL).  Outputs are compact: entry i belongs to
  * query_ids[i] (or to query i).  tie_out[i] = 1 when some comparison made for
  * that query put two different keys within tie_rel * max(sum|q k|) of each
@@ -293,12 +339,15 @@ int oracle_pm_scores(const double* Q, const double* K, int64_t S, int64_t Hq, in
  */
 int oracle_pm_iteration(const double* Q, const double* K, int64_t S, int64_t Hq, int64_t Wq,
                         int64_t Hk, int64_t Wk, int d, uint64_t seed, int64_t t, uint32_t flags,
-                        double tie_rel, const int32_t* J_prev, const double* s_prev,
+                        double tie_rel, const int32_t* prev, int64_t n_prev, int64_t sep,
+                        const int32_t* J_prev, const double* s_prev,
                         const int64_t* query_ids, int64_t nq, int32_t* J_out, double* s_out,
                         uint8_t* tie_out, int64_t* ncand_out)
 {
-    if (check_dims(S, Hq, Wq, Hk, Wk, d) || t < 1) return -2;
-    pm_problem P = {Q, K, S, Hq, Wq, Hk, Wk, d, {0, 0}, flags, tie_rel};
+    if (check_dims(S, Hq, Wq, Hk, Wk, d) || t < 1 || n_prev < 0 || sep < 1) return -2;
+    if ((flags & OR_CAUSAL) && (Hq != Hk || Wq != Wk)) return -2;
+    if (n_prev > 0 && !prev) return -1;
+    pm_problem P = {Q, K, S, Hq, Wq, Hk, Wk, d, {0, 0}, flags, tie_rel, prev, n_prev, sep};
     seed_key(seed, P.key);
     const int64_t n = S * Hq * Wq;
     const int64_t count = query_ids ? nq : n;
@@ -324,19 +373,22 @@ int oracle_pm_iteration(const double* Q, const double* K, int64_t S, int64_t Hq,
 }
 
 /*
- * Trace of one query's iteration t: every scored candidate in order, its kind
+ * Trace of one query's iteration t: every scored (valid) candidate in order, its kind
  * (1 + 4*jump_index + direction_index for propagation, 100 + k for random
  * search step k) and, for random-search entries, the clipped window
  * (lo_r, hi_r, lo_c, hi_c) it was drawn from.  Returns the entry count.
  */
 int64_t oracle_pm_trace(const double* Q, const double* K, int64_t S, int64_t Hq, int64_t Wq,
                         int64_t Hk, int64_t Wk, int d, uint64_t seed, int64_t t, uint32_t flags,
+                        const int32_t* prev, int64_t n_prev, int64_t sep,
                         const int32_t* J_prev, const double* s_prev, int64_t g, int64_t cap,
                         int64_t* idx_out, int32_t* kind_out, double* window_out,
                         int32_t* final_out)
 {
     if (check_dims(S, Hq, Wq, Hk, Wk, d) || t < 1 || g < 0 || g >= S * Hq * Wq) return -2;
-    pm_problem P = {Q, K, S, Hq, Wq, Hk, Wk, d, {0, 0}, flags, 0.0};
+    if (n_prev < 0 || sep < 1 || (n_prev > 0 && !prev)) return -2;
+    if ((flags & OR_CAUSAL) && (Hq != Hk || Wq != Wk)) return -2;
+    pm_problem P = {Q, K, S, Hq, Wq, Hk, Wk, d, {0, 0}, flags, 0.0, prev, n_prev, sep};
     seed_key(seed, P.key);
     pm_state st;
     memset(&st, 0, sizeof st);
@@ -350,14 +402,16 @@ int64_t oracle_pm_trace(const double* Q, const double* K, int64_t S, int64_t Hq,
 }
 
 /*
- * Whole PatchMatch run (Algorithm 1, kappa = 1): random initialisation when
- * init is NULL (else J_0 = init and s_0 its fp64 scores), then iterations
- * t0 .. t0 + iters - 1.  ties_out (nullable) is [iters, n]: the tie flags of
+ * Whole PatchMatch run (Algorithm 1) number n_prev, given the maps of the
+ * n_prev previous runs: random initialisation when init is NULL (else J_0 =
+ * init and s_0 its fp64 scores), then iterations t0 .. t0 + iters - 1.
+ * s_out holds minus infinity for a query whose final match is not valid.  ties_out (nullable) is [iters, n]: the tie flags of
  * each iteration.  ncand_out (nullable) receives the total candidates scored.
  */
 int oracle_patchmatch(const double* Q, const double* K, int64_t S, int64_t Hq, int64_t Wq,
                       int64_t Hk, int64_t Wk, int d, int64_t iters, uint64_t seed,
                       const int32_t* init, int64_t t0, uint32_t flags, double tie_rel,
+                      const int32_t* prev, int64_t n_prev, int64_t sep,
                       int32_t* J_out, double* s_out, uint8_t* ties_out, int64_t* ncand_out)
 {
     if (check_dims(S, Hq, Wq, Hk, Wk, d) || iters < 0 || t0 < 1) return -2;
@@ -373,13 +427,13 @@ int oracle_patchmatch(const double* Q, const double* K, int64_t S, int64_t Hq, i
         memcpy(Ja, init, sizeof(int32_t) * n);
         rc = oracle_pm_scores(Q, K, S, Hq, Wq, Hk, Wk, d, Ja, sa, NULL);
     } else {
-        rc = oracle_pm_init(Q, K, S, Hq, Wq, Hk, Wk, d, seed, Ja, sa);
+        rc = oracle_pm_init(Q, K, S, Hq, Wq, Hk, Wk, d, seed, flags, n_prev, Ja, sa);
     }
     if (rc) goto done;
     for (int64_t it = 0; it < iters; ++it) {
         int64_t nc = 0;
-        rc = oracle_pm_iteration(Q, K, S, Hq, Wq, Hk, Wk, d, seed, t0 + it, flags, tie_rel, Ja,
-                                 sa, NULL, 0, Jb, sb, ties_out ? ties_out + it * n : NULL, &nc);
+        rc = oracle_pm_iteration(Q, K, S, Hq, Wq, Hk, Wk, d, seed, t0 + it, flags, tie_rel, prev, n_prev,
+                                 sep, Ja, sa, NULL, 0, Jb, sb, ties_out ? ties_out + it * n : NULL, &nc);
         if (rc) goto done;
         total += nc;
         int32_t* tj = Ja; Ja = Jb; Jb = tj;
@@ -393,59 +447,86 @@ done:
     return rc;
 }
 
+/* key (r, c) lies in the window of half-width b centred on flat key index centre */
+static int in_window(int64_t r, int64_t c, int64_t centre, int64_t Wk, int64_t b)
+{
+    return llabs(r - centre / Wk) <= b && llabs(c - centre % Wk) <= b;
+}
+
 /*
- * Sparse non-local mean (Algorithm 2, Equations 8-9) at kappa = 1: for each
- * listed query i with match (u, v) = J[i], the window
- * {(u + a, v + b') : |a|, |b'| <= b} intersected with the key grid, scores
- * a_j = scale * q_i . k_j, and the output sum_j softmax(a)_j v_j.  Two
- * passes: the maximum score first, then exp(a_j - max) weights.
- * out is compact [count, dv].
+ * Sparse non-local mean (Algorithm 2, Equations 8-9): for each listed query i
+ * the set J_i = union over the kappa matches e of the window
+ * {(u_e + a, v_e + c) : |a|, |c| <= b} (each key once), intersected with the
+ * key grid (and, with OR_CAUSAL, with the keys up to i), scores
+ * a_j = scale * q_i . k_j and the output sum_j softmax(a)_j v_j.  J is
+ * [kappa, S, Hq, Wq].  Two passes: the maximum score first, then
+ * exp(a_j - max) weights.  out is compact [count, dv].
  */
 int oracle_sparse_attend(const double* Q, const double* K, const double* V, const int32_t* J,
-                         int64_t S, int64_t Hq, int64_t Wq, int64_t Hk, int64_t Wk, int d, int dv,
-                         int window, double scale, const int64_t* query_ids, int64_t nq,
-                         double* out)
+                         int64_t kappa, int64_t S, int64_t Hq, int64_t Wq, int64_t Hk, int64_t Wk, int d,
+                         int dv, int window, double scale, uint32_t flags, const int64_t* query_ids,
+                         int64_t nq, double* out)
 {
-    if (check_dims(S, Hq, Wq, Hk, Wk, d) || dv <= 0 || window < 1 || window % 2 == 0) return -2;
+    if (check_dims(S, Hq, Wq, Hk, Wk, d) || dv <= 0 || window < 1 || window % 2 == 0 || kappa < 1) return -2;
+    if ((flags & OR_CAUSAL) && (Hq != Hk || Wq != Wk)) return -2;
     const int64_t n = S * Hq * Wq, plane = Hq * Wq;
     const int64_t b = window / 2;
     const int64_t count = query_ids ? nq : n;
-    for (int64_t g = 0; g < n; ++g)
+    for (int64_t g = 0; g < kappa * n; ++g)
         if (J[g] < 0 || J[g] >= Hk * Wk) return -2;
     if (query_ids)
         for (int64_t i = 0; i < nq; ++i)
             if (query_ids[i] < 0 || query_ids[i] >= n) return -2;
+    const int64_t wr = window < Hk ? window : Hk, wc = window < Wk ? window : Wk;
+    const int64_t cap = kappa * wr * wc; /* at most this many keys in one query's set */
+    int rc = 0;
 #pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < count; ++i) {
         int64_t g = query_ids ? query_ids[i] : i;
         int64_t s = g / plane;
+        const int64_t last = (flags & OR_CAUSAL) ? g % plane : Hk * Wk - 1;
         const double* q = Q + g * d;
         const double* Ks = K + s * Hk * Wk * d;
         const double* Vs = V + s * Hk * Wk * dv;
-        int64_t u = J[g] / Wk, v = J[g] % Wk;
-        double m = -INFINITY;
-        for (int64_t a = -b; a <= b; ++a)
-            for (int64_t c = -b; c <= b; ++c) {
-                int64_t r = u + a, col = v + c;
-                if (r < 0 || r >= Hk || col < 0 || col >= Wk) continue;
-                double sc = scale * dot(q, Ks + (r * Wk + col) * d, d);
-                if (sc > m) m = sc;
-            }
-        double denom = 0.0;
         double* o = out + i * dv;
+        int64_t* keys = (int64_t*)malloc(sizeof(int64_t) * cap);
+        if (!keys) {
+            rc = -6;
+            continue;
+        }
+        /* 1. the key set: every window, clipped to the grid, each key once */
+        int64_t nk = 0;
+        for (int64_t e = 0; e < kappa; ++e) {
+            const int64_t centre = J[e * n + g];
+            const int64_t u = centre / Wk, v = centre % Wk;
+            for (int64_t a = -b; a <= b; ++a)
+                for (int64_t c = -b; c <= b; ++c) {
+                    int64_t r = u + a, col = v + c;
+                    if (r < 0 || r >= Hk || col < 0 || col >= Wk) continue;
+                    if (r * Wk + col > last) continue;
+                    int seen = 0; /* already in the window of an earlier match */
+                    for (int64_t f = 0; f < e && !seen; ++f) seen = in_window(r, col, J[f * n + g], Wk, b);
+                    if (!seen) keys[nk++] = r * Wk + col;
+                }
+        }
+        /* 2. softmax over the set (two passes) and the weighted sum of values */
+        double m = -INFINITY;
+        for (int64_t j = 0; j < nk; ++j) {
+            double sc = scale * dot(q, Ks + keys[j] * d, d);
+            if (sc > m) m = sc;
+        }
+        double denom = 0.0;
         for (int e = 0; e < dv; ++e) o[e] = 0.0;
-        for (int64_t a = -b; a <= b; ++a)
-            for (int64_t c = -b; c <= b; ++c) {
-                int64_t r = u + a, col = v + c;
-                if (r < 0 || r >= Hk || col < 0 || col >= Wk) continue;
-                double w = exp(scale * dot(q, Ks + (r * Wk + col) * d, d) - m);
-                denom += w;
-                const double* vv = Vs + (r * Wk + col) * dv;
-                for (int e = 0; e < dv; ++e) o[e] += w * vv[e];
-            }
+        for (int64_t j = 0; j < nk; ++j) {
+            double w = exp(scale * dot(q, Ks + keys[j] * d, d) - m);
+            denom += w;
+            const double* vv = Vs + keys[j] * dv;
+            for (int e = 0; e < dv; ++e) o[e] += w * vv[e];
+        }
         for (int e = 0; e < dv; ++e) o[e] /= denom;
+        free(keys);
     }
-    return 0;
+    return rc;
 }
 
 /* Threads the OpenMP runtime would use (1 when built without OpenMP). */
