@@ -3,7 +3,9 @@
 A step is one pass of the whole path over one batch of resident synthetic
 input: PatchMatch (random init + T Jacobi sweeps, one library call) then the
 sparse window attention (one call), on the 256x256, d=64, bf16, 4-slice
-workload by default.  Two timed regions: A runs the steps as a caller would
+workload by default.  ``--kappa K`` runs K constrained PatchMatch runs (run c
+given the maps of runs 0..c-1, separation ``--sep``) and attends over the
+union of their windows; ``--causal`` masks keys after each query.  Two timed regions: A runs the steps as a caller would
 (throughput: ``value``, ``ms_per_step``); B runs the same steps with every
 kernel dispatch stamping caller-created HIP start/stop events on the launch
 stream (per-kernel durations for ``kernels_ms`` and ``roofline``; the stamps
@@ -31,18 +33,19 @@ KERNEL_SRC = os.path.join(ROOT, "paper_1905_10308_amd", "csrc", "scram_kernels.h
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pm_iter_traffic.json")
 
 
-def pm_bytes_per_query_sweep(cfg) -> int:
+def pm_bytes_per_query_sweep(cfg, n_prev: int = 0) -> int:
     """Algorithmic bytes of one query in one sweep: its q row, C candidate key
-    rows, and 4 B each for the previous index and score read and the new index
-    and score written."""
+    rows, 4 B each for the previous index and score read and the new index
+    and score written, and 4 B per previous run's match."""
     row = cfg.d * cfg.elem_bytes
-    return row * (1 + cfg.candidates) + 16
+    return row * (1 + cfg.candidates) + 16 + 4 * n_prev
 
 
-def attend_bytes_per_query(cfg) -> int:
-    """q row, w^2 key rows, w^2 value rows, the 4 B index, the output row."""
+def attend_bytes_per_query(cfg, kappa: int = 1) -> int:
+    """q row, kappa windows of w^2 key rows and w^2 value rows (every window
+    read in full), kappa 4 B indices, the output row."""
     row = cfg.d * cfg.elem_bytes
-    return row * (2 + 2 * cfg.window ** 2) + 4
+    return row * (2 + 2 * kappa * cfg.window ** 2) + 4 * kappa
 
 
 def init_bytes_per_query(cfg) -> int:
@@ -67,7 +70,7 @@ def load_traffic(cfg):
     return t.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(cfg, arrays, min_s: float):
+def cpu_baseline(cfg, arrays, min_s: float, kappa: int = 1, sep: int = 1, causal: bool = False):
     """The fp64 oracle on the host cores, on whole slices of the same workload.
 
     Slices are run in turn (wrapping around) until at least ``min_s`` seconds
@@ -78,14 +81,15 @@ def cpu_baseline(cfg, arrays, min_s: float):
     import oracle
 
     threads = oracle.num_threads()
+    flags = oracle.CAUSAL if causal else 0
     Q, K, V = (arrays[k].astype(np.float64) for k in ("Q", "K", "V"))
     done_q, elapsed, runs = 0, 0.0, 0
     per_slice = cfg.Hq * cfg.Wq
     while elapsed < min_s and runs < 64 * cfg.S:
         s = runs % cfg.S
         t0 = time.perf_counter()
-        J, _, _, _ = oracle.patchmatch(Q[s:s + 1], K[s:s + 1], cfg.iters, cfg.pm_seed)
-        oracle.sparse_attend(Q[s:s + 1], K[s:s + 1], V[s:s + 1], J, cfg.window, cfg.scale)
+        J, _, _ = oracle.patchmatch_kappa(Q[s:s + 1], K[s:s + 1], kappa, cfg.iters, cfg.pm_seed, sep=sep, flags=flags)
+        oracle.sparse_attend(Q[s:s + 1], K[s:s + 1], V[s:s + 1], J, cfg.window, cfg.scale, flags=flags)
         elapsed += time.perf_counter() - t0
         done_q += per_slice
         runs += 1
@@ -94,8 +98,8 @@ def cpu_baseline(cfg, arrays, min_s: float):
         "unit": "queries/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": f"{runs} slice passes over the {cfg.S}-slice workload ({done_q} queries; {cfg.iters} sweeps + "
-                  f"{cfg.window}x{cfg.window} attend each), fp64, {elapsed:.1f} s",
+        "sample": f"{runs} slice passes over the {cfg.S}-slice workload ({done_q} queries; {kappa} x {cfg.iters} "
+                  f"sweeps + {cfg.window}x{cfg.window} attend each), fp64, {elapsed:.1f} s",
     }
 
 
@@ -105,6 +109,9 @@ def main(argv=None) -> int:
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=None, help="workload index (default: the 256x256 bf16 one)")
+    ap.add_argument("--kappa", type=int, default=1, help="matches per query (constrained PatchMatch runs)")
+    ap.add_argument("--sep", type=int, default=1, help="separation between the runs' matches (Chebyshev)")
+    ap.add_argument("--causal", action="store_true", help="mask keys after each query (raster order)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="seconds of oracle work for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -146,21 +153,26 @@ def main(argv=None) -> int:
     dev = Q.device
     stream = torch.cuda.current_stream(dev)
 
-    J = torch.empty((S, Hq, Wq), dtype=torch.int32, device=dev)
+    kappa, sep, causal = args.kappa, args.sep, args.causal
+    J = torch.empty((kappa, S, Hq, Wq), dtype=torch.int32, device=dev)
     ws = torch.empty(scram.patchmatch_workspace_bytes(S, Hq, Wq), dtype=torch.uint8, device=dev)
     out = torch.empty((S, Hq, Wq, cfg.dv), dtype=Q.dtype, device=dev)
     T = cfg.iters
+    per_run = 2 * (T + 1)  # events of one PatchMatch call: init, T sweeps
 
     def new_events():
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(2 * (T + 1) + 2)]
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(kappa * per_run + 2)]
         for e in evs:  # create the underlying HIP events before handing them to the library
             e.record(stream)
         return evs
 
     def step(ev=None):
-        # the dispatches stamp start/stop events: init, T sweeps, attend
-        scram.patchmatch(Q, K, T, cfg.pm_seed, out=J, workspace=ws, events=None if ev is None else ev[:-2])
-        scram.sparse_attend(Q, K, V, J, cfg.window, cfg.scale, out=out, events=None if ev is None else ev[-2:])
+        # the dispatches stamp start/stop events: per run init and T sweeps, then attend
+        for c in range(kappa):
+            scram.patchmatch(Q, K, T, cfg.pm_seed, prev=J[:c] if c else None, sep=sep, causal=causal, out=J[c],
+                             workspace=ws, events=None if ev is None else ev[c * per_run:(c + 1) * per_run])
+        scram.sparse_attend(Q, K, V, J if kappa > 1 else J[0], cfg.window, cfg.scale, causal=causal, out=out,
+                            events=None if ev is None else ev[-2:])
 
     for _ in range(args.warmup):
         step()
@@ -187,15 +199,19 @@ def main(argv=None) -> int:
         return ev[2 * k].elapsed_time(ev[2 * k + 1])
 
     ms_step = start.elapsed_time(stop) / args.steps
-    init_ms = sum(dur(ev, 0) for ev in events) / args.steps
-    iter_ms = sum(dur(ev, t) for ev in events for t in range(1, T + 1)) / (args.steps * T)
-    att_ms = sum(dur(ev, T + 1) for ev in events) / args.steps
+    init_ms = sum(dur(ev, c * (T + 1)) for ev in events for c in range(kappa)) / (args.steps * kappa)
+    iter_by_run = [sum(dur(ev, c * (T + 1) + t) for ev in events for t in range(1, T + 1)) / (args.steps * T)
+                   for c in range(kappa)]
+    iter_ms = sum(iter_by_run) / kappa
+    att_ms = sum(dur(ev, kappa * (T + 1)) for ev in events) / args.steps
 
     nq = cfg.nq
-    pm_launch_bytes = nq * pm_bytes_per_query_sweep(cfg)
-    att_bytes = nq * attend_bytes_per_query(cfg)
+    # the dominant kernel: the sweep, averaged over the runs (run c reads c previous maps)
+    pm_launch_bytes = nq * sum(pm_bytes_per_query_sweep(cfg, c) for c in range(kappa)) / kappa
+    att_bytes = nq * attend_bytes_per_query(cfg, kappa)
     achieved = pm_launch_bytes / (iter_ms * 1e-3) / 1e9
-    traffic_bytes = load_traffic(cfg)
+    default_path = kappa == 1 and not causal
+    traffic_bytes = load_traffic(cfg) if default_path else None
     traffic = None if traffic_bytes is None else traffic_bytes / (iter_ms * 1e-3) / 1e9
 
     res = {
@@ -221,6 +237,9 @@ def main(argv=None) -> int:
             "storage": cfg.dtype,
             "iters": T,
             "window": cfg.window,
+            "kappa": kappa,
+            "separation": sep,
+            "causal": causal,
             "queries_per_step": nq,
         },
         "roofline": {
@@ -235,14 +254,15 @@ def main(argv=None) -> int:
             "algorithmic_bytes_per_launch": pm_launch_bytes,
         },
         "kernels_ms": {"pm_init": init_ms, "pm_iter": iter_ms, "attend": att_ms},
+        "pm_iter_ms_by_run": iter_by_run,
         "kernels_ms_source": "dispatch-stamped HIP events, timed region B",
         "attend_GBps": att_bytes / (att_ms * 1e-3) / 1e9,
-        "candidate_evals_per_s_nominal": nq * T * cfg.candidates / (ms_step * 1e-3),
+        "candidate_evals_per_s_nominal": kappa * nq * T * cfg.candidates / (ms_step * 1e-3),
         "wall_ms_per_step": wall * 1e3 / args.steps,
         "device": torch.cuda.get_device_name(dev),
     }
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(cfg, data["np"], args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(cfg, data["np"], args.cpu_seconds, kappa, sep, causal)
     print(json.dumps(res), flush=True)
     return 0
 

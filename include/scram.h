@@ -15,6 +15,15 @@
  *      window of keys around each query's match, then the weighted sum of
  *      the values of those keys.
  *
+ * Several matches per query (kappa > 1, Section 4.2 and Algorithm 2's first
+ * step) come from kappa runs of scram_patchmatch, run c receiving the maps of
+ * runs 0..c-1 (Algorithm 1's input J) and a separation L: is_index_valid
+ * keeps a key only if its Chebyshev distance max(|du|, |dv|) to each earlier
+ * match is at least L (L = 1: distinct keys, the top-kappa-max variant;
+ * L > 1: separated modes, top-kappa-mode).  scram_sparse_attend then takes
+ * the union of the kappa windows, each key once.  SCRAM_CAUSAL (Section
+ * 4.2.1) restricts both steps to keys at or before the query in raster order.
+ *
  * Conventions shared by every entry point
  * ----------------------------------------
  * - Data layout: row-major, channels innermost.  Q is [S, Hq, Wq, d], K is
@@ -72,6 +81,13 @@ enum {
 /* flags of scram_patchmatch: switch one step of an iteration off (tests) */
 enum { SCRAM_PM_NO_PROPAGATION = 1u, SCRAM_PM_NO_RANDOM_SEARCH = 2u };
 
+/* flag of both entry points: autoregressive masking (query grid == key grid) */
+enum { SCRAM_CAUSAL = 4u };
+
+/* most previous runs one PatchMatch run may be constrained by, and most maps
+ * one attend call may unite */
+enum { SCRAM_MAX_PREV = 7, SCRAM_MAX_KAPPA = 8 };
+
 /*
  * Bytes of workspace scram_patchmatch needs for S*Hq*Wq queries: one int32
  * index map and two fp32 score maps, each rounded up to 256 bytes.
@@ -85,8 +101,9 @@ size_t scram_patchmatch_workspace_bytes(int S, int Hq, int Wq);
  * Initialisation (Algorithm 1, first loop): when `init` is NULL, query g
  * draws J0[g] = u * Wk + v with u = floor(w0 * Hk / 2^32),
  * v = floor(w1 * Wk / 2^32), where (w0, w1, ., .) is the Philox4x32-10 block
- * (Salmon et al., SC 2011) of counter (g, 0, 0, 0) and key
- * (seed mod 2^32, seed div 2^32).  When `init` is given it is J0 (not
+ * (Salmon et al., SC 2011) of counter (g, 0, 0, n_prev) and key
+ * (seed mod 2^32, seed div 2^32); with SCRAM_CAUSAL, J0[g] =
+ * floor(w0 * (i + 1) / 2^32) for the query's raster index i in its slice.  When `init` is given it is J0 (not
  * modified; entries clamped into the key grid).  The incumbent scores s0 are
  * the fp32 dot products q_g . k_J0[g], or `init_score` when given (which
  * must then hold exactly what this library computed for that map, e.g. a
@@ -101,10 +118,12 @@ size_t scram_patchmatch_workspace_bytes(int S, int Hq, int Wq);
  *   - random search: with D = R = max(Hk, Wk), halved (integer) down to 1,
  *     a key drawn uniformly from the square of half-side D around the
  *     running best, clipped to the key grid; step k uses the Philox block of
- *     counter (g, t, k div 2, 0), words 2(k mod 2) and 2(k mod 2) + 1 mapped
- *     like the initial draw onto the clipped rows and columns;
- *   - a candidate replaces the incumbent iff its unscaled fp32 score q.k is
- *     larger, or equal with a lower flat key index.
+ *     counter (g, t, k div 2, n_prev), words 2(k mod 2) and 2(k mod 2) + 1
+ *     mapped like the initial draw onto the clipped rows and columns;
+ *   - a candidate replaces the incumbent iff it is valid (see the several
+ *     matches and causal notes above) and its unscaled fp32 score q.k is
+ *     larger, or equal with a lower flat key index.  An incumbent that is
+ *     not valid counts as minus infinity.
  *
  * Arguments:
  *   Q, K        inputs, layouts above, element type `dtype`
@@ -117,9 +136,16 @@ size_t scram_patchmatch_workspace_bytes(int S, int Hq, int Wq);
  *   t0          index of the first sweep, >= 1 (1 for a fresh run; a run
  *               split as (T1 sweeps) then (init = its map, t0 = T1 + 1)
  *               equals the unsplit run bit for bit)
- *   flags       0, or SCRAM_PM_NO_PROPAGATION / SCRAM_PM_NO_RANDOM_SEARCH
+ *   flags       0, or SCRAM_PM_NO_PROPAGATION / SCRAM_PM_NO_RANDOM_SEARCH /
+ *               SCRAM_CAUSAL
+ *   prev        int32 [n_prev, S, Hq, Wq] maps of the previous runs (NULL
+ *               when n_prev = 0); read only
+ *   n_prev      0 <= n_prev <= SCRAM_MAX_PREV: previous runs, and this run's
+ *               index in the Philox counter (0 for a single-match run)
+ *   sep         separation L >= 1 from the previous runs' matches
  *   argmax_out  int32 [S, Hq, Wq] final map J_T (written)
- *   score_out   nullable fp32 [S, Hq, Wq] final scores q . k_{J_T} (unscaled)
+ *   score_out   nullable fp32 [S, Hq, Wq] final scores q . k_{J_T} (unscaled;
+ *               minus infinity where no valid key was found)
  *   workspace   >= scram_patchmatch_workspace_bytes(S, Hq, Wq) bytes of
  *               device memory, contents ignored and overwritten
  *   events      nullable array of 2 * (iters + 1) caller-created HIP
@@ -135,30 +161,36 @@ size_t scram_patchmatch_workspace_bytes(int S, int Hq, int Wq);
  */
 int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int Wq, int Hk, int Wk,
                      int d, int iters, uint64_t seed, const int32_t* init, const float* init_score,
-                     int t0, uint32_t flags, int32_t* argmax_out, float* score_out, void* workspace,
-                     size_t workspace_bytes, hipEvent_t* events, hipStream_t stream);
+                     int t0, uint32_t flags, const int32_t* prev, int n_prev, int sep, int32_t* argmax_out,
+                     float* score_out, void* workspace, size_t workspace_bytes, hipEvent_t* events,
+                     hipStream_t stream);
 
 /*
- * Sparse attention around the argmax (Algorithm 2 with kappa = 1,
- * Equations 8-9).  For query g with match (u, v) = divmod(argmax[g], Wk):
- * the window W_g = {(u + a, v + c) : |a|, |c| <= b} with b = (window - 1)/2,
- * keys outside the key grid dropped (the match itself is always inside);
+ * Sparse attention around the matches (Algorithm 2, Equations 8-9).  For
+ * query g with matches (u_e, v_e) = divmod(argmax[e][g], Wk), e < kappa: the
+ * set W_g = union over e of {(u_e + a, v_e + c) : |a|, |c| <= b} with
+ * b = (window - 1)/2, each key once, keys outside the key grid dropped (and,
+ * with SCRAM_CAUSAL, keys after the query in raster order);
  * out[g] = sum_{j in W_g} softmax_j(scale * q_g . k_j) v_j, computed with an
- * fp32 online softmax and written in `dtype`.
+ * fp32 online softmax and written in `dtype` (a zero row if W_g is empty,
+ * which cannot happen without SCRAM_CAUSAL).
  *
  * Arguments:
  *   Q, K, V   inputs, layouts above; V has dv channels (dv == d)
- *   argmax    int32 [S, Hq, Wq] flat key indices (e.g. scram_patchmatch's)
+ *   argmax    int32 [kappa, S, Hq, Wq] flat key indices (e.g. kappa runs of
+ *             scram_patchmatch)
+ *   kappa     1 <= kappa <= SCRAM_MAX_KAPPA
  *   window    odd side 2b + 1 >= 1 of the square window (<= 32767)
  *   scale     softmax temperature, 1/sqrt(d_k) for Equation 1; finite
+ *   flags     0 or SCRAM_CAUSAL
  *   out       [S, Hq, Wq, dv] in `dtype` (written; must not overlap inputs)
  *   events    nullable array of 2 caller-created HIP events stamped with the
  *             kernel's start and end (as in scram_patchmatch)
  * Returns a status code.
  */
-int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype,
-                        const int32_t* argmax, int S, int Hq, int Wq, int Hk, int Wk, int d, int dv,
-                        int window, float scale, void* out, hipEvent_t* events, hipStream_t stream);
+int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype, const int32_t* argmax, int kappa,
+                        int S, int Hq, int Wq, int Hk, int Wk, int d, int dv, int window, float scale,
+                        uint32_t flags, void* out, hipEvent_t* events, hipStream_t stream);
 
 /* Static, NUL-terminated description of a status code. */
 const char* scram_status_string(int status);
@@ -166,7 +198,7 @@ const char* scram_status_string(int status);
 /* ABI version of this header: (major << 16) | minor. */
 int scram_abi_version(void);
 
-#define SCRAM_ABI_VERSION ((1 << 16) | 0)
+#define SCRAM_ABI_VERSION ((2 << 16) | 0)
 
 #ifdef __cplusplus
 }

@@ -460,7 +460,8 @@ static int in_window(int64_t r, int64_t c, int64_t centre, int64_t Wk, int64_t b
  * key grid (and, with OR_CAUSAL, with the keys up to i), scores
  * a_j = scale * q_i . k_j and the output sum_j softmax(a)_j v_j.  J is
  * [kappa, S, Hq, Wq].  Two passes: the maximum score first, then
- * exp(a_j - max) weights.  out is compact [count, dv].
+ * exp(a_j - max) weights.  An empty set (possible only with OR_CAUSAL and a
+ * match after the query) gives a zero row.  out is compact [count, dv].
  */
 int oracle_sparse_attend(const double* Q, const double* K, const double* V, const int32_t* J,
                          int64_t kappa, int64_t S, int64_t Hq, int64_t Wq, int64_t Hk, int64_t Wk, int d,
@@ -523,7 +524,7 @@ int oracle_sparse_attend(const double* Q, const double* K, const double* V, cons
             const double* vv = Vs + keys[j] * dv;
             for (int e = 0; e < dv; ++e) o[e] += w * vv[e];
         }
-        for (int e = 0; e < dv; ++e) o[e] /= denom;
+        for (int e = 0; e < dv; ++e) o[e] = nk > 0 ? o[e] / denom : 0.0; /* empty set: zero row */
         free(keys);
     }
     return rc;

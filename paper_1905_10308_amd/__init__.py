@@ -6,12 +6,16 @@ Importing the package does not load the library; the first call does, and
 raises if it is missing.
 """
 from .binding import (  # noqa: F401
+    CAUSAL,
+    MAX_KAPPA,
+    MAX_PREV,
     NO_PROPAGATION,
     NO_RANDOM_SEARCH,
     ScramError,
     forward,
     lib,
     patchmatch,
+    patchmatch_kappa,
     patchmatch_workspace_bytes,
     sparse_attend,
     status_string,

@@ -17,6 +17,9 @@ SCRAM_F32 = 0
 SCRAM_BF16 = 1
 NO_PROPAGATION = 1
 NO_RANDOM_SEARCH = 2
+CAUSAL = 4
+MAX_PREV = 7
+MAX_KAPPA = 8
 
 STATUS = {
     0: "SCRAM_OK",
@@ -50,9 +53,9 @@ def lib() -> ctypes.CDLL:
     P, I, U32, U64, SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_size_t
     L.scram_patchmatch_workspace_bytes.argtypes = [I, I, I]
     L.scram_patchmatch_workspace_bytes.restype = SZ
-    L.scram_patchmatch.argtypes = [P, P, I, I, I, I, I, I, I, I, U64, P, P, I, U32, P, P, P, SZ, P, P]
+    L.scram_patchmatch.argtypes = [P, P, I, I, I, I, I, I, I, I, U64, P, P, I, U32, P, I, I, P, P, P, SZ, P, P]
     L.scram_patchmatch.restype = I
-    L.scram_sparse_attend.argtypes = [P, P, P, I, P, I, I, I, I, I, I, I, I, ctypes.c_float, P, P, P]
+    L.scram_sparse_attend.argtypes = [P, P, P, I, P, I, I, I, I, I, I, I, I, I, ctypes.c_float, U32, P, P, P]
     L.scram_sparse_attend.restype = I
     L.scram_status_string.argtypes = [I]
     L.scram_status_string.restype = ctypes.c_char_p
@@ -120,12 +123,16 @@ def _event_array(events, n):
 
 
 def patchmatch(Q, K, iters: int, seed: int, *, init=None, init_score=None, t0: int = 1, flags: int = 0,
-               out=None, score_out=None, workspace=None, return_score: bool = False, events=None):
+               prev=None, sep: int = 1, causal: bool = False, out=None, score_out=None, workspace=None,
+               return_score: bool = False, events=None):
     """PatchMatch argmax map (``scram_patchmatch``).
 
     Q ``[S, Hq, Wq, d]``, K ``[S, Hk, Wk, d]`` (float32 or bfloat16, same dtype).
     Returns int32 ``[S, Hq, Wq]`` flat key indices (and fp32 scores if
     ``return_score``).  ``init``/``init_score``/``t0`` resume a run.
+    ``prev`` (int32 ``[C, S, Hq, Wq]``) and ``sep`` constrain this run to keys
+    at Chebyshev distance >= ``sep`` from the C previous runs' matches (this
+    is run C); ``causal`` keeps keys at or before the query in raster order.
     ``events``: optional ``2 * (iters + 1)`` timing-enabled torch.cuda.Event
     objects, stamped with the start and end of each launch (init, then each
     sweep).
@@ -150,23 +157,37 @@ def patchmatch(Q, K, iters: int, seed: int, *, init=None, init_score=None, t0: i
             _dev_tensor(t, name)
             if t.dtype != dt or tuple(t.shape) != (S, Hq, Wq):
                 raise ValueError(f"{name} must be {dt} of shape {(S, Hq, Wq)}")
+    n_prev = 0
+    if prev is not None:
+        _dev_tensor(prev, "prev")
+        if prev.dtype != torch.int32 or prev.dim() != 4 or tuple(prev.shape[1:]) != (S, Hq, Wq):
+            raise ValueError("prev must be int32 [C, S, Hq, Wq]")
+        n_prev = prev.shape[0]
+        if n_prev == 0:
+            prev = None
+    if causal:
+        flags |= CAUSAL
     need = patchmatch_workspace_bytes(S, Hq, Wq)
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
     ev = None if events is None else _event_array(events, 2 * (int(iters) + 1))
     rc = lib().scram_patchmatch(_ptr(Q), _ptr(K), _dtype_code(Q), S, Hq, Wq, Hk, Wk, d, int(iters),
                                 ctypes.c_uint64(int(seed) & 0xFFFFFFFFFFFFFFFF), _ptr(init), _ptr(init_score),
-                                int(t0), int(flags), _ptr(out), _ptr(score_out), _ptr(workspace),
+                                int(t0), int(flags), _ptr(prev), int(n_prev), int(sep), _ptr(out), _ptr(score_out),
+                                _ptr(workspace),
                                 workspace.numel() * workspace.element_size(), ev, _stream(dev))
     if rc != 0:
         raise ScramError(rc, "scram_patchmatch")
     return (out, score_out) if return_score else out
 
 
-def sparse_attend(Q, K, V, argmax, window: int, scale: float | None = None, *, out=None, events=None):
+def sparse_attend(Q, K, V, argmax, window: int, scale: float | None = None, *, causal: bool = False, out=None,
+                  events=None):
     """Window softmax + value gather around ``argmax`` (``scram_sparse_attend``).
 
-    Returns ``[S, Hq, Wq, dv]`` in Q's dtype.  ``scale`` defaults to 1/sqrt(d).
+    ``argmax`` is int32 ``[S, Hq, Wq]`` or ``[kappa, S, Hq, Wq]`` (union of the
+    kappa windows).  Returns ``[S, Hq, Wq, dv]`` in Q's dtype.  ``scale``
+    defaults to 1/sqrt(d).
     ``events``: optional 2 timing-enabled torch.cuda.Event objects stamped with
     the kernel's start and end.
     """
@@ -175,28 +196,48 @@ def sparse_attend(Q, K, V, argmax, window: int, scale: float | None = None, *, o
         _dev_tensor(t, name, 4)
         if t.dtype != Q.dtype:
             raise TypeError("Q, K, V must share a dtype")
-    _dev_tensor(argmax, "argmax", 3)
+    _dev_tensor(argmax, "argmax")
     S, Hq, Wq, d = Q.shape
     _, Hk, Wk, _ = K.shape
     dv = V.shape[3]
     if tuple(K.shape[:3]) != tuple(V.shape[:3]) or K.shape[0] != S or K.shape[3] != d:
         raise ValueError("K and V must share the key grid; K must match Q's slices and channels")
-    if argmax.dtype != torch.int32 or tuple(argmax.shape) != (S, Hq, Wq):
-        raise ValueError("argmax must be int32 [S, Hq, Wq]")
+    if argmax.dtype != torch.int32 or tuple(argmax.shape[-3:]) != (S, Hq, Wq) or argmax.dim() not in (3, 4):
+        raise ValueError("argmax must be int32 [S, Hq, Wq] or [kappa, S, Hq, Wq]")
+    kappa = 1 if argmax.dim() == 3 else argmax.shape[0]
     if scale is None:
         scale = d ** -0.5
     if out is None:
         out = torch.empty((S, Hq, Wq, dv), dtype=Q.dtype, device=Q.device)
     _dev_tensor(out, "out", 4)
     ev = None if events is None else _event_array(events, 2)
-    rc = lib().scram_sparse_attend(_ptr(Q), _ptr(K), _ptr(V), _dtype_code(Q), _ptr(argmax), S, Hq, Wq, Hk, Wk,
-                                   d, dv, int(window), float(scale), _ptr(out), ev, _stream(Q.device))
+    rc = lib().scram_sparse_attend(_ptr(Q), _ptr(K), _ptr(V), _dtype_code(Q), _ptr(argmax), int(kappa), S, Hq, Wq,
+                                   Hk, Wk, d, dv, int(window), float(scale), CAUSAL if causal else 0, _ptr(out), ev,
+                                   _stream(Q.device))
     if rc != 0:
         raise ScramError(rc, "scram_sparse_attend")
     return out
 
 
-def forward(Q, K, V, iters: int, seed: int, window: int, scale: float | None = None):
-    """The whole hot path: argmax map, then the sparse attention output."""
-    J = patchmatch(Q, K, iters, seed)
-    return sparse_attend(Q, K, V, J, window, scale), J
+def patchmatch_kappa(Q, K, kappa: int, iters: int, seed: int, *, sep: int = 1, causal: bool = False, flags: int = 0):
+    """kappa constrained runs of ``scram_patchmatch`` -> int32 ``[kappa, S, Hq, Wq]``.
+
+    Run c receives the maps of runs 0..c-1 (Algorithm 2's first step).
+    """
+    torch = _torch()
+    S, Hq, Wq, _ = Q.shape
+    if not 1 <= kappa <= MAX_KAPPA:
+        raise ValueError(f"kappa must be in [1, {MAX_KAPPA}]")
+    maps = torch.empty((kappa, S, Hq, Wq), dtype=torch.int32, device=Q.device)
+    ws = torch.empty(patchmatch_workspace_bytes(S, Hq, Wq), dtype=torch.uint8, device=Q.device)
+    for c in range(kappa):
+        patchmatch(Q, K, iters, seed, flags=flags, prev=maps[:c] if c else None, sep=sep, causal=causal,
+                   out=maps[c], workspace=ws)
+    return maps
+
+
+def forward(Q, K, V, iters: int, seed: int, window: int, scale: float | None = None, *, kappa: int = 1,
+            sep: int = 1, causal: bool = False):
+    """The whole path: kappa argmax maps, then the sparse attention output over their windows."""
+    J = patchmatch_kappa(Q, K, kappa, iters, seed, sep=sep, causal=causal)
+    return sparse_attend(Q, K, V, J, window, scale, causal=causal), J

@@ -67,21 +67,28 @@ size_t scram_patchmatch_workspace_bytes(int S, int Hq, int Wq)
 
 int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int Wq, int Hk, int Wk,
                      int d, int iters, uint64_t seed, const int32_t* init, const float* init_score,
-                     int t0, uint32_t flags, int32_t* argmax_out, float* score_out, void* workspace,
-                     size_t workspace_bytes, hipEvent_t* events, hipStream_t stream)
+                     int t0, uint32_t flags, const int32_t* prev, int n_prev, int sep, int32_t* argmax_out,
+                     float* score_out, void* workspace, size_t workspace_bytes, hipEvent_t* events,
+                     hipStream_t stream)
 {
     // ---- validation (no HIP call above this line) ----
     if (!Q || !K || !argmax_out) return SCRAM_ERR_NULL;
+    if (n_prev > 0 && !prev) return SCRAM_ERR_NULL;
     if (!workspace) return SCRAM_ERR_WORKSPACE;
     int rc = check_grid(S, Hq, Wq, Hk, Wk);
     if (rc) return rc;
     if (iters < 0 || t0 < 1 || int64_t(t0) + iters > int64_t(0xFFFFFFFFu)) return SCRAM_ERR_SHAPE;
+    if (n_prev < 0 || n_prev > SCRAM_MAX_PREV || sep < 1) return SCRAM_ERR_SHAPE;
     if ((rc = check_type(dtype, d))) return rc;
-    if (flags & ~uint32_t(SCRAM_PM_NO_PROPAGATION | SCRAM_PM_NO_RANDOM_SEARCH)) return SCRAM_ERR_UNSUPPORTED;
+    if (flags & ~uint32_t(SCRAM_PM_NO_PROPAGATION | SCRAM_PM_NO_RANDOM_SEARCH | SCRAM_CAUSAL))
+        return SCRAM_ERR_UNSUPPORTED;
+    const bool causal = (flags & SCRAM_CAUSAL) != 0;
+    if (causal && (Hq != Hk || Wq != Wk)) return SCRAM_ERR_SHAPE;
     if (!init) init_score = nullptr;
+    if (n_prev == 0) prev = nullptr;
     if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(argmax_out, 4) || !aligned(workspace, 256) ||
         (score_out && !aligned(score_out, 4)) || (init && !aligned(init, 4)) ||
-        (init_score && !aligned(init_score, 4)))
+        (init_score && !aligned(init_score, 4)) || (prev && !aligned(prev, 4)))
         return SCRAM_ERR_ALIGN;
     const size_t n = size_t(S) * Hq * Wq;
     const size_t need = scram_patchmatch_workspace_bytes(S, Hq, Wq);
@@ -93,8 +100,9 @@ int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int
     const Range rS = score_out ? range(score_out, 4 * n) : Range{0, 0};
     const Range rI = init ? range(init, 4 * n) : Range{0, 0};
     const Range rIS = init_score ? range(init_score, 4 * n) : Range{0, 0};
+    const Range rP = prev ? range(prev, 4 * n * size_t(n_prev)) : Range{0, 0};
     for (const Range& out : {rJ, rS, rW}) {
-        for (const Range& other : {rQ, rK, rI, rIS}) {
+        for (const Range& other : {rQ, rK, rI, rIS, rP}) {
             if (overlap(out, other)) return SCRAM_ERR_ALIAS;
         }
     }
@@ -110,6 +118,8 @@ int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int
     float* s_ws1 = reinterpret_cast<float*>(ws + 2 * round256(4 * n));
     float* sbuf[2] = {score_out ? score_out : s_ws0, s_ws1};
     const scram::Grid grid{S, Hq, Wq, Hk, Wk, d};
+    const scram::RunSpec run{prev, n_prev, sep, causal};
+    flags &= ~uint32_t(SCRAM_CAUSAL);
 
     const int p0 = iters % 2;
     const int32_t* Jcur;
@@ -125,8 +135,8 @@ int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int
                 if (e == hipSuccess) e = hipEventRecord(ev[1], stream);
             }
         } else {
-            e = scram::launch_pm_init(dtype, Q, K, grid, seed, init, nullptr, sbuf[p0], stream, ev ? ev[0] : nullptr,
-                                      ev ? ev[1] : nullptr);
+            e = scram::launch_pm_init(dtype, Q, K, grid, seed, run, init, nullptr, sbuf[p0], stream,
+                                      ev ? ev[0] : nullptr, ev ? ev[1] : nullptr);
             scur = sbuf[p0];
         }
         if (e == hipSuccess && iters == 0) {
@@ -135,14 +145,14 @@ int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int
                 e = hipMemcpyAsync(score_out, init_score, 4 * n, hipMemcpyDeviceToDevice, stream);
         }
     } else {
-        e = scram::launch_pm_init(dtype, Q, K, grid, seed, nullptr, Jbuf[p0], sbuf[p0], stream, ev ? ev[0] : nullptr,
-                                  ev ? ev[1] : nullptr);
+        e = scram::launch_pm_init(dtype, Q, K, grid, seed, run, nullptr, Jbuf[p0], sbuf[p0], stream,
+                                  ev ? ev[0] : nullptr, ev ? ev[1] : nullptr);
         Jcur = Jbuf[p0];
         scur = sbuf[p0];
     }
     for (int k = 1; k <= iters && e == hipSuccess; ++k) {
         const int pk = (iters - k) % 2;
-        e = scram::launch_pm_iter(dtype, Q, K, grid, seed, uint32_t(t0 + k - 1), flags, Jcur, scur, Jbuf[pk],
+        e = scram::launch_pm_iter(dtype, Q, K, grid, seed, run, uint32_t(t0 + k - 1), flags, Jcur, scur, Jbuf[pk],
                                   sbuf[pk], stream, ev ? ev[2 * k] : nullptr, ev ? ev[2 * k + 1] : nullptr);
         Jcur = Jbuf[pk];
         scur = sbuf[pk];
@@ -150,27 +160,31 @@ int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int
     return e == hipSuccess ? SCRAM_OK : SCRAM_ERR_HIP;
 }
 
-int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype,
-                        const int32_t* argmax, int S, int Hq, int Wq, int Hk, int Wk, int d, int dv,
-                        int window, float scale, void* out, hipEvent_t* events, hipStream_t stream)
+int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype, const int32_t* argmax, int kappa,
+                        int S, int Hq, int Wq, int Hk, int Wk, int d, int dv, int window, float scale,
+                        uint32_t flags, void* out, hipEvent_t* events, hipStream_t stream)
 {
     if (!Q || !K || !V || !argmax || !out) return SCRAM_ERR_NULL;
     int rc = check_grid(S, Hq, Wq, Hk, Wk);
     if (rc) return rc;
     if (window < 1 || window % 2 == 0 || window > 32767) return SCRAM_ERR_SHAPE;
+    if (kappa < 1 || kappa > SCRAM_MAX_KAPPA) return SCRAM_ERR_SHAPE;
     if (!isfinite(scale)) return SCRAM_ERR_SHAPE;
     if ((rc = check_type(dtype, d))) return rc;
     if (dv != d) return SCRAM_ERR_UNSUPPORTED;
+    if (flags & ~uint32_t(SCRAM_CAUSAL)) return SCRAM_ERR_UNSUPPORTED;
+    const bool causal = (flags & SCRAM_CAUSAL) != 0;
+    if (causal && (Hq != Hk || Wq != Wk)) return SCRAM_ERR_SHAPE;
     if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(out, 16) || !aligned(argmax, 4))
         return SCRAM_ERR_ALIGN;
     const size_t n = size_t(S) * Hq * Wq, eb = elem_bytes(dtype);
     const Range rO = range(out, n * dv * eb);
     for (const Range& other : {range(Q, n * d * eb), range(K, size_t(S) * Hk * Wk * d * eb),
-                               range(V, size_t(S) * Hk * Wk * dv * eb), range(argmax, 4 * n)}) {
+                               range(V, size_t(S) * Hk * Wk * dv * eb), range(argmax, 4 * n * size_t(kappa))}) {
         if (overlap(rO, other)) return SCRAM_ERR_ALIAS;
     }
     const scram::Grid grid{S, Hq, Wq, Hk, Wk, d};
-    const hipError_t e = scram::launch_attend(dtype, Q, K, V, argmax, grid, window, scale, out, stream,
+    const hipError_t e = scram::launch_attend(dtype, Q, K, V, argmax, kappa, grid, window, scale, causal, out, stream,
                                               events ? events[0] : nullptr, events ? events[1] : nullptr);
     return e == hipSuccess ? SCRAM_OK : SCRAM_ERR_HIP;
 }

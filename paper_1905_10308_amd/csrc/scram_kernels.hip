@@ -249,6 +249,10 @@ struct PmParams {
     uint32_t t;           // sweep index (Philox counter word 1)
     int R;                // max(Hk, Wk)
     int rs_steps;         // floor(log2 R) + 1
+    const int32_t* prev;  // [n_prev, n] maps of the previous runs (validity variant)
+    int n_prev;           // also this run's index: Philox counter word 3
+    int sep;              // minimum Chebyshev distance to every previous match
+    int causal;           // keys after the query (raster order) are not valid
 };
 
 struct AttParams {
@@ -263,6 +267,34 @@ struct AttParams {
     Div div_plane, div_wk;
     int b;                // window half-width
     float scale_log2e;    // scale * log2(e): scores live in the base-2 domain
+    int kappa;            // maps in J ([kappa, n]): the union of their windows
+    int causal;           // drop keys after the query (raster order)
+};
+
+constexpr int kMaxPrev = 7;   // previous runs a PatchMatch run may be constrained by
+constexpr int kMaxKappa = 8;  // maps whose windows attend may unite
+
+// is_index_valid for one query: not after the query when causal, and at
+// Chebyshev distance >= sep from each previous run's match.
+struct Validity {
+    int n, sep;
+    bool causal;
+    uint32_t local;  // the query's raster index in its slice
+    uint32_t pu[kMaxPrev], pv[kMaxPrev];
+
+    __device__ bool ok(uint32_t r, uint32_t c, int32_t idx) const
+    {
+        bool v = !(causal && static_cast<uint32_t>(idx) > local);
+#pragma unroll
+        for (int i = 0; i < kMaxPrev; ++i) {
+            if (i < n) {
+                const int du = abs(static_cast<int>(r) - static_cast<int>(pu[i]));
+                const int dv = abs(static_cast<int>(c) - static_cast<int>(pv[i]));
+                v = v && max(du, dv) >= sep;
+            }
+        }
+        return v;
+    }
 };
 
 // ---------------------------------------------------------------------------
@@ -282,10 +314,14 @@ __global__ __launch_bounds__(kBlock) void pm_init_kernel(PmParams p)
     if (p.init) {
         idx = clamp_index(p.init[g], p.nkeys);
     } else {
-        const uint4 w = philox4x32_10(g, 0u, 0u, 0u, p.key0, p.key1);
-        const uint32_t u = __umulhi(w.x, static_cast<uint32_t>(p.Hk));
-        const uint32_t v = __umulhi(w.y, static_cast<uint32_t>(p.Wk));
-        idx = static_cast<int32_t>(u * p.Wk + v);
+        const uint4 w = philox4x32_10(g, 0u, 0u, static_cast<uint32_t>(p.n_prev), p.key0, p.key1);
+        if (p.causal) {  // uniform over the keys up to the query's raster index
+            idx = static_cast<int32_t>(__umulhi(w.x, rem + 1u));
+        } else {
+            const uint32_t u = __umulhi(w.x, static_cast<uint32_t>(p.Hk));
+            const uint32_t v = __umulhi(w.y, static_cast<uint32_t>(p.Wk));
+            idx = static_cast<int32_t>(u * p.Wk + v);
+        }
     }
     const T* Ks = static_cast<const T*>(p.K) + static_cast<size_t>(s) * p.nkeys * D;
     uint4 q[RW::kCh], k[RW::kCh];
@@ -315,7 +351,7 @@ __global__ __launch_bounds__(kBlock) void pm_init_kernel(PmParams p)
 // Because "better" is a strict total order, visiting the candidates of
 // stage 1 in any order gives the same result as the order of Algorithm 1.
 // ---------------------------------------------------------------------------
-template <typename T, int D, int G, int QPG, int kNb, bool PROP, bool RS>
+template <typename T, int D, int G, int QPG, int kNb, bool PROP, bool RS, bool VALID>
 __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
 {
     using RW = Row<T, D, G>;
@@ -354,6 +390,28 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
         cur0[j] = cur[j];
         best[j] = p.sp[g[j]];
     }
+    // validity variant: the previous runs' matches of each query; an invalid
+    // incumbent counts as minus infinity
+    Validity val[QPG];
+    if constexpr (VALID) {
+#pragma unroll
+        for (int j = 0; j < QPG; ++j) {
+            val[j].n = p.n_prev;
+            val[j].sep = p.sep;
+            val[j].causal = p.causal != 0;
+            val[j].local = x[j] * p.Wq + y[j];
+#pragma unroll
+            for (int i = 0; i < kMaxPrev; ++i) {
+                val[j].pu[i] = val[j].pv[i] = 0u;
+                if (i < p.n_prev)
+                    divmod(static_cast<uint32_t>(clamp_index(p.prev[static_cast<size_t>(i) * p.n + g[j]], p.nkeys)),
+                           p.div_wk, val[j].pu[i], val[j].pv[i]);
+            }
+            uint32_t u0, v0;
+            divmod(static_cast<uint32_t>(cur[j]), p.div_wk, u0, v0);
+            if (!val[j].ok(u0, v0, cur[j])) best[j] = -INFINITY;
+        }
+    }
 
     // Philox blocks of this sweep: block m serves random-search steps 2m and
     // 2m+1; lane l draws block l (the first round; later rounds below).
@@ -362,7 +420,9 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
 #pragma unroll
     for (int j = 0; j < QPG; ++j) {
         w0[j] = make_uint4(0u, 0u, 0u, 0u);
-        if (lane < nblk) w0[j] = philox4x32_10(g[j], p.t, static_cast<uint32_t>(lane), 0u, p.key0, p.key1);
+        if (lane < nblk)
+            w0[j] = philox4x32_10(g[j], p.t, static_cast<uint32_t>(lane), static_cast<uint32_t>(p.n_prev), p.key0,
+                                  p.key1);
     }
 
     // ---- stage 1 ----
@@ -389,13 +449,17 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
                     uint32_t nu, nv;
                     divmod(nb, p.div_wk, nu, nv);
                     const int r = static_cast<int>(nu) - ox, cc = static_cast<int>(nv) - oy;
-                    if (r >= 0 && r < p.Hk && cc >= 0 && cc < p.Wk) c = r * p.Wk + cc;
+                    if (r >= 0 && r < p.Hk && cc >= 0 && cc < p.Wk) {
+                        c = r * p.Wk + cc;
+                        if (VALID && !val[j].ok(r, cc, c)) c = -1;
+                    }
                 }
             } else if (RS && i == 16) {
                 // random-search step 0: uniform over the whole key grid
                 const uint32_t r = __umulhi(w0[j].x, static_cast<uint32_t>(p.Hk));
                 const uint32_t cc = __umulhi(w0[j].y, static_cast<uint32_t>(p.Wk));
                 c = static_cast<int32_t>(r * p.Wk + cc);
+                if (VALID && !val[j].ok(r, cc, c)) c = -1;
             }
             const bool keep = c >= 0 && c != cur0[j];
             const uint64_t bal = __ballot(keep);
@@ -470,7 +534,8 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
                 for (int j = 0; j < QPG; ++j) {
                     w[j] = make_uint4(0u, 0u, 0u, 0u);
                     if (m + lane < nblk)
-                        w[j] = philox4x32_10(g[j], p.t, static_cast<uint32_t>(m + lane), 0u, p.key0, p.key1);
+                        w[j] = philox4x32_10(g[j], p.t, static_cast<uint32_t>(m + lane),
+                                             static_cast<uint32_t>(p.n_prev), p.key0, p.key1);
                 }
             }
             const int src = gbase + m % G;
@@ -494,7 +559,7 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
 #pragma unroll
             for (int j = 0; j < QPG; ++j) {
                 const float sc = row_score<T, D, G>(q[j], kr[j]);
-                const bool take = better(sc, idx[j], best[j], cur[j]);
+                const bool take = (!VALID || val[j].ok(rr[j], rc[j], idx[j])) & better(sc, idx[j], best[j], cur[j]);
                 best[j] = take ? sc : best[j];
                 cur[j] = take ? idx[j] : cur[j];
                 cu[j] = take ? rr[j] : cu[j];
@@ -558,12 +623,51 @@ __device__ __forceinline__ void store_row(void* out, uint32_t g, int lane, const
     }
 }
 
+// Several windows and/or the causal mask: the centres of all kappa windows
+// and the query's raster index.  skip(e, r, c): key (r, c) of window e is
+// left out because an earlier window already holds it or it comes after the
+// query.
+struct WindowSet {
+    int kappa, b;
+    bool causal;
+    uint32_t local, Wk;
+    int cu[kMaxKappa], cv[kMaxKappa];
+
+    __device__ bool skip(int e, int r, int c) const
+    {
+        bool s = causal && static_cast<uint32_t>(r) * Wk + static_cast<uint32_t>(c) > local;
+#pragma unroll
+        for (int f = 0; f < kMaxKappa; ++f)
+            if (f < e) s = s || (abs(r - cu[f]) <= b && abs(c - cv[f]) <= b);
+        return s;
+    }
+};
+
+__device__ __forceinline__ WindowSet make_window_set(const AttParams& p, uint32_t g, uint32_t rem)
+{
+    WindowSet ws;
+    ws.kappa = p.kappa;
+    ws.b = p.b;
+    ws.causal = p.causal != 0;
+    ws.local = rem;
+    ws.Wk = static_cast<uint32_t>(p.Wk);
+#pragma unroll
+    for (int e = 0; e < kMaxKappa; ++e) {
+        uint32_t u = 0, v = 0;
+        if (e < p.kappa)
+            divmod(static_cast<uint32_t>(clamp_index(p.J[static_cast<size_t>(e) * p.n + g], p.nkeys)), p.div_wk, u, v);
+        ws.cu[e] = static_cast<int>(u);
+        ws.cv[e] = static_cast<int>(v);
+    }
+    return ws;
+}
+
 // Fixed window side W (odd), one window row per step: the W key rows and W
 // value rows of a window row are gathered together (2W loads in flight),
 // then the W scores (base-2 domain), one online-softmax rescale, and the
 // value accumulation.  Keys outside the grid read a clamped (valid) row and
 // get weight 0; window rows entirely outside the grid are skipped.
-template <typename T, int D, int G, int W>
+template <typename T, int D, int G, int W, bool MULTI>
 __global__ __launch_bounds__(kBlock) void attend_window_kernel(AttParams p)
 {
     using RW = Row<T, D, G>;
@@ -582,60 +686,78 @@ __global__ __launch_bounds__(kBlock) void attend_window_kernel(AttParams p)
     const T* Vs = static_cast<const T*>(p.V) + slice;
     uint4 q[CH];
     load_row<T, D, G>(static_cast<const T*>(p.Q), g, lane, q);
-    uint32_t u, v;
-    divmod(static_cast<uint32_t>(clamp_index(p.J[g], p.nkeys)), p.div_wk, u, v);
-
-    // column of each window column, clamped, and whether it is inside
-    int cols[W];
-    bool col_ok[W];
-#pragma unroll
-    for (int c = 0; c < W; ++c) {
-        const int col = static_cast<int>(v) + c - B;
-        col_ok[c] = col >= 0 && col < p.Wk;
-        cols[c] = min(max(col, 0), p.Wk - 1);
-    }
+    WindowSet wset;
+    if constexpr (MULTI) wset = make_window_set(p, g, rem);
+    const int nwin = MULTI ? p.kappa : 1;
 
     float m = -INFINITY, l = 0.f;
     float acc[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[e] = 0.f;
 
-    for (int a = 0; a < W; ++a) {
-        const int r = static_cast<int>(u) + a - B;
-        if (r < 0 || r >= p.Hk) continue;
-        const uint32_t row0 = static_cast<uint32_t>(r * p.Wk);
-        uint4 kr[W][CH], vr[W][CH];
+    for (int e = 0; e < nwin; ++e) {
+        uint32_t u, v;
+        if constexpr (MULTI) {
+            u = static_cast<uint32_t>(wset.cu[0]);
+            v = static_cast<uint32_t>(wset.cv[0]);
+#pragma unroll
+            for (int f = 1; f < kMaxKappa; ++f)
+                if (f == e) {
+                    u = static_cast<uint32_t>(wset.cu[f]);
+                    v = static_cast<uint32_t>(wset.cv[f]);
+                }
+        } else {
+            divmod(static_cast<uint32_t>(clamp_index(p.J[g], p.nkeys)), p.div_wk, u, v);
+        }
+        // column of each window column, clamped, and whether it is inside
+        int cols[W];
+        bool col_ok[W];
 #pragma unroll
         for (int c = 0; c < W; ++c) {
-            load_row<T, D, G>(Ks, row0 + cols[c], lane, kr[c]);
-            load_row<T, D, G>(Vs, row0 + cols[c], lane, vr[c]);
+            const int col = static_cast<int>(v) + c - B;
+            col_ok[c] = col >= 0 && col < p.Wk;
+            cols[c] = min(max(col, 0), p.Wk - 1);
         }
-        float sc[W];
-        float mb = m;
+        for (int a = 0; a < W; ++a) {
+            const int r = static_cast<int>(u) + a - B;
+            if (r < 0 || r >= p.Hk) continue;
+            const uint32_t row0 = static_cast<uint32_t>(r * p.Wk);
+            uint4 kr[W][CH], vr[W][CH];
 #pragma unroll
-        for (int c = 0; c < W; ++c) {
-            sc[c] = col_ok[c] ? row_score<T, D, G>(q, kr[c]) * p.scale_log2e : -INFINITY;
-            mb = fmaxf(mb, sc[c]);
+            for (int c = 0; c < W; ++c) {
+                load_row<T, D, G>(Ks, row0 + cols[c], lane, kr[c]);
+                load_row<T, D, G>(Vs, row0 + cols[c], lane, vr[c]);
+            }
+            float sc[W];
+            float mb = m;
+#pragma unroll
+            for (int c = 0; c < W; ++c) {
+                bool use = col_ok[c];
+                if constexpr (MULTI) use = use && !wset.skip(e, r, cols[c]);
+                sc[c] = use ? row_score<T, D, G>(q, kr[c]) * p.scale_log2e : -INFINITY;
+                mb = fmaxf(mb, sc[c]);
+            }
+            if (mb == -INFINITY) continue;  // nothing of this row is in the set
+            const float alpha = __builtin_amdgcn_exp2f(m - mb);  // 0 on the first row
+            l *= alpha;
+#pragma unroll
+            for (int i = 0; i < E; ++i) acc[i] *= alpha;
+#pragma unroll
+            for (int c = 0; c < W; ++c) {
+                const float pj = __builtin_amdgcn_exp2f(sc[c] - mb);  // exp2(-inf) = 0
+                l += pj;
+                accumulate_row<T, CH>(acc, pj, vr[c]);
+            }
+            m = mb;
         }
-        const float alpha = __builtin_amdgcn_exp2f(m - mb);  // 0 on the first row
-        l *= alpha;
-#pragma unroll
-        for (int e = 0; e < E; ++e) acc[e] *= alpha;
-#pragma unroll
-        for (int c = 0; c < W; ++c) {
-            const float pj = __builtin_amdgcn_exp2f(sc[c] - mb);  // exp2(-inf) = 0
-            l += pj;
-            accumulate_row<T, CH>(acc, pj, vr[c]);
-        }
-        m = mb;
     }
-    store_row<T, D, G>(p.out, g, lane, acc, 1.f / l);
+    store_row<T, D, G>(p.out, g, lane, acc, l > 0.f ? 1.f / l : 0.f);  // an empty set gives a zero row
 }
 
 // Any window side: the clipped window is visited in row order, kNb keys at a
 // time with their key and value loads in flight together; an online softmax
 // keeps (running max m, running sum l, accumulator) in the base-2 domain.
-template <typename T, int D, int G>
+template <typename T, int D, int G, bool MULTI>
 __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
 {
     using RW = Row<T, D, G>;
@@ -654,55 +776,74 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
     const T* Vs = static_cast<const T*>(p.V) + slice;
     uint4 q[CH];
     load_row<T, D, G>(static_cast<const T*>(p.Q), g, lane, q);
-    uint32_t u, v;
-    divmod(static_cast<uint32_t>(clamp_index(p.J[g], p.nkeys)), p.div_wk, u, v);
-    const int r0 = max(static_cast<int>(u) - p.b, 0), r1 = min(static_cast<int>(u) + p.b, p.Hk - 1);
-    const int c0 = max(static_cast<int>(v) - p.b, 0), c1 = min(static_cast<int>(v) + p.b, p.Wk - 1);
-    const int nwin = (r1 - r0 + 1) * (c1 - c0 + 1);
-    const uint32_t centre = u * p.Wk + v;
+    WindowSet wset;
+    if constexpr (MULTI) wset = make_window_set(p, g, rem);
+    const int nsets = MULTI ? p.kappa : 1;
 
     float m = -INFINITY, l = 0.f;
     float acc[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[e] = 0.f;
 
-    // (r, c) walks the clipped window in row order; slots past its end read
-    // the centre row and get weight 0
-    int r = r0, c = c0;
-    for (int k0 = 0; k0 < nwin; k0 += kNb) {
-        uint4 kr[kNb][CH], vr[kNb][CH];
-        bool ok[kNb];
+    for (int e = 0; e < nsets; ++e) {
+        uint32_t u, v;
+        if constexpr (MULTI) {
+            u = static_cast<uint32_t>(wset.cu[0]);
+            v = static_cast<uint32_t>(wset.cv[0]);
 #pragma unroll
-        for (int j = 0; j < kNb; ++j) {
-            ok[j] = k0 + j < nwin;
-            const uint32_t row = ok[j] ? static_cast<uint32_t>(r * p.Wk + c) : centre;
-            load_row<T, D, G>(Ks, row, lane, kr[j]);
-            load_row<T, D, G>(Vs, row, lane, vr[j]);
-            if (ok[j] && ++c > c1) {
-                c = c0;
-                ++r;
+            for (int f = 1; f < kMaxKappa; ++f)
+                if (f == e) {
+                    u = static_cast<uint32_t>(wset.cu[f]);
+                    v = static_cast<uint32_t>(wset.cv[f]);
+                }
+        } else {
+            divmod(static_cast<uint32_t>(clamp_index(p.J[g], p.nkeys)), p.div_wk, u, v);
+        }
+        const int r0 = max(static_cast<int>(u) - p.b, 0), r1 = min(static_cast<int>(u) + p.b, p.Hk - 1);
+        const int c0 = max(static_cast<int>(v) - p.b, 0), c1 = min(static_cast<int>(v) + p.b, p.Wk - 1);
+        const int nwin = (r1 - r0 + 1) * (c1 - c0 + 1);
+        const uint32_t centre = u * p.Wk + v;
+
+        // (r, c) walks the clipped window in row order; slots past its end read
+        // the centre row and get weight 0
+        int r = r0, c = c0;
+        for (int k0 = 0; k0 < nwin; k0 += kNb) {
+            uint4 kr[kNb][CH], vr[kNb][CH];
+            bool ok[kNb];
+#pragma unroll
+            for (int j = 0; j < kNb; ++j) {
+                ok[j] = k0 + j < nwin;
+                if constexpr (MULTI) ok[j] = ok[j] && !wset.skip(e, r, c);
+                const uint32_t row = k0 + j < nwin ? static_cast<uint32_t>(r * p.Wk + c) : centre;
+                load_row<T, D, G>(Ks, row, lane, kr[j]);
+                load_row<T, D, G>(Vs, row, lane, vr[j]);
+                if (k0 + j < nwin && ++c > c1) {
+                    c = c0;
+                    ++r;
+                }
             }
-        }
-        float sc[kNb];
-        float mb = m;
+            float sc[kNb];
+            float mb = m;
 #pragma unroll
-        for (int j = 0; j < kNb; ++j) {
-            sc[j] = ok[j] ? row_score<T, D, G>(q, kr[j]) * p.scale_log2e : -INFINITY;
-            mb = fmaxf(mb, sc[j]);
-        }
-        const float alpha = __builtin_amdgcn_exp2f(m - mb);
-        l *= alpha;
+            for (int j = 0; j < kNb; ++j) {
+                sc[j] = ok[j] ? row_score<T, D, G>(q, kr[j]) * p.scale_log2e : -INFINITY;
+                mb = fmaxf(mb, sc[j]);
+            }
+            if (mb == -INFINITY) continue;
+            const float alpha = __builtin_amdgcn_exp2f(m - mb);
+            l *= alpha;
 #pragma unroll
-        for (int e = 0; e < E; ++e) acc[e] *= alpha;
+            for (int i = 0; i < E; ++i) acc[i] *= alpha;
 #pragma unroll
-        for (int j = 0; j < kNb; ++j) {
-            const float pj = __builtin_amdgcn_exp2f(sc[j] - mb);
-            l += pj;
-            accumulate_row<T, CH>(acc, pj, vr[j]);
+            for (int j = 0; j < kNb; ++j) {
+                const float pj = __builtin_amdgcn_exp2f(sc[j] - mb);
+                l += pj;
+                accumulate_row<T, CH>(acc, pj, vr[j]);
+            }
+            m = mb;
         }
-        m = mb;
     }
-    store_row<T, D, G>(p.out, g, lane, acc, 1.f / l);
+    store_row<T, D, G>(p.out, g, lane, acc, l > 0.f ? 1.f / l : 0.f);  // an empty set gives a zero row
 }
 
 // ---------------------------------------------------------------------------
@@ -759,20 +900,42 @@ hipError_t run_init(const PmParams& p, hipStream_t st, hipEvent_t e0, hipEvent_t
 #define SCRAM_PM_BATCH 4
 #endif
 
-template <typename T, int D>
-hipError_t run_iter(const PmParams& p, uint32_t flags, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
+template <typename T, int D, bool VALID>
+hipError_t run_iter_v(const PmParams& p, uint32_t flags, uint32_t blocks, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
 {
     constexpr int G = Lanes<T, D>::kPm;
     constexpr int QPG = SCRAM_PM_QPG;
     constexpr int NB = SCRAM_PM_BATCH;
-    constexpr int kQpb = Row<T, D, G>::kQpb * QPG;
-    const uint32_t blocks = (p.n + kQpb - 1) / kQpb;
     const bool prop = !(flags & SCRAM_PM_NO_PROPAGATION);
     const bool rs = !(flags & SCRAM_PM_NO_RANDOM_SEARCH);
-    if (prop && rs) return launch(pm_iter_kernel<T, D, G, QPG, NB, true, true>, blocks, st, e0, e1, p);
-    if (prop) return launch(pm_iter_kernel<T, D, G, QPG, NB, true, false>, blocks, st, e0, e1, p);
-    if (rs) return launch(pm_iter_kernel<T, D, G, QPG, NB, false, true>, blocks, st, e0, e1, p);
-    return launch(pm_iter_kernel<T, D, G, QPG, NB, false, false>, blocks, st, e0, e1, p);
+    if (prop && rs) return launch(pm_iter_kernel<T, D, G, QPG, NB, true, true, VALID>, blocks, st, e0, e1, p);
+    if (prop) return launch(pm_iter_kernel<T, D, G, QPG, NB, true, false, VALID>, blocks, st, e0, e1, p);
+    if (rs) return launch(pm_iter_kernel<T, D, G, QPG, NB, false, true, VALID>, blocks, st, e0, e1, p);
+    return launch(pm_iter_kernel<T, D, G, QPG, NB, false, false, VALID>, blocks, st, e0, e1, p);
+}
+
+template <typename T, int D>
+hipError_t run_iter(const PmParams& p, uint32_t flags, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
+{
+    constexpr int G = Lanes<T, D>::kPm;
+    constexpr int kQpb = Row<T, D, G>::kQpb * SCRAM_PM_QPG;
+    const uint32_t blocks = (p.n + kQpb - 1) / kQpb;
+    if (p.n_prev > 0 || p.causal) return run_iter_v<T, D, true>(p, flags, blocks, st, e0, e1);
+    return run_iter_v<T, D, false>(p, flags, blocks, st, e0, e1);
+}
+
+template <typename T, int D, bool MULTI>
+hipError_t run_attend_m(const AttParams& p, int window, uint32_t blocks, hipStream_t st, hipEvent_t e0,
+                        hipEvent_t e1)
+{
+    constexpr int G = Lanes<T, D>::kAttend;
+    switch (window) {
+        case 1: return launch(attend_window_kernel<T, D, G, 1, MULTI>, blocks, st, e0, e1, p);
+        case 3: return launch(attend_window_kernel<T, D, G, 3, MULTI>, blocks, st, e0, e1, p);
+        case 5: return launch(attend_window_kernel<T, D, G, 5, MULTI>, blocks, st, e0, e1, p);
+        case 7: return launch(attend_window_kernel<T, D, G, 7, MULTI>, blocks, st, e0, e1, p);
+        default: return launch(attend_kernel<T, D, G, MULTI>, blocks, st, e0, e1, p);
+    }
 }
 
 template <typename T, int D>
@@ -780,13 +943,8 @@ hipError_t run_attend(const AttParams& p, int window, hipStream_t st, hipEvent_t
 {
     constexpr int G = Lanes<T, D>::kAttend;
     const uint32_t blocks = (p.n + Row<T, D, G>::kQpb - 1) / Row<T, D, G>::kQpb;
-    switch (window) {
-        case 1: return launch(attend_window_kernel<T, D, G, 1>, blocks, st, e0, e1, p);
-        case 3: return launch(attend_window_kernel<T, D, G, 3>, blocks, st, e0, e1, p);
-        case 5: return launch(attend_window_kernel<T, D, G, 5>, blocks, st, e0, e1, p);
-        case 7: return launch(attend_window_kernel<T, D, G, 7>, blocks, st, e0, e1, p);
-        default: return launch(attend_kernel<T, D, G>, blocks, st, e0, e1, p);
-    }
+    if (p.kappa > 1 || p.causal) return run_attend_m<T, D, true>(p, window, blocks, st, e0, e1);
+    return run_attend_m<T, D, false>(p, window, blocks, st, e0, e1);
 }
 
 // (dtype, d) -> instantiation
@@ -814,21 +972,23 @@ hipError_t dispatch(int dtype, int d, F&& f)
 }  // namespace
 
 hipError_t launch_pm_init(int dtype, const void* Q, const void* K, const Grid& g, uint64_t seed,
-                          const int32_t* init, int32_t* J, float* s, hipStream_t stream, hipEvent_t start,
-                          hipEvent_t stop)
+                          const RunSpec& run, const int32_t* init, int32_t* J, float* s, hipStream_t stream,
+                          hipEvent_t start, hipEvent_t stop)
 {
     PmParams p = make_pm_params(Q, K, g, seed);
     p.init = init;
     p.Jn = J;
     p.sn = s;
+    p.n_prev = run.n_prev;
+    p.causal = run.causal ? 1 : 0;
     return dispatch(dtype, g.d, [&](auto t, auto d) {
         return run_init<decltype(t), decltype(d)::value>(p, stream, start, stop);
     });
 }
 
 hipError_t launch_pm_iter(int dtype, const void* Q, const void* K, const Grid& g, uint64_t seed,
-                          uint32_t t, uint32_t flags, const int32_t* Jp, const float* sp, int32_t* Jn,
-                          float* sn, hipStream_t stream, hipEvent_t start, hipEvent_t stop)
+                          const RunSpec& run, uint32_t t, uint32_t flags, const int32_t* Jp, const float* sp,
+                          int32_t* Jn, float* sn, hipStream_t stream, hipEvent_t start, hipEvent_t stop)
 {
     PmParams p = make_pm_params(Q, K, g, seed);
     p.t = t;
@@ -836,13 +996,17 @@ hipError_t launch_pm_iter(int dtype, const void* Q, const void* K, const Grid& g
     p.sp = sp;
     p.Jn = Jn;
     p.sn = sn;
+    p.prev = run.prev;
+    p.n_prev = run.n_prev;
+    p.sep = run.sep;
+    p.causal = run.causal ? 1 : 0;
     return dispatch(dtype, g.d, [&](auto ty, auto d) {
         return run_iter<decltype(ty), decltype(d)::value>(p, flags, stream, start, stop);
     });
 }
 
-hipError_t launch_attend(int dtype, const void* Q, const void* K, const void* V, const int32_t* J,
-                         const Grid& g, int window, float scale, void* out, hipStream_t stream,
+hipError_t launch_attend(int dtype, const void* Q, const void* K, const void* V, const int32_t* J, int kappa,
+                         const Grid& g, int window, float scale, bool causal, void* out, hipStream_t stream,
                          hipEvent_t start, hipEvent_t stop)
 {
     AttParams p{};
@@ -859,6 +1023,8 @@ hipError_t launch_attend(int dtype, const void* Q, const void* K, const void* V,
     p.div_wk = make_div(g.Wk);
     p.b = window / 2;
     p.scale_log2e = scale * 1.4426950408889634f;
+    p.kappa = kappa;
+    p.causal = causal ? 1 : 0;
     return dispatch(dtype, g.d, [&](auto ty, auto d) {
         return run_attend<decltype(ty), decltype(d)::value>(p, window, stream, start, stop);
     });

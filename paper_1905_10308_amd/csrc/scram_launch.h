@@ -12,23 +12,32 @@ struct Grid {
     int S, Hq, Wq, Hk, Wk, d;
 };
 
+// Constraints of one PatchMatch run: the maps of the n_prev previous runs
+// (n_prev is also this run's index), their minimum separation, causality.
+struct RunSpec {
+    const int32_t* prev;
+    int n_prev;
+    int sep;
+    bool causal;
+};
+
 // Every launch takes optional start/stop events that the dispatch itself
 // stamps with the kernel's start and end times (null: plain launch).
 
 // Random initial map (init == nullptr) or the scores of a given map.
 // J may be nullptr when init is given (the map is not copied).
 hipError_t launch_pm_init(int dtype, const void* Q, const void* K, const Grid& g, uint64_t seed,
-                          const int32_t* init, int32_t* J, float* s, hipStream_t stream, hipEvent_t start,
-                          hipEvent_t stop);
+                          const RunSpec& run, const int32_t* init, int32_t* J, float* s, hipStream_t stream,
+                          hipEvent_t start, hipEvent_t stop);
 
 // One Jacobi sweep t: (Jp, sp) -> (Jn, sn).
 hipError_t launch_pm_iter(int dtype, const void* Q, const void* K, const Grid& g, uint64_t seed,
-                          uint32_t t, uint32_t flags, const int32_t* Jp, const float* sp, int32_t* Jn,
-                          float* sn, hipStream_t stream, hipEvent_t start, hipEvent_t stop);
+                          const RunSpec& run, uint32_t t, uint32_t flags, const int32_t* Jp, const float* sp,
+                          int32_t* Jn, float* sn, hipStream_t stream, hipEvent_t start, hipEvent_t stop);
 
-// Window softmax + value gather around argmax.
-hipError_t launch_attend(int dtype, const void* Q, const void* K, const void* V, const int32_t* J,
-                         const Grid& g, int window, float scale, void* out, hipStream_t stream,
+// Window softmax + value gather around the kappa maps in J ([kappa, n]).
+hipError_t launch_attend(int dtype, const void* Q, const void* K, const void* V, const int32_t* J, int kappa,
+                         const Grid& g, int window, float scale, bool causal, void* out, hipStream_t stream,
                          hipEvent_t start, hipEvent_t stop);
 
 }  // namespace scram

@@ -1,0 +1,73 @@
+"""Helpers shared by the GPU parity tests (no test functions here).
+
+Tolerances:
+  * argmax maps are integers and must equal the oracle's, except where the
+    oracle records a near tie (two different keys whose fp64 scores differ by
+    at most 1e-5 of sum_e |q_e k_e|) and, after several sweeps, inside the
+    region such a tie can reach by propagation (offsets 1, 2, 4, 8 along an
+    axis per sweep);
+  * fp32 scores: at most 40 roundings on the longest summation path of any
+    lane split built here, each 2^-24 of sum_e |q_e k_e|;
+  * attention rows: 1e-5 (fp32 storage) or 1e-2 (bf16 storage) of the row's
+    largest magnitude.
+"""
+import numpy as np
+import torch
+
+import scram_inputs as si
+from scram_inputs.synth import resized
+
+TOL = {"f32": 1e-5, "bf16": 1e-2}
+SCORE_TOL = 40 * 2.0 ** -24
+
+# small versions of the five workloads: several blocks and a ragged tail
+SMALL = [
+    si.get(0),
+    resized(si.get(1), batch=1, heads=3, Hq=40, Wq=36, Hk=40, Wk=36),
+    resized(si.get(2), batch=1, heads=2, Hq=48, Wq=50, Hk=48, Wk=50, F=12),
+    resized(si.get(3), batch=1, heads=1, Hq=72, Wq=64, Hk=72, Wk=64, F=16),
+    resized(si.get(4), batch=1, heads=2, Hq=30, Wq=26, Hk=45, Wk=39, F=8),
+]
+IDS = [c.name for c in SMALL]
+
+
+def log(*a):
+    print(*a, flush=True)
+
+
+def dilate(mask):
+    """mask + M for M = {0, +-1, +-2, +-4, +-8 along each axis}, per slice."""
+    out = mask.copy()
+    H, W = mask.shape[-2:]
+    for j in (8, 4, 2, 1):
+        if j < H:
+            out[..., j:, :] |= mask[..., :-j, :]
+            out[..., :-j, :] |= mask[..., j:, :]
+        if j < W:
+            out[..., :, j:] |= mask[..., :, :-j]
+            out[..., :, :-j] |= mask[..., :, j:]
+    return out
+
+
+def reach_of_ties(ties, start=None):
+    """Queries a near tie in sweep t (or a query in ``start``) can influence by the last sweep."""
+    A = np.zeros(ties.shape[1:], bool) if start is None else start.copy()
+    for t in range(ties.shape[0]):
+        A = dilate(A) | ties[t]
+    return A
+
+
+def to_dev(arr, dtype):
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    return torch.from_numpy(np.ascontiguousarray(arr, np.float32)).to(tdt).contiguous().cuda()
+
+
+def row_rel_err(got, ref):
+    got = np.asarray(got, np.float64).reshape(-1, ref.shape[-1])
+    ref = np.asarray(ref, np.float64).reshape(-1, ref.shape[-1])
+    return np.abs(got - ref).max(axis=1) / np.maximum(np.abs(ref).max(axis=1), 1e-6)
+
+
+def cheb(a, b, W):
+    """Chebyshev distance between flat key indices on a grid of width W."""
+    return np.maximum(np.abs(a // W - b // W), np.abs(a % W - b % W))

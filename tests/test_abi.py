@@ -16,7 +16,8 @@ OK, ENULL, ESHAPE, EUNSUP, EALIGN, EALIAS, EHIP, EWS = 0, -1, -2, -3, -4, -5, -6
 F32, BF16 = 0, 1
 
 # fake, well-aligned, non-overlapping "device" addresses (never dereferenced)
-A_Q, A_K, A_V, A_J, A_S, A_W, A_I, A_IS, A_O = (0x10000000 * (i + 1) for i in range(9))
+A_Q, A_K, A_V, A_J, A_S, A_W, A_I, A_IS, A_O, A_P = (0x10000000 * (i + 1) for i in range(10))
+CAUSAL, MAX_PREV, MAX_KAPPA = 4, 7, 8
 
 
 @pytest.fixture(scope="module")
@@ -50,7 +51,7 @@ def test_library_exports_every_declared_symbol(L):
 
 
 def test_abi_version(L):
-    assert L.scram_abi_version() == (1 << 16)
+    assert L.scram_abi_version() == (2 << 16)
 
 
 def test_status_strings(L):
@@ -74,19 +75,21 @@ def test_workspace_formula(L):
 
 def pm(L, **kw):
     a = dict(Q=A_Q, K=A_K, dtype=F32, S=2, Hq=8, Wq=8, Hk=8, Wk=8, d=16, iters=2, seed=1, init=None,
-             init_score=None, t0=1, flags=0, out=A_J, score=A_S, ws=A_W, ws_bytes=1 << 20)
+             init_score=None, t0=1, flags=0, prev=None, n_prev=0, sep=1, out=A_J, score=A_S, ws=A_W,
+             ws_bytes=1 << 20)
     a.update(kw)
     return L.scram_patchmatch(a["Q"], a["K"], a["dtype"], a["S"], a["Hq"], a["Wq"], a["Hk"], a["Wk"], a["d"],
-                              a["iters"], a["seed"], a["init"], a["init_score"], a["t0"], a["flags"], a["out"],
-                              a["score"], a["ws"], a["ws_bytes"], None, None)
+                              a["iters"], a["seed"], a["init"], a["init_score"], a["t0"], a["flags"], a["prev"],
+                              a["n_prev"], a["sep"], a["out"], a["score"], a["ws"], a["ws_bytes"], None, None)
 
 
 def at(L, **kw):
-    a = dict(Q=A_Q, K=A_K, V=A_V, dtype=F32, J=A_J, S=2, Hq=8, Wq=8, Hk=8, Wk=8, d=16, dv=16, window=3,
-             scale=0.25, out=A_O)
+    a = dict(Q=A_Q, K=A_K, V=A_V, dtype=F32, J=A_J, kappa=1, S=2, Hq=8, Wq=8, Hk=8, Wk=8, d=16, dv=16, window=3,
+             scale=0.25, flags=0, out=A_O)
     a.update(kw)
-    return L.scram_sparse_attend(a["Q"], a["K"], a["V"], a["dtype"], a["J"], a["S"], a["Hq"], a["Wq"], a["Hk"],
-                                 a["Wk"], a["d"], a["dv"], a["window"], a["scale"], a["out"], None, None)
+    return L.scram_sparse_attend(a["Q"], a["K"], a["V"], a["dtype"], a["J"], a["kappa"], a["S"], a["Hq"], a["Wq"],
+                                 a["Hk"], a["Wk"], a["d"], a["dv"], a["window"], a["scale"], a["flags"], a["out"],
+                                 None, None)
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -95,7 +98,12 @@ def at(L, **kw):
     (dict(t0=0), ESHAPE), (dict(S=1 << 16, Hq=1 << 8, Wq=1 << 7), ESHAPE),
     (dict(Hk=1 << 16, Wk=1 << 15), ESHAPE), (dict(Hq=(1 << 30) + 1, S=1, Wq=1), ESHAPE),
     (dict(t0=-5), ESHAPE),
-    (dict(d=48), EUNSUP), (dict(d=8), EUNSUP), (dict(dtype=7), EUNSUP), (dict(flags=4), EUNSUP),
+    (dict(d=48), EUNSUP), (dict(d=8), EUNSUP), (dict(dtype=7), EUNSUP), (dict(flags=8), EUNSUP),
+    (dict(n_prev=1), ENULL), (dict(n_prev=-1, prev=A_P), ESHAPE), (dict(n_prev=MAX_PREV + 1, prev=A_P), ESHAPE),
+    (dict(sep=0), ESHAPE), (dict(flags=CAUSAL, Hk=4), ESHAPE), (dict(flags=CAUSAL, Wq=7), ESHAPE),
+    (dict(n_prev=1, prev=A_P + 2), EALIGN),
+    (dict(n_prev=1, prev=A_J), EALIAS), (dict(n_prev=2, prev=A_S - 4 * 2 * 64 * 2 + 4), EALIAS),
+    (dict(n_prev=1, prev=A_P, ws=A_P + 256), EALIAS),
     (dict(Q=A_Q + 8), EALIGN), (dict(K=A_K + 4), EALIGN), (dict(out=A_J + 2), EALIGN),
     (dict(ws=A_W + 16), EALIGN), (dict(score=A_S + 1), EALIGN), (dict(init=A_I + 2), EALIGN),
     (dict(ws_bytes=100), EWS),
@@ -114,6 +122,9 @@ def test_patchmatch_rejects(L, kw, code):
     (dict(d=24), EUNSUP), (dict(dv=32), EUNSUP), (dict(dtype=2), EUNSUP),
     (dict(V=A_V + 8), EALIGN), (dict(out=A_O + 4), EALIGN), (dict(J=A_J + 1), EALIGN),
     (dict(out=A_Q), EALIAS), (dict(out=A_V + 64), EALIAS), (dict(out=A_J - 16), EALIAS),
+    (dict(kappa=0), ESHAPE), (dict(kappa=MAX_KAPPA + 1), ESHAPE), (dict(flags=1), EUNSUP), (dict(flags=8), EUNSUP),
+    (dict(flags=CAUSAL, Hk=4), ESHAPE), (dict(flags=CAUSAL, Wk=9), ESHAPE),
+    (dict(kappa=3, J=A_O - 4 * 2 * 64 * 3 + 4), EALIAS),
 ])
 def test_sparse_attend_rejects(L, kw, code):
     assert at(L, **kw) == code

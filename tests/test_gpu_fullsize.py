@@ -21,16 +21,6 @@ SAMPLES = 4096
 TOL = {"f32": 1e-5, "bf16": 1e-2}
 
 
-@pytest.fixture(scope="module")
-def scram():
-    if not torch.cuda.is_available():
-        pytest.skip("no GPU")
-    import paper_1905_10308_amd as scram
-
-    scram.lib()
-    return scram
-
-
 @pytest.mark.parametrize("ci", range(len(si.CONFIGS)), ids=[c.name for c in si.CONFIGS])
 def test_full_size_sampled(scram, ci):
     cfg = si.get(ci)

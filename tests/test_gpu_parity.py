@@ -19,74 +19,13 @@ import pytest
 import oracle
 import oracle.dense as dense
 import scram_inputs as si
-from scram_inputs.synth import resized
 
 torch = pytest.importorskip("torch")
+from gpu_util import IDS, SCORE_TOL, SMALL, TOL, dilate, log, reach_of_ties, row_rel_err, to_dev  # noqa: E402
+
 pytestmark = pytest.mark.gpu
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
-TOL = {"f32": 1e-5, "bf16": 1e-2}
-# fp32 score vs fp64: at most (roundings on the longest summation path) * 2^-24 * sum|q_e k_e|;
-# every lane split built here has at most 40 roundings on that path
-SCORE_TOL = 40 * 2.0 ** -24
-
-
-@pytest.fixture(scope="module")
-def scram():
-    if not torch.cuda.is_available():
-        pytest.skip("no GPU")
-    import paper_1905_10308_amd as scram
-
-    scram.lib()  # raises if the HIP library is missing: no fallback
-    return scram
-
-
-def log(*a):
-    print(*a, flush=True)
-
-
-def dilate(mask):
-    """mask + M for M = {0, +-1, +-2, +-4, +-8 along each axis}, per slice."""
-    out = mask.copy()
-    H, W = mask.shape[-2:]
-    for j in (8, 4, 2, 1):
-        if j < H:
-            out[..., j:, :] |= mask[..., :-j, :]
-            out[..., :-j, :] |= mask[..., j:, :]
-        if j < W:
-            out[..., :, j:] |= mask[..., :, :-j]
-            out[..., :, :-j] |= mask[..., :, j:]
-    return out
-
-
-def reach_of_ties(ties):
-    """Queries a near tie in sweep t can influence by the last sweep."""
-    A = np.zeros(ties.shape[1:], bool)
-    for t in range(ties.shape[0]):
-        A = dilate(A) | ties[t]
-    return A
-
-
-def to_dev(arr, dtype):
-    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
-    return torch.from_numpy(np.ascontiguousarray(arr, np.float32)).to(tdt).contiguous().cuda()
-
-
-def row_rel_err(got, ref):
-    got = np.asarray(got, np.float64).reshape(-1, ref.shape[-1])
-    ref = np.asarray(ref, np.float64).reshape(-1, ref.shape[-1])
-    return np.abs(got - ref).max(axis=1) / np.maximum(np.abs(ref).max(axis=1), 1e-6)
-
-
-# small versions of the five workloads: several blocks and a ragged tail
-SMALL = [
-    si.get(0),
-    resized(si.get(1), batch=1, heads=3, Hq=40, Wq=36, Hk=40, Wk=36),
-    resized(si.get(2), batch=1, heads=2, Hq=48, Wq=50, Hk=48, Wk=50, F=12),
-    resized(si.get(3), batch=1, heads=1, Hq=72, Wq=64, Hk=72, Wk=64, F=16),
-    resized(si.get(4), batch=1, heads=2, Hq=30, Wq=26, Hk=45, Wk=39, F=8),
-]
-IDS = [c.name for c in SMALL]
 
 
 @pytest.fixture(scope="module", params=range(len(SMALL)), ids=IDS)
