@@ -75,6 +75,11 @@ def _load():
                                       P, i64, ctypes.c_uint32, ctypes.c_double, P, i64, i64, P, P, P, P]
     lib.oracle_sparse_attend.argtypes = [P, P, P, P, i64, i64, i64, i64, i64, i64, ctypes.c_int,
                                          ctypes.c_int, ctypes.c_int, ctypes.c_double, ctypes.c_uint32, P, i64, P]
+    lib.oracle_snis_density.argtypes = [P, i64, i64, i64, ctypes.c_int, ctypes.c_double, P]
+    lib.oracle_snis_draws.argtypes = [P, i64, i64, i64, ctypes.c_int, ctypes.c_double, ctypes.c_uint64, i64, i64, P]
+    lib.oracle_snis.argtypes = [P, P, P, P, i64, i64, i64, i64, i64, i64, ctypes.c_int, ctypes.c_int, i64,
+                                ctypes.c_double, ctypes.c_int, ctypes.c_double, ctypes.c_uint64, ctypes.c_uint32, P,
+                                i64, P, P, P]
     lib.oracle_num_threads.restype = ctypes.c_int
     lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
     _lib = lib
@@ -256,3 +261,47 @@ def sparse_attend(Q, K, V, J, window, scale, query_ids=None, flags=0):
     _check(_load().oracle_sparse_attend(_ptr(Q), _ptr(K), _ptr(V), _ptr(J), kappa, S, Hq, Wq, Hk, Wk, d, dv,
                                         window, scale, flags, _ptr(ids), nq, _ptr(out)), "sparse_attend")
     return out
+
+
+def snis_density(modes, Hk, Wk, radius, alpha):
+    """Equation 17's importance distribution r_i over the key grid for one query's modes -> [Hk, Wk]."""
+    modes = _i32(np.atleast_1d(modes))
+    out = np.empty((Hk, Wk), np.float64)
+    _check(_load().oracle_snis_density(_ptr(modes), modes.size, Hk, Wk, radius, float(alpha), _ptr(out)),
+           "snis_density")
+    return out
+
+
+def snis_draws(modes, Hk, Wk, radius, alpha, seed, g, T):
+    """Samples t = 0..T-1 of query g (Equation 12) -> int64 [T] flat key indices."""
+    modes = _i32(np.atleast_1d(modes))
+    out = np.empty(T, np.int64)
+    _check(_load().oracle_snis_draws(_ptr(modes), modes.size, Hk, Wk, radius, float(alpha),
+                                     ctypes.c_uint64(int(seed) & 0xFFFFFFFFFFFFFFFF), g, T, _ptr(out)), "snis_draws")
+    return out
+
+
+def snis(Q, K, V, modes, samples, alpha, radius, scale, seed, flags=0, query_ids=None):
+    """SNIS estimate (Equations 11-17) -> (out [S,Hq,Wq,dv] or [nq,dv], ess, var), float64.
+
+    ``modes`` is one map ``[S, Hq, Wq]`` or kappa maps ``[kappa, S, Hq, Wq]``.
+    """
+    Q, K, V, modes = _f64(Q), _f64(K), _f64(V), _i32(modes)
+    S, Hq, Wq, Hk, Wk, d = _dims(Q, K)
+    modes = modes.reshape(-1, S, Hq, Wq)
+    if V.shape[:3] != K.shape[:3]:
+        raise ValueError("V must share K's grid")
+    dv = V.shape[3]
+    if query_ids is None:
+        ids, nq, lead = None, 0, (S, Hq, Wq)
+    else:
+        ids = np.ascontiguousarray(query_ids, dtype=np.int64)
+        nq, lead = ids.size, (ids.size,)
+    out = np.empty(lead + (dv,), np.float64)
+    var = np.empty(lead + (dv,), np.float64)
+    ess = np.empty(lead, np.float64)
+    _check(_load().oracle_snis(_ptr(Q), _ptr(K), _ptr(V), _ptr(modes), modes.shape[0], S, Hq, Wq, Hk, Wk, d, dv,
+                               int(samples), float(alpha), int(radius), float(scale),
+                               ctypes.c_uint64(int(seed) & 0xFFFFFFFFFFFFFFFF), flags, _ptr(ids), nq, _ptr(out),
+                               _ptr(ess), _ptr(var)), "snis")
+    return out, ess, var

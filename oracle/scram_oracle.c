@@ -56,6 +56,25 @@
  * key is valid for query i only if its raster index is at most i.  The
  * initial match is drawn uniformly from the valid keys, and the attend
  * window drops keys after the query.
+ *
+ * Self-normalised importance sampling (Section 4.2, Monte Carlo estimators,
+ * Equations 11-17): the importance distribution mixes, with weight alpha, a
+ * local density around each of the kappa PatchMatch modes and, with weight
+ * 1 - alpha, the uniform distribution over the n = Hk * Wk keys.  Readings:
+ *   - the local density is a discrete Gaussian written as a centred binomial
+ *     per axis: offset = (number of ones among 2m fair bits) - m, so its
+ *     pmf is C(2m, offset + m) / 4^m and its variance m / 2 (length-scale
+ *     phi = sqrt(m / 2)); a row or column beyond the grid is clamped to the
+ *     edge, which then holds the tail mass of that side;
+ *   - alpha is used as round(alpha * 65536) / 65536;
+ *   - sample t of query g uses the Philox block of counter
+ *     (g, t, 0, 0x534E4953): word 0's upper 16 bits below round(alpha *
+ *     65536) choose a mode (word 1, uniform over the kappa modes; words 2
+ *     and 3 give the 2m row and 2m column bits, m <= 16), otherwise words
+ *     2 and 3 draw a uniform row and column;
+ *   - the variance estimate of Equation 15 uses the self-normalised weights
+ *     w_t / sum_s w_s (with raw weights it would change with any constant
+ *     factor in p^(u), which the estimator itself ignores).
  */
 #include <math.h>
 #include <stdint.h>
@@ -526,6 +545,200 @@ int oracle_sparse_attend(const double* Q, const double* K, const double* V, cons
         }
         for (int e = 0; e < dv; ++e) o[e] = nk > 0 ? o[e] / denom : 0.0; /* empty set: zero row */
         free(keys);
+    }
+    return rc;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Self-normalised importance sampling (Section 4.2, Equations 11-17).      */
+/* ------------------------------------------------------------------------ */
+#define OR_SNIS_TAG 0x534E4953u
+
+/* binomial coefficient C(n, k) for n <= 32, exact (integer arithmetic) */
+static double choose(int n, int k)
+{
+    if (k < 0 || k > n) return 0.0;
+    uint64_t c = 1;
+    for (int i = 1; i <= k; ++i) c = c * (uint64_t)(n - k + i) / (uint64_t)i;
+    return (double)c;
+}
+
+/* pmf of the centred binomial offset (2m fair bits, minus m) */
+static double offset_pmf(int64_t delta, int m)
+{
+    if (delta < -m || delta > m) return 0.0;
+    return choose(2 * m, (int)(delta + m)) / ldexp(1.0, 2 * m);
+}
+
+/* P(offset <= x) */
+static double offset_cdf(int64_t x, int m)
+{
+    double acc = 0.0;
+    for (int64_t delta = -m; delta <= x && delta <= m; ++delta) acc += offset_pmf(delta, m);
+    return acc;
+}
+
+/* probability that the clamped coordinate centre + offset lands on r, 0 <= r < len */
+static double axis_density(int64_t r, int64_t centre, int64_t len, int m)
+{
+    if (len == 1) return 1.0;
+    if (r == 0) return offset_cdf(-centre, m);               /* every offset reaching row 0 or beyond */
+    if (r == len - 1) return offset_cdf(centre - (len - 1), m); /* by symmetry, the far tail */
+    return offset_pmf(r - centre, m);
+}
+
+static int alpha_q16(double alpha) { return (int)floor(alpha * 65536.0 + 0.5); }
+
+static int popcount32(uint32_t x)
+{
+    int c = 0;
+    for (; x; x &= x - 1) ++c;
+    return c;
+}
+
+/* r_i(j) of Equation 17 for one query with modes[kappa] (flat key indices) */
+static double snis_density(const int32_t* modes, int64_t kappa, int64_t Hk, int64_t Wk, int m, double alpha,
+                           int64_t j)
+{
+    const double a = alpha_q16(alpha) / 65536.0;
+    const int64_t r = j / Wk, c = j % Wk;
+    double local = 0.0;
+    for (int64_t e = 0; e < kappa; ++e)
+        local += axis_density(r, modes[e] / Wk, Hk, m) * axis_density(c, modes[e] % Wk, Wk, m);
+    return a / (double)kappa * local + (1.0 - a) / (double)(Hk * Wk);
+}
+
+/* sample t of query g drawn from r_i (Equation 12) */
+static int64_t snis_draw(const int32_t* modes, int64_t kappa, int64_t Hk, int64_t Wk, int m, double alpha,
+                         const uint32_t key[2], int64_t g, int64_t t)
+{
+    const uint32_t ctr[4] = {(uint32_t)g, (uint32_t)t, 0u, OR_SNIS_TAG};
+    uint32_t w[4];
+    philox4x32_10(ctr, key, w);
+    int64_t r, c;
+    if ((int)(w[0] >> 16) < alpha_q16(alpha)) {
+        const int64_t e = pick_in_range(w[1], 0, kappa - 1);
+        const uint32_t mask = m == 16 ? 0xFFFFFFFFu : ((1u << (2 * m)) - 1u);
+        r = modes[e] / Wk + (popcount32(w[2] & mask) - m);
+        c = modes[e] % Wk + (popcount32(w[3] & mask) - m);
+        r = r < 0 ? 0 : (r > Hk - 1 ? Hk - 1 : r);
+        c = c < 0 ? 0 : (c > Wk - 1 ? Wk - 1 : c);
+    } else {
+        r = pick_in_range(w[2], 0, Hk - 1);
+        c = pick_in_range(w[3], 0, Wk - 1);
+    }
+    return r * Wk + c;
+}
+
+static int snis_args_ok(int64_t kappa, int radius, double alpha)
+{
+    return kappa >= 1 && radius >= 0 && radius <= 16 && alpha >= 0.0 && alpha <= 1.0;
+}
+
+/* r_i(j) for every key j of one query's modes (exposed for tests) */
+int oracle_snis_density(const int32_t* modes, int64_t kappa, int64_t Hk, int64_t Wk, int radius, double alpha,
+                        double* out)
+{
+    if (!snis_args_ok(kappa, radius, alpha) || Hk <= 0 || Wk <= 0) return -2;
+    for (int64_t j = 0; j < Hk * Wk; ++j) out[j] = snis_density(modes, kappa, Hk, Wk, radius, alpha, j);
+    return 0;
+}
+
+/* samples t = 0..T-1 of query g (exposed for tests) */
+int oracle_snis_draws(const int32_t* modes, int64_t kappa, int64_t Hk, int64_t Wk, int radius, double alpha,
+                      uint64_t seed, int64_t g, int64_t T, int64_t* out)
+{
+    if (!snis_args_ok(kappa, radius, alpha) || Hk <= 0 || Wk <= 0 || T < 0) return -2;
+    uint32_t key[2];
+    seed_key(seed, key);
+    for (int64_t t = 0; t < T; ++t) out[t] = snis_draw(modes, kappa, Hk, Wk, radius, alpha, key, g, t);
+    return 0;
+}
+
+/*
+ * The SNIS estimate (Equations 11-17) for each listed query i: T samples
+ * j_t ~ r_i, weights w_t = exp(a_ij_t) / r_i(j_t) with a = scale * q.k
+ * (Equation 13; a key after the query under OR_CAUSAL has p^(u) = 0, so
+ * weight 0), the estimate sum_t w_t v_j_t / sum_t w_t (Equation 14), the
+ * effective sample size (sum w)^2 / sum w^2 (Equation 16) and the variance
+ * sum_t (w_t / sum w)^2 (v_j_t - estimate)^2 per channel (Equation 15).
+ * The weights are formed as exp(log w_t - max_s log w_s), which leaves every
+ * ratio unchanged.  If every weight is 0 the row, its ESS and its variance
+ * are 0.  modes is [kappa, S, Hq, Wq]; out and var are compact [count, dv],
+ * ess is [count]; ess and var may be NULL.
+ */
+int oracle_snis(const double* Q, const double* K, const double* V, const int32_t* modes, int64_t kappa,
+                int64_t S, int64_t Hq, int64_t Wq, int64_t Hk, int64_t Wk, int d, int dv, int64_t T,
+                double alpha, int radius, double scale, uint64_t seed, uint32_t flags, const int64_t* query_ids,
+                int64_t nq, double* out, double* ess, double* var)
+{
+    if (check_dims(S, Hq, Wq, Hk, Wk, d) || dv <= 0 || T < 1 || !snis_args_ok(kappa, radius, alpha)) return -2;
+    if ((flags & OR_CAUSAL) && (Hq != Hk || Wq != Wk)) return -2;
+    const int64_t n = S * Hq * Wq, plane = Hq * Wq;
+    const int64_t count = query_ids ? nq : n;
+    for (int64_t g = 0; g < kappa * n; ++g)
+        if (modes[g] < 0 || modes[g] >= Hk * Wk) return -2;
+    if (query_ids)
+        for (int64_t i = 0; i < nq; ++i)
+            if (query_ids[i] < 0 || query_ids[i] >= n) return -2;
+    uint32_t key[2];
+    seed_key(seed, key);
+    int rc = 0;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < count; ++i) {
+        const int64_t g = query_ids ? query_ids[i] : i;
+        const int64_t s = g / plane;
+        const int64_t last = (flags & OR_CAUSAL) ? g % plane : Hk * Wk - 1;
+        const double* q = Q + g * d;
+        const double* Ks = K + s * Hk * Wk * d;
+        const double* Vs = V + s * Hk * Wk * dv;
+        int32_t* qm = (int32_t*)malloc(sizeof(int32_t) * kappa);
+        int64_t* js = (int64_t*)malloc(sizeof(int64_t) * T);
+        double* lw = (double*)malloc(sizeof(double) * T);
+        if (!qm || !js || !lw) {
+            free(qm), free(js), free(lw);
+            rc = -6;
+            continue;
+        }
+        for (int64_t e = 0; e < kappa; ++e) qm[e] = modes[e * n + g];
+        /* samples and log weights */
+        double mx = -INFINITY;
+        for (int64_t t = 0; t < T; ++t) {
+            js[t] = snis_draw(qm, kappa, Hk, Wk, radius, alpha, key, g, t);
+            if (js[t] > last) {
+                lw[t] = -INFINITY;
+            } else {
+                const double a = scale * dot(q, Ks + js[t] * d, d);
+                lw[t] = a - log(snis_density(qm, kappa, Hk, Wk, radius, alpha, js[t]));
+            }
+            if (lw[t] > mx) mx = lw[t];
+        }
+        double* o = out + i * dv;
+        double* vr = var ? var + i * dv : NULL;
+        for (int e = 0; e < dv; ++e) {
+            o[e] = 0.0;
+            if (vr) vr[e] = 0.0;
+        }
+        double s1 = 0.0, s2 = 0.0;
+        if (mx > -INFINITY) {
+            for (int64_t t = 0; t < T; ++t) {
+                const double w = exp(lw[t] - mx);
+                s1 += w;
+                s2 += w * w;
+                const double* v = Vs + js[t] * dv;
+                for (int e = 0; e < dv; ++e) o[e] += w * v[e];
+            }
+            for (int e = 0; e < dv; ++e) o[e] /= s1;
+            if (vr) {
+                for (int64_t t = 0; t < T; ++t) {
+                    const double wn = exp(lw[t] - mx) / s1;
+                    const double* v = Vs + js[t] * dv;
+                    for (int e = 0; e < dv; ++e) vr[e] += wn * wn * (v[e] - o[e]) * (v[e] - o[e]);
+                }
+            }
+        }
+        if (ess) ess[i] = s2 > 0.0 ? s1 * s1 / s2 : 0.0;
+        free(qm), free(js), free(lw);
     }
     return rc;
 }
