@@ -5,7 +5,9 @@ input: PatchMatch (random init + T Jacobi sweeps, one library call) then the
 sparse window attention (one call), on the 256x256, d=64, bf16, 4-slice
 workload by default.  ``--kappa K`` runs K constrained PatchMatch runs (run c
 given the maps of runs 0..c-1, separation ``--sep``) and attends over the
-union of their windows; ``--causal`` masks keys after each query.  Two timed regions: A runs the steps as a caller would
+union of their windows; ``--causal`` masks keys after each query;
+``--snis T`` replaces the window softmax by the importance-sampling estimate
+with T samples per query (``--alpha``, ``--radius``).  Two timed regions: A runs the steps as a caller would
 (throughput: ``value``, ``ms_per_step``); B runs the same steps with every
 kernel dispatch stamping caller-created HIP start/stop events on the launch
 stream (per-kernel durations for ``kernels_ms`` and ``roofline``; the stamps
@@ -48,6 +50,12 @@ def attend_bytes_per_query(cfg, kappa: int = 1) -> int:
     return row * (2 + 2 * kappa * cfg.window ** 2) + 4 * kappa
 
 
+def snis_bytes_per_query(cfg, samples: int, kappa: int = 1) -> int:
+    """q row, T key rows and T value rows, kappa 4 B modes, the output row."""
+    row = cfg.d * cfg.elem_bytes
+    return row * (2 + 2 * samples) + 4 * kappa
+
+
 def init_bytes_per_query(cfg) -> int:
     return 2 * cfg.d * cfg.elem_bytes + 8
 
@@ -70,7 +78,7 @@ def load_traffic(cfg):
     return t.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(cfg, arrays, min_s: float, kappa: int = 1, sep: int = 1, causal: bool = False):
+def cpu_baseline(cfg, arrays, min_s: float, kappa: int = 1, sep: int = 1, causal: bool = False, snis=None):
     """The fp64 oracle on the host cores, on whole slices of the same workload.
 
     Slices are run in turn (wrapping around) until at least ``min_s`` seconds
@@ -89,7 +97,11 @@ def cpu_baseline(cfg, arrays, min_s: float, kappa: int = 1, sep: int = 1, causal
         s = runs % cfg.S
         t0 = time.perf_counter()
         J, _, _ = oracle.patchmatch_kappa(Q[s:s + 1], K[s:s + 1], kappa, cfg.iters, cfg.pm_seed, sep=sep, flags=flags)
-        oracle.sparse_attend(Q[s:s + 1], K[s:s + 1], V[s:s + 1], J, cfg.window, cfg.scale, flags=flags)
+        if snis:
+            T, alpha, radius = snis
+            oracle.snis(Q[s:s + 1], K[s:s + 1], V[s:s + 1], J, T, alpha, radius, cfg.scale, cfg.pm_seed, flags=flags)
+        else:
+            oracle.sparse_attend(Q[s:s + 1], K[s:s + 1], V[s:s + 1], J, cfg.window, cfg.scale, flags=flags)
         elapsed += time.perf_counter() - t0
         done_q += per_slice
         runs += 1
@@ -99,7 +111,8 @@ def cpu_baseline(cfg, arrays, min_s: float, kappa: int = 1, sep: int = 1, causal
         "cores": threads,
         "kind": "oracle",
         "sample": f"{runs} slice passes over the {cfg.S}-slice workload ({done_q} queries; {kappa} x {cfg.iters} "
-                  f"sweeps + {cfg.window}x{cfg.window} attend each), fp64, {elapsed:.1f} s",
+                  f"sweeps + " + (f"{snis[0]}-sample SNIS" if snis else f"{cfg.window}x{cfg.window} attend")
+                  + f" each), fp64, {elapsed:.1f} s",
     }
 
 
@@ -112,6 +125,10 @@ def main(argv=None) -> int:
     ap.add_argument("--kappa", type=int, default=1, help="matches per query (constrained PatchMatch runs)")
     ap.add_argument("--sep", type=int, default=1, help="separation between the runs' matches (Chebyshev)")
     ap.add_argument("--causal", action="store_true", help="mask keys after each query (raster order)")
+    ap.add_argument("--snis", type=int, default=0, metavar="T",
+                    help="estimate with T importance samples per query instead of the window softmax")
+    ap.add_argument("--alpha", type=float, default=0.9, help="SNIS mixture weight of the local densities")
+    ap.add_argument("--radius", type=int, default=4, help="SNIS binomial radius m (variance m/2)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="seconds of oracle work for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -171,8 +188,13 @@ def main(argv=None) -> int:
         for c in range(kappa):
             scram.patchmatch(Q, K, T, cfg.pm_seed, prev=J[:c] if c else None, sep=sep, causal=causal, out=J[c],
                              workspace=ws, events=None if ev is None else ev[c * per_run:(c + 1) * per_run])
-        scram.sparse_attend(Q, K, V, J if kappa > 1 else J[0], cfg.window, cfg.scale, causal=causal, out=out,
-                            events=None if ev is None else ev[-2:])
+        maps = J if kappa > 1 else J[0]
+        if args.snis:
+            scram.snis_attend(Q, K, V, maps, args.snis, alpha=args.alpha, radius=args.radius, scale=cfg.scale,
+                              seed=cfg.pm_seed, causal=causal, out=out, events=None if ev is None else ev[-2:])
+        else:
+            scram.sparse_attend(Q, K, V, maps, cfg.window, cfg.scale, causal=causal, out=out,
+                                events=None if ev is None else ev[-2:])
 
     for _ in range(args.warmup):
         step()
@@ -208,9 +230,9 @@ def main(argv=None) -> int:
     nq = cfg.nq
     # the dominant kernel: the sweep, averaged over the runs (run c reads c previous maps)
     pm_launch_bytes = nq * sum(pm_bytes_per_query_sweep(cfg, c) for c in range(kappa)) / kappa
-    att_bytes = nq * attend_bytes_per_query(cfg, kappa)
+    att_bytes = nq * (snis_bytes_per_query(cfg, args.snis, kappa) if args.snis else attend_bytes_per_query(cfg, kappa))
     achieved = pm_launch_bytes / (iter_ms * 1e-3) / 1e9
-    default_path = kappa == 1 and not causal
+    default_path = kappa == 1 and not causal and not args.snis
     traffic_bytes = load_traffic(cfg) if default_path else None
     traffic = None if traffic_bytes is None else traffic_bytes / (iter_ms * 1e-3) / 1e9
 
@@ -240,6 +262,7 @@ def main(argv=None) -> int:
             "kappa": kappa,
             "separation": sep,
             "causal": causal,
+            "estimator": f"snis T={args.snis} alpha={args.alpha} m={args.radius}" if args.snis else "window",
             "queries_per_step": nq,
         },
         "roofline": {
@@ -262,7 +285,8 @@ def main(argv=None) -> int:
         "device": torch.cuda.get_device_name(dev),
     }
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(cfg, data["np"], args.cpu_seconds, kappa, sep, causal)
+        res["cpu_baseline"] = cpu_baseline(cfg, data["np"], args.cpu_seconds, kappa, sep, causal,
+                                           (args.snis, args.alpha, args.radius) if args.snis else None)
     print(json.dumps(res), flush=True)
     return 0
 

@@ -24,6 +24,12 @@
  * the union of the kappa windows, each key once.  SCRAM_CAUSAL (Section
  * 4.2.1) restricts both steps to keys at or before the query in raster order.
  *
+ * scram_snis_attend replaces the window of step 2 by the self-normalised
+ * importance-sampling estimator of Section 4.2 (Monte Carlo estimators,
+ * Equations 11-17): T keys per query drawn from a mixture of local densities
+ * around the kappa matches and a uniform distribution, weighted by
+ * exp(a_ij) / r_i(j).
+ *
  * Conventions shared by every entry point
  * ----------------------------------------
  * - Data layout: row-major, channels innermost.  Q is [S, Hq, Wq, d], K is
@@ -87,6 +93,9 @@ enum { SCRAM_CAUSAL = 4u };
 /* most previous runs one PatchMatch run may be constrained by, and most maps
  * one attend call may unite */
 enum { SCRAM_MAX_PREV = 7, SCRAM_MAX_KAPPA = 8 };
+
+/* limits of scram_snis_attend: samples per query, binomial radius m */
+enum { SCRAM_SNIS_MAX_SAMPLES = 1 << 20, SCRAM_SNIS_MAX_RADIUS = 16 };
 
 /*
  * Bytes of workspace scram_patchmatch needs for S*Hq*Wq queries: one int32
@@ -192,13 +201,60 @@ int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype, 
                         int S, int Hq, int Wq, int Hk, int Wk, int d, int dv, int window, float scale,
                         uint32_t flags, void* out, hipEvent_t* events, hipStream_t stream);
 
+/*
+ * Self-normalised importance sampling around the matches (Section 4.2,
+ * Monte Carlo estimators, Equations 11-17).  For query i with matches
+ * (u_e, v_e) = divmod(modes[e][i], Wk), e < kappa:
+ *   - importance distribution (Equation 17):
+ *       r_i(j) = alpha' / kappa * sum_e g(j; u_e, v_e) + (1 - alpha') / (Hk Wk)
+ *     with alpha' = round(alpha * 65536) / 65536 and g the product over the
+ *     two axes of a centred binomial offset (the number of ones among 2m fair
+ *     bits, minus m: a discrete Gaussian of variance m / 2), the coordinate
+ *     clamped to the grid (the edge row or column holds that side's tail);
+ *   - sample t (Equation 12) of query g uses the Philox4x32-10 block
+ *     (w0, w1, w2, w3) of counter (g, t, 0, 0x534E4953) and key (seed mod 2^32,
+ *     seed div 2^32): if (w0 >> 16) < round(alpha * 65536), mode
+ *     e = floor(w1 * kappa / 2^32) and offsets popcount(w2 & (2^2m - 1)) - m,
+ *     popcount(w3 & (2^2m - 1)) - m; otherwise row floor(w2 * Hk / 2^32) and
+ *     column floor(w3 * Wk / 2^32);
+ *   - weights w_t = exp(scale * q_i . k_j_t) / r_i(j_t) (Equation 13; with
+ *     SCRAM_CAUSAL a key after the query has weight 0);
+ *   - out[i] = sum_t w_t v_j_t / sum_t w_t (Equation 14), written in `dtype`;
+ *   - ess_out[i] = (sum_t w_t)^2 / sum_t w_t^2 (Equation 16);
+ *   - var_out[i][e] = sum_t (w_t / sum_s w_s)^2 (v_j_t,e - out[i][e])^2
+ *     (Equation 15 with self-normalised weights).
+ * All in fp32, with weights kept relative to their running maximum (ratios
+ * unchanged).  A query whose weights are all 0 gets a zero row, ESS 0 and
+ * variance 0.  The variance takes a second pass over the same samples.
+ *
+ * Arguments:
+ *   Q, K, V   inputs, layouts above; dv == d
+ *   modes     int32 [kappa, S, Hq, Wq] flat key indices (e.g. PatchMatch maps)
+ *   kappa     1 <= kappa <= SCRAM_MAX_KAPPA
+ *   samples   T, 1 <= T <= SCRAM_SNIS_MAX_SAMPLES
+ *   alpha     mixture weight of the local densities, 0 <= alpha <= 1
+ *   radius    m, 0 <= m <= SCRAM_SNIS_MAX_RADIUS (m = 0: the mode itself)
+ *   scale     softmax temperature (1/sqrt(d_k)); finite
+ *   seed      Philox key
+ *   flags     0 or SCRAM_CAUSAL
+ *   out       [S, Hq, Wq, dv] in `dtype` (written)
+ *   ess_out   nullable fp32 [S, Hq, Wq] (written)
+ *   var_out   nullable fp32 [S, Hq, Wq, dv], 16-byte aligned (written)
+ *   events    NULL or 2 events, as for scram_sparse_attend
+ * Outputs must not overlap the inputs or each other.  Returns a status code.
+ */
+int scram_snis_attend(const void* Q, const void* K, const void* V, int dtype, const int32_t* modes, int kappa, int S,
+                      int Hq, int Wq, int Hk, int Wk, int d, int dv, int samples, float alpha, int radius, float scale,
+                      uint64_t seed, uint32_t flags, void* out, float* ess_out, float* var_out, hipEvent_t* events,
+                      hipStream_t stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* scram_status_string(int status);
 
 /* ABI version of this header: (major << 16) | minor. */
 int scram_abi_version(void);
 
-#define SCRAM_ABI_VERSION ((2 << 16) | 0)
+#define SCRAM_ABI_VERSION ((2 << 16) | 1)
 
 #ifdef __cplusplus
 }

@@ -17,6 +17,7 @@ from .binding import (  # noqa: F401
     patchmatch,
     patchmatch_kappa,
     patchmatch_workspace_bytes,
+    snis_attend,
     sparse_attend,
     status_string,
 )

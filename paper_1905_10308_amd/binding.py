@@ -57,6 +57,9 @@ def lib() -> ctypes.CDLL:
     L.scram_patchmatch.restype = I
     L.scram_sparse_attend.argtypes = [P, P, P, I, P, I, I, I, I, I, I, I, I, I, ctypes.c_float, U32, P, P, P]
     L.scram_sparse_attend.restype = I
+    L.scram_snis_attend.argtypes = [P, P, P, I, P, I, I, I, I, I, I, I, I, I, ctypes.c_float, I, ctypes.c_float,
+                                    U64, U32, P, P, P, P, P]
+    L.scram_snis_attend.restype = I
     L.scram_status_string.argtypes = [I]
     L.scram_status_string.restype = ctypes.c_char_p
     L.scram_abi_version.argtypes = []
@@ -217,6 +220,48 @@ def sparse_attend(Q, K, V, argmax, window: int, scale: float | None = None, *, c
     if rc != 0:
         raise ScramError(rc, "scram_sparse_attend")
     return out
+
+
+def snis_attend(Q, K, V, modes, samples: int, *, alpha: float = 0.9, radius: int = 4, scale: float | None = None,
+                seed: int = 0, causal: bool = False, ess: bool = False, var: bool = False, out=None, events=None):
+    """Self-normalised importance-sampling estimate around ``modes`` (``scram_snis_attend``).
+
+    ``modes`` is int32 ``[S, Hq, Wq]`` or ``[kappa, S, Hq, Wq]``; ``samples``
+    keys per query from the mixture of centred-binomial local densities
+    (radius ``m = radius``, weight ``alpha``) and the uniform distribution.
+    Returns the ``[S, Hq, Wq, dv]`` estimate in Q's dtype, or, when ``ess`` or
+    ``var`` is set, ``(out, ess [S, Hq, Wq] fp32 | None, var [S, Hq, Wq, dv] fp32 | None)``.
+    """
+    torch = _torch()
+    for name, t in (("Q", Q), ("K", K), ("V", V)):
+        _dev_tensor(t, name, 4)
+        if t.dtype != Q.dtype:
+            raise TypeError("Q, K, V must share a dtype")
+    _dev_tensor(modes, "modes")
+    S, Hq, Wq, d = Q.shape
+    _, Hk, Wk, _ = K.shape
+    dv = V.shape[3]
+    if tuple(K.shape[:3]) != tuple(V.shape[:3]) or K.shape[0] != S or K.shape[3] != d:
+        raise ValueError("K and V must share the key grid; K must match Q's slices and channels")
+    if modes.dtype != torch.int32 or tuple(modes.shape[-3:]) != (S, Hq, Wq) or modes.dim() not in (3, 4):
+        raise ValueError("modes must be int32 [S, Hq, Wq] or [kappa, S, Hq, Wq]")
+    kappa = 1 if modes.dim() == 3 else modes.shape[0]
+    if scale is None:
+        scale = d ** -0.5
+    dev = Q.device
+    if out is None:
+        out = torch.empty((S, Hq, Wq, dv), dtype=Q.dtype, device=dev)
+    _dev_tensor(out, "out", 4)
+    ess_t = torch.empty((S, Hq, Wq), dtype=torch.float32, device=dev) if ess else None
+    var_t = torch.empty((S, Hq, Wq, dv), dtype=torch.float32, device=dev) if var else None
+    ev = None if events is None else _event_array(events, 2)
+    rc = lib().scram_snis_attend(_ptr(Q), _ptr(K), _ptr(V), _dtype_code(Q), _ptr(modes), int(kappa), S, Hq, Wq, Hk,
+                                 Wk, d, dv, int(samples), float(alpha), int(radius), float(scale),
+                                 ctypes.c_uint64(int(seed) & 0xFFFFFFFFFFFFFFFF), CAUSAL if causal else 0, _ptr(out),
+                                 _ptr(ess_t), _ptr(var_t), ev, _stream(dev))
+    if rc != 0:
+        raise ScramError(rc, "scram_snis_attend")
+    return (out, ess_t, var_t) if (ess or var) else out
 
 
 def patchmatch_kappa(Q, K, kappa: int, iters: int, seed: int, *, sep: int = 1, causal: bool = False, flags: int = 0):

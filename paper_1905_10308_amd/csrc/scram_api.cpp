@@ -189,6 +189,45 @@ int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype, 
     return e == hipSuccess ? SCRAM_OK : SCRAM_ERR_HIP;
 }
 
+int scram_snis_attend(const void* Q, const void* K, const void* V, int dtype, const int32_t* modes, int kappa, int S,
+                      int Hq, int Wq, int Hk, int Wk, int d, int dv, int samples, float alpha, int radius, float scale,
+                      uint64_t seed, uint32_t flags, void* out, float* ess_out, float* var_out, hipEvent_t* events,
+                      hipStream_t stream)
+{
+    if (!Q || !K || !V || !modes || !out) return SCRAM_ERR_NULL;
+    int rc = check_grid(S, Hq, Wq, Hk, Wk);
+    if (rc) return rc;
+    if (kappa < 1 || kappa > SCRAM_MAX_KAPPA) return SCRAM_ERR_SHAPE;
+    if (samples < 1 || samples > SCRAM_SNIS_MAX_SAMPLES) return SCRAM_ERR_SHAPE;
+    if (!(alpha >= 0.f && alpha <= 1.f)) return SCRAM_ERR_SHAPE;  // also rejects NaN
+    if (radius < 0 || radius > SCRAM_SNIS_MAX_RADIUS) return SCRAM_ERR_SHAPE;
+    if (!isfinite(scale)) return SCRAM_ERR_SHAPE;
+    if ((rc = check_type(dtype, d))) return rc;
+    if (dv != d) return SCRAM_ERR_UNSUPPORTED;
+    if (flags & ~uint32_t(SCRAM_CAUSAL)) return SCRAM_ERR_UNSUPPORTED;
+    const bool causal = (flags & SCRAM_CAUSAL) != 0;
+    if (causal && (Hq != Hk || Wq != Wk)) return SCRAM_ERR_SHAPE;
+    if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(out, 16) || !aligned(modes, 4) ||
+        (ess_out && !aligned(ess_out, 4)) || (var_out && !aligned(var_out, 16)))
+        return SCRAM_ERR_ALIGN;
+    const size_t n = size_t(S) * Hq * Wq, eb = elem_bytes(dtype);
+    const Range rO = range(out, n * dv * eb);
+    const Range rE = ess_out ? range(ess_out, 4 * n) : Range{0, 0};
+    const Range rV = var_out ? range(var_out, 4 * n * dv) : Range{0, 0};
+    for (const Range& o : {rO, rE, rV}) {
+        for (const Range& other : {range(Q, n * d * eb), range(K, size_t(S) * Hk * Wk * d * eb),
+                                   range(V, size_t(S) * Hk * Wk * dv * eb), range(modes, 4 * n * size_t(kappa))}) {
+            if (overlap(o, other)) return SCRAM_ERR_ALIAS;
+        }
+    }
+    if (overlap(rO, rE) || overlap(rO, rV) || overlap(rE, rV)) return SCRAM_ERR_ALIAS;
+    const scram::Grid grid{S, Hq, Wq, Hk, Wk, d};
+    const scram::SnisSpec spec{samples, alpha, radius, scale, seed};
+    const hipError_t e = scram::launch_snis(dtype, Q, K, V, modes, kappa, grid, spec, causal, out, ess_out, var_out,
+                                            stream, events ? events[0] : nullptr, events ? events[1] : nullptr);
+    return e == hipSuccess ? SCRAM_OK : SCRAM_ERR_HIP;
+}
+
 const char* scram_status_string(int status)
 {
     switch (status) {

@@ -40,4 +40,19 @@ hipError_t launch_attend(int dtype, const void* Q, const void* K, const void* V,
                          const Grid& g, int window, float scale, bool causal, void* out, hipStream_t stream,
                          hipEvent_t start, hipEvent_t stop);
 
+// Self-normalised importance sampling around the kappa maps in modes
+// ([kappa, n]): samples per query, mixture weight, binomial radius m,
+// softmax scale and Philox seed.
+struct SnisSpec {
+    int samples;
+    float alpha;
+    int radius;
+    float scale;
+    uint64_t seed;
+};
+
+hipError_t launch_snis(int dtype, const void* Q, const void* K, const void* V, const int32_t* modes, int kappa,
+                       const Grid& g, const SnisSpec& spec, bool causal, void* out, float* ess, float* var,
+                       hipStream_t stream, hipEvent_t start, hipEvent_t stop);
+
 }  // namespace scram

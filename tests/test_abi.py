@@ -40,7 +40,7 @@ def declared_functions():
 
 def test_header_declares_entry_points():
     names = declared_functions()
-    for n in ("scram_patchmatch", "scram_sparse_attend", "scram_patchmatch_workspace_bytes",
+    for n in ("scram_patchmatch", "scram_sparse_attend", "scram_snis_attend", "scram_patchmatch_workspace_bytes",
               "scram_status_string", "scram_abi_version"):
         assert n in names
 
@@ -51,7 +51,7 @@ def test_library_exports_every_declared_symbol(L):
 
 
 def test_abi_version(L):
-    assert L.scram_abi_version() == (2 << 16)
+    assert L.scram_abi_version() == (2 << 16) | 1
 
 
 def test_status_strings(L):
@@ -128,6 +128,35 @@ def test_patchmatch_rejects(L, kw, code):
 ])
 def test_sparse_attend_rejects(L, kw, code):
     assert at(L, **kw) == code
+
+
+A_E, A_VAR = 0x10000000 * 11, 0x10000000 * 12
+
+
+def sn(L, **kw):
+    a = dict(Q=A_Q, K=A_K, V=A_V, dtype=F32, modes=A_J, kappa=2, S=2, Hq=8, Wq=8, Hk=8, Wk=8, d=16, dv=16,
+             samples=32, alpha=0.9, radius=4, scale=0.25, seed=3, flags=0, out=A_O, ess=A_E, var=A_VAR)
+    a.update(kw)
+    return L.scram_snis_attend(a["Q"], a["K"], a["V"], a["dtype"], a["modes"], a["kappa"], a["S"], a["Hq"], a["Wq"],
+                               a["Hk"], a["Wk"], a["d"], a["dv"], a["samples"], a["alpha"], a["radius"], a["scale"],
+                               a["seed"], a["flags"], a["out"], a["ess"], a["var"], None, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(Q=None), ENULL), (dict(K=None), ENULL), (dict(V=None), ENULL), (dict(modes=None), ENULL),
+    (dict(out=None), ENULL),
+    (dict(S=0), ESHAPE), (dict(kappa=0), ESHAPE), (dict(kappa=MAX_KAPPA + 1), ESHAPE), (dict(samples=0), ESHAPE),
+    (dict(samples=(1 << 20) + 1), ESHAPE), (dict(alpha=-0.01), ESHAPE), (dict(alpha=1.5), ESHAPE),
+    (dict(alpha=float("nan")), ESHAPE), (dict(radius=-1), ESHAPE), (dict(radius=17), ESHAPE),
+    (dict(scale=float("inf")), ESHAPE), (dict(flags=CAUSAL, Wk=4), ESHAPE),
+    (dict(d=24), EUNSUP), (dict(dv=32), EUNSUP), (dict(dtype=3), EUNSUP), (dict(flags=1), EUNSUP),
+    (dict(Q=A_Q + 4), EALIGN), (dict(out=A_O + 8), EALIGN), (dict(modes=A_J + 2), EALIGN),
+    (dict(ess=A_E + 2), EALIGN), (dict(var=A_VAR + 4), EALIGN),
+    (dict(out=A_Q), EALIAS), (dict(ess=A_K + 64), EALIAS), (dict(var=A_J), EALIAS), (dict(ess=A_VAR + 16), EALIAS),
+    (dict(var=A_O + 2 * 64 * 16 * 4 - 16), EALIAS), (dict(modes=A_O - 4 * 128 * 2 + 4), EALIAS),
+])
+def test_snis_rejects(L, kw, code):
+    assert sn(L, **kw) == code
 
 
 def test_python_binding_refuses_host_tensors():
