@@ -75,6 +75,8 @@ def _load():
                                       P, i64, ctypes.c_uint32, ctypes.c_double, P, i64, i64, P, P, P, P]
     lib.oracle_sparse_attend.argtypes = [P, P, P, P, i64, i64, i64, i64, i64, i64, ctypes.c_int,
                                          ctypes.c_int, ctypes.c_int, ctypes.c_double, ctypes.c_uint32, P, i64, P]
+    lib.oracle_sparse_attend_backward.argtypes = [P, P, P, P, i64, i64, i64, i64, i64, i64, ctypes.c_int, ctypes.c_int,
+                                                  ctypes.c_int, ctypes.c_double, ctypes.c_uint32, P, P, P, P]
     lib.oracle_snis_density.argtypes = [P, i64, i64, i64, ctypes.c_int, ctypes.c_double, P]
     lib.oracle_snis_draws.argtypes = [P, i64, i64, i64, ctypes.c_int, ctypes.c_double, ctypes.c_uint64, i64, i64, P]
     lib.oracle_snis.argtypes = [P, P, P, P, i64, i64, i64, i64, i64, i64, ctypes.c_int, ctypes.c_int, i64,
@@ -261,6 +263,21 @@ def sparse_attend(Q, K, V, J, window, scale, query_ids=None, flags=0):
     _check(_load().oracle_sparse_attend(_ptr(Q), _ptr(K), _ptr(V), _ptr(J), kappa, S, Hq, Wq, Hk, Wk, d, dv,
                                         window, scale, flags, _ptr(ids), nq, _ptr(out)), "sparse_attend")
     return out
+
+
+def sparse_attend_backward(Q, K, V, J, window, scale, dO, flags=0):
+    """Gradients of ``sparse_attend`` with the maps held fixed -> (dQ, dK, dV), float64."""
+    Q, K, V, J, dO = _f64(Q), _f64(K), _f64(V), _i32(J), _f64(dO)
+    S, Hq, Wq, Hk, Wk, d = _dims(Q, K)
+    J = J.reshape(-1, S, Hq, Wq)
+    if V.shape[:3] != K.shape[:3] or dO.shape != Q.shape[:3] + (V.shape[3],):
+        raise ValueError("V must share K's grid and dO must be [S, Hq, Wq, dv]")
+    dv = V.shape[3]
+    dQ, dK, dV = np.empty(Q.shape), np.empty(K.shape), np.empty(V.shape)
+    _check(_load().oracle_sparse_attend_backward(_ptr(Q), _ptr(K), _ptr(V), _ptr(J), J.shape[0], S, Hq, Wq, Hk, Wk,
+                                                 d, dv, window, scale, flags, _ptr(dO), _ptr(dQ), _ptr(dK), _ptr(dV)),
+           "sparse_attend_backward")
+    return dQ, dK, dV
 
 
 def snis_density(modes, Hk, Wk, radius, alpha):

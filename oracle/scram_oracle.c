@@ -57,6 +57,9 @@
  * initial match is drawn uniformly from the valid keys, and the attend
  * window drops keys after the query.
  *
+ * Backward of the sparse attention: the gradients with respect to Q, K and
+ * V with the maps held fixed (the key sets are not differentiable).
+ *
  * Self-normalised importance sampling (Section 4.2, Monte Carlo estimators,
  * Equations 11-17): the importance distribution mixes, with weight alpha, a
  * local density around each of the kappa PatchMatch modes and, with weight
@@ -473,27 +476,59 @@ static int in_window(int64_t r, int64_t c, int64_t centre, int64_t Wk, int64_t b
 }
 
 /*
+ * The key set of query g in Algorithm 2: the union over the kappa matches
+ * e of the windows {(u_e + a, v_e + c) : |a|, |c| <= b} (each key once, in
+ * the order first met), intersected with the key grid and, with OR_CAUSAL,
+ * with the keys up to the query.  keys must hold kappa * (2b+1)^2 entries.
+ */
+static int64_t window_keys(const int32_t* J, int64_t kappa, int64_t n, int64_t g, int64_t Hk, int64_t Wk, int64_t b,
+                           int64_t last, int64_t* keys)
+{
+    int64_t nk = 0;
+    for (int64_t e = 0; e < kappa; ++e) {
+        const int64_t centre = J[e * n + g];
+        const int64_t u = centre / Wk, v = centre % Wk;
+        for (int64_t a = -b; a <= b; ++a)
+            for (int64_t c = -b; c <= b; ++c) {
+                int64_t r = u + a, col = v + c;
+                if (r < 0 || r >= Hk || col < 0 || col >= Wk) continue;
+                if (r * Wk + col > last) continue;
+                int seen = 0; /* already in the window of an earlier match */
+                for (int64_t f = 0; f < e && !seen; ++f) seen = in_window(r, col, J[f * n + g], Wk, b);
+                if (!seen) keys[nk++] = r * Wk + col;
+            }
+    }
+    return nk;
+}
+
+static int attend_args(const int32_t* J, int64_t kappa, int64_t S, int64_t Hq, int64_t Wq, int64_t Hk, int64_t Wk,
+                       int d, int dv, int window, uint32_t flags)
+{
+    if (check_dims(S, Hq, Wq, Hk, Wk, d) || dv <= 0 || window < 1 || window % 2 == 0 || kappa < 1) return -2;
+    if ((flags & OR_CAUSAL) && (Hq != Hk || Wq != Wk)) return -2;
+    const int64_t n = S * Hq * Wq;
+    for (int64_t g = 0; g < kappa * n; ++g)
+        if (J[g] < 0 || J[g] >= Hk * Wk) return -2;
+    return 0;
+}
+
+/*
  * Sparse non-local mean (Algorithm 2, Equations 8-9): for each listed query i
- * the set J_i = union over the kappa matches e of the window
- * {(u_e + a, v_e + c) : |a|, |c| <= b} (each key once), intersected with the
- * key grid (and, with OR_CAUSAL, with the keys up to i), scores
- * a_j = scale * q_i . k_j and the output sum_j softmax(a)_j v_j.  J is
- * [kappa, S, Hq, Wq].  Two passes: the maximum score first, then
- * exp(a_j - max) weights.  An empty set (possible only with OR_CAUSAL and a
- * match after the query) gives a zero row.  out is compact [count, dv].
+ * the key set above, scores a_j = scale * q_i . k_j and the output
+ * sum_j softmax(a)_j v_j.  J is [kappa, S, Hq, Wq].  Two passes: the maximum
+ * score first, then exp(a_j - max) weights.  An empty set (possible only with
+ * OR_CAUSAL and a match after the query) gives a zero row.  out is compact
+ * [count, dv].
  */
 int oracle_sparse_attend(const double* Q, const double* K, const double* V, const int32_t* J,
                          int64_t kappa, int64_t S, int64_t Hq, int64_t Wq, int64_t Hk, int64_t Wk, int d,
                          int dv, int window, double scale, uint32_t flags, const int64_t* query_ids,
                          int64_t nq, double* out)
 {
-    if (check_dims(S, Hq, Wq, Hk, Wk, d) || dv <= 0 || window < 1 || window % 2 == 0 || kappa < 1) return -2;
-    if ((flags & OR_CAUSAL) && (Hq != Hk || Wq != Wk)) return -2;
+    if (attend_args(J, kappa, S, Hq, Wq, Hk, Wk, d, dv, window, flags)) return -2;
     const int64_t n = S * Hq * Wq, plane = Hq * Wq;
     const int64_t b = window / 2;
     const int64_t count = query_ids ? nq : n;
-    for (int64_t g = 0; g < kappa * n; ++g)
-        if (J[g] < 0 || J[g] >= Hk * Wk) return -2;
     if (query_ids)
         for (int64_t i = 0; i < nq; ++i)
             if (query_ids[i] < 0 || query_ids[i] >= n) return -2;
@@ -515,20 +550,7 @@ int oracle_sparse_attend(const double* Q, const double* K, const double* V, cons
             continue;
         }
         /* 1. the key set: every window, clipped to the grid, each key once */
-        int64_t nk = 0;
-        for (int64_t e = 0; e < kappa; ++e) {
-            const int64_t centre = J[e * n + g];
-            const int64_t u = centre / Wk, v = centre % Wk;
-            for (int64_t a = -b; a <= b; ++a)
-                for (int64_t c = -b; c <= b; ++c) {
-                    int64_t r = u + a, col = v + c;
-                    if (r < 0 || r >= Hk || col < 0 || col >= Wk) continue;
-                    if (r * Wk + col > last) continue;
-                    int seen = 0; /* already in the window of an earlier match */
-                    for (int64_t f = 0; f < e && !seen; ++f) seen = in_window(r, col, J[f * n + g], Wk, b);
-                    if (!seen) keys[nk++] = r * Wk + col;
-                }
-        }
+        const int64_t nk = window_keys(J, kappa, n, g, Hk, Wk, b, last, keys);
         /* 2. softmax over the set (two passes) and the weighted sum of values */
         double m = -INFINITY;
         for (int64_t j = 0; j < nk; ++j) {
@@ -547,6 +569,75 @@ int oracle_sparse_attend(const double* Q, const double* K, const double* V, cons
         free(keys);
     }
     return rc;
+}
+
+/*
+ * Gradients of the sparse attention output with the maps held fixed (the
+ * key sets do not depend on Q, K, V).  With p_j the softmax weights of query
+ * i over its key set, dp_j = dO_i . v_j and D_i = sum_j p_j dp_j
+ * (= dO_i . o_i), the score gradient is ds_j = p_j (dp_j - D_i), and
+ *   dQ_i += scale * sum_j ds_j k_j,   dK_j += scale * ds_j q_i,   dV_j += p_j dO_i.
+ * Queries are visited in order (the scatter into dK, dV is sequential).
+ * dQ [S,Hq,Wq,d], dK [S,Hk,Wk,d], dV [S,Hk,Wk,dv] are overwritten.
+ */
+int oracle_sparse_attend_backward(const double* Q, const double* K, const double* V, const int32_t* J, int64_t kappa,
+                                  int64_t S, int64_t Hq, int64_t Wq, int64_t Hk, int64_t Wk, int d, int dv, int window,
+                                  double scale, uint32_t flags, const double* dO, double* dQ, double* dK, double* dV)
+{
+    if (attend_args(J, kappa, S, Hq, Wq, Hk, Wk, d, dv, window, flags)) return -2;
+    const int64_t n = S * Hq * Wq, plane = Hq * Wq, nkeys = Hk * Wk;
+    const int64_t b = window / 2;
+    const int64_t wr = window < Hk ? window : Hk, wc = window < Wk ? window : Wk;
+    const int64_t cap = kappa * wr * wc;
+    int64_t* keys = (int64_t*)malloc(sizeof(int64_t) * cap);
+    double* p = (double*)malloc(sizeof(double) * cap);
+    double* dp = (double*)malloc(sizeof(double) * cap);
+    if (!keys || !p || !dp) {
+        free(keys), free(p), free(dp);
+        return -6;
+    }
+    memset(dQ, 0, sizeof(double) * n * d);
+    memset(dK, 0, sizeof(double) * S * nkeys * d);
+    memset(dV, 0, sizeof(double) * S * nkeys * dv);
+    for (int64_t g = 0; g < n; ++g) {
+        const int64_t s = g / plane;
+        const int64_t last = (flags & OR_CAUSAL) ? g % plane : nkeys - 1;
+        const double* q = Q + g * d;
+        const double* go = dO + g * dv;
+        const double* Ks = K + s * nkeys * d;
+        const double* Vs = V + s * nkeys * dv;
+        double* gK = dK + s * nkeys * d;
+        double* gV = dV + s * nkeys * dv;
+        const int64_t nk = window_keys(J, kappa, n, g, Hk, Wk, b, last, keys);
+        if (nk == 0) continue;
+        /* softmax weights over the set */
+        double m = -INFINITY, l = 0.0;
+        for (int64_t j = 0; j < nk; ++j) {
+            p[j] = scale * dot(q, Ks + keys[j] * d, d);
+            if (p[j] > m) m = p[j];
+        }
+        for (int64_t j = 0; j < nk; ++j) {
+            p[j] = exp(p[j] - m);
+            l += p[j];
+        }
+        double D = 0.0;
+        for (int64_t j = 0; j < nk; ++j) {
+            p[j] /= l;
+            dp[j] = dot(go, Vs + keys[j] * dv, dv);
+            D += p[j] * dp[j];
+        }
+        for (int64_t j = 0; j < nk; ++j) {
+            const double ds = p[j] * (dp[j] - D);
+            const double* k = Ks + keys[j] * d;
+            for (int e = 0; e < d; ++e) {
+                dQ[g * d + e] += scale * ds * k[e];
+                gK[keys[j] * d + e] += scale * ds * q[e];
+            }
+            for (int e = 0; e < dv; ++e) gV[keys[j] * dv + e] += p[j] * go[e];
+        }
+    }
+    free(keys), free(p), free(dp);
+    return 0;
 }
 
 /* ------------------------------------------------------------------------ */
