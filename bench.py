@@ -7,7 +7,8 @@ workload by default.  ``--kappa K`` runs K constrained PatchMatch runs (run c
 given the maps of runs 0..c-1, separation ``--sep``) and attends over the
 union of their windows; ``--causal`` masks keys after each query;
 ``--snis T`` replaces the window softmax by the importance-sampling estimate
-with T samples per query (``--alpha``, ``--radius``).  Two timed regions: A runs the steps as a caller would
+with T samples per query (``--alpha``, ``--radius``); ``--backward`` adds the
+gradients of the window attention to every step.  Two timed regions: A runs the steps as a caller would
 (throughput: ``value``, ``ms_per_step``); B runs the same steps with every
 kernel dispatch stamping caller-created HIP start/stop events on the launch
 stream (per-kernel durations for ``kernels_ms`` and ``roofline``; the stamps
@@ -127,6 +128,7 @@ def main(argv=None) -> int:
     ap.add_argument("--causal", action="store_true", help="mask keys after each query (raster order)")
     ap.add_argument("--snis", type=int, default=0, metavar="T",
                     help="estimate with T importance samples per query instead of the window softmax")
+    ap.add_argument("--backward", action="store_true", help="add the attend backward (maps held fixed) to each step")
     ap.add_argument("--alpha", type=float, default=0.9, help="SNIS mixture weight of the local densities")
     ap.add_argument("--radius", type=int, default=4, help="SNIS binomial radius m (variance m/2)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="seconds of oracle work for the CPU baseline")
@@ -176,9 +178,17 @@ def main(argv=None) -> int:
     out = torch.empty((S, Hq, Wq, cfg.dv), dtype=Q.dtype, device=dev)
     T = cfg.iters
     per_run = 2 * (T + 1)  # events of one PatchMatch call: init, T sweeps
+    n_bwd_ev = 6 if args.backward else 0
+    if args.backward and args.snis:
+        print("bench.py: --backward applies to the window attention, not to --snis", file=sys.stderr)
+        return 2
+    dO = torch.randn((S, Hq, Wq, cfg.dv), generator=torch.Generator(device=dev).manual_seed(7), device=dev,
+                     dtype=torch.float32).to(Q.dtype) if args.backward else None
+    bwd_ws = torch.empty(scram.sparse_attend_backward_workspace_bytes(S, Hq, Wq, cfg.Hk, cfg.Wk, kappa),
+                         dtype=torch.uint8, device=dev) if args.backward else None
 
     def new_events():
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(kappa * per_run + 2)]
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(kappa * per_run + 2 + n_bwd_ev)]
         for e in evs:  # create the underlying HIP events before handing them to the library
             e.record(stream)
         return evs
@@ -189,12 +199,16 @@ def main(argv=None) -> int:
             scram.patchmatch(Q, K, T, cfg.pm_seed, prev=J[:c] if c else None, sep=sep, causal=causal, out=J[c],
                              workspace=ws, events=None if ev is None else ev[c * per_run:(c + 1) * per_run])
         maps = J if kappa > 1 else J[0]
+        a0 = kappa * per_run  # the attend step's events
         if args.snis:
             scram.snis_attend(Q, K, V, maps, args.snis, alpha=args.alpha, radius=args.radius, scale=cfg.scale,
-                              seed=cfg.pm_seed, causal=causal, out=out, events=None if ev is None else ev[-2:])
+                              seed=cfg.pm_seed, causal=causal, out=out, events=None if ev is None else ev[a0:a0 + 2])
         else:
             scram.sparse_attend(Q, K, V, maps, cfg.window, cfg.scale, causal=causal, out=out,
-                                events=None if ev is None else ev[-2:])
+                                events=None if ev is None else ev[a0:a0 + 2])
+        if args.backward:
+            scram.sparse_attend_backward(Q, K, V, maps, dO, cfg.window, cfg.scale, causal=causal,
+                                         workspace=bwd_ws, events=None if ev is None else ev[a0 + 2:a0 + 8])
 
     for _ in range(args.warmup):
         step()
@@ -226,6 +240,10 @@ def main(argv=None) -> int:
                    for c in range(kappa)]
     iter_ms = sum(iter_by_run) / kappa
     att_ms = sum(dur(ev, kappa * (T + 1)) for ev in events) / args.steps
+    bwd = {}
+    if args.backward:
+        for i, name in enumerate(("backward_inverse_map", "backward_query", "backward_key")):
+            bwd[name] = sum(dur(ev, kappa * (T + 1) + 1 + i) for ev in events) / args.steps
 
     nq = cfg.nq
     # the dominant kernel: the sweep, averaged over the runs (run c reads c previous maps)
@@ -263,6 +281,7 @@ def main(argv=None) -> int:
             "separation": sep,
             "causal": causal,
             "estimator": f"snis T={args.snis} alpha={args.alpha} m={args.radius}" if args.snis else "window",
+            "backward": args.backward,
             "queries_per_step": nq,
         },
         "roofline": {
@@ -276,7 +295,7 @@ def main(argv=None) -> int:
             "traffic_bytes_per_launch": traffic_bytes,
             "algorithmic_bytes_per_launch": pm_launch_bytes,
         },
-        "kernels_ms": {"pm_init": init_ms, "pm_iter": iter_ms, "attend": att_ms},
+        "kernels_ms": {"pm_init": init_ms, "pm_iter": iter_ms, "attend": att_ms, **bwd},
         "pm_iter_ms_by_run": iter_by_run,
         "kernels_ms_source": "dispatch-stamped HIP events, timed region B",
         "attend_GBps": att_bytes / (att_ms * 1e-3) / 1e9,

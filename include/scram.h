@@ -24,6 +24,9 @@
  * the union of the kappa windows, each key once.  SCRAM_CAUSAL (Section
  * 4.2.1) restricts both steps to keys at or before the query in raster order.
  *
+ * scram_sparse_attend_backward gives the gradients of step 2 with respect to
+ * Q, K and V with the maps held fixed.
+ *
  * scram_snis_attend replaces the window of step 2 by the self-normalised
  * importance-sampling estimator of Section 4.2 (Monte Carlo estimators,
  * Equations 11-17): T keys per query drawn from a mixture of local densities
@@ -202,6 +205,46 @@ int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype, 
                         uint32_t flags, void* out, hipEvent_t* events, hipStream_t stream);
 
 /*
+ * Backward of scram_sparse_attend with the maps held fixed (the key sets
+ * W_i depend only on argmax, window and flags, so they carry no gradient).
+ * With p_ij the softmax weights of query i over W_i, dp_ij = dO_i . v_j and
+ * D_i = sum_j p_ij dp_ij:
+ *   dQ_i = scale * sum_j p_ij (dp_ij - D_i) k_j
+ *   dK_j = scale * sum_i p_ij (dp_ij - D_i) q_i
+ *   dV_j = sum_i p_ij dO_i
+ * (the derivative of Equations 8-9).  fp32 throughout; the scores and
+ * weights are recomputed from Q, K, V (the forward output is not needed).
+ * Key j lies in W_i exactly when a match of query i lies in the
+ * (2b+1) x (2b+1) neighbourhood of j, so dK_j and dV_j gather over the
+ * queries found through the inverse of the maps (kept in the workspace).
+ * Every gradient row has a single writer; the order in which the queries of
+ * one match key are summed is the order the inverse map was filled in,
+ * which may differ between calls (dK, dV may differ in the last bits; dQ is
+ * deterministic).  A query with an empty set (causal only) contributes
+ * nothing and gets dQ = 0.
+ *
+ * Arguments: as scram_sparse_attend, plus
+ *   dO        [S, Hq, Wq, dv] in `dtype`: gradient of the output
+ *   dQ        fp32 [S, Hq, Wq, d] (written)
+ *   dK        fp32 [S, Hk, Wk, d] (written)
+ *   dV        fp32 [S, Hk, Wk, dv] (written)
+ *   workspace device scratch of at least
+ *             scram_sparse_attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk,
+ *             kappa) bytes, 256-byte aligned; contents undefined on return
+ *   events    NULL or 6 events: start/stop of building the inverse map, of
+ *             the per-query kernel and of the per-key kernel
+ * Also requires S*Hq*Wq*kappa < 2^31.  dQ, dK, dV must be 16-byte aligned;
+ * no output or the workspace may overlap an input or another output.
+ * Returns a status code.
+ */
+size_t scram_sparse_attend_backward_workspace_bytes(int S, int Hq, int Wq, int Hk, int Wk, int kappa);
+
+int scram_sparse_attend_backward(const void* Q, const void* K, const void* V, int dtype, const int32_t* argmax,
+                                 int kappa, int S, int Hq, int Wq, int Hk, int Wk, int d, int dv, int window,
+                                 float scale, uint32_t flags, const void* dO, float* dQ, float* dK, float* dV,
+                                 void* workspace, size_t workspace_bytes, hipEvent_t* events, hipStream_t stream);
+
+/*
  * Self-normalised importance sampling around the matches (Section 4.2,
  * Monte Carlo estimators, Equations 11-17).  For query i with matches
  * (u_e, v_e) = divmod(modes[e][i], Wk), e < kappa:
@@ -254,7 +297,7 @@ const char* scram_status_string(int status);
 /* ABI version of this header: (major << 16) | minor. */
 int scram_abi_version(void);
 
-#define SCRAM_ABI_VERSION ((2 << 16) | 1)
+#define SCRAM_ABI_VERSION ((2 << 16) | 3)
 
 #ifdef __cplusplus
 }

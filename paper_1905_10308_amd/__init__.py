@@ -19,5 +19,7 @@ from .binding import (  # noqa: F401
     patchmatch_workspace_bytes,
     snis_attend,
     sparse_attend,
+    sparse_attend_backward,
+    sparse_attend_backward_workspace_bytes,
     status_string,
 )

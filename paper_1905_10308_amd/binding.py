@@ -57,6 +57,11 @@ def lib() -> ctypes.CDLL:
     L.scram_patchmatch.restype = I
     L.scram_sparse_attend.argtypes = [P, P, P, I, P, I, I, I, I, I, I, I, I, I, ctypes.c_float, U32, P, P, P]
     L.scram_sparse_attend.restype = I
+    L.scram_sparse_attend_backward.argtypes = [P, P, P, I, P, I, I, I, I, I, I, I, I, I, ctypes.c_float, U32, P, P,
+                                               P, P, P, SZ, P, P]
+    L.scram_sparse_attend_backward.restype = I
+    L.scram_sparse_attend_backward_workspace_bytes.argtypes = [I, I, I, I, I, I]
+    L.scram_sparse_attend_backward_workspace_bytes.restype = SZ
     L.scram_snis_attend.argtypes = [P, P, P, I, P, I, I, I, I, I, I, I, I, I, ctypes.c_float, I, ctypes.c_float,
                                     U64, U32, P, P, P, P, P]
     L.scram_snis_attend.restype = I
@@ -220,6 +225,55 @@ def sparse_attend(Q, K, V, argmax, window: int, scale: float | None = None, *, c
     if rc != 0:
         raise ScramError(rc, "scram_sparse_attend")
     return out
+
+
+def sparse_attend_backward(Q, K, V, argmax, dO, window: int, scale: float | None = None, *, causal: bool = False,
+                           workspace=None, events=None):
+    """Gradients of ``sparse_attend`` with the maps held fixed (``scram_sparse_attend_backward``).
+
+    Returns fp32 ``(dQ [S,Hq,Wq,d], dK [S,Hk,Wk,d], dV [S,Hk,Wk,dv])``.
+    ``workspace``: optional uint8 device tensor of at least
+    ``sparse_attend_backward_workspace_bytes(...)`` bytes.
+    ``events``: optional 6 timing-enabled events (inverse map, query kernel, key kernel).
+    """
+    torch = _torch()
+    for name, t in (("Q", Q), ("K", K), ("V", V), ("dO", dO)):
+        _dev_tensor(t, name, 4)
+        if t.dtype != Q.dtype:
+            raise TypeError("Q, K, V, dO must share a dtype")
+    _dev_tensor(argmax, "argmax")
+    S, Hq, Wq, d = Q.shape
+    _, Hk, Wk, _ = K.shape
+    dv = V.shape[3]
+    if tuple(K.shape[:3]) != tuple(V.shape[:3]) or K.shape[0] != S or K.shape[3] != d:
+        raise ValueError("K and V must share the key grid; K must match Q's slices and channels")
+    if tuple(dO.shape) != (S, Hq, Wq, dv):
+        raise ValueError("dO must be [S, Hq, Wq, dv]")
+    if argmax.dtype != torch.int32 or tuple(argmax.shape[-3:]) != (S, Hq, Wq) or argmax.dim() not in (3, 4):
+        raise ValueError("argmax must be int32 [S, Hq, Wq] or [kappa, S, Hq, Wq]")
+    kappa = 1 if argmax.dim() == 3 else argmax.shape[0]
+    if scale is None:
+        scale = d ** -0.5
+    dev = Q.device
+    dQ = torch.empty((S, Hq, Wq, d), dtype=torch.float32, device=dev)
+    dK = torch.empty((S, Hk, Wk, d), dtype=torch.float32, device=dev)
+    dV = torch.empty((S, Hk, Wk, dv), dtype=torch.float32, device=dev)
+    need = sparse_attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, kappa)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    ev = None if events is None else _event_array(events, 6)
+    rc = lib().scram_sparse_attend_backward(_ptr(Q), _ptr(K), _ptr(V), _dtype_code(Q), _ptr(argmax), int(kappa), S,
+                                            Hq, Wq, Hk, Wk, d, dv, int(window), float(scale),
+                                            CAUSAL if causal else 0, _ptr(dO), _ptr(dQ), _ptr(dK), _ptr(dV),
+                                            _ptr(workspace), workspace.numel() * workspace.element_size(), ev,
+                                            _stream(dev))
+    if rc != 0:
+        raise ScramError(rc, "scram_sparse_attend_backward")
+    return dQ, dK, dV
+
+
+def sparse_attend_backward_workspace_bytes(S: int, Hq: int, Wq: int, Hk: int, Wk: int, kappa: int = 1) -> int:
+    return int(lib().scram_sparse_attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, kappa))
 
 
 def snis_attend(Q, K, V, modes, samples: int, *, alpha: float = 0.9, radius: int = 4, scale: float | None = None,

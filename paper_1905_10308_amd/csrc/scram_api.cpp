@@ -189,6 +189,54 @@ int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype, 
     return e == hipSuccess ? SCRAM_OK : SCRAM_ERR_HIP;
 }
 
+size_t scram_sparse_attend_backward_workspace_bytes(int S, int Hq, int Wq, int Hk, int Wk, int kappa)
+{
+    if (check_grid(S, Hq, Wq, Hk, Wk) || kappa < 1 || kappa > SCRAM_MAX_KAPPA) return 0;
+    return scram::attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, kappa);
+}
+
+int scram_sparse_attend_backward(const void* Q, const void* K, const void* V, int dtype, const int32_t* argmax,
+                                 int kappa, int S, int Hq, int Wq, int Hk, int Wk, int d, int dv, int window,
+                                 float scale, uint32_t flags, const void* dO, float* dQ, float* dK, float* dV,
+                                 void* workspace, size_t workspace_bytes, hipEvent_t* events, hipStream_t stream)
+{
+    if (!Q || !K || !V || !argmax || !dO || !dQ || !dK || !dV) return SCRAM_ERR_NULL;
+    int rc = check_grid(S, Hq, Wq, Hk, Wk);
+    if (rc) return rc;
+    // the inverse map codes (match, query) pairs as e * n + i in an int32
+    if (int64_t(S) * Hq * Wq * (kappa < 1 ? 1 : kappa) >= kMaxCount) return SCRAM_ERR_SHAPE;
+    if (window < 1 || window % 2 == 0 || window > 32767) return SCRAM_ERR_SHAPE;
+    if (kappa < 1 || kappa > SCRAM_MAX_KAPPA) return SCRAM_ERR_SHAPE;
+    if (!isfinite(scale)) return SCRAM_ERR_SHAPE;
+    if ((rc = check_type(dtype, d))) return rc;
+    if (dv != d) return SCRAM_ERR_UNSUPPORTED;
+    if (flags & ~uint32_t(SCRAM_CAUSAL)) return SCRAM_ERR_UNSUPPORTED;
+    const bool causal = (flags & SCRAM_CAUSAL) != 0;
+    if (causal && (Hq != Hk || Wq != Wk)) return SCRAM_ERR_SHAPE;
+    if (!workspace) return SCRAM_ERR_WORKSPACE;
+    if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(dO, 16) || !aligned(argmax, 4) ||
+        !aligned(dQ, 16) || !aligned(dK, 16) || !aligned(dV, 16) || !aligned(workspace, 256))
+        return SCRAM_ERR_ALIGN;
+    const size_t need = scram::attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, kappa);
+    if (workspace_bytes < need) return SCRAM_ERR_WORKSPACE;
+    const size_t n = size_t(S) * Hq * Wq, nk = size_t(S) * Hk * Wk, eb = elem_bytes(dtype);
+    const Range rQ = range(dQ, 4 * n * d), rK = range(dK, 4 * nk * d), rV = range(dV, 4 * nk * dv);
+    const Range rW = range(workspace, need);
+    for (const Range& o : {rQ, rK, rV, rW}) {
+        for (const Range& other : {range(Q, n * d * eb), range(K, nk * d * eb), range(V, nk * dv * eb),
+                                   range(argmax, 4 * n * size_t(kappa)), range(dO, n * dv * eb)}) {
+            if (overlap(o, other)) return SCRAM_ERR_ALIAS;
+        }
+    }
+    if (overlap(rQ, rK) || overlap(rQ, rV) || overlap(rK, rV) || overlap(rW, rQ) || overlap(rW, rK) ||
+        overlap(rW, rV))
+        return SCRAM_ERR_ALIAS;
+    const scram::Grid grid{S, Hq, Wq, Hk, Wk, d};
+    const hipError_t e = scram::launch_attend_backward(dtype, Q, K, V, argmax, kappa, grid, window, scale, causal, dO,
+                                                       dQ, dK, dV, workspace, stream, events);
+    return e == hipSuccess ? SCRAM_OK : SCRAM_ERR_HIP;
+}
+
 int scram_snis_attend(const void* Q, const void* K, const void* V, int dtype, const int32_t* modes, int kappa, int S,
                       int Hq, int Wq, int Hk, int Wk, int d, int dv, int samples, float alpha, int radius, float scale,
                       uint64_t seed, uint32_t flags, void* out, float* ess_out, float* var_out, hipEvent_t* events,

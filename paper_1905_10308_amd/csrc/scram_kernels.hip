@@ -606,6 +606,26 @@ __device__ __forceinline__ void accumulate_row(float* acc, float pj, const uint4
     }
 }
 
+// The lane's channels of one value row as floats (the channel order of
+// accumulate_row).
+template <typename T, int CH>
+__device__ __forceinline__ void unpack_row(const uint4 (&vr)[CH], float* out)
+{
+#pragma unroll
+    for (int cc = 0; cc < CH; ++cc) {
+        const uint32_t w[4] = {vr[cc].x, vr[cc].y, vr[cc].z, vr[cc].w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if constexpr (std::is_same<T, uint16_t>::value) {
+                out[cc * 8 + 2 * i] = __uint_as_float(w[i] << 16);
+                out[cc * 8 + 2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+            } else {
+                out[cc * 4 + i] = __uint_as_float(w[i]);
+            }
+        }
+    }
+}
+
 // out row slice = acc * inv in the storage type.
 template <typename T, int D, int G>
 __device__ __forceinline__ void store_row(void* out, uint32_t g, int lane, const float* acc, float inv)
@@ -648,7 +668,8 @@ struct WindowSet {
     }
 };
 
-__device__ __forceinline__ WindowSet make_window_set(const AttParams& p, uint32_t g, uint32_t rem)
+template <typename P>
+__device__ __forceinline__ WindowSet make_window_set(const P& p, uint32_t g, uint32_t rem)
 {
     WindowSet ws;
     ws.kappa = p.kappa;
@@ -852,6 +873,377 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
 }
 
 // ---------------------------------------------------------------------------
+// K6: backward of the sparse attention, maps held fixed
+//
+// For query i with key set W_i (as in the forward), p_ij its softmax
+// weights, dp_ij = dO_i . v_j and D_i = sum_j p_ij dp_ij:
+//   dQ_i = scale sum_j p_ij (dp_ij - D_i) k_j
+//   dK_j = scale sum_i p_ij (dp_ij - D_i) q_i,   dV_j = sum_i p_ij dO_i
+// Query side (one lane group per query): pass A walks W_i for the running
+// max, the normaliser and D_i and stores log2 of the normaliser (with the
+// max) and D_i; pass B walks it again for dQ_i.  Key side (one lane group
+// per key): key j lies in W_i exactly when a match of i lies in the
+// (2b+1)^2 neighbourhood of j, so the queries are found through the inverse
+// map -- the (query, match) entries sorted by match key (a counting sort).
+// The keys of one neighbourhood row are consecutive, so their entries form
+// one contiguous range.  No float atomics: every gradient row has one
+// writer.
+// ---------------------------------------------------------------------------
+constexpr int kScanItems = 8;                          // counts per thread in the scan
+constexpr int kScanTile = kBlock * kScanItems;         // counts per scan block
+
+struct BwdParams {
+    const void* Q;
+    const void* K;
+    const void* V;
+    const int32_t* J;      // [kappa, n]
+    const void* dO;
+    float* dQ;
+    float* dK;
+    float* dV;
+    float* lse2;           // [n] max + log2(normaliser), base-2 scores
+    float* Dq;             // [n] D_i
+    const int32_t* offsets;  // [S * nkeys + 1] start of each key's entries
+    const int32_t* entries;  // [kappa * n] e * n + i, grouped by match key
+    uint32_t n;
+    uint32_t keys_total;   // S * nkeys
+    int Hq, Wq, Hk, Wk;
+    uint32_t nkeys;
+    Div div_plane, div_wk, div_n, div_keys;
+    int b;
+    float scale;
+    float scale_log2e;
+    int kappa;
+    int causal;
+};
+
+__global__ __launch_bounds__(kBlock) void zero_i32_kernel(int32_t* a, size_t count)
+{
+    for (size_t i = static_cast<size_t>(blockIdx.x) * kBlock + threadIdx.x; i < count;
+         i += static_cast<size_t>(gridDim.x) * kBlock)
+        a[i] = 0;
+}
+
+// counts[s * nkeys + J[e][i]] += 1 for every (query, match)
+__global__ __launch_bounds__(kBlock) void bwd_count_kernel(BwdParams p, int32_t* counts)
+{
+    const size_t total = static_cast<size_t>(p.kappa) * p.n;
+    for (size_t x = static_cast<size_t>(blockIdx.x) * kBlock + threadIdx.x; x < total;
+         x += static_cast<size_t>(gridDim.x) * kBlock) {
+        const uint32_t g = static_cast<uint32_t>(x % p.n);
+        const uint32_t s = g / (static_cast<uint32_t>(p.Hq) * p.Wq);
+        atomicAdd(counts + static_cast<size_t>(s) * p.nkeys + clamp_index(p.J[x], p.nkeys), 1);
+    }
+}
+
+// Exclusive scan, step 1: each block scans a tile of kScanTile counts into
+// out (tile-local prefixes) and writes the tile's total to sums[tile].
+__global__ __launch_bounds__(kBlock) void scan_tiles_kernel(const int32_t* in, int32_t* out, int32_t* sums, size_t count)
+{
+    __shared__ int32_t wave_tot[kBlock / 64];
+    const size_t base = static_cast<size_t>(blockIdx.x) * kScanTile + static_cast<size_t>(threadIdx.x) * kScanItems;
+    int32_t v[kScanItems];
+    int32_t run = 0;
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        v[i] = base + i < count ? in[base + i] : 0;
+        const int32_t x = v[i];
+        v[i] = run;  // exclusive within the thread
+        run += x;
+    }
+    // exclusive prefix of the thread totals: within the wave, then across waves
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int32_t incl = run;
+#pragma unroll
+    for (int k = 1; k < 64; k <<= 1) {
+        const int32_t y = __shfl_up(incl, k, 64);
+        if (lane >= k) incl += y;
+    }
+    if (lane == 63) wave_tot[wave] = incl;
+    __syncthreads();
+    int32_t before = incl - run;
+    for (int w = 0; w < wave; ++w) before += wave_tot[w];
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i)
+        if (base + i < count) out[base + i] = before + v[i];
+    if (threadIdx.x == kBlock - 1) {
+        int32_t tot = 0;
+        for (int w = 0; w < kBlock / 64; ++w) tot += wave_tot[w];
+        sums[blockIdx.x] = tot;
+    }
+}
+
+// Exclusive scan, step 2 (one block): sums[0..tiles) in place, total in sums[tiles].
+__global__ __launch_bounds__(kBlock) void scan_sums_kernel(int32_t* sums, uint32_t tiles)
+{
+    __shared__ int32_t wave_tot[kBlock / 64];
+    __shared__ int32_t carry_s;
+    if (threadIdx.x == 0) carry_s = 0;
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    for (uint32_t c0 = 0; c0 < tiles; c0 += kBlock) {
+        const uint32_t i = c0 + threadIdx.x;
+        const int32_t x = i < tiles ? sums[i] : 0;
+        int32_t incl = x;
+#pragma unroll
+        for (int k = 1; k < 64; k <<= 1) {
+            const int32_t y = __shfl_up(incl, k, 64);
+            if (lane >= k) incl += y;
+        }
+        if (lane == 63) wave_tot[wave] = incl;
+        __syncthreads();
+        int32_t before = carry_s + incl - x;
+        for (int w = 0; w < wave; ++w) before += wave_tot[w];
+        if (i < tiles) sums[i] = before;
+        __syncthreads();  // every thread has read carry_s and wave_tot
+        if (threadIdx.x == kBlock - 1) carry_s = before + x;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) sums[tiles] = carry_s;
+}
+
+// Exclusive scan, step 3: add each tile's offset; out[count] = total.
+__global__ __launch_bounds__(kBlock) void scan_add_kernel(int32_t* out, const int32_t* sums, size_t count,
+                                                          uint32_t tiles)
+{
+    const size_t base = static_cast<size_t>(blockIdx.x) * kScanTile;
+    const int32_t add = sums[blockIdx.x];
+    for (int i = threadIdx.x; i < kScanTile; i += kBlock)
+        if (base + i < count) out[base + i] += add;
+    if (blockIdx.x == 0 && threadIdx.x == 0) out[count] = sums[tiles];
+}
+
+// entries[offsets[key] + (a slot of that key)] = e * n + i; counts end at 0
+__global__ __launch_bounds__(kBlock) void bwd_fill_kernel(BwdParams p, int32_t* counts, int32_t* entries)
+{
+    const size_t total = static_cast<size_t>(p.kappa) * p.n;
+    for (size_t x = static_cast<size_t>(blockIdx.x) * kBlock + threadIdx.x; x < total;
+         x += static_cast<size_t>(gridDim.x) * kBlock) {
+        const uint32_t g = static_cast<uint32_t>(x % p.n);
+        const uint32_t s = g / (static_cast<uint32_t>(p.Hq) * p.Wq);
+        const size_t key = static_cast<size_t>(s) * p.nkeys + clamp_index(p.J[x], p.nkeys);
+        const int32_t slot = atomicSub(counts + key, 1) - 1;
+        entries[p.offsets[key] + slot] = static_cast<int32_t>(x);
+    }
+}
+
+template <typename T, int D, int G, bool MULTI>
+__global__ __launch_bounds__(kBlock) void bwd_query_kernel(BwdParams p)
+{
+    using RW = Row<T, D, G>;
+    constexpr int CH = RW::kCh;
+    constexpr int E = CH * RW::kEpc;
+    constexpr int kEpc = RW::kEpc;
+    constexpr int kNb = CH >= 2 ? 4 : 8;
+    const int lane = threadIdx.x & (G - 1);
+    const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+    const uint32_t g = blk * RW::kQpb + threadIdx.x / G;
+    if (g >= p.n) return;
+
+    uint32_t s, rem;
+    divmod(g, p.div_plane, s, rem);
+    const size_t slice = static_cast<size_t>(s) * p.nkeys * D;
+    const T* Ks = static_cast<const T*>(p.K) + slice;
+    const T* Vs = static_cast<const T*>(p.V) + slice;
+    uint4 q[CH], go[CH];
+    load_row<T, D, G>(static_cast<const T*>(p.Q), g, lane, q);
+    load_row<T, D, G>(static_cast<const T*>(p.dO), g, lane, go);
+    WindowSet wset;
+    if constexpr (MULTI) wset = make_window_set(p, g, rem);
+    const int nsets = MULTI ? p.kappa : 1;
+
+    // visit(fn): every key of the set, kNb at a time with their key and
+    // value rows loaded together; fn(ok[], kr, vr) per batch
+    auto visit = [&](auto&& fn) {
+        for (int e = 0; e < nsets; ++e) {
+            uint32_t u, v;
+            if constexpr (MULTI) {
+                u = static_cast<uint32_t>(wset.cu[0]);
+                v = static_cast<uint32_t>(wset.cv[0]);
+#pragma unroll
+                for (int f = 1; f < kMaxKappa; ++f)
+                    if (f == e) {
+                        u = static_cast<uint32_t>(wset.cu[f]);
+                        v = static_cast<uint32_t>(wset.cv[f]);
+                    }
+            } else {
+                divmod(static_cast<uint32_t>(clamp_index(p.J[g], p.nkeys)), p.div_wk, u, v);
+            }
+            const int r0 = max(static_cast<int>(u) - p.b, 0), r1 = min(static_cast<int>(u) + p.b, p.Hk - 1);
+            const int c0 = max(static_cast<int>(v) - p.b, 0), c1 = min(static_cast<int>(v) + p.b, p.Wk - 1);
+            const int nwin = (r1 - r0 + 1) * (c1 - c0 + 1);
+            const uint32_t centre = u * p.Wk + v;
+            int r = r0, c = c0;
+            for (int k0 = 0; k0 < nwin; k0 += kNb) {
+                uint4 kr[kNb][CH], vr[kNb][CH];
+                bool ok[kNb];
+#pragma unroll
+                for (int j = 0; j < kNb; ++j) {
+                    ok[j] = k0 + j < nwin;
+                    if constexpr (MULTI) ok[j] = ok[j] && !wset.skip(e, r, c);
+                    const uint32_t row = k0 + j < nwin ? static_cast<uint32_t>(r * p.Wk + c) : centre;
+                    load_row<T, D, G>(Ks, row, lane, kr[j]);
+                    load_row<T, D, G>(Vs, row, lane, vr[j]);
+                    if (k0 + j < nwin && ++c > c1) {
+                        c = c0;
+                        ++r;
+                    }
+                }
+                fn(ok, kr, vr);
+            }
+        }
+    };
+
+    // pass A: running max m, normaliser l, sum of e^(a - m) dp (base-2 scores)
+    float m = -INFINITY, l = 0.f, dn = 0.f;
+    visit([&](const bool (&ok)[kNb], const uint4 (&kr)[kNb][CH], const uint4 (&vr)[kNb][CH]) {
+        float sc[kNb], dp[kNb];
+        float mb = m;
+#pragma unroll
+        for (int j = 0; j < kNb; ++j) {
+            sc[j] = ok[j] ? row_score<T, D, G>(q, kr[j]) * p.scale_log2e : -INFINITY;
+            dp[j] = row_score<T, D, G>(go, vr[j]);
+            mb = fmaxf(mb, sc[j]);
+        }
+        if (mb == -INFINITY) return;
+        const float alpha = __builtin_amdgcn_exp2f(m - mb);
+        l *= alpha;
+        dn *= alpha;
+#pragma unroll
+        for (int j = 0; j < kNb; ++j) {
+            const float pj = __builtin_amdgcn_exp2f(sc[j] - mb);
+            l += pj;
+            dn = fmaf(pj, dp[j], dn);
+        }
+        m = mb;
+    });
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+    const float Dg = dn * inv;
+    if (lane == 0) {
+        p.lse2[g] = l > 0.f ? m + log2f(l) : INFINITY;  // +inf: every weight is 0
+        p.Dq[g] = Dg;
+    }
+
+    // pass B: dQ with the exact weights
+    float dq[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) dq[e] = 0.f;
+    if (l > 0.f) {
+        visit([&](const bool (&ok)[kNb], const uint4 (&kr)[kNb][CH], const uint4 (&vr)[kNb][CH]) {
+#pragma unroll
+            for (int j = 0; j < kNb; ++j) {
+                const float sc = ok[j] ? row_score<T, D, G>(q, kr[j]) * p.scale_log2e : -INFINITY;
+                const float dp = row_score<T, D, G>(go, vr[j]);
+                const float ds = __builtin_amdgcn_exp2f(sc - m) * inv * (dp - Dg);  // 0 when !ok
+                float kf[E];
+                unpack_row<T, CH>(kr[j], kf);
+#pragma unroll
+                for (int e = 0; e < E; ++e) dq[e] = fmaf(ds, kf[e], dq[e]);
+            }
+        });
+    }
+#pragma unroll
+    for (int cc = 0; cc < CH; ++cc) {
+        float4* o = reinterpret_cast<float4*>(p.dQ + static_cast<size_t>(g) * D + (cc * G + lane) * kEpc);
+#pragma unroll
+        for (int i = 0; i < kEpc / 4; ++i)
+            o[i] = make_float4(dq[cc * kEpc + 4 * i] * p.scale, dq[cc * kEpc + 4 * i + 1] * p.scale,
+                               dq[cc * kEpc + 4 * i + 2] * p.scale, dq[cc * kEpc + 4 * i + 3] * p.scale);
+    }
+}
+
+// One lane group per key j of slice s: sum over the entries (i, e) whose
+// match e lies in the neighbourhood of j (so j is in window e of i), each
+// query once (its first such window), causal pairs only.
+template <typename T, int D, int G>
+__global__ __launch_bounds__(kBlock) void bwd_key_kernel(BwdParams p)
+{
+    using RW = Row<T, D, G>;
+    constexpr int CH = RW::kCh;
+    constexpr int E = CH * RW::kEpc;
+    constexpr int kEpc = RW::kEpc;
+    constexpr int kNb = CH >= 2 ? 4 : 8;
+    const int lane = threadIdx.x & (G - 1);
+    const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+    const uint32_t kg = blk * RW::kQpb + threadIdx.x / G;  // global key id s * nkeys + j
+    if (kg >= p.keys_total) return;
+    uint32_t s, j;
+    divmod(kg, p.div_keys, s, j);
+    uint32_t ju, jv;
+    divmod(j, p.div_wk, ju, jv);
+    const size_t krow = static_cast<size_t>(s) * p.nkeys + j;
+    uint4 kj[CH], vj[CH];
+    load_row<T, D, G>(static_cast<const T*>(p.K), static_cast<uint32_t>(krow), lane, kj);
+    load_row<T, D, G>(static_cast<const T*>(p.V), static_cast<uint32_t>(krow), lane, vj);
+
+    float dk[E], dv[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) dk[e] = dv[e] = 0.f;
+    const int r0 = max(static_cast<int>(ju) - p.b, 0), r1 = min(static_cast<int>(ju) + p.b, p.Hk - 1);
+    const int c0 = max(static_cast<int>(jv) - p.b, 0), c1 = min(static_cast<int>(jv) + p.b, p.Wk - 1);
+    const size_t sbase = static_cast<size_t>(s) * p.nkeys;
+    for (int r = r0; r <= r1; ++r) {
+        const int lo = p.offsets[sbase + static_cast<size_t>(r) * p.Wk + c0];
+        const int hi = p.offsets[sbase + static_cast<size_t>(r) * p.Wk + c1 + 1];
+        for (int x0 = lo; x0 < hi; x0 += kNb) {
+            uint4 qr[kNb][CH], gr[kNb][CH];
+            bool ok[kNb];
+            uint32_t gq[kNb];
+#pragma unroll
+            for (int t = 0; t < kNb; ++t) {
+                const int x = x0 + t;
+                uint32_t e = 0, g = 0;
+                ok[t] = x < hi;
+                if (ok[t]) divmod(static_cast<uint32_t>(p.entries[x]), p.div_n, e, g);
+                // the pair counts once: through the query's first window holding j
+                for (int f = 0; f < static_cast<int>(e) && ok[t]; ++f) {
+                    uint32_t fu, fv;
+                    divmod(static_cast<uint32_t>(clamp_index(p.J[static_cast<size_t>(f) * p.n + g], p.nkeys)),
+                           p.div_wk, fu, fv);
+                    if (abs(static_cast<int>(fu) - static_cast<int>(ju)) <= p.b &&
+                        abs(static_cast<int>(fv) - static_cast<int>(jv)) <= p.b)
+                        ok[t] = false;
+                }
+                if (ok[t] && p.causal) {
+                    uint32_t gs, grem;
+                    divmod(g, p.div_plane, gs, grem);
+                    ok[t] = j <= grem;
+                }
+                gq[t] = g;
+                load_row<T, D, G>(static_cast<const T*>(p.Q), g, lane, qr[t]);
+                load_row<T, D, G>(static_cast<const T*>(p.dO), g, lane, gr[t]);
+            }
+#pragma unroll
+            for (int t = 0; t < kNb; ++t) {
+                const float sc = row_score<T, D, G>(qr[t], kj) * p.scale_log2e;
+                const float dp = row_score<T, D, G>(gr[t], vj);
+                const float pj = ok[t] ? __builtin_amdgcn_exp2f(sc - p.lse2[gq[t]]) : 0.f;
+                const float ds = pj * (dp - p.Dq[gq[t]]);
+                float qf[E], gf[E];
+                unpack_row<T, CH>(qr[t], qf);
+                unpack_row<T, CH>(gr[t], gf);
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    dk[e] = fmaf(ds, qf[e], dk[e]);
+                    dv[e] = fmaf(pj, gf[e], dv[e]);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int cc = 0; cc < CH; ++cc) {
+        float4* ok_ = reinterpret_cast<float4*>(p.dK + krow * D + (cc * G + lane) * kEpc);
+        float4* ov = reinterpret_cast<float4*>(p.dV + krow * D + (cc * G + lane) * kEpc);
+#pragma unroll
+        for (int i = 0; i < kEpc / 4; ++i) {
+            const int e0 = cc * kEpc + 4 * i;
+            ok_[i] = make_float4(dk[e0] * p.scale, dk[e0 + 1] * p.scale, dk[e0 + 2] * p.scale, dk[e0 + 3] * p.scale);
+            ov[i] = make_float4(dv[e0], dv[e0 + 1], dv[e0 + 2], dv[e0 + 3]);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // K5: self-normalised importance sampling (Section 4.2, Equations 11-17)
 //
 // Importance distribution of query i: with probability alpha a mode m of
@@ -937,26 +1329,6 @@ __device__ __forceinline__ void snis_draw(const SnisParams& p, uint32_t g, uint3
         if (e < p.kappa)
             local += axis_density(r, cu[e], p.Hk, p.m, pmf, cdf) * axis_density(c, cv[e], p.Wk, p.m, pmf, cdf);
     lr2 = log2f(fmaf(p.w_local, local, p.w_unif));
-}
-
-// The lane's channels of one value row as floats (the channel order of
-// accumulate_row).
-template <typename T, int CH>
-__device__ __forceinline__ void unpack_row(const uint4 (&vr)[CH], float* out)
-{
-#pragma unroll
-    for (int cc = 0; cc < CH; ++cc) {
-        const uint32_t w[4] = {vr[cc].x, vr[cc].y, vr[cc].z, vr[cc].w};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            if constexpr (std::is_same<T, uint16_t>::value) {
-                out[cc * 8 + 2 * i] = __uint_as_float(w[i] << 16);
-                out[cc * 8 + 2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
-            } else {
-                out[cc * 4 + i] = __uint_as_float(w[i]);
-            }
-        }
-    }
 }
 
 template <typename T, int D, int G, bool VAR>
@@ -1107,15 +1479,21 @@ __global__ __launch_bounds__(kBlock) void snis_kernel(SnisParams p)
 // ---------------------------------------------------------------------------
 // host-side launch helpers
 // ---------------------------------------------------------------------------
-// Launch with the dispatch stamping optional start/stop events.
-template <typename P>
-hipError_t launch(void (*kernel)(P), uint32_t blocks, hipStream_t st, hipEvent_t start, hipEvent_t stop,
-                  const P& p)
+// Launch with the dispatch stamping optional start/stop events (the kernel's
+// parameter types fix the argument types).
+template <typename T>
+struct NoDeduce {
+    using type = T;
+};
+
+template <typename... A>
+hipError_t launch(void (*kernel)(A...), uint32_t blocks, hipStream_t st, hipEvent_t start, hipEvent_t stop,
+                  typename NoDeduce<A>::type... args)
 {
     if (start || stop)
-        hipExtLaunchKernelGGL(kernel, dim3(blocks), dim3(kBlock), 0, st, start, stop, 0, p);
+        hipExtLaunchKernelGGL(kernel, dim3(blocks), dim3(kBlock), 0, st, start, stop, 0, args...);
     else
-        hipLaunchKernelGGL(kernel, dim3(blocks), dim3(kBlock), 0, st, p);
+        hipLaunchKernelGGL(kernel, dim3(blocks), dim3(kBlock), 0, st, args...);
     return hipGetLastError();
 }
 
@@ -1203,6 +1581,20 @@ hipError_t run_attend(const AttParams& p, int window, hipStream_t st, hipEvent_t
     const uint32_t blocks = (p.n + Row<T, D, G>::kQpb - 1) / Row<T, D, G>::kQpb;
     if (p.kappa > 1 || p.causal) return run_attend_m<T, D, true>(p, window, blocks, st, e0, e1);
     return run_attend_m<T, D, false>(p, window, blocks, st, e0, e1);
+}
+
+template <typename T, int D>
+hipError_t run_backward(const BwdParams& p, hipStream_t st, hipEvent_t* ev)
+{
+    constexpr int G = Lanes<T, D>::kAttend;
+    const uint32_t qblocks = (p.n + Row<T, D, G>::kQpb - 1) / Row<T, D, G>::kQpb;
+    const uint32_t kblocks = (p.keys_total + Row<T, D, G>::kQpb - 1) / Row<T, D, G>::kQpb;
+    hipEvent_t q0 = ev ? ev[2] : nullptr, q1 = ev ? ev[3] : nullptr, k0 = ev ? ev[4] : nullptr,
+               k1 = ev ? ev[5] : nullptr;
+    hipError_t e = (p.kappa > 1 || p.causal) ? launch(bwd_query_kernel<T, D, G, true>, qblocks, st, q0, q1, p)
+                                             : launch(bwd_query_kernel<T, D, G, false>, qblocks, st, q0, q1, p);
+    if (e != hipSuccess) return e;
+    return launch(bwd_key_kernel<T, D, G>, kblocks, st, k0, k1, p);
 }
 
 template <typename T, int D>
@@ -1294,6 +1686,89 @@ hipError_t launch_attend(int dtype, const void* Q, const void* K, const void* V,
     p.causal = causal ? 1 : 0;
     return dispatch(dtype, g.d, [&](auto ty, auto d) {
         return run_attend<decltype(ty), decltype(d)::value>(p, window, stream, start, stop);
+    });
+}
+
+size_t attend_backward_workspace_bytes(int S, int Hq, int Wq, int Hk, int Wk, int kappa)
+{
+    const size_t n = static_cast<size_t>(S) * Hq * Wq, N = static_cast<size_t>(S) * Hk * Wk;
+    const size_t tiles = (N + kScanTile - 1) / kScanTile;
+    auto r256 = [](size_t b) { return (b + 255) & ~static_cast<size_t>(255); };
+    return r256(4 * N) + r256(4 * (N + 1)) + r256(4 * (tiles + 1)) + r256(4 * n * kappa) + 2 * r256(4 * n);
+}
+
+hipError_t launch_attend_backward(int dtype, const void* Q, const void* K, const void* V, const int32_t* J, int kappa,
+                                  const Grid& g, int window, float scale, bool causal, const void* dO, float* dQ,
+                                  float* dK, float* dV, void* workspace, hipStream_t stream, hipEvent_t* events)
+{
+    BwdParams p{};
+    p.Q = Q;
+    p.K = K;
+    p.V = V;
+    p.J = J;
+    p.dO = dO;
+    p.dQ = dQ;
+    p.dK = dK;
+    p.dV = dV;
+    p.n = static_cast<uint32_t>(g.S) * g.Hq * g.Wq;
+    p.Hq = g.Hq;
+    p.Wq = g.Wq;
+    p.Hk = g.Hk;
+    p.Wk = g.Wk;
+    p.nkeys = static_cast<uint32_t>(g.Hk) * g.Wk;
+    p.keys_total = static_cast<uint32_t>(g.S) * p.nkeys;
+    p.div_plane = make_div(static_cast<uint32_t>(g.Hq) * g.Wq);
+    p.div_wk = make_div(g.Wk);
+    p.div_n = make_div(p.n);
+    p.div_keys = make_div(p.nkeys);
+    p.b = window / 2;
+    p.scale = scale;
+    p.scale_log2e = scale * 1.4426950408889634f;
+    p.kappa = kappa;
+    p.causal = causal ? 1 : 0;
+
+    // workspace: counts, offsets, tile sums, entries, log2 normalisers, D
+    const size_t N = p.keys_total;
+    const uint32_t tiles = static_cast<uint32_t>((N + kScanTile - 1) / kScanTile);
+    auto r256 = [](size_t b) { return (b + 255) & ~static_cast<size_t>(255); };
+    char* w = static_cast<char*>(workspace);
+    int32_t* counts = reinterpret_cast<int32_t*>(w);
+    w += r256(4 * N);
+    int32_t* offsets = reinterpret_cast<int32_t*>(w);
+    w += r256(4 * (N + 1));
+    int32_t* sums = reinterpret_cast<int32_t*>(w);
+    w += r256(4 * (static_cast<size_t>(tiles) + 1));
+    int32_t* entries = reinterpret_cast<int32_t*>(w);
+    w += r256(4 * static_cast<size_t>(p.n) * kappa);
+    p.lse2 = reinterpret_cast<float*>(w);
+    w += r256(4 * static_cast<size_t>(p.n));
+    p.Dq = reinterpret_cast<float*>(w);
+    p.offsets = offsets;
+    p.entries = entries;
+
+    auto grid_for = [](size_t items) {
+        const size_t b = (items + kBlock - 1) / kBlock;
+        return static_cast<uint32_t>(b < 1 ? 1 : (b > 4096 ? 4096 : b));
+    };
+    hipEvent_t e0 = events ? events[0] : nullptr, e1 = events ? events[1] : nullptr;
+    const size_t entries_total = static_cast<size_t>(p.n) * kappa;
+    hipError_t e;
+    // inverse map: counting sort of the (query, match) entries by match key
+    if ((e = launch(zero_i32_kernel, grid_for(N), stream, e0, nullptr, counts, N)) != hipSuccess) return e;
+    if ((e = launch(bwd_count_kernel, grid_for(entries_total), stream, nullptr, nullptr, p, counts)) != hipSuccess)
+        return e;
+    if ((e = launch(scan_tiles_kernel, tiles, stream, nullptr, nullptr, static_cast<const int32_t*>(counts), offsets,
+                    sums, N)) != hipSuccess)
+        return e;
+    if ((e = launch(scan_sums_kernel, 1u, stream, nullptr, nullptr, sums, tiles)) != hipSuccess) return e;
+    if ((e = launch(scan_add_kernel, tiles, stream, nullptr, nullptr, offsets, static_cast<const int32_t*>(sums), N,
+                    tiles)) != hipSuccess)
+        return e;
+    if ((e = launch(bwd_fill_kernel, grid_for(entries_total), stream, nullptr, e1, p, counts, entries)) != hipSuccess)
+        return e;
+    // gradients
+    return dispatch(dtype, g.d, [&](auto ty, auto d) {
+        return run_backward<decltype(ty), decltype(d)::value>(p, stream, events);
     });
 }
 

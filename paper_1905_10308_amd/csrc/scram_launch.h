@@ -40,6 +40,15 @@ hipError_t launch_attend(int dtype, const void* Q, const void* K, const void* V,
                          const Grid& g, int window, float scale, bool causal, void* out, hipStream_t stream,
                          hipEvent_t start, hipEvent_t stop);
 
+// Gradients of the attend step with the maps held fixed.  The workspace
+// (attend_backward_workspace_bytes) holds the inverse map and per-query
+// softmax statistics.  events: null or 6 (inverse map start/stop, query
+// kernel start/stop, key kernel start/stop).
+size_t attend_backward_workspace_bytes(int S, int Hq, int Wq, int Hk, int Wk, int kappa);
+hipError_t launch_attend_backward(int dtype, const void* Q, const void* K, const void* V, const int32_t* J, int kappa,
+                                  const Grid& g, int window, float scale, bool causal, const void* dO, float* dQ,
+                                  float* dK, float* dV, void* workspace, hipStream_t stream, hipEvent_t* events);
+
 // Self-normalised importance sampling around the kappa maps in modes
 // ([kappa, n]): samples per query, mixture weight, binomial radius m,
 // softmax scale and Philox seed.

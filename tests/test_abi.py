@@ -40,7 +40,8 @@ def declared_functions():
 
 def test_header_declares_entry_points():
     names = declared_functions()
-    for n in ("scram_patchmatch", "scram_sparse_attend", "scram_snis_attend", "scram_patchmatch_workspace_bytes",
+    for n in ("scram_patchmatch", "scram_sparse_attend", "scram_snis_attend", "scram_sparse_attend_backward",
+              "scram_patchmatch_workspace_bytes",
               "scram_status_string", "scram_abi_version"):
         assert n in names
 
@@ -51,7 +52,7 @@ def test_library_exports_every_declared_symbol(L):
 
 
 def test_abi_version(L):
-    assert L.scram_abi_version() == (2 << 16) | 1
+    assert L.scram_abi_version() == (2 << 16) | 3
 
 
 def test_status_strings(L):
@@ -157,6 +158,50 @@ def sn(L, **kw):
 ])
 def test_snis_rejects(L, kw, code):
     assert sn(L, **kw) == code
+
+
+A_DO, A_DQ, A_DK, A_DV, A_BW = (0x10000000 * (13 + i) for i in range(5))
+
+
+def bw(L, **kw):
+    a = dict(Q=A_Q, K=A_K, V=A_V, dtype=BF16, J=A_J, kappa=1, S=2, Hq=8, Wq=8, Hk=8, Wk=8, d=16, dv=16, window=3,
+             scale=0.25, flags=0, dO=A_DO, dQ=A_DQ, dK=A_DK, dV=A_DV, ws=A_BW, ws_bytes=1 << 20)
+    a.update(kw)
+    return L.scram_sparse_attend_backward(a["Q"], a["K"], a["V"], a["dtype"], a["J"], a["kappa"], a["S"], a["Hq"],
+                                          a["Wq"], a["Hk"], a["Wk"], a["d"], a["dv"], a["window"], a["scale"],
+                                          a["flags"], a["dO"], a["dQ"], a["dK"], a["dV"], a["ws"], a["ws_bytes"],
+                                          None, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(Q=None), ENULL), (dict(dO=None), ENULL), (dict(dQ=None), ENULL), (dict(dK=None), ENULL),
+    (dict(dV=None), ENULL), (dict(J=None), ENULL),
+    (dict(window=2), ESHAPE), (dict(kappa=0), ESHAPE), (dict(kappa=9), ESHAPE), (dict(scale=float("nan")), ESHAPE),
+    (dict(Hq=0), ESHAPE), (dict(flags=CAUSAL, Hk=9), ESHAPE),
+    (dict(d=20), EUNSUP), (dict(dv=64), EUNSUP), (dict(flags=2), EUNSUP), (dict(dtype=5), EUNSUP),
+    (dict(dO=A_DO + 2), EALIGN), (dict(dQ=A_DQ + 4), EALIGN), (dict(dK=A_DK + 8), EALIGN), (dict(dV=A_DV + 12), EALIGN),
+    (dict(dQ=A_Q), EALIAS), (dict(dK=A_DO + 16), EALIAS), (dict(dV=A_J), EALIAS), (dict(dK=A_DQ + 16), EALIAS),
+    (dict(dV=A_DK + 4 * 128 * 16 - 16), EALIAS), (dict(dQ=A_V + 32), EALIAS),
+    (dict(ws=None), EWS), (dict(ws_bytes=100), EWS), (dict(ws=A_BW + 16), EALIGN), (dict(ws=A_DQ), EALIAS),
+    (dict(ws=A_Q + 256), EALIAS), (dict(S=1 << 14, Hq=1 << 8, Wq=1 << 8, Hk=4, Wk=4, kappa=2), ESHAPE),
+])
+
+
+def test_backward_rejects(L, kw, code):
+    assert bw(L, **kw) == code
+
+
+def test_backward_workspace_formula(L):
+    def r256(b):
+        return (b + 255) // 256 * 256
+
+    for S, Hq, Wq, Hk, Wk, kappa in ((1, 1, 1, 1, 1, 1), (4, 256, 256, 256, 256, 1), (3, 7, 5, 9, 11, 3)):
+        N, n = S * Hk * Wk, S * Hq * Wq
+        tiles = (N + 2047) // 2048
+        want = r256(4 * N) + r256(4 * (N + 1)) + r256(4 * (tiles + 1)) + r256(4 * n * kappa) + 2 * r256(4 * n)
+        L.scram_sparse_attend_backward_workspace_bytes.restype = ctypes.c_size_t
+        assert L.scram_sparse_attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, kappa) == want
+    assert L.scram_sparse_attend_backward_workspace_bytes(0, 4, 4, 4, 4, 1) == 0
 
 
 def test_python_binding_refuses_host_tensors():

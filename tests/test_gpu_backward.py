@@ -1,0 +1,172 @@
+"""Parity of the attend backward (HIP, through the C ABI) with the oracle.
+
+Gradients of Algorithm 2 (Equations 8-9) with respect to Q, K, V, the maps
+held fixed.  Everything is fp32 on the GPU from the same stored inputs the
+oracle reads exactly; dK and dV are sums over the queries whose key set holds
+a key, gathered through the inverse map in the order it was filled.  Bar: each gradient
+within 2e-5 of that gradient's largest magnitude (a key gathers at most
+kappa * (2b+1)^2-ish terms of fp32 products, each rounded at ~1e-7).
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import scram_inputs as si
+
+torch = pytest.importorskip("torch")
+from gpu_util import IDS, SMALL, log, to_dev  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-5
+
+
+def grads_close(got, ref, tag):
+    worst = []
+    for name, g, r in zip(("dQ", "dK", "dV"), got, ref):
+        g = g.cpu().numpy().astype(np.float64)
+        scale = float(np.abs(r).max())
+        err = float(np.abs(g - r).max()) / max(scale, 1e-30)
+        assert err <= TOL, f"{tag} {name}: {err:.3e} of max |ref| {scale:.3e}"
+        worst.append(err)
+    return worst
+
+
+@pytest.fixture(scope="module", params=range(len(SMALL)), ids=IDS)
+def work(request, scram):
+    cfg = SMALL[request.param]
+    a = si.make_arrays(cfg)
+    dev = {k: to_dev(a[k], cfg.dtype) for k in ("Q", "K", "V")}
+    rng = np.random.default_rng(100 + request.param)
+    dO = to_dev(rng.standard_normal((cfg.S, cfg.Hq, cfg.Wq, cfg.dv)), cfg.dtype)
+    a["dO"] = dO.float().cpu().numpy()  # the values the kernel reads
+    maps = scram.patchmatch_kappa(dev["Q"], dev["K"], 2, cfg.iters, cfg.pm_seed, sep=2)
+    return cfg, a, dev, dO, maps
+
+
+@pytest.mark.parametrize("kappa,window", [(1, None), (1, 1), (1, 7), (2, None), (2, 9)])
+def test_backward_parity(scram, work, kappa, window):
+    cfg, a, dev, dO, maps = work
+    w = cfg.window if window is None else window
+    J = maps[0] if kappa == 1 else maps
+    got = scram.sparse_attend_backward(dev["Q"], dev["K"], dev["V"], J.contiguous(), dO, w, cfg.scale)
+    ref = oracle.sparse_attend_backward(a["Q"], a["K"], a["V"], J.cpu().numpy(), w, cfg.scale, a["dO"])
+    worst = grads_close(got, ref, f"{cfg.name} kappa={kappa} w={w}")
+    log(f"{cfg.name} backward kappa={kappa} window={w}: rel err dQ {worst[0]:.2e} dK {worst[1]:.2e} "
+        f"dV {worst[2]:.2e}")
+
+
+def test_backward_causal(scram, work):
+    cfg, a, dev, dO, maps = work
+    if (cfg.Hq, cfg.Wq) != (cfg.Hk, cfg.Wk):
+        pytest.skip("causal masking needs one grid")
+    J = scram.patchmatch_kappa(dev["Q"], dev["K"], 2, cfg.iters, cfg.pm_seed, sep=2, causal=True)
+    got = scram.sparse_attend_backward(dev["Q"], dev["K"], dev["V"], J, dO, cfg.window, cfg.scale, causal=True)
+    ref = oracle.sparse_attend_backward(a["Q"], a["K"], a["V"], J.cpu().numpy(), cfg.window, cfg.scale, a["dO"],
+                                        flags=oracle.CAUSAL)
+    grads_close(got, ref, f"{cfg.name} causal")
+
+
+def test_backward_dq_deterministic_dkdv_close(scram, work):
+    cfg, a, dev, dO, maps = work
+    g1 = scram.sparse_attend_backward(dev["Q"], dev["K"], dev["V"], maps[0], dO, cfg.window, cfg.scale)
+    g2 = scram.sparse_attend_backward(dev["Q"], dev["K"], dev["V"], maps[0], dO, cfg.window, cfg.scale)
+    assert torch.equal(g1[0], g2[0])
+    for x, y in zip(g1[1:], g2[1:]):
+        assert torch.allclose(x, y, rtol=1e-5, atol=1e-6 * float(x.abs().max()))
+
+
+def test_backward_invariants(scram, work):
+    """sum_j dV_j = sum_i dO_i and sum_j dK_j = 0 per slice."""
+    cfg, a, dev, dO, maps = work
+    dQ, dK, dV = scram.sparse_attend_backward(dev["Q"], dev["K"], dev["V"], maps, dO, cfg.window, cfg.scale)
+    sdv = dV.double().sum(dim=(1, 2)).cpu().numpy()
+    sdo = dO.double().sum(dim=(1, 2)).cpu().numpy()
+    np.testing.assert_allclose(sdv, sdo, rtol=1e-4, atol=1e-3)
+    mag = float(dK.abs().double().sum(dim=(1, 2)).max())
+    assert np.abs(dK.double().sum(dim=(1, 2)).cpu().numpy()).max() <= 1e-5 * mag
+
+
+def test_backward_full_window_is_dense(scram):
+    rng = np.random.default_rng(9)
+    S, H, W, d = 2, 5, 7, 32
+    Q, K, V, dO = (rng.standard_normal((S, H, W, d)).astype(np.float32) for _ in range(4))
+    J = rng.integers(0, H * W, (S, H, W)).astype(np.int32)
+    scale = 1 / math.sqrt(d)
+    for causal in (False, True):
+        got = scram.sparse_attend_backward(*(to_dev(x, "f32") for x in (Q, K, V)), torch.from_numpy(J).cuda(),
+                                           to_dev(dO, "f32"), 2 * max(H, W) - 1, scale, causal=causal)
+        ref = oracle.sparse_attend_backward(Q, K, V, J, 2 * max(H, W) - 1, scale, dO,
+                                            flags=oracle.CAUSAL if causal else 0)
+        grads_close(got, ref, f"full window causal={causal}")
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 1, 1, 1, 16, "f32"), (2, 3, 17, 5, 19, 128, "bf16"),
+                                   (1, 21, 1, 30, 1, 64, "f32"), (3, 9, 7, 4, 6, 32, "bf16")],
+                         ids=lambda s: "x".join(map(str, s[:-1])) + s[-1])
+def test_backward_shapes(scram, shape):
+    S, Hq, Wq, Hk, Wk, d, dtype = shape
+    rng = np.random.default_rng(sum(shape[:-1]))
+    Q = rng.standard_normal((S, Hq, Wq, d)).astype(np.float32)
+    K, V = (rng.standard_normal((S, Hk, Wk, d)).astype(np.float32) for _ in range(2))
+    dO = rng.standard_normal((S, Hq, Wq, d)).astype(np.float32)
+    if dtype == "bf16":
+        Q, K, V, dO = (to_dev(x, "bf16").float().cpu().numpy() for x in (Q, K, V, dO))
+    J = rng.integers(0, Hk * Wk, (2, S, Hq, Wq)).astype(np.int32)
+    for window in (1, 3, 5):
+        got = scram.sparse_attend_backward(*(to_dev(x, dtype) for x in (Q, K, V)), torch.from_numpy(J).cuda(),
+                                           to_dev(dO, dtype), window, d ** -0.5)
+        ref = oracle.sparse_attend_backward(Q, K, V, J, window, d ** -0.5, dO)
+        grads_close(got, ref, f"{shape} window {window}")
+
+
+def test_backward_full_size(scram):
+    """The 256x256 bf16 workload at full size with the GPU's own map."""
+    cfg = si.get(si.HEADLINE)
+    data = si.make(cfg, device="cuda")
+    a = data["np"]
+    J = scram.patchmatch(data["Q"], data["K"], cfg.iters, cfg.pm_seed)
+    rng = np.random.default_rng(5)
+    dO = to_dev(rng.standard_normal((cfg.S, cfg.Hq, cfg.Wq, cfg.dv)).astype(np.float32), cfg.dtype)
+    got = scram.sparse_attend_backward(data["Q"], data["K"], data["V"], J, dO, cfg.window, cfg.scale)
+    ref = oracle.sparse_attend_backward(a["Q"], a["K"], a["V"], J.cpu().numpy(), cfg.window, cfg.scale,
+                                        dO.float().cpu().numpy())
+    worst = grads_close(got, ref, "full size")
+    log(f"{cfg.name} full-size backward: rel err dQ {worst[0]:.2e} dK {worst[1]:.2e} dV {worst[2]:.2e}")
+
+
+def test_backward_events(scram):
+    cfg = SMALL[1]
+    a = si.make_arrays(cfg)
+    dev = {k: to_dev(a[k], cfg.dtype) for k in ("Q", "K", "V")}
+    J = scram.patchmatch(dev["Q"], dev["K"], 2, 1)
+    dO = torch.ones_like(dev["Q"])
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    for e in evs:
+        e.record()
+    g1 = scram.sparse_attend_backward(dev["Q"], dev["K"], dev["V"], J, dO, 3, events=evs)
+    torch.cuda.synchronize()
+    assert all(evs[2 * k].elapsed_time(evs[2 * k + 1]) > 0 for k in range(3))
+    g2 = scram.sparse_attend_backward(dev["Q"], dev["K"], dev["V"], J, dO, 3)
+    assert torch.equal(g1[0], g2[0])
+
+
+@pytest.mark.parametrize("pattern", ["one_key", "two_keys_and_random"])
+def test_backward_hot_keys(scram, pattern):
+    """Skewed inverse maps: every query on one key, or most on two keys -- one bucket holds thousands of entries."""
+    cfg = SMALL[1]
+    a = si.make_arrays(cfg)
+    dev = {k: to_dev(a[k], cfg.dtype) for k in ("Q", "K", "V")}
+    rng = np.random.default_rng(17)
+    n_keys = cfg.Hk * cfg.Wk
+    if pattern == "one_key":
+        J = np.full((cfg.S, cfg.Hq, cfg.Wq), n_keys // 2, np.int32)
+    else:
+        J = rng.choice([0, n_keys - 1], size=(cfg.S, cfg.Hq, cfg.Wq)).astype(np.int32)
+        J.reshape(-1)[::7] = rng.integers(0, n_keys, J.size)[::7]
+    dO = to_dev(rng.standard_normal((cfg.S, cfg.Hq, cfg.Wq, cfg.dv)), cfg.dtype)
+    got = scram.sparse_attend_backward(dev["Q"], dev["K"], dev["V"], torch.from_numpy(J).cuda(), dO, 3, cfg.scale)
+    ref = oracle.sparse_attend_backward(a["Q"], a["K"], a["V"], J, 3, cfg.scale, dO.float().cpu().numpy())
+    grads_close(got, ref, pattern)
