@@ -32,7 +32,8 @@ if ROOT not in sys.path:
 
 METRIC = "queries/sec (PatchMatch argmax + sparse attend), 256×256 grid d=64; HBM GB/s"
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, public spec
-KERNEL_SRC = os.path.join(ROOT, "paper_1905_10308_amd", "csrc", "scram_kernels.hip")
+# sources of the sweep kernel: its traffic figures hold only while these are unchanged
+KERNEL_SRCS = [os.path.join(ROOT, "paper_1905_10308_amd", "csrc", f) for f in ("scram_device.h", "scram_pm.hip")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pm_iter_traffic.json")
 
 
@@ -62,8 +63,11 @@ def init_bytes_per_query(cfg) -> int:
 
 
 def kernel_source_hash() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in KERNEL_SRCS:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def load_traffic(cfg):
@@ -184,7 +188,8 @@ def main(argv=None) -> int:
         return 2
     dO = torch.randn((S, Hq, Wq, cfg.dv), generator=torch.Generator(device=dev).manual_seed(7), device=dev,
                      dtype=torch.float32).to(Q.dtype) if args.backward else None
-    bwd_ws = torch.empty(scram.sparse_attend_backward_workspace_bytes(S, Hq, Wq, cfg.Hk, cfg.Wk, kappa),
+    bwd_ws = torch.empty(scram.sparse_attend_backward_workspace_bytes(S, Hq, Wq, cfg.Hk, cfg.Wk, kappa, d=cfg.d,
+                                                                      dtype=Q.dtype),
                          dtype=torch.uint8, device=dev) if args.backward else None
 
     def new_events():
@@ -242,7 +247,7 @@ def main(argv=None) -> int:
     att_ms = sum(dur(ev, kappa * (T + 1)) for ev in events) / args.steps
     bwd = {}
     if args.backward:
-        for i, name in enumerate(("backward_inverse_map", "backward_query", "backward_key")):
+        for i, name in enumerate(("backward_inverse_map", "backward_query", "backward_key_side")):
             bwd[name] = sum(dur(ev, kappa * (T + 1) + 1 + i) for ev in events) / args.steps
 
     nq = cfg.nq

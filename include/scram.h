@@ -216,7 +216,8 @@ int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype, 
  * weights are recomputed from Q, K, V (the forward output is not needed).
  * Key j lies in W_i exactly when a match of query i lies in the
  * (2b+1) x (2b+1) neighbourhood of j, so dK_j and dV_j gather over the
- * queries found through the inverse of the maps (kept in the workspace).
+ * queries found through the inverse of the maps (kept in the workspace,
+ * with copies of those queries' q, dO rows in the inverse map's order).
  * Every gradient row has a single writer; the order in which the queries of
  * one match key are summed is the order the inverse map was filled in,
  * which may differ between calls (dK, dV may differ in the last bits; dQ is
@@ -230,14 +231,18 @@ int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype, 
  *   dV        fp32 [S, Hk, Wk, dv] (written)
  *   workspace device scratch of at least
  *             scram_sparse_attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk,
- *             kappa) bytes, 256-byte aligned; contents undefined on return
+ *             d, dtype, kappa) bytes, 256-byte aligned; contents undefined
+ *             on return (about 2 * kappa * S*Hq*Wq rows of d elements plus
+ *             a few int32 / fp32 per key and query)
  *   events    NULL or 6 events: start/stop of building the inverse map, of
- *             the per-query kernel and of the per-key kernel
+ *             the per-query kernel and of the key side (row copies and the
+ *             per-key kernel)
  * Also requires S*Hq*Wq*kappa < 2^31.  dQ, dK, dV must be 16-byte aligned;
  * no output or the workspace may overlap an input or another output.
  * Returns a status code.
  */
-size_t scram_sparse_attend_backward_workspace_bytes(int S, int Hq, int Wq, int Hk, int Wk, int kappa);
+size_t scram_sparse_attend_backward_workspace_bytes(int S, int Hq, int Wq, int Hk, int Wk, int d, int dtype,
+                                                    int kappa);
 
 int scram_sparse_attend_backward(const void* Q, const void* K, const void* V, int dtype, const int32_t* argmax,
                                  int kappa, int S, int Hq, int Wq, int Hk, int Wk, int d, int dv, int window,
@@ -297,7 +302,7 @@ const char* scram_status_string(int status);
 /* ABI version of this header: (major << 16) | minor. */
 int scram_abi_version(void);
 
-#define SCRAM_ABI_VERSION ((2 << 16) | 3)
+#define SCRAM_ABI_VERSION ((2 << 16) | 4)
 
 #ifdef __cplusplus
 }

@@ -60,7 +60,7 @@ def lib() -> ctypes.CDLL:
     L.scram_sparse_attend_backward.argtypes = [P, P, P, I, P, I, I, I, I, I, I, I, I, I, ctypes.c_float, U32, P, P,
                                                P, P, P, SZ, P, P]
     L.scram_sparse_attend_backward.restype = I
-    L.scram_sparse_attend_backward_workspace_bytes.argtypes = [I, I, I, I, I, I]
+    L.scram_sparse_attend_backward_workspace_bytes.argtypes = [I, I, I, I, I, I, I, I]
     L.scram_sparse_attend_backward_workspace_bytes.restype = SZ
     L.scram_snis_attend.argtypes = [P, P, P, I, P, I, I, I, I, I, I, I, I, I, ctypes.c_float, I, ctypes.c_float,
                                     U64, U32, P, P, P, P, P]
@@ -90,13 +90,17 @@ def _torch():
     return torch
 
 
-def _dtype_code(t) -> int:
+def _dtype_code_of(dtype) -> int:
     torch = _torch()
-    if t.dtype == torch.float32:
+    if dtype == torch.float32:
         return SCRAM_F32
-    if t.dtype == torch.bfloat16:
+    if dtype == torch.bfloat16:
         return SCRAM_BF16
-    raise TypeError(f"unsupported dtype {t.dtype}; expected float32 or bfloat16")
+    raise TypeError(f"unsupported dtype {dtype}; expected float32 or bfloat16")
+
+
+def _dtype_code(t) -> int:
+    return _dtype_code_of(t.dtype)
 
 
 def _dev_tensor(t, name, ndim=None):
@@ -258,7 +262,7 @@ def sparse_attend_backward(Q, K, V, argmax, dO, window: int, scale: float | None
     dQ = torch.empty((S, Hq, Wq, d), dtype=torch.float32, device=dev)
     dK = torch.empty((S, Hk, Wk, d), dtype=torch.float32, device=dev)
     dV = torch.empty((S, Hk, Wk, dv), dtype=torch.float32, device=dev)
-    need = sparse_attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, kappa)
+    need = sparse_attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, kappa, d=d, dtype=Q.dtype)
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
     ev = None if events is None else _event_array(events, 6)
@@ -272,8 +276,11 @@ def sparse_attend_backward(Q, K, V, argmax, dO, window: int, scale: float | None
     return dQ, dK, dV
 
 
-def sparse_attend_backward_workspace_bytes(S: int, Hq: int, Wq: int, Hk: int, Wk: int, kappa: int = 1) -> int:
-    return int(lib().scram_sparse_attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, kappa))
+def sparse_attend_backward_workspace_bytes(S: int, Hq: int, Wq: int, Hk: int, Wk: int, kappa: int = 1, *,
+                                           d: int, dtype) -> int:
+    """Bytes of device workspace ``sparse_attend_backward`` needs (``dtype``: torch dtype of Q, K, V)."""
+    return int(lib().scram_sparse_attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, d, _dtype_code_of(dtype),
+                                                                   kappa))
 
 
 def snis_attend(Q, K, V, modes, samples: int, *, alpha: float = 0.9, radius: int = 4, scale: float | None = None,

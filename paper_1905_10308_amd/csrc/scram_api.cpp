@@ -189,10 +189,11 @@ int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype, 
     return e == hipSuccess ? SCRAM_OK : SCRAM_ERR_HIP;
 }
 
-size_t scram_sparse_attend_backward_workspace_bytes(int S, int Hq, int Wq, int Hk, int Wk, int kappa)
+size_t scram_sparse_attend_backward_workspace_bytes(int S, int Hq, int Wq, int Hk, int Wk, int d, int dtype,
+                                                    int kappa)
 {
-    if (check_grid(S, Hq, Wq, Hk, Wk) || kappa < 1 || kappa > SCRAM_MAX_KAPPA) return 0;
-    return scram::attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, kappa);
+    if (check_grid(S, Hq, Wq, Hk, Wk) || kappa < 1 || kappa > SCRAM_MAX_KAPPA || check_type(dtype, d)) return 0;
+    return scram::attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, d, dtype, kappa);
 }
 
 int scram_sparse_attend_backward(const void* Q, const void* K, const void* V, int dtype, const int32_t* argmax,
@@ -217,7 +218,7 @@ int scram_sparse_attend_backward(const void* Q, const void* K, const void* V, in
     if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(dO, 16) || !aligned(argmax, 4) ||
         !aligned(dQ, 16) || !aligned(dK, 16) || !aligned(dV, 16) || !aligned(workspace, 256))
         return SCRAM_ERR_ALIGN;
-    const size_t need = scram::attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, kappa);
+    const size_t need = scram::attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, d, dtype, kappa);
     if (workspace_bytes < need) return SCRAM_ERR_WORKSPACE;
     const size_t n = size_t(S) * Hq * Wq, nk = size_t(S) * Hk * Wk, eb = elem_bytes(dtype);
     const Range rQ = range(dQ, 4 * n * d), rK = range(dK, 4 * nk * d), rV = range(dV, 4 * nk * dv);

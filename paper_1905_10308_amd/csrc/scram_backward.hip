@@ -1,0 +1,688 @@
+// Backward of the sparse window attention with the maps held fixed.
+
+#include "scram_device.h"
+
+namespace scram {
+namespace {
+
+// ---------------------------------------------------------------------------
+// K6: backward of the sparse attention, maps held fixed
+//
+// For query i with key set W_i (as in the forward), p_ij its softmax
+// weights, dp_ij = dO_i . v_j and D_i = sum_j p_ij dp_ij:
+//   dQ_i = scale sum_j p_ij (dp_ij - D_i) k_j
+//   dK_j = scale sum_i p_ij (dp_ij - D_i) q_i,   dV_j = sum_i p_ij dO_i
+// Query side (one lane group per query): pass A walks W_i for the running
+// max, the normaliser and D_i and stores log2 of the normaliser (with the
+// max) and D_i; pass B walks it again for dQ_i.  Key side (one lane group
+// per key): key j lies in W_i exactly when a match of i lies in the
+// (2b+1)^2 neighbourhood of j, so the queries are found through the inverse
+// map -- the (query, match) entries sorted by match key (a counting sort).
+// The keys of one neighbourhood row are consecutive, so their entries form
+// one contiguous range; after the query kernel, q_i, dO_i and the query's
+// statistics are copied into entry order, so the key kernel reads each
+// range as contiguous rows.  No float atomics: every gradient row has one
+// writer.
+// ---------------------------------------------------------------------------
+constexpr int kScanItems = 8;                          // counts per thread in the scan
+constexpr int kScanTile = kBlock * kScanItems;         // counts per scan block
+
+struct BwdParams {
+    const void* Q;
+    const void* K;
+    const void* V;
+    const int32_t* J;      // [kappa, n]
+    const void* dO;
+    float* dQ;
+    float* dK;
+    float* dV;
+    float* lse2;           // [n] max + log2(normaliser), base-2 scores
+    float* Dq;             // [n] D_i
+    const int32_t* offsets;  // [S * nkeys + 1] start of each key's entries
+    const int32_t* entries;  // [kappa * n] e * n + i, grouped by match key
+    int32_t* heavy;          // [S * nkeys] keys left to bwd_heavy_kernel
+    int32_t* n_heavy;        // their count
+    void* qs;                // [kappa * n, D] q_i of each entry, in entry order
+    void* gs;                // [kappa * n, D] dO_i of each entry, in entry order
+    float2* st;              // [kappa * n] (log2 normaliser, D_i) of each entry
+    uint32_t n;
+    uint32_t keys_total;   // S * nkeys
+    int Hq, Wq, Hk, Wk;
+    uint32_t nkeys;
+    Div div_plane, div_wk, div_n, div_keys;
+    int b;
+    float scale;
+    float scale_log2e;
+    int kappa;
+    int causal;
+};
+
+__global__ __launch_bounds__(kBlock) void zero_i32_kernel(int32_t* a, size_t count)
+{
+    for (size_t i = static_cast<size_t>(blockIdx.x) * kBlock + threadIdx.x; i < count;
+         i += static_cast<size_t>(gridDim.x) * kBlock)
+        a[i] = 0;
+}
+
+// counts[s * nkeys + J[e][i]] += 1 for every (query, match)
+__global__ __launch_bounds__(kBlock) void bwd_count_kernel(BwdParams p, int32_t* counts)
+{
+    const size_t total = static_cast<size_t>(p.kappa) * p.n;
+    for (size_t x = static_cast<size_t>(blockIdx.x) * kBlock + threadIdx.x; x < total;
+         x += static_cast<size_t>(gridDim.x) * kBlock) {
+        const uint32_t g = static_cast<uint32_t>(x % p.n);
+        const uint32_t s = g / (static_cast<uint32_t>(p.Hq) * p.Wq);
+        atomicAdd(counts + static_cast<size_t>(s) * p.nkeys + clamp_index(p.J[x], p.nkeys), 1);
+    }
+}
+
+// Exclusive scan, step 1: each block scans a tile of kScanTile counts into
+// out (tile-local prefixes) and writes the tile's total to sums[tile].
+__global__ __launch_bounds__(kBlock) void scan_tiles_kernel(const int32_t* in, int32_t* out, int32_t* sums, size_t count)
+{
+    __shared__ int32_t wave_tot[kBlock / 64];
+    const size_t base = static_cast<size_t>(blockIdx.x) * kScanTile + static_cast<size_t>(threadIdx.x) * kScanItems;
+    int32_t v[kScanItems];
+    int32_t run = 0;
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        v[i] = base + i < count ? in[base + i] : 0;
+        const int32_t x = v[i];
+        v[i] = run;  // exclusive within the thread
+        run += x;
+    }
+    // exclusive prefix of the thread totals: within the wave, then across waves
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int32_t incl = run;
+#pragma unroll
+    for (int k = 1; k < 64; k <<= 1) {
+        const int32_t y = __shfl_up(incl, k, 64);
+        if (lane >= k) incl += y;
+    }
+    if (lane == 63) wave_tot[wave] = incl;
+    __syncthreads();
+    int32_t before = incl - run;
+    for (int w = 0; w < wave; ++w) before += wave_tot[w];
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i)
+        if (base + i < count) out[base + i] = before + v[i];
+    if (threadIdx.x == kBlock - 1) {
+        int32_t tot = 0;
+        for (int w = 0; w < kBlock / 64; ++w) tot += wave_tot[w];
+        sums[blockIdx.x] = tot;
+    }
+}
+
+// Exclusive scan, step 2 (one block): sums[0..tiles) in place, total in sums[tiles].
+__global__ __launch_bounds__(kBlock) void scan_sums_kernel(int32_t* sums, uint32_t tiles)
+{
+    __shared__ int32_t wave_tot[kBlock / 64];
+    __shared__ int32_t carry_s;
+    if (threadIdx.x == 0) carry_s = 0;
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    for (uint32_t c0 = 0; c0 < tiles; c0 += kBlock) {
+        const uint32_t i = c0 + threadIdx.x;
+        const int32_t x = i < tiles ? sums[i] : 0;
+        int32_t incl = x;
+#pragma unroll
+        for (int k = 1; k < 64; k <<= 1) {
+            const int32_t y = __shfl_up(incl, k, 64);
+            if (lane >= k) incl += y;
+        }
+        if (lane == 63) wave_tot[wave] = incl;
+        __syncthreads();
+        int32_t before = carry_s + incl - x;
+        for (int w = 0; w < wave; ++w) before += wave_tot[w];
+        if (i < tiles) sums[i] = before;
+        __syncthreads();  // every thread has read carry_s and wave_tot
+        if (threadIdx.x == kBlock - 1) carry_s = before + x;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) sums[tiles] = carry_s;
+}
+
+// Exclusive scan, step 3: add each tile's offset; out[count] = total.
+__global__ __launch_bounds__(kBlock) void scan_add_kernel(int32_t* out, const int32_t* sums, size_t count,
+                                                          uint32_t tiles)
+{
+    const size_t base = static_cast<size_t>(blockIdx.x) * kScanTile;
+    const int32_t add = sums[blockIdx.x];
+    for (int i = threadIdx.x; i < kScanTile; i += kBlock)
+        if (base + i < count) out[base + i] += add;
+    if (blockIdx.x == 0 && threadIdx.x == 0) out[count] = sums[tiles];
+}
+
+// entries[offsets[key] + (a slot of that key)] = e * n + i; counts end at 0
+__global__ __launch_bounds__(kBlock) void bwd_fill_kernel(BwdParams p, int32_t* counts, int32_t* entries)
+{
+    const size_t total = static_cast<size_t>(p.kappa) * p.n;
+    for (size_t x = static_cast<size_t>(blockIdx.x) * kBlock + threadIdx.x; x < total;
+         x += static_cast<size_t>(gridDim.x) * kBlock) {
+        const uint32_t g = static_cast<uint32_t>(x % p.n);
+        const uint32_t s = g / (static_cast<uint32_t>(p.Hq) * p.Wq);
+        const size_t key = static_cast<size_t>(s) * p.nkeys + clamp_index(p.J[x], p.nkeys);
+        const int32_t slot = atomicSub(counts + key, 1) - 1;
+        entries[p.offsets[key] + slot] = static_cast<int32_t>(x);
+    }
+}
+
+template <typename T, int D, int G, bool MULTI>
+__global__ __launch_bounds__(kBlock) void bwd_query_kernel(BwdParams p)
+{
+    using RW = Row<T, D, G>;
+    constexpr int CH = RW::kCh;
+    constexpr int E = CH * RW::kEpc;
+    constexpr int kEpc = RW::kEpc;
+    constexpr int kNb = CH >= 2 ? 4 : 8;
+    const int lane = threadIdx.x & (G - 1);
+    const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+    const uint32_t g = blk * RW::kQpb + threadIdx.x / G;
+    if (g >= p.n) return;
+
+    uint32_t s, rem;
+    divmod(g, p.div_plane, s, rem);
+    const size_t slice = static_cast<size_t>(s) * p.nkeys * D;
+    const T* Ks = static_cast<const T*>(p.K) + slice;
+    const T* Vs = static_cast<const T*>(p.V) + slice;
+    uint4 q[CH], go[CH];
+    load_row<T, D, G>(static_cast<const T*>(p.Q), g, lane, q);
+    load_row<T, D, G>(static_cast<const T*>(p.dO), g, lane, go);
+    WindowSet wset;
+    if constexpr (MULTI) wset = make_window_set(p, g, rem);
+    const int nsets = MULTI ? p.kappa : 1;
+
+    // visit(fn): every key of the set, kNb at a time with their key and
+    // value rows loaded together; fn(ok[], kr, vr) per batch
+    auto visit = [&](auto&& fn) {
+        for (int e = 0; e < nsets; ++e) {
+            uint32_t u, v;
+            if constexpr (MULTI) {
+                u = static_cast<uint32_t>(wset.cu[0]);
+                v = static_cast<uint32_t>(wset.cv[0]);
+#pragma unroll
+                for (int f = 1; f < kMaxKappa; ++f)
+                    if (f == e) {
+                        u = static_cast<uint32_t>(wset.cu[f]);
+                        v = static_cast<uint32_t>(wset.cv[f]);
+                    }
+            } else {
+                divmod(static_cast<uint32_t>(clamp_index(p.J[g], p.nkeys)), p.div_wk, u, v);
+            }
+            const int r0 = max(static_cast<int>(u) - p.b, 0), r1 = min(static_cast<int>(u) + p.b, p.Hk - 1);
+            const int c0 = max(static_cast<int>(v) - p.b, 0), c1 = min(static_cast<int>(v) + p.b, p.Wk - 1);
+            const int nwin = (r1 - r0 + 1) * (c1 - c0 + 1);
+            const uint32_t centre = u * p.Wk + v;
+            int r = r0, c = c0;
+            for (int k0 = 0; k0 < nwin; k0 += kNb) {
+                uint4 kr[kNb][CH], vr[kNb][CH];
+                bool ok[kNb];
+#pragma unroll
+                for (int j = 0; j < kNb; ++j) {
+                    ok[j] = k0 + j < nwin;
+                    if constexpr (MULTI) ok[j] = ok[j] && !wset.skip(e, r, c);
+                    const uint32_t row = k0 + j < nwin ? static_cast<uint32_t>(r * p.Wk + c) : centre;
+                    load_row<T, D, G>(Ks, row, lane, kr[j]);
+                    load_row<T, D, G>(Vs, row, lane, vr[j]);
+                    if (k0 + j < nwin && ++c > c1) {
+                        c = c0;
+                        ++r;
+                    }
+                }
+                fn(ok, kr, vr);
+            }
+        }
+    };
+
+    // pass A: running max m, normaliser l, sum of e^(a - m) dp (base-2 scores)
+    float m = -INFINITY, l = 0.f, dn = 0.f;
+    visit([&](const bool (&ok)[kNb], const uint4 (&kr)[kNb][CH], const uint4 (&vr)[kNb][CH]) {
+        float sc[kNb], dp[kNb];
+        float mb = m;
+#pragma unroll
+        for (int j = 0; j < kNb; ++j) {
+            sc[j] = ok[j] ? row_score<T, D, G>(q, kr[j]) * p.scale_log2e : -INFINITY;
+            dp[j] = row_score<T, D, G>(go, vr[j]);
+            mb = fmaxf(mb, sc[j]);
+        }
+        if (mb == -INFINITY) return;
+        const float alpha = __builtin_amdgcn_exp2f(m - mb);
+        l *= alpha;
+        dn *= alpha;
+#pragma unroll
+        for (int j = 0; j < kNb; ++j) {
+            const float pj = __builtin_amdgcn_exp2f(sc[j] - mb);
+            l += pj;
+            dn = fmaf(pj, dp[j], dn);
+        }
+        m = mb;
+    });
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+    const float Dg = dn * inv;
+    if (lane == 0) {
+        p.lse2[g] = l > 0.f ? m + log2f(l) : INFINITY;  // +inf: every weight is 0
+        p.Dq[g] = Dg;
+    }
+
+    // pass B: dQ with the exact weights
+    float dq[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) dq[e] = 0.f;
+    if (l > 0.f) {
+        visit([&](const bool (&ok)[kNb], const uint4 (&kr)[kNb][CH], const uint4 (&vr)[kNb][CH]) {
+#pragma unroll
+            for (int j = 0; j < kNb; ++j) {
+                const float sc = ok[j] ? row_score<T, D, G>(q, kr[j]) * p.scale_log2e : -INFINITY;
+                const float dp = row_score<T, D, G>(go, vr[j]);
+                const float ds = __builtin_amdgcn_exp2f(sc - m) * inv * (dp - Dg);  // 0 when !ok
+                float kf[E];
+                unpack_row<T, CH>(kr[j], kf);
+#pragma unroll
+                for (int e = 0; e < E; ++e) dq[e] = fmaf(ds, kf[e], dq[e]);
+            }
+        });
+    }
+#pragma unroll
+    for (int cc = 0; cc < CH; ++cc) {
+        float4* o = reinterpret_cast<float4*>(p.dQ + static_cast<size_t>(g) * D + (cc * G + lane) * kEpc);
+#pragma unroll
+        for (int i = 0; i < kEpc / 4; ++i)
+            o[i] = make_float4(dq[cc * kEpc + 4 * i] * p.scale, dq[cc * kEpc + 4 * i + 1] * p.scale,
+                               dq[cc * kEpc + 4 * i + 2] * p.scale, dq[cc * kEpc + 4 * i + 3] * p.scale);
+    }
+}
+
+// Copy q_i, dO_i and (log2 normaliser, D_i) of every entry into entry order.
+template <typename T, int D, int G>
+__global__ __launch_bounds__(kBlock) void bwd_gather_kernel(BwdParams p)
+{
+    using RW = Row<T, D, G>;
+    constexpr int CH = RW::kCh;
+    const int lane = threadIdx.x & (G - 1);
+    const uint32_t x = blockIdx.x * RW::kQpb + threadIdx.x / G;
+    if (x >= static_cast<uint32_t>(p.kappa) * p.n) return;
+    uint32_t e, g;
+    divmod(static_cast<uint32_t>(p.entries[x]), p.div_n, e, g);
+    uint4 q[CH], go[CH];
+    load_row<T, D, G>(static_cast<const T*>(p.Q), g, lane, q);
+    load_row<T, D, G>(static_cast<const T*>(p.dO), g, lane, go);
+    uint4* qd = reinterpret_cast<uint4*>(static_cast<T*>(p.qs) + static_cast<size_t>(x) * D) + lane;
+    uint4* gd = reinterpret_cast<uint4*>(static_cast<T*>(p.gs) + static_cast<size_t>(x) * D) + lane;
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+        qd[c * G] = q[c];
+        gd[c * G] = go[c];
+    }
+    if (lane == 0) p.st[x] = make_float2(p.lse2[g], p.Dq[g]);
+}
+
+// Contributions of kNb entries (slots x[t], valid where ok[t]) to dK_j, dV_j
+// (unscaled dK) for key j at (ju, jv): each query once -- through its first
+// window holding j -- and, with the causal mask, only if j is not after it.
+template <typename T, int D, int G, bool MULTI, int kNb>
+__device__ __forceinline__ void key_batch(const BwdParams& p, const int (&x)[kNb], const bool (&valid)[kNb], uint32_t j,
+                                          uint32_t ju, uint32_t jv, int lane, const uint4 (&kj)[Row<T, D, G>::kCh],
+                                          const uint4 (&vj)[Row<T, D, G>::kCh], float* dk, float* dv)
+{
+    using RW = Row<T, D, G>;
+    constexpr int CH = RW::kCh;
+    constexpr int E = CH * RW::kEpc;
+    const T* qs = static_cast<const T*>(p.qs);
+    const T* gs = static_cast<const T*>(p.gs);
+    uint4 qr[kNb][CH], gr[kNb][CH];
+    float2 st[kNb];
+    int32_t code[kNb];
+#pragma unroll
+    for (int t = 0; t < kNb; ++t) {
+        code[t] = p.entries[x[t]];
+        st[t] = p.st[x[t]];
+        load_row<T, D, G>(qs, static_cast<uint32_t>(x[t]), lane, qr[t]);
+        load_row<T, D, G>(gs, static_cast<uint32_t>(x[t]), lane, gr[t]);
+    }
+#pragma unroll
+    for (int t = 0; t < kNb; ++t) {
+        bool ok = valid[t];
+        if constexpr (MULTI) {
+            uint32_t e, g;
+            divmod(static_cast<uint32_t>(code[t]), p.div_n, e, g);
+            for (int f = 0; f < static_cast<int>(e) && ok; ++f) {
+                uint32_t fu, fv;
+                divmod(static_cast<uint32_t>(clamp_index(p.J[static_cast<size_t>(f) * p.n + g], p.nkeys)), p.div_wk,
+                       fu, fv);
+                if (abs(static_cast<int>(fu) - static_cast<int>(ju)) <= p.b &&
+                    abs(static_cast<int>(fv) - static_cast<int>(jv)) <= p.b)
+                    ok = false;
+            }
+            if (ok && p.causal) {
+                uint32_t gsl, grem;
+                divmod(g, p.div_plane, gsl, grem);
+                ok = j <= grem;
+            }
+        }
+        const float sc = row_score<T, D, G>(qr[t], kj) * p.scale_log2e;
+        const float dp = row_score<T, D, G>(gr[t], vj);
+        const float pj = ok ? __builtin_amdgcn_exp2f(sc - st[t].x) : 0.f;
+        const float ds = pj * (dp - st[t].y);
+        float qf[E], gf[E];
+        unpack_row<T, CH>(qr[t], qf);
+        unpack_row<T, CH>(gr[t], gf);
+#pragma unroll
+        for (int e2 = 0; e2 < E; ++e2) {
+            dk[e2] = fmaf(ds, qf[e2], dk[e2]);
+            dv[e2] = fmaf(pj, gf[e2], dv[e2]);
+        }
+    }
+}
+
+// Keys whose neighbourhood holds more entries than this are handed to
+// bwd_heavy_kernel (a whole wave per key) instead of one lane group.
+#ifndef SCRAM_BWD_HEAVY_ENTRIES
+#define SCRAM_BWD_HEAVY_ENTRIES 64
+#endif
+constexpr int kHeavyEntries = SCRAM_BWD_HEAVY_ENTRIES;
+constexpr int kMaxRows = 8;  // neighbourhoods of up to this many rows are walked as one flat list
+
+// The entry ranges of the neighbourhood rows r0..r1 of key j: row i covers
+// entries [lo[i], lo[i] + pre[i+1] - pre[i]); pre[] is the running count.
+struct Neighbourhood {
+    int lo[kMaxRows];
+    int pre[kMaxRows + 1];
+    int total;
+};
+
+__device__ __forceinline__ Neighbourhood load_neighbourhood(const int32_t* off, int Wk, int r0, int r1, int c0, int c1)
+{
+    Neighbourhood nb;
+    nb.pre[0] = 0;
+#pragma unroll
+    for (int i = 0; i < kMaxRows; ++i) {
+        int lo = 0, len = 0;
+        if (r0 + i <= r1) {
+            lo = off[(r0 + i) * Wk + c0];
+            len = off[(r0 + i) * Wk + c1 + 1] - lo;
+        }
+        nb.lo[i] = lo;
+        nb.pre[i + 1] = nb.pre[i] + len;
+    }
+    nb.total = nb.pre[kMaxRows];
+    return nb;
+}
+
+// Entry slot of flat position v (0 <= v < total): the last row with pre <= v.
+__device__ __forceinline__ int flat_slot(const Neighbourhood& nb, int v)
+{
+    int x = nb.lo[0] + v;
+#pragma unroll
+    for (int i = 1; i < kMaxRows; ++i)
+        if (v >= nb.pre[i]) x = nb.lo[i] + (v - nb.pre[i]);
+    return x;
+}
+
+// Accumulate the entries of key j's neighbourhood taken by member `member`
+// of a team of `team` lane groups (positions member, member + team, ...).
+template <typename T, int D, int G, bool MULTI>
+__device__ __forceinline__ void key_accumulate(const BwdParams& p, uint32_t j, uint32_t ju, uint32_t jv, int r0,
+                                               int r1, int c0, int c1, const int32_t* off, int member, int team,
+                                               int lane, const uint4 (&kj)[Row<T, D, G>::kCh],
+                                               const uint4 (&vj)[Row<T, D, G>::kCh], float* dk, float* dv)
+{
+    constexpr int kNb = Row<T, D, G>::kCh >= 2 ? 4 : 8;
+    if (r1 - r0 + 1 <= kMaxRows) {
+        const Neighbourhood nb = load_neighbourhood(off, p.Wk, r0, r1, c0, c1);
+        for (int v0 = member; v0 < nb.total; v0 += kNb * team) {
+            int x[kNb];
+            bool valid[kNb];
+#pragma unroll
+            for (int t = 0; t < kNb; ++t) {
+                const int v = v0 + t * team;
+                valid[t] = v < nb.total;
+                x[t] = flat_slot(nb, min(v, nb.total - 1));  // in bounds; invalid slots get weight 0
+            }
+            key_batch<T, D, G, MULTI, kNb>(p, x, valid, j, ju, jv, lane, kj, vj, dk, dv);
+        }
+    } else {
+        for (int r = r0; r <= r1; ++r) {
+            const int lo = off[r * p.Wk + c0], hi = off[r * p.Wk + c1 + 1];
+            for (int x0 = lo + member; x0 < hi; x0 += kNb * team) {
+                int x[kNb];
+                bool valid[kNb];
+#pragma unroll
+                for (int t = 0; t < kNb; ++t) {
+                    valid[t] = x0 + t * team < hi;
+                    x[t] = min(x0 + t * team, hi - 1);
+                }
+                key_batch<T, D, G, MULTI, kNb>(p, x, valid, j, ju, jv, lane, kj, vj, dk, dv);
+            }
+        }
+    }
+}
+
+// dK_j (times scale) and dV_j from the lane's channels.
+template <typename T, int D, int G>
+__device__ __forceinline__ void store_key_grads(const BwdParams& p, uint32_t kg, int lane, const float* dk,
+                                                const float* dv)
+{
+    constexpr int CH = Row<T, D, G>::kCh;
+    constexpr int kEpc = Row<T, D, G>::kEpc;
+#pragma unroll
+    for (int cc = 0; cc < CH; ++cc) {
+        float4* ok = reinterpret_cast<float4*>(p.dK + static_cast<size_t>(kg) * D + (cc * G + lane) * kEpc);
+        float4* ov = reinterpret_cast<float4*>(p.dV + static_cast<size_t>(kg) * D + (cc * G + lane) * kEpc);
+#pragma unroll
+        for (int i = 0; i < kEpc / 4; ++i) {
+            const int e0 = cc * kEpc + 4 * i;
+            ok[i] = make_float4(dk[e0] * p.scale, dk[e0 + 1] * p.scale, dk[e0 + 2] * p.scale, dk[e0 + 3] * p.scale);
+            ov[i] = make_float4(dv[e0], dv[e0 + 1], dv[e0 + 2], dv[e0 + 3]);
+        }
+    }
+}
+
+struct KeyPos {
+    uint32_t s, j, ju, jv;
+    int r0, r1, c0, c1;
+};
+
+__device__ __forceinline__ KeyPos key_pos(const BwdParams& p, uint32_t kg)
+{
+    KeyPos k;
+    divmod(kg, p.div_keys, k.s, k.j);
+    divmod(k.j, p.div_wk, k.ju, k.jv);
+    k.r0 = max(static_cast<int>(k.ju) - p.b, 0);
+    k.r1 = min(static_cast<int>(k.ju) + p.b, p.Hk - 1);
+    k.c0 = max(static_cast<int>(k.jv) - p.b, 0);
+    k.c1 = min(static_cast<int>(k.jv) + p.b, p.Wk - 1);
+    return k;
+}
+
+// One lane group per key j: sum over the entries (i, e) whose match e lies
+// in the neighbourhood of j (so j is in window e of i).  Keys with more than
+// kHeavyEntries entries are appended to the heavy list instead.
+template <typename T, int D, int G, bool MULTI>
+__global__ __launch_bounds__(kBlock) void bwd_key_kernel(BwdParams p)
+{
+    using RW = Row<T, D, G>;
+    constexpr int CH = RW::kCh;
+    constexpr int E = CH * RW::kEpc;
+    const int lane = threadIdx.x & (G - 1);
+    const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+    const uint32_t kg = blk * RW::kQpb + threadIdx.x / G;  // global key id s * nkeys + j
+    if (kg >= p.keys_total) return;
+    const KeyPos k = key_pos(p, kg);
+    const int32_t* off = p.offsets + static_cast<size_t>(k.s) * p.nkeys;
+    int total = 0;
+    for (int r = k.r0; r <= k.r1; ++r) total += off[r * p.Wk + k.c1 + 1] - off[r * p.Wk + k.c0];
+    if (total > kHeavyEntries) {
+        if (lane == 0) p.heavy[atomicAdd(p.n_heavy, 1)] = static_cast<int32_t>(kg);
+        return;
+    }
+    uint4 kj[CH], vj[CH];
+    load_row<T, D, G>(static_cast<const T*>(p.K), kg, lane, kj);
+    load_row<T, D, G>(static_cast<const T*>(p.V), kg, lane, vj);
+    float dk[E], dv[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) dk[e] = dv[e] = 0.f;
+    key_accumulate<T, D, G, MULTI>(p, k.j, k.ju, k.jv, k.r0, k.r1, k.c0, k.c1, off, 0, 1, lane, kj, vj, dk, dv);
+    store_key_grads<T, D, G>(p, kg, lane, dk, dv);
+}
+
+// The heavy keys, one wave each (waves take keys w, w + total waves, ...):
+// the wave's lane groups stride over the key's entries and their partial
+// sums are added across the wave with xor shuffles.
+template <typename T, int D, int G, bool MULTI>
+__global__ __launch_bounds__(kBlock) void bwd_heavy_kernel(BwdParams p)
+{
+    using RW = Row<T, D, G>;
+    constexpr int CH = RW::kCh;
+    constexpr int E = CH * RW::kEpc;
+    constexpr int kTeam = 64 / G;  // lane groups per wave
+    const int lane = threadIdx.x & (G - 1);
+    const int member = (threadIdx.x & 63) / G;
+    const int wave = blockIdx.x * (kBlock / 64) + threadIdx.x / 64;
+    const int waves = gridDim.x * (kBlock / 64);
+    const int n_heavy = *p.n_heavy;
+    for (int h = wave; h < n_heavy; h += waves) {
+        const uint32_t kg = static_cast<uint32_t>(p.heavy[h]);
+        const KeyPos k = key_pos(p, kg);
+        const int32_t* off = p.offsets + static_cast<size_t>(k.s) * p.nkeys;
+        uint4 kj[CH], vj[CH];
+        load_row<T, D, G>(static_cast<const T*>(p.K), kg, lane, kj);
+        load_row<T, D, G>(static_cast<const T*>(p.V), kg, lane, vj);
+        float dk[E], dv[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) dk[e] = dv[e] = 0.f;
+        key_accumulate<T, D, G, MULTI>(p, k.j, k.ju, k.jv, k.r0, k.r1, k.c0, k.c1, off, member, kTeam, lane, kj, vj,
+                                       dk, dv);
+#pragma unroll
+        for (int m = G; m < 64; m <<= 1)
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                dk[e] += __shfl_xor(dk[e], m);
+                dv[e] += __shfl_xor(dv[e], m);
+            }
+        if (member == 0) store_key_grads<T, D, G>(p, kg, lane, dk, dv);
+    }
+}
+
+template <typename T, int D>
+hipError_t run_backward(const BwdParams& p, hipStream_t st, hipEvent_t* ev)
+{
+    constexpr int G = Lanes<T, D>::kAttend;
+    constexpr uint32_t kQpb = Row<T, D, G>::kQpb;
+    const uint32_t qblocks = (p.n + kQpb - 1) / kQpb;
+    const uint32_t gblocks = static_cast<uint32_t>((static_cast<size_t>(p.kappa) * p.n + kQpb - 1) / kQpb);
+    const uint32_t kblocks = (p.keys_total + kQpb - 1) / kQpb;
+    hipEvent_t q0 = ev ? ev[2] : nullptr, q1 = ev ? ev[3] : nullptr, k0 = ev ? ev[4] : nullptr,
+               k1 = ev ? ev[5] : nullptr;
+    const bool multi = p.kappa > 1 || p.causal;
+    hipError_t e = multi ? launch(bwd_query_kernel<T, D, G, true>, qblocks, st, q0, q1, p)
+                         : launch(bwd_query_kernel<T, D, G, false>, qblocks, st, q0, q1, p);
+    if (e != hipSuccess) return e;
+    if ((e = launch(bwd_gather_kernel<T, D, G>, gblocks, st, k0, nullptr, p)) != hipSuccess) return e;
+    e = multi ? launch(bwd_key_kernel<T, D, G, true>, kblocks, st, nullptr, nullptr, p)
+              : launch(bwd_key_kernel<T, D, G, false>, kblocks, st, nullptr, nullptr, p);
+    if (e != hipSuccess) return e;
+    constexpr uint32_t kHeavyBlocks = 2048;  // loops over however many heavy keys there are
+    return multi ? launch(bwd_heavy_kernel<T, D, G, true>, kHeavyBlocks, st, nullptr, k1, p)
+                 : launch(bwd_heavy_kernel<T, D, G, false>, kHeavyBlocks, st, nullptr, k1, p);
+}
+
+}  // namespace
+
+size_t attend_backward_workspace_bytes(int S, int Hq, int Wq, int Hk, int Wk, int d, int dtype, int kappa)
+{
+    const size_t n = static_cast<size_t>(S) * Hq * Wq, N = static_cast<size_t>(S) * Hk * Wk;
+    const size_t tiles = (N + kScanTile - 1) / kScanTile;
+    const size_t row = static_cast<size_t>(d) * (dtype == SCRAM_BF16 ? 2 : 4);
+    auto r256 = [](size_t b) { return (b + 255) & ~static_cast<size_t>(255); };
+    return r256(4 * N) + r256(4 * (N + 1)) + r256(4 * (tiles + 1)) + r256(4 * n * kappa) + 2 * r256(4 * n) +
+           2 * r256(row * n * kappa) + r256(8 * n * kappa) + r256(4 * (N + 1));
+}
+
+hipError_t launch_attend_backward(int dtype, const void* Q, const void* K, const void* V, const int32_t* J, int kappa,
+                                  const Grid& g, int window, float scale, bool causal, const void* dO, float* dQ,
+                                  float* dK, float* dV, void* workspace, hipStream_t stream, hipEvent_t* events)
+{
+    BwdParams p{};
+    p.Q = Q;
+    p.K = K;
+    p.V = V;
+    p.J = J;
+    p.dO = dO;
+    p.dQ = dQ;
+    p.dK = dK;
+    p.dV = dV;
+    p.n = static_cast<uint32_t>(g.S) * g.Hq * g.Wq;
+    p.Hq = g.Hq;
+    p.Wq = g.Wq;
+    p.Hk = g.Hk;
+    p.Wk = g.Wk;
+    p.nkeys = static_cast<uint32_t>(g.Hk) * g.Wk;
+    p.keys_total = static_cast<uint32_t>(g.S) * p.nkeys;
+    p.div_plane = make_div(static_cast<uint32_t>(g.Hq) * g.Wq);
+    p.div_wk = make_div(g.Wk);
+    p.div_n = make_div(p.n);
+    p.div_keys = make_div(p.nkeys);
+    p.b = window / 2;
+    p.scale = scale;
+    p.scale_log2e = scale * 1.4426950408889634f;
+    p.kappa = kappa;
+    p.causal = causal ? 1 : 0;
+
+    // workspace: counts, offsets, tile sums, entries, log2 normalisers, D
+    const size_t N = p.keys_total;
+    const uint32_t tiles = static_cast<uint32_t>((N + kScanTile - 1) / kScanTile);
+    auto r256 = [](size_t b) { return (b + 255) & ~static_cast<size_t>(255); };
+    char* w = static_cast<char*>(workspace);
+    int32_t* counts = reinterpret_cast<int32_t*>(w);
+    w += r256(4 * N);
+    int32_t* offsets = reinterpret_cast<int32_t*>(w);
+    w += r256(4 * (N + 1));
+    int32_t* sums = reinterpret_cast<int32_t*>(w);
+    w += r256(4 * (static_cast<size_t>(tiles) + 1));
+    int32_t* entries = reinterpret_cast<int32_t*>(w);
+    w += r256(4 * static_cast<size_t>(p.n) * kappa);
+    p.lse2 = reinterpret_cast<float*>(w);
+    w += r256(4 * static_cast<size_t>(p.n));
+    p.Dq = reinterpret_cast<float*>(w);
+    w += r256(4 * static_cast<size_t>(p.n));
+    const size_t rows_bytes = static_cast<size_t>(g.d) * (dtype == SCRAM_BF16 ? 2 : 4) * p.n * kappa;
+    p.qs = w;
+    w += r256(rows_bytes);
+    p.gs = w;
+    w += r256(rows_bytes);
+    p.st = reinterpret_cast<float2*>(w);
+    w += r256(8 * static_cast<size_t>(p.n) * kappa);
+    p.n_heavy = reinterpret_cast<int32_t*>(w);  // counter, then the list
+    p.heavy = p.n_heavy + 1;
+    p.offsets = offsets;
+    p.entries = entries;
+
+    auto grid_for = [](size_t items) {
+        const size_t b = (items + kBlock - 1) / kBlock;
+        return static_cast<uint32_t>(b < 1 ? 1 : (b > 4096 ? 4096 : b));
+    };
+    hipEvent_t e0 = events ? events[0] : nullptr, e1 = events ? events[1] : nullptr;
+    const size_t entries_total = static_cast<size_t>(p.n) * kappa;
+    hipError_t e;
+    // inverse map: counting sort of the (query, match) entries by match key
+    if ((e = launch(zero_i32_kernel, grid_for(N), stream, e0, nullptr, counts, N)) != hipSuccess) return e;
+    if ((e = launch(bwd_count_kernel, grid_for(entries_total), stream, nullptr, nullptr, p, counts)) != hipSuccess)
+        return e;
+    if ((e = launch(scan_tiles_kernel, tiles, stream, nullptr, nullptr, static_cast<const int32_t*>(counts), offsets,
+                    sums, N)) != hipSuccess)
+        return e;
+    if ((e = launch(scan_sums_kernel, 1u, stream, nullptr, nullptr, sums, tiles)) != hipSuccess) return e;
+    if ((e = launch(scan_add_kernel, tiles, stream, nullptr, nullptr, offsets, static_cast<const int32_t*>(sums), N,
+                    tiles)) != hipSuccess)
+        return e;
+    if ((e = launch(bwd_fill_kernel, grid_for(entries_total), stream, nullptr, nullptr, p, counts, entries)) !=
+        hipSuccess)
+        return e;
+    if ((e = launch(zero_i32_kernel, 1u, stream, nullptr, e1, p.n_heavy, static_cast<size_t>(1))) != hipSuccess) return e;
+    // gradients
+    return dispatch(dtype, g.d, [&](auto ty, auto d) {
+        return run_backward<decltype(ty), decltype(d)::value>(p, stream, events);
+    });
+}
+
+}  // namespace scram

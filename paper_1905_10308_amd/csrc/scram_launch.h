@@ -1,5 +1,6 @@
 // Internal interface between the C-ABI front end (scram_api.cpp) and the
-// kernels (scram_kernels.hip).  Arguments reaching these functions have been
+// kernels (scram_pm.hip, scram_attend.hip, scram_backward.hip,
+// scram_snis.hip).  Arguments reaching these functions have been
 // validated by the front end.
 #pragma once
 
@@ -41,10 +42,11 @@ hipError_t launch_attend(int dtype, const void* Q, const void* K, const void* V,
                          hipEvent_t start, hipEvent_t stop);
 
 // Gradients of the attend step with the maps held fixed.  The workspace
-// (attend_backward_workspace_bytes) holds the inverse map and per-query
-// softmax statistics.  events: null or 6 (inverse map start/stop, query
-// kernel start/stop, key kernel start/stop).
-size_t attend_backward_workspace_bytes(int S, int Hq, int Wq, int Hk, int Wk, int kappa);
+// (attend_backward_workspace_bytes) holds the inverse map, per-query
+// softmax statistics and the entry-ordered copies of q, dO and those
+// statistics.  events: null or 6 (inverse map start/stop, query kernel
+// start/stop, key side (copies + key kernel) start/stop).
+size_t attend_backward_workspace_bytes(int S, int Hq, int Wq, int Hk, int Wk, int d, int dtype, int kappa);
 hipError_t launch_attend_backward(int dtype, const void* Q, const void* K, const void* V, const int32_t* J, int kappa,
                                   const Grid& g, int window, float scale, bool causal, const void* dO, float* dQ,
                                   float* dK, float* dV, void* workspace, hipStream_t stream, hipEvent_t* events);

@@ -52,7 +52,7 @@ def test_library_exports_every_declared_symbol(L):
 
 
 def test_abi_version(L):
-    assert L.scram_abi_version() == (2 << 16) | 3
+    assert L.scram_abi_version() == (2 << 16) | 4
 
 
 def test_status_strings(L):
@@ -195,13 +195,17 @@ def test_backward_workspace_formula(L):
     def r256(b):
         return (b + 255) // 256 * 256
 
-    for S, Hq, Wq, Hk, Wk, kappa in ((1, 1, 1, 1, 1, 1), (4, 256, 256, 256, 256, 1), (3, 7, 5, 9, 11, 3)):
+    for S, Hq, Wq, Hk, Wk, d, dtype, kappa in ((1, 1, 1, 1, 1, 16, F32, 1), (4, 256, 256, 256, 256, 64, BF16, 1),
+                                               (3, 7, 5, 9, 11, 128, F32, 3)):
         N, n = S * Hk * Wk, S * Hq * Wq
         tiles = (N + 2047) // 2048
-        want = r256(4 * N) + r256(4 * (N + 1)) + r256(4 * (tiles + 1)) + r256(4 * n * kappa) + 2 * r256(4 * n)
+        row = d * (2 if dtype == BF16 else 4)
+        want = (r256(4 * N) + r256(4 * (N + 1)) + r256(4 * (tiles + 1)) + r256(4 * n * kappa) + 2 * r256(4 * n)
+                + 2 * r256(row * n * kappa) + r256(8 * n * kappa) + r256(4 * (N + 1)))
         L.scram_sparse_attend_backward_workspace_bytes.restype = ctypes.c_size_t
-        assert L.scram_sparse_attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, kappa) == want
-    assert L.scram_sparse_attend_backward_workspace_bytes(0, 4, 4, 4, 4, 1) == 0
+        assert L.scram_sparse_attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, d, dtype, kappa) == want
+    assert L.scram_sparse_attend_backward_workspace_bytes(0, 4, 4, 4, 4, 16, F32, 1) == 0
+    assert L.scram_sparse_attend_backward_workspace_bytes(1, 4, 4, 4, 4, 24, F32, 1) == 0
 
 
 def test_python_binding_refuses_host_tensors():

@@ -153,20 +153,26 @@ def test_backward_events(scram):
     assert torch.equal(g1[0], g2[0])
 
 
-@pytest.mark.parametrize("pattern", ["one_key", "two_keys_and_random"])
+@pytest.mark.parametrize("pattern", ["one_key", "two_keys_and_random", "one_key_kappa2_causal"])
 def test_backward_hot_keys(scram, pattern):
-    """Skewed inverse maps: every query on one key, or most on two keys -- one bucket holds thousands of entries."""
+    """Skewed inverse maps: every query on one key, or most on two keys -- one bucket holds thousands of
+    entries, so those keys take the block-per-key path."""
     cfg = SMALL[1]
     a = si.make_arrays(cfg)
     dev = {k: to_dev(a[k], cfg.dtype) for k in ("Q", "K", "V")}
     rng = np.random.default_rng(17)
     n_keys = cfg.Hk * cfg.Wk
-    if pattern == "one_key":
+    causal = pattern.endswith("causal")
+    if pattern.startswith("one_key"):
         J = np.full((cfg.S, cfg.Hq, cfg.Wq), n_keys // 2, np.int32)
+        if "kappa2" in pattern:
+            J = np.stack([J, rng.integers(0, n_keys, J.shape).astype(np.int32)])
     else:
         J = rng.choice([0, n_keys - 1], size=(cfg.S, cfg.Hq, cfg.Wq)).astype(np.int32)
         J.reshape(-1)[::7] = rng.integers(0, n_keys, J.size)[::7]
     dO = to_dev(rng.standard_normal((cfg.S, cfg.Hq, cfg.Wq, cfg.dv)), cfg.dtype)
-    got = scram.sparse_attend_backward(dev["Q"], dev["K"], dev["V"], torch.from_numpy(J).cuda(), dO, 3, cfg.scale)
-    ref = oracle.sparse_attend_backward(a["Q"], a["K"], a["V"], J, 3, cfg.scale, dO.float().cpu().numpy())
+    got = scram.sparse_attend_backward(dev["Q"], dev["K"], dev["V"], torch.from_numpy(J).cuda(), dO, 3, cfg.scale,
+                                       causal=causal)
+    ref = oracle.sparse_attend_backward(a["Q"], a["K"], a["V"], J, 3, cfg.scale, dO.float().cpu().numpy(),
+                                        flags=oracle.CAUSAL if causal else 0)
     grads_close(got, ref, pattern)
