@@ -133,6 +133,8 @@ def main(argv=None) -> int:
     ap.add_argument("--snis", type=int, default=0, metavar="T",
                     help="estimate with T importance samples per query instead of the window softmax")
     ap.add_argument("--backward", action="store_true", help="add the attend backward (maps held fixed) to each step")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture one step in a HIP graph and time its replays (region A)")
     ap.add_argument("--alpha", type=float, default=0.9, help="SNIS mixture weight of the local densities")
     ap.add_argument("--radius", type=int, default=4, help="SNIS binomial radius m (variance m/2)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="seconds of oracle work for the CPU baseline")
@@ -217,13 +219,27 @@ def main(argv=None) -> int:
 
     for _ in range(args.warmup):
         step()
+    run = step
+    if args.graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            step()
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        run = graph.replay
+        for _ in range(args.warmup):
+            run()
     # timed region A: the path as a caller runs it (throughput)
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     start.record(stream)
     for _ in range(args.steps):
-        step()
+        run()
     stop.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
@@ -287,6 +303,7 @@ def main(argv=None) -> int:
             "causal": causal,
             "estimator": f"snis T={args.snis} alpha={args.alpha} m={args.radius}" if args.snis else "window",
             "backward": args.backward,
+            "launch": "hip graph replay" if args.graph else "eager",
             "queries_per_step": nq,
         },
         "roofline": {
