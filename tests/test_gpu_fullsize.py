@@ -13,6 +13,7 @@ import pytest
 
 import oracle
 import scram_inputs as si
+from scram_inputs.synth import resized
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -60,4 +61,32 @@ def test_full_size_sampled(scram, ci):
     err = np.abs(got - ref).max(axis=1) / np.maximum(np.abs(ref).max(axis=1), 1e-6)
     print(f"  sampled near ties {ties}, mismatches at them {mism}; attend max rel err {err.max():.3e}",
           flush=True)
+    assert err.max() <= TOL[cfg.dtype]
+
+
+def test_large_grid_sampled(scram):
+    """One 2048 x 2048 slice (4.2M queries, bf16, d=16: one lane per query): R = 2048 gives 12
+    random-search steps, whose 6 Philox blocks a query draws in rounds; the first three sweeps and the
+    attend output on sampled queries."""
+    cfg = resized(si.get(si.HEADLINE), batch=1, heads=1, Hq=2048, Wq=2048, Hk=2048, Wk=2048, d=16, F=128)
+    print(f"large-grid parity: {cfg.describe()}", flush=True)
+    data = si.make(cfg, device="cuda")
+    a = data["np"]
+    Q64, K64 = a["Q"].astype(np.float64), a["K"].astype(np.float64)
+    rng = np.random.default_rng(11)
+    ids = np.sort(rng.choice(cfg.nq, size=SAMPLES, replace=False))
+    J, s = scram.patchmatch(data["Q"], data["K"], 0, cfg.pm_seed, return_score=True)
+    J0, _ = oracle.pm_init(Q64, K64, cfg.pm_seed)
+    np.testing.assert_array_equal(J.cpu().numpy(), J0)
+    for t in range(1, 4):
+        Jprev = J.cpu().numpy()
+        J, s = scram.patchmatch(data["Q"], data["K"], 1, cfg.pm_seed, init=J, init_score=s, t0=t, return_score=True)
+        Jo, _, tie, _ = oracle.pm_iteration(Q64, K64, Jprev, t, cfg.pm_seed, query_ids=ids)
+        bad = (J.cpu().numpy().reshape(-1)[ids] != Jo) & ~tie
+        assert not bad.any(), f"sweep {t}: {int(bad.sum())} sampled mismatches outside near ties"
+    out = scram.sparse_attend(data["Q"], data["K"], data["V"], J, cfg.window, cfg.scale)
+    ref = oracle.sparse_attend(Q64, K64, a["V"].astype(np.float64), J.cpu().numpy(), cfg.window, cfg.scale,
+                               query_ids=ids)
+    got = out.float().reshape(cfg.nq, -1)[torch.from_numpy(ids).cuda()].cpu().numpy()
+    err = np.abs(got - ref).max(axis=1) / np.maximum(np.abs(ref).max(axis=1), 1e-6)
     assert err.max() <= TOL[cfg.dtype]
