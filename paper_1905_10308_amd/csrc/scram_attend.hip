@@ -30,9 +30,11 @@ struct AttParams {
 // then the W scores (base-2 domain), one online-softmax rescale, and the
 // value accumulation.  Keys outside the grid read a clamped (valid) row and
 // get weight 0; window rows entirely outside the grid are skipped.
-template <typename T, int D, int G, int W, bool MULTI>
+// MK = 0: one window, no mask; MK >= 1: up to MK windows and/or the causal mask.
+template <typename T, int D, int G, int W, int MK>
 __global__ __launch_bounds__(kBlock) void attend_window_kernel(AttParams p)
 {
+    constexpr bool MULTI = MK > 0;
     using RW = Row<T, D, G>;
     constexpr int CH = RW::kCh;
     constexpr int E = CH * RW::kEpc;  // channels per lane
@@ -49,8 +51,8 @@ __global__ __launch_bounds__(kBlock) void attend_window_kernel(AttParams p)
     const T* Vs = static_cast<const T*>(p.V) + slice;
     uint4 q[CH];
     load_row<T, D, G>(static_cast<const T*>(p.Q), g, lane, q);
-    WindowSet wset;
-    if constexpr (MULTI) wset = make_window_set(p, g, rem);
+    WindowSet<(MK > 0 ? MK : 1)> wset;
+    if constexpr (MULTI) wset = make_window_set<MK>(p, g, rem);
     const int nwin = MULTI ? p.kappa : 1;
 
     float m = -INFINITY, l = 0.f;
@@ -61,14 +63,7 @@ __global__ __launch_bounds__(kBlock) void attend_window_kernel(AttParams p)
     for (int e = 0; e < nwin; ++e) {
         uint32_t u, v;
         if constexpr (MULTI) {
-            u = static_cast<uint32_t>(wset.cu[0]);
-            v = static_cast<uint32_t>(wset.cv[0]);
-#pragma unroll
-            for (int f = 1; f < kMaxKappa; ++f)
-                if (f == e) {
-                    u = static_cast<uint32_t>(wset.cu[f]);
-                    v = static_cast<uint32_t>(wset.cv[f]);
-                }
+            wset.centre(e, u, v);
         } else {
             divmod(static_cast<uint32_t>(clamp_index(p.J[g], p.nkeys)), p.div_wk, u, v);
         }
@@ -120,9 +115,10 @@ __global__ __launch_bounds__(kBlock) void attend_window_kernel(AttParams p)
 // Any window side: the clipped window is visited in row order, kNb keys at a
 // time with their key and value loads in flight together; an online softmax
 // keeps (running max m, running sum l, accumulator) in the base-2 domain.
-template <typename T, int D, int G, bool MULTI>
+template <typename T, int D, int G, int MK>
 __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
 {
+    constexpr bool MULTI = MK > 0;
     using RW = Row<T, D, G>;
     constexpr int CH = RW::kCh;
     constexpr int E = CH * RW::kEpc;
@@ -139,8 +135,8 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
     const T* Vs = static_cast<const T*>(p.V) + slice;
     uint4 q[CH];
     load_row<T, D, G>(static_cast<const T*>(p.Q), g, lane, q);
-    WindowSet wset;
-    if constexpr (MULTI) wset = make_window_set(p, g, rem);
+    WindowSet<(MK > 0 ? MK : 1)> wset;
+    if constexpr (MULTI) wset = make_window_set<MK>(p, g, rem);
     const int nsets = MULTI ? p.kappa : 1;
 
     float m = -INFINITY, l = 0.f;
@@ -151,14 +147,7 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
     for (int e = 0; e < nsets; ++e) {
         uint32_t u, v;
         if constexpr (MULTI) {
-            u = static_cast<uint32_t>(wset.cu[0]);
-            v = static_cast<uint32_t>(wset.cv[0]);
-#pragma unroll
-            for (int f = 1; f < kMaxKappa; ++f)
-                if (f == e) {
-                    u = static_cast<uint32_t>(wset.cu[f]);
-                    v = static_cast<uint32_t>(wset.cv[f]);
-                }
+            wset.centre(e, u, v);
         } else {
             divmod(static_cast<uint32_t>(clamp_index(p.J[g], p.nkeys)), p.div_wk, u, v);
         }
@@ -209,17 +198,17 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
     store_row<T, D, G>(p.out, g, lane, acc, l > 0.f ? 1.f / l : 0.f);  // an empty set gives a zero row
 }
 
-template <typename T, int D, bool MULTI>
+template <typename T, int D, int MK>
 hipError_t run_attend_m(const AttParams& p, int window, uint32_t blocks, hipStream_t st, hipEvent_t e0,
                         hipEvent_t e1)
 {
     constexpr int G = Lanes<T, D>::kAttend;
     switch (window) {
-        case 1: return launch(attend_window_kernel<T, D, G, 1, MULTI>, blocks, st, e0, e1, p);
-        case 3: return launch(attend_window_kernel<T, D, G, 3, MULTI>, blocks, st, e0, e1, p);
-        case 5: return launch(attend_window_kernel<T, D, G, 5, MULTI>, blocks, st, e0, e1, p);
-        case 7: return launch(attend_window_kernel<T, D, G, 7, MULTI>, blocks, st, e0, e1, p);
-        default: return launch(attend_kernel<T, D, G, MULTI>, blocks, st, e0, e1, p);
+        case 1: return launch(attend_window_kernel<T, D, G, 1, MK>, blocks, st, e0, e1, p);
+        case 3: return launch(attend_window_kernel<T, D, G, 3, MK>, blocks, st, e0, e1, p);
+        case 5: return launch(attend_window_kernel<T, D, G, 5, MK>, blocks, st, e0, e1, p);
+        case 7: return launch(attend_window_kernel<T, D, G, 7, MK>, blocks, st, e0, e1, p);
+        default: return launch(attend_kernel<T, D, G, MK>, blocks, st, e0, e1, p);
     }
 }
 
@@ -228,8 +217,14 @@ hipError_t run_attend(const AttParams& p, int window, hipStream_t st, hipEvent_t
 {
     constexpr int G = Lanes<T, D>::kAttend;
     const uint32_t blocks = (p.n + Row<T, D, G>::kQpb - 1) / Row<T, D, G>::kQpb;
-    if (p.kappa > 1 || p.causal) return run_attend_m<T, D, true>(p, window, blocks, st, e0, e1);
-    return run_attend_m<T, D, false>(p, window, blocks, st, e0, e1);
+    // the smallest register budget that holds this call's window centres
+    if (p.kappa == 1) {
+        return p.causal ? run_attend_m<T, D, 1>(p, window, blocks, st, e0, e1)
+                        : run_attend_m<T, D, 0>(p, window, blocks, st, e0, e1);
+    }
+    if (p.kappa == 2) return run_attend_m<T, D, 2>(p, window, blocks, st, e0, e1);
+    if (p.kappa <= 4) return run_attend_m<T, D, 4>(p, window, blocks, st, e0, e1);
+    return run_attend_m<T, D, kMaxKappa>(p, window, blocks, st, e0, e1);
 }
 
 }  // namespace

@@ -188,8 +188,8 @@ __global__ __launch_bounds__(kBlock) void bwd_query_kernel(BwdParams p)
     uint4 q[CH], go[CH];
     load_row<T, D, G>(static_cast<const T*>(p.Q), g, lane, q);
     load_row<T, D, G>(static_cast<const T*>(p.dO), g, lane, go);
-    WindowSet wset;
-    if constexpr (MULTI) wset = make_window_set(p, g, rem);
+    WindowSet<kMaxKappa> wset;
+    if constexpr (MULTI) wset = make_window_set<kMaxKappa>(p, g, rem);
     const int nsets = MULTI ? p.kappa : 1;
 
     // visit(fn): every key of the set, kNb at a time with their key and
@@ -198,14 +198,7 @@ __global__ __launch_bounds__(kBlock) void bwd_query_kernel(BwdParams p)
         for (int e = 0; e < nsets; ++e) {
             uint32_t u, v;
             if constexpr (MULTI) {
-                u = static_cast<uint32_t>(wset.cu[0]);
-                v = static_cast<uint32_t>(wset.cv[0]);
-#pragma unroll
-                for (int f = 1; f < kMaxKappa; ++f)
-                    if (f == e) {
-                        u = static_cast<uint32_t>(wset.cu[f]);
-                        v = static_cast<uint32_t>(wset.cv[f]);
-                    }
+                wset.centre(e, u, v);
             } else {
                 divmod(static_cast<uint32_t>(clamp_index(p.J[g], p.nkeys)), p.div_wk, u, v);
             }

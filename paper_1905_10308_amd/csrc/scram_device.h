@@ -308,37 +308,51 @@ __device__ __forceinline__ void store_row(void* out, uint32_t g, int lane, const
     }
 }
 
-// Several windows and/or the causal mask: the centres of all kappa windows
-// and the query's raster index.  skip(e, r, c): key (r, c) of window e is
-// left out because an earlier window already holds it or it comes after the
-// query.
+// Several windows and/or the causal mask: the centres of the kappa <= MK
+// windows (MK a compile-time bound, so they live in registers) and the
+// query's raster index.  skip(e, r, c): key (r, c) of window e is left out
+// because an earlier window already holds it or it comes after the query.
+template <int MK>
 struct WindowSet {
     int kappa, b;
     bool causal;
     uint32_t local, Wk;
-    int cu[kMaxKappa], cv[kMaxKappa];
+    int cu[MK], cv[MK];
 
     __device__ bool skip(int e, int r, int c) const
     {
         bool s = causal && static_cast<uint32_t>(r) * Wk + static_cast<uint32_t>(c) > local;
 #pragma unroll
-        for (int f = 0; f < kMaxKappa; ++f)
+        for (int f = 0; f < MK; ++f)
             if (f < e) s = s || (abs(r - cu[f]) <= b && abs(c - cv[f]) <= b);
         return s;
     }
+
+    // centre (u, v) of window e
+    __device__ void centre(int e, uint32_t& u, uint32_t& v) const
+    {
+        u = static_cast<uint32_t>(cu[0]);
+        v = static_cast<uint32_t>(cv[0]);
+#pragma unroll
+        for (int f = 1; f < MK; ++f)
+            if (f == e) {
+                u = static_cast<uint32_t>(cu[f]);
+                v = static_cast<uint32_t>(cv[f]);
+            }
+    }
 };
 
-template <typename P>
-__device__ __forceinline__ WindowSet make_window_set(const P& p, uint32_t g, uint32_t rem)
+template <int MK, typename P>
+__device__ __forceinline__ WindowSet<MK> make_window_set(const P& p, uint32_t g, uint32_t rem)
 {
-    WindowSet ws;
+    WindowSet<MK> ws;
     ws.kappa = p.kappa;
     ws.b = p.b;
     ws.causal = p.causal != 0;
     ws.local = rem;
     ws.Wk = static_cast<uint32_t>(p.Wk);
 #pragma unroll
-    for (int e = 0; e < kMaxKappa; ++e) {
+    for (int e = 0; e < MK; ++e) {
         uint32_t u = 0, v = 0;
         if (e < p.kappa)
             divmod(static_cast<uint32_t>(clamp_index(p.J[static_cast<size_t>(e) * p.n + g], p.nkeys)), p.div_wk, u, v);

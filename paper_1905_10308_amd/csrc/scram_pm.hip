@@ -33,18 +33,21 @@ struct PmParams {
 constexpr int kMaxPrev = 7;  // previous runs a PatchMatch run may be constrained by
 
 // is_index_valid for one query: not after the query when causal, and at
-// Chebyshev distance >= sep from each previous run's match.
+// Chebyshev distance >= sep from each previous run's match (at most NP of
+// them, a compile-time bound so the matches live in registers).
+template <int NP>
 struct Validity {
+    static constexpr int kSlots = NP > 0 ? NP : 1;
     int n, sep;
     bool causal;
     uint32_t local;  // the query's raster index in its slice
-    uint32_t pu[kMaxPrev], pv[kMaxPrev];
+    uint32_t pu[kSlots], pv[kSlots];
 
     __device__ bool ok(uint32_t r, uint32_t c, int32_t idx) const
     {
         bool v = !(causal && static_cast<uint32_t>(idx) > local);
 #pragma unroll
-        for (int i = 0; i < kMaxPrev; ++i) {
+        for (int i = 0; i < NP; ++i) {
             if (i < n) {
                 const int du = abs(static_cast<int>(r) - static_cast<int>(pu[i]));
                 const int dv = abs(static_cast<int>(c) - static_cast<int>(pv[i]));
@@ -109,9 +112,12 @@ __global__ __launch_bounds__(kBlock) void pm_init_kernel(PmParams p)
 // Because "better" is a strict total order, visiting the candidates of
 // stage 1 in any order gives the same result as the order of Algorithm 1.
 // ---------------------------------------------------------------------------
-template <typename T, int D, int G, int QPG, int kNb, bool PROP, bool RS, bool VALID>
+// NP < 0: no validity test (a single-match run without masking); NP >= 0:
+// causal masking and/or up to NP previous runs.
+template <typename T, int D, int G, int QPG, int kNb, bool PROP, bool RS, int NP>
 __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
 {
+    constexpr bool VALID = NP >= 0;
     using RW = Row<T, D, G>;
     constexpr int CH = RW::kCh;
     constexpr int kGroups = RW::kQpb;           // lane groups per block
@@ -150,7 +156,7 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
     }
     // validity variant: the previous runs' matches of each query; an invalid
     // incumbent counts as minus infinity
-    Validity val[QPG];
+    Validity<NP> val[QPG];
     if constexpr (VALID) {
 #pragma unroll
         for (int j = 0; j < QPG; ++j) {
@@ -159,7 +165,7 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
             val[j].causal = p.causal != 0;
             val[j].local = x[j] * p.Wq + y[j];
 #pragma unroll
-            for (int i = 0; i < kMaxPrev; ++i) {
+            for (int i = 0; i < Validity<NP>::kSlots; ++i) {
                 val[j].pu[i] = val[j].pv[i] = 0u;
                 if (i < p.n_prev)
                     divmod(static_cast<uint32_t>(clamp_index(p.prev[static_cast<size_t>(i) * p.n + g[j]], p.nkeys)),
@@ -376,7 +382,7 @@ hipError_t run_init(const PmParams& p, hipStream_t st, hipEvent_t e0, hipEvent_t
 #define SCRAM_PM_BATCH 4
 #endif
 
-template <typename T, int D, bool VALID>
+template <typename T, int D, int NP>
 hipError_t run_iter_v(const PmParams& p, uint32_t flags, uint32_t blocks, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
 {
     constexpr int G = Lanes<T, D>::kPm;
@@ -384,10 +390,10 @@ hipError_t run_iter_v(const PmParams& p, uint32_t flags, uint32_t blocks, hipStr
     constexpr int NB = SCRAM_PM_BATCH;
     const bool prop = !(flags & SCRAM_PM_NO_PROPAGATION);
     const bool rs = !(flags & SCRAM_PM_NO_RANDOM_SEARCH);
-    if (prop && rs) return launch(pm_iter_kernel<T, D, G, QPG, NB, true, true, VALID>, blocks, st, e0, e1, p);
-    if (prop) return launch(pm_iter_kernel<T, D, G, QPG, NB, true, false, VALID>, blocks, st, e0, e1, p);
-    if (rs) return launch(pm_iter_kernel<T, D, G, QPG, NB, false, true, VALID>, blocks, st, e0, e1, p);
-    return launch(pm_iter_kernel<T, D, G, QPG, NB, false, false, VALID>, blocks, st, e0, e1, p);
+    if (prop && rs) return launch(pm_iter_kernel<T, D, G, QPG, NB, true, true, NP>, blocks, st, e0, e1, p);
+    if (prop) return launch(pm_iter_kernel<T, D, G, QPG, NB, true, false, NP>, blocks, st, e0, e1, p);
+    if (rs) return launch(pm_iter_kernel<T, D, G, QPG, NB, false, true, NP>, blocks, st, e0, e1, p);
+    return launch(pm_iter_kernel<T, D, G, QPG, NB, false, false, NP>, blocks, st, e0, e1, p);
 }
 
 template <typename T, int D>
@@ -396,8 +402,14 @@ hipError_t run_iter(const PmParams& p, uint32_t flags, hipStream_t st, hipEvent_
     constexpr int G = Lanes<T, D>::kPm;
     constexpr int kQpb = Row<T, D, G>::kQpb * SCRAM_PM_QPG;
     const uint32_t blocks = (p.n + kQpb - 1) / kQpb;
-    if (p.n_prev > 0 || p.causal) return run_iter_v<T, D, true>(p, flags, blocks, st, e0, e1);
-    return run_iter_v<T, D, false>(p, flags, blocks, st, e0, e1);
+    // the smallest register budget that holds this run's previous matches
+    if (p.n_prev == 0) {
+        return p.causal ? run_iter_v<T, D, 0>(p, flags, blocks, st, e0, e1)
+                        : run_iter_v<T, D, -1>(p, flags, blocks, st, e0, e1);
+    }
+    if (p.n_prev <= 1) return run_iter_v<T, D, 1>(p, flags, blocks, st, e0, e1);
+    if (p.n_prev <= 3) return run_iter_v<T, D, 3>(p, flags, blocks, st, e0, e1);
+    return run_iter_v<T, D, kMaxPrev>(p, flags, blocks, st, e0, e1);
 }
 
 }  // namespace
