@@ -61,10 +61,12 @@ __device__ __forceinline__ float axis_density(int r, int centre, int len, int m,
     return x < -m ? 0.f : (x >= m ? 1.f : cdf[x + m]);
 }
 
-// Sample t of query g: flat key index and log2 of its importance density.
-__device__ __forceinline__ void snis_draw(const SnisParams& p, uint32_t g, uint32_t t, const int (&cu)[kMaxKappa],
-                                          const int (&cv)[kMaxKappa], const float* pmf, const float* cdf,
-                                          int32_t& j, float& lr2)
+// Sample t of query g: flat key index and log2 of its importance density
+// (the query's kappa <= MK modes in cu, cv).
+template <int MK>
+__device__ __forceinline__ void snis_draw(const SnisParams& p, uint32_t g, uint32_t t, const int (&cu)[MK],
+                                          const int (&cv)[MK], const float* pmf, const float* cdf, int32_t& j,
+                                          float& lr2)
 {
     const uint4 w = philox4x32_10(g, t, 0u, kSnisStream, p.key0, p.key1);
     int r, c;
@@ -72,7 +74,7 @@ __device__ __forceinline__ void snis_draw(const SnisParams& p, uint32_t g, uint3
         const uint32_t e = __umulhi(w.y, static_cast<uint32_t>(p.kappa));
         int u = cu[0], v = cv[0];
 #pragma unroll
-        for (int f = 1; f < kMaxKappa; ++f)
+        for (int f = 1; f < MK; ++f)
             if (static_cast<uint32_t>(f) == e) {
                 u = cu[f];
                 v = cv[f];
@@ -87,14 +89,21 @@ __device__ __forceinline__ void snis_draw(const SnisParams& p, uint32_t g, uint3
     j = r * p.Wk + c;
     float local = 0.f;
 #pragma unroll
-    for (int e = 0; e < kMaxKappa; ++e)
+    for (int e = 0; e < MK; ++e)
         if (e < p.kappa)
             local += axis_density(r, cu[e], p.Hk, p.m, pmf, cdf) * axis_density(c, cv[e], p.Wk, p.m, pmf, cdf);
     lr2 = log2f(fmaf(p.w_local, local, p.w_unif));
 }
 
-template <typename T, int D, int G, bool VAR>
-__global__ __launch_bounds__(kBlock) void snis_kernel(SnisParams p)
+// Without the variance pass and with at most two modes the kernel fits 128
+// VGPRs, i.e. four waves per SIMD; ask for that.  Otherwise the compiler's own
+// allocation (three waves) stands.
+template <bool VAR, int MK>
+constexpr int snis_waves() { return !VAR && MK <= 2 ? 4 : 1; }
+
+template <typename T, int D, int G, bool VAR, int MK>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(snis_waves<VAR, MK>())))
+void snis_kernel(SnisParams p)
 {
     using RW = Row<T, D, G>;
     constexpr int CH = RW::kCh;
@@ -130,9 +139,9 @@ __global__ __launch_bounds__(kBlock) void snis_kernel(SnisParams p)
     const T* Vs = static_cast<const T*>(p.V) + slice;
     uint4 q[CH];
     load_row<T, D, G>(static_cast<const T*>(p.Q), g, lane, q);
-    int cu[kMaxKappa], cv[kMaxKappa];
+    int cu[MK], cv[MK];
 #pragma unroll
-    for (int e = 0; e < kMaxKappa; ++e) {
+    for (int e = 0; e < MK; ++e) {
         uint32_t u = 0, v = 0;
         if (e < p.kappa)
             divmod(static_cast<uint32_t>(clamp_index(p.modes[static_cast<size_t>(e) * p.n + g], p.nkeys)), p.div_wk,
@@ -151,7 +160,7 @@ __global__ __launch_bounds__(kBlock) void snis_kernel(SnisParams p)
             const int sl = lane + i * G;
             mj[i] = 0;
             ml[i] = 0.f;
-            if (sl < kNb && t0 + sl < p.samples) snis_draw(p, g, t0 + sl, cu, cv, s_pmf, s_cdf, mj[i], ml[i]);
+            if (sl < kNb && t0 + sl < p.samples) snis_draw<MK>(p, g, t0 + sl, cu, cv, s_pmf, s_cdf, mj[i], ml[i]);
         }
         int32_t j[kNb];
         float lr[kNb];
@@ -243,8 +252,16 @@ hipError_t run_snis(const SnisParams& p, hipStream_t st, hipEvent_t e0, hipEvent
 {
     constexpr int G = Lanes<T, D>::kAttend;
     const uint32_t blocks = (p.n + Row<T, D, G>::kQpb - 1) / Row<T, D, G>::kQpb;
-    if (p.var) return launch(snis_kernel<T, D, G, true>, blocks, st, e0, e1, p);
-    return launch(snis_kernel<T, D, G, false>, blocks, st, e0, e1, p);
+    // the smallest register budget that holds the query's modes
+    auto go = [&](auto mk) {
+        constexpr int MK = decltype(mk)::value;
+        if (p.var) return launch(snis_kernel<T, D, G, true, MK>, blocks, st, e0, e1, p);
+        return launch(snis_kernel<T, D, G, false, MK>, blocks, st, e0, e1, p);
+    };
+    if (p.kappa == 1) return go(std::integral_constant<int, 1>{});
+    if (p.kappa == 2) return go(std::integral_constant<int, 2>{});
+    if (p.kappa <= 4) return go(std::integral_constant<int, 4>{});
+    return go(std::integral_constant<int, kMaxKappa>{});
 }
 
 }  // namespace
