@@ -237,7 +237,7 @@ int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype, 
  *   events    NULL or 6 events: start/stop of building the inverse map, of
  *             the per-query kernel and of the key side (row copies and the
  *             per-key kernel)
- * Also requires S*Hq*Wq*kappa < 2^31.  dQ, dK, dV must be 16-byte aligned;
+ * Also requires S*Hq*Wq*kappa < 2^31 and S*Hk*Wk < 2^31.  dQ, dK, dV must be 16-byte aligned;
  * no output or the workspace may overlap an input or another output.
  * Returns a status code.
  */

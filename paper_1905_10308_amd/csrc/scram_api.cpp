@@ -144,6 +144,15 @@ int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int
             if (e == hipSuccess && score_out && init_score)
                 e = hipMemcpyAsync(score_out, init_score, 4 * n, hipMemcpyDeviceToDevice, stream);
         }
+    } else if (iters > 0 && flags == 0) {
+        // the first sweep recomputes the random initial field itself: no
+        // init launch, and the init's event pair brackets no work
+        Jcur = nullptr;
+        scur = nullptr;
+        if (ev) {
+            e = hipEventRecord(ev[0], stream);
+            if (e == hipSuccess) e = hipEventRecord(ev[1], stream);
+        }
     } else {
         e = scram::launch_pm_init(dtype, Q, K, grid, seed, run, nullptr, Jbuf[p0], sbuf[p0], stream,
                                   ev ? ev[0] : nullptr, ev ? ev[1] : nullptr);
@@ -204,8 +213,10 @@ int scram_sparse_attend_backward(const void* Q, const void* K, const void* V, in
     if (!Q || !K || !V || !argmax || !dO || !dQ || !dK || !dV) return SCRAM_ERR_NULL;
     int rc = check_grid(S, Hq, Wq, Hk, Wk);
     if (rc) return rc;
-    // the inverse map codes (match, query) pairs as e * n + i in an int32
+    // the inverse map codes (match, query) pairs as e * n + i in an int32, and
+    // keys are numbered across slices (s * Hk * Wk + j)
     if (int64_t(S) * Hq * Wq * (kappa < 1 ? 1 : kappa) >= kMaxCount) return SCRAM_ERR_SHAPE;
+    if (int64_t(S) * Hk * Wk >= kMaxCount) return SCRAM_ERR_SHAPE;
     if (window < 1 || window % 2 == 0 || window > 32767) return SCRAM_ERR_SHAPE;
     if (kappa < 1 || kappa > SCRAM_MAX_KAPPA) return SCRAM_ERR_SHAPE;
     if (!isfinite(scale)) return SCRAM_ERR_SHAPE;

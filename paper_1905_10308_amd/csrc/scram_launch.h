@@ -31,7 +31,9 @@ hipError_t launch_pm_init(int dtype, const void* Q, const void* K, const Grid& g
                           const RunSpec& run, const int32_t* init, int32_t* J, float* s, hipStream_t stream,
                           hipEvent_t start, hipEvent_t stop);
 
-// One Jacobi sweep t: (Jp, sp) -> (Jn, sn).
+// One Jacobi sweep t: (Jp, sp) -> (Jn, sn).  Jp == sp == nullptr: the first
+// sweep of a run from the random initial field (flags must be 0), which the
+// sweep recomputes instead of reading.
 hipError_t launch_pm_iter(int dtype, const void* Q, const void* K, const Grid& g, uint64_t seed,
                           const RunSpec& run, uint32_t t, uint32_t flags, const int32_t* Jp, const float* sp,
                           int32_t* Jn, float* sn, hipStream_t stream, hipEvent_t start, hipEvent_t stop);

@@ -27,6 +27,7 @@ struct PmParams {
     int n_prev;           // also this run's index: Philox counter word 3
     int sep;              // minimum Chebyshev distance to every previous match
     int causal;           // keys after the query (raster order) are not valid
+    int first;            // the sweep recomputes the random initial field (Jp, sp unused)
 };
 
 
@@ -61,6 +62,19 @@ struct Validity {
 // ---------------------------------------------------------------------------
 // K1: initial field and its scores
 // ---------------------------------------------------------------------------
+
+// The random initial match of query g (raster index rem in its slice): the
+// Philox block (g, 0, 0, run) mapped onto the key grid, or, with the causal
+// mask, onto the keys up to the query.  The first sweep of a fresh run
+// recomputes its neighbours' initial matches with this same function.
+__device__ __forceinline__ int32_t initial_draw(const PmParams& p, uint32_t g, uint32_t rem)
+{
+    const uint4 w = philox4x32_10(g, 0u, 0u, static_cast<uint32_t>(p.n_prev), p.key0, p.key1);
+    if (p.causal) return static_cast<int32_t>(__umulhi(w.x, rem + 1u));
+    const uint32_t u = __umulhi(w.x, static_cast<uint32_t>(p.Hk));
+    const uint32_t v = __umulhi(w.y, static_cast<uint32_t>(p.Wk));
+    return static_cast<int32_t>(u * p.Wk + v);
+}
 template <typename T, int D, int G>
 __global__ __launch_bounds__(kBlock) void pm_init_kernel(PmParams p)
 {
@@ -71,19 +85,7 @@ __global__ __launch_bounds__(kBlock) void pm_init_kernel(PmParams p)
     uint32_t s, rem;
     divmod(g, p.div_plane, s, rem);
 
-    int32_t idx;
-    if (p.init) {
-        idx = clamp_index(p.init[g], p.nkeys);
-    } else {
-        const uint4 w = philox4x32_10(g, 0u, 0u, static_cast<uint32_t>(p.n_prev), p.key0, p.key1);
-        if (p.causal) {  // uniform over the keys up to the query's raster index
-            idx = static_cast<int32_t>(__umulhi(w.x, rem + 1u));
-        } else {
-            const uint32_t u = __umulhi(w.x, static_cast<uint32_t>(p.Hk));
-            const uint32_t v = __umulhi(w.y, static_cast<uint32_t>(p.Wk));
-            idx = static_cast<int32_t>(u * p.Wk + v);
-        }
-    }
+    const int32_t idx = p.init ? clamp_index(p.init[g], p.nkeys) : initial_draw(p, g, rem);
     const T* Ks = static_cast<const T*>(p.K) + static_cast<size_t>(s) * p.nkeys * D;
     uint4 q[RW::kCh], k[RW::kCh];
     load_row<T, D, G>(static_cast<const T*>(p.Q), g, lane, q);
@@ -113,8 +115,11 @@ __global__ __launch_bounds__(kBlock) void pm_init_kernel(PmParams p)
 // stage 1 in any order gives the same result as the order of Algorithm 1.
 // ---------------------------------------------------------------------------
 // NP < 0: no validity test (a single-match run without masking); NP >= 0:
-// causal masking and/or up to NP previous runs.
-template <typename T, int D, int G, int QPG, int kNb, bool PROP, bool RS, int NP>
+// causal masking and/or up to NP previous runs.  FIRST: the first sweep of a
+// run started from the random initial field, which is not read from memory:
+// each query recomputes its own initial match and those of its neighbours
+// (initial_draw) and scores its own.
+template <typename T, int D, int G, int QPG, int kNb, bool PROP, bool RS, int NP, bool FIRST = false>
 __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
 {
     constexpr bool VALID = NP >= 0;
@@ -150,9 +155,19 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
         divmod(rem, p.div_wq, x[j], y[j]);
         Ks[j] = static_cast<const T*>(p.K) + static_cast<size_t>(s[j]) * p.nkeys * D;
         load_row<T, D, G>(static_cast<const T*>(p.Q), g[j], lane, q[j]);
-        cur[j] = clamp_index(p.Jp[g[j]], p.nkeys);
+        if constexpr (FIRST) {
+            cur[j] = initial_draw(p, g[j], x[j] * p.Wq + y[j]);
+        } else {
+            cur[j] = clamp_index(p.Jp[g[j]], p.nkeys);
+            best[j] = p.sp[g[j]];
+        }
         cur0[j] = cur[j];
-        best[j] = p.sp[g[j]];
+    }
+    // FIRST: the incumbent's row, scored once stage 1's candidates are built
+    uint4 kinc[QPG][CH];
+    if constexpr (FIRST) {
+#pragma unroll
+        for (int j = 0; j < QPG; ++j) load_row<T, D, G>(Ks[j], cur[j], lane, kinc[j]);
     }
     // validity variant: the previous runs' matches of each query; an invalid
     // incumbent counts as minus infinity
@@ -171,9 +186,11 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
                     divmod(static_cast<uint32_t>(clamp_index(p.prev[static_cast<size_t>(i) * p.n + g[j]], p.nkeys)),
                            p.div_wk, val[j].pu[i], val[j].pv[i]);
             }
-            uint32_t u0, v0;
-            divmod(static_cast<uint32_t>(cur[j]), p.div_wk, u0, v0);
-            if (!val[j].ok(u0, v0, cur[j])) best[j] = -INFINITY;
+            if constexpr (!FIRST) {
+                uint32_t u0, v0;
+                divmod(static_cast<uint32_t>(cur[j]), p.div_wk, u0, v0);
+                if (!val[j].ok(u0, v0, cur[j])) best[j] = -INFINITY;
+            }
         }
     }
 
@@ -209,7 +226,12 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
                 const int oy = dir == 2 ? -jump : (dir == 3 ? jump : 0);
                 const int nx = static_cast<int>(x[j]) + ox, ny = static_cast<int>(y[j]) + oy;
                 if (nx >= 0 && nx < p.Hq && ny >= 0 && ny < p.Wq) {
-                    const uint32_t nb = clamp_index(Jp[(static_cast<size_t>(s[j]) * p.Hq + nx) * p.Wq + ny], p.nkeys);
+                    const uint32_t ng = static_cast<uint32_t>((static_cast<size_t>(s[j]) * p.Hq + nx) * p.Wq + ny);
+                    uint32_t nb;
+                    if constexpr (FIRST)
+                        nb = static_cast<uint32_t>(initial_draw(p, ng, static_cast<uint32_t>(nx * p.Wq + ny)));
+                    else
+                        nb = clamp_index(Jp[ng], p.nkeys);
                     uint32_t nu, nv;
                     divmod(nb, p.div_wk, nu, nv);
                     const int r = static_cast<int>(nu) - ox, cc = static_cast<int>(nv) - oy;
@@ -230,6 +252,17 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
             const uint32_t grp = static_cast<uint32_t>(bal >> gbase) & (G == 32 ? 0xFFFFFFFFu : ((1u << G) - 1u));
             if (keep) list[count[j] + __popc(grp & ((1u << lane) - 1u))] = c;
             count[j] += __popc(grp);
+        }
+    }
+    if constexpr (FIRST) {
+#pragma unroll
+        for (int j = 0; j < QPG; ++j) {
+            best[j] = row_score<T, D, G>(q[j], kinc[j]);
+            if constexpr (VALID) {
+                uint32_t u0, v0;
+                divmod(static_cast<uint32_t>(cur[j]), p.div_wk, u0, v0);
+                if (!val[j].ok(u0, v0, cur[j])) best[j] = -INFINITY;
+            }
         }
     }
     __syncthreads();
@@ -390,6 +423,7 @@ hipError_t run_iter_v(const PmParams& p, uint32_t flags, uint32_t blocks, hipStr
     constexpr int NB = SCRAM_PM_BATCH;
     const bool prop = !(flags & SCRAM_PM_NO_PROPAGATION);
     const bool rs = !(flags & SCRAM_PM_NO_RANDOM_SEARCH);
+    if (p.first) return launch(pm_iter_kernel<T, D, G, QPG, NB, true, true, NP, true>, blocks, st, e0, e1, p);
     if (prop && rs) return launch(pm_iter_kernel<T, D, G, QPG, NB, true, true, NP>, blocks, st, e0, e1, p);
     if (prop) return launch(pm_iter_kernel<T, D, G, QPG, NB, true, false, NP>, blocks, st, e0, e1, p);
     if (rs) return launch(pm_iter_kernel<T, D, G, QPG, NB, false, true, NP>, blocks, st, e0, e1, p);
@@ -434,6 +468,9 @@ hipError_t launch_pm_iter(int dtype, const void* Q, const void* K, const Grid& g
                           int32_t* Jn, float* sn, hipStream_t stream, hipEvent_t start, hipEvent_t stop)
 {
     PmParams p = make_pm_params(Q, K, g, seed);
+    // no previous map: the first sweep of a fresh run (propagation and random
+    // search both on) starts from the random initial field it recomputes
+    p.first = Jp == nullptr ? 1 : 0;
     p.t = t;
     p.Jp = Jp;
     p.sp = sp;

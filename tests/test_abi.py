@@ -184,6 +184,7 @@ def bw(L, **kw):
     (dict(dV=A_DK + 4 * 128 * 16 - 16), EALIAS), (dict(dQ=A_V + 32), EALIAS),
     (dict(ws=None), EWS), (dict(ws_bytes=100), EWS), (dict(ws=A_BW + 16), EALIGN), (dict(ws=A_DQ), EALIAS),
     (dict(ws=A_Q + 256), EALIAS), (dict(S=1 << 14, Hq=1 << 8, Wq=1 << 8, Hk=4, Wk=4, kappa=2), ESHAPE),
+    (dict(S=1 << 12, Hq=1, Wq=1, Hk=1 << 10, Wk=1 << 9), ESHAPE),
 ])
 
 

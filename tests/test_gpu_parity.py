@@ -256,3 +256,20 @@ def test_bad_arguments_raise(scram):
     Q = torch.zeros(1, 4, 4, 16, device="cuda")
     with pytest.raises(scram.ScramError):
         scram.sparse_attend(Q, Q, Q, torch.zeros(1, 4, 4, dtype=torch.int32, device="cuda"), 2)
+
+
+@pytest.mark.parametrize("variant", ["plain", "causal", "kappa2"])
+def test_fused_first_sweep_equals_init_then_sweep(scram, variant):
+    """A fresh run's first sweep recomputes the random initial field instead of reading it: it must equal
+    the init kernel followed by an ordinary sweep, bit for bit (maps and scores)."""
+    cfg = SMALL[2]
+    a = si.make_arrays(cfg)
+    Q, K = to_dev(a["Q"], cfg.dtype), to_dev(a["K"], cfg.dtype)
+    causal = variant == "causal"
+    prev = scram.patchmatch(Q, K, 2, cfg.pm_seed)[None] if variant == "kappa2" else None
+    kw = dict(prev=prev, sep=2, causal=causal)
+    J0, s0 = scram.patchmatch(Q, K, 0, cfg.pm_seed, return_score=True, **kw)
+    for T in (1, 3):
+        fused, sf = scram.patchmatch(Q, K, T, cfg.pm_seed, return_score=True, **kw)
+        split, ss = scram.patchmatch(Q, K, T, cfg.pm_seed, init=J0, init_score=s0, return_score=True, **kw)
+        assert torch.equal(fused, split) and torch.equal(sf, ss), f"T={T}"
