@@ -117,6 +117,35 @@ def cpu_baseline(cfg, arrays, min_s: float, kappa: int = 1, sep: int = 1, causal
     }
 
 
+def dense_attention(cfg, Q, K, V, reps: int = 3):
+    """Dense exact softmax attention over the same slices, for scale: torch's
+    scaled-dot-product attention restricted to its fused (flash / memory
+    efficient) kernels, so no n x n matrix is formed.  None if neither runs."""
+    import torch
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+
+    S, n = cfg.S, cfg.Hq * cfg.Wq
+    q = Q.reshape(S, 1, n, cfg.d).contiguous()
+    k = K.reshape(S, 1, cfg.Hk * cfg.Wk, cfg.d).contiguous()
+    v = V.reshape(S, 1, cfg.Hk * cfg.Wk, cfg.dv).contiguous()
+    for backend in (SDPBackend.EFFICIENT_ATTENTION, SDPBackend.FLASH_ATTENTION):
+        try:
+            with sdpa_kernel([backend]):
+                torch.nn.functional.scaled_dot_product_attention(q, k, v, scale=cfg.scale)
+                torch.cuda.synchronize()
+                start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                start.record()
+                for _ in range(reps):
+                    torch.nn.functional.scaled_dot_product_attention(q, k, v, scale=cfg.scale)
+                stop.record()
+                torch.cuda.synchronize()
+            return {"ms": start.elapsed_time(stop) / reps, "backend": f"torch SDPA {backend.name.lower()}",
+                    "dtype": str(q.dtype).replace("torch.", "")}
+        except RuntimeError:
+            continue
+    return None
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -324,6 +353,10 @@ def main(argv=None) -> int:
         "wall_ms_per_step": wall * 1e3 / args.steps,
         "device": torch.cuda.get_device_name(dev),
     }
+    dense = dense_attention(cfg, Q, K, V) if not (kappa > 1 or causal or args.snis) else None
+    if dense is not None:
+        dense["step_speedup"] = dense["ms"] / ms_step
+        res["dense_exact_attention"] = dense
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg, data["np"], args.cpu_seconds, kappa, sep, causal,
                                            (args.snis, args.alpha, args.radius) if args.snis else None)
