@@ -412,7 +412,7 @@ hipError_t run_init(const PmParams& p, hipStream_t st, hipEvent_t e0, hipEvent_t
 #define SCRAM_PM_QPG 1
 #endif
 #ifndef SCRAM_PM_BATCH
-#define SCRAM_PM_BATCH 4
+#define SCRAM_PM_BATCH 3
 #endif
 
 template <typename T, int D, int NP>
