@@ -104,7 +104,8 @@ def test_backward_full_window_is_dense(scram):
 
 
 @pytest.mark.parametrize("shape", [(1, 1, 1, 1, 1, 16, "f32"), (2, 3, 17, 5, 19, 128, "bf16"),
-                                   (1, 21, 1, 30, 1, 64, "f32"), (3, 9, 7, 4, 6, 32, "bf16")],
+                                   (1, 21, 1, 30, 1, 64, "f32"), (3, 9, 7, 4, 6, 32, "bf16"),
+                                   (2, 7, 9, 6, 5, 128, "f32"), (1, 13, 11, 13, 11, 16, "bf16")],
                          ids=lambda s: "x".join(map(str, s[:-1])) + s[-1])
 def test_backward_shapes(scram, shape):
     S, Hq, Wq, Hk, Wk, d, dtype = shape
