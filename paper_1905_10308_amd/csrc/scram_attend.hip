@@ -29,7 +29,9 @@ struct AttParams {
 // value rows of a window row are gathered together (2W loads in flight),
 // then the W scores (base-2 domain), one online-softmax rescale, and the
 // value accumulation.  Keys outside the grid read a clamped (valid) row and
-// get weight 0; window rows entirely outside the grid are skipped.
+// get weight 0; window rows entirely outside the grid are skipped, and so,
+// before any load, are rows whose every key an earlier window holds or the
+// causal mask drops.
 // MK = 0: one window, no mask; MK >= 1: up to MK windows and/or the causal mask.
 template <typename T, int D, int G, int W, int MK>
 __global__ __launch_bounds__(kBlock) void attend_window_kernel(AttParams p)
@@ -80,6 +82,17 @@ __global__ __launch_bounds__(kBlock) void attend_window_kernel(AttParams p)
             const int r = static_cast<int>(u) + a - B;
             if (r < 0 || r >= p.Hk) continue;
             const uint32_t row0 = static_cast<uint32_t>(r * p.Wk);
+            bool use[W];
+            bool any = false;
+#pragma unroll
+            for (int c = 0; c < W; ++c) {
+                use[c] = col_ok[c];
+                if constexpr (MULTI) use[c] = use[c] && !wset.skip(e, r, cols[c]);
+                any = any || use[c];
+            }
+            if constexpr (MULTI) {
+                if (!any) continue;
+            }
             uint4 kr[W][CH], vr[W][CH];
 #pragma unroll
             for (int c = 0; c < W; ++c) {
@@ -90,9 +103,7 @@ __global__ __launch_bounds__(kBlock) void attend_window_kernel(AttParams p)
             float mb = m;
 #pragma unroll
             for (int c = 0; c < W; ++c) {
-                bool use = col_ok[c];
-                if constexpr (MULTI) use = use && !wset.skip(e, r, cols[c]);
-                sc[c] = use ? row_score<T, D, G>(q, kr[c]) * p.scale_log2e : -INFINITY;
+                sc[c] = use[c] ? row_score<T, D, G>(q, kr[c]) * p.scale_log2e : -INFINITY;
                 mb = fmaxf(mb, sc[c]);
             }
             if (mb == -INFINITY) continue;  // nothing of this row is in the set
