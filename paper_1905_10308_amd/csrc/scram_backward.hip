@@ -12,9 +12,9 @@ namespace {
 // weights, dp_ij = dO_i . v_j and D_i = sum_j p_ij dp_ij:
 //   dQ_i = scale sum_j p_ij (dp_ij - D_i) k_j
 //   dK_j = scale sum_i p_ij (dp_ij - D_i) q_i,   dV_j = sum_i p_ij dO_i
-// Query side (one lane group per query): pass A walks W_i for the running
-// max, the normaliser and D_i and stores log2 of the normaliser (with the
-// max) and D_i; pass B walks it again for dQ_i.  Key side (one lane group
+// Query side (one lane group per query): one walk over W_i accumulates,
+// online, the normaliser, D_i and the two sums dQ_i is made of, and stores
+// log2 of the normaliser (with the max) and D_i for the key side.  Key side (one lane group
 // per key): key j lies in W_i exactly when a match of i lies in the
 // (2b+1)^2 neighbourhood of j, so the queries are found through the inverse
 // map -- the (query, match) entries sorted by match key (a counting sort).
@@ -174,7 +174,7 @@ __global__ __launch_bounds__(kBlock) void bwd_query_kernel(BwdParams p)
     constexpr int CH = RW::kCh;
     constexpr int E = CH * RW::kEpc;
     constexpr int kEpc = RW::kEpc;
-    constexpr int kNb = CH >= 2 ? 4 : 8;
+    constexpr int kNb = CH >= 2 ? 2 : 4;
     const int lane = threadIdx.x & (G - 1);
     const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
     const uint32_t g = blk * RW::kQpb + threadIdx.x / G;
@@ -227,8 +227,23 @@ __global__ __launch_bounds__(kBlock) void bwd_query_kernel(BwdParams p)
         }
     };
 
-    // pass A: running max m, normaliser l, sum of e^(a - m) dp (base-2 scores)
+    // One pass, online in the base-2 domain: running max m, normaliser l,
+    // dn = sum e^(a - m) dp, and with k~ = k_j - k_ref the sums
+    // A = sum e^(a - m) dp k~ and B = sum e^(a - m) k~.  Since the weights of
+    // the set sum to one, dQ_i = scale (A - D_i B) / l for any fixed k_ref;
+    // k_ref = the key at the first match keeps k~ small where neighbouring
+    // keys are alike, so A - D_i B does not cancel, and a one-key set gives
+    // exactly zero.
+    float kref[E];
+    {
+        uint4 kr0[CH];
+        load_row<T, D, G>(Ks, clamp_index(p.J[g], p.nkeys), lane, kr0);
+        unpack_row<T, CH>(kr0, kref);
+    }
     float m = -INFINITY, l = 0.f, dn = 0.f;
+    float acc_a[E], acc_b[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc_a[e] = acc_b[e] = 0.f;
     visit([&](const bool (&ok)[kNb], const uint4 (&kr)[kNb][CH], const uint4 (&vr)[kNb][CH]) {
         float sc[kNb], dp[kNb];
         float mb = m;
@@ -243,10 +258,24 @@ __global__ __launch_bounds__(kBlock) void bwd_query_kernel(BwdParams p)
         l *= alpha;
         dn *= alpha;
 #pragma unroll
+        for (int e = 0; e < E; ++e) {
+            acc_a[e] *= alpha;
+            acc_b[e] *= alpha;
+        }
+#pragma unroll
         for (int j = 0; j < kNb; ++j) {
-            const float pj = __builtin_amdgcn_exp2f(sc[j] - mb);
+            const float pj = __builtin_amdgcn_exp2f(sc[j] - mb);  // 0 when !ok
+            const float pd = pj * dp[j];
             l += pj;
-            dn = fmaf(pj, dp[j], dn);
+            dn += pd;
+            float kf[E];
+            unpack_row<T, CH>(kr[j], kf);
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const float kd = kf[e] - kref[e];
+                acc_a[e] = fmaf(pd, kd, acc_a[e]);
+                acc_b[e] = fmaf(pj, kd, acc_b[e]);
+            }
         }
         m = mb;
     });
@@ -256,25 +285,9 @@ __global__ __launch_bounds__(kBlock) void bwd_query_kernel(BwdParams p)
         p.lse2[g] = l > 0.f ? m + log2f(l) : INFINITY;  // +inf: every weight is 0
         p.Dq[g] = Dg;
     }
-
-    // pass B: dQ with the exact weights
     float dq[E];
 #pragma unroll
-    for (int e = 0; e < E; ++e) dq[e] = 0.f;
-    if (l > 0.f) {
-        visit([&](const bool (&ok)[kNb], const uint4 (&kr)[kNb][CH], const uint4 (&vr)[kNb][CH]) {
-#pragma unroll
-            for (int j = 0; j < kNb; ++j) {
-                const float sc = ok[j] ? row_score<T, D, G>(q, kr[j]) * p.scale_log2e : -INFINITY;
-                const float dp = row_score<T, D, G>(go, vr[j]);
-                const float ds = __builtin_amdgcn_exp2f(sc - m) * inv * (dp - Dg);  // 0 when !ok
-                float kf[E];
-                unpack_row<T, CH>(kr[j], kf);
-#pragma unroll
-                for (int e = 0; e < E; ++e) dq[e] = fmaf(ds, kf[e], dq[e]);
-            }
-        });
-    }
+    for (int e = 0; e < E; ++e) dq[e] = (acc_a[e] - Dg * acc_b[e]) * inv;
 #pragma unroll
     for (int cc = 0; cc < CH; ++cc) {
         float4* o = reinterpret_cast<float4*>(p.dQ + static_cast<size_t>(g) * D + (cc * G + lane) * kEpc);
