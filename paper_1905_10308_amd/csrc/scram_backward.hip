@@ -381,12 +381,16 @@ __device__ __forceinline__ void key_batch(const BwdParams& p, const int (&x)[kNb
 }
 
 // Keys whose neighbourhood holds more entries than this are handed to
-// bwd_heavy_kernel (a whole wave per key) instead of one lane group.
+// bwd_heavy_kernel (a team of lane groups per key) instead of one lane group.
 #ifndef SCRAM_BWD_HEAVY_ENTRIES
 #define SCRAM_BWD_HEAVY_ENTRIES 64
 #endif
 constexpr int kHeavyEntries = SCRAM_BWD_HEAVY_ENTRIES;
-constexpr int kMaxRows = 8;  // neighbourhoods of up to this many rows are walked as one flat list
+constexpr int kMaxRows = 8;
+// Lane groups that share one heavy key (half a wave at four lanes per group).
+#ifndef SCRAM_BWD_TEAM
+#define SCRAM_BWD_TEAM 8
+#endif  // neighbourhoods of up to this many rows are walked as one flat list
 
 // The entry ranges of the neighbourhood rows r0..r1 of key j: row i covers
 // entries [lo[i], lo[i] + pre[i+1] - pre[i]); pre[] is the running count.
@@ -432,7 +436,7 @@ __device__ __forceinline__ void key_accumulate(const BwdParams& p, uint32_t j, u
                                                int lane, const uint4 (&kj)[Row<T, D, G>::kCh],
                                                const uint4 (&vj)[Row<T, D, G>::kCh], float* dk, float* dv)
 {
-    constexpr int kNb = Row<T, D, G>::kCh >= 2 ? 4 : 8;
+    constexpr int kNb = Row<T, D, G>::kCh >= 2 ? 2 : 4;
     if (r1 - r0 + 1 <= kMaxRows) {
         const Neighbourhood nb = load_neighbourhood(off, p.Wk, r0, r1, c0, c1);
         for (int v0 = member; v0 < nb.total; v0 += kNb * team) {
@@ -531,20 +535,22 @@ __global__ __launch_bounds__(kBlock) void bwd_key_kernel(BwdParams p)
     store_key_grads<T, D, G>(p, kg, lane, dk, dv);
 }
 
-// The heavy keys, one wave each (waves take keys w, w + total waves, ...):
-// the wave's lane groups stride over the key's entries and their partial
-// sums are added across the wave with xor shuffles.
+// The heavy keys, one team of SCRAM_BWD_TEAM lane groups each (teams take
+// keys w, w + total teams, ...): the team's lane groups stride over the
+// key's entries and their partial sums are added across the team with xor
+// shuffles.
 template <typename T, int D, int G, bool MULTI>
 __global__ __launch_bounds__(kBlock) void bwd_heavy_kernel(BwdParams p)
 {
     using RW = Row<T, D, G>;
     constexpr int CH = RW::kCh;
     constexpr int E = CH * RW::kEpc;
-    constexpr int kTeam = 64 / G;  // lane groups per wave
+    constexpr int kTeam = SCRAM_BWD_TEAM * G <= 64 ? SCRAM_BWD_TEAM : 64 / G;  // lane groups per key
+    constexpr int kTeamLanes = kTeam * G;
     const int lane = threadIdx.x & (G - 1);
-    const int member = (threadIdx.x & 63) / G;
-    const int wave = blockIdx.x * (kBlock / 64) + threadIdx.x / 64;
-    const int waves = gridDim.x * (kBlock / 64);
+    const int member = (threadIdx.x & (kTeamLanes - 1)) / G;
+    const int wave = blockIdx.x * (kBlock / kTeamLanes) + threadIdx.x / kTeamLanes;
+    const int waves = gridDim.x * (kBlock / kTeamLanes);
     const int n_heavy = *p.n_heavy;
     for (int h = wave; h < n_heavy; h += waves) {
         const uint32_t kg = static_cast<uint32_t>(p.heavy[h]);
@@ -559,7 +565,7 @@ __global__ __launch_bounds__(kBlock) void bwd_heavy_kernel(BwdParams p)
         key_accumulate<T, D, G, MULTI>(p, k.j, k.ju, k.jv, k.r0, k.r1, k.c0, k.c1, off, member, kTeam, lane, kj, vj,
                                        dk, dv);
 #pragma unroll
-        for (int m = G; m < 64; m <<= 1)
+        for (int m = G; m < kTeamLanes; m <<= 1)
 #pragma unroll
             for (int e = 0; e < E; ++e) {
                 dk[e] += __shfl_xor(dk[e], m);
