@@ -187,18 +187,22 @@ def pm_iteration(Q, K, J_prev, t, seed, flags=0, query_ids=None, s_prev=None, ti
     return J, s, tie.astype(bool), int(nc.value)
 
 
-def pm_trace(Q, K, J_prev, t, seed, g, flags=0, cap=256, prev=None, sep=1):
+def pm_trace(Q, K, J_prev, t, seed, g, flags=0, cap=256, prev=None, sep=1, s_prev=None):
     """Every candidate scored by query ``g`` in iteration ``t``.
 
     Returns ``(idx[n], kind[n], window[n, 4], final)``; kind is
     ``1 + 4*jump_index + direction_index`` for propagation (jumps 8, 4, 2, 1;
     directions row-1, row+1, col-1, col+1) and ``100 + k`` for random-search
-    step k, whose window row is ``(lo_r, hi_r, lo_c, hi_c)``.
+    step k, whose window row is ``(lo_r, hi_r, lo_c, hi_c)``.  ``s_prev``
+    (the scores of ``J_prev``, as ``pm_scores`` gives them) saves their
+    recomputation when many queries are traced.
     """
     Q, K, J_prev = _f64(Q), _f64(K), _i32(J_prev)
     S, Hq, Wq, Hk, Wk, d = _dims(Q, K)
     prev, n_prev = _prev(prev, S, Hq, Wq)
-    s_prev, _ = pm_scores(Q, K, J_prev)
+    if s_prev is None:
+        s_prev, _ = pm_scores(Q, K, J_prev)
+    s_prev = _f64(s_prev)
     idx = np.zeros(cap, np.int64)
     kind = np.zeros(cap, np.int32)
     win = np.zeros((cap, 4), np.float64)
