@@ -19,6 +19,8 @@ struct AttParams {
     float scale_log2e;    // scale * log2(e): scores live in the base-2 domain
     int kappa;            // maps in J ([kappa, n]): the union of their windows
     int causal;           // drop keys after the query (raster order)
+    int Hq, Wq;
+    Tiling tq;            // blocks -> tiles of the query grid (set per storage type and width)
 };
 
 // ---------------------------------------------------------------------------
@@ -43,8 +45,8 @@ __global__ __launch_bounds__(kBlock) void attend_window_kernel(AttParams p)
     constexpr int B = W / 2;
     const int lane = threadIdx.x & (G - 1);
     const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
-    const uint32_t g = blk * RW::kQpb + threadIdx.x / G;
-    if (g >= p.n) return;
+    uint32_t g;
+    if (!tile_item<RW::kQpb>(p.tq, blk, threadIdx.x / G, g)) return;
 
     uint32_t s, rem;
     divmod(g, p.div_plane, s, rem);
@@ -136,8 +138,8 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
     constexpr int kNb = CH >= 2 ? 4 : 8;
     const int lane = threadIdx.x & (G - 1);
     const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
-    const uint32_t g = blk * RW::kQpb + threadIdx.x / G;
-    if (g >= p.n) return;
+    uint32_t g;
+    if (!tile_item<RW::kQpb>(p.tq, blk, threadIdx.x / G, g)) return;
 
     uint32_t s, rem;
     divmod(g, p.div_plane, s, rem);
@@ -224,10 +226,12 @@ hipError_t run_attend_m(const AttParams& p, int window, uint32_t blocks, hipStre
 }
 
 template <typename T, int D>
-hipError_t run_attend(const AttParams& p, int window, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
+hipError_t run_attend(const AttParams& p0, int window, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
 {
     constexpr int G = Lanes<T, D>::kAttend;
-    const uint32_t blocks = (p.n + Row<T, D, G>::kQpb - 1) / Row<T, D, G>::kQpb;
+    AttParams p = p0;
+    p.tq = make_tiling(p.Hq, p.Wq, Row<T, D, G>::kQpb);
+    const uint32_t blocks = tiling_blocks(p.tq, p.n / p.tq.plane);
     // the smallest register budget that holds this call's window centres
     if (p.kappa == 1) {
         return p.causal ? run_attend_m<T, D, 1>(p, window, blocks, st, e0, e1)
@@ -256,6 +260,8 @@ hipError_t launch_attend(int dtype, const void* Q, const void* K, const void* V,
     p.nkeys = static_cast<uint32_t>(g.Hk) * g.Wk;
     p.div_plane = make_div(static_cast<uint32_t>(g.Hq) * g.Wq);
     p.div_wk = make_div(g.Wk);
+    p.Hq = g.Hq;
+    p.Wq = g.Wq;
     p.b = window / 2;
     p.scale_log2e = scale * 1.4426950408889634f;
     p.kappa = kappa;

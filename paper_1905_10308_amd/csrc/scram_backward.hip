@@ -47,6 +47,7 @@ struct BwdParams {
     float2* st;              // [kappa * n] (log2 normaliser, D_i) of each entry
     uint32_t n;
     uint32_t keys_total;   // S * nkeys
+    Tiling tq, tk;         // blocks -> tiles of the query grid (query kernel), the key grid (key kernel)
     int Hq, Wq, Hk, Wk;
     uint32_t nkeys;
     Div div_plane, div_wk, div_n, div_keys;
@@ -177,8 +178,8 @@ __global__ __launch_bounds__(kBlock) void bwd_query_kernel(BwdParams p)
     constexpr int kNb = CH >= 2 ? 2 : 4;
     const int lane = threadIdx.x & (G - 1);
     const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
-    const uint32_t g = blk * RW::kQpb + threadIdx.x / G;
-    if (g >= p.n) return;
+    uint32_t g;
+    if (!tile_item<RW::kQpb>(p.tq, blk, threadIdx.x / G, g)) return;
 
     uint32_t s, rem;
     divmod(g, p.div_plane, s, rem);
@@ -515,8 +516,8 @@ __global__ __launch_bounds__(kBlock) void bwd_key_kernel(BwdParams p)
     constexpr int E = CH * RW::kEpc;
     const int lane = threadIdx.x & (G - 1);
     const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
-    const uint32_t kg = blk * RW::kQpb + threadIdx.x / G;  // global key id s * nkeys + j
-    if (kg >= p.keys_total) return;
+    uint32_t kg;  // global key id s * nkeys + j
+    if (!tile_item<RW::kQpb>(p.tk, blk, threadIdx.x / G, kg)) return;
     const KeyPos k = key_pos(p, kg);
     const int32_t* off = p.offsets + static_cast<size_t>(k.s) * p.nkeys;
     int total = 0;
@@ -576,13 +577,16 @@ __global__ __launch_bounds__(kBlock) void bwd_heavy_kernel(BwdParams p)
 }
 
 template <typename T, int D>
-hipError_t run_backward(const BwdParams& p, hipStream_t st, hipEvent_t* ev)
+hipError_t run_backward(const BwdParams& p0, hipStream_t st, hipEvent_t* ev)
 {
     constexpr int G = Lanes<T, D>::kAttend;
     constexpr uint32_t kQpb = Row<T, D, G>::kQpb;
-    const uint32_t qblocks = (p.n + kQpb - 1) / kQpb;
+    BwdParams p = p0;
+    p.tq = make_tiling(p.Hq, p.Wq, kQpb);
+    p.tk = make_tiling(p.Hk, p.Wk, kQpb);
+    const uint32_t qblocks = tiling_blocks(p.tq, p.n / p.tq.plane);
     const uint32_t gblocks = static_cast<uint32_t>((static_cast<size_t>(p.kappa) * p.n + kQpb - 1) / kQpb);
-    const uint32_t kblocks = (p.keys_total + kQpb - 1) / kQpb;
+    const uint32_t kblocks = tiling_blocks(p.tk, p.keys_total / p.nkeys);
     hipEvent_t q0 = ev ? ev[2] : nullptr, q1 = ev ? ev[3] : nullptr, k0 = ev ? ev[4] : nullptr,
                k1 = ev ? ev[5] : nullptr;
     const bool multi = p.kappa > 1 || p.causal;

@@ -91,6 +91,63 @@ __device__ __forceinline__ uint32_t xcd_remap(uint32_t b, uint32_t nb)
     return start + local;
 }
 
+// Block tiles.  The lane groups of a block cover a tile of `items` positions
+// (a power of two; raster order inside the tile) of one slice's 2-D grid;
+// blocks take the tiles of slice 0 in raster order, then those of slice 1,
+// ...  Neighbouring positions have nearby matches, so a squarish tile shares
+// more of the rows its lane groups read in L1 than a row segment of the same
+// size.  Grids narrower than the squarish tile get a flatter one, so that
+// 1-D grids keep every lane group busy.
+struct Tiling {
+    uint32_t H, W, plane;  // one slice's grid
+    uint32_t lw;           // log2 of the tile width
+    Div div_w, div_slice;  // tiles per grid row, tiles per slice
+};
+
+// Host: the tiling of one slice's H x W grid by blocks of `items` positions.
+inline Tiling make_tiling(int H, int W, uint32_t items)
+{
+    auto pow2_at_least = [](uint32_t v) {
+        uint32_t p = 1;
+        while (p < v) p <<= 1;
+        return p;
+    };
+    uint32_t lw = 0;
+    while ((1u << (2 * (lw + 1))) <= items) ++lw;  // squarish: width = sqrt(items) rounded down to a power of two
+    uint32_t tw = 1u << lw, th = items / tw;
+    if (th > pow2_at_least(static_cast<uint32_t>(H))) {  // short grid: wider tiles
+        th = pow2_at_least(static_cast<uint32_t>(H));
+        tw = items / th;
+    }
+    if (tw > pow2_at_least(static_cast<uint32_t>(W))) {  // narrow grid: taller tiles
+        tw = pow2_at_least(static_cast<uint32_t>(W));
+        th = items / tw;
+    }
+    lw = 0;
+    while ((1u << lw) < tw) ++lw;
+    const uint32_t nw = (static_cast<uint32_t>(W) + tw - 1) / tw, nh = (static_cast<uint32_t>(H) + th - 1) / th;
+    return Tiling{static_cast<uint32_t>(H), static_cast<uint32_t>(W), static_cast<uint32_t>(H) * W, lw,
+                  make_div(nw), make_div(nw * nh)};
+}
+
+inline uint32_t tiling_blocks(const Tiling& t, uint32_t slices) { return slices * t.div_slice.d; }
+
+// Flat position g = s * H * W + x * W + y of item i (< kItems) of (remapped)
+// block blk; false past the grid's right or bottom edge (g is then not
+// meaningful).
+template <uint32_t kItems>
+__device__ __forceinline__ bool tile_item(const Tiling& t, uint32_t blk, uint32_t i, uint32_t& g)
+{
+    static_assert((kItems & (kItems - 1)) == 0, "tiles of a power-of-two size");
+    uint32_t s, k, tr, tc;
+    divmod(blk, t.div_slice, s, k);
+    divmod(k, t.div_w, tr, tc);
+    const uint32_t th = kItems >> t.lw;
+    const uint32_t x = tr * th + (i >> t.lw), y = (tc << t.lw) + (i & ((1u << t.lw) - 1u));
+    g = s * t.plane + x * t.W + y;
+    return x < t.H && y < t.W;
+}
+
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC 2011): ten rounds of two
 // 32x32->64 multiplies mixed with the other two words and the round key; the
 // key advances by the two Weyl increments after every round.

@@ -28,6 +28,7 @@ struct PmParams {
     int sep;              // minimum Chebyshev distance to every previous match
     int causal;           // keys after the query (raster order) are not valid
     int first;            // the sweep recomputes the random initial field (Jp, sp unused)
+    Tiling tq;            // sweep blocks -> tiles of the query grid
 };
 
 
@@ -145,9 +146,9 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
     float best[QPG];
 #pragma unroll
     for (int j = 0; j < QPG; ++j) {
-        const uint32_t gr = blk * kQpb + j * kGroups + qslot;
-        live[j] = gr < p.n;
-        // groups past the end work on the last query and write nothing, so
+        uint32_t gr;
+        live[j] = tile_item<kQpb>(p.tq, blk, j * kGroups + qslot, gr);
+        // groups past the grid's edge work on the last query and write nothing, so
         // every lane reaches the block barrier below
         g[j] = live[j] ? gr : p.n - 1;
         uint32_t rem;
@@ -431,11 +432,12 @@ hipError_t run_iter_v(const PmParams& p, uint32_t flags, uint32_t blocks, hipStr
 }
 
 template <typename T, int D>
-hipError_t run_iter(const PmParams& p, uint32_t flags, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
+hipError_t run_iter(const PmParams& p0, uint32_t flags, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
 {
     constexpr int G = Lanes<T, D>::kPm;
-    constexpr int kQpb = Row<T, D, G>::kQpb * SCRAM_PM_QPG;
-    const uint32_t blocks = (p.n + kQpb - 1) / kQpb;
+    PmParams p = p0;
+    p.tq = make_tiling(p.Hq, p.Wq, Row<T, D, G>::kQpb * SCRAM_PM_QPG);
+    const uint32_t blocks = tiling_blocks(p.tq, p.n / p.plane_q);
     // the smallest register budget that holds this run's previous matches
     if (p.n_prev == 0) {
         return p.causal ? run_iter_v<T, D, 0>(p, flags, blocks, st, e0, e1)

@@ -42,6 +42,8 @@ struct SnisParams {
     float scale_log2e;
     uint32_t key0, key1;
     int causal;
+    int Hq, Wq;
+    Tiling tq;             // blocks -> tiles of the query grid
 };
 
 // Probability that the clamped coordinate centre + offset lands on r, read
@@ -129,8 +131,8 @@ void snis_kernel(SnisParams p)
     const int lane = threadIdx.x & (G - 1);
     const int gbase = (threadIdx.x & 63) - lane;
     const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
-    const uint32_t g = blk * RW::kQpb + threadIdx.x / G;
-    if (g >= p.n) return;  // whole lane groups leave together
+    uint32_t g;
+    if (!tile_item<RW::kQpb>(p.tq, blk, threadIdx.x / G, g)) return;  // whole lane groups leave together
 
     uint32_t s, rem;
     divmod(g, p.div_plane, s, rem);
@@ -248,10 +250,12 @@ void snis_kernel(SnisParams p)
 }
 
 template <typename T, int D>
-hipError_t run_snis(const SnisParams& p, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
+hipError_t run_snis(const SnisParams& p0, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
 {
     constexpr int G = Lanes<T, D>::kAttend;
-    const uint32_t blocks = (p.n + Row<T, D, G>::kQpb - 1) / Row<T, D, G>::kQpb;
+    SnisParams p = p0;
+    p.tq = make_tiling(p.Hq, p.Wq, Row<T, D, G>::kQpb);
+    const uint32_t blocks = tiling_blocks(p.tq, p.n / p.tq.plane);
     // the smallest register budget that holds the query's modes
     auto go = [&](auto mk) {
         constexpr int MK = decltype(mk)::value;
@@ -284,6 +288,8 @@ hipError_t launch_snis(int dtype, const void* Q, const void* K, const void* V, c
     p.nkeys = static_cast<uint32_t>(g.Hk) * g.Wk;
     p.div_plane = make_div(static_cast<uint32_t>(g.Hq) * g.Wq);
     p.div_wk = make_div(g.Wk);
+    p.Hq = g.Hq;
+    p.Wq = g.Wq;
     p.kappa = kappa;
     p.samples = spec.samples;
     p.m = spec.radius;
