@@ -19,18 +19,18 @@ SOURCES = [os.path.join(CSRC, f) for f in ("scram_pm.hip", "scram_attend.hip", "
                                              "scram_api.cpp")]
 ARCH = "gfx950"
 
-HIPCC_FLAGS = [
+COMPILE_FLAGS = [
     f"--offload-arch={ARCH}",
     "-O3",
     "-std=c++17",
     "-fPIC",
-    "-shared",
     "-Wall",
     # fixed operation order: explicit fmaf only, no implicit contraction
     "-ffp-contract=off",
     # never emit packed fp32 arithmetic
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
+LINK_FLAGS = [f"--offload-arch={ARCH}", "-shared", "-fPIC"]
 
 
 def hipcc() -> str:
@@ -40,19 +40,40 @@ def hipcc() -> str:
     return "hipcc"
 
 
+def _noise_free(res) -> list:
+    # the host pass does not know the packed-fp32 feature and says so; drop that line
+    return [ln for ln in (res.stdout + res.stderr).splitlines() if "packed-fp32-ops" not in ln and ln.strip()]
+
+
 def build(verbose: bool = False) -> str:
-    os.makedirs(LIB_DIR, exist_ok=True)
+    """Compile every source to an object (in parallel), then link the shared library."""
+    obj_dir = os.path.join(LIB_DIR, "obj")
+    os.makedirs(obj_dir, exist_ok=True)
+    jobs = []
+    for src in SOURCES:
+        obj = os.path.join(obj_dir, os.path.splitext(os.path.basename(src))[0] + ".o")
+        cmd = [hipcc(), *COMPILE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", src, "-o", obj]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        jobs.append((obj, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)))
+    failed, objs = [], []
+    for obj, proc in jobs:
+        out, err = proc.communicate()
+        res = subprocess.CompletedProcess(proc.args, proc.returncode, out, err)
+        if proc.returncode != 0:
+            failed.append(f"{os.path.basename(obj)}:\n" + "\n".join(_noise_free(res)))
+        elif verbose and _noise_free(res):
+            print("\n".join(_noise_free(res)))
+        objs.append(obj)
+    if failed:
+        raise RuntimeError("hipcc failed:\n" + "\n".join(failed))
     tmp = LIB_PATH + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", *SOURCES, "-o", tmp]
+    cmd = [hipcc(), *LINK_FLAGS, *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
-    # the host pass does not know the packed-fp32 feature and says so; drop that line
-    noise = [ln for ln in (res.stdout + res.stderr).splitlines() if "packed-fp32-ops" not in ln and ln.strip()]
     if res.returncode != 0:
-        raise RuntimeError("hipcc failed:\n" + "\n".join(noise))
-    if verbose and noise:
-        print("\n".join(noise))
+        raise RuntimeError("hipcc link failed:\n" + "\n".join(_noise_free(res)))
     os.replace(tmp, LIB_PATH)
     return LIB_PATH
 

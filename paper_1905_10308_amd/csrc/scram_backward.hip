@@ -168,7 +168,10 @@ __global__ __launch_bounds__(kBlock) void bwd_fill_kernel(BwdParams p, int32_t* 
     }
 }
 
-template <typename T, int D, int G, bool MULTI>
+// W > 0: window side W (odd), visited one window row at a time with its W
+// key and W value rows loaded together (as the forward's window kernel);
+// W = 0: any side, kNb keys at a time in row order.
+template <typename T, int D, int G, bool MULTI, int W>
 __global__ __launch_bounds__(kBlock) void bwd_query_kernel(BwdParams p)
 {
     using RW = Row<T, D, G>;
@@ -206,6 +209,38 @@ __global__ __launch_bounds__(kBlock) void bwd_query_kernel(BwdParams p)
             const int r0 = max(static_cast<int>(u) - p.b, 0), r1 = min(static_cast<int>(u) + p.b, p.Hk - 1);
             const int c0 = max(static_cast<int>(v) - p.b, 0), c1 = min(static_cast<int>(v) + p.b, p.Wk - 1);
             const int nwin = (r1 - r0 + 1) * (c1 - c0 + 1);
+            if constexpr (W > 0) {
+                constexpr int B = W / 2;
+                int cols[W];
+                bool col_ok[W];
+#pragma unroll
+                for (int cc = 0; cc < W; ++cc) {
+                    const int col = static_cast<int>(v) + cc - B;
+                    col_ok[cc] = col >= 0 && col < p.Wk;
+                    cols[cc] = min(max(col, 0), p.Wk - 1);
+                }
+                for (int a = 0; a < W; ++a) {
+                    const int rr = static_cast<int>(u) + a - B;
+                    if (rr < 0 || rr >= p.Hk) continue;
+                    bool ok[W];
+                    bool any = false;
+#pragma unroll
+                    for (int cc = 0; cc < W; ++cc) {
+                        ok[cc] = col_ok[cc];
+                        if constexpr (MULTI) ok[cc] = ok[cc] && !wset.skip(e, rr, cols[cc]);
+                        any = any || ok[cc];
+                    }
+                    if (!any) continue;
+                    uint4 kr[W][CH], vr[W][CH];
+#pragma unroll
+                    for (int cc = 0; cc < W; ++cc) {
+                        load_row<T, D, G>(Ks, static_cast<uint32_t>(rr * p.Wk + cols[cc]), lane, kr[cc]);
+                        load_row<T, D, G>(Vs, static_cast<uint32_t>(rr * p.Wk + cols[cc]), lane, vr[cc]);
+                    }
+                    fn(ok, kr, vr);
+                }
+                continue;
+            }
             const uint32_t centre = u * p.Wk + v;
             int r = r0, c = c0;
             for (int k0 = 0; k0 < nwin; k0 += kNb) {
@@ -245,7 +280,8 @@ __global__ __launch_bounds__(kBlock) void bwd_query_kernel(BwdParams p)
     float acc_a[E], acc_b[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) acc_a[e] = acc_b[e] = 0.f;
-    visit([&](const bool (&ok)[kNb], const uint4 (&kr)[kNb][CH], const uint4 (&vr)[kNb][CH]) {
+    visit([&](const auto& ok, const auto& kr, const auto& vr) {
+        constexpr int kNb = std::extent<std::remove_reference_t<decltype(ok)>>::value;
         float sc[kNb], dp[kNb];
         float mb = m;
 #pragma unroll
@@ -590,8 +626,17 @@ hipError_t run_backward(const BwdParams& p0, hipStream_t st, hipEvent_t* ev)
     hipEvent_t q0 = ev ? ev[2] : nullptr, q1 = ev ? ev[3] : nullptr, k0 = ev ? ev[4] : nullptr,
                k1 = ev ? ev[5] : nullptr;
     const bool multi = p.kappa > 1 || p.causal;
-    hipError_t e = multi ? launch(bwd_query_kernel<T, D, G, true>, qblocks, st, q0, q1, p)
-                         : launch(bwd_query_kernel<T, D, G, false>, qblocks, st, q0, q1, p);
+    auto query = [&](auto w) {
+        constexpr int W = decltype(w)::value;
+        return multi ? launch(bwd_query_kernel<T, D, G, true, W>, qblocks, st, q0, q1, p)
+                     : launch(bwd_query_kernel<T, D, G, false, W>, qblocks, st, q0, q1, p);
+    };
+    const int side = 2 * p.b + 1;
+    hipError_t e = side == 1   ? query(std::integral_constant<int, 1>{})
+                   : side == 3 ? query(std::integral_constant<int, 3>{})
+                   : side == 5 ? query(std::integral_constant<int, 5>{})
+                   : side == 7 ? query(std::integral_constant<int, 7>{})
+                               : query(std::integral_constant<int, 0>{});
     if (e != hipSuccess) return e;
     if ((e = launch(bwd_gather_kernel<T, D, G>, gblocks, st, k0, nullptr, p)) != hipSuccess) return e;
     e = multi ? launch(bwd_key_kernel<T, D, G, true>, kblocks, st, nullptr, nullptr, p)
