@@ -45,7 +45,11 @@
  * - Element types: SCRAM_F32 (fp32) or SCRAM_BF16 (bfloat16) storage for Q,
  *   K, V and the attend output; all arithmetic accumulates in fp32.
  * - Supported sizes: d in {16, 32, 64, 128}; dv == d; S*Hq*Wq < 2^31 and
- *   Hk*Wk < 2^31.
+ *   Hk*Wk < 2^31.  One kernel dispatch holds at most 2^32 - 1 work-items, and
+ *   the kernels give each query (or key) d * elem_bytes / 32 lanes (at least
+ *   one), so a call is also rejected with SCRAM_ERR_SHAPE when its largest
+ *   grid, rounded up to whole tiles of the query or key grid, would exceed
+ *   that -- roughly when the query (or key) tensor passes 128 GiB.
  * - Pointers are device pointers (HIP) owned by the caller.  Q, K, V and the
  *   attend output must be 16-byte aligned; index and score buffers 4-byte
  *   aligned; the workspace 256-byte aligned.  The library allocates no memory

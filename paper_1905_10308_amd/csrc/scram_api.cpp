@@ -15,6 +15,7 @@ namespace {
 
 constexpr int64_t kMaxSide = int64_t(1) << 30;
 constexpr int64_t kMaxCount = int64_t(1) << 31;
+constexpr uint64_t kMaxBlocks = 0xFFFFFFFFull / 256;  // one dispatch: at most 2^32 - 1 work-items
 
 size_t round256(size_t b) { return (b + 255) & ~size_t(255); }
 
@@ -80,6 +81,7 @@ int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int
     if (iters < 0 || t0 < 1 || int64_t(t0) + iters > int64_t(0xFFFFFFFFu)) return SCRAM_ERR_SHAPE;
     if (n_prev < 0 || n_prev > SCRAM_MAX_PREV || sep < 1) return SCRAM_ERR_SHAPE;
     if ((rc = check_type(dtype, d))) return rc;
+    if (scram::patchmatch_max_blocks(dtype, scram::Grid{S, Hq, Wq, Hk, Wk, d}) > kMaxBlocks) return SCRAM_ERR_SHAPE;
     if (flags & ~uint32_t(SCRAM_PM_NO_PROPAGATION | SCRAM_PM_NO_RANDOM_SEARCH | SCRAM_CAUSAL))
         return SCRAM_ERR_UNSUPPORTED;
     const bool causal = (flags & SCRAM_CAUSAL) != 0;
@@ -180,6 +182,7 @@ int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype, 
     if (kappa < 1 || kappa > SCRAM_MAX_KAPPA) return SCRAM_ERR_SHAPE;
     if (!isfinite(scale)) return SCRAM_ERR_SHAPE;
     if ((rc = check_type(dtype, d))) return rc;
+    if (scram::attend_max_blocks(dtype, scram::Grid{S, Hq, Wq, Hk, Wk, d}) > kMaxBlocks) return SCRAM_ERR_SHAPE;
     if (dv != d) return SCRAM_ERR_UNSUPPORTED;
     if (flags & ~uint32_t(SCRAM_CAUSAL)) return SCRAM_ERR_UNSUPPORTED;
     const bool causal = (flags & SCRAM_CAUSAL) != 0;
@@ -221,6 +224,8 @@ int scram_sparse_attend_backward(const void* Q, const void* K, const void* V, in
     if (kappa < 1 || kappa > SCRAM_MAX_KAPPA) return SCRAM_ERR_SHAPE;
     if (!isfinite(scale)) return SCRAM_ERR_SHAPE;
     if ((rc = check_type(dtype, d))) return rc;
+    if (scram::attend_backward_max_blocks(dtype, scram::Grid{S, Hq, Wq, Hk, Wk, d}, kappa) > kMaxBlocks)
+        return SCRAM_ERR_SHAPE;
     if (dv != d) return SCRAM_ERR_UNSUPPORTED;
     if (flags & ~uint32_t(SCRAM_CAUSAL)) return SCRAM_ERR_UNSUPPORTED;
     const bool causal = (flags & SCRAM_CAUSAL) != 0;
@@ -263,6 +268,7 @@ int scram_snis_attend(const void* Q, const void* K, const void* V, int dtype, co
     if (radius < 0 || radius > SCRAM_SNIS_MAX_RADIUS) return SCRAM_ERR_SHAPE;
     if (!isfinite(scale)) return SCRAM_ERR_SHAPE;
     if ((rc = check_type(dtype, d))) return rc;
+    if (scram::snis_max_blocks(dtype, scram::Grid{S, Hq, Wq, Hk, Wk, d}) > kMaxBlocks) return SCRAM_ERR_SHAPE;
     if (dv != d) return SCRAM_ERR_UNSUPPORTED;
     if (flags & ~uint32_t(SCRAM_CAUSAL)) return SCRAM_ERR_UNSUPPORTED;
     const bool causal = (flags & SCRAM_CAUSAL) != 0;

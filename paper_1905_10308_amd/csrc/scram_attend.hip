@@ -212,7 +212,7 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
 }
 
 template <typename T, int D, int MK>
-hipError_t run_attend_m(const AttParams& p, int window, uint32_t blocks, hipStream_t st, hipEvent_t e0,
+hipError_t run_attend_m(const AttParams& p, int window, uint64_t blocks, hipStream_t st, hipEvent_t e0,
                         hipEvent_t e1)
 {
     constexpr int G = Lanes<T, D>::kAttend;
@@ -231,7 +231,7 @@ hipError_t run_attend(const AttParams& p0, int window, hipStream_t st, hipEvent_
     constexpr int G = Lanes<T, D>::kAttend;
     AttParams p = p0;
     p.tq = make_tiling(p.Hq, p.Wq, Row<T, D, G>::kQpb);
-    const uint32_t blocks = tiling_blocks(p.tq, p.n / p.tq.plane);
+    const uint64_t blocks = tiling_blocks(p.tq, p.n / p.tq.plane);
     // the smallest register budget that holds this call's window centres
     if (p.kappa == 1) {
         return p.causal ? run_attend_m<T, D, 1>(p, window, blocks, st, e0, e1)
@@ -268,6 +268,15 @@ hipError_t launch_attend(int dtype, const void* Q, const void* K, const void* V,
     p.causal = causal ? 1 : 0;
     return dispatch(dtype, g.d, [&](auto ty, auto d) {
         return run_attend<decltype(ty), decltype(d)::value>(p, window, stream, start, stop);
+    });
+}
+
+uint64_t attend_max_blocks(int dtype, const Grid& g)
+{
+    return dispatch_value(dtype, g.d, uint64_t(0), [&](auto t, auto d) {
+        using T = decltype(t);
+        constexpr int D = decltype(d)::value;
+        return tiling_blocks(make_tiling(g.Hq, g.Wq, Row<T, D, Lanes<T, D>::kAttend>::kQpb), g.S);
     });
 }
 

@@ -620,9 +620,9 @@ hipError_t run_backward(const BwdParams& p0, hipStream_t st, hipEvent_t* ev)
     BwdParams p = p0;
     p.tq = make_tiling(p.Hq, p.Wq, kQpb);
     p.tk = make_tiling(p.Hk, p.Wk, kQpb);
-    const uint32_t qblocks = tiling_blocks(p.tq, p.n / p.tq.plane);
-    const uint32_t gblocks = static_cast<uint32_t>((static_cast<size_t>(p.kappa) * p.n + kQpb - 1) / kQpb);
-    const uint32_t kblocks = tiling_blocks(p.tk, p.keys_total / p.nkeys);
+    const uint64_t qblocks = tiling_blocks(p.tq, p.n / p.tq.plane);
+    const uint64_t gblocks = (static_cast<uint64_t>(p.kappa) * p.n + kQpb - 1) / kQpb;
+    const uint64_t kblocks = tiling_blocks(p.tk, p.keys_total / p.nkeys);
     hipEvent_t q0 = ev ? ev[2] : nullptr, q1 = ev ? ev[3] : nullptr, k0 = ev ? ev[4] : nullptr,
                k1 = ev ? ev[5] : nullptr;
     const bool multi = p.kappa > 1 || p.causal;
@@ -743,6 +743,23 @@ hipError_t launch_attend_backward(int dtype, const void* Q, const void* K, const
     // gradients
     return dispatch(dtype, g.d, [&](auto ty, auto d) {
         return run_backward<decltype(ty), decltype(d)::value>(p, stream, events);
+    });
+}
+
+uint64_t attend_backward_max_blocks(int dtype, const Grid& g, int kappa)
+{
+    return dispatch_value(dtype, g.d, uint64_t(0), [&](auto t, auto d) {
+        using T = decltype(t);
+        constexpr int D = decltype(d)::value;
+        constexpr uint32_t kQpb = Row<T, D, Lanes<T, D>::kAttend>::kQpb;
+        const uint64_t n = uint64_t(g.S) * g.Hq * g.Wq, keys = uint64_t(g.S) * g.Hk * g.Wk;
+        uint64_t most = 4096;  // the grid-stride kernels of the inverse map
+        auto keep = [&](uint64_t b) { most = b > most ? b : most; };
+        keep(tiling_blocks(make_tiling(g.Hq, g.Wq, kQpb), g.S));    // query kernel
+        keep((uint64_t(kappa) * n + kQpb - 1) / kQpb);              // entry-order copies
+        keep(tiling_blocks(make_tiling(g.Hk, g.Wk, kQpb), g.S));    // key kernel
+        keep((keys + kScanTile - 1) / kScanTile);                   // scan tiles
+        return most;
     });
 }
 

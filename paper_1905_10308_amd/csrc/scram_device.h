@@ -51,6 +51,7 @@ namespace {
 
 constexpr int kBlock = 256;  // threads per block: four wave64s
 constexpr int kXcds = 8;     // XCDs per MI355X; blocks are dealt round-robin
+constexpr uint64_t kMaxBlocks = 0xFFFFFFFFull / kBlock;  // blocks of one dispatch (2^32 - 1 work-items)
 
 // ---------------------------------------------------------------------------
 // integer helpers
@@ -130,7 +131,7 @@ inline Tiling make_tiling(int H, int W, uint32_t items)
                   make_div(nw), make_div(nw * nh)};
 }
 
-inline uint32_t tiling_blocks(const Tiling& t, uint32_t slices) { return slices * t.div_slice.d; }
+inline uint64_t tiling_blocks(const Tiling& t, uint32_t slices) { return uint64_t(slices) * t.div_slice.d; }
 
 // Flat position g = s * H * W + x * W + y of item i (< kItems) of (remapped)
 // block blk; false past the grid's right or bottom edge (g is then not
@@ -430,9 +431,11 @@ struct NoDeduce {
 };
 
 template <typename... A>
-hipError_t launch(void (*kernel)(A...), uint32_t blocks, hipStream_t st, hipEvent_t start, hipEvent_t stop,
+hipError_t launch(void (*kernel)(A...), uint64_t blocks, hipStream_t st, hipEvent_t start, hipEvent_t stop,
                   typename NoDeduce<A>::type... args)
 {
+    // a dispatch holds at most 2^32 - 1 work-items; the front end rejects larger grids first
+    if (blocks == 0 || blocks > kMaxBlocks) return hipErrorInvalidConfiguration;
     if (start || stop)
         hipExtLaunchKernelGGL(kernel, dim3(blocks), dim3(kBlock), 0, st, start, stop, 0, args...);
     else
@@ -440,9 +443,9 @@ hipError_t launch(void (*kernel)(A...), uint32_t blocks, hipStream_t st, hipEven
     return hipGetLastError();
 }
 
-// (dtype, d) -> instantiation
-template <typename F>
-hipError_t dispatch(int dtype, int d, F&& f)
+// (dtype, d) -> instantiation; `none` for an unsupported pair
+template <typename R, typename F>
+R dispatch_value(int dtype, int d, R none, F&& f)
 {
     if (dtype == SCRAM_F32) {
         switch (d) {
@@ -459,7 +462,13 @@ hipError_t dispatch(int dtype, int d, F&& f)
             case 128: return f(uint16_t{}, std::integral_constant<int, 128>{});
         }
     }
-    return hipErrorInvalidValue;
+    return none;
+}
+
+template <typename F>
+hipError_t dispatch(int dtype, int d, F&& f)
+{
+    return dispatch_value(dtype, d, hipErrorInvalidValue, static_cast<F&&>(f));
 }
 
 }  // namespace

@@ -68,4 +68,12 @@ hipError_t launch_snis(int dtype, const void* Q, const void* K, const void* V, c
                        const Grid& g, const SnisSpec& spec, bool causal, void* out, float* ess, float* var,
                        hipStream_t stream, hipEvent_t start, hipEvent_t stop);
 
+// Blocks (of 256 threads) of the largest dispatch an entry point makes for
+// this shape; 0 for an unsupported (dtype, d).  One dispatch holds at most
+// 2^32 - 1 work-items, so the front end rejects shapes above that.
+uint64_t patchmatch_max_blocks(int dtype, const Grid& g);
+uint64_t attend_max_blocks(int dtype, const Grid& g);
+uint64_t snis_max_blocks(int dtype, const Grid& g);
+uint64_t attend_backward_max_blocks(int dtype, const Grid& g, int kappa);
+
 }  // namespace scram

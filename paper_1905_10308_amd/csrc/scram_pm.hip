@@ -405,7 +405,7 @@ template <typename T, int D>
 hipError_t run_init(const PmParams& p, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
 {
     constexpr int G = Lanes<T, D>::kPm;
-    const uint32_t blocks = (p.n + Row<T, D, G>::kQpb - 1) / Row<T, D, G>::kQpb;
+    const uint64_t blocks = (uint64_t(p.n) + Row<T, D, G>::kQpb - 1) / Row<T, D, G>::kQpb;
     return launch(pm_init_kernel<T, D, G>, blocks, st, e0, e1, p);
 }
 
@@ -417,7 +417,7 @@ hipError_t run_init(const PmParams& p, hipStream_t st, hipEvent_t e0, hipEvent_t
 #endif
 
 template <typename T, int D, int NP>
-hipError_t run_iter_v(const PmParams& p, uint32_t flags, uint32_t blocks, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
+hipError_t run_iter_v(const PmParams& p, uint32_t flags, uint64_t blocks, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
 {
     constexpr int G = Lanes<T, D>::kPm;
     constexpr int QPG = SCRAM_PM_QPG;
@@ -437,7 +437,7 @@ hipError_t run_iter(const PmParams& p0, uint32_t flags, hipStream_t st, hipEvent
     constexpr int G = Lanes<T, D>::kPm;
     PmParams p = p0;
     p.tq = make_tiling(p.Hq, p.Wq, Row<T, D, G>::kQpb * SCRAM_PM_QPG);
-    const uint32_t blocks = tiling_blocks(p.tq, p.n / p.plane_q);
+    const uint64_t blocks = tiling_blocks(p.tq, p.n / p.plane_q);
     // the smallest register budget that holds this run's previous matches
     if (p.n_prev == 0) {
         return p.causal ? run_iter_v<T, D, 0>(p, flags, blocks, st, e0, e1)
@@ -484,6 +484,18 @@ hipError_t launch_pm_iter(int dtype, const void* Q, const void* K, const Grid& g
     p.causal = run.causal ? 1 : 0;
     return dispatch(dtype, g.d, [&](auto ty, auto d) {
         return run_iter<decltype(ty), decltype(d)::value>(p, flags, stream, start, stop);
+    });
+}
+
+uint64_t patchmatch_max_blocks(int dtype, const Grid& g)
+{
+    return dispatch_value(dtype, g.d, uint64_t(0), [&](auto t, auto d) {
+        using T = decltype(t);
+        constexpr int D = decltype(d)::value;
+        constexpr uint32_t kQpb = Row<T, D, Lanes<T, D>::kPm>::kQpb;
+        const uint64_t init = (uint64_t(g.S) * g.Hq * g.Wq + kQpb - 1) / kQpb;
+        const uint64_t iter = tiling_blocks(make_tiling(g.Hq, g.Wq, kQpb * SCRAM_PM_QPG), g.S);
+        return init > iter ? init : iter;
     });
 }
 

@@ -99,6 +99,8 @@ def at(L, **kw):
     (dict(t0=0), ESHAPE), (dict(S=1 << 16, Hq=1 << 8, Wq=1 << 7), ESHAPE),
     (dict(Hk=1 << 16, Wk=1 << 15), ESHAPE), (dict(Hq=(1 << 30) + 1, S=1, Wq=1), ESHAPE),
     (dict(t0=-5), ESHAPE),
+    # 2^29 queries at fp32 d=128: 16 lanes each, past one dispatch's 2^32 - 1 work-items
+    (dict(d=128, S=1, Hq=1 << 15, Wq=1 << 14), ESHAPE),
     (dict(d=48), EUNSUP), (dict(d=8), EUNSUP), (dict(dtype=7), EUNSUP), (dict(flags=8), EUNSUP),
     (dict(n_prev=1), ENULL), (dict(n_prev=-1, prev=A_P), ESHAPE), (dict(n_prev=MAX_PREV + 1, prev=A_P), ESHAPE),
     (dict(sep=0), ESHAPE), (dict(flags=CAUSAL, Hk=4), ESHAPE), (dict(flags=CAUSAL, Wq=7), ESHAPE),
@@ -126,9 +128,21 @@ def test_patchmatch_rejects(L, kw, code):
     (dict(kappa=0), ESHAPE), (dict(kappa=MAX_KAPPA + 1), ESHAPE), (dict(flags=1), EUNSUP), (dict(flags=8), EUNSUP),
     (dict(flags=CAUSAL, Hk=4), ESHAPE), (dict(flags=CAUSAL, Wk=9), ESHAPE),
     (dict(kappa=3, J=A_O - 4 * 2 * 64 * 3 + 4), EALIAS),
+    (dict(d=128, dv=128, S=1, Hq=1 << 15, Wq=1 << 14), ESHAPE),
 ])
 def test_sparse_attend_rejects(L, kw, code):
     assert at(L, **kw) == code
+
+
+def test_dispatch_limit_boundary(L):
+    """fp32 d=128 gives 16 lanes per query: 2^28 queries need exactly 2^32 work-items (one too many);
+    2^28 - 2^16 queries fit.  (The fake pointers then overlap, so a shape that passes reports aliasing.)"""
+    big = dict(d=128, S=1, Hq=1 << 14, Wq=1 << 14)
+    fits = dict(d=128, S=1, Hq=1 << 14, Wq=(1 << 14) - 4)
+    assert pm(L, **big) == ESHAPE
+    assert pm(L, **fits) != ESHAPE
+    assert at(L, dv=128, **big) == ESHAPE
+    assert at(L, dv=128, **fits) != ESHAPE
 
 
 A_E, A_VAR = 0x10000000 * 11, 0x10000000 * 12
@@ -155,6 +169,7 @@ def sn(L, **kw):
     (dict(ess=A_E + 2), EALIGN), (dict(var=A_VAR + 4), EALIGN),
     (dict(out=A_Q), EALIAS), (dict(ess=A_K + 64), EALIAS), (dict(var=A_J), EALIAS), (dict(ess=A_VAR + 16), EALIAS),
     (dict(var=A_O + 2 * 64 * 16 * 4 - 16), EALIAS), (dict(modes=A_O - 4 * 128 * 2 + 4), EALIAS),
+    (dict(d=128, dv=128, S=1, Hq=1 << 15, Wq=1 << 14), ESHAPE),
 ])
 def test_snis_rejects(L, kw, code):
     assert sn(L, **kw) == code
@@ -185,6 +200,8 @@ def bw(L, **kw):
     (dict(ws=None), EWS), (dict(ws_bytes=100), EWS), (dict(ws=A_BW + 16), EALIGN), (dict(ws=A_DQ), EALIAS),
     (dict(ws=A_Q + 256), EALIAS), (dict(S=1 << 14, Hq=1 << 8, Wq=1 << 8, Hk=4, Wk=4, kappa=2), ESHAPE),
     (dict(S=1 << 12, Hq=1, Wq=1, Hk=1 << 10, Wk=1 << 9), ESHAPE),
+    # 2^30 queries at bf16 d=128 (8 lanes each): the query kernel's grid passes one dispatch
+    (dict(d=128, dv=128, S=1, Hq=1 << 15, Wq=1 << 15), ESHAPE),
 ])
 
 
