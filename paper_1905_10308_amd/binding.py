@@ -113,8 +113,37 @@ def _dev_tensor(t, name, ndim=None):
     return t
 
 
+def _same_device(device, **tensors):
+    for name, t in tensors.items():
+        if t is not None and t.device != device:
+            raise ValueError(f"{name} is on {t.device}, expected {device}")
+
+
+def _check_buffer(t, name, shape, dtype):
+    """A caller-supplied output: contiguous, on the device, exactly ``shape`` and ``dtype``."""
+    _dev_tensor(t, name)
+    if t.dtype != dtype or tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must be {dtype} of shape {tuple(shape)}, got {t.dtype} {tuple(t.shape)}")
+
+
+def _workspace(ws, need, device):
+    """A caller-supplied workspace: contiguous device memory of at least ``need`` bytes (else allocate one)."""
+    torch = _torch()
+    if ws is None:
+        return torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+    _dev_tensor(ws, "workspace")
+    if ws.device != device:
+        raise ValueError(f"workspace is on {ws.device}, expected {device}")
+    return ws
+
+
 def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _on(device):
+    """Make ``device`` current for the call: the library launches on the current device."""
+    return _torch().cuda.device(device)
 
 
 def _stream(device):
@@ -159,6 +188,8 @@ def patchmatch(Q, K, iters: int, seed: int, *, init=None, init_score=None, t0: i
     if Sk != S or dk != d:
         raise ValueError(f"Q {tuple(Q.shape)} and K {tuple(K.shape)} disagree on slices or channels")
     dev = Q.device
+    _same_device(dev, K=K, init=init, init_score=init_score, prev=prev, out=out, score_out=score_out,
+                 workspace=workspace)
     if out is None:
         out = torch.empty((S, Hq, Wq), dtype=torch.int32, device=dev)
     if return_score and score_out is None:
@@ -179,15 +210,14 @@ def patchmatch(Q, K, iters: int, seed: int, *, init=None, init_score=None, t0: i
             prev = None
     if causal:
         flags |= CAUSAL
-    need = patchmatch_workspace_bytes(S, Hq, Wq)
-    if workspace is None:
-        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    workspace = _workspace(workspace, patchmatch_workspace_bytes(S, Hq, Wq), dev)
     ev = None if events is None else _event_array(events, 2 * (int(iters) + 1))
-    rc = lib().scram_patchmatch(_ptr(Q), _ptr(K), _dtype_code(Q), S, Hq, Wq, Hk, Wk, d, int(iters),
-                                ctypes.c_uint64(int(seed) & 0xFFFFFFFFFFFFFFFF), _ptr(init), _ptr(init_score),
-                                int(t0), int(flags), _ptr(prev), int(n_prev), int(sep), _ptr(out), _ptr(score_out),
-                                _ptr(workspace),
-                                workspace.numel() * workspace.element_size(), ev, _stream(dev))
+    with _on(dev):
+            rc = lib().scram_patchmatch(_ptr(Q), _ptr(K), _dtype_code(Q), S, Hq, Wq, Hk, Wk, d, int(iters),
+                                    ctypes.c_uint64(int(seed) & 0xFFFFFFFFFFFFFFFF), _ptr(init), _ptr(init_score),
+                                    int(t0), int(flags), _ptr(prev), int(n_prev), int(sep), _ptr(out),
+                                    _ptr(score_out), _ptr(workspace), workspace.numel() * workspace.element_size(), ev,
+                                    _stream(dev))
     if rc != 0:
         raise ScramError(rc, "scram_patchmatch")
     return (out, score_out) if return_score else out
@@ -219,13 +249,16 @@ def sparse_attend(Q, K, V, argmax, window: int, scale: float | None = None, *, c
     kappa = 1 if argmax.dim() == 3 else argmax.shape[0]
     if scale is None:
         scale = d ** -0.5
+    dev = Q.device
+    _same_device(dev, K=K, V=V, argmax=argmax, out=out)
     if out is None:
-        out = torch.empty((S, Hq, Wq, dv), dtype=Q.dtype, device=Q.device)
-    _dev_tensor(out, "out", 4)
+        out = torch.empty((S, Hq, Wq, dv), dtype=Q.dtype, device=dev)
+    _check_buffer(out, "out", (S, Hq, Wq, dv), Q.dtype)
     ev = None if events is None else _event_array(events, 2)
-    rc = lib().scram_sparse_attend(_ptr(Q), _ptr(K), _ptr(V), _dtype_code(Q), _ptr(argmax), int(kappa), S, Hq, Wq,
-                                   Hk, Wk, d, dv, int(window), float(scale), CAUSAL if causal else 0, _ptr(out), ev,
-                                   _stream(Q.device))
+    with _on(dev):
+        rc = lib().scram_sparse_attend(_ptr(Q), _ptr(K), _ptr(V), _dtype_code(Q), _ptr(argmax), int(kappa), S, Hq,
+                                       Wq, Hk, Wk, d, dv, int(window), float(scale), CAUSAL if causal else 0,
+                                       _ptr(out), ev, _stream(dev))
     if rc != 0:
         raise ScramError(rc, "scram_sparse_attend")
     return out
@@ -259,18 +292,19 @@ def sparse_attend_backward(Q, K, V, argmax, dO, window: int, scale: float | None
     if scale is None:
         scale = d ** -0.5
     dev = Q.device
+    _same_device(dev, K=K, V=V, argmax=argmax, dO=dO, workspace=workspace)
     dQ = torch.empty((S, Hq, Wq, d), dtype=torch.float32, device=dev)
     dK = torch.empty((S, Hk, Wk, d), dtype=torch.float32, device=dev)
     dV = torch.empty((S, Hk, Wk, dv), dtype=torch.float32, device=dev)
     need = sparse_attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, kappa, d=d, dtype=Q.dtype)
-    if workspace is None:
-        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    workspace = _workspace(workspace, need, dev)
     ev = None if events is None else _event_array(events, 6)
-    rc = lib().scram_sparse_attend_backward(_ptr(Q), _ptr(K), _ptr(V), _dtype_code(Q), _ptr(argmax), int(kappa), S,
-                                            Hq, Wq, Hk, Wk, d, dv, int(window), float(scale),
-                                            CAUSAL if causal else 0, _ptr(dO), _ptr(dQ), _ptr(dK), _ptr(dV),
-                                            _ptr(workspace), workspace.numel() * workspace.element_size(), ev,
-                                            _stream(dev))
+    with _on(dev):
+        rc = lib().scram_sparse_attend_backward(_ptr(Q), _ptr(K), _ptr(V), _dtype_code(Q), _ptr(argmax), int(kappa),
+                                                S, Hq, Wq, Hk, Wk, d, dv, int(window), float(scale),
+                                                CAUSAL if causal else 0, _ptr(dO), _ptr(dQ), _ptr(dK), _ptr(dV),
+                                                _ptr(workspace), workspace.numel() * workspace.element_size(), ev,
+                                                _stream(dev))
     if rc != 0:
         raise ScramError(rc, "scram_sparse_attend_backward")
     return dQ, dK, dV
@@ -310,16 +344,18 @@ def snis_attend(Q, K, V, modes, samples: int, *, alpha: float = 0.9, radius: int
     if scale is None:
         scale = d ** -0.5
     dev = Q.device
+    _same_device(dev, K=K, V=V, modes=modes, out=out)
     if out is None:
         out = torch.empty((S, Hq, Wq, dv), dtype=Q.dtype, device=dev)
-    _dev_tensor(out, "out", 4)
+    _check_buffer(out, "out", (S, Hq, Wq, dv), Q.dtype)
     ess_t = torch.empty((S, Hq, Wq), dtype=torch.float32, device=dev) if ess else None
     var_t = torch.empty((S, Hq, Wq, dv), dtype=torch.float32, device=dev) if var else None
     ev = None if events is None else _event_array(events, 2)
-    rc = lib().scram_snis_attend(_ptr(Q), _ptr(K), _ptr(V), _dtype_code(Q), _ptr(modes), int(kappa), S, Hq, Wq, Hk,
-                                 Wk, d, dv, int(samples), float(alpha), int(radius), float(scale),
-                                 ctypes.c_uint64(int(seed) & 0xFFFFFFFFFFFFFFFF), CAUSAL if causal else 0, _ptr(out),
-                                 _ptr(ess_t), _ptr(var_t), ev, _stream(dev))
+    with _on(dev):
+        rc = lib().scram_snis_attend(_ptr(Q), _ptr(K), _ptr(V), _dtype_code(Q), _ptr(modes), int(kappa), S, Hq, Wq,
+                                     Hk, Wk, d, dv, int(samples), float(alpha), int(radius), float(scale),
+                                     ctypes.c_uint64(int(seed) & 0xFFFFFFFFFFFFFFFF), CAUSAL if causal else 0,
+                                     _ptr(out), _ptr(ess_t), _ptr(var_t), ev, _stream(dev))
     if rc != 0:
         raise ScramError(rc, "scram_snis_attend")
     return (out, ess_t, var_t) if (ess or var) else out

@@ -258,6 +258,27 @@ def test_bad_arguments_raise(scram):
         scram.sparse_attend(Q, Q, Q, torch.zeros(1, 4, 4, dtype=torch.int32, device="cuda"), 2)
 
 
+def test_binding_checks_caller_buffers(scram):
+    """Caller-supplied outputs and workspaces are checked before the library is called: a buffer of the
+    wrong shape, dtype or layout raises instead of being written past its end."""
+    Q = torch.zeros(2, 4, 4, 16, device="cuda")
+    J = torch.zeros(2, 4, 4, dtype=torch.int32, device="cuda")
+    for bad in (torch.empty(1, 4, 4, 16, device="cuda"), torch.empty(2, 4, 4, 16, device="cuda", dtype=torch.bfloat16),
+                torch.empty(2, 4, 4, 32, device="cuda")[..., :16]):
+        with pytest.raises(ValueError):
+            scram.sparse_attend(Q, Q, Q, J, 3, out=bad)
+        with pytest.raises(ValueError):
+            scram.snis_attend(Q, Q, Q, J, 4, out=bad)
+    with pytest.raises(ValueError):
+        scram.patchmatch(Q, Q, 1, 0, out=torch.empty(2, 4, 3, dtype=torch.int32, device="cuda"))
+    with pytest.raises(ValueError):
+        scram.patchmatch(Q, Q, 1, 0, workspace=torch.empty(8192, dtype=torch.uint8, device="cuda")[::2])
+    with pytest.raises(ValueError):
+        scram.sparse_attend(Q, Q, Q, J.cpu(), 3)
+    ok = torch.empty(2, 4, 4, 16, device="cuda")
+    assert scram.sparse_attend(Q, Q, Q, J, 3, out=ok) is ok
+
+
 @pytest.mark.parametrize("variant", ["plain", "causal", "kappa2"])
 def test_fused_first_sweep_equals_init_then_sweep(scram, variant):
     """A fresh run's first sweep recomputes the random initial field instead of reading it: it must equal
