@@ -3,7 +3,10 @@
 Argument marshalling only: torch tensors provide device memory and the
 current HIP stream; every step of the computation runs in the library's HIP
 kernels.  There is no fallback -- if the library is missing or a call fails,
-these functions raise.
+these functions raise.  The kernels take d in {16, 32, 64, 128} with dv == d;
+other widths up to 128 (the paper's Figure 4 uses d_k = 3) are zero-padded
+here to the next of those -- exact, since zero channels add exact zeros to
+every dot product -- and results are cut back to the caller's widths.
 """
 from __future__ import annotations
 
@@ -20,6 +23,7 @@ NO_RANDOM_SEARCH = 2
 CAUSAL = 4
 MAX_PREV = 7
 MAX_KAPPA = 8
+NATIVE_WIDTHS = (16, 32, 64, 128)  # channel counts the kernels take; others up to 128 are zero-padded
 
 STATUS = {
     0: "SCRAM_OK",
@@ -141,6 +145,40 @@ def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
+def _unpad_into(res, width: int, out=None):
+    """The first ``width`` channels of ``res``, in ``out`` when given (else a new contiguous tensor)."""
+    if res.shape[-1] == width:
+        if out is not None and out is not res:
+            out.copy_(res)
+            return out
+        return res
+    if out is not None:
+        out.copy_(res[..., :width])
+        return out
+    return res[..., :width].contiguous()
+
+
+def _native_width(c: int) -> int:
+    """The smallest channel count the kernels take that holds ``c`` (``c`` itself above 128: the library
+    rejects it)."""
+    for w in NATIVE_WIDTHS:
+        if c <= w:
+            return w
+    return c
+
+
+def _pad_channels(t, width: int):
+    """``t`` with its last dimension zero-padded to ``width`` (``t`` itself when it already has it).
+
+    Zero channels add exact zeros to every dot product, so scores, weights and outputs in the original
+    channels are unchanged; the softmax scale is taken from the original width."""
+    if t.shape[-1] == width:
+        return t
+    out = t.new_zeros(tuple(t.shape[:-1]) + (width,))
+    out[..., : t.shape[-1]] = t
+    return out
+
+
 def _on(device):
     """Make ``device`` current for the call: the library launches on the current device."""
     return _torch().cuda.device(device)
@@ -210,6 +248,8 @@ def patchmatch(Q, K, iters: int, seed: int, *, init=None, init_score=None, t0: i
             prev = None
     if causal:
         flags |= CAUSAL
+    d = _native_width(d)
+    Q, K = _pad_channels(Q, d), _pad_channels(K, d)
     workspace = _workspace(workspace, patchmatch_workspace_bytes(S, Hq, Wq), dev)
     ev = None if events is None else _event_array(events, 2 * (int(iters) + 1))
     with _on(dev):
@@ -251,17 +291,19 @@ def sparse_attend(Q, K, V, argmax, window: int, scale: float | None = None, *, c
         scale = d ** -0.5
     dev = Q.device
     _same_device(dev, K=K, V=V, argmax=argmax, out=out)
-    if out is None:
-        out = torch.empty((S, Hq, Wq, dv), dtype=Q.dtype, device=dev)
-    _check_buffer(out, "out", (S, Hq, Wq, dv), Q.dtype)
+    if out is not None:
+        _check_buffer(out, "out", (S, Hq, Wq, dv), Q.dtype)
+    w = _native_width(max(d, dv))
+    Q, K, V = (_pad_channels(t, w) for t in (Q, K, V))
+    res = out if out is not None and w == dv else torch.empty((S, Hq, Wq, w), dtype=Q.dtype, device=dev)
     ev = None if events is None else _event_array(events, 2)
     with _on(dev):
         rc = lib().scram_sparse_attend(_ptr(Q), _ptr(K), _ptr(V), _dtype_code(Q), _ptr(argmax), int(kappa), S, Hq,
-                                       Wq, Hk, Wk, d, dv, int(window), float(scale), CAUSAL if causal else 0,
-                                       _ptr(out), ev, _stream(dev))
+                                       Wq, Hk, Wk, w, w, int(window), float(scale), CAUSAL if causal else 0,
+                                       _ptr(res), ev, _stream(dev))
     if rc != 0:
         raise ScramError(rc, "scram_sparse_attend")
-    return out
+    return _unpad_into(res, dv, out)
 
 
 def sparse_attend_backward(Q, K, V, argmax, dO, window: int, scale: float | None = None, *, causal: bool = False,
@@ -296,18 +338,22 @@ def sparse_attend_backward(Q, K, V, argmax, dO, window: int, scale: float | None
     dQ = torch.empty((S, Hq, Wq, d), dtype=torch.float32, device=dev)
     dK = torch.empty((S, Hk, Wk, d), dtype=torch.float32, device=dev)
     dV = torch.empty((S, Hk, Wk, dv), dtype=torch.float32, device=dev)
-    need = sparse_attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, kappa, d=d, dtype=Q.dtype)
+    w = _native_width(max(d, dv))
+    Q, K, V, dO = (_pad_channels(t, w) for t in (Q, K, V, dO))
+    if w != d or w != dv:
+        dQ, dK, dV = (torch.empty(tuple(t.shape[:-1]) + (w,), dtype=torch.float32, device=dev) for t in (dQ, dK, dV))
+    need = sparse_attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, kappa, d=w, dtype=Q.dtype)
     workspace = _workspace(workspace, need, dev)
     ev = None if events is None else _event_array(events, 6)
     with _on(dev):
         rc = lib().scram_sparse_attend_backward(_ptr(Q), _ptr(K), _ptr(V), _dtype_code(Q), _ptr(argmax), int(kappa),
-                                                S, Hq, Wq, Hk, Wk, d, dv, int(window), float(scale),
+                                                S, Hq, Wq, Hk, Wk, w, w, int(window), float(scale),
                                                 CAUSAL if causal else 0, _ptr(dO), _ptr(dQ), _ptr(dK), _ptr(dV),
                                                 _ptr(workspace), workspace.numel() * workspace.element_size(), ev,
                                                 _stream(dev))
     if rc != 0:
         raise ScramError(rc, "scram_sparse_attend_backward")
-    return dQ, dK, dV
+    return _unpad_into(dQ, d), _unpad_into(dK, d), _unpad_into(dV, dv)
 
 
 def sparse_attend_backward_workspace_bytes(S: int, Hq: int, Wq: int, Hk: int, Wk: int, kappa: int = 1, *,
@@ -345,19 +391,24 @@ def snis_attend(Q, K, V, modes, samples: int, *, alpha: float = 0.9, radius: int
         scale = d ** -0.5
     dev = Q.device
     _same_device(dev, K=K, V=V, modes=modes, out=out)
-    if out is None:
-        out = torch.empty((S, Hq, Wq, dv), dtype=Q.dtype, device=dev)
-    _check_buffer(out, "out", (S, Hq, Wq, dv), Q.dtype)
+    if out is not None:
+        _check_buffer(out, "out", (S, Hq, Wq, dv), Q.dtype)
+    w = _native_width(max(d, dv))
+    Q, K, V = (_pad_channels(t, w) for t in (Q, K, V))
+    res = out if out is not None and w == dv else torch.empty((S, Hq, Wq, w), dtype=Q.dtype, device=dev)
     ess_t = torch.empty((S, Hq, Wq), dtype=torch.float32, device=dev) if ess else None
-    var_t = torch.empty((S, Hq, Wq, dv), dtype=torch.float32, device=dev) if var else None
+    var_t = torch.empty((S, Hq, Wq, w), dtype=torch.float32, device=dev) if var else None
     ev = None if events is None else _event_array(events, 2)
     with _on(dev):
         rc = lib().scram_snis_attend(_ptr(Q), _ptr(K), _ptr(V), _dtype_code(Q), _ptr(modes), int(kappa), S, Hq, Wq,
-                                     Hk, Wk, d, dv, int(samples), float(alpha), int(radius), float(scale),
+                                     Hk, Wk, w, w, int(samples), float(alpha), int(radius), float(scale),
                                      ctypes.c_uint64(int(seed) & 0xFFFFFFFFFFFFFFFF), CAUSAL if causal else 0,
-                                     _ptr(out), _ptr(ess_t), _ptr(var_t), ev, _stream(dev))
+                                     _ptr(res), _ptr(ess_t), _ptr(var_t), ev, _stream(dev))
     if rc != 0:
         raise ScramError(rc, "scram_snis_attend")
+    out = _unpad_into(res, dv, out)
+    if var_t is not None:
+        var_t = _unpad_into(var_t, dv)
     return (out, ess_t, var_t) if (ess or var) else out
 
 

@@ -249,8 +249,45 @@ def test_shapes(scram, shape):
         assert row_rel_err(out.float().cpu().numpy(), ref).max() <= TOL[dtype]
 
 
+@pytest.mark.parametrize("d,dv,dtype", [(3, 3, "f32"), (4, 4, "bf16"), (20, 20, "f32"), (100, 100, "bf16"),
+                                        (5, 9, "f32")])
+def test_channel_padding(scram, d, dv, dtype):
+    """Channel counts the kernels do not take (the paper's Figure 4 uses d_k = 3) are zero-padded by the
+    binding: maps, outputs, estimates and gradients equal the oracle's on the unpadded arrays."""
+    rng = np.random.default_rng(d * 31 + dv)
+    S, H, W = 2, 13, 11
+    Q, K = (rng.standard_normal((S, H, W, d)).astype(np.float32) for _ in range(2))
+    V, dO = (rng.standard_normal((S, H, W, dv)).astype(np.float32) for _ in range(2))
+    if dtype == "bf16":
+        Q, K, V, dO = (to_dev(x, "bf16").float().cpu().numpy() for x in (Q, K, V, dO))
+    Qd, Kd, Vd, dOd = (to_dev(x, dtype) for x in (Q, K, V, dO))
+    Jg, sg = scram.patchmatch(Qd, Kd, 3, 5, return_score=True)
+    Jo, so, ties, _ = oracle.patchmatch(Q, K, 3, 5)
+    Jg = Jg.cpu().numpy()
+    assert not ((Jg != Jo) & ~reach_of_ties(ties)).any()
+    sref = oracle.pm_scores(Q, K, Jg)[0]
+    assert np.abs(sg.cpu().numpy() - sref).max() <= 1e-5 * max(1.0, np.abs(sref).max())
+    Jt = torch.from_numpy(Jg).cuda()
+    scale = d ** -0.5
+    out = scram.sparse_attend(Qd, Kd, Vd, Jt, 3)  # default scale: 1/sqrt of the unpadded width
+    assert out.shape == (S, H, W, dv) and out.is_contiguous()
+    ref = oracle.sparse_attend(Q, K, V, Jg, 3, scale)
+    assert row_rel_err(out.float().cpu().numpy(), ref).max() <= TOL[dtype]
+    got = scram.sparse_attend_backward(Qd, Kd, Vd, Jt, dOd, 3, scale)
+    for g, r in zip(got, oracle.sparse_attend_backward(Q, K, V, Jg, 3, scale, dO)):
+        assert g.shape == r.shape
+        assert np.abs(g.cpu().numpy() - r).max() <= 2e-5 * np.abs(r).max()
+    est, ess, var = scram.snis_attend(Qd, Kd, Vd, Jt, 16, alpha=0.8, radius=2, scale=scale, seed=3, ess=True,
+                                      var=True)
+    rest, ress, _ = oracle.snis(Q, K, V, Jg, 16, 0.8, 2, scale, 3)
+    assert est.shape == (S, H, W, dv) and var.shape == (S, H, W, dv)
+    tol = 5e-5 * np.abs(V).max() + (2.0 ** -8 * np.abs(rest) if dtype == "bf16" else 0.0)
+    assert (np.abs(est.float().cpu().numpy() - rest) <= tol).all()
+    assert np.abs(ess.cpu().numpy() - ress).max() <= 1e-4 * ress.max()
+
+
 def test_bad_arguments_raise(scram):
-    Q = torch.zeros(1, 4, 4, 24, device="cuda")
+    Q = torch.zeros(1, 4, 4, 136, device="cuda")  # above 128 channels: not padded, rejected by the library
     with pytest.raises(scram.ScramError):
         scram.patchmatch(Q, Q, 1, 0)
     Q = torch.zeros(1, 4, 4, 16, device="cuda")
