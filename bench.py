@@ -92,12 +92,18 @@ def cpu_baseline(cfg, arrays, min_s: float, kappa: int = 1, sep: int = 1, causal
     threads = oracle.num_threads()
     flags = oracle.CAUSAL if causal else 0
     Q, K, V = (arrays[k].astype(np.float64) for k in ("Q", "K", "V"))
-    done_q, elapsed, runs = 0, 0.0, 0
+    done_q, elapsed, runs, scored = 0, 0.0, 0, 0
     per_slice = cfg.Hq * cfg.Wq
     while elapsed < min_s and runs < 64 * cfg.S:
         s = runs % cfg.S
         t0 = time.perf_counter()
-        J, _, _ = oracle.patchmatch_kappa(Q[s:s + 1], K[s:s + 1], kappa, cfg.iters, cfg.pm_seed, sep=sep, flags=flags)
+        maps = []  # kappa constrained runs; the oracle counts the valid candidates it scores
+        for _ in range(kappa):
+            J1, _, _, ncand = oracle.patchmatch(Q[s:s + 1], K[s:s + 1], cfg.iters, cfg.pm_seed, flags=flags,
+                                                prev=np.stack(maps) if maps else None, sep=sep)
+            maps.append(J1)
+            scored += ncand
+        J = np.stack(maps)
         if snis:
             T, alpha, radius = snis
             oracle.snis(Q[s:s + 1], K[s:s + 1], V[s:s + 1], J, T, alpha, radius, cfg.scale, cfg.pm_seed, flags=flags)
@@ -111,10 +117,30 @@ def cpu_baseline(cfg, arrays, min_s: float, kappa: int = 1, sep: int = 1, causal
         "unit": "queries/s",
         "cores": threads,
         "kind": "oracle",
+        "candidates_per_query_sweep": scored / (done_q * kappa * cfg.iters),
         "sample": f"{runs} slice passes over the {cfg.S}-slice workload ({done_q} queries; {kappa} x {cfg.iters} "
                   f"sweeps + " + (f"{snis[0]}-sample SNIS" if snis else f"{cfg.window}x{cfg.window} attend")
                   + f" each), fp64, {elapsed:.1f} s",
     }
+
+
+def copy_bandwidth(device, mib: int = 1024, reps: int = 10) -> float:
+    """Achievable HBM bandwidth on this device: a plain device-to-device copy of ``mib`` MiB (read + write
+    bytes / time), for context beside the published peak."""
+    import torch
+
+    src = torch.empty(mib << 20, dtype=torch.uint8, device=device)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    b.synchronize()
+    gbps = 2 * src.numel() * reps / (a.elapsed_time(b) * 1e-3) / 1e9
+    del src, dst
+    return gbps
 
 
 def dense_attention(cfg, Q, K, V, reps: int = 3):
@@ -350,6 +376,8 @@ def main(argv=None) -> int:
         "kernels_ms_source": "dispatch-stamped HIP events, timed region B",
         "attend_GBps": att_bytes / (att_ms * 1e-3) / 1e9,
         "candidate_evals_per_s_nominal": kappa * nq * T * cfg.candidates / (ms_step * 1e-3),
+        "step_GBps": (T * kappa * pm_launch_bytes + att_bytes) / (ms_step * 1e-3) / 1e9,
+        "hbm_copy_GBps": copy_bandwidth(dev),
         "wall_ms_per_step": wall * 1e3 / args.steps,
         "device": torch.cuda.get_device_name(dev),
     }
@@ -358,8 +386,13 @@ def main(argv=None) -> int:
         dense["step_speedup"] = dense["ms"] / ms_step
         res["dense_exact_attention"] = dense
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(cfg, data["np"], args.cpu_seconds, kappa, sep, causal,
-                                           (args.snis, args.alpha, args.radius) if args.snis else None)
+        base = cpu_baseline(cfg, data["np"], args.cpu_seconds, kappa, sep, causal,
+                            (args.snis, args.alpha, args.radius) if args.snis else None)
+        # valid candidates per query-sweep as the oracle counts them on its sample (duplicates included)
+        per_sweep = base.pop("candidates_per_query_sweep")
+        res["candidate_evals_per_s"] = kappa * nq * T * per_sweep / (ms_step * 1e-3)
+        res["candidates_per_query_sweep"] = per_sweep
+        res["cpu_baseline"] = base
     print(json.dumps(res), flush=True)
     return 0
 
