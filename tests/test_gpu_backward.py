@@ -60,8 +60,10 @@ def test_backward_parity(scram, work, kappa, window):
 
 def test_backward_causal(scram, work):
     cfg, a, dev, dO, maps = work
-    if (cfg.Hq, cfg.Wq) != (cfg.Hk, cfg.Wk):
-        pytest.skip("causal masking needs one grid")
+    if (cfg.Hq, cfg.Wq) != (cfg.Hk, cfg.Wk):  # raster order needs one grid: rejected
+        with pytest.raises(scram.ScramError):
+            scram.sparse_attend_backward(dev["Q"], dev["K"], dev["V"], maps, dO, cfg.window, cfg.scale, causal=True)
+        return
     J = scram.patchmatch_kappa(dev["Q"], dev["K"], 2, cfg.iters, cfg.pm_seed, sep=2, causal=True)
     got = scram.sparse_attend_backward(dev["Q"], dev["K"], dev["V"], J, dO, cfg.window, cfg.scale, causal=True)
     ref = oracle.sparse_attend_backward(a["Q"], a["K"], a["V"], J.cpu().numpy(), cfg.window, cfg.scale, a["dO"],
