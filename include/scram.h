@@ -277,7 +277,9 @@ int scram_sparse_attend_backward(const void* Q, const void* K, const void* V, in
  *     (Equation 15 with self-normalised weights).
  * All in fp32, with weights kept relative to their running maximum (ratios
  * unchanged).  A query whose weights are all 0 gets a zero row, ESS 0 and
- * variance 0.  The variance takes a second pass over the same samples.
+ * variance 0.  The variance takes a second pass over the same samples.  Sums
+ * over more than 256 samples are compensated (Kahan), so the estimate, ESS and
+ * variance keep fp32 accuracy up to SCRAM_SNIS_MAX_SAMPLES.
  *
  * Arguments:
  *   Q, K, V   inputs, layouts above; dv == d

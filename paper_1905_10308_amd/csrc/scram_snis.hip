@@ -100,11 +100,26 @@ __device__ __forceinline__ void snis_draw(const SnisParams& p, uint32_t g, uint3
 // Without the variance pass and with at most two modes the kernel fits 128
 // VGPRs, i.e. four waves per SIMD; ask for that.  Otherwise the compiler's own
 // allocation (three waves) stands.
-template <bool VAR, int MK>
-constexpr int snis_waves() { return !VAR && MK <= 2 ? 4 : 1; }
+template <bool VAR, int MK, bool KAHAN>
+constexpr int snis_waves() { return !VAR && !KAHAN && MK <= 2 ? 4 : 1; }
 
-template <typename T, int D, int G, bool VAR, int MK>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(snis_waves<VAR, MK>())))
+// Compensated (Kahan) accumulation: s + x with the rounding error of each
+// addition carried in c (the sum is s - c).  Sums of thousands of weights
+// that repeat the same few values would otherwise round the same way at
+// every addition and drift by up to T * 2^-24 relative.
+__device__ __forceinline__ void kahan_add(float& s, float& c, float y_minus_c)
+{
+    const float t = s + y_minus_c;
+    c = (t - s) - y_minus_c;
+    s = t;
+}
+
+// Samples above which the sums are compensated (below, plain fp32 sums stay
+// within a few hundred units of the last place).
+constexpr int kKahanSamples = 256;
+
+template <typename T, int D, int G, bool VAR, int MK, bool KAHAN>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(snis_waves<VAR, MK, KAHAN>())))
 void snis_kernel(SnisParams p)
 {
     using RW = Row<T, D, G>;
@@ -180,10 +195,12 @@ void snis_kernel(SnisParams p)
         }
     };
 
-    float M = -INFINITY, S1 = 0.f, S2 = 0.f;
-    float acc[E];
+    float M = -INFINITY, S1 = 0.f, S2 = 0.f, S1c = 0.f, S2c = 0.f;  // *c: Kahan compensations
+    float acc[E], accc[KAHAN ? E : 1];
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[e] = 0.f;
+#pragma unroll
+    for (int e = 0; e < (KAHAN ? E : 1); ++e) accc[e] = 0.f;
     for (int t0 = 0; t0 < p.samples; t0 += kNb) {
         uint4 kr[kNb][CH], vr[kNb][CH];
         float lw[kNb];
@@ -197,25 +214,48 @@ void snis_kernel(SnisParams p)
         S2 *= alpha * alpha;
 #pragma unroll
         for (int e = 0; e < E; ++e) acc[e] *= alpha;
+        if constexpr (KAHAN) {
+            S1c *= alpha;
+            S2c *= alpha * alpha;
+#pragma unroll
+            for (int e = 0; e < E; ++e) accc[e] *= alpha;
+        }
 #pragma unroll
         for (int sl = 0; sl < kNb; ++sl) {
             const float pj = __builtin_amdgcn_exp2f(lw[sl] - mb);  // exp2(-inf) = 0
-            S1 += pj;
-            S2 += pj * pj;
-            accumulate_row<T, CH>(acc, pj, vr[sl]);
+            if constexpr (KAHAN) {
+                kahan_add(S1, S1c, pj - S1c);
+                kahan_add(S2, S2c, fmaf(pj, pj, -S2c));
+                float vals[E];
+                unpack_row<T, CH>(vr[sl], vals);
+#pragma unroll
+                for (int e = 0; e < E; ++e) kahan_add(acc[e], accc[e], fmaf(pj, vals[e], -accc[e]));
+            } else {
+                S1 += pj;
+                S2 += pj * pj;
+                accumulate_row<T, CH>(acc, pj, vr[sl]);
+            }
         }
         M = mb;
+    }
+    if constexpr (KAHAN) {
+        S1 -= S1c;
+        S2 -= S2c;
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] -= accc[e];
     }
     const float inv = S1 > 0.f ? 1.f / S1 : 0.f;  // no usable sample: zero row
 
     if constexpr (VAR) {
         // second pass over the same samples: sum_t (w_t / sum w)^2 (v_t - estimate)^2
-        float mean[E], vacc[E];
+        float mean[E], vacc[E], vaccc[KAHAN ? E : 1];
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             mean[e] = acc[e] * inv;
             vacc[e] = 0.f;
         }
+#pragma unroll
+        for (int e = 0; e < (KAHAN ? E : 1); ++e) vaccc[e] = 0.f;
         if (S1 > 0.f) {
             for (int t0 = 0; t0 < p.samples; t0 += kNb) {
                 uint4 kr[kNb][CH], vr[kNb][CH];
@@ -230,9 +270,16 @@ void snis_kernel(SnisParams p)
 #pragma unroll
                     for (int e = 0; e < E; ++e) {
                         const float dlt = vals[e] - mean[e];
-                        vacc[e] = fmaf(wn2 * dlt, dlt, vacc[e]);
+                        if constexpr (KAHAN)
+                            kahan_add(vacc[e], vaccc[e], fmaf(wn2 * dlt, dlt, -vaccc[e]));
+                        else
+                            vacc[e] = fmaf(wn2 * dlt, dlt, vacc[e]);
                     }
                 }
+            }
+            if constexpr (KAHAN) {
+#pragma unroll
+                for (int e = 0; e < E; ++e) vacc[e] -= vaccc[e];
             }
         }
         constexpr int kEpc = RW::kEpc;
@@ -259,8 +306,12 @@ hipError_t run_snis(const SnisParams& p0, hipStream_t st, hipEvent_t e0, hipEven
     // the smallest register budget that holds the query's modes
     auto go = [&](auto mk) {
         constexpr int MK = decltype(mk)::value;
-        if (p.var) return launch(snis_kernel<T, D, G, true, MK>, blocks, st, e0, e1, p);
-        return launch(snis_kernel<T, D, G, false, MK>, blocks, st, e0, e1, p);
+        if (p.samples > kKahanSamples) {
+            if (p.var) return launch(snis_kernel<T, D, G, true, MK, true>, blocks, st, e0, e1, p);
+            return launch(snis_kernel<T, D, G, false, MK, true>, blocks, st, e0, e1, p);
+        }
+        if (p.var) return launch(snis_kernel<T, D, G, true, MK, false>, blocks, st, e0, e1, p);
+        return launch(snis_kernel<T, D, G, false, MK, false>, blocks, st, e0, e1, p);
     };
     if (p.kappa == 1) return go(std::integral_constant<int, 1>{});
     if (p.kappa == 2) return go(std::integral_constant<int, 2>{});

@@ -54,7 +54,7 @@ def check(cfg_dtype, a_V, got, ref, tag=""):
 
 
 @pytest.mark.parametrize("T,alpha,radius,kappa", [(1, 0.9, 3, 1), (7, 0.9, 4, 2), (32, 0.5, 2, 2), (64, 1.0, 0, 1),
-                                                  (33, 0.0, 5, 2), (48, 0.8, 16, 2)])
+                                                  (33, 0.0, 5, 2), (48, 0.8, 16, 2), (257, 0.9, 4, 2)])
 def test_snis_parity(scram, work, T, alpha, radius, kappa):
     cfg, a, dev, modes = work
     m = modes[:kappa] if kappa > 1 else modes[0]
@@ -146,6 +146,21 @@ def test_snis_full_size_sampled(scram):
     e_out, e_ess = check(cfg.dtype, a["V"], sel, ref, "full size")
     log(f"{cfg.name} full size T={T}: estimate err/max|V| {e_out:.2e}, ESS rel {e_ess:.2e}, "
         f"mean ESS {float(ref[1].mean()):.2f}")
+
+
+def test_snis_maximum_samples(scram):
+    """The largest sample count the ABI takes (2^20 per query) on a 2 x 3 grid, both statistics on.  Six
+    keys give six distinct weights, each added some 10^5 times: plain fp32 sums would round the same way
+    at every addition and drift by up to 2^20 * 2^-24 relative (compensated sums keep to fp32 level)."""
+    T = 1 << 20  # SCRAM_SNIS_MAX_SAMPLES
+    rng = np.random.default_rng(8)
+    Q, K, V = (rng.standard_normal((1, 2, 3, 16)).astype(np.float32) for _ in range(3))
+    modes = np.array([[[5, 0, 3], [1, 4, 2]]], np.int32)
+    got = scram.snis_attend(to_dev(Q, "f32"), to_dev(K, "f32"), to_dev(V, "f32"), torch.from_numpy(modes).cuda(), T,
+                            alpha=0.6, radius=1, scale=0.25, seed=21, ess=True, var=True)
+    ref = oracle.snis(Q, K, V, modes, T, 0.6, 1, 0.25, 21)
+    e_out, e_ess = check("f32", V, got, ref, "2^20 samples")
+    log(f"2^20 samples: mean ESS {float(ref[1].mean()):.0f}, estimate err/max|V| {e_out:.2e}, ESS rel {e_ess:.2e}")
 
 
 def test_snis_bad_arguments_raise(scram):
