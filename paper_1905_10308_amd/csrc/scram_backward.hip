@@ -543,25 +543,57 @@ __device__ __forceinline__ KeyPos key_pos(const BwdParams& p, uint32_t kg)
 
 // One lane group per key j: sum over the entries (i, e) whose match e lies
 // in the neighbourhood of j (so j is in window e of i).  Keys with more than
-// kHeavyEntries entries are appended to the heavy list instead.
+// kHeavyEntries entries are appended to the heavy list instead.  The block
+// ranks its tile's keys by entry count and hands them out in that order, so
+// the keys of one wave carry similar work (a wave lasts as long as its
+// busiest lane group).
 template <typename T, int D, int G, bool MULTI>
 __global__ __launch_bounds__(kBlock) void bwd_key_kernel(BwdParams p)
 {
     using RW = Row<T, D, G>;
     constexpr int CH = RW::kCh;
     constexpr int E = CH * RW::kEpc;
+    constexpr int kKeys = RW::kQpb;  // keys of the block's tile
+    __shared__ int32_t s_total[kKeys], s_key[kKeys], s_order[kKeys];
     const int lane = threadIdx.x & (G - 1);
+    const int grp = threadIdx.x / G;
     const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
-    uint32_t kg;  // global key id s * nkeys + j
-    if (!tile_item<RW::kQpb>(p.tk, blk, threadIdx.x / G, kg)) return;
+    {
+        // the tile's keys and their entry counts; -1: past the grid's edge or heavy
+        uint32_t kg0;
+        int total = -1;
+        if (tile_item<RW::kQpb>(p.tk, blk, grp, kg0)) {
+            const KeyPos k0 = key_pos(p, kg0);
+            const int32_t* off0 = p.offsets + static_cast<size_t>(k0.s) * p.nkeys;
+            total = 0;
+            for (int r = k0.r0; r <= k0.r1; ++r) total += off0[r * p.Wk + k0.c1 + 1] - off0[r * p.Wk + k0.c0];
+            if (total > kHeavyEntries) {
+                if (lane == 0) p.heavy[atomicAdd(p.n_heavy, 1)] = static_cast<int32_t>(kg0);
+                total = -1;
+            }
+        }
+        if (lane == 0) {
+            s_total[grp] = total;
+            s_key[grp] = static_cast<int32_t>(kg0);
+        }
+    }
+    __syncthreads();
+    {
+        // rank by entry count, most first (ties by position), so each wave takes keys of similar work
+        const int mine = s_total[grp];
+        int rank = 0;
+        for (int i = 0; i < kKeys; ++i) {
+            const int other = s_total[i];
+            rank += (other > mine || (other == mine && i < grp)) ? 1 : 0;
+        }
+        if (lane == 0) s_order[rank] = grp;
+    }
+    __syncthreads();
+    const int src = s_order[grp];
+    if (s_total[src] < 0) return;
+    const uint32_t kg = static_cast<uint32_t>(s_key[src]);  // global key id s * nkeys + j
     const KeyPos k = key_pos(p, kg);
     const int32_t* off = p.offsets + static_cast<size_t>(k.s) * p.nkeys;
-    int total = 0;
-    for (int r = k.r0; r <= k.r1; ++r) total += off[r * p.Wk + k.c1 + 1] - off[r * p.Wk + k.c0];
-    if (total > kHeavyEntries) {
-        if (lane == 0) p.heavy[atomicAdd(p.n_heavy, 1)] = static_cast<int32_t>(kg);
-        return;
-    }
     uint4 kj[CH], vj[CH];
     load_row<T, D, G>(static_cast<const T*>(p.K), kg, lane, kj);
     load_row<T, D, G>(static_cast<const T*>(p.V), kg, lane, vj);
