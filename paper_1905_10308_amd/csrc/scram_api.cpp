@@ -163,8 +163,11 @@ int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int
     }
     for (int k = 1; k <= iters && e == hipSuccess; ++k) {
         const int pk = (iters - k) % 2;
-        e = scram::launch_pm_iter(dtype, Q, K, grid, seed, run, uint32_t(t0 + k - 1), flags, Jcur, scur, Jbuf[pk],
-                                  sbuf[pk], stream, ev ? ev[2 * k] : nullptr, ev ? ev[2 * k + 1] : nullptr);
+        // maps between two sweeps of this call carry the stable-entry mark;
+        // the caller's init and the final map do not
+        e = scram::launch_pm_iter(dtype, Q, K, grid, seed, run, uint32_t(t0 + k - 1), flags, Jcur, scur, k > 1,
+                                  k < iters, Jbuf[pk], sbuf[pk], stream, ev ? ev[2 * k] : nullptr,
+                                  ev ? ev[2 * k + 1] : nullptr);
         Jcur = Jbuf[pk];
         scur = sbuf[pk];
     }

@@ -33,10 +33,14 @@ hipError_t launch_pm_init(int dtype, const void* Q, const void* K, const Grid& g
 
 // One Jacobi sweep t: (Jp, sp) -> (Jn, sn).  Jp == sp == nullptr: the first
 // sweep of a run from the random initial field (flags must be 0), which the
-// sweep recomputes instead of reading.
+// sweep recomputes instead of reading.  marked_in: Jp was written by the
+// previous sweep of the same call with mark_out, so its entries carry the
+// stable mark (bit 31) that lets this sweep skip candidates it already
+// scored; mark_out: write that mark (never into a map the caller reads).
 hipError_t launch_pm_iter(int dtype, const void* Q, const void* K, const Grid& g, uint64_t seed,
                           const RunSpec& run, uint32_t t, uint32_t flags, const int32_t* Jp, const float* sp,
-                          int32_t* Jn, float* sn, hipStream_t stream, hipEvent_t start, hipEvent_t stop);
+                          bool marked_in, bool mark_out, int32_t* Jn, float* sn, hipStream_t stream,
+                          hipEvent_t start, hipEvent_t stop);
 
 // Window softmax + value gather around the kappa maps in J ([kappa, n]).
 hipError_t launch_attend(int dtype, const void* Q, const void* K, const void* V, const int32_t* J, int kappa,

@@ -28,11 +28,22 @@ struct PmParams {
     int sep;              // minimum Chebyshev distance to every previous match
     int causal;           // keys after the query (raster order) are not valid
     int first;            // the sweep recomputes the random initial field (Jp, sp unused)
+    int marked_in;        // Jp entries carry kStable (Jp was written by a sweep with mark_out)
+    int mark_out;         // set kStable on Jn entries whose match did not change
     Tiling tq;            // sweep blocks -> tiles of the query grid
 };
 
 
 constexpr int kMaxPrev = 7;  // previous runs a PatchMatch run may be constrained by
+
+// Between two sweeps of one call the map entries carry a mark in bit 31:
+// set when the sweep that wrote the entry kept its incumbent.  A query's
+// propagation candidate from a marked neighbour is the candidate that query
+// already scored in the previous sweep (same neighbour match, same offset),
+// and that sweep ended on a running best at least as good in the strict
+// total order; the best only improves, so the candidate cannot win again and
+// is not gathered.  The result is identical with or without the mark.
+constexpr uint32_t kStable = 0x80000000u;
 
 // is_index_valid for one query: not after the query when causal, and at
 // Chebyshev distance >= sep from each previous run's match (at most NP of
@@ -159,7 +170,8 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
         if constexpr (FIRST) {
             cur[j] = initial_draw(p, g[j], x[j] * p.Wq + y[j]);
         } else {
-            cur[j] = clamp_index(p.Jp[g[j]], p.nkeys);
+            const int32_t raw = p.Jp[g[j]];
+            cur[j] = clamp_index(p.marked_in ? static_cast<int32_t>(raw & ~kStable) : raw, p.nkeys);
             best[j] = p.sp[g[j]];
         }
         cur0[j] = cur[j];
@@ -229,14 +241,21 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
                 if (nx >= 0 && nx < p.Hq && ny >= 0 && ny < p.Wq) {
                     const uint32_t ng = static_cast<uint32_t>((static_cast<size_t>(s[j]) * p.Hq + nx) * p.Wq + ny);
                     uint32_t nb;
-                    if constexpr (FIRST)
+                    bool seen = false;  // scored by this query in the previous sweep
+                    if constexpr (FIRST) {
                         nb = static_cast<uint32_t>(initial_draw(p, ng, static_cast<uint32_t>(nx * p.Wq + ny)));
-                    else
-                        nb = clamp_index(Jp[ng], p.nkeys);
+                    } else {
+                        int32_t raw = Jp[ng];
+                        if (p.marked_in) {
+                            seen = (static_cast<uint32_t>(raw) & kStable) != 0u;
+                            raw = static_cast<int32_t>(raw & ~kStable);
+                        }
+                        nb = clamp_index(raw, p.nkeys);
+                    }
                     uint32_t nu, nv;
                     divmod(nb, p.div_wk, nu, nv);
                     const int r = static_cast<int>(nu) - ox, cc = static_cast<int>(nv) - oy;
-                    if (r >= 0 && r < p.Hk && cc >= 0 && cc < p.Wk) {
+                    if (!seen && r >= 0 && r < p.Hk && cc >= 0 && cc < p.Wk) {
                         c = r * p.Wk + cc;
                         if (VALID && !val[j].ok(r, cc, c)) c = -1;
                     }
@@ -371,7 +390,8 @@ __global__ __launch_bounds__(kBlock) void pm_iter_kernel(PmParams p)
 #pragma unroll
     for (int j = 0; j < QPG; ++j) {
         if (live[j] && lane == 0) {
-            p.Jn[g[j]] = cur[j];
+            p.Jn[g[j]] = static_cast<int32_t>(static_cast<uint32_t>(cur[j]) |
+                                              (p.mark_out && cur[j] == cur0[j] ? kStable : 0u));
             p.sn[g[j]] = best[j];
         }
     }
@@ -467,9 +487,12 @@ hipError_t launch_pm_init(int dtype, const void* Q, const void* K, const Grid& g
 
 hipError_t launch_pm_iter(int dtype, const void* Q, const void* K, const Grid& g, uint64_t seed,
                           const RunSpec& run, uint32_t t, uint32_t flags, const int32_t* Jp, const float* sp,
-                          int32_t* Jn, float* sn, hipStream_t stream, hipEvent_t start, hipEvent_t stop)
+                          bool marked_in, bool mark_out, int32_t* Jn, float* sn, hipStream_t stream,
+                          hipEvent_t start, hipEvent_t stop)
 {
     PmParams p = make_pm_params(Q, K, g, seed);
+    p.marked_in = marked_in && Jp != nullptr ? 1 : 0;
+    p.mark_out = mark_out ? 1 : 0;
     // no previous map: the first sweep of a fresh run (propagation and random
     // search both on) starts from the random initial field it recomputes
     p.first = Jp == nullptr ? 1 : 0;

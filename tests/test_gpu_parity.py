@@ -331,3 +331,23 @@ def test_fused_first_sweep_equals_init_then_sweep(scram, variant):
         fused, sf = scram.patchmatch(Q, K, T, cfg.pm_seed, return_score=True, **kw)
         split, ss = scram.patchmatch(Q, K, T, cfg.pm_seed, init=J0, init_score=s0, return_score=True, **kw)
         assert torch.equal(fused, split) and torch.equal(sf, ss), f"T={T}"
+
+
+@pytest.mark.parametrize("variant", ["plain", "causal", "kappa2", "no_random_search"])
+def test_stable_marks_leave_the_map_unchanged(scram, work, variant):
+    """Within one call a sweep skips the propagation candidates whose source entry the previous sweep
+    left unchanged (this query already scored them then).  A run issued one sweep per call carries no
+    such marks and gathers every candidate: both must give the same maps and scores, bit for bit."""
+    cfg, a, dev = work
+    Q, K = dev["Q"], dev["K"]
+    if variant == "causal" and (cfg.Hq, cfg.Wq) != (cfg.Hk, cfg.Wk):
+        pytest.skip("the causal mask needs one grid")
+    prev = scram.patchmatch(Q, K, 2, cfg.pm_seed)[None] if variant == "kappa2" else None
+    kw = dict(prev=prev, sep=2, causal=variant == "causal", flags=2 if variant == "no_random_search" else 0)
+    T = cfg.iters + 2
+    whole, sw = scram.patchmatch(Q, K, T, cfg.pm_seed, return_score=True, **kw)
+    J, s = scram.patchmatch(Q, K, 0, cfg.pm_seed, return_score=True, **kw)
+    for t in range(1, T + 1):
+        J, s = scram.patchmatch(Q, K, 1, cfg.pm_seed, init=J, init_score=s, t0=t, return_score=True, **kw)
+    assert torch.equal(whole, J) and torch.equal(sw, s)
+    assert int(whole.min()) >= 0 and int(whole.max()) < cfg.Hk * cfg.Wk  # no mark leaks into the result
