@@ -45,3 +45,22 @@ def dense_attend(Q, K, V, scale):
     P /= P.sum(axis=2, keepdims=True)
     v = np.asarray(V, np.float64).reshape(S, -1, dv)
     return np.einsum("sij,sjd->sid", P, v).reshape(S, Hq, Wq, dv)
+
+
+def brute_argmax_rows(Q, K, query_ids):
+    """:func:`brute_argmax` for the flat query ids ``query_ids`` only -> (J int32 [m], best float64 [m]).
+
+    Each sampled query is scored against every key of its own slice, so the
+    full-size grids can be sampled without the O(n^2) score matrix."""
+    S, Hq, Wq, d = Q.shape
+    q, k = _flat(Q, K)
+    ids = np.asarray(query_ids, np.int64)
+    s, r = np.divmod(ids, Hq * Wq)
+    J = np.empty(ids.size, np.int32)
+    best = np.empty(ids.size, np.float64)
+    for sl in np.unique(s):
+        pick = np.nonzero(s == sl)[0]
+        A = q[sl, r[pick]] @ k[sl].T
+        J[pick] = np.argmax(A, axis=1)  # first occurrence = lowest index among ties
+        best[pick] = A[np.arange(pick.size), J[pick]]
+    return J, best

@@ -644,6 +644,343 @@ __global__ __launch_bounds__(kBlock) void bwd_heavy_kernel(BwdParams p)
     }
 }
 
+// ---------------------------------------------------------------------------
+// Key side on the matrix cores (bf16 storage).  A block takes a tile of 64
+// keys; the queries whose key sets reach into the tile are exactly the
+// entries whose match lies in the tile's halo (the tile widened by b), one
+// contiguous entry range per halo row.  Between the tile's keys and those
+// entries the pairs form a dense 64 x E block, of which the window test keeps
+// the pairs with |match - key|_inf <= b.  Per chunk of kCE entries staged in
+// LDS (q and dO rows, row-major and transposed, plus match, log2 normaliser
+// and D of each entry), each wave, owning 16 keys, computes on the matrix cores
+//   S^T = Q_E K_w^T,  dP^T = dO_E V_w^T                 (entries x keys)
+// then in registers P = window test ? 2^(S scale log2 e - lse2) : 0 and
+// dS = P (dP - D), and again on the matrix cores
+//   dV_w += P dO_E,   dK_w += dS Q_E                    (keys x channels).
+// The output layout of the first products is the operand layout of the
+// second (lane l holds key l mod 16 and four entries), so P and dS never
+// leave registers; the entries' order along the contraction only has to be
+// the same in both operands.  P and dS enter the matrix cores as three bf16
+// parts each (hi + mid + lo: 24 significant bits of the fp32 value, the
+// products exact), so the gradients carry fp32 precision; all sums are fp32.
+// ---------------------------------------------------------------------------
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kTileKeys = 64;                             // keys per block, 16 per wave
+constexpr int kTileMaxB = 7;                              // windows up to 15 x 15
+constexpr int kTileMaxRows = kTileKeys + 2 * kTileMaxB;   // halo rows of the tallest tile
+
+template <int D>
+struct KeyTile {
+    static constexpr int kCE = D == 16 ? 128 : (D == 128 ? 32 : 64);  // entries per staged chunk
+    static constexpr int kRowB = 2 * D + 16;           // row-major row stride in bytes (padded)
+    static constexpr int kTrB = 2 * kCE + 8;           // transposed row stride in bytes (padded)
+    static constexpr int kDs = D >= 32 ? D / 32 : 1;   // 32-channel steps of the first products
+    static constexpr int kOt = D / 16;                 // 16-channel tiles of dK_w, dV_w
+    static constexpr int kPieces = D / 8;              // 16-byte pieces per row
+    static constexpr int kWaves = D > 64 ? 2 : 3;      // waves per SIMD the registers are sized for
+    // staging: a unit is one 16-byte piece of the q or dO row of a pair of
+    // entry slots; thread t takes units t, t + kBlock, ... -- always the same
+    // slot pair, kUpt pieces
+    static constexpr int kPairs = kCE / 2;
+    static constexpr int kUpt = kPairs * 2 * kPieces / kBlock;
+    static_assert(kUpt >= 1 && kUpt * kBlock == kPairs * 2 * kPieces && kBlock % kPairs == 0, "whole units");
+};
+
+// x = hi + mid + lo + O(2^-27 |x|), each part bf16 (round to nearest even;
+// x - hi and (x - hi) - mid are exact in fp32)
+__device__ __forceinline__ void split3(float x, __bf16& hi, __bf16& mid, __bf16& lo)
+{
+    hi = static_cast<__bf16>(x);
+    const float r1 = x - static_cast<float>(hi);
+    mid = static_cast<__bf16>(r1);
+    lo = static_cast<__bf16>(r1 - static_cast<float>(mid));
+}
+
+template <int D, bool MULTI>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(KeyTile<D>::kWaves))) void bwd_key_tile_kernel(BwdParams p)
+{
+    using KT = KeyTile<D>;
+    constexpr int kCE = KT::kCE;
+    __shared__ __align__(16) unsigned char s_row[2][kCE * KT::kRowB];  // q, dO rows of the chunk's entries
+    __shared__ __align__(16) unsigned char s_tr[2][D * KT::kTrB];      // the same, channel-major
+    __shared__ int4 s_meta[kCE];        // match row, match column, lse2 bits, D bits
+    __shared__ int32_t s_el[MULTI ? kCE : 1][2];                 // window index e, query's raster index
+    __shared__ int32_t s_prevc[MULTI ? kCE : 1][kMaxKappa - 1];  // centres of windows 0..e-1
+    __shared__ int32_t s_lo[kTileMaxRows], s_pre[kTileMaxRows + 1];
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int m = lane & 15, g4 = lane >> 4;
+    const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+
+    // the tile: rows x0.., columns y0.. of slice s (th x tw keys, clipped to the grid)
+    uint32_t s, k, tr, tc;
+    divmod(blk, p.tk.div_slice, s, k);
+    divmod(k, p.tk.div_w, tr, tc);
+    const int tw = 1 << p.tk.lw, th = kTileKeys >> p.tk.lw;
+    const int x0 = static_cast<int>(tr) * th, y0 = static_cast<int>(tc) * tw;
+    const int hr0 = max(x0 - p.b, 0), hr1 = min(x0 + th - 1 + p.b, p.Hk - 1);
+    const int hc0 = max(y0 - p.b, 0), hc1 = min(y0 + tw - 1 + p.b, p.Wk - 1);
+    const int nrows = hr1 - hr0 + 1;
+    const int32_t* off = p.offsets + static_cast<size_t>(s) * p.nkeys;
+    if (wave == 0) {
+        // entry counts of halo rows lane and lane + 64, then an inclusive scan across the wave
+        static_assert(kTileMaxRows <= 128, "two halo rows per lane");
+        int cnt[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int i = lane + 64 * h;
+            cnt[h] = 0;
+            if (i < nrows) {
+                const int r = hr0 + i;
+                const int32_t lo = off[r * p.Wk + hc0];
+                s_lo[i] = lo;
+                cnt[h] = off[r * p.Wk + hc1 + 1] - lo;
+            }
+        }
+        int carry = 0;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            int incl = cnt[h];
+#pragma unroll
+            for (int k2 = 1; k2 < 64; k2 <<= 1) {
+                const int y = __shfl_up(incl, k2, 64);
+                if (lane >= k2) incl += y;
+            }
+            if (lane + 64 * h < nrows) s_pre[lane + 64 * h + 1] = carry + incl;
+            carry += __shfl(incl, 63, 64);
+        }
+        if (lane == 0) s_pre[0] = 0;
+    }
+
+    // this lane's key (column of the first products): item 16 wave + m of the tile
+    const int item = 16 * wave + m;
+    const int kx = x0 + (item >> p.tk.lw), ky = y0 + (item & (tw - 1));
+    const bool key_ok = kx < p.Hk && ky < p.Wk;
+    const size_t kslice = static_cast<size_t>(s) * p.nkeys;
+    const size_t krow = kslice + (key_ok ? static_cast<size_t>(kx) * p.Wk + ky : static_cast<size_t>(x0) * p.Wk + y0);
+    bf16x8_t kf[KT::kDs], vf[KT::kDs];
+#pragma unroll
+    for (int ds = 0; ds < KT::kDs; ++ds) {
+        const int d = 32 * ds + 8 * g4;
+        uint4 kw = make_uint4(0u, 0u, 0u, 0u), vw = kw;
+        if (d < D) {
+            kw = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p.K) + krow * D + d);
+            vw = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p.V) + krow * D + d);
+        }
+        kf[ds] = __builtin_bit_cast(bf16x8_t, kw);
+        vf[ds] = __builtin_bit_cast(bf16x8_t, vw);
+    }
+    const uint32_t key_local = static_cast<uint32_t>(kx) * p.Wk + ky;  // raster index (causal test)
+
+    f32x4_t dk[KT::kOt], dv[KT::kOt];
+#pragma unroll
+    for (int o = 0; o < KT::kOt; ++o) dk[o] = dv[o] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    __syncthreads();
+    const int E = s_pre[nrows];
+    const uint16_t* Qb = static_cast<const uint16_t*>(p.Q);
+    const uint16_t* Gb = static_cast<const uint16_t*>(p.dO);
+    // Staging is software-pipelined: while a chunk is multiplied, the next
+    // chunk's rows and statistics are in flight into registers and the entry
+    // codes of the one after it into registers as well.
+    const int pair = static_cast<int>(threadIdx.x) % KT::kPairs;
+    const int piece0 = static_cast<int>(threadIdx.x) / KT::kPairs;  // first piece; then + kBlock / kPairs
+    // the statistics of the pairs are loaded by a quarter of the pairs' threads in each wave, so that no
+    // wave waits on more of them than the others
+    // (the threads of pair P are P + kPairs k, k = 0 .. kBlock / kPairs - 1; quarter q of the pairs takes
+    // the k whose thread lies in wave q)
+    static_assert(64 % KT::kPairs == 0 && KT::kPairs % 4 == 0, "every wave holds every pair");
+    const bool meta_thread = piece0 == (pair / (KT::kPairs / 4)) * (64 / KT::kPairs);
+    // entry code of slot 2 pair + h of the chunk starting at c0, -1 past the end
+    auto slot_code = [&](int c0, int h) {
+        const int v = c0 + 2 * pair + h;
+        if (v >= E) return -1;
+        int lo = 0, hi = nrows - 1;  // halo row holding flat position v: the last with s_pre <= v
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (s_pre[mid] <= v) lo = mid; else hi = mid - 1;
+        }
+        return static_cast<int>(p.entries[s_lo[lo] + (v - s_pre[lo])]);
+    };
+    struct Staged {
+        uint4 row[KT::kUpt][2];  // [unit][slot of the pair]
+        int32_t match[2];
+        float lse2[2], dq[2];
+    };
+    auto fetch = [&](const int (&code)[2], Staged& st) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            uint32_t e = 0, g = 0;
+            if (code[h] >= 0) divmod(static_cast<uint32_t>(code[h]), p.div_n, e, g);
+#pragma unroll
+            for (int i = 0; i < KT::kUpt; ++i) {
+                const int w = piece0 + i * (kBlock / KT::kPairs);
+                const int which = w / KT::kPieces, piece = w % KT::kPieces;
+                st.row[i][h] = code[h] >= 0
+                                   ? reinterpret_cast<const uint4*>((which ? Gb : Qb) + static_cast<size_t>(g) * D)[piece]
+                                   : make_uint4(0u, 0u, 0u, 0u);  // zeros past the end: finite operands
+            }
+            st.match[h] = -1;
+            st.lse2[h] = st.dq[h] = 0.f;
+            if (meta_thread && code[h] >= 0) {
+                st.match[h] = p.J[code[h]];  // clamped when stored: no wait here
+                st.lse2[h] = p.lse2[g];
+                st.dq[h] = p.Dq[g];
+            }
+        }
+    };
+    auto store = [&](const int (&code)[2], const Staged& st) {
+#pragma unroll
+        for (int i = 0; i < KT::kUpt; ++i) {
+            const int w = piece0 + i * (kBlock / KT::kPairs);
+            const int which = w / KT::kPieces, piece = w % KT::kPieces;
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+                *reinterpret_cast<uint4*>(s_row[which] + (2 * pair + h) * KT::kRowB + piece * 16) = st.row[i][h];
+            const uint32_t a[4] = {st.row[i][0].x, st.row[i][0].y, st.row[i][0].z, st.row[i][0].w};
+            const uint32_t b2[4] = {st.row[i][1].x, st.row[i][1].y, st.row[i][1].z, st.row[i][1].w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {  // channels 2j, 2j+1 of the piece: (slot 2 pair, slot 2 pair + 1) words
+                *reinterpret_cast<uint32_t*>(s_tr[which] + (piece * 8 + 2 * j) * KT::kTrB + pair * 4) =
+                    (a[j] & 0xFFFFu) | (b2[j] << 16);
+                *reinterpret_cast<uint32_t*>(s_tr[which] + (piece * 8 + 2 * j + 1) * KT::kTrB + pair * 4) =
+                    (a[j] >> 16) | (b2[j] & 0xFFFF0000u);
+            }
+        }
+        if (meta_thread) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int t = 2 * pair + h;
+                int4 meta = make_int4(-(1 << 30), -(1 << 30), 0, 0);  // no key is near this match
+                if constexpr (MULTI) s_el[t][0] = s_el[t][1] = 0;
+                if (code[h] >= 0) {
+                    uint32_t mu, mv;
+                    divmod(static_cast<uint32_t>(clamp_index(st.match[h], p.nkeys)), p.div_wk, mu, mv);
+                    meta = make_int4(static_cast<int>(mu), static_cast<int>(mv), __float_as_int(st.lse2[h]),
+                                     __float_as_int(st.dq[h]));
+                    if constexpr (MULTI) {
+                        uint32_t e, g, sl, local;
+                        divmod(static_cast<uint32_t>(code[h]), p.div_n, e, g);
+                        divmod(g, p.div_plane, sl, local);
+                        s_el[t][0] = static_cast<int32_t>(e);
+                        s_el[t][1] = static_cast<int32_t>(local);
+                        for (int f = 0; f < static_cast<int>(e); ++f)
+                            s_prevc[t][f] = clamp_index(p.J[static_cast<size_t>(f) * p.n + g], p.nkeys);
+                    }
+                }
+                s_meta[t] = meta;
+            }
+        }
+    };
+    int code[2] = {slot_code(0, 0), slot_code(0, 1)};
+    Staged stg;
+    fetch(code, stg);
+    int code_next[2] = {slot_code(kCE, 0), slot_code(kCE, 1)};
+    for (int c0 = 0; c0 < E; c0 += kCE) {
+        __syncthreads();  // the previous chunk is consumed
+        store(code, stg);
+        __syncthreads();
+        code[0] = code_next[0];
+        code[1] = code_next[1];
+        if (c0 + kCE < E) fetch(code, stg);  // the next chunk, in flight during the products
+        code_next[0] = slot_code(c0 + 2 * kCE, 0);
+        code_next[1] = slot_code(c0 + 2 * kCE, 1);
+
+#pragma unroll 1
+        for (int ks = 0; ks < kCE / 32; ++ks) {
+            // S^T, dP^T for entries ks*32 + 16 et + (0..15) against the wave's 16 keys
+            f32x4_t sc[2], dp[2];
+#pragma unroll
+            for (int et = 0; et < 2; ++et) {
+                sc[et] = dp[et] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+                const int er = ks * 32 + et * 16 + m;
+#pragma unroll
+                for (int ds = 0; ds < KT::kDs; ++ds) {
+                    const int d = 32 * ds + 8 * g4;
+                    uint4 aq = make_uint4(0u, 0u, 0u, 0u), ag = aq;
+                    if (d < D) {
+                        aq = *reinterpret_cast<const uint4*>(s_row[0] + er * KT::kRowB + d * 2);
+                        ag = *reinterpret_cast<const uint4*>(s_row[1] + er * KT::kRowB + d * 2);
+                    }
+                    sc[et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, aq), kf[ds], sc[et],
+                                                                     0, 0, 0);
+                    dp[et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ag), vf[ds], dp[et],
+                                                                     0, 0, 0);
+                }
+            }
+            // P and dS of (key m, entry ks*32 + 16 et + 4 g4 + r), split for the matrix cores; operand
+            // slot 4 et + r of this lane
+            bf16x8_t ph, pm, pl, sh, sm, sl;
+#pragma unroll
+            for (int et = 0; et < 2; ++et) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int te = ks * 32 + et * 16 + 4 * g4 + r;
+                    const int4 mt = s_meta[te];
+                    bool ok = key_ok && abs(mt.x - kx) <= p.b && abs(mt.y - ky) <= p.b;
+                    if constexpr (MULTI) {
+                        const int e = s_el[te][0];
+                        for (int f = 0; f < e && ok; ++f) {
+                            uint32_t fu, fv;
+                            divmod(static_cast<uint32_t>(s_prevc[te][f]), p.div_wk, fu, fv);
+                            if (abs(static_cast<int>(fu) - kx) <= p.b && abs(static_cast<int>(fv) - ky) <= p.b)
+                                ok = false;  // an earlier window of the query holds this key
+                        }
+                        if (p.causal) ok = ok && key_local <= static_cast<uint32_t>(s_el[te][1]);
+                    }
+                    const float pr =
+                        ok ? __builtin_amdgcn_exp2f(sc[et][r] * p.scale_log2e - __int_as_float(mt.z)) : 0.f;
+                    const float dsr = pr * (dp[et][r] - __int_as_float(mt.w));
+                    __bf16 a0, a1, a2;
+                    split3(pr, a0, a1, a2);
+                    ph[4 * et + r] = a0;
+                    pm[4 * et + r] = a1;
+                    pl[4 * et + r] = a2;
+                    split3(dsr, a0, a1, a2);
+                    sh[4 * et + r] = a0;
+                    sm[4 * et + r] = a1;
+                    sl[4 * et + r] = a2;
+                }
+            }
+            // dV_w += P dO_E, dK_w += dS Q_E: operand slot kk of this lane is entry
+            // ks*32 + (kk < 4 ? 4 g4 + kk : 16 + 4 g4 + kk - 4), channel 16 o + m
+#pragma unroll
+            for (int o = 0; o < KT::kOt; ++o) {
+                const int ch = 16 * o + m;
+                const int e0 = ks * 32 + 4 * g4;
+                const uint2 g_lo = *reinterpret_cast<const uint2*>(s_tr[1] + ch * KT::kTrB + e0 * 2);
+                const uint2 g_hi = *reinterpret_cast<const uint2*>(s_tr[1] + ch * KT::kTrB + (e0 + 16) * 2);
+                const uint2 q_lo = *reinterpret_cast<const uint2*>(s_tr[0] + ch * KT::kTrB + e0 * 2);
+                const uint2 q_hi = *reinterpret_cast<const uint2*>(s_tr[0] + ch * KT::kTrB + (e0 + 16) * 2);
+                const bf16x8_t bg = __builtin_bit_cast(bf16x8_t, make_uint4(g_lo.x, g_lo.y, g_hi.x, g_hi.y));
+                const bf16x8_t bq = __builtin_bit_cast(bf16x8_t, make_uint4(q_lo.x, q_lo.y, q_hi.x, q_hi.y));
+                dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, bg, dv[o], 0, 0, 0);
+                dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pm, bg, dv[o], 0, 0, 0);
+                dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, bg, dv[o], 0, 0, 0);
+                dk[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sh, bq, dk[o], 0, 0, 0);
+                dk[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sm, bq, dk[o], 0, 0, 0);
+                dk[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sl, bq, dk[o], 0, 0, 0);
+            }
+        }
+    }
+
+    // lane holds keys 4 g4 + r of the wave, channel 16 o + m
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int it = 16 * wave + 4 * g4 + r;
+        const int ox = x0 + (it >> p.tk.lw), oy = y0 + (it & (tw - 1));
+        if (ox >= p.Hk || oy >= p.Wk) continue;
+        const size_t row = (kslice + static_cast<size_t>(ox) * p.Wk + oy) * D;
+#pragma unroll
+        for (int o = 0; o < KT::kOt; ++o) {
+            p.dK[row + 16 * o + m] = dk[o][r] * p.scale;
+            p.dV[row + 16 * o + m] = dv[o][r];
+        }
+    }
+}
+
 template <typename T, int D>
 hipError_t run_backward(const BwdParams& p0, hipStream_t st, hipEvent_t* ev)
 {
@@ -670,6 +1007,17 @@ hipError_t run_backward(const BwdParams& p0, hipStream_t st, hipEvent_t* ev)
                    : side == 7 ? query(std::integral_constant<int, 7>{})
                                : query(std::integral_constant<int, 0>{});
     if (e != hipSuccess) return e;
+    if constexpr (std::is_same<T, uint16_t>::value) {
+        // key side on the matrix cores; a one-key window (b = 0) stays on the lane-group kernels, whose dp
+        // is the query kernel's own arithmetic, so that dS = p (dp - D) is exactly 0 there
+        if (p.b >= 1 && p.b <= kTileMaxB) {
+            BwdParams pt = p;
+            pt.tk = make_tiling(p.Hk, p.Wk, kTileKeys);
+            const uint64_t tblocks = tiling_blocks(pt.tk, p.keys_total / p.nkeys);
+            return multi ? launch(bwd_key_tile_kernel<D, true>, tblocks, st, k0, k1, pt)
+                         : launch(bwd_key_tile_kernel<D, false>, tblocks, st, k0, k1, pt);
+        }
+    }
     if ((e = launch(bwd_gather_kernel<T, D, G>, gblocks, st, k0, nullptr, p)) != hipSuccess) return e;
     e = multi ? launch(bwd_key_kernel<T, D, G, true>, kblocks, st, nullptr, nullptr, p)
               : launch(bwd_key_kernel<T, D, G, false>, kblocks, st, nullptr, nullptr, p);
@@ -790,6 +1138,7 @@ uint64_t attend_backward_max_blocks(int dtype, const Grid& g, int kappa)
         keep(tiling_blocks(make_tiling(g.Hq, g.Wq, kQpb), g.S));    // query kernel
         keep((uint64_t(kappa) * n + kQpb - 1) / kQpb);              // entry-order copies
         keep(tiling_blocks(make_tiling(g.Hk, g.Wk, kQpb), g.S));    // key kernel
+        keep(tiling_blocks(make_tiling(g.Hk, g.Wk, kTileKeys), g.S));  // key tiles on the matrix cores
         keep((keys + kScanTile - 1) / kScanTile);                   // scan tiles
         return most;
     });

@@ -107,9 +107,13 @@ def test_backward_full_window_is_dense(scram):
 
 @pytest.mark.parametrize("shape", [(1, 1, 1, 1, 1, 16, "f32"), (2, 3, 17, 5, 19, 128, "bf16"),
                                    (1, 21, 1, 30, 1, 64, "f32"), (3, 9, 7, 4, 6, 32, "bf16"),
-                                   (2, 7, 9, 6, 5, 128, "f32"), (1, 13, 11, 13, 11, 16, "bf16")],
+                                   (2, 7, 9, 6, 5, 128, "f32"), (1, 13, 11, 13, 11, 16, "bf16"),
+                                   (1, 21, 1, 90, 1, 64, "bf16"), (2, 5, 70, 3, 67, 64, "bf16"),
+                                   (1, 30, 30, 20, 24, 32, "bf16")],
                          ids=lambda s: "x".join(map(str, s[:-1])) + s[-1])
 def test_backward_shapes(scram, shape):
+    """Ragged grids, 1-D and short wide key grids (the bf16 key tiles become 64 x 1 or 4 x 16), every
+    width; windows up to 15 x 15 (the largest the bf16 key tiles take) and one beyond."""
     S, Hq, Wq, Hk, Wk, d, dtype = shape
     rng = np.random.default_rng(sum(shape[:-1]))
     Q = rng.standard_normal((S, Hq, Wq, d)).astype(np.float32)
@@ -118,7 +122,7 @@ def test_backward_shapes(scram, shape):
     if dtype == "bf16":
         Q, K, V, dO = (to_dev(x, "bf16").float().cpu().numpy() for x in (Q, K, V, dO))
     J = rng.integers(0, Hk * Wk, (2, S, Hq, Wq)).astype(np.int32)
-    for window in (1, 3, 5):
+    for window in (1, 3, 5, 15, 17) if dtype == "bf16" else (1, 3, 5):
         got = scram.sparse_attend_backward(*(to_dev(x, dtype) for x in (Q, K, V)), torch.from_numpy(J).cuda(),
                                            to_dev(dO, dtype), window, d ** -0.5)
         ref = oracle.sparse_attend_backward(Q, K, V, J, window, d ** -0.5, dO)
@@ -157,10 +161,12 @@ def test_backward_events(scram):
 
 
 @pytest.mark.parametrize("pattern", ["one_key", "two_keys_and_random", "one_key_kappa2_causal"])
-def test_backward_hot_keys(scram, pattern):
+@pytest.mark.parametrize("ci", [1, 3], ids=["f32", "bf16"])
+def test_backward_hot_keys(scram, pattern, ci):
     """Skewed inverse maps: every query on one key, or most on two keys -- one bucket holds thousands of
-    entries, so those keys take the block-per-key path."""
-    cfg = SMALL[1]
+    entries (fp32: those keys go to the teams of lane groups; bf16: their key tiles stage dozens of
+    chunks)."""
+    cfg = SMALL[ci]
     a = si.make_arrays(cfg)
     dev = {k: to_dev(a[k], cfg.dtype) for k in ("Q", "K", "V")}
     rng = np.random.default_rng(17)

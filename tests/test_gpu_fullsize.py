@@ -12,6 +12,7 @@ import numpy as np
 import pytest
 
 import oracle
+import oracle.dense as dense
 import scram_inputs as si
 from scram_inputs.synth import resized
 
@@ -59,9 +60,18 @@ def test_full_size_sampled(scram, ci):
                                query_ids=ids)
     got = out.float().cpu().numpy().reshape(n, cfg.dv)[ids].astype(np.float64)
     err = np.abs(got - ref).max(axis=1) / np.maximum(np.abs(ref).max(axis=1), 1e-6)
-    print(f"  sampled near ties {ties}, mismatches at them {mism}; attend max rel err {err.max():.3e}",
+    # quality, reported and not gated (the paper prints none): recall of the final map against the
+    # exact argmax and the mean ratio of their scores, on the sampled queries
+    Jb, sb = dense.brute_argmax_rows(Q64, K64, ids)
+    Jf = J.cpu().numpy().reshape(-1)[ids]
+    sT = np.einsum("md,md->m", Q64.reshape(n, cfg.d)[ids],
+                   K64.reshape(cfg.S, cfg.Hk * cfg.Wk, cfg.d)[ids // (cfg.Hq * cfg.Wq), Jf])
+    pos = sb > 0
+    print(f"  sampled near ties {ties}, mismatches at them {mism}; attend max rel err {err.max():.3e}; "
+          f"recall vs brute force {np.mean(Jf == Jb):.4f}, mean s_T/s* {np.mean(sT[pos] / sb[pos]):.4f}",
           flush=True)
     assert err.max() <= TOL[cfg.dtype]
+    assert (sT <= sb + 1e-9 * np.abs(sb)).all()  # no map beats the exact argmax
 
 
 def test_large_grid_sampled(scram):

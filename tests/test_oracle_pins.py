@@ -436,3 +436,20 @@ def test_brute_argmax_by_loops():
                 assert J[s, x, y] == sc.index(m)
                 assert best[s, x, y] == pytest.approx(m, rel=1e-14)
     assert J[1, 0, 0] == 2
+
+
+def test_brute_argmax_rows_by_loops():
+    """The sampled brute force scores each query against its own slice's keys only."""
+    rng = np.random.default_rng(1)
+    Q = rng.standard_normal((3, 4, 3, 6))
+    K = rng.standard_normal((3, 5, 2, 6))
+    K[2, 4, 1] = K[2, 0, 0]
+    Q[2, 1, 1] = 3 * K[2, 0, 0]     # query 28: equal maxima at flat keys 0 and 9, the lower one wins
+    ids = np.array([23, 0, 35, 16, 11, 12])
+    J, best = dense.brute_argmax_rows(Q, K, ids)
+    for m, g in enumerate(ids):
+        s, x, y = g // 12, (g % 12) // 3, g % 3
+        sc = [float(Q[s, x, y] @ K[s, r, c]) for r in range(5) for c in range(2)]
+        assert J[m] == sc.index(max(sc))
+        assert best[m] == pytest.approx(max(sc), rel=1e-14)
+    assert dense.brute_argmax_rows(Q, K, [28])[0][0] == 0
