@@ -661,8 +661,8 @@ __global__ __launch_bounds__(kBlock) void bwd_heavy_kernel(BwdParams p)
 // second (lane l holds key l mod 16 and four entries), so P and dS never
 // leave registers; the entries' order along the contraction only has to be
 // the same in both operands.  P and dS enter the matrix cores as three bf16
-// parts each (hi + mid + lo: 24 significant bits of the fp32 value, the
-// products exact), so the gradients carry fp32 precision; all sums are fp32.
+// parts each that add up to the fp32 value exactly (the products of bf16
+// parts are exact), so the gradients carry fp32 precision; all sums are fp32.
 // ---------------------------------------------------------------------------
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
@@ -688,14 +688,22 @@ struct KeyTile {
     static_assert(kUpt >= 1 && kUpt * kBlock == kPairs * 2 * kPieces && kBlock % kPairs == 0, "whole units");
 };
 
-// x = hi + mid + lo + O(2^-27 |x|), each part bf16 (round to nearest even;
-// x - hi and (x - hi) - mid are exact in fp32)
-__device__ __forceinline__ void split3(float x, __bf16& hi, __bf16& mid, __bf16& lo)
+// x = hi + mid + lo exactly, each part a bf16 value held as an fp32 bit
+// pattern with a zero low half: hi keeps the top 8 significant bits of x
+// (truncation), x - hi is exact in fp32 and mid keeps its top 8, and the
+// remaining lo has at most 8 significant bits (x has 24).
+__device__ __forceinline__ void split3(float x, uint32_t& hi, uint32_t& mid, uint32_t& lo)
 {
-    hi = static_cast<__bf16>(x);
-    const float r1 = x - static_cast<float>(hi);
-    mid = static_cast<__bf16>(r1);
-    lo = static_cast<__bf16>(r1 - static_cast<float>(mid));
+    hi = __float_as_uint(x) & 0xFFFF0000u;
+    const float r1 = x - __uint_as_float(hi);
+    mid = __float_as_uint(r1) & 0xFFFF0000u;
+    lo = __float_as_uint(r1 - __uint_as_float(mid));
+}
+
+// bf16 pair (a in the low half, b in the high half) from two such patterns
+__device__ __forceinline__ uint32_t pack_hi16(uint32_t a, uint32_t b)
+{
+    return __builtin_amdgcn_perm(b, a, 0x07060302u);
 }
 
 template <int D, bool MULTI>
@@ -773,6 +781,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(KeyTile<
         vf[ds] = __builtin_bit_cast(bf16x8_t, vw);
     }
     const uint32_t key_local = static_cast<uint32_t>(kx) * p.Wk + ky;  // raster index (causal test)
+    // rows of the wave's keys (items 16 wave .. 16 wave + 15 of the tile, raster order)
+    const int wrow_lo = x0 + ((16 * wave) >> p.tk.lw), wrow_hi = x0 + ((16 * wave + 15) >> p.tk.lw);
 
     f32x4_t dk[KT::kOt], dv[KT::kOt];
 #pragma unroll
@@ -890,6 +900,14 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(KeyTile<
 
 #pragma unroll 1
         for (int ks = 0; ks < kCE / 32; ++ks) {
+            // Entries are staged in halo-row order: the first and last valid entry of the step bound its
+            // match rows.  A step whose rows all lie more than b from the wave's key rows has no pair in
+            // any window, and the wave skips it (slots past the end carry row -2^30).
+            {
+                const int c_first = s_meta[ks * 32].x, c_last = s_meta[ks * 32 + 31].x;
+                const int row_lo = c_first, row_hi = c_last < 0 ? (1 << 30) : c_last;
+                if (c_first < 0 || row_hi < wrow_lo - p.b || row_lo > wrow_hi + p.b) continue;
+            }
             // S^T, dP^T for entries ks*32 + 16 et + (0..15) against the wave's 16 keys
             f32x4_t sc[2], dp[2];
 #pragma unroll
@@ -912,7 +930,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(KeyTile<
             }
             // P and dS of (key m, entry ks*32 + 16 et + 4 g4 + r), split for the matrix cores; operand
             // slot 4 et + r of this lane
-            bf16x8_t ph, pm, pl, sh, sm, sl;
+            uint32_t ph[8], pm[8], pl[8], sh[8], sm[8], sl[8];
 #pragma unroll
             for (int et = 0; et < 2; ++et) {
 #pragma unroll
@@ -933,17 +951,16 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(KeyTile<
                     const float pr =
                         ok ? __builtin_amdgcn_exp2f(sc[et][r] * p.scale_log2e - __int_as_float(mt.z)) : 0.f;
                     const float dsr = pr * (dp[et][r] - __int_as_float(mt.w));
-                    __bf16 a0, a1, a2;
-                    split3(pr, a0, a1, a2);
-                    ph[4 * et + r] = a0;
-                    pm[4 * et + r] = a1;
-                    pl[4 * et + r] = a2;
-                    split3(dsr, a0, a1, a2);
-                    sh[4 * et + r] = a0;
-                    sm[4 * et + r] = a1;
-                    sl[4 * et + r] = a2;
+                    split3(pr, ph[4 * et + r], pm[4 * et + r], pl[4 * et + r]);
+                    split3(dsr, sh[4 * et + r], sm[4 * et + r], sl[4 * et + r]);
                 }
             }
+            auto operand = [](const uint32_t (&v)[8]) {
+                return __builtin_bit_cast(bf16x8_t, make_uint4(pack_hi16(v[0], v[1]), pack_hi16(v[2], v[3]),
+                                                               pack_hi16(v[4], v[5]), pack_hi16(v[6], v[7])));
+            };
+            const bf16x8_t aph = operand(ph), apm = operand(pm), apl = operand(pl);
+            const bf16x8_t ash = operand(sh), asm_ = operand(sm), asl = operand(sl);
             // dV_w += P dO_E, dK_w += dS Q_E: operand slot kk of this lane is entry
             // ks*32 + (kk < 4 ? 4 g4 + kk : 16 + 4 g4 + kk - 4), channel 16 o + m
 #pragma unroll
@@ -956,12 +973,12 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(KeyTile<
                 const uint2 q_hi = *reinterpret_cast<const uint2*>(s_tr[0] + ch * KT::kTrB + (e0 + 16) * 2);
                 const bf16x8_t bg = __builtin_bit_cast(bf16x8_t, make_uint4(g_lo.x, g_lo.y, g_hi.x, g_hi.y));
                 const bf16x8_t bq = __builtin_bit_cast(bf16x8_t, make_uint4(q_lo.x, q_lo.y, q_hi.x, q_hi.y));
-                dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, bg, dv[o], 0, 0, 0);
-                dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pm, bg, dv[o], 0, 0, 0);
-                dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, bg, dv[o], 0, 0, 0);
-                dk[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sh, bq, dk[o], 0, 0, 0);
-                dk[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sm, bq, dk[o], 0, 0, 0);
-                dk[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sl, bq, dk[o], 0, 0, 0);
+                dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aph, bg, dv[o], 0, 0, 0);
+                dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(apm, bg, dv[o], 0, 0, 0);
+                dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(apl, bg, dv[o], 0, 0, 0);
+                dk[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ash, bq, dk[o], 0, 0, 0);
+                dk[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(asm_, bq, dk[o], 0, 0, 0);
+                dk[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(asl, bq, dk[o], 0, 0, 0);
             }
         }
     }
