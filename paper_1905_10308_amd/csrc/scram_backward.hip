@@ -645,48 +645,44 @@ __global__ __launch_bounds__(kBlock) void bwd_heavy_kernel(BwdParams p)
 }
 
 // ---------------------------------------------------------------------------
-// Key side on the matrix cores (bf16 storage).  A block takes a tile of 64
-// keys; the queries whose key sets reach into the tile are exactly the
-// entries whose match lies in the tile's halo (the tile widened by b), one
-// contiguous entry range per halo row.  Between the tile's keys and those
-// entries the pairs form a dense 64 x E block, of which the window test keeps
-// the pairs with |match - key|_inf <= b.  Per chunk of kCE entries staged in
-// LDS (q and dO rows, row-major and transposed, plus match, log2 normaliser
-// and D of each entry), each wave, owning 16 keys, computes on the matrix cores
-//   S^T = Q_E K_w^T,  dP^T = dO_E V_w^T                 (entries x keys)
-// then in registers P = window test ? 2^(S scale log2 e - lse2) : 0 and
+// Key side on the matrix cores (bf16 storage).  Each wave takes a strip of 16
+// keys (items 16 w .. 16 w + 15, raster order, of the block's 64-key tile: 2
+// rows of 8 on square grids) and works alone: no block barriers.  The
+// queries whose key sets reach the strip are exactly the entries whose match
+// lies in the strip's halo (the strip widened by b), one contiguous entry
+// range per halo row.  Per chunk of 32 of those entries, staged in the wave's
+// own LDS (q and dO rows, match, log2 normaliser, D), on the matrix cores
+//   S^T = Q_E K_w^T,  dP^T = dO_E V_w^T                 (entries x keys),
+// in registers P = window test ? 2^(S scale log2 e - lse2) : 0 and
 // dS = P (dP - D), and again on the matrix cores
 //   dV_w += P dO_E,   dK_w += dS Q_E                    (keys x channels).
-// The output layout of the first products is the operand layout of the
-// second (lane l holds key l mod 16 and four entries), so P and dS never
-// leave registers; the entries' order along the contraction only has to be
-// the same in both operands.  P and dS enter the matrix cores as three bf16
-// parts each that add up to the fp32 value exactly (the products of bf16
-// parts are exact), so the gradients carry fp32 precision; all sums are fp32.
+// The output layout of the first products (lane l: key l mod 16 and four
+// entries) is the operand layout of the second, so P and dS never leave
+// registers (the entries' order along the contraction only has to agree
+// between the two operands).  The channel-major operands dO_E, Q_E of the
+// second products are the row-major fragments the first products read,
+// multiplied by identity blocks on the matrix cores (exact for bf16 values).
+// P and dS enter as three bf16 parts that add up to the fp32 values exactly
+// (products of bf16 parts are exact); all sums are fp32.
 // ---------------------------------------------------------------------------
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kTileKeys = 64;                             // keys per block, 16 per wave
-constexpr int kTileMaxB = 7;                              // windows up to 15 x 15
-constexpr int kTileMaxRows = kTileKeys + 2 * kTileMaxB;   // halo rows of the tallest tile
+constexpr int kTileKeys = 64;                          // keys per block, 16 per wave
+constexpr int kTileMaxB = 7;                           // windows up to 15 x 15
+constexpr int kStripMaxRows = 16 + 2 * kTileMaxB;      // halo rows of the tallest strip (16 x 1)
+constexpr int kStripCE = 32;                           // entries per chunk: one contraction step
 
 template <int D>
-struct KeyTile {
-    static constexpr int kCE = D == 16 ? 128 : (D == 128 ? 32 : 64);  // entries per staged chunk
-    static constexpr int kRowB = 2 * D + 16;           // row-major row stride in bytes (padded)
-    static constexpr int kTrB = 2 * kCE + 8;           // transposed row stride in bytes (padded)
+struct KeyStrip {
+    static constexpr int kRowB = 2 * D + 16;           // row stride in LDS, bytes (padded)
     static constexpr int kDs = D >= 32 ? D / 32 : 1;   // 32-channel steps of the first products
     static constexpr int kOt = D / 16;                 // 16-channel tiles of dK_w, dV_w
     static constexpr int kPieces = D / 8;              // 16-byte pieces per row
-    static constexpr int kWaves = D > 64 ? 2 : 3;      // waves per SIMD the registers are sized for
-    // staging: a unit is one 16-byte piece of the q or dO row of a pair of
-    // entry slots; thread t takes units t, t + kBlock, ... -- always the same
-    // slot pair, kUpt pieces
-    static constexpr int kPairs = kCE / 2;
-    static constexpr int kUpt = kPairs * 2 * kPieces / kBlock;
-    static_assert(kUpt >= 1 && kUpt * kBlock == kPairs * 2 * kPieces && kBlock % kPairs == 0, "whole units");
 };
+
+// waves per SIMD the strip kernel's registers are sized for
+constexpr int strip_waves(int D, bool multi) { return D > 64 || (D == 64 && multi) ? 2 : 3; }
 
 // x = hi + mid + lo exactly, each part a bf16 value held as an fp32 bit
 // pattern with a zero low half: hi keeps the top 8 significant bits of x
@@ -700,77 +696,90 @@ __device__ __forceinline__ void split3(float x, uint32_t& hi, uint32_t& mid, uin
     lo = __float_as_uint(r1 - __uint_as_float(mid));
 }
 
-// bf16 pair (a in the low half, b in the high half) from two such patterns
+// bf16 pair (a in the low half, b in the high half) from the high halves of two fp32 patterns
 __device__ __forceinline__ uint32_t pack_hi16(uint32_t a, uint32_t b)
 {
     return __builtin_amdgcn_perm(b, a, 0x07060302u);
 }
 
-template <int D, bool MULTI>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(KeyTile<D>::kWaves))) void bwd_key_tile_kernel(BwdParams p)
+// LDS written by some lanes of a wave and then read by others: keep the
+// compiler from moving accesses across this point (a wave's LDS instructions
+// execute in order)
+__device__ __forceinline__ void wave_lds_sync()
 {
-    using KT = KeyTile<D>;
-    constexpr int kCE = KT::kCE;
-    __shared__ __align__(16) unsigned char s_row[2][kCE * KT::kRowB];  // q, dO rows of the chunk's entries
-    __shared__ __align__(16) unsigned char s_tr[2][D * KT::kTrB];      // the same, channel-major
-    __shared__ int4 s_meta[kCE];        // match row, match column, lse2 bits, D bits
-    __shared__ int32_t s_el[MULTI ? kCE : 1][2];                 // window index e, query's raster index
-    __shared__ int32_t s_prevc[MULTI ? kCE : 1][kMaxKappa - 1];  // centres of windows 0..e-1
-    __shared__ int32_t s_lo[kTileMaxRows], s_pre[kTileMaxRows + 1];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ bf16x8_t lds_frag(const unsigned char* p)
+{
+    return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(p));
+}
+
+template <int D, bool MULTI>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(strip_waves(D, MULTI)))) void
+bwd_key_strip_kernel(BwdParams p)
+{
+    using KS = KeyStrip<D>;
+    constexpr int kCE = kStripCE;
+    constexpr int kW = kBlock / 64;
+    __shared__ __align__(16) unsigned char s_row[kW][2][kCE * KS::kRowB];  // q, dO rows of the chunk
+    __shared__ int4 s_meta[kW][kCE];        // match row, match column, lse2 bits, D bits
+    __shared__ int32_t s_el[kW][MULTI ? kCE : 1][2];                 // window index e, query's raster index
+    __shared__ int32_t s_prevc[kW][MULTI ? kCE : 1][kMaxKappa - 1];  // centres of windows 0..e-1
+    __shared__ int32_t s_lo[kW][kStripMaxRows], s_pre[kW][kStripMaxRows + 1];
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int m = lane & 15, g4 = lane >> 4;
     const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
 
-    // the tile: rows x0.., columns y0.. of slice s (th x tw keys, clipped to the grid)
+    // the block's tile (th x tw keys at x0, y0 of slice s) and this wave's strip in it
     uint32_t s, k, tr, tc;
     divmod(blk, p.tk.div_slice, s, k);
     divmod(k, p.tk.div_w, tr, tc);
     const int tw = 1 << p.tk.lw, th = kTileKeys >> p.tk.lw;
     const int x0 = static_cast<int>(tr) * th, y0 = static_cast<int>(tc) * tw;
-    const int hr0 = max(x0 - p.b, 0), hr1 = min(x0 + th - 1 + p.b, p.Hk - 1);
-    const int hc0 = max(y0 - p.b, 0), hc1 = min(y0 + tw - 1 + p.b, p.Wk - 1);
-    const int nrows = hr1 - hr0 + 1;
+    const int it0 = 16 * wave;
+    const int sr0 = x0 + (it0 >> p.tk.lw), sr1 = x0 + ((it0 + 15) >> p.tk.lw);
+    const int sc0 = y0 + (it0 & (tw - 1)), sc1 = sc0 + min(tw, 16) - 1;
+    if (sr0 >= p.Hk || sc0 >= p.Wk) return;  // the strip lies past the grid's edge
+    const int hr0 = max(sr0 - p.b, 0), hr1 = min(sr1 + p.b, p.Hk - 1);
+    const int hc0 = max(sc0 - p.b, 0), hc1 = min(sc1 + p.b, p.Wk - 1);
+    const int nrows = hr1 - hr0 + 1;  // at most kStripMaxRows
     const int32_t* off = p.offsets + static_cast<size_t>(s) * p.nkeys;
-    if (wave == 0) {
-        // entry counts of halo rows lane and lane + 64, then an inclusive scan across the wave
-        static_assert(kTileMaxRows <= 128, "two halo rows per lane");
-        int cnt[2];
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const int i = lane + 64 * h;
-            cnt[h] = 0;
-            if (i < nrows) {
-                const int r = hr0 + i;
-                const int32_t lo = off[r * p.Wk + hc0];
-                s_lo[i] = lo;
-                cnt[h] = off[r * p.Wk + hc1 + 1] - lo;
-            }
+    int32_t* const lo_w = s_lo[wave];
+    int32_t* const pre_w = s_pre[wave];
+    int E;
+    {
+        // entry count of halo row `lane`, then an inclusive scan across the wave
+        int cnt = 0;
+        if (lane < nrows) {
+            const int r = hr0 + lane;
+            const int32_t lo = off[r * p.Wk + hc0];
+            lo_w[lane] = lo;
+            cnt = off[r * p.Wk + hc1 + 1] - lo;
         }
-        int carry = 0;
+        int incl = cnt;
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            int incl = cnt[h];
-#pragma unroll
-            for (int k2 = 1; k2 < 64; k2 <<= 1) {
-                const int y = __shfl_up(incl, k2, 64);
-                if (lane >= k2) incl += y;
-            }
-            if (lane + 64 * h < nrows) s_pre[lane + 64 * h + 1] = carry + incl;
-            carry += __shfl(incl, 63, 64);
+        for (int k2 = 1; k2 < 64; k2 <<= 1) {
+            const int y = __shfl_up(incl, k2, 64);
+            if (lane >= k2) incl += y;
         }
-        if (lane == 0) s_pre[0] = 0;
+        if (lane < nrows) pre_w[lane + 1] = incl;
+        if (lane == 0) pre_w[0] = 0;
+        E = __shfl(incl, nrows - 1, 64);
     }
+    wave_lds_sync();
 
-    // this lane's key (column of the first products): item 16 wave + m of the tile
-    const int item = 16 * wave + m;
-    const int kx = x0 + (item >> p.tk.lw), ky = y0 + (item & (tw - 1));
+    // this lane's key (column of the first products): item it0 + m of the tile
+    const int kx = x0 + ((it0 + m) >> p.tk.lw), ky = y0 + ((it0 + m) & (tw - 1));
     const bool key_ok = kx < p.Hk && ky < p.Wk;
     const size_t kslice = static_cast<size_t>(s) * p.nkeys;
-    const size_t krow = kslice + (key_ok ? static_cast<size_t>(kx) * p.Wk + ky : static_cast<size_t>(x0) * p.Wk + y0);
-    bf16x8_t kf[KT::kDs], vf[KT::kDs];
+    const size_t krow = kslice + (key_ok ? static_cast<size_t>(kx) * p.Wk + ky : static_cast<size_t>(sr0) * p.Wk + sc0);
+    bf16x8_t kf[KS::kDs], vf[KS::kDs];
 #pragma unroll
-    for (int ds = 0; ds < KT::kDs; ++ds) {
+    for (int ds = 0; ds < KS::kDs; ++ds) {
         const int d = 32 * ds + 8 * g4;
         uint4 kw = make_uint4(0u, 0u, 0u, 0u), vw = kw;
         if (d < D) {
@@ -781,217 +790,169 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(KeyTile<
         vf[ds] = __builtin_bit_cast(bf16x8_t, vw);
     }
     const uint32_t key_local = static_cast<uint32_t>(kx) * p.Wk + ky;  // raster index (causal test)
-    // rows of the wave's keys (items 16 wave .. 16 wave + 15 of the tile, raster order)
-    const int wrow_lo = x0 + ((16 * wave) >> p.tk.lw), wrow_hi = x0 + ((16 * wave + 15) >> p.tk.lw);
-
-    f32x4_t dk[KT::kOt], dv[KT::kOt];
+    // identity blocks: I_h[k][n] = (k == 16 h + n), lane (n, g4) holding k = 8 g4 .. 8 g4 + 7
+    bf16x8_t eye[2];
 #pragma unroll
-    for (int o = 0; o < KT::kOt; ++o) dk[o] = dv[o] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-    __syncthreads();
-    const int E = s_pre[nrows];
-    const uint16_t* Qb = static_cast<const uint16_t*>(p.Q);
-    const uint16_t* Gb = static_cast<const uint16_t*>(p.dO);
-    // Staging is software-pipelined: while a chunk is multiplied, the next
-    // chunk's rows and statistics are in flight into registers and the entry
-    // codes of the one after it into registers as well.
-    const int pair = static_cast<int>(threadIdx.x) % KT::kPairs;
-    const int piece0 = static_cast<int>(threadIdx.x) / KT::kPairs;  // first piece; then + kBlock / kPairs
-    // the statistics of the pairs are loaded by a quarter of the pairs' threads in each wave, so that no
-    // wave waits on more of them than the others
-    // (the threads of pair P are P + kPairs k, k = 0 .. kBlock / kPairs - 1; quarter q of the pairs takes
-    // the k whose thread lies in wave q)
-    static_assert(64 % KT::kPairs == 0 && KT::kPairs % 4 == 0, "every wave holds every pair");
-    const bool meta_thread = piece0 == (pair / (KT::kPairs / 4)) * (64 / KT::kPairs);
-    // entry code of slot 2 pair + h of the chunk starting at c0, -1 past the end
-    auto slot_code = [&](int c0, int h) {
-        const int v = c0 + 2 * pair + h;
-        if (v >= E) return -1;
-        int lo = 0, hi = nrows - 1;  // halo row holding flat position v: the last with s_pre <= v
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (s_pre[mid] <= v) lo = mid; else hi = mid - 1;
-        }
-        return static_cast<int>(p.entries[s_lo[lo] + (v - s_pre[lo])]);
-    };
-    struct Staged {
-        uint4 row[KT::kUpt][2];  // [unit][slot of the pair]
-        int32_t match[2];
-        float lse2[2], dq[2];
-    };
-    auto fetch = [&](const int (&code)[2], Staged& st) {
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            uint32_t e = 0, g = 0;
-            if (code[h] >= 0) divmod(static_cast<uint32_t>(code[h]), p.div_n, e, g);
-#pragma unroll
-            for (int i = 0; i < KT::kUpt; ++i) {
-                const int w = piece0 + i * (kBlock / KT::kPairs);
-                const int which = w / KT::kPieces, piece = w % KT::kPieces;
-                st.row[i][h] = code[h] >= 0
-                                   ? reinterpret_cast<const uint4*>((which ? Gb : Qb) + static_cast<size_t>(g) * D)[piece]
-                                   : make_uint4(0u, 0u, 0u, 0u);  // zeros past the end: finite operands
-            }
-            st.match[h] = -1;
-            st.lse2[h] = st.dq[h] = 0.f;
-            if (meta_thread && code[h] >= 0) {
-                st.match[h] = p.J[code[h]];  // clamped when stored: no wait here
-                st.lse2[h] = p.lse2[g];
-                st.dq[h] = p.Dq[g];
-            }
-        }
-    };
-    auto store = [&](const int (&code)[2], const Staged& st) {
-#pragma unroll
-        for (int i = 0; i < KT::kUpt; ++i) {
-            const int w = piece0 + i * (kBlock / KT::kPairs);
-            const int which = w / KT::kPieces, piece = w % KT::kPieces;
-#pragma unroll
-            for (int h = 0; h < 2; ++h)
-                *reinterpret_cast<uint4*>(s_row[which] + (2 * pair + h) * KT::kRowB + piece * 16) = st.row[i][h];
-            const uint32_t a[4] = {st.row[i][0].x, st.row[i][0].y, st.row[i][0].z, st.row[i][0].w};
-            const uint32_t b2[4] = {st.row[i][1].x, st.row[i][1].y, st.row[i][1].z, st.row[i][1].w};
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {  // channels 2j, 2j+1 of the piece: (slot 2 pair, slot 2 pair + 1) words
-                *reinterpret_cast<uint32_t*>(s_tr[which] + (piece * 8 + 2 * j) * KT::kTrB + pair * 4) =
-                    (a[j] & 0xFFFFu) | (b2[j] << 16);
-                *reinterpret_cast<uint32_t*>(s_tr[which] + (piece * 8 + 2 * j + 1) * KT::kTrB + pair * 4) =
-                    (a[j] >> 16) | (b2[j] & 0xFFFF0000u);
-            }
-        }
-        if (meta_thread) {
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int t = 2 * pair + h;
-                int4 meta = make_int4(-(1 << 30), -(1 << 30), 0, 0);  // no key is near this match
-                if constexpr (MULTI) s_el[t][0] = s_el[t][1] = 0;
-                if (code[h] >= 0) {
-                    uint32_t mu, mv;
-                    divmod(static_cast<uint32_t>(clamp_index(st.match[h], p.nkeys)), p.div_wk, mu, mv);
-                    meta = make_int4(static_cast<int>(mu), static_cast<int>(mv), __float_as_int(st.lse2[h]),
-                                     __float_as_int(st.dq[h]));
-                    if constexpr (MULTI) {
-                        uint32_t e, g, sl, local;
-                        divmod(static_cast<uint32_t>(code[h]), p.div_n, e, g);
-                        divmod(g, p.div_plane, sl, local);
-                        s_el[t][0] = static_cast<int32_t>(e);
-                        s_el[t][1] = static_cast<int32_t>(local);
-                        for (int f = 0; f < static_cast<int>(e); ++f)
-                            s_prevc[t][f] = clamp_index(p.J[static_cast<size_t>(f) * p.n + g], p.nkeys);
-                    }
-                }
-                s_meta[t] = meta;
-            }
-        }
-    };
-    int code[2] = {slot_code(0, 0), slot_code(0, 1)};
-    Staged stg;
-    fetch(code, stg);
-    int code_next[2] = {slot_code(kCE, 0), slot_code(kCE, 1)};
-    for (int c0 = 0; c0 < E; c0 += kCE) {
-        __syncthreads();  // the previous chunk is consumed
-        store(code, stg);
-        __syncthreads();
-        code[0] = code_next[0];
-        code[1] = code_next[1];
-        if (c0 + kCE < E) fetch(code, stg);  // the next chunk, in flight during the products
-        code_next[0] = slot_code(c0 + 2 * kCE, 0);
-        code_next[1] = slot_code(c0 + 2 * kCE, 1);
-
-#pragma unroll 1
-        for (int ks = 0; ks < kCE / 32; ++ks) {
-            // Entries are staged in halo-row order: the first and last valid entry of the step bound its
-            // match rows.  A step whose rows all lie more than b from the wave's key rows has no pair in
-            // any window, and the wave skips it (slots past the end carry row -2^30).
-            {
-                const int c_first = s_meta[ks * 32].x, c_last = s_meta[ks * 32 + 31].x;
-                const int row_lo = c_first, row_hi = c_last < 0 ? (1 << 30) : c_last;
-                if (c_first < 0 || row_hi < wrow_lo - p.b || row_lo > wrow_hi + p.b) continue;
-            }
-            // S^T, dP^T for entries ks*32 + 16 et + (0..15) against the wave's 16 keys
-            f32x4_t sc[2], dp[2];
-#pragma unroll
-            for (int et = 0; et < 2; ++et) {
-                sc[et] = dp[et] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-                const int er = ks * 32 + et * 16 + m;
-#pragma unroll
-                for (int ds = 0; ds < KT::kDs; ++ds) {
-                    const int d = 32 * ds + 8 * g4;
-                    uint4 aq = make_uint4(0u, 0u, 0u, 0u), ag = aq;
-                    if (d < D) {
-                        aq = *reinterpret_cast<const uint4*>(s_row[0] + er * KT::kRowB + d * 2);
-                        ag = *reinterpret_cast<const uint4*>(s_row[1] + er * KT::kRowB + d * 2);
-                    }
-                    sc[et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, aq), kf[ds], sc[et],
-                                                                     0, 0, 0);
-                    dp[et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ag), vf[ds], dp[et],
-                                                                     0, 0, 0);
-                }
-            }
-            // P and dS of (key m, entry ks*32 + 16 et + 4 g4 + r), split for the matrix cores; operand
-            // slot 4 et + r of this lane
-            uint32_t ph[8], pm[8], pl[8], sh[8], sm[8], sl[8];
-#pragma unroll
-            for (int et = 0; et < 2; ++et) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int te = ks * 32 + et * 16 + 4 * g4 + r;
-                    const int4 mt = s_meta[te];
-                    bool ok = key_ok && abs(mt.x - kx) <= p.b && abs(mt.y - ky) <= p.b;
-                    if constexpr (MULTI) {
-                        const int e = s_el[te][0];
-                        for (int f = 0; f < e && ok; ++f) {
-                            uint32_t fu, fv;
-                            divmod(static_cast<uint32_t>(s_prevc[te][f]), p.div_wk, fu, fv);
-                            if (abs(static_cast<int>(fu) - kx) <= p.b && abs(static_cast<int>(fv) - ky) <= p.b)
-                                ok = false;  // an earlier window of the query holds this key
-                        }
-                        if (p.causal) ok = ok && key_local <= static_cast<uint32_t>(s_el[te][1]);
-                    }
-                    const float pr =
-                        ok ? __builtin_amdgcn_exp2f(sc[et][r] * p.scale_log2e - __int_as_float(mt.z)) : 0.f;
-                    const float dsr = pr * (dp[et][r] - __int_as_float(mt.w));
-                    split3(pr, ph[4 * et + r], pm[4 * et + r], pl[4 * et + r]);
-                    split3(dsr, sh[4 * et + r], sm[4 * et + r], sl[4 * et + r]);
-                }
-            }
-            auto operand = [](const uint32_t (&v)[8]) {
-                return __builtin_bit_cast(bf16x8_t, make_uint4(pack_hi16(v[0], v[1]), pack_hi16(v[2], v[3]),
-                                                               pack_hi16(v[4], v[5]), pack_hi16(v[6], v[7])));
-            };
-            const bf16x8_t aph = operand(ph), apm = operand(pm), apl = operand(pl);
-            const bf16x8_t ash = operand(sh), asm_ = operand(sm), asl = operand(sl);
-            // dV_w += P dO_E, dK_w += dS Q_E: operand slot kk of this lane is entry
-            // ks*32 + (kk < 4 ? 4 g4 + kk : 16 + 4 g4 + kk - 4), channel 16 o + m
-#pragma unroll
-            for (int o = 0; o < KT::kOt; ++o) {
-                const int ch = 16 * o + m;
-                const int e0 = ks * 32 + 4 * g4;
-                const uint2 g_lo = *reinterpret_cast<const uint2*>(s_tr[1] + ch * KT::kTrB + e0 * 2);
-                const uint2 g_hi = *reinterpret_cast<const uint2*>(s_tr[1] + ch * KT::kTrB + (e0 + 16) * 2);
-                const uint2 q_lo = *reinterpret_cast<const uint2*>(s_tr[0] + ch * KT::kTrB + e0 * 2);
-                const uint2 q_hi = *reinterpret_cast<const uint2*>(s_tr[0] + ch * KT::kTrB + (e0 + 16) * 2);
-                const bf16x8_t bg = __builtin_bit_cast(bf16x8_t, make_uint4(g_lo.x, g_lo.y, g_hi.x, g_hi.y));
-                const bf16x8_t bq = __builtin_bit_cast(bf16x8_t, make_uint4(q_lo.x, q_lo.y, q_hi.x, q_hi.y));
-                dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aph, bg, dv[o], 0, 0, 0);
-                dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(apm, bg, dv[o], 0, 0, 0);
-                dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(apl, bg, dv[o], 0, 0, 0);
-                dk[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ash, bq, dk[o], 0, 0, 0);
-                dk[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(asm_, bq, dk[o], 0, 0, 0);
-                dk[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(asl, bq, dk[o], 0, 0, 0);
-            }
-        }
+    for (int kk = 0; kk < 8; ++kk) {
+        eye[0][kk] = static_cast<__bf16>(8 * g4 + kk == m ? 1.f : 0.f);
+        eye[1][kk] = static_cast<__bf16>(8 * g4 + kk == 16 + m ? 1.f : 0.f);
     }
 
-    // lane holds keys 4 g4 + r of the wave, channel 16 o + m
+    f32x4_t dk[KS::kOt], dv[KS::kOt];
+#pragma unroll
+    for (int o = 0; o < KS::kOt; ++o) dk[o] = dv[o] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    // staging: lane pair (2 t, 2 t + 1) brings entry slot t's q and dO rows; the even lane also its statistics
+    const int t = lane >> 1, hf = lane & 1;
+    const uint16_t* const Qb = static_cast<const uint16_t*>(p.Q);
+    const uint16_t* const Gb = static_cast<const uint16_t*>(p.dO);
+    auto slot_code = [&](int c0) {
+        const int v = c0 + t;
+        if (v >= E) return -1;
+        int lo = 0, hi = nrows - 1;  // halo row holding flat position v: the last with pre <= v
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (pre_w[mid] <= v) lo = mid; else hi = mid - 1;
+        }
+        return static_cast<int>(p.entries[lo_w[lo] + (v - pre_w[lo])]);
+    };
+    unsigned char* const rows_q = s_row[wave][0];
+    unsigned char* const rows_g = s_row[wave][1];
+    int code = slot_code(0);
+    for (int c0 = 0; c0 < E; c0 += kCE) {
+        {
+            uint32_t qe = 0, qg = 0;
+            if (code >= 0) divmod(static_cast<uint32_t>(code), p.div_n, qe, qg);
+            int32_t match = -1;
+            float lse = 0.f, dq = 0.f;
+            if (hf == 0 && code >= 0) {
+                match = p.J[code];
+                lse = p.lse2[qg];
+                dq = p.Dq[qg];
+            }
+            const uint4* src = reinterpret_cast<const uint4*>((hf ? Gb : Qb) + static_cast<size_t>(qg) * D);
+            unsigned char* dst = s_row[wave][hf] + t * KS::kRowB;
+#pragma unroll
+            for (int i0 = 0; i0 < KS::kPieces; i0 += 8) {
+                uint4 val[8];
+#pragma unroll
+                for (int i = 0; i < 8; ++i)
+                    if (i0 + i < KS::kPieces)
+                        val[i] = code >= 0 ? src[i0 + i] : make_uint4(0u, 0u, 0u, 0u);  // zeros: finite operands
+#pragma unroll
+                for (int i = 0; i < 8; ++i)
+                    if (i0 + i < KS::kPieces) *reinterpret_cast<uint4*>(dst + (i0 + i) * 16) = val[i];
+            }
+            if (hf == 0) {
+                int4 meta = make_int4(-(1 << 30), -(1 << 30), 0, 0);  // no key is near this match
+                if constexpr (MULTI) s_el[wave][t][0] = s_el[wave][t][1] = 0;
+                if (code >= 0) {
+                    uint32_t mu, mv;
+                    divmod(static_cast<uint32_t>(clamp_index(match, p.nkeys)), p.div_wk, mu, mv);
+                    meta = make_int4(static_cast<int>(mu), static_cast<int>(mv), __float_as_int(lse),
+                                     __float_as_int(dq));
+                    if constexpr (MULTI) {
+                        uint32_t sl, local;
+                        divmod(qg, p.div_plane, sl, local);
+                        s_el[wave][t][0] = static_cast<int32_t>(qe);
+                        s_el[wave][t][1] = static_cast<int32_t>(local);
+                        for (int f = 0; f < static_cast<int>(qe); ++f)
+                            s_prevc[wave][t][f] = clamp_index(p.J[static_cast<size_t>(f) * p.n + qg], p.nkeys);
+                    }
+                }
+                s_meta[wave][t] = meta;
+            }
+        }
+        code = slot_code(c0 + kCE);  // the next chunk's entries load during the products
+        wave_lds_sync();
+
+        // S^T, dP^T for entries 16 et + (0..15) of the chunk against the strip's 16 keys
+        bf16x8_t aq[2][KS::kDs], ag[2][KS::kDs];
+        f32x4_t sc[2], dp[2];
+#pragma unroll
+        for (int et = 0; et < 2; ++et) {
+            sc[et] = dp[et] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            const int er = et * 16 + m;
+#pragma unroll
+            for (int ds = 0; ds < KS::kDs; ++ds) {
+                const int d = 32 * ds + 8 * g4;
+                aq[et][ds] = ag[et][ds] = __builtin_bit_cast(bf16x8_t, make_uint4(0u, 0u, 0u, 0u));
+                if (d < D) {
+                    aq[et][ds] = lds_frag(rows_q + er * KS::kRowB + d * 2);
+                    ag[et][ds] = lds_frag(rows_g + er * KS::kRowB + d * 2);
+                }
+                sc[et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq[et][ds], kf[ds], sc[et], 0, 0, 0);
+                dp[et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ag[et][ds], vf[ds], dp[et], 0, 0, 0);
+            }
+        }
+        // P and dS of (key m, entry 16 et + 4 g4 + r): operand slot 4 et + r of this lane, in three parts
+        uint32_t ph[8], pm[8], pl[8], sh[8], sm[8], sl[8];
+#pragma unroll
+        for (int et = 0; et < 2; ++et) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int te = et * 16 + 4 * g4 + r;
+                const int4 mt = s_meta[wave][te];
+                bool ok = key_ok && abs(mt.x - kx) <= p.b && abs(mt.y - ky) <= p.b;
+                if constexpr (MULTI) {
+                    const int e = s_el[wave][te][0];
+                    for (int f = 0; f < e && ok; ++f) {
+                        uint32_t fu, fv;
+                        divmod(static_cast<uint32_t>(s_prevc[wave][te][f]), p.div_wk, fu, fv);
+                        if (abs(static_cast<int>(fu) - kx) <= p.b && abs(static_cast<int>(fv) - ky) <= p.b)
+                            ok = false;  // an earlier window of the query holds this key
+                    }
+                    if (p.causal) ok = ok && key_local <= static_cast<uint32_t>(s_el[wave][te][1]);
+                }
+                const float pr = ok ? __builtin_amdgcn_exp2f(sc[et][r] * p.scale_log2e - __int_as_float(mt.z)) : 0.f;
+                const float dsr = pr * (dp[et][r] - __int_as_float(mt.w));
+                split3(pr, ph[4 * et + r], pm[4 * et + r], pl[4 * et + r]);
+                split3(dsr, sh[4 * et + r], sm[4 * et + r], sl[4 * et + r]);
+            }
+        }
+        auto operand = [](const uint32_t (&v)[8]) {
+            return __builtin_bit_cast(bf16x8_t, make_uint4(pack_hi16(v[0], v[1]), pack_hi16(v[2], v[3]),
+                                                           pack_hi16(v[4], v[5]), pack_hi16(v[6], v[7])));
+        };
+        const bf16x8_t aph = operand(ph), apm = operand(pm), apl = operand(pl);
+        const bf16x8_t ash = operand(sh), asm_ = operand(sm), asl = operand(sl);
+        // dV_w += P dO_E, dK_w += dS Q_E per 16-channel tile o: the channel-major operands (lane (n, g4): entries
+        // 4 g4 .. 4 g4 + 3 and 16 + 4 g4 .. 16 + 4 g4 + 3, channel 16 o + n) are the row-major fragments times I_h
+        const f32x4_t zero = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int o = 0; o < KS::kOt; ++o) {
+            const int ds = o >> 1, h = o & 1;
+            const f32x4_t q0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq[0][ds], eye[h], zero, 0, 0, 0);
+            const f32x4_t q1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq[1][ds], eye[h], zero, 0, 0, 0);
+            const f32x4_t g0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ag[0][ds], eye[h], zero, 0, 0, 0);
+            const f32x4_t g1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ag[1][ds], eye[h], zero, 0, 0, 0);
+            auto bop = [](const f32x4_t& a, const f32x4_t& b) {
+                return __builtin_bit_cast(
+                    bf16x8_t, make_uint4(pack_hi16(__float_as_uint(a[0]), __float_as_uint(a[1])),
+                                         pack_hi16(__float_as_uint(a[2]), __float_as_uint(a[3])),
+                                         pack_hi16(__float_as_uint(b[0]), __float_as_uint(b[1])),
+                                         pack_hi16(__float_as_uint(b[2]), __float_as_uint(b[3]))));
+            };
+            const bf16x8_t bq = bop(q0, q1), bg = bop(g0, g1);
+            dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aph, bg, dv[o], 0, 0, 0);
+            dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(apm, bg, dv[o], 0, 0, 0);
+            dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(apl, bg, dv[o], 0, 0, 0);
+            dk[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ash, bq, dk[o], 0, 0, 0);
+            dk[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(asm_, bq, dk[o], 0, 0, 0);
+            dk[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(asl, bq, dk[o], 0, 0, 0);
+        }
+        wave_lds_sync();  // this chunk's LDS reads come before the next chunk's writes
+    }
+
+    // lane holds keys 4 g4 + r of the strip, channel 16 o + m
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-        const int it = 16 * wave + 4 * g4 + r;
+        const int it = it0 + 4 * g4 + r;
         const int ox = x0 + (it >> p.tk.lw), oy = y0 + (it & (tw - 1));
         if (ox >= p.Hk || oy >= p.Wk) continue;
         const size_t row = (kslice + static_cast<size_t>(ox) * p.Wk + oy) * D;
 #pragma unroll
-        for (int o = 0; o < KT::kOt; ++o) {
+        for (int o = 0; o < KS::kOt; ++o) {
             p.dK[row + 16 * o + m] = dk[o][r] * p.scale;
             p.dV[row + 16 * o + m] = dv[o][r];
         }
@@ -1031,8 +992,8 @@ hipError_t run_backward(const BwdParams& p0, hipStream_t st, hipEvent_t* ev)
             BwdParams pt = p;
             pt.tk = make_tiling(p.Hk, p.Wk, kTileKeys);
             const uint64_t tblocks = tiling_blocks(pt.tk, p.keys_total / p.nkeys);
-            return multi ? launch(bwd_key_tile_kernel<D, true>, tblocks, st, k0, k1, pt)
-                         : launch(bwd_key_tile_kernel<D, false>, tblocks, st, k0, k1, pt);
+            return multi ? launch(bwd_key_strip_kernel<D, true>, tblocks, st, k0, k1, pt)
+                         : launch(bwd_key_strip_kernel<D, false>, tblocks, st, k0, k1, pt);
         }
     }
     if ((e = launch(bwd_gather_kernel<T, D, G>, gblocks, st, k0, nullptr, p)) != hipSuccess) return e;
