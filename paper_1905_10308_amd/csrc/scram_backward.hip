@@ -724,7 +724,10 @@ bwd_key_strip_kernel(BwdParams p)
     using KS = KeyStrip<D>;
     constexpr int kCE = kStripCE;
     constexpr int kW = kBlock / 64;
-    __shared__ __align__(16) unsigned char s_row[kW][2][kCE * KS::kRowB];  // q, dO rows of the chunk
+    // q rows of the chunk, then 64 bytes of skew, then its dO rows: lanes 2t and 2t + 1 stage row t of
+    // each; with the skew the eight lanes of one 128-bit access (rows t .. t + 3 of both) use disjoint
+    // halves of the 32 banks, without it the two rows of each pair share banks
+    __shared__ __align__(16) unsigned char s_row[kW][2 * kCE * KS::kRowB + 64];
     __shared__ int4 s_meta[kW][kCE];        // match row, match column, lse2 bits, D bits
     __shared__ int32_t s_el[kW][MULTI ? kCE : 1][2];                 // window index e, query's raster index
     __shared__ int32_t s_prevc[kW][MULTI ? kCE : 1][kMaxKappa - 1];  // centres of windows 0..e-1
@@ -816,8 +819,8 @@ bwd_key_strip_kernel(BwdParams p)
         }
         return static_cast<int>(p.entries[lo_w[lo] + (v - pre_w[lo])]);
     };
-    unsigned char* const rows_q = s_row[wave][0];
-    unsigned char* const rows_g = s_row[wave][1];
+    unsigned char* const rows_q = s_row[wave];
+    unsigned char* const rows_g = s_row[wave] + kCE * KS::kRowB + 64;
     int code = slot_code(0);
     for (int c0 = 0; c0 < E; c0 += kCE) {
         {
@@ -831,7 +834,7 @@ bwd_key_strip_kernel(BwdParams p)
                 dq = p.Dq[qg];
             }
             const uint4* src = reinterpret_cast<const uint4*>((hf ? Gb : Qb) + static_cast<size_t>(qg) * D);
-            unsigned char* dst = s_row[wave][hf] + t * KS::kRowB;
+            unsigned char* dst = (hf ? rows_g : rows_q) + t * KS::kRowB;
 #pragma unroll
             for (int i0 = 0; i0 < KS::kPieces; i0 += 8) {
                 uint4 val[8];
