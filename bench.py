@@ -316,7 +316,7 @@ def main(argv=None) -> int:
     att_ms = sum(dur(ev, kappa * (T + 1)) for ev in events) / args.steps
     bwd = {}
     if args.backward:
-        for i, name in enumerate(("backward_inverse_map", "backward_query", "backward_key_side")):
+        for i, name in enumerate(("backward_scan_fill", "backward_query", "backward_key_side")):
             bwd[name] = sum(dur(ev, kappa * (T + 1) + 1 + i) for ev in events) / args.steps
 
     nq = cfg.nq

@@ -238,9 +238,10 @@ int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype, 
  *             d, dtype, kappa) bytes, 256-byte aligned; contents undefined
  *             on return (about 2 * kappa * S*Hq*Wq rows of d elements plus
  *             a few int32 / fp32 per key and query)
- *   events    NULL or 6 events: start/stop of building the inverse map, of
- *             the per-query kernel and of the key side (row copies and the
- *             per-key kernel)
+ *   events    NULL or 6 events: start/stop of the inverse map's scan and
+ *             fill, of the query side (clearing the counts, then the
+ *             per-query kernel, which also counts the inverse map's entries)
+ *             and of the key side
  * Also requires S*Hq*Wq*kappa < 2^31 and S*Hk*Wk < 2^31.  dQ, dK, dV must be 16-byte aligned;
  * no output or the workspace may overlap an input or another output.
  * Returns a status code.
@@ -308,7 +309,7 @@ const char* scram_status_string(int status);
 /* ABI version of this header: (major << 16) | minor. */
 int scram_abi_version(void);
 
-#define SCRAM_ABI_VERSION ((2 << 16) | 4)
+#define SCRAM_ABI_VERSION ((2 << 16) | 5)
 
 #ifdef __cplusplus
 }

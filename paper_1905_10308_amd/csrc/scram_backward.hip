@@ -17,7 +17,10 @@ namespace {
 // log2 of the normaliser (with the max) and D_i for the key side.  Key side (one lane group
 // per key): key j lies in W_i exactly when a match of i lies in the
 // (2b+1)^2 neighbourhood of j, so the queries are found through the inverse
-// map -- the (query, match) entries sorted by match key (a counting sort).
+// map -- the (query, match) entries sorted by match key (a counting sort:
+// the query kernel counts each match key's entries and records each entry's
+// slot among them, a scan turns the counts into offsets, and the fill puts
+// every entry at its key's offset plus its slot, without atomics).
 // The keys of one neighbourhood row are consecutive, so their entries form
 // one contiguous range; after the query kernel, q_i, dO_i and the query's
 // statistics are copied into entry order, so the key kernel reads each
@@ -40,6 +43,8 @@ struct BwdParams {
     float* Dq;             // [n] D_i
     const int32_t* offsets;  // [S * nkeys + 1] start of each key's entries
     const int32_t* entries;  // [kappa * n] e * n + i, grouped by match key
+    int32_t* counts;         // [S * nkeys] entries per match key (zeroed before the query kernel)
+    int32_t* slots;          // [kappa * n] each entry's slot among its key's entries
     int32_t* heavy;          // [S * nkeys] keys left to bwd_heavy_kernel
     int32_t* n_heavy;        // their count
     void* qs;                // [kappa * n, D] q_i of each entry, in entry order
@@ -58,31 +63,21 @@ struct BwdParams {
     int causal;
 };
 
-__global__ __launch_bounds__(kBlock) void zero_i32_kernel(int32_t* a, size_t count)
+// a[0 .. count) = 0 and, when given, *word = 0
+__global__ __launch_bounds__(kBlock) void zero_i32_kernel(int32_t* a, size_t count, int32_t* word)
 {
     for (size_t i = static_cast<size_t>(blockIdx.x) * kBlock + threadIdx.x; i < count;
          i += static_cast<size_t>(gridDim.x) * kBlock)
         a[i] = 0;
+    if (word != nullptr && blockIdx.x == 0 && threadIdx.x == 0) *word = 0;
 }
 
-// counts[s * nkeys + J[e][i]] += 1 for every (query, match)
-__global__ __launch_bounds__(kBlock) void bwd_count_kernel(BwdParams p, int32_t* counts)
+// Exclusive scan of in[0 .. count) by one block, count <= kScanTile, into
+// out (which may be in, in global or shared memory); returns the total to
+// thread kBlock - 1.  wave_tot: kBlock / 64 ints of shared memory.
+__device__ int32_t block_exclusive_scan(const int32_t* in, int32_t* out, size_t count, int32_t* wave_tot)
 {
-    const size_t total = static_cast<size_t>(p.kappa) * p.n;
-    for (size_t x = static_cast<size_t>(blockIdx.x) * kBlock + threadIdx.x; x < total;
-         x += static_cast<size_t>(gridDim.x) * kBlock) {
-        const uint32_t g = static_cast<uint32_t>(x % p.n);
-        const uint32_t s = g / (static_cast<uint32_t>(p.Hq) * p.Wq);
-        atomicAdd(counts + static_cast<size_t>(s) * p.nkeys + clamp_index(p.J[x], p.nkeys), 1);
-    }
-}
-
-// Exclusive scan, step 1: each block scans a tile of kScanTile counts into
-// out (tile-local prefixes) and writes the tile's total to sums[tile].
-__global__ __launch_bounds__(kBlock) void scan_tiles_kernel(const int32_t* in, int32_t* out, int32_t* sums, size_t count)
-{
-    __shared__ int32_t wave_tot[kBlock / 64];
-    const size_t base = static_cast<size_t>(blockIdx.x) * kScanTile + static_cast<size_t>(threadIdx.x) * kScanItems;
+    const size_t base = static_cast<size_t>(threadIdx.x) * kScanItems;
     int32_t v[kScanItems];
     int32_t run = 0;
 #pragma unroll
@@ -107,11 +102,19 @@ __global__ __launch_bounds__(kBlock) void scan_tiles_kernel(const int32_t* in, i
 #pragma unroll
     for (int i = 0; i < kScanItems; ++i)
         if (base + i < count) out[base + i] = before + v[i];
-    if (threadIdx.x == kBlock - 1) {
-        int32_t tot = 0;
-        for (int w = 0; w < kBlock / 64; ++w) tot += wave_tot[w];
-        sums[blockIdx.x] = tot;
-    }
+    return before + run;
+}
+
+// Exclusive scan, step 1: each block scans a tile of kScanTile counts into
+// out (tile-local prefixes; out may be in) and writes the tile's total to
+// sums[tile].
+__global__ __launch_bounds__(kBlock) void scan_tiles_kernel(const int32_t* in, int32_t* out, int32_t* sums, size_t count)
+{
+    __shared__ int32_t wave_tot[kBlock / 64];
+    const size_t base = static_cast<size_t>(blockIdx.x) * kScanTile;
+    const int32_t tot = block_exclusive_scan(in + base, out + base, count - base < kScanTile ? count - base : kScanTile,
+                                             wave_tot);
+    if (threadIdx.x == kBlock - 1) sums[blockIdx.x] = tot;
 }
 
 // Exclusive scan, step 2 (one block): sums[0..tiles) in place, total in sums[tiles].
@@ -143,29 +146,38 @@ __global__ __launch_bounds__(kBlock) void scan_sums_kernel(int32_t* sums, uint32
     if (threadIdx.x == 0) sums[tiles] = carry_s;
 }
 
-// Exclusive scan, step 3: add each tile's offset; out[count] = total.
-__global__ __launch_bounds__(kBlock) void scan_add_kernel(int32_t* out, const int32_t* sums, size_t count,
-                                                          uint32_t tiles)
+// The inverse map from the scan: key k's entries start at
+// offsets[k] = local[k] + pre[k / kScanTile] (local: tile-local exclusive
+// prefixes of the counts, pre: exclusive prefixes of the tile totals, the
+// grand total in pre[tiles]), and entry x goes to its key's start plus the
+// slot the count recorded for it.  OWN_SCAN (tiles <= kScanTile): sums holds
+// the raw tile totals and every block scans them into shared memory itself;
+// otherwise scan_sums_kernel has turned sums into pre.
+template <bool OWN_SCAN>
+__global__ __launch_bounds__(kBlock) void bwd_fill_kernel(BwdParams p, const int32_t* local, const int32_t* sums,
+                                                          uint32_t tiles, int32_t* offsets, int32_t* entries)
 {
-    const size_t base = static_cast<size_t>(blockIdx.x) * kScanTile;
-    const int32_t add = sums[blockIdx.x];
-    for (int i = threadIdx.x; i < kScanTile; i += kBlock)
-        if (base + i < count) out[base + i] += add;
-    if (blockIdx.x == 0 && threadIdx.x == 0) out[count] = sums[tiles];
-}
-
-// entries[offsets[key] + (a slot of that key)] = e * n + i; counts end at 0
-__global__ __launch_bounds__(kBlock) void bwd_fill_kernel(BwdParams p, int32_t* counts, int32_t* entries)
-{
-    const size_t total = static_cast<size_t>(p.kappa) * p.n;
-    for (size_t x = static_cast<size_t>(blockIdx.x) * kBlock + threadIdx.x; x < total;
-         x += static_cast<size_t>(gridDim.x) * kBlock) {
-        const uint32_t g = static_cast<uint32_t>(x % p.n);
-        const uint32_t s = g / (static_cast<uint32_t>(p.Hq) * p.Wq);
-        const size_t key = static_cast<size_t>(s) * p.nkeys + clamp_index(p.J[x], p.nkeys);
-        const int32_t slot = atomicSub(counts + key, 1) - 1;
-        entries[p.offsets[key] + slot] = static_cast<int32_t>(x);
+    __shared__ int32_t s_pre[OWN_SCAN ? kScanTile + 1 : 1];
+    __shared__ int32_t wave_tot[kBlock / 64];
+    const int32_t* pre = sums;
+    if constexpr (OWN_SCAN) {
+        const int32_t tot = block_exclusive_scan(sums, s_pre, tiles, wave_tot);
+        if (threadIdx.x == kBlock - 1) s_pre[tiles] = tot;
+        __syncthreads();
+        pre = s_pre;
     }
+    const size_t stride = static_cast<size_t>(gridDim.x) * kBlock;
+    const size_t first = static_cast<size_t>(blockIdx.x) * kBlock + threadIdx.x;
+    const size_t total = static_cast<size_t>(p.kappa) * p.n;
+    for (size_t x = first; x < total; x += stride) {
+        const uint32_t g = static_cast<uint32_t>(x % p.n);
+        uint32_t s, rem;
+        divmod(g, p.div_plane, s, rem);
+        const size_t key = static_cast<size_t>(s) * p.nkeys + clamp_index(p.J[x], p.nkeys);
+        entries[local[key] + pre[key / kScanTile] + p.slots[x]] = static_cast<int32_t>(x);
+    }
+    for (size_t k = first; k < p.keys_total; k += stride) offsets[k] = local[k] + pre[k / kScanTile];
+    if (first == 0) offsets[p.keys_total] = pre[tiles];
 }
 
 // W > 0: window side W (odd), visited one window row at a time with its W
@@ -186,6 +198,14 @@ __global__ __launch_bounds__(kBlock) void bwd_query_kernel(BwdParams p)
 
     uint32_t s, rem;
     divmod(g, p.div_plane, s, rem);
+    // the inverse map's count: one entry per match of this query, and its
+    // slot among the entries of that match key
+    if (lane == 0) {
+        for (int e = 0; e < (MULTI ? p.kappa : 1); ++e) {
+            const size_t x = static_cast<size_t>(e) * p.n + g;
+            p.slots[x] = atomicAdd(p.counts + static_cast<size_t>(s) * p.nkeys + clamp_index(p.J[x], p.nkeys), 1);
+        }
+    }
     const size_t slice = static_cast<size_t>(s) * p.nkeys * D;
     const T* Ks = static_cast<const T*>(p.K) + slice;
     const T* Vs = static_cast<const T*>(p.V) + slice;
@@ -962,8 +982,10 @@ bwd_key_strip_kernel(BwdParams p)
     }
 }
 
-template <typename T, int D>
-hipError_t run_backward(const BwdParams& p0, hipStream_t st, hipEvent_t* ev)
+// The query kernel, then the rest of the inverse map (inverse()), then the
+// key side.
+template <typename T, int D, typename Inverse>
+hipError_t run_backward(const BwdParams& p0, hipStream_t st, hipEvent_t* ev, Inverse&& inverse)
 {
     constexpr int G = Lanes<T, D>::kAttend;
     constexpr uint32_t kQpb = Row<T, D, G>::kQpb;
@@ -973,13 +995,13 @@ hipError_t run_backward(const BwdParams& p0, hipStream_t st, hipEvent_t* ev)
     const uint64_t qblocks = tiling_blocks(p.tq, p.n / p.tq.plane);
     const uint64_t gblocks = (static_cast<uint64_t>(p.kappa) * p.n + kQpb - 1) / kQpb;
     const uint64_t kblocks = tiling_blocks(p.tk, p.keys_total / p.nkeys);
-    hipEvent_t q0 = ev ? ev[2] : nullptr, q1 = ev ? ev[3] : nullptr, k0 = ev ? ev[4] : nullptr,
-               k1 = ev ? ev[5] : nullptr;
+    // the query-side interval opens with the clearing kernel launched before this
+    hipEvent_t q1 = ev ? ev[3] : nullptr, k0 = ev ? ev[4] : nullptr, k1 = ev ? ev[5] : nullptr;
     const bool multi = p.kappa > 1 || p.causal;
     auto query = [&](auto w) {
         constexpr int W = decltype(w)::value;
-        return multi ? launch(bwd_query_kernel<T, D, G, true, W>, qblocks, st, q0, q1, p)
-                     : launch(bwd_query_kernel<T, D, G, false, W>, qblocks, st, q0, q1, p);
+        return multi ? launch(bwd_query_kernel<T, D, G, true, W>, qblocks, st, nullptr, q1, p)
+                     : launch(bwd_query_kernel<T, D, G, false, W>, qblocks, st, nullptr, q1, p);
     };
     const int side = 2 * p.b + 1;
     hipError_t e = side == 1   ? query(std::integral_constant<int, 1>{})
@@ -988,6 +1010,7 @@ hipError_t run_backward(const BwdParams& p0, hipStream_t st, hipEvent_t* ev)
                    : side == 7 ? query(std::integral_constant<int, 7>{})
                                : query(std::integral_constant<int, 0>{});
     if (e != hipSuccess) return e;
+    if ((e = inverse()) != hipSuccess) return e;
     if constexpr (std::is_same<T, uint16_t>::value) {
         // key side on the matrix cores; a one-key window (b = 0) stays on the lane-group kernels, whose dp
         // is the query kernel's own arithmetic, so that dS = p (dp - D) is exactly 0 there
@@ -1017,7 +1040,7 @@ size_t attend_backward_workspace_bytes(int S, int Hq, int Wq, int Hk, int Wk, in
     const size_t row = static_cast<size_t>(d) * (dtype == SCRAM_BF16 ? 2 : 4);
     auto r256 = [](size_t b) { return (b + 255) & ~static_cast<size_t>(255); };
     return r256(4 * N) + r256(4 * (N + 1)) + r256(4 * (tiles + 1)) + r256(4 * n * kappa) + 2 * r256(4 * n) +
-           2 * r256(row * n * kappa) + r256(8 * n * kappa) + r256(4 * (N + 1));
+           2 * r256(row * n * kappa) + r256(8 * n * kappa) + r256(4 * (N + 1)) + r256(4 * n * kappa);
 }
 
 hipError_t launch_attend_backward(int dtype, const void* Q, const void* K, const void* V, const int32_t* J, int kappa,
@@ -1076,6 +1099,9 @@ hipError_t launch_attend_backward(int dtype, const void* Q, const void* K, const
     w += r256(8 * static_cast<size_t>(p.n) * kappa);
     p.n_heavy = reinterpret_cast<int32_t*>(w);  // counter, then the list
     p.heavy = p.n_heavy + 1;
+    w += r256(4 * (N + 1));
+    p.slots = reinterpret_cast<int32_t*>(w);
+    p.counts = counts;
     p.offsets = offsets;
     p.entries = entries;
 
@@ -1084,26 +1110,31 @@ hipError_t launch_attend_backward(int dtype, const void* Q, const void* K, const
         return static_cast<uint32_t>(b < 1 ? 1 : (b > 4096 ? 4096 : b));
     };
     hipEvent_t e0 = events ? events[0] : nullptr, e1 = events ? events[1] : nullptr;
+    hipEvent_t q0 = events ? events[2] : nullptr;
     const size_t entries_total = static_cast<size_t>(p.n) * kappa;
     hipError_t e;
-    // inverse map: counting sort of the (query, match) entries by match key
-    if ((e = launch(zero_i32_kernel, grid_for(N), stream, e0, nullptr, counts, N)) != hipSuccess) return e;
-    if ((e = launch(bwd_count_kernel, grid_for(entries_total), stream, nullptr, nullptr, p, counts)) != hipSuccess)
-        return e;
-    if ((e = launch(scan_tiles_kernel, tiles, stream, nullptr, nullptr, static_cast<const int32_t*>(counts), offsets,
-                    sums, N)) != hipSuccess)
-        return e;
-    if ((e = launch(scan_sums_kernel, 1u, stream, nullptr, nullptr, sums, tiles)) != hipSuccess) return e;
-    if ((e = launch(scan_add_kernel, tiles, stream, nullptr, nullptr, offsets, static_cast<const int32_t*>(sums), N,
-                    tiles)) != hipSuccess)
-        return e;
-    if ((e = launch(bwd_fill_kernel, grid_for(entries_total), stream, nullptr, nullptr, p, counts, entries)) !=
-        hipSuccess)
-        return e;
-    if ((e = launch(zero_i32_kernel, 1u, stream, nullptr, e1, p.n_heavy, static_cast<size_t>(1))) != hipSuccess) return e;
+    // inverse map: a counting sort of the (query, match) entries by match key.
+    // The counts (and the heavy-key counter) start at zero; the query kernel
+    // counts; the scan and the fill follow it.
+    if ((e = launch(zero_i32_kernel, grid_for(N), stream, q0, nullptr, counts, N, p.n_heavy)) != hipSuccess) return e;
+    auto inverse = [&]() -> hipError_t {
+        hipError_t r;
+        if ((r = launch(scan_tiles_kernel, tiles, stream, e0, nullptr, static_cast<const int32_t*>(counts), counts,
+                        sums, N)) != hipSuccess)
+            return r;
+        const uint32_t fill_blocks = grid_for(entries_total > N ? entries_total : N + 1);
+        if (tiles <= static_cast<uint32_t>(kScanTile))
+            return launch(bwd_fill_kernel<true>, fill_blocks, stream, nullptr, e1, p,
+                          static_cast<const int32_t*>(counts), static_cast<const int32_t*>(sums), tiles, offsets,
+                          entries);
+        if ((r = launch(scan_sums_kernel, 1u, stream, nullptr, nullptr, sums, tiles)) != hipSuccess) return r;
+        return launch(bwd_fill_kernel<false>, fill_blocks, stream, nullptr, e1, p,
+                      static_cast<const int32_t*>(counts), static_cast<const int32_t*>(sums), tiles, offsets,
+                      entries);
+    };
     // gradients
     return dispatch(dtype, g.d, [&](auto ty, auto d) {
-        return run_backward<decltype(ty), decltype(d)::value>(p, stream, events);
+        return run_backward<decltype(ty), decltype(d)::value>(p, stream, events, inverse);
     });
 }
 

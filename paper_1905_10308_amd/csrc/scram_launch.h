@@ -50,8 +50,9 @@ hipError_t launch_attend(int dtype, const void* Q, const void* K, const void* V,
 // Gradients of the attend step with the maps held fixed.  The workspace
 // (attend_backward_workspace_bytes) holds the inverse map, per-query
 // softmax statistics and the entry-ordered copies of q, dO and those
-// statistics.  events: null or 6 (inverse map start/stop, query kernel
-// start/stop, key side (copies + key kernel) start/stop).
+// statistics.  events: null or 6 (inverse map's scan and fill start/stop,
+// query side (clearing the counts, then the query kernel, which counts the
+// inverse map's entries) start/stop, key side start/stop).
 size_t attend_backward_workspace_bytes(int S, int Hq, int Wq, int Hk, int Wk, int d, int dtype, int kappa);
 hipError_t launch_attend_backward(int dtype, const void* Q, const void* K, const void* V, const int32_t* J, int kappa,
                                   const Grid& g, int window, float scale, bool causal, const void* dO, float* dQ,

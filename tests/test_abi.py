@@ -52,7 +52,7 @@ def test_library_exports_every_declared_symbol(L):
 
 
 def test_abi_version(L):
-    assert L.scram_abi_version() == (2 << 16) | 4
+    assert L.scram_abi_version() == (2 << 16) | 5
 
 
 def test_status_strings(L):
@@ -219,7 +219,7 @@ def test_backward_workspace_formula(L):
         tiles = (N + 2047) // 2048
         row = d * (2 if dtype == BF16 else 4)
         want = (r256(4 * N) + r256(4 * (N + 1)) + r256(4 * (tiles + 1)) + r256(4 * n * kappa) + 2 * r256(4 * n)
-                + 2 * r256(row * n * kappa) + r256(8 * n * kappa) + r256(4 * (N + 1)))
+                + 2 * r256(row * n * kappa) + r256(8 * n * kappa) + r256(4 * (N + 1)) + r256(4 * n * kappa))
         L.scram_sparse_attend_backward_workspace_bytes.restype = ctypes.c_size_t
         assert L.scram_sparse_attend_backward_workspace_bytes(S, Hq, Wq, Hk, Wk, d, dtype, kappa) == want
     assert L.scram_sparse_attend_backward_workspace_bytes(0, 4, 4, 4, 4, 16, F32, 1) == 0

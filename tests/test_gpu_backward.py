@@ -144,6 +144,29 @@ def test_backward_full_size(scram):
     log(f"{cfg.name} full-size backward: rel err dQ {worst[0]:.2e} dK {worst[1]:.2e} dV {worst[2]:.2e}")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("grid", [(1, 2048, 2048), (3, 1200, 1200)], ids=["2048sq_keys", "3x1200sq_keys"])
+def test_backward_many_keys(scram, grid, dtype):
+    """Key grids at and past the size whose 2048-count scan tiles number at most 2048 (4,194,304 keys), where
+    the fill scans the tile totals itself; past it a separate kernel scans them.  Few queries, so almost every
+    key gets zero gradients; some matches sit on the grid's first and last keys."""
+    S, Hk, Wk = grid
+    Hq = Wq = 4
+    d = 16
+    rng = np.random.default_rng(Hk + S)
+    Q, dO = (rng.standard_normal((S, Hq, Wq, d)).astype(np.float32) for _ in range(2))
+    K, V = (rng.standard_normal((S, Hk, Wk, d)).astype(np.float32) for _ in range(2))
+    if dtype == "bf16":
+        Q, K, V, dO = (to_dev(x, "bf16").float().cpu().numpy() for x in (Q, K, V, dO))
+    J = rng.integers(0, Hk * Wk, (2, S, Hq, Wq)).astype(np.int32)
+    J[0, :, 0, 0], J[1, :, 0, 1] = 0, Hk * Wk - 1
+    log(f"backward many keys: S={S} keys {Hk}x{Wk} {dtype}")
+    got = scram.sparse_attend_backward(*(to_dev(x, dtype) for x in (Q, K, V)), torch.from_numpy(J).cuda(),
+                                       to_dev(dO, dtype), 3, d ** -0.5)
+    ref = oracle.sparse_attend_backward(Q, K, V, J, 3, d ** -0.5, dO)
+    grads_close(got, ref, f"{grid} {dtype}")
+
+
 def test_backward_events(scram):
     cfg = SMALL[1]
     a = si.make_arrays(cfg)
