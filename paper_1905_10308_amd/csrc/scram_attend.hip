@@ -109,17 +109,19 @@ __global__ __launch_bounds__(kBlock) void attend_window_kernel(AttParams p)
                 mb = fmaxf(mb, sc[c]);
             }
             if (mb == -INFINITY) continue;  // nothing of this row is in the set
-            const float alpha = __builtin_amdgcn_exp2f(m - mb);  // 0 on the first row
-            l *= alpha;
+            if (mb > m + kRescaleSlack) {
+                const float alpha = __builtin_amdgcn_exp2f(m - mb);  // 0 on the first row
+                l *= alpha;
 #pragma unroll
-            for (int i = 0; i < E; ++i) acc[i] *= alpha;
+                for (int i = 0; i < E; ++i) acc[i] *= alpha;
+                m = mb;
+            }
 #pragma unroll
             for (int c = 0; c < W; ++c) {
-                const float pj = __builtin_amdgcn_exp2f(sc[c] - mb);  // exp2(-inf) = 0
+                const float pj = __builtin_amdgcn_exp2f(sc[c] - m);  // exp2(-inf) = 0
                 l += pj;
                 accumulate_row<T, CH>(acc, pj, vr[c]);
             }
-            m = mb;
         }
     }
     store_row<T, D, G>(p.out, g, lane, acc, l > 0.f ? 1.f / l : 0.f);  // an empty set gives a zero row
@@ -195,17 +197,19 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
                 mb = fmaxf(mb, sc[j]);
             }
             if (mb == -INFINITY) continue;
-            const float alpha = __builtin_amdgcn_exp2f(m - mb);
-            l *= alpha;
+            if (mb > m + kRescaleSlack) {
+                const float alpha = __builtin_amdgcn_exp2f(m - mb);
+                l *= alpha;
 #pragma unroll
-            for (int i = 0; i < E; ++i) acc[i] *= alpha;
+                for (int i = 0; i < E; ++i) acc[i] *= alpha;
+                m = mb;
+            }
 #pragma unroll
             for (int j = 0; j < kNb; ++j) {
-                const float pj = __builtin_amdgcn_exp2f(sc[j] - mb);
+                const float pj = __builtin_amdgcn_exp2f(sc[j] - m);
                 l += pj;
                 accumulate_row<T, CH>(acc, pj, vr[j]);
             }
-            m = mb;
         }
     }
     store_row<T, D, G>(p.out, g, lane, acc, l > 0.f ? 1.f / l : 0.f);  // an empty set gives a zero row

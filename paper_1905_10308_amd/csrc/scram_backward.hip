@@ -311,17 +311,20 @@ __global__ __launch_bounds__(kBlock) void bwd_query_kernel(BwdParams p)
             mb = fmaxf(mb, sc[j]);
         }
         if (mb == -INFINITY) return;
-        const float alpha = __builtin_amdgcn_exp2f(m - mb);
-        l *= alpha;
-        dn *= alpha;
+        if (mb > m + kRescaleSlack) {
+            const float alpha = __builtin_amdgcn_exp2f(m - mb);
+            l *= alpha;
+            dn *= alpha;
 #pragma unroll
-        for (int e = 0; e < E; ++e) {
-            acc_a[e] *= alpha;
-            acc_b[e] *= alpha;
+            for (int e = 0; e < E; ++e) {
+                acc_a[e] *= alpha;
+                acc_b[e] *= alpha;
+            }
+            m = mb;
         }
 #pragma unroll
         for (int j = 0; j < kNb; ++j) {
-            const float pj = __builtin_amdgcn_exp2f(sc[j] - mb);  // 0 when !ok
+            const float pj = __builtin_amdgcn_exp2f(sc[j] - m);  // 0 when !ok
             const float pd = pj * dp[j];
             l += pj;
             dn += pd;
@@ -334,7 +337,6 @@ __global__ __launch_bounds__(kBlock) void bwd_query_kernel(BwdParams p)
                 acc_b[e] = fmaf(pj, kd, acc_b[e]);
             }
         }
-        m = mb;
     });
     const float inv = l > 0.f ? 1.f / l : 0.f;
     const float Dg = dn * inv;

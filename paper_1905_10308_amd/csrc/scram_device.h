@@ -298,6 +298,12 @@ struct Lanes {
     static constexpr int kAttend = LanesFor<T, D, SCRAM_ATTEND_LANE_BYTES>::kG;
 };
 
+// Online softmax in the base-2 domain: the running reference m is raised
+// (and the sums rescaled by 2^(m_old - m_new)) only when a score passes it by
+// more than this, so weights 2^(s - m) stay below 2^kRescaleSlack and most
+// window rows need no rescale; the ratio of the sums does not depend on m.
+constexpr float kRescaleSlack = 8.f;
+
 constexpr int kMaxKappa = 8;  // maps whose windows attend may unite
 
 // ---------------------------------------------------------------------------
