@@ -167,6 +167,27 @@ def test_backward_many_keys(scram, grid, dtype):
     grads_close(got, ref, f"{grid} {dtype}")
 
 
+@pytest.mark.parametrize("dtype,d,scale", [("f32", 16, 1 / 2), ("bf16", 64, 1 / 4)])
+def test_backward_wide_score_range(scram, dtype, d, scale):
+    """Small-integer q, k (exact dot products) with a power-of-two scale near 2/sqrt(d): window scores
+    spread with a standard deviation of about 10 in base-2 units, so the query kernel's online softmax
+    raises its reference and rescales its sums after the first window row for many queries; single
+    windows, the union of two, and causal."""
+    rng = np.random.default_rng(11 + d)
+    S, H, W = 2, 13, 11
+    Q, K = (rng.integers(-3, 4, (S, H, W, d)).astype(np.float32) for _ in range(2))
+    V, dO = (rng.integers(-4, 5, (S, H, W, d)).astype(np.float32) for _ in range(2))
+    J = rng.integers(0, H * W, (2, S, H, W)).astype(np.int32)
+    dev = [to_dev(x, dtype) for x in (Q, K, V)]
+    for window in (3, 5, 9):
+        for maps, causal in ((J[0], False), (J, False), (J, True)):
+            got = scram.sparse_attend_backward(*dev, torch.from_numpy(np.ascontiguousarray(maps)).cuda(),
+                                               to_dev(dO, dtype), window, scale, causal=causal)
+            ref = oracle.sparse_attend_backward(Q, K, V, maps, window, scale, dO,
+                                                flags=oracle.CAUSAL if causal else 0)
+            grads_close(got, ref, f"wide scores {dtype} window {window} kappa {maps.ndim - 2} causal {causal}")
+
+
 def test_backward_events(scram):
     cfg = SMALL[1]
     a = si.make_arrays(cfg)

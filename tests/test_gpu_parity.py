@@ -137,6 +137,61 @@ def test_attend_parity(scram, work):
     assert err.max() <= TOL[cfg.dtype]
 
 
+def _rescaling_queries(Q, K, J, window, scale):
+    """Queries whose online softmax, visiting the window row by row from the top, meets a row whose best
+    score passes the running reference by more than 8 (base-2 units): the case where the kernels raise
+    the reference and rescale their sums after the first row."""
+    S, Hq, Wq, d = Q.shape
+    Hk, Wk = K.shape[1:3]
+    b = window // 2
+    hits = 0
+    for s_ in range(S):
+        for x in range(Hq):
+            for y in range(Wq):
+                u, v = divmod(int(J[s_, x, y]), Wk)
+                ref = -np.inf
+                for r in range(max(u - b, 0), min(u + b, Hk - 1) + 1):
+                    cols = slice(max(v - b, 0), min(v + b, Wk - 1) + 1)
+                    best = float((K[s_, r, cols] @ Q[s_, x, y]).max()) * scale * math.log2(math.e)
+                    if best > ref + 8:
+                        if ref > -np.inf:
+                            hits += 1
+                            break
+                        ref = best
+    return hits
+
+
+@pytest.mark.parametrize("dtype,d,scale", [("f32", 16, 1 / 2), ("bf16", 64, 1 / 4), ("f32", 128, 1 / 8)])
+def test_attend_wide_score_range(scram, dtype, d, scale):
+    """Small-integer q and k (every dot product exact in fp32 and bf16) with a power-of-two scale near
+    2/sqrt(d), so window scores spread with a standard deviation of 8-12 in base-2 units and later window
+    rows often pass the softmax's running reference by more than 8: the kernels then rescale their sums
+    (checked to happen for a quarter of the queries or more).  Row kernels (sides 3, 5, 7), the any-side
+    kernel (9, 11), the union of two windows and the causal mask."""
+    rng = np.random.default_rng(7 + d)
+    S, H, W = 2, 13, 11
+    Q = rng.integers(-3, 4, (S, H, W, d)).astype(np.float32)
+    K = rng.integers(-3, 4, (S, H, W, d)).astype(np.float32)
+    V = rng.integers(-4, 5, (S, H, W, d)).astype(np.float32)
+    J = rng.integers(0, H * W, (2, S, H, W)).astype(np.int32)
+    assert _rescaling_queries(Q, K, J[0], 5, scale) >= S * H * W // 4
+    dev = [to_dev(x, dtype) for x in (Q, K, V)]
+    worst = 0.0
+    for window in (3, 5, 7, 9, 11):
+        for maps, causal in ((J[0], False), (J, False), (J[0], True), (J, True)):
+            out = scram.sparse_attend(*dev, torch.from_numpy(np.ascontiguousarray(maps)).cuda(), window, scale,
+                                      causal=causal)
+            ref = oracle.sparse_attend(Q, K, V, maps, window, scale, flags=oracle.CAUSAL if causal else 0)
+            got = out.float().cpu().numpy()
+            if causal:  # a query whose windows hold no key at or before it gets a zero row
+                empty = np.abs(ref).max(axis=-1) == 0
+                assert np.all(got[empty] == 0)
+            err = row_rel_err(got, ref)
+            worst = max(worst, float(err.max()))
+            assert err.max() <= TOL[dtype], f"window {window} kappa {maps.ndim - 2} causal {causal}: {err.max():.3e}"
+    log(f"wide score range {dtype} d={d}: attend max rel err {worst:.3e}")
+
+
 def test_attend_window_one_is_value_gather(scram, work):
     """b = 0: the output is exactly v at the match."""
     cfg, a, dev = work
