@@ -79,6 +79,35 @@ def load_traffic(cfg):
     return t.get("hbm_bytes_per_launch")
 
 
+def map_quality(cfg, Q, K, J, per_slice: int = 4096, seed: int = 3):
+    """Quality of a final map, outside the timed regions: recall against the exact argmax over all keys
+    (fp64 products on the GPU, the first index among equal maxima) and the mean ratio of the map's
+    score to the exact maximum, on ``per_slice`` sampled queries of each slice.  A comparator, like the
+    dense attention timing; the paper prints no quality figure for these workloads."""
+    import torch
+
+    gen = torch.Generator(device="cpu").manual_seed(seed)
+    plane, nk = cfg.Hq * cfg.Wq, cfg.Hk * cfg.Wk
+    hits = total = 0
+    ratios = []
+    for s in range(cfg.S):
+        ids = torch.randperm(plane, generator=gen)[:per_slice].to(Q.device)
+        q = Q[s].reshape(plane, cfg.d)[ids].double()
+        kt = K[s].reshape(nk, cfg.d).double().t().contiguous()
+        jm = J[s].reshape(plane)[ids].long()
+        for c0 in range(0, ids.numel(), 1024):
+            sc = q[c0:c0 + 1024] @ kt
+            best, arg = sc.max(dim=1)
+            mine = sc.gather(1, jm[c0:c0 + 1024, None]).squeeze(1)
+            hits += int((arg == jm[c0:c0 + 1024]).sum())
+            total += arg.numel()
+            pos = best > 0
+            ratios.append(mine[pos] / best[pos])
+    return {"recall_vs_exact_argmax": hits / total, "mean_score_ratio": float(torch.cat(ratios).mean()),
+            "sample": f"{min(per_slice, plane)} queries per slice ({total} in all), exact argmax from fp64 "
+                      "products on the GPU"}
+
+
 def cpu_baseline(cfg, arrays, min_s: float, kappa: int = 1, sep: int = 1, causal: bool = False, snis=None):
     """The fp64 oracle on the host cores, on whole slices of the same workload.
 
@@ -381,6 +410,8 @@ def main(argv=None) -> int:
         "wall_ms_per_step": wall * 1e3 / args.steps,
         "device": torch.cuda.get_device_name(dev),
     }
+    if kappa == 1 and not causal:
+        res["map_quality"] = map_quality(cfg, Q, K, J[0])
     dense = dense_attention(cfg, Q, K, V) if not (kappa > 1 or causal or args.snis) else None
     if dense is not None:
         dense["step_speedup"] = dense["ms"] / ms_step
