@@ -103,6 +103,29 @@ def test_resume_bit_exact(scram, work):
     assert torch.equal(sfull, srest)
 
 
+@pytest.mark.parametrize("seed", [0xDEADBEEF12345678, (1 << 64) - 1])
+def test_largest_sweep_index_and_wide_seeds(scram, seed):
+    """The last sweep indices a call can reach (t0 is an int: sweeps 2^31 - 2 and 2^31 - 1, chained in one
+    call) with seeds whose high word is set, so both Philox key words and the top of the counter's sweep
+    word are exercised; teacher-forced against the oracle's sweeps at the same indices."""
+    cfg = SMALL[0]
+    a = si.make_arrays(cfg)
+    dev = {k: to_dev(a[k], cfg.dtype) for k in ("Q", "K")}
+    J0, s0 = oracle.pm_init(a["Q"], a["K"], seed)
+    Jg0 = scram.patchmatch(dev["Q"], dev["K"], 0, seed).cpu().numpy()
+    np.testing.assert_array_equal(Jg0, J0)
+    t0 = (1 << 31) - 2
+    J1, s1, tie1, _ = oracle.pm_iteration(a["Q"], a["K"], J0, t0, seed, s_prev=s0)
+    J2, _, tie2, _ = oracle.pm_iteration(a["Q"], a["K"], J1, t0 + 1, seed, s_prev=s1)
+    g1 = scram.patchmatch(dev["Q"], dev["K"], 1, seed, init=torch.from_numpy(J0).cuda(), t0=t0).cpu().numpy()
+    assert not ((g1 != J1) & ~tie1).any()
+    if (g1 == J1).all():  # the second sweep is compared from the same start
+        g2 = scram.patchmatch(dev["Q"], dev["K"], 2, seed, init=torch.from_numpy(J0).cuda(), t0=t0).cpu().numpy()
+        assert not ((g2 != J2) & ~tie2).any()
+    with pytest.raises(Exception):  # one sweep past the last index the counter word can take from an int t0
+        scram.patchmatch(dev["Q"], dev["K"], 2, seed, init=torch.from_numpy(J0).cuda(), t0=(1 << 31) - 1 + 1)
+
+
 def test_timing_events_leave_results_unchanged(scram, work):
     cfg, a, dev = work
     ref = scram.patchmatch(dev["Q"], dev["K"], cfg.iters, cfg.pm_seed)
