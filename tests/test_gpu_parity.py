@@ -21,7 +21,8 @@ import oracle.dense as dense
 import scram_inputs as si
 
 torch = pytest.importorskip("torch")
-from gpu_util import IDS, SCORE_TOL, SMALL, TOL, dilate, log, reach_of_ties, row_rel_err, to_dev  # noqa: E402
+from gpu_util import (IDS, MAX_TIE_FRAC, SCORE_TOL, SMALL, TOL, add_counts, compare_maps, dilate,  # noqa: E402
+                      log, reach_of_ties, row_rel_err, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -49,17 +50,13 @@ def test_teacher_forced_sweeps(scram, work):
     """Each sweep t, fed the oracle's map J_{t-1}, gives the oracle's J_t (up to recorded near ties)."""
     cfg, a, dev = work
     J, s = oracle.pm_init(a["Q"], a["K"], cfg.pm_seed)
-    total_ties = total_mism = 0
+    total = {}
     for t in range(1, cfg.iters + 1):
         Jn, sn, tie, _ = oracle.pm_iteration(a["Q"], a["K"], J, t, cfg.pm_seed, s_prev=s)
         Jg = scram.patchmatch(dev["Q"], dev["K"], 1, cfg.pm_seed, init=torch.from_numpy(J).cuda(), t0=t)
-        Jg = Jg.cpu().numpy()
-        mism = Jg != Jn
-        assert not (mism & ~tie).any(), f"sweep {t}: {int((mism & ~tie).sum())} mismatches outside near ties"
-        total_ties += int(tie.sum())
-        total_mism += int(mism.sum())
+        add_counts(total, compare_maps(a["Q"], a["K"], Jg.cpu().numpy(), Jn, tie, f"sweep {t}"))
         J, s = Jn, sn
-    log(f"{cfg.name}: teacher-forced near ties {total_ties}, mismatches at them {total_mism}")
+    log(f"{cfg.name}: teacher-forced {total}")
 
 
 @pytest.mark.parametrize("flags", [1, 2], ids=["no_propagation", "no_random_search"])
@@ -75,20 +72,33 @@ def test_teacher_forced_single_step(scram, work, flags):
 
 
 def test_end_to_end_map(scram, work):
+    """The GPU's T-sweep map against the oracle's own chain.  A difference can only start where the GPU,
+    fed its own previous map, took a decision the oracle flags as a near tie the other way (a flip), and
+    spread from there by propagation; with no flip the two maps are equal bit for bit."""
     cfg, a, dev = work
     Jg, sg = scram.patchmatch(dev["Q"], dev["K"], cfg.iters, cfg.pm_seed, return_score=True)
     Jg, sg = Jg.cpu().numpy(), sg.cpu().numpy()
     Jo, so, ties, nc = oracle.patchmatch(a["Q"], a["K"], cfg.iters, cfg.pm_seed)
+    flips = []
+    J, s = scram.patchmatch(dev["Q"], dev["K"], 0, cfg.pm_seed, return_score=True)
+    for t in range(1, cfg.iters + 1):
+        Jprev = J.cpu().numpy()
+        J, s = scram.patchmatch(dev["Q"], dev["K"], 1, cfg.pm_seed, init=J, init_score=s, t0=t, return_score=True)
+        Jt, _, tie, _ = oracle.pm_iteration(a["Q"], a["K"], Jprev, t, cfg.pm_seed)
+        flips.append(J.cpu().numpy() != Jt)
+        assert not (flips[-1] & ~tie).any()
+    np.testing.assert_array_equal(J.cpu().numpy(), Jg)
     mism = Jg != Jo
-    allowed = reach_of_ties(ties)
-    assert not (mism & ~allowed).any(), f"{int((mism & ~allowed).sum())} mismatches outside near-tie reach"
+    allowed = reach_of_ties(np.stack(flips))
+    assert not (mism & ~allowed).any(), f"{int((mism & ~allowed).sum())} mismatches outside the flips' reach"
+    assert ties.reshape(cfg.iters, -1).mean(axis=1).max() <= MAX_TIE_FRAC
     # the fp32 scores are the scores of the returned keys
     s_of_g, sabs = oracle.pm_scores(a["Q"], a["K"], Jg)
     assert (np.abs(sg - s_of_g) <= SCORE_TOL * sabs).all()
     Jb, sb = dense.brute_argmax(a["Q"], a["K"]) if cfg.nq <= 8192 else (None, None)
     rec = float((Jg == Jb).mean()) if Jb is not None else float("nan")
-    log(f"{cfg.name}: end-to-end mismatches {int(mism.sum())} / {mism.size}, near ties {int(ties.sum())}, "
-        f"candidates {nc}, recall vs brute force {rec:.4f}")
+    log(f"{cfg.name}: end-to-end mismatches {int(mism.sum())} / {mism.size}, flips {int(np.sum(flips))}, "
+        f"near ties {int(ties.sum())}, candidates {nc}, recall vs brute force {rec:.4f}")
 
 
 def test_resume_bit_exact(scram, work):
@@ -359,7 +369,7 @@ def test_channel_padding(scram, d, dv, dtype):
                                       var=True)
     rest, ress, _ = oracle.snis(Q, K, V, Jg, 16, 0.8, 2, scale, 3)
     assert est.shape == (S, H, W, dv) and var.shape == (S, H, W, dv)
-    tol = 5e-5 * np.abs(V).max() + (2.0 ** -8 * np.abs(rest) if dtype == "bf16" else 0.0)
+    tol = 1e-5 * np.abs(V).max() + (2.0 ** -8 * np.abs(rest) if dtype == "bf16" else 0.0)
     assert (np.abs(est.float().cpu().numpy() - rest) <= tol).all()
     assert np.abs(ess.cpu().numpy() - ress).max() <= 1e-4 * ress.max()
 
