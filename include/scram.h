@@ -53,7 +53,9 @@
  * - Pointers are device pointers (HIP) owned by the caller.  Q, K, V and the
  *   attend output must be 16-byte aligned; index and score buffers 4-byte
  *   aligned; the workspace 256-byte aligned.  The library allocates no memory
- *   and keeps no state between calls; calls are re-entrant.
+ *   and keeps no state between calls; calls are re-entrant.  (The one
+ *   exception is scram_patchmatch_noalloc, whose buffers are a fixed device
+ *   array the library holds; see there.)
  * - Every call only enqueues work on `stream` (0 = the null stream) and
  *   returns without synchronising.  Arguments are validated on the host
  *   before any HIP call; a non-zero status means nothing was enqueued
@@ -88,7 +90,8 @@ enum {
     SCRAM_ERR_ALIGN = -4,       /* a pointer is not aligned as required */
     SCRAM_ERR_ALIAS = -5,       /* an output overlaps an input or another output */
     SCRAM_ERR_HIP = -6,         /* a HIP call failed */
-    SCRAM_ERR_WORKSPACE = -7    /* workspace missing or smaller than required */
+    SCRAM_ERR_WORKSPACE = -7,   /* workspace missing or smaller than required */
+    SCRAM_ERR_SCRATCH = -8      /* more queries than scram_patchmatch_noalloc's fixed scratch holds */
 };
 
 /* flags of scram_patchmatch: switch one step of an iteration off (tests) */
@@ -180,6 +183,39 @@ int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int
                      int t0, uint32_t flags, const int32_t* prev, int n_prev, int sep, int32_t* argmax_out,
                      float* score_out, void* workspace, size_t workspace_bytes, hipEvent_t* events,
                      hipStream_t stream);
+
+/*
+ * scram_patchmatch without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  The sweeps' ping-pong buffers (one int32
+ * map and two fp32 score maps) live in a fixed array of
+ * SCRAM_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it has
+ * run this entry point on, from that first call until the process ends; the
+ * call itself allocates nothing.
+ *
+ * Arguments, outputs, events and semantics are those of scram_patchmatch
+ * (results bit for bit equal to it), minus workspace and workspace_bytes.
+ * Limit: S * Hq * Wq <= SCRAM_NOALLOC_MAX_QUERIES, else SCRAM_ERR_SCRATCH;
+ * like every other argument error, this is found on the host before any
+ * HIP call.  The first call on a device looks up that device's copy of the
+ * array (the device of `stream`, or the current device for the null
+ * stream); a failure there is SCRAM_ERR_HIP.  The scratch needs no
+ * clearing: every buffer in it is written before it is read.
+ *
+ * All calls on one GPU share its array, which keeps the last call's
+ * contents: calls ordered on one stream are safe, but calls that may
+ * overlap in time on one GPU (several streams, or host threads without an
+ * ordering between their streams) race on it and give undefined results.
+ */
+enum {
+    SCRAM_NOALLOC_MAX_QUERIES = 1 << 20,
+    SCRAM_NOALLOC_SCRATCH_BYTES = 3 * 4 * SCRAM_NOALLOC_MAX_QUERIES /* 12 MiB */
+};
+
+int scram_patchmatch_noalloc(const void* Q, const void* K, int dtype, int S, int Hq, int Wq, int Hk, int Wk, int d,
+                             int iters, uint64_t seed, const int32_t* init, const float* init_score, int t0,
+                             uint32_t flags, const int32_t* prev, int n_prev, int sep, int32_t* argmax_out,
+                             float* score_out, hipEvent_t* events, hipStream_t stream);
 
 /*
  * Sparse attention around the matches (Algorithm 2, Equations 8-9).  For
@@ -309,7 +345,7 @@ const char* scram_status_string(int status);
 /* ABI version of this header: (major << 16) | minor. */
 int scram_abi_version(void);
 
-#define SCRAM_ABI_VERSION ((2 << 16) | 5)
+#define SCRAM_ABI_VERSION ((2 << 16) | 6)
 
 #ifdef __cplusplus
 }

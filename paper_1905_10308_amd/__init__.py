@@ -9,6 +9,7 @@ from .binding import (  # noqa: F401
     CAUSAL,
     MAX_KAPPA,
     MAX_PREV,
+    NOALLOC_MAX_QUERIES,
     NO_PROPAGATION,
     NO_RANDOM_SEARCH,
     ScramError,
@@ -16,6 +17,7 @@ from .binding import (  # noqa: F401
     lib,
     patchmatch,
     patchmatch_kappa,
+    patchmatch_noalloc,
     patchmatch_workspace_bytes,
     snis_attend,
     sparse_attend,

@@ -34,7 +34,10 @@ STATUS = {
     -5: "SCRAM_ERR_ALIAS",
     -6: "SCRAM_ERR_HIP",
     -7: "SCRAM_ERR_WORKSPACE",
+    -8: "SCRAM_ERR_SCRATCH",
 }
+#: most queries (S * Hq * Wq) one ``patchmatch_noalloc`` call takes (the library's fixed scratch)
+NOALLOC_MAX_QUERIES = 1 << 20
 
 _lib = None
 
@@ -59,6 +62,8 @@ def lib() -> ctypes.CDLL:
     L.scram_patchmatch_workspace_bytes.restype = SZ
     L.scram_patchmatch.argtypes = [P, P, I, I, I, I, I, I, I, I, U64, P, P, I, U32, P, I, I, P, P, P, SZ, P, P]
     L.scram_patchmatch.restype = I
+    L.scram_patchmatch_noalloc.argtypes = [P, P, I, I, I, I, I, I, I, I, U64, P, P, I, U32, P, I, I, P, P, P, P]
+    L.scram_patchmatch_noalloc.restype = I
     L.scram_sparse_attend.argtypes = [P, P, P, I, P, I, I, I, I, I, I, I, I, I, ctypes.c_float, U32, P, P, P]
     L.scram_sparse_attend.restype = I
     L.scram_sparse_attend_backward.argtypes = [P, P, P, I, P, I, I, I, I, I, I, I, I, I, ctypes.c_float, U32, P, P,
@@ -216,6 +221,26 @@ def patchmatch(Q, K, iters: int, seed: int, *, init=None, init_score=None, t0: i
     objects, stamped with the start and end of each launch (init, then each
     sweep).
     """
+    return _patchmatch(False, Q, K, iters, seed, init, init_score, t0, flags, prev, sep, causal, out, score_out,
+                       workspace, return_score, events)
+
+
+def patchmatch_noalloc(Q, K, iters: int, seed: int, *, init=None, init_score=None, t0: int = 1, flags: int = 0,
+                       prev=None, sep: int = 1, causal: bool = False, out=None, score_out=None,
+                       return_score: bool = False, events=None):
+    """:func:`patchmatch` through ``scram_patchmatch_noalloc``: the library call allocates nothing (its
+    buffers are the library's fixed per-GPU scratch), for at most ``NOALLOC_MAX_QUERIES`` queries.
+
+    Calls that may overlap in time on one GPU race on that scratch.  Pass ``out`` (and ``score_out``)
+    and channel counts the kernels take (16, 32, 64, 128) for a call in which this wrapper allocates
+    nothing either.
+    """
+    return _patchmatch(True, Q, K, iters, seed, init, init_score, t0, flags, prev, sep, causal, out, score_out,
+                       None, return_score, events)
+
+
+def _patchmatch(noalloc, Q, K, iters, seed, init, init_score, t0, flags, prev, sep, causal, out, score_out,
+                workspace, return_score, events):
     torch = _torch()
     _dev_tensor(Q, "Q", 4)
     _dev_tensor(K, "K", 4)
@@ -250,16 +275,22 @@ def patchmatch(Q, K, iters: int, seed: int, *, init=None, init_score=None, t0: i
         flags |= CAUSAL
     d = _native_width(d)
     Q, K = _pad_channels(Q, d), _pad_channels(K, d)
-    workspace = _workspace(workspace, patchmatch_workspace_bytes(S, Hq, Wq), dev)
     ev = None if events is None else _event_array(events, 2 * (int(iters) + 1))
-    with _on(dev):
-            rc = lib().scram_patchmatch(_ptr(Q), _ptr(K), _dtype_code(Q), S, Hq, Wq, Hk, Wk, d, int(iters),
-                                    ctypes.c_uint64(int(seed) & 0xFFFFFFFFFFFFFFFF), _ptr(init), _ptr(init_score),
-                                    int(t0), int(flags), _ptr(prev), int(n_prev), int(sep), _ptr(out),
-                                    _ptr(score_out), _ptr(workspace), workspace.numel() * workspace.element_size(), ev,
-                                    _stream(dev))
-    if rc != 0:
-        raise ScramError(rc, "scram_patchmatch")
+    args = (_ptr(Q), _ptr(K), _dtype_code(Q), S, Hq, Wq, Hk, Wk, d, int(iters),
+            ctypes.c_uint64(int(seed) & 0xFFFFFFFFFFFFFFFF), _ptr(init), _ptr(init_score), int(t0), int(flags),
+            _ptr(prev), int(n_prev), int(sep), _ptr(out), _ptr(score_out))
+    if noalloc:
+        with _on(dev):
+            rc = lib().scram_patchmatch_noalloc(*args, ev, _stream(dev))
+        if rc != 0:
+            raise ScramError(rc, "scram_patchmatch_noalloc")
+    else:
+        workspace = _workspace(workspace, patchmatch_workspace_bytes(S, Hq, Wq), dev)
+        with _on(dev):
+            rc = lib().scram_patchmatch(*args, _ptr(workspace), workspace.numel() * workspace.element_size(), ev,
+                                        _stream(dev))
+        if rc != 0:
+            raise ScramError(rc, "scram_patchmatch")
     return (out, score_out) if return_score else out
 
 

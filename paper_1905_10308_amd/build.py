@@ -16,7 +16,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB_DIR = os.path.join(HERE, "_lib")
 LIB_PATH = os.path.join(LIB_DIR, "libscram.so")
 SOURCES = [os.path.join(CSRC, f) for f in ("scram_pm.hip", "scram_attend.hip", "scram_backward.hip", "scram_snis.hip",
-                                             "scram_api.cpp")]
+                                             "scram_noalloc.hip", "scram_api.cpp")]
 ARCH = "gfx950"
 
 COMPILE_FLAGS = [

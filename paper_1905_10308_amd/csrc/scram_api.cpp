@@ -57,6 +57,56 @@ int check_type(int dtype, int d)
 
 }  // namespace
 
+namespace scram {
+
+// Every check of scram_patchmatch's arguments, on the host (no HIP call).  A
+// null workspace is the library's own scratch (scram_patchmatch_noalloc):
+// its presence, size and overlap are then not checked here.
+int patchmatch_check(const void* Q, const void* K, int dtype, int S, int Hq, int Wq, int Hk, int Wk, int d,
+                     int iters, const int32_t* init, const float* init_score, int t0, uint32_t flags,
+                     const int32_t* prev, int n_prev, int sep, const int32_t* argmax_out, const float* score_out,
+                     const void* workspace, size_t workspace_bytes)
+{
+    if (!Q || !K || !argmax_out) return SCRAM_ERR_NULL;
+    if (n_prev > 0 && !prev) return SCRAM_ERR_NULL;
+    int rc = check_grid(S, Hq, Wq, Hk, Wk);
+    if (rc) return rc;
+    if (iters < 0 || t0 < 1 || int64_t(t0) + iters > int64_t(0xFFFFFFFFu)) return SCRAM_ERR_SHAPE;
+    if (n_prev < 0 || n_prev > SCRAM_MAX_PREV || sep < 1) return SCRAM_ERR_SHAPE;
+    if ((rc = check_type(dtype, d))) return rc;
+    if (patchmatch_max_blocks(dtype, Grid{S, Hq, Wq, Hk, Wk, d}) > kMaxBlocks) return SCRAM_ERR_SHAPE;
+    if (flags & ~uint32_t(SCRAM_PM_NO_PROPAGATION | SCRAM_PM_NO_RANDOM_SEARCH | SCRAM_CAUSAL))
+        return SCRAM_ERR_UNSUPPORTED;
+    const bool causal = (flags & SCRAM_CAUSAL) != 0;
+    if (causal && (Hq != Hk || Wq != Wk)) return SCRAM_ERR_SHAPE;
+    if (!init) init_score = nullptr;
+    if (n_prev == 0) prev = nullptr;
+    if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(argmax_out, 4) || (workspace && !aligned(workspace, 256)) ||
+        (score_out && !aligned(score_out, 4)) || (init && !aligned(init, 4)) ||
+        (init_score && !aligned(init_score, 4)) || (prev && !aligned(prev, 4)))
+        return SCRAM_ERR_ALIGN;
+    const size_t n = size_t(S) * Hq * Wq;
+    const size_t need = scram_patchmatch_workspace_bytes(S, Hq, Wq);
+    if (workspace && workspace_bytes < need) return SCRAM_ERR_WORKSPACE;
+
+    const size_t eb = elem_bytes(dtype);
+    const Range rQ = range(Q, n * d * eb), rK = range(K, size_t(S) * Hk * Wk * d * eb);
+    const Range rJ = range(argmax_out, 4 * n), rW = workspace ? range(workspace, need) : Range{0, 0};
+    const Range rS = score_out ? range(score_out, 4 * n) : Range{0, 0};
+    const Range rI = init ? range(init, 4 * n) : Range{0, 0};
+    const Range rIS = init_score ? range(init_score, 4 * n) : Range{0, 0};
+    const Range rP = prev ? range(prev, 4 * n * size_t(n_prev)) : Range{0, 0};
+    for (const Range& out : {rJ, rS, rW}) {
+        for (const Range& other : {rQ, rK, rI, rIS, rP}) {
+            if (overlap(out, other)) return SCRAM_ERR_ALIAS;
+        }
+    }
+    if (overlap(rJ, rS) || overlap(rJ, rW) || overlap(rS, rW)) return SCRAM_ERR_ALIAS;
+    return SCRAM_OK;
+}
+
+}  // namespace scram
+
 extern "C" {
 
 size_t scram_patchmatch_workspace_bytes(int S, int Hq, int Wq)
@@ -73,42 +123,14 @@ int scram_patchmatch(const void* Q, const void* K, int dtype, int S, int Hq, int
                      hipStream_t stream)
 {
     // ---- validation (no HIP call above this line) ----
-    if (!Q || !K || !argmax_out) return SCRAM_ERR_NULL;
-    if (n_prev > 0 && !prev) return SCRAM_ERR_NULL;
-    if (!workspace) return SCRAM_ERR_WORKSPACE;
-    int rc = check_grid(S, Hq, Wq, Hk, Wk);
+    if (Q && K && argmax_out && !(n_prev > 0 && !prev) && !workspace) return SCRAM_ERR_WORKSPACE;
+    int rc = scram::patchmatch_check(Q, K, dtype, S, Hq, Wq, Hk, Wk, d, iters, init, init_score, t0, flags, prev,
+                                     n_prev, sep, argmax_out, score_out, workspace, workspace_bytes);
     if (rc) return rc;
-    if (iters < 0 || t0 < 1 || int64_t(t0) + iters > int64_t(0xFFFFFFFFu)) return SCRAM_ERR_SHAPE;
-    if (n_prev < 0 || n_prev > SCRAM_MAX_PREV || sep < 1) return SCRAM_ERR_SHAPE;
-    if ((rc = check_type(dtype, d))) return rc;
-    if (scram::patchmatch_max_blocks(dtype, scram::Grid{S, Hq, Wq, Hk, Wk, d}) > kMaxBlocks) return SCRAM_ERR_SHAPE;
-    if (flags & ~uint32_t(SCRAM_PM_NO_PROPAGATION | SCRAM_PM_NO_RANDOM_SEARCH | SCRAM_CAUSAL))
-        return SCRAM_ERR_UNSUPPORTED;
     const bool causal = (flags & SCRAM_CAUSAL) != 0;
-    if (causal && (Hq != Hk || Wq != Wk)) return SCRAM_ERR_SHAPE;
     if (!init) init_score = nullptr;
     if (n_prev == 0) prev = nullptr;
-    if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(argmax_out, 4) || !aligned(workspace, 256) ||
-        (score_out && !aligned(score_out, 4)) || (init && !aligned(init, 4)) ||
-        (init_score && !aligned(init_score, 4)) || (prev && !aligned(prev, 4)))
-        return SCRAM_ERR_ALIGN;
     const size_t n = size_t(S) * Hq * Wq;
-    const size_t need = scram_patchmatch_workspace_bytes(S, Hq, Wq);
-    if (workspace_bytes < need) return SCRAM_ERR_WORKSPACE;
-
-    const size_t eb = elem_bytes(dtype);
-    const Range rQ = range(Q, n * d * eb), rK = range(K, size_t(S) * Hk * Wk * d * eb);
-    const Range rJ = range(argmax_out, 4 * n), rW = range(workspace, need);
-    const Range rS = score_out ? range(score_out, 4 * n) : Range{0, 0};
-    const Range rI = init ? range(init, 4 * n) : Range{0, 0};
-    const Range rIS = init_score ? range(init_score, 4 * n) : Range{0, 0};
-    const Range rP = prev ? range(prev, 4 * n * size_t(n_prev)) : Range{0, 0};
-    for (const Range& out : {rJ, rS, rW}) {
-        for (const Range& other : {rQ, rK, rI, rIS, rP}) {
-            if (overlap(out, other)) return SCRAM_ERR_ALIAS;
-        }
-    }
-    if (overlap(rJ, rS) || overlap(rJ, rW) || overlap(rS, rW)) return SCRAM_ERR_ALIAS;
 
     // ---- plan the ping-pong buffers ----
     // The map after sweep k (k = 0 is the initial map) lives in buffer
@@ -308,6 +330,7 @@ const char* scram_status_string(int status)
         case SCRAM_ERR_ALIAS: return "an output overlaps an input or another output";
         case SCRAM_ERR_HIP: return "a HIP launch or copy failed";
         case SCRAM_ERR_WORKSPACE: return "workspace missing or too small";
+        case SCRAM_ERR_SCRATCH: return "more queries than the no-allocation entry point's fixed scratch holds";
         default: return "unknown status";
     }
 }

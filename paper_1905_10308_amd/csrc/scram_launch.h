@@ -22,6 +22,13 @@ struct RunSpec {
     bool causal;
 };
 
+// Host-side validation of scram_patchmatch's arguments (no HIP call); a null
+// workspace stands for the library's own scratch and is not checked.
+int patchmatch_check(const void* Q, const void* K, int dtype, int S, int Hq, int Wq, int Hk, int Wk, int d,
+                     int iters, const int32_t* init, const float* init_score, int t0, uint32_t flags,
+                     const int32_t* prev, int n_prev, int sep, const int32_t* argmax_out, const float* score_out,
+                     const void* workspace, size_t workspace_bytes);
+
 // Every launch takes optional start/stop events that the dispatch itself
 // stamps with the kernel's start and end times (null: plain launch).
 

@@ -12,7 +12,7 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "scram.h")
 
-OK, ENULL, ESHAPE, EUNSUP, EALIGN, EALIAS, EHIP, EWS = 0, -1, -2, -3, -4, -5, -6, -7
+OK, ENULL, ESHAPE, EUNSUP, EALIGN, EALIAS, EHIP, EWS, ESCRATCH = 0, -1, -2, -3, -4, -5, -6, -7, -8
 F32, BF16 = 0, 1
 
 # fake, well-aligned, non-overlapping "device" addresses (never dereferenced)
@@ -41,7 +41,7 @@ def declared_functions():
 def test_header_declares_entry_points():
     names = declared_functions()
     for n in ("scram_patchmatch", "scram_sparse_attend", "scram_snis_attend", "scram_sparse_attend_backward",
-              "scram_patchmatch_workspace_bytes",
+              "scram_patchmatch_workspace_bytes", "scram_patchmatch_noalloc",
               "scram_status_string", "scram_abi_version"):
         assert n in names
 
@@ -52,16 +52,16 @@ def test_library_exports_every_declared_symbol(L):
 
 
 def test_abi_version(L):
-    assert L.scram_abi_version() == (2 << 16) | 5
+    assert L.scram_abi_version() == (2 << 16) | 6
 
 
 def test_status_strings(L):
     seen = set()
-    for code in (OK, ENULL, ESHAPE, EUNSUP, EALIGN, EALIAS, EHIP, EWS):
+    for code in (OK, ENULL, ESHAPE, EUNSUP, EALIGN, EALIAS, EHIP, EWS, ESCRATCH):
         s = L.scram_status_string(code).decode()
         assert s and s != "unknown status"
         seen.add(s)
-    assert len(seen) == 8
+    assert len(seen) == 9
     assert L.scram_status_string(12345).decode() == "unknown status"
 
 
@@ -91,6 +91,31 @@ def at(L, **kw):
     return L.scram_sparse_attend(a["Q"], a["K"], a["V"], a["dtype"], a["J"], a["kappa"], a["S"], a["Hq"], a["Wq"],
                                  a["Hk"], a["Wk"], a["d"], a["dv"], a["window"], a["scale"], a["flags"], a["out"],
                                  None, None)
+
+
+def pm_noalloc(L, **kw):
+    a = dict(Q=A_Q, K=A_K, dtype=F32, S=2, Hq=8, Wq=8, Hk=8, Wk=8, d=16, iters=2, seed=1, init=None,
+             init_score=None, t0=1, flags=0, prev=None, n_prev=0, sep=1, out=A_J, score=A_S)
+    a.update(kw)
+    return L.scram_patchmatch_noalloc(a["Q"], a["K"], a["dtype"], a["S"], a["Hq"], a["Wq"], a["Hk"], a["Wk"], a["d"],
+                                      a["iters"], a["seed"], a["init"], a["init_score"], a["t0"], a["flags"],
+                                      a["prev"], a["n_prev"], a["sep"], a["out"], a["score"], None, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(Q=None), ENULL), (dict(out=None), ENULL), (dict(n_prev=1), ENULL),
+    (dict(S=0), ESHAPE), (dict(t0=0), ESHAPE), (dict(sep=0), ESHAPE), (dict(flags=CAUSAL, Hk=4), ESHAPE),
+    (dict(d=48), EUNSUP), (dict(flags=8), EUNSUP),
+    (dict(Q=A_Q + 8), EALIGN), (dict(score=A_S + 1), EALIGN),
+    (dict(out=A_Q), EALIAS), (dict(init=A_J), EALIAS),
+    # one query past the fixed scratch (2^20 queries), square and ragged, and far past it
+    (dict(S=4, Hq=512, Wq=513, Hk=4, Wk=4), ESCRATCH), (dict(S=1, Hq=1, Wq=(1 << 20) + 1, Hk=4, Wk=4), ESCRATCH),
+    (dict(S=2, Hq=1024, Wq=1024, Hk=4, Wk=4), ESCRATCH),
+])
+def test_patchmatch_noalloc_rejects(L, kw, code):
+    """The no-allocation variant checks every argument on the host, its scratch limit among them, before it
+    looks up the scratch's device address (no HIP call here, no GPU needed)."""
+    assert pm_noalloc(L, **kw) == code
 
 
 @pytest.mark.parametrize("kw,code", [
