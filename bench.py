@@ -20,9 +20,11 @@ GPU (independent slices would shard across GPUs with no communication).
 from __future__ import annotations
 
 import argparse
+import csv
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -32,9 +34,20 @@ if ROOT not in sys.path:
 
 METRIC = "queries/sec (PatchMatch argmax + sparse attend), 256×256 grid d=64; HBM GB/s"
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, public spec
-# sources of the sweep kernel: its traffic figures hold only while these are unchanged
-KERNEL_SRCS = [os.path.join(ROOT, "paper_1905_10308_amd", "csrc", f) for f in ("scram_device.h", "scram_pm.hip")]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pm_iter_traffic.json")
+BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, public spec
+CSRC = os.path.join(ROOT, "paper_1905_10308_amd", "csrc")
+# the sources of each timed kernel: its traffic record holds only while they are unchanged
+KERNEL_SRCS = {
+    "pm_iter": ("scram_device.h", "scram_pm.hip"),
+    "attend": ("scram_device.h", "scram_attend.hip"),
+}
+# how each timed kernel appears in a rocprofv3 trace (its function name)
+KERNEL_NAMES = {
+    "pm_iter": re.compile(r"::pm_iter_kernel<"),
+    "attend": re.compile(r"::attend(_window)?_kernel<"),
+}
+COPY_NAME = re.compile(r"neg_kernel")  # the known-size reference kernel of --copy-calibration (torch.neg)
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
 def pm_bytes_per_query_sweep(cfg, n_prev: int = 0) -> int:
@@ -58,25 +71,119 @@ def snis_bytes_per_query(cfg, samples: int, kappa: int = 1) -> int:
     return row * (2 + 2 * samples) + 4 * kappa
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(kernel: str = "pm_iter") -> str:
     h = hashlib.sha256()
-    for path in KERNEL_SRCS:
-        with open(path, "rb") as f:
+    for name in KERNEL_SRCS[kernel]:
+        with open(os.path.join(CSRC, name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def load_traffic(cfg):
-    """Measured bytes past L2 per sweep launch (copy-calibrated FETCH_SIZE + WRITE_SIZE), if
-    they were taken on the current kernel source and this workload; else None."""
+def load_traffic(cfg, kernel: str = "pm_iter"):
+    """The measured traffic record of ``kernel`` on this workload -- bytes past L2 per launch from
+    copy-calibrated FETCH_SIZE + WRITE_SIZE -- if it was taken on the kernel's current source; else None."""
     try:
         with open(TRAFFIC_FILE) as f:
-            t = json.load(f)
-    except (OSError, ValueError):
+            records = json.load(f)["records"]
+    except (OSError, ValueError, KeyError):
         return None
-    if t.get("kernel_source_sha256_16") != kernel_source_hash() or t.get("workload") != cfg.name:
-        return None
-    return t.get("hbm_bytes_per_launch")
+    for r in records:
+        if r.get("workload") == cfg.name and r.get("kernel") == kernel and \
+                r.get("kernel_source_sha256_16") == kernel_source_hash(kernel):
+            return r
+    return None
+
+
+def _per_dispatch(path, counter):
+    """{dispatch id: (kernel name, summed counter value)} from a rocprofv3 counter-collection CSV."""
+    out = {}
+    with open(path, newline="") as f:
+        for row in csv.DictReader(f):
+            if row["Counter_Name"] != counter:
+                continue
+            d = row["Dispatch_Id"]
+            name, v = out.get(d, (row["Kernel_Name"], 0.0))
+            out[d] = (name, v + float(row["Counter_Value"]))
+    return out
+
+
+def record_traffic(cfg, fetch_csv: str, write_csv: str, stats_csv: str | None, copy_mib: int) -> list:
+    """Turn two rocprofv3 --pmc runs of this bench (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch) into
+    traffic records of the timed kernels, written to ``profiles/traffic.json``.
+
+    Each counter is scaled by what it reads for the --copy-calibration kernel, which reads and writes
+    exactly ``copy_mib`` MiB; a kernel's bytes per launch are the mean over its dispatches.  With the
+    --kernel-trace --stats CSV of the same command, the rocprof mean duration is kept beside them."""
+    fetch, write = _per_dispatch(fetch_csv, "FETCH_SIZE"), _per_dispatch(write_csv, "WRITE_SIZE")
+
+    def mean_of(table, pattern):
+        vals = [v for name, v in table.values() if pattern.search(name)]
+        if not vals:
+            raise ValueError(f"no dispatch of {pattern.pattern} in the counter file")
+        return sum(vals) / len(vals), len(vals)
+
+    (cf, _), (cw, _) = mean_of(fetch, COPY_NAME), mean_of(write, COPY_NAME)
+    fs, ws = copy_mib * 1024 / cf, copy_mib * 1024 / cw
+    stats = {}
+    if stats_csv:
+        with open(stats_csv, newline="") as f:
+            for row in csv.DictReader(f):
+                for k, pat in KERNEL_NAMES.items():
+                    if pat.search(row["Name"]):
+                        calls, tot = stats.get(k, (0, 0.0))
+                        stats[k] = (calls + int(row["Calls"]), tot + float(row["TotalDurationNs"]))
+    new = []
+    for k, pat in KERNEL_NAMES.items():
+        try:
+            (f_kib, nf), (w_kib, nw) = mean_of(fetch, pat), mean_of(write, pat)
+        except ValueError:
+            continue
+        rec = {"workload": cfg.name, "kernel": k, "kernel_source_sha256_16": kernel_source_hash(k),
+               "bytes_per_launch": (f_kib * fs + w_kib * ws) * 1024, "read_bytes_per_launch": f_kib * fs * 1024,
+               "write_bytes_per_launch": w_kib * ws * 1024, "dispatches": [nf, nw], "fetch_scale": fs,
+               "write_scale": ws}
+        if k in stats:
+            rec["rocprof_avg_ns"] = stats[k][1] / stats[k][0]
+        new.append(rec)
+    try:
+        with open(TRAFFIC_FILE) as f:
+            records = json.load(f)["records"]
+    except (OSError, ValueError, KeyError):
+        records = []
+    keep = [r for r in records if (r.get("workload"), r.get("kernel")) not in {(n["workload"], n["kernel"]) for n in new}]
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump({"note": "bytes past L2 per launch: FETCH_SIZE and WRITE_SIZE (KiB per dispatch) scaled by "
+                           "their reading for a copy of known size; written by bench.py --record-traffic",
+                   "records": keep + new}, f, indent=1)
+        f.write("\n")
+    return new
+
+
+def roofline_entry(cfg, kernel: str, launch_ms: float, requested_bytes: float, with_traffic: bool) -> dict:
+    """The HBM roofline of one kernel: measured bytes past L2 per launch (its traffic record) over the
+    live mean launch time, against the 8 TB/s peak.  The bytes past L2 include Infinity-Cache hits, so
+    actual HBM bytes are at most these and the fraction cannot exceed 1 by more than counter noise.  The
+    requested bytes (every row the algorithm names, the nominal count) are reported beside them: they
+    are mostly served by the L1 and L2 caches, so their rate is a cache-level figure, not an HBM one."""
+    rec = load_traffic(cfg, kernel) if with_traffic else None
+    measured = None if rec is None else rec["bytes_per_launch"]
+    achieved = None if measured is None else measured / (launch_ms * 1e-3) / 1e9
+    return {
+        "bound": "hbm",
+        "kernel": kernel,
+        "achieved": achieved,
+        "peak": HBM_PEAK_GBPS,
+        "unit": "GB/s",
+        "frac": None if achieved is None else achieved / HBM_PEAK_GBPS,
+        "traffic": achieved,
+        "traffic_bytes_per_launch": measured,
+        "launch_ms": launch_ms,
+        "rocprof_launch_ms": None if rec is None or "rocprof_avg_ns" not in rec else rec["rocprof_avg_ns"] * 1e-6,
+        "requested_bytes_per_launch": requested_bytes,
+        "requested_GBps": requested_bytes / (launch_ms * 1e-3) / 1e9,
+        "basis": "achieved = bytes past L2 per launch (copy-calibrated FETCH_SIZE + WRITE_SIZE, "
+                 "profiles/traffic.json, tied to the kernel's source hash) / live mean launch time",
+    }
 
 
 def map_quality(cfg, Q, K, J, per_slice: int = 4096, seed: int = 3):
@@ -95,11 +202,12 @@ def map_quality(cfg, Q, K, J, per_slice: int = 4096, seed: int = 3):
         q = Q[s].reshape(plane, cfg.d)[ids].double()
         kt = K[s].reshape(nk, cfg.d).double().t().contiguous()
         jm = J[s].reshape(plane)[ids].long()
-        for c0 in range(0, ids.numel(), 1024):
-            sc = q[c0:c0 + 1024] @ kt
+        step = max(1, min(1024, (1 << 27) // nk))  # score rows per product: at most 1 GiB of fp64 scores
+        for c0 in range(0, ids.numel(), step):
+            sc = q[c0:c0 + step] @ kt
             best, arg = sc.max(dim=1)
-            mine = sc.gather(1, jm[c0:c0 + 1024, None]).squeeze(1)
-            hits += int((arg == jm[c0:c0 + 1024]).sum())
+            mine = sc.gather(1, jm[c0:c0 + step, None]).squeeze(1)
+            hits += int((arg == jm[c0:c0 + step]).sum())
             total += arg.numel()
             pos = best > 0
             ratios.append(mine[pos] / best[pos])
@@ -108,48 +216,69 @@ def map_quality(cfg, Q, K, J, per_slice: int = 4096, seed: int = 3):
                       "products on the GPU"}
 
 
-def cpu_baseline(cfg, arrays, min_s: float, kappa: int = 1, sep: int = 1, causal: bool = False, snis=None):
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(cfg, arrays, min_s: float, kappa: int = 1, sep: int = 1, causal: bool = False, snis=None,
+                 threads: int | None = None):
     """The fp64 oracle on the host cores, on whole slices of the same workload.
 
     Slices are run in turn (wrapping around) until at least ``min_s`` seconds
     of oracle work have been timed, so the rate is stable but the run bounded.
+    ``threads`` sets the oracle's OpenMP thread count for this run (default:
+    what the runtime gives it, i.e. OMP_NUM_THREADS or every core).
     """
     import numpy as np
 
     import oracle
 
-    threads = oracle.num_threads()
+    before = oracle.num_threads()
+    if threads is not None:
+        oracle.set_num_threads(threads)
+    used = oracle.num_threads()
     flags = oracle.CAUSAL if causal else 0
     Q, K, V = (arrays[k].astype(np.float64) for k in ("Q", "K", "V"))
     done_q, elapsed, runs, scored = 0, 0.0, 0, 0
     per_slice = cfg.Hq * cfg.Wq
-    while elapsed < min_s and runs < 64 * cfg.S:
-        s = runs % cfg.S
-        t0 = time.perf_counter()
-        maps = []  # kappa constrained runs; the oracle counts the valid candidates it scores
-        for _ in range(kappa):
-            J1, _, _, ncand = oracle.patchmatch(Q[s:s + 1], K[s:s + 1], cfg.iters, cfg.pm_seed, flags=flags,
-                                                prev=np.stack(maps) if maps else None, sep=sep)
-            maps.append(J1)
-            scored += ncand
-        J = np.stack(maps)
-        if snis:
-            T, alpha, radius = snis
-            oracle.snis(Q[s:s + 1], K[s:s + 1], V[s:s + 1], J, T, alpha, radius, cfg.scale, cfg.pm_seed, flags=flags)
-        else:
-            oracle.sparse_attend(Q[s:s + 1], K[s:s + 1], V[s:s + 1], J, cfg.window, cfg.scale, flags=flags)
-        elapsed += time.perf_counter() - t0
-        done_q += per_slice
-        runs += 1
+    try:
+        while elapsed < min_s and runs < 64 * cfg.S:
+            s = runs % cfg.S
+            t0 = time.perf_counter()
+            maps = []  # kappa constrained runs; the oracle counts the valid candidates it scores
+            for _ in range(kappa):
+                J1, _, _, ncand = oracle.patchmatch(Q[s:s + 1], K[s:s + 1], cfg.iters, cfg.pm_seed, flags=flags,
+                                                    prev=np.stack(maps) if maps else None, sep=sep)
+                maps.append(J1)
+                scored += ncand
+            J = np.stack(maps)
+            if snis:
+                T, alpha, radius = snis
+                oracle.snis(Q[s:s + 1], K[s:s + 1], V[s:s + 1], J, T, alpha, radius, cfg.scale, cfg.pm_seed,
+                            flags=flags)
+            else:
+                oracle.sparse_attend(Q[s:s + 1], K[s:s + 1], V[s:s + 1], J, cfg.window, cfg.scale, flags=flags)
+            elapsed += time.perf_counter() - t0
+            done_q += per_slice
+            runs += 1
+    finally:
+        oracle.set_num_threads(before)
     return {
         "value": done_q / elapsed,
         "unit": "queries/s",
-        "cores": threads,
+        "cores": used,
         "kind": "oracle",
         "candidates_per_query_sweep": scored / (done_q * kappa * cfg.iters),
         "sample": f"{runs} slice passes over the {cfg.S}-slice workload ({done_q} queries; {kappa} x {cfg.iters} "
                   f"sweeps + " + (f"{snis[0]}-sample SNIS" if snis else f"{cfg.window}x{cfg.window} attend")
-                  + f" each), fp64, {elapsed:.1f} s",
+                  + f" each), fp64, {used} thread{'s' if used > 1 else ''}, {elapsed:.1f} s",
     }
 
 
@@ -172,10 +301,13 @@ def copy_bandwidth(device, mib: int = 1024, reps: int = 10) -> float:
     return gbps
 
 
-def dense_attention(cfg, Q, K, V, reps: int = 3):
+def dense_attention(cfg, Q, K, V, reps: int | None = None):
     """Dense exact softmax attention over the same slices, for scale: torch's
-    scaled-dot-product attention restricted to its fused (flash / memory
-    efficient) kernels, so no n x n matrix is formed.  None if neither runs."""
+    scaled-dot-product attention restricted in turn to each of its fused
+    kernels (flash, memory efficient), so no n x n matrix is formed.  Each
+    backend that runs is timed; the fastest is the comparator.  Its matrix
+    work is 4 * S * nq * nk * d flops (QK^T and PV), reported against the
+    bf16 matrix-core peak.  None if no backend runs."""
     import torch
     from torch.nn.attention import SDPBackend, sdpa_kernel
 
@@ -183,7 +315,11 @@ def dense_attention(cfg, Q, K, V, reps: int = 3):
     q = Q.reshape(S, 1, n, cfg.d).contiguous()
     k = K.reshape(S, 1, cfg.Hk * cfg.Wk, cfg.d).contiguous()
     v = V.reshape(S, 1, cfg.Hk * cfg.Wk, cfg.dv).contiguous()
-    for backend in (SDPBackend.EFFICIENT_ATTENTION, SDPBackend.FLASH_ATTENTION):
+    flops = 4.0 * S * n * cfg.Hk * cfg.Wk * cfg.d
+    if reps is None:
+        reps = 1 if flops > 1e15 else 3  # seconds per call on the largest grids
+    timed = {}
+    for backend in (SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION):
         try:
             with sdpa_kernel([backend]):
                 torch.nn.functional.scaled_dot_product_attention(q, k, v, scale=cfg.scale)
@@ -194,11 +330,22 @@ def dense_attention(cfg, Q, K, V, reps: int = 3):
                     torch.nn.functional.scaled_dot_product_attention(q, k, v, scale=cfg.scale)
                 stop.record()
                 torch.cuda.synchronize()
-            return {"ms": start.elapsed_time(stop) / reps, "backend": f"torch SDPA {backend.name.lower()}",
-                    "dtype": str(q.dtype).replace("torch.", "")}
         except RuntimeError:
             continue
-    return None
+        ms = start.elapsed_time(stop) / reps
+        tflops = flops / (ms * 1e-3) / 1e12
+        timed[backend.name.lower()] = {"ms": ms, "TFLOPs": tflops,
+                                       "frac_of_bf16_mfma_peak": tflops / BF16_MFMA_PEAK_TFLOPS}
+    if not timed:
+        return None
+    best = min(timed, key=lambda b: timed[b]["ms"])
+    return {"ms": timed[best]["ms"], "backend": f"torch SDPA {best}", "dtype": str(q.dtype).replace("torch.", ""),
+            "flops": flops, "backends": timed}
+
+
+def progress(msg: str) -> None:
+    """A progress line on stderr (stdout carries only the JSON line)."""
+    print(f"bench.py: {msg}", file=sys.stderr, flush=True)
 
 
 def main(argv=None) -> int:
@@ -206,7 +353,9 @@ def main(argv=None) -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=None, help="workload index (default: the 256x256 bf16 one)")
+    ap.add_argument("--config", default=None,
+                    help="workload index or name (default: the 256x256 bf16 one; large2048_bf16: one 2048x2048 "
+                         "slice whose working set exceeds the Infinity Cache)")
     ap.add_argument("--kappa", type=int, default=1, help="matches per query (constrained PatchMatch runs)")
     ap.add_argument("--sep", type=int, default=1, help="separation between the runs' matches (Chebyshev)")
     ap.add_argument("--causal", action="store_true", help="mask keys after each query (raster order)")
@@ -218,12 +367,31 @@ def main(argv=None) -> int:
     ap.add_argument("--alpha", type=float, default=0.9, help="SNIS mixture weight of the local densities")
     ap.add_argument("--radius", type=int, default=4, help="SNIS binomial radius m (variance m/2)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="seconds of oracle work for the CPU baseline")
+    ap.add_argument("--cpu-seconds-1t", type=float, default=3.0,
+                    help="seconds of single-thread oracle work for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="before timing, run one plain device copy of this many MiB (a known-size "
                          "reference kernel for hardware byte counters)")
+    ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="no benchmark: write the traffic records of the workload's timed kernels from the "
+                         "counter CSVs of two rocprofv3 --pmc runs of this bench (FETCH_SIZE, then WRITE_SIZE, "
+                         "both with --copy-calibration MIB) into profiles/traffic.json")
+    ap.add_argument("--stats-csv", default=None,
+                    help="with --record-traffic: the kernel_stats CSV of a --kernel-trace --stats run of the "
+                         "same command, whose mean kernel durations are kept in the record")
     args = ap.parse_args(argv)
 
+    if args.record_traffic:
+        import scram_inputs as si
+
+        if args.copy_calibration <= 0:
+            print("bench.py: --record-traffic needs the --copy-calibration MIB of the profiled runs", file=sys.stderr)
+            return 2
+        cfg = si.get(si.HEADLINE if args.config is None else args.config)
+        for r in record_traffic(cfg, *args.record_traffic, args.stats_csv, args.copy_calibration):
+            print(json.dumps(r), flush=True)
+        return 0
     if args.gpus != 1:
         print(f"bench.py: this path runs on one GPU; --gpus {args.gpus} is not supported "
               "(slices are independent and would shard across GPUs without communication)", file=sys.stderr)
@@ -250,9 +418,10 @@ def main(argv=None) -> int:
         torch.neg(src, out=dst)
         torch.cuda.synchronize()
         del src, dst
-    ci = si.HEADLINE if args.config is None else args.config
-    cfg = si.get(ci)
+    cfg = si.get(si.HEADLINE if args.config is None else args.config)
+    progress(f"generating {cfg.describe()}")
     data = si.make(cfg, device="cuda")
+    progress("inputs resident; timing")
     Q, K, V = data["Q"], data["K"], data["V"]
     S, Hq, Wq = cfg.S, cfg.Hq, cfg.Wq
     dev = Q.device
@@ -352,10 +521,9 @@ def main(argv=None) -> int:
     # the dominant kernel: the sweep, averaged over the runs (run c reads c previous maps)
     pm_launch_bytes = nq * sum(pm_bytes_per_query_sweep(cfg, c) for c in range(kappa)) / kappa
     att_bytes = nq * (snis_bytes_per_query(cfg, args.snis, kappa) if args.snis else attend_bytes_per_query(cfg, kappa))
-    achieved = pm_launch_bytes / (iter_ms * 1e-3) / 1e9
     default_path = kappa == 1 and not causal and not args.snis
-    traffic_bytes = load_traffic(cfg) if default_path else None
-    traffic = None if traffic_bytes is None else traffic_bytes / (iter_ms * 1e-3) / 1e9
+    roof = roofline_entry(cfg, "pm_iter", iter_ms, pm_launch_bytes, default_path)
+    att_roof = roofline_entry(cfg, "attend", att_ms, att_bytes, default_path)
 
     res = {
         "metric": METRIC,
@@ -368,7 +536,8 @@ def main(argv=None) -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": cfg.dtype,
+        "accumulate": "f32",
         "data": "synthetic",
         "config": {
             "workload": cfg.name,
@@ -388,41 +557,41 @@ def main(argv=None) -> int:
             "launch": "hip graph replay" if args.graph else "eager",
             "queries_per_step": nq,
         },
-        "roofline": {
-            "bound": "hbm",
-            "kernel": "pm_iter",
-            "achieved": achieved,
-            "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": traffic,
-            "traffic_bytes_per_launch": traffic_bytes,
-            "algorithmic_bytes_per_launch": pm_launch_bytes,
-        },
+        "roofline": roof,
+        "attend_roofline": att_roof,
         "kernels_ms": {"pm_iter": iter_ms, "attend": att_ms, **bwd},
         "pm_init": "fused into the first sweep",
         "pm_iter_ms_by_run": iter_by_run,
         "kernels_ms_source": "dispatch-stamped HIP events, timed region B",
-        "attend_GBps": att_bytes / (att_ms * 1e-3) / 1e9,
         "candidate_evals_per_s_nominal": kappa * nq * T * cfg.candidates / (ms_step * 1e-3),
-        "step_GBps": (T * kappa * pm_launch_bytes + att_bytes) / (ms_step * 1e-3) / 1e9,
+        "step_requested_GBps": (T * kappa * pm_launch_bytes + att_bytes) / (ms_step * 1e-3) / 1e9,
         "hbm_copy_GBps": copy_bandwidth(dev),
         "wall_ms_per_step": wall * 1e3 / args.steps,
         "device": torch.cuda.get_device_name(dev),
     }
+    progress("timed regions done; comparators")
     if kappa == 1 and not causal:
         res["map_quality"] = map_quality(cfg, Q, K, J[0])
     dense = dense_attention(cfg, Q, K, V) if not (kappa > 1 or causal or args.snis) else None
     if dense is not None:
         dense["step_speedup"] = dense["ms"] / ms_step
         res["dense_exact_attention"] = dense
-    if not args.no_cpu_baseline:
-        base = cpu_baseline(cfg, data["np"], args.cpu_seconds, kappa, sep, causal,
-                            (args.snis, args.alpha, args.radius) if args.snis else None)
+    if not args.no_cpu_baseline and cfg.Hq * cfg.Wq > (1 << 18):
+        # one slice pass of the oracle would take minutes on one thread
+        res["cpu_baseline"] = None
+        res["cpu_baseline_skipped"] = f"{cfg.Hq}x{cfg.Wq} slices: one oracle pass exceeds the bounded sample"
+    elif not args.no_cpu_baseline:
+        progress("oracle on the host cores")
+        snis_opt = (args.snis, args.alpha, args.radius) if args.snis else None
+        base = cpu_baseline(cfg, data["np"], args.cpu_seconds, kappa, sep, causal, snis_opt)
+        one = cpu_baseline(cfg, data["np"], args.cpu_seconds_1t, kappa, sep, causal, snis_opt, threads=1)
         # valid candidates per query-sweep as the oracle counts them on its sample (duplicates included)
         per_sweep = base.pop("candidates_per_query_sweep")
+        one.pop("candidates_per_query_sweep")
         res["candidate_evals_per_s"] = kappa * nq * T * per_sweep / (ms_step * 1e-3)
         res["candidates_per_query_sweep"] = per_sweep
+        base["cpu_model"] = cpu_model()
+        base["single_thread"] = one
         res["cpu_baseline"] = base
     print(json.dumps(res), flush=True)
     return 0

@@ -23,5 +23,5 @@ Recipe (all numpy, fp32, deterministic from ``data_seed``):
 """
 from __future__ import annotations
 
-from .configs import CONFIGS, HEADLINE, Workload, get  # noqa: F401
+from .configs import CONFIGS, EXTRA, HEADLINE, Workload, get  # noqa: F401
 from .synth import make, make_arrays  # noqa: F401

@@ -88,6 +88,20 @@ CONFIGS = [
 #: the headline workload (256x256 grid, d = 64, bf16 storage, 4 slices)
 HEADLINE = 3
 
+#: Measurement-only workloads (not parity cases): one 2048 x 2048 slice with the headline's
+#: generator, d, storage, sweeps and window.  Q, K and V are 512 MiB each, so the working set
+#: (1.5 GiB) is far past the 256 MB Infinity Cache and HBM serves the gathers.
+EXTRA = [
+    Workload("large2048_bf16", 1, 1, 2048, 2048, 2048, 2048, 64, "bf16", sigma=6, F=128, iters=7, window=5,
+             outlier_frac=0.05, data_seed=1005),
+]
 
-def get(i: int) -> Workload:
-    return CONFIGS[i]
+
+def get(i) -> Workload:
+    """A workload by index into CONFIGS, or by name (CONFIGS and EXTRA)."""
+    if isinstance(i, str) and not i.isdigit():
+        for w in CONFIGS + EXTRA:
+            if w.name == i:
+                return w
+        raise KeyError(f"no workload named {i!r}")
+    return CONFIGS[int(i)]

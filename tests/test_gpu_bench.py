@@ -1,7 +1,7 @@
 """bench.py's JSON line on the GPU: every field of the contract, with numbers that agree with each other.
 
-Runs the headline 256x256 bf16 workload for two timed steps with a short CPU-baseline sample (the
-traffic figure is only attached to that workload), and the 32x32 workload for the
+Runs the headline 256x256 bf16 workload for two timed steps with short CPU-baseline samples (the
+traffic figures are attached to the workloads they were measured on), and the 32x32 workload for the
 several-match and causal options.
 """
 import json
@@ -32,20 +32,30 @@ def run(capsys, *argv):
 
 
 def test_headline_line_has_the_contract_fields(capsys):
-    d = run(capsys, "--steps", "2", "--warmup", "1", "--cpu-seconds", "0.5")
+    d = run(capsys, "--steps", "2", "--warmup", "1", "--cpu-seconds", "0.5", "--cpu-seconds-1t", "0.5")
     for k in TOP:
         assert k in d, k
     assert d["n_gpus"] == 1 and d["steps"] == 2 and d["warmup"] == 1 and d["unit"] == "queries/s"
     assert d["config"]["workload"] == "self256_bf16"
     assert d["value"] == pytest.approx(d["config"]["queries_per_step"] / (d["ms_per_step"] * 1e-3))
-    r = d["roofline"]
-    assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
-    assert r["frac"] == pytest.approx(r["achieved"] / r["peak"])
-    assert r["achieved"] == pytest.approx(r["algorithmic_bytes_per_launch"] / (d["kernels_ms"]["pm_iter"] * 1e-3) / 1e9)
-    # the traffic figure is present while the committed counters match the sweep's sources
-    assert r["traffic"] is None or r["traffic"] > 0
+    assert d["dtype"] == "bf16" and d["accumulate"] == "f32"
+    for key, kernel in (("roofline", "pm_iter"), ("attend_roofline", "attend")):
+        r = d[key]
+        assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0 and r["kernel"] == kernel
+        assert r["requested_GBps"] == pytest.approx(
+            r["requested_bytes_per_launch"] / (d["kernels_ms"][kernel] * 1e-3) / 1e9)
+        # measured bytes past L2 while the committed counters match the kernel's sources: a real fraction
+        if r["achieved"] is not None:
+            assert r["frac"] == pytest.approx(r["achieved"] / r["peak"]) and 0 < r["frac"] <= 1.05
+            assert r["achieved"] == pytest.approx(r["traffic_bytes_per_launch"] / (r["launch_ms"] * 1e-3) / 1e9)
+        else:
+            assert r["frac"] is None
     c = d["cpu_baseline"]
-    assert c["kind"] == "oracle" and c["cores"] >= 1 and c["value"] > 0 and c["sample"]
+    assert c["kind"] == "oracle" and c["cores"] >= 1 and c["value"] > 0 and c["sample"] and c["cpu_model"]
+    one = c["single_thread"]
+    assert one["cores"] == 1 and one["value"] > 0
+    dense = d["dense_exact_attention"]
+    assert dense["ms"] == min(b["ms"] for b in dense["backends"].values())
     q = d["map_quality"]
     assert 0.5 < q["recall_vs_exact_argmax"] <= 1 and 0.9 < q["mean_score_ratio"] <= 1 + 1e-12
     assert all(math.isfinite(v) and v > 0 for v in d["kernels_ms"].values())
@@ -56,6 +66,7 @@ def test_option_lines(capsys, opts):
     d = run(capsys, "--config", "0", "--steps", "2", "--warmup", "1", "--no-cpu-baseline", *opts)
     for k in TOP[:-1]:
         assert k in d, k
-    assert d["value"] > 0 and d["roofline"]["traffic"] is None  # traffic belongs to the default headline path
+    # traffic records belong to the default path of the workloads they were taken on
+    assert d["value"] > 0 and d["roofline"]["traffic"] is None and d["attend_roofline"]["frac"] is None
     if "--backward" in opts:
         assert {"backward_scan_fill", "backward_query", "backward_key_side"} <= set(d["kernels_ms"])
