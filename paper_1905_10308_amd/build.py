@@ -31,6 +31,9 @@ COMPILE_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
 LINK_FLAGS = [f"--offload-arch={ARCH}", "-shared", "-fPIC"]
+# per-source additions: the attend step's matrix-core kernel keeps its accumulators in VGPRs (the
+# compiler would otherwise copy them between AGPRs and VGPRs around every rescale)
+EXTRA_FLAGS = {"scram_attend.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def hipcc() -> str:
@@ -52,7 +55,8 @@ def build(verbose: bool = False) -> str:
     jobs = []
     for src in SOURCES:
         obj = os.path.join(obj_dir, os.path.splitext(os.path.basename(src))[0] + ".o")
-        cmd = [hipcc(), *COMPILE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", src, "-o", obj]
+        cmd = [hipcc(), *COMPILE_FLAGS, *EXTRA_FLAGS.get(os.path.basename(src), []), f"-I{INCLUDE}", f"-I{CSRC}",
+               "-c", src, "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         jobs.append((obj, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)))

@@ -21,6 +21,7 @@ struct AttParams {
     int causal;           // drop keys after the query (raster order)
     int Hq, Wq;
     Tiling tq;            // blocks -> tiles of the query grid (set per storage type and width)
+    int rc;               // cluster radius of the tile kernel (Chebyshev, between match centres)
 };
 
 // ---------------------------------------------------------------------------
@@ -215,6 +216,341 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
     store_row<T, D, G>(p.out, g, lane, acc, l > 0.f ? 1.f / l : 0.f);  // an empty set gives a zero row
 }
 
+
+// ---------------------------------------------------------------------------
+// K4 on the matrix cores (bf16 storage, one window per query, no mask)
+// ---------------------------------------------------------------------------
+// A wave takes a 4 x 4 tile of queries (16 on an 8 x 8 block tile; 16
+// consecutive items of narrower tiles).  Neighbouring queries' windows
+// overlap -- the matches of a coherent region are a shifted copy of it -- so
+// the wave reads each key and value row of the union of its 16 windows once
+// instead of once per query: the queries' match centres are grouped into
+// clusters (a query joins the cluster of the first unassigned query whose
+// centre lies within Chebyshev distance rc), and each cluster's key box (its
+// members' windows, clipped to the grid) is visited in blocks of 16 keys in
+// raster order.  A block's rows are gathered a row per 4 consecutive lanes
+// (whole 64-byte spans per load, as in the lane-group kernels), staged in the
+// wave's LDS tile and read back in the operand layout of the products, while
+// the next block's rows load.  Per block (lane (m, g4) = lane (l mod 16,
+// l div 16)):
+//   S^T = K_blk Q^T          keys x queries, 16x16x32 bf16 products over the
+//                            channels; lane holds keys 4 g4 + i, query m
+//   p = 2^(scale log2e s - m_ref) for the keys of the query's own window in
+//                            its own cluster, 0 otherwise
+//   O^T += V_blk^T P^T       channels x queries, 16x16x16 bf16 products over
+//                            the block's 16 keys: V_blk^T comes out of products
+//                            of the row fragments with identity blocks (exact
+//                            for bf16 values) in exactly the lane layout of
+//                            P^T, and P enters as two bf16 parts (top 8
+//                            significant bits, then the top 8 of the rest), so
+//                            its relative error is below 2^-16
+// The softmax reference of a query is raised (and its sums rescaled) only
+// when a score passes it by more than kRescaleSlack, as in the other kernels;
+// every query is in exactly one cluster, and each key of its window is in
+// that cluster's box exactly once, so the weights are those of the window.
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// bf16 pair (a in the low half, b in the high half) from the high halves of two fp32 patterns
+__device__ __forceinline__ uint32_t hi16_pair(uint32_t a, uint32_t b) { return __builtin_amdgcn_perm(b, a, 0x07060302u); }
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int x)
+{
+    return __builtin_amdgcn_mov_dpp(x, CTRL, 0xF, 0xF, true);
+}
+
+// min and max over the 16 lanes of a DPP row (every lane of the row gets both)
+__device__ __forceinline__ void row_minmax(int& lo, int& hi)
+{
+    lo = min(lo, dpp_i<0xB1>(lo)), hi = max(hi, dpp_i<0xB1>(hi));
+    lo = min(lo, dpp_i<0x4E>(lo)), hi = max(hi, dpp_i<0x4E>(hi));
+    lo = min(lo, dpp_i<0x141>(lo)), hi = max(hi, dpp_i<0x141>(hi));
+    lo = min(lo, dpp_i<0x140>(lo)), hi = max(hi, dpp_i<0x140>(hi));
+}
+
+// (row, column) of raster slot j of a box `bw` wide: exact for j < 1024 and
+// bw <= 31 (the fraction of (j + 1/2) / bw stays 1/(2 bw) away from an
+// integer, far more than the float error of the product)
+__device__ __forceinline__ void box_slot(int j, int bw, float inv_bw, int& r, int& c)
+{
+    r = static_cast<int>((static_cast<float>(j) + 0.5f) * inv_bw);
+    c = j - r * bw;
+}
+
+// LDS written by some lanes of a wave and then read by others: keep the
+// compiler from moving accesses across this point (a wave's LDS instructions
+// execute in order)
+__device__ __forceinline__ void wave_lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+
+template <int D, int W>
+__global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
+{
+    constexpr int B = W / 2;
+    constexpr int kDs = D / 32;        // 32-channel contraction steps of S^T
+    constexpr int kOt = D / 16;        // 16-channel tiles of O^T
+    constexpr int kRowB = 2 * D + 16;  // LDS row stride: the 16-byte pad spreads a column read over the banks
+    constexpr int kPer = D / 32;       // 16-byte pieces per lane: a row (D / 8 pieces) is read by 4 consecutive lanes
+    constexpr int kWaves = kBlock / 64;
+    __shared__ __align__(16) unsigned char s_k[kWaves][16 * kRowB], s_v[kWaves][16 * kRowB];
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int m = lane & 15, g4 = lane >> 4;
+    const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+    // this lane's query m: a 4 x 4 quarter of an 8 x 8 block tile, else 16 consecutive items
+    const uint32_t item = p.tq.lw == 3 ? ((4u * (wave >> 1) + (m >> 2)) << 3) + 4u * (wave & 1) + (m & 3)
+                                       : 16u * wave + m;
+    uint32_t g, g0;
+    const bool valid = tile_item<kBlock / 4>(p.tq, blk, item, g);
+    tile_item<kBlock / 4>(p.tq, blk, 0, g0);  // item 0 of a tile is always inside the grid
+    const uint32_t gq = valid ? g : g0;
+    uint32_t s, rem;
+    divmod(gq, p.div_plane, s, rem);
+    const size_t slice = static_cast<size_t>(s) * p.nkeys;
+    const uint16_t* const Ks = static_cast<const uint16_t*>(p.K) + slice * D;
+    const uint16_t* const Vs = static_cast<const uint16_t*>(p.V) + slice * D;
+    int u, v;
+    {
+        uint32_t uu, vv;
+        divmod(static_cast<uint32_t>(clamp_index(p.J[gq], p.nkeys)), p.div_wk, uu, vv);
+        u = static_cast<int>(uu);
+        v = static_cast<int>(vv);
+    }
+    // B operand of S^T: query m, channels 32 ds + 8 g4 .. + 7
+    bf16x8_t qf[kDs];
+    const uint16_t* const qrow = static_cast<const uint16_t*>(p.Q) + static_cast<size_t>(gq) * D;
+#pragma unroll
+    for (int ds = 0; ds < kDs; ++ds)
+        qf[ds] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(qrow + 32 * ds + 8 * g4));
+
+    // ---- clusters of the 16 match centres and their key boxes ----
+    // Cluster c's box (rows r0 .. r0 + height - 1, columns c0 .. c0 + width - 1, `nb` blocks of 16 raster
+    // slots) is held by lane c of these registers and read back with readlane.
+    int t_r0 = 0, t_c0 = 0, t_bw = 1, t_h = 0;
+    int nclu = 0, mine = -1;
+    uint32_t todo = static_cast<uint32_t>(__ballot(valid)) & 0xFFFFu;  // bit m: query m (lanes 16.. repeat 0..15)
+    while (todo) {
+        const int a = __builtin_ctz(todo);
+        const int ua = __builtin_amdgcn_readlane(u, a), va = __builtin_amdgcn_readlane(v, a);
+        const bool mem = ((todo >> m) & 1u) && abs(u - ua) <= p.rc && abs(v - va) <= p.rc;
+        todo &= ~(static_cast<uint32_t>(__ballot(mem)) & 0xFFFFu);
+        mine = mem ? nclu : mine;
+        int ulo = mem ? u : ua, uhi = ulo, vlo = mem ? v : va, vhi = vlo;
+        row_minmax(ulo, uhi);
+        row_minmax(vlo, vhi);
+        const bool here = lane == nclu;
+        t_r0 = here ? max(ulo - B, 0) : t_r0;
+        t_c0 = here ? max(vlo - B, 0) : t_c0;
+        t_h = here ? min(uhi + B, p.Hk - 1) - max(ulo - B, 0) + 1 : t_h;
+        t_bw = here ? min(vhi + B, p.Wk - 1) - max(vlo - B, 0) + 1 : t_bw;
+        ++nclu;
+    }
+    // the window of query m in its cluster's box: rows wr0 .. wr0 + wrn, and a bit per box column
+    int wr0 = 0, wrn = -1;
+    uint32_t wcols = 0;
+    {
+        const int mc = max(mine, 0);
+        const int r0 = __shfl(t_r0, mc), c0 = __shfl(t_c0, mc), bw = __shfl(t_bw, mc), h = __shfl(t_h, mc);
+        if (mine >= 0) {
+            wr0 = u - B - r0;
+            wrn = min(u + B - r0, h - 1) - wr0;
+            const int lo = max(v - B - c0, 0), hi = min(v + B - c0, bw - 1);  // box columns, bw <= 31
+            wcols = ((2u << hi) - 1u) & ~((1u << lo) - 1u);
+        }
+    }
+
+    // identity blocks: I_h[k][n] = (k == 16 h + n), lane (n, g4) holding k = 8 g4 .. 8 g4 + 7
+    bf16x8_t eye[2];
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) {
+        eye[0][kk] = static_cast<__bf16>(8 * g4 + kk == m ? 1.f : 0.f);
+        eye[1][kk] = static_cast<__bf16>(8 * g4 + kk == 16 + m ? 1.f : 0.f);
+    }
+    const f32x4_t zero = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    f32x4_t acc[kOt];
+#pragma unroll
+    for (int o = 0; o < kOt; ++o) acc[o] = zero;
+    float mref = -INFINITY, lsum = 0.f;
+
+    // ---- the clusters' blocks of 16 keys, one at a time; the next block's rows load during this one's
+    // products.  Block k of a cluster holds raster slots 16 k .. 16 k + 15 of its box; its 16 key rows and
+    // 16 value rows are read a row per 4 consecutive lanes, staged in this wave's LDS tile and read back in
+    // the products' operand layout.
+    const int lslot = lane >> 2, lpiece = lane & 3;  // every lane: one key slot, 16-byte pieces lpiece (+ 4)
+    static_assert(kPer == 1 || kPer == 2, "32 or 64 channels");
+    uint4 kr0, kr1, vr0, vr1;
+    auto fetch = [&](uint32_t key) {
+        const uint16_t* const kp = Ks + static_cast<size_t>(key) * D + 8 * lpiece;
+        const uint16_t* const vp = Vs + static_cast<size_t>(key) * D + 8 * lpiece;
+        kr0 = *reinterpret_cast<const uint4*>(kp);
+        vr0 = *reinterpret_cast<const uint4*>(vp);
+        if constexpr (kPer == 2) {
+            kr1 = *reinterpret_cast<const uint4*>(kp + 32);
+            vr1 = *reinterpret_cast<const uint4*>(vp + 32);
+        }
+    };
+    // A cluster's scalars; (r, c) of raster slot j of its box, and the step of 16 slots with its carry.
+    struct Box {
+        int r0, c0, bw, h, nb, q16, r16;
+        float inv;
+    };
+    auto box_of = [&](int cl) {
+        Box bx;
+        bx.r0 = __builtin_amdgcn_readlane(t_r0, cl);
+        bx.c0 = __builtin_amdgcn_readlane(t_c0, cl);
+        bx.bw = __builtin_amdgcn_readlane(t_bw, cl);
+        bx.h = __builtin_amdgcn_readlane(t_h, cl);
+        bx.nb = (bx.h * bx.bw + 15) >> 4;
+        bx.q16 = 16 / bx.bw;
+        bx.r16 = 16 - bx.q16 * bx.bw;
+        bx.inv = __builtin_amdgcn_rcpf(static_cast<float>(bx.bw));
+        return bx;
+    };
+    auto step16 = [](const Box& bx, int& r, int& c) {  // slot j -> slot j + 16
+        c += bx.r16;
+        const bool carry = c >= bx.bw;
+        c -= carry ? bx.bw : 0;
+        r += bx.q16 + (carry ? 1 : 0);
+    };
+    auto key_at = [&](const Box& bx, int r, int c) {  // past the box's last row: its first key (weight 0)
+        const uint32_t key = r < bx.h ? static_cast<uint32_t>(bx.r0 + r) * static_cast<uint32_t>(p.Wk) + (bx.c0 + c)
+                                      : static_cast<uint32_t>(bx.r0) * static_cast<uint32_t>(p.Wk) + bx.c0;
+        return min(key, p.nkeys - 1u);  // (the clamp is a guard only)
+    };
+    if (nclu > 0) {
+        Box nbx = box_of(0);  // the box of the block being fetched
+        int lr, lc;           // this lane's load slot of that block
+        box_slot(lslot, nbx.bw, nbx.inv, lr, lc);
+        fetch(key_at(nbx, lr, lc));
+        unsigned char* const tk = s_k[wave];
+        unsigned char* const tv = s_v[wave];
+        for (int c = 0; c < nclu; ++c) {
+            const Box bx = nbx;
+            const bool here = c == mine;
+            int mr, mcl;  // slot 16 k + 4 g4 of this lane's score rows
+            box_slot(4 * g4, bx.bw, bx.inv, mr, mcl);
+            for (int k = 0; k < bx.nb; ++k) {
+                {
+                    const int off = lslot * kRowB + 16 * lpiece;
+                    *reinterpret_cast<uint4*>(tk + off) = kr0;
+                    *reinterpret_cast<uint4*>(tv + off) = vr0;
+                    if constexpr (kPer == 2) {
+                        *reinterpret_cast<uint4*>(tk + off + 64) = kr1;
+                        *reinterpret_cast<uint4*>(tv + off + 64) = vr1;
+                    }
+                }
+                // the next block: the rest of this cluster's, then the next cluster's first
+                if (k + 1 < bx.nb) {
+                    step16(bx, lr, lc);
+                    fetch(key_at(bx, lr, lc));
+                } else if (c + 1 < nclu) {
+                    nbx = box_of(c + 1);
+                    box_slot(lslot, nbx.bw, nbx.inv, lr, lc);
+                    fetch(key_at(nbx, lr, lc));
+                }
+                wave_lds_sync();
+
+                // S^T of this block: lane holds keys 4 g4 + i (slots 16 k + 4 g4 + i) for query m
+                f32x4_t sc = zero;
+#pragma unroll
+                for (int ds = 0; ds < kDs; ++ds) {
+                    const bf16x8_t kf = __builtin_bit_cast(
+                        bf16x8_t, *reinterpret_cast<const uint4*>(tk + m * kRowB + 16 * (4 * ds + g4)));
+                    sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ds], sc, 0, 0, 0);
+                }
+                // which of the 4 slots lie in query m's window (bit i: slot 16 k + 4 g4 + i)
+                uint32_t bits = 0;
+                if (bx.bw >= 4) {  // the 4 slots span at most two box rows
+                    const int na = min(4, bx.bw - mcl);
+                    const uint32_t first = (1u << na) - 1u;
+                    const bool ok0 = static_cast<unsigned>(mr - wr0) <= static_cast<unsigned>(wrn);
+                    const bool ok1 = static_cast<unsigned>(mr + 1 - wr0) <= static_cast<unsigned>(wrn);
+                    bits = (ok0 ? (wcols >> mcl) & first : 0u) | (ok1 ? (wcols << na) & 0xFu & ~first : 0u);
+                } else {  // narrow boxes (grids narrower than the window): slot by slot
+                    int r = mr, cc = mcl;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const bool ok = static_cast<unsigned>(r - wr0) <= static_cast<unsigned>(wrn) &&
+                                        ((wcols >> cc) & 1u);
+                        bits |= ok ? 1u << i : 0u;
+                        ++cc;
+                        const bool wrap = cc == bx.bw;
+                        cc = wrap ? 0 : cc;
+                        r += wrap ? 1 : 0;
+                    }
+                }
+                bits = here ? bits : 0u;
+                float sv[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) sv[i] = (bits >> i) & 1u ? sc[i] * p.scale_log2e : -INFINITY;
+                float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+                if (__ballot(mx > mref + kRescaleSlack)) {  // some query passes its reference: raise it
+                    mx = fmaxf(mx, __shfl_xor(mx, 16));
+                    mx = fmaxf(mx, __shfl_xor(mx, 32));
+                    if (mx > mref + kRescaleSlack) {
+                        const float alpha = __builtin_amdgcn_exp2f(mref - mx);  // 0 on the first raise
+                        lsum *= alpha;
+#pragma unroll
+                        for (int o = 0; o < kOt; ++o) acc[o] *= alpha;
+                        mref = mx;
+                    }
+                }
+                const float mref0 = mref == -INFINITY ? 0.f : mref;  // no key of this query yet: every weight is 0
+                uint32_t ph[4], pl[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float pk = __builtin_amdgcn_exp2f(sv[i] - mref0);  // exp2(-inf) = 0
+                    lsum += pk;
+                    ph[i] = __float_as_uint(pk) & 0xFFFF0000u;
+                    pl[i] = __float_as_uint(pk - __uint_as_float(ph[i]));
+                }
+                const bf16x4_t pth =
+                    __builtin_bit_cast(bf16x4_t, make_uint2(hi16_pair(ph[0], ph[1]), hi16_pair(ph[2], ph[3])));
+                const bf16x4_t ptl =
+                    __builtin_bit_cast(bf16x4_t, make_uint2(hi16_pair(pl[0], pl[1]), hi16_pair(pl[2], pl[3])));
+#pragma unroll
+                for (int ds = 0; ds < kDs; ++ds) {
+                    const bf16x8_t vf = __builtin_bit_cast(
+                        bf16x8_t, *reinterpret_cast<const uint4*>(tv + m * kRowB + 16 * (4 * ds + g4)));
+#pragma unroll
+                    for (int hh = 0; hh < 2; ++hh) {
+                        const int o = 2 * ds + hh;
+                        // lane: value rows 4 g4 + i of the block at channel 16 o + m, as bf16 (exact)
+                        const f32x4_t t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, eye[hh], zero, 0, 0, 0);
+                        const bf16x4_t vt = __builtin_bit_cast(
+                            bf16x4_t, make_uint2(hi16_pair(__float_as_uint(t[0]), __float_as_uint(t[1])),
+                                                 hi16_pair(__float_as_uint(t[2]), __float_as_uint(t[3]))));
+                        acc[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, pth, acc[o], 0, 0, 0);
+                        acc[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, ptl, acc[o], 0, 0, 0);
+                    }
+                }
+                step16(bx, mr, mcl);
+                wave_lds_sync();  // this block's LDS reads come before the next block's writes
+            }
+        }
+    }
+    float lt = lsum;
+    lt += __shfl_xor(lt, 16);
+    lt += __shfl_xor(lt, 32);
+    if (!valid) return;
+    const float inv = lt > 0.f ? 1.f / lt : 0.f;
+    // lane holds channels 16 o + 4 g4 + i of query m
+    uint16_t* const orow = static_cast<uint16_t*>(p.out) + static_cast<size_t>(g) * D;
+#pragma unroll
+    for (int o = 0; o < kOt; ++o) {
+        const uint32_t w0 = f32_to_bf16_rne(acc[o][0] * inv) | (f32_to_bf16_rne(acc[o][1] * inv) << 16);
+        const uint32_t w1 = f32_to_bf16_rne(acc[o][2] * inv) | (f32_to_bf16_rne(acc[o][3] * inv) << 16);
+        *reinterpret_cast<uint2*>(orow + 16 * o + 4 * g4) = make_uint2(w0, w1);
+    }
+}
+
 template <typename T, int D, int MK>
 hipError_t run_attend_m(const AttParams& p, int window, uint64_t blocks, hipStream_t st, hipEvent_t e0,
                         hipEvent_t e1)
@@ -229,11 +565,32 @@ hipError_t run_attend_m(const AttParams& p, int window, uint64_t blocks, hipStre
     }
 }
 
+// The matrix-core kernel takes bf16 storage with 32 or 64 channels, one
+// window of side 3, 5 or 7 per query and no mask; the lane-group kernels
+// take every other call.
+#ifndef SCRAM_ATTEND_TILE
+#define SCRAM_ATTEND_TILE 1
+#endif
+template <typename T, int D>
+constexpr bool kTileKernel = SCRAM_ATTEND_TILE && std::is_same<T, uint16_t>::value && (D == 32 || D == 64);
+
 template <typename T, int D>
 hipError_t run_attend(const AttParams& p0, int window, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
 {
     constexpr int G = Lanes<T, D>::kAttend;
     AttParams p = p0;
+    if constexpr (kTileKernel<T, D>) {
+        if (p.kappa == 1 && !p.causal && (window == 3 || window == 5 || window == 7)) {
+            p.tq = make_tiling(p.Hq, p.Wq, kBlock / 4);
+            p.rc = 6;  // boxes at most 12 + window wide: slots of a box stay below 1024
+            const uint64_t tiles = tiling_blocks(p.tq, p.n / p.tq.plane);
+            switch (window) {
+                case 3: return launch(attend_tile_kernel<D, 3>, tiles, st, e0, e1, p);
+                case 5: return launch(attend_tile_kernel<D, 5>, tiles, st, e0, e1, p);
+                default: return launch(attend_tile_kernel<D, 7>, tiles, st, e0, e1, p);
+            }
+        }
+    }
     p.tq = make_tiling(p.Hq, p.Wq, Row<T, D, G>::kQpb);
     const uint64_t blocks = tiling_blocks(p.tq, p.n / p.tq.plane);
     // the smallest register budget that holds this call's window centres
@@ -280,7 +637,9 @@ uint64_t attend_max_blocks(int dtype, const Grid& g)
     return dispatch_value(dtype, g.d, uint64_t(0), [&](auto t, auto d) {
         using T = decltype(t);
         constexpr int D = decltype(d)::value;
-        return tiling_blocks(make_tiling(g.Hq, g.Wq, Row<T, D, Lanes<T, D>::kAttend>::kQpb), g.S);
+        const uint64_t lanes = tiling_blocks(make_tiling(g.Hq, g.Wq, Row<T, D, Lanes<T, D>::kAttend>::kQpb), g.S);
+        const uint64_t tiles = kTileKernel<T, D> ? tiling_blocks(make_tiling(g.Hq, g.Wq, kBlock / 4), g.S) : 0;
+        return lanes > tiles ? lanes : tiles;
     });
 }
 

@@ -439,3 +439,53 @@ def test_stable_marks_leave_the_map_unchanged(scram, work, variant):
         J, s = scram.patchmatch(Q, K, 1, cfg.pm_seed, init=J, init_score=s, t0=t, return_score=True, **kw)
     assert torch.equal(whole, J) and torch.equal(sw, s)
     assert int(whole.min()) >= 0 and int(whole.max()) < cfg.Hk * cfg.Wk  # no mark leaks into the result
+
+
+# --------------------------------------------------------------------------
+# the matrix-core attend (bf16, 32 or 64 channels, windows 3/5/7, one map, no mask): maps that stress
+# its clusters of match centres and their key boxes
+# --------------------------------------------------------------------------
+def _tile_maps(S, Hq, Wq, Hk, Wk, rng):
+    xs, ys = np.meshgrid(np.arange(Hq), np.arange(Wq), indexing="ij")
+    cu = np.clip(xs * Hk // max(Hq, 1), 0, Hk - 1)
+    cv = np.clip(ys * Wk // max(Wq, 1), 0, Wk - 1)
+    coherent = np.broadcast_to(cu * Wk + cv, (S, Hq, Wq))
+    maps = {
+        "random": rng.integers(0, Hk * Wk, (S, Hq, Wq)),
+        "constant": np.full((S, Hq, Wq), (Hk // 2) * Wk + Wk // 2),
+        "corner0": np.zeros((S, Hq, Wq)),
+        "corner_last": np.full((S, Hq, Wq), Hk * Wk - 1),
+        "coherent": coherent,
+        # centres on a lattice 6 and 7 apart: exactly at and just past the cluster radius
+        "lattice6": np.broadcast_to(np.clip(xs * 6, 0, Hk - 1) * Wk + np.clip(ys * 6, 0, Wk - 1), (S, Hq, Wq)),
+        "lattice7": np.broadcast_to(np.clip(xs * 7, 0, Hk - 1) * Wk + np.clip(ys * 7, 0, Wk - 1), (S, Hq, Wq)),
+        # two far-apart keys alternating: two clusters in every wave
+        "two_far": np.where((xs + ys) % 2 == 0, 0, Hk * Wk - 1) + np.zeros((S, 1, 1), np.int64),
+        # coherent with 10 % random outliers
+        "outliers": np.where(rng.random((S, Hq, Wq)) < 0.1, rng.integers(0, Hk * Wk, (S, Hq, Wq)), coherent),
+    }
+    return {k: np.ascontiguousarray(v, dtype=np.int32) for k, v in maps.items()}
+
+
+@pytest.mark.parametrize("d", [32, 64])
+@pytest.mark.parametrize("grid", [(2, 37, 45, 37, 45), (1, 8, 8, 8, 8), (1, 1, 50, 1, 50), (1, 50, 1, 50, 1),
+                                  (3, 5, 3, 5, 3), (1, 19, 23, 40, 31), (2, 64, 64, 64, 64)],
+                         ids=lambda g: "x".join(map(str, g)))
+def test_attend_tile_kernel_maps(scram, d, grid):
+    S, Hq, Wq, Hk, Wk = grid
+    rng = np.random.default_rng(Hq * 131 + Wq * 7 + d)
+    Q = rng.standard_normal((S, Hq, Wq, d)).astype(np.float32)
+    K = rng.standard_normal((S, Hk, Wk, d)).astype(np.float32)
+    V = rng.standard_normal((S, Hk, Wk, d)).astype(np.float32)
+    Q, K, V = (to_dev(x, "bf16").float().cpu().numpy() for x in (Q, K, V))  # the bf16 values both sides read
+    dev = [to_dev(x, "bf16") for x in (Q, K, V)]
+    worst = 0.0
+    for name, J in _tile_maps(S, Hq, Wq, Hk, Wk, rng).items():
+        Jd = torch.from_numpy(J).cuda()
+        for window in (3, 5, 7):
+            out = scram.sparse_attend(*dev, Jd, window, d ** -0.5)
+            ref = oracle.sparse_attend(Q, K, V, J, window, d ** -0.5)
+            err = row_rel_err(out.float().cpu().numpy(), ref)
+            worst = max(worst, float(err.max()))
+            assert err.max() <= TOL["bf16"], f"{name} window {window}: {err.max():.3e}"
+    log(f"tile attend {grid} d={d}: max rel err {worst:.3e}")
