@@ -44,7 +44,7 @@ KERNEL_SRCS = {
 # how each timed kernel appears in a rocprofv3 trace (its function name)
 KERNEL_NAMES = {
     "pm_iter": re.compile(r"::pm_iter_kernel<"),
-    "attend": re.compile(r"::attend(_window)?_kernel<"),
+    "attend": re.compile(r"::attend(_window|_tile)?_kernel<"),
 }
 COPY_NAME = re.compile(r"neg_kernel")  # the known-size reference kernel of --copy-calibration (torch.neg)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
