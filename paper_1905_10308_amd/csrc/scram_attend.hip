@@ -366,18 +366,16 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
         }
     }
 
-    // identity blocks: I_h[k][n] = (k == 16 h + n), lane (n, g4) holding k = 8 g4 .. 8 g4 + 7
-    bf16x8_t eye[2];
-#pragma unroll
-    for (int kk = 0; kk < 8; ++kk) {
-        eye[0][kk] = static_cast<__bf16>(8 * g4 + kk == m ? 1.f : 0.f);
-        eye[1][kk] = static_cast<__bf16>(8 * g4 + kk == 16 + m ? 1.f : 0.f);
-    }
     const f32x4_t zero = f32x4_t{0.f, 0.f, 0.f, 0.f};
     f32x4_t acc[kOt];
 #pragma unroll
     for (int o = 0; o < kOt; ++o) acc[o] = zero;
-    float mref = -INFINITY, lsum = 0.f;
+    // the softmax denominators: an all-ones row block times P^T sums P over the keys, for every query
+    f32x4_t lacc = zero;
+    const bf16x4_t ones = bf16x4_t{static_cast<__bf16>(1.f), static_cast<__bf16>(1.f), static_cast<__bf16>(1.f),
+                                   static_cast<__bf16>(1.f)};
+    float mref = -INFINITY;
+    const float sl2e = p.scale_log2e;  // > 0 (the caller routes other scales to the lane-group kernels)
 
     // ---- the clusters' blocks of 16 keys, one at a time; the next block's rows load during this one's
     // products.  Block k of a cluster holds raster slots 16 k .. 16 k + 15 of its box; its 16 key rows and
@@ -487,27 +485,26 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
                     }
                 }
                 bits = here ? bits : 0u;
-                float sv[4];
+                float sv[4];  // raw scores of the window's keys, -inf elsewhere
 #pragma unroll
-                for (int i = 0; i < 4; ++i) sv[i] = (bits >> i) & 1u ? sc[i] * p.scale_log2e : -INFINITY;
-                float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+                for (int i = 0; i < 4; ++i) sv[i] = (bits >> i) & 1u ? sc[i] : -INFINITY;
+                float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])) * sl2e;
                 if (__ballot(mx > mref + kRescaleSlack)) {  // some query passes its reference: raise it
                     mx = fmaxf(mx, __shfl_xor(mx, 16));
                     mx = fmaxf(mx, __shfl_xor(mx, 32));
                     if (mx > mref + kRescaleSlack) {
                         const float alpha = __builtin_amdgcn_exp2f(mref - mx);  // 0 on the first raise
-                        lsum *= alpha;
+                        lacc *= alpha;
 #pragma unroll
                         for (int o = 0; o < kOt; ++o) acc[o] *= alpha;
                         mref = mx;
                     }
                 }
-                const float mref0 = mref == -INFINITY ? 0.f : mref;  // no key of this query yet: every weight is 0
+                const float nref = mref == -INFINITY ? 0.f : -mref;  // no key of this query yet: every weight is 0
                 uint32_t ph[4], pl[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const float pk = __builtin_amdgcn_exp2f(sv[i] - mref0);  // exp2(-inf) = 0
-                    lsum += pk;
+                    const float pk = __builtin_amdgcn_exp2f(fmaf(sv[i], sl2e, nref));  // exp2(-inf) = 0
                     ph[i] = __float_as_uint(pk) & 0xFFFF0000u;
                     pl[i] = __float_as_uint(pk - __uint_as_float(ph[i]));
                 }
@@ -515,38 +512,34 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
                     __builtin_bit_cast(bf16x4_t, make_uint2(hi16_pair(ph[0], ph[1]), hi16_pair(ph[2], ph[3])));
                 const bf16x4_t ptl =
                     __builtin_bit_cast(bf16x4_t, make_uint2(hi16_pair(pl[0], pl[1]), hi16_pair(pl[2], pl[3])));
+                lacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ones, pth, lacc, 0, 0, 0);
+                lacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ones, ptl, lacc, 0, 0, 0);
+                // V_blk^T operand of tile o: lane holds the value rows 4 g4 + i of the block at channel 16 o + m
+                const uint16_t* const tv16 = reinterpret_cast<const uint16_t*>(tv);
 #pragma unroll
-                for (int ds = 0; ds < kDs; ++ds) {
-                    const bf16x8_t vf = __builtin_bit_cast(
-                        bf16x8_t, *reinterpret_cast<const uint4*>(tv + m * kRowB + 16 * (4 * ds + g4)));
-#pragma unroll
-                    for (int hh = 0; hh < 2; ++hh) {
-                        const int o = 2 * ds + hh;
-                        // lane: value rows 4 g4 + i of the block at channel 16 o + m, as bf16 (exact)
-                        const f32x4_t t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, eye[hh], zero, 0, 0, 0);
-                        const bf16x4_t vt = __builtin_bit_cast(
-                            bf16x4_t, make_uint2(hi16_pair(__float_as_uint(t[0]), __float_as_uint(t[1])),
-                                                 hi16_pair(__float_as_uint(t[2]), __float_as_uint(t[3]))));
-                        acc[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, pth, acc[o], 0, 0, 0);
-                        acc[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, ptl, acc[o], 0, 0, 0);
-                    }
+                for (int o = 0; o < kOt; ++o) {
+                    const uint16_t* const col = tv16 + (4 * g4) * (kRowB / 2) + 16 * o + m;
+                    const uint32_t w0 = col[0] | (static_cast<uint32_t>(col[kRowB / 2]) << 16);
+                    const uint32_t w1 = col[kRowB] | (static_cast<uint32_t>(col[3 * (kRowB / 2)]) << 16);
+                    const bf16x4_t vt = __builtin_bit_cast(bf16x4_t, make_uint2(w0, w1));
+                    acc[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, pth, acc[o], 0, 0, 0);
+                    acc[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, ptl, acc[o], 0, 0, 0);
                 }
                 step16(bx, mr, mcl);
                 wave_lds_sync();  // this block's LDS reads come before the next block's writes
             }
         }
     }
-    float lt = lsum;
-    lt += __shfl_xor(lt, 16);
-    lt += __shfl_xor(lt, 32);
     if (!valid) return;
+    const float lt = lacc[0];  // every row of the ones-block product holds query m's sum of weights
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
-    // lane holds channels 16 o + 4 g4 + i of query m
+    // lane holds channels 16 o + 4 g4 + i of query m; bf16 with round to nearest even
     uint16_t* const orow = static_cast<uint16_t*>(p.out) + static_cast<size_t>(g) * D;
+    auto bf = [](float x) { return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(x))); };
 #pragma unroll
     for (int o = 0; o < kOt; ++o) {
-        const uint32_t w0 = f32_to_bf16_rne(acc[o][0] * inv) | (f32_to_bf16_rne(acc[o][1] * inv) << 16);
-        const uint32_t w1 = f32_to_bf16_rne(acc[o][2] * inv) | (f32_to_bf16_rne(acc[o][3] * inv) << 16);
+        const uint32_t w0 = bf(acc[o][0] * inv) | (bf(acc[o][1] * inv) << 16);
+        const uint32_t w1 = bf(acc[o][2] * inv) | (bf(acc[o][3] * inv) << 16);
         *reinterpret_cast<uint2*>(orow + 16 * o + 4 * g4) = make_uint2(w0, w1);
     }
 }
@@ -566,8 +559,8 @@ hipError_t run_attend_m(const AttParams& p, int window, uint64_t blocks, hipStre
 }
 
 // The matrix-core kernel takes bf16 storage with 32 or 64 channels, one
-// window of side 3, 5 or 7 per query and no mask; the lane-group kernels
-// take every other call.
+// window of side 3, 5 or 7 per query, no mask and a positive scale; the
+// lane-group kernels take every other call.
 #ifndef SCRAM_ATTEND_TILE
 #define SCRAM_ATTEND_TILE 1
 #endif
@@ -580,7 +573,7 @@ hipError_t run_attend(const AttParams& p0, int window, hipStream_t st, hipEvent_
     constexpr int G = Lanes<T, D>::kAttend;
     AttParams p = p0;
     if constexpr (kTileKernel<T, D>) {
-        if (p.kappa == 1 && !p.causal && (window == 3 || window == 5 || window == 7)) {
+        if (p.kappa == 1 && !p.causal && (window == 3 || window == 5 || window == 7) && p.scale_log2e > 0.f) {
             p.tq = make_tiling(p.Hq, p.Wq, kBlock / 4);
             p.rc = 6;  // boxes at most 12 + window wide: slots of a box stay below 1024
             const uint64_t tiles = tiling_blocks(p.tq, p.n / p.tq.plane);
