@@ -228,7 +228,11 @@ int scram_patchmatch_noalloc(const void* Q, const void* K, int dtype, int S, int
  * which cannot happen without SCRAM_CAUSAL).
  *
  * Arguments:
- *   Q, K, V   inputs, layouts above; V has dv channels (dv == d)
+ *   Q, K, V   inputs, layouts above; V has dv channels (dv == d); finite
+ *             values (with bf16 storage and d of 32 or 64, the keys of
+ *             neighbouring queries' windows are read in shared blocks in
+ *             which a key outside a query's window has weight 0, and
+ *             0 * inf would reach that query)
  *   argmax    int32 [kappa, S, Hq, Wq] flat key indices (e.g. kappa runs of
  *             scram_patchmatch)
  *   kappa     1 <= kappa <= SCRAM_MAX_KAPPA

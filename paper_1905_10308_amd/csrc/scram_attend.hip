@@ -238,16 +238,19 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
 //   p = 2^(scale log2e s - m_ref) for the keys of the query's own window in
 //                            its own cluster, 0 otherwise
 //   O^T += V_blk^T P^T       channels x queries, 16x16x16 bf16 products over
-//                            the block's 16 keys: V_blk^T comes out of products
-//                            of the row fragments with identity blocks (exact
-//                            for bf16 values) in exactly the lane layout of
-//                            P^T, and P enters as two bf16 parts (top 8
-//                            significant bits, then the top 8 of the rest), so
-//                            its relative error is below 2^-16
+//                            the block's 16 keys: the transposing LDS load
+//                            hands each lane 4 consecutive staged value rows at
+//                            one channel, the operand layout that matches P^T,
+//                            and P enters as two bf16 parts (top 8 significant
+//                            bits, then the top 8 of the rest), so its relative
+//                            error is below 2^-16
 // The softmax reference of a query is raised (and its sums rescaled) only
 // when a score passes it by more than kRescaleSlack, as in the other kernels;
 // every query is in exactly one cluster, and each key of its window is in
 // that cluster's box exactly once, so the weights are those of the window.
+// The other keys of the box enter with weight exactly 0, which leaves the
+// sums unchanged for finite value rows (a non-finite value anywhere in the
+// box would reach every query of the cluster through 0 * inf).
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
@@ -352,6 +355,12 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
         t_bw = here ? min(vhi + B, p.Wk - 1) - max(vlo - B, 0) + 1 : t_bw;
         ++nclu;
     }
+    // the rest of each cluster's scalars, once for all clusters: blocks of 16 slots, and the step of 16
+    // raster slots as q16 rows and r16 columns
+    const float t_inv = __builtin_amdgcn_rcpf(static_cast<float>(t_bw));
+    const int t_nb = (t_h * t_bw + 15) >> 4;
+    int t_q16, t_r16;
+    box_slot(16, t_bw, t_inv, t_q16, t_r16);
     // the window of query m in its cluster's box: rows wr0 .. wr0 + wrn, and a bit per box column
     int wr0 = 0, wrn = -1;
     uint32_t wcols = 0;
@@ -374,8 +383,11 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
     f32x4_t lacc = zero;
     const bf16x4_t ones = bf16x4_t{static_cast<__bf16>(1.f), static_cast<__bf16>(1.f), static_cast<__bf16>(1.f),
                                    static_cast<__bf16>(1.f)};
-    float mref = -INFINITY;
     const float sl2e = p.scale_log2e;  // > 0 (the caller routes other scales to the lane-group kernels)
+    // online softmax state of query m: reference mref (base-2 domain), its negation as the exponent's
+    // offset (0 while no key of the window has been seen), and the raw score above which a block may
+    // raise the reference (a little below the exact test, which decides)
+    float mref = -INFINITY, nref = 0.f, thr = -INFINITY;
 
     // ---- the clusters' blocks of 16 keys, one at a time; the next block's rows load during this one's
     // products.  Block k of a cluster holds raster slots 16 k .. 16 k + 15 of its box; its 16 key rows and
@@ -383,18 +395,14 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
     // the products' operand layout.
     const int lslot = lane >> 2, lpiece = lane & 3;  // every lane: one key slot, 16-byte pieces lpiece (+ 4)
     static_assert(kPer == 1 || kPer == 2, "32 or 64 channels");
-    uint4 kr0, kr1, vr0, vr1;
-    auto fetch = [&](uint32_t key) {
-        const uint16_t* const kp = Ks + static_cast<size_t>(key) * D + 8 * lpiece;
-        const uint16_t* const vp = Vs + static_cast<size_t>(key) * D + 8 * lpiece;
-        kr0 = *reinterpret_cast<const uint4*>(kp);
-        vr0 = *reinterpret_cast<const uint4*>(vp);
-        if constexpr (kPer == 2) {
-            kr1 = *reinterpret_cast<const uint4*>(kp + 32);
-            vr1 = *reinterpret_cast<const uint4*>(vp + 32);
-        }
-    };
-    // A cluster's scalars; (r, c) of raster slot j of its box, and the step of 16 slots with its carry.
+    unsigned char* const tk = s_k[wave];
+    unsigned char* const tv = s_v[wave];
+    // A operand of O^T for tile o, read with the transposing LDS load: in each 16-lane group the load
+    // hands lane i element e of the 8 bytes that lane 4 e + i / 4 addresses, so lane (m, g4) addresses
+    // value row 4 g4 + m / 4 at channels 4 (m mod 4) .. + 3 (+ 16 o) and receives rows 4 g4 .. + 3 at
+    // channel 16 o + m
+    const unsigned char* const tvt = tv + (4 * g4 + (m >> 2)) * kRowB + 8 * (m & 3);
+    // A cluster's scalars, read from the lanes that hold them
     struct Box {
         int r0, c0, bw, h, nb, q16, r16;
         float inv;
@@ -405,10 +413,10 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
         bx.c0 = __builtin_amdgcn_readlane(t_c0, cl);
         bx.bw = __builtin_amdgcn_readlane(t_bw, cl);
         bx.h = __builtin_amdgcn_readlane(t_h, cl);
-        bx.nb = (bx.h * bx.bw + 15) >> 4;
-        bx.q16 = 16 / bx.bw;
-        bx.r16 = 16 - bx.q16 * bx.bw;
-        bx.inv = __builtin_amdgcn_rcpf(static_cast<float>(bx.bw));
+        bx.nb = __builtin_amdgcn_readlane(t_nb, cl);
+        bx.q16 = __builtin_amdgcn_readlane(t_q16, cl);
+        bx.r16 = __builtin_amdgcn_readlane(t_r16, cl);
+        bx.inv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(t_inv), cl));
         return bx;
     };
     auto step16 = [](const Box& bx, int& r, int& c) {  // slot j -> slot j + 16
@@ -417,117 +425,135 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
         c -= carry ? bx.bw : 0;
         r += bx.q16 + (carry ? 1 : 0);
     };
-    auto key_at = [&](const Box& bx, int r, int c) {  // past the box's last row: its first key (weight 0)
-        const uint32_t key = r < bx.h ? static_cast<uint32_t>(bx.r0 + r) * static_cast<uint32_t>(p.Wk) + (bx.c0 + c)
-                                      : static_cast<uint32_t>(bx.r0) * static_cast<uint32_t>(p.Wk) + bx.c0;
-        return min(key, p.nkeys - 1u);  // (the clamp is a guard only)
-    };
-    if (nclu > 0) {
-        Box nbx = box_of(0);  // the box of the block being fetched
-        int lr, lc;           // this lane's load slot of that block
-        box_slot(lslot, nbx.bw, nbx.inv, lr, lc);
-        fetch(key_at(nbx, lr, lc));
-        unsigned char* const tk = s_k[wave];
-        unsigned char* const tv = s_v[wave];
-        for (int c = 0; c < nclu; ++c) {
-            const Box bx = nbx;
-            const bool here = c == mine;
-            int mr, mcl;  // slot 16 k + 4 g4 of this lane's score rows
-            box_slot(4 * g4, bx.bw, bx.inv, mr, mcl);
-            for (int k = 0; k < bx.nb; ++k) {
-                {
-                    const int off = lslot * kRowB + 16 * lpiece;
-                    *reinterpret_cast<uint4*>(tk + off) = kr0;
-                    *reinterpret_cast<uint4*>(tv + off) = vr0;
-                    if constexpr (kPer == 2) {
-                        *reinterpret_cast<uint4*>(tk + off + 64) = kr1;
-                        *reinterpret_cast<uint4*>(tv + off + 64) = vr1;
-                    }
-                }
-                // the next block: the rest of this cluster's, then the next cluster's first
-                if (k + 1 < bx.nb) {
-                    step16(bx, lr, lc);
-                    fetch(key_at(bx, lr, lc));
-                } else if (c + 1 < nclu) {
-                    nbx = box_of(c + 1);
-                    box_slot(lslot, nbx.bw, nbx.inv, lr, lc);
-                    fetch(key_at(nbx, lr, lc));
-                }
-                wave_lds_sync();
 
-                // S^T of this block: lane holds keys 4 g4 + i (slots 16 k + 4 g4 + i) for query m
-                f32x4_t sc = zero;
-#pragma unroll
-                for (int ds = 0; ds < kDs; ++ds) {
-                    const bf16x8_t kf = __builtin_bit_cast(
-                        bf16x8_t, *reinterpret_cast<const uint4*>(tk + m * kRowB + 16 * (4 * ds + g4)));
-                    sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ds], sc, 0, 0, 0);
+    // load cursor: block fk of cluster fc, this lane's load slot (lr, lc) in it; one block ahead
+    int fc = 0, fk = 0, lr = 0, lc = 0;
+    Box fb = box_of(0);
+    uint4 kr0, kr1, vr0, vr1;  // this lane's pieces of the rows in flight
+    auto fetch = [&]() {  // past the box's last row: its first key (weight 0)
+        const uint32_t key0 = static_cast<uint32_t>(fb.r0) * static_cast<uint32_t>(p.Wk) + fb.c0;
+        const uint32_t key = lr < fb.h ? key0 + static_cast<uint32_t>(lr) * static_cast<uint32_t>(p.Wk) + lc : key0;
+        const size_t row = static_cast<size_t>(min(key, p.nkeys - 1u)) * D + 8 * lpiece;  // (the clamp is a guard)
+        kr0 = *reinterpret_cast<const uint4*>(Ks + row);
+        vr0 = *reinterpret_cast<const uint4*>(Vs + row);
+        if constexpr (kPer == 2) {
+            kr1 = *reinterpret_cast<const uint4*>(Ks + row + 32);
+            vr1 = *reinterpret_cast<const uint4*>(Vs + row + 32);
+        }
+        if (++fk < fb.nb) {
+            step16(fb, lr, lc);
+        } else if (++fc < nclu) {
+            fk = 0;
+            fb = box_of(fc);
+            box_slot(lslot, fb.bw, fb.inv, lr, lc);
+        }
+    };
+    // compute cursor: block k of cluster c; slot 16 k + 4 g4 of this lane's scores is box row wr0 + rr,
+    // column mcl; the window's column bits of that row (wc) and of the next one (wc2, shifted past the
+    // row's end), zero outside query m's own cluster
+    int c = 0, k = 0, rr = 0, mcl = 0;
+    uint32_t wc = 0, wc2 = 0;
+    Box bx = fb;
+    auto enter = [&]() {  // the first block of cluster c
+        int mr;
+        box_slot(4 * g4, bx.bw, bx.inv, mr, mcl);
+        rr = mr - wr0;
+        const bool here = c == mine;
+        wc = here ? wcols : 0u;
+        wc2 = here ? wcols << bx.bw : 0u;  // bw <= 19, and only bits below bw + 3 are read
+    };
+
+    if (nclu > 0) {
+        box_slot(lslot, fb.bw, fb.inv, lr, lc);
+        fetch();
+        enter();
+        for (;;) {
+            {
+                const int off = lslot * kRowB + 16 * lpiece;
+                *reinterpret_cast<uint4*>(tk + off) = kr0;
+                *reinterpret_cast<uint4*>(tv + off) = vr0;
+                if constexpr (kPer == 2) {
+                    *reinterpret_cast<uint4*>(tk + off + 64) = kr1;
+                    *reinterpret_cast<uint4*>(tv + off + 64) = vr1;
                 }
-                // which of the 4 slots lie in query m's window (bit i: slot 16 k + 4 g4 + i)
-                uint32_t bits = 0;
-                if (bx.bw >= 4) {  // the 4 slots span at most two box rows
-                    const int na = min(4, bx.bw - mcl);
-                    const uint32_t first = (1u << na) - 1u;
-                    const bool ok0 = static_cast<unsigned>(mr - wr0) <= static_cast<unsigned>(wrn);
-                    const bool ok1 = static_cast<unsigned>(mr + 1 - wr0) <= static_cast<unsigned>(wrn);
-                    bits = (ok0 ? (wcols >> mcl) & first : 0u) | (ok1 ? (wcols << na) & 0xFu & ~first : 0u);
-                } else {  // narrow boxes (grids narrower than the window): slot by slot
-                    int r = mr, cc = mcl;
+            }
+            const bool last = fc >= nclu;
+            if (!last) fetch();
+            wave_lds_sync();
+
+            // S^T of this block: lane holds keys 4 g4 + i (slots 16 k + 4 g4 + i) for query m
+            f32x4_t sc = zero;
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const bool ok = static_cast<unsigned>(r - wr0) <= static_cast<unsigned>(wrn) &&
-                                        ((wcols >> cc) & 1u);
-                        bits |= ok ? 1u << i : 0u;
-                        ++cc;
-                        const bool wrap = cc == bx.bw;
-                        cc = wrap ? 0 : cc;
-                        r += wrap ? 1 : 0;
-                    }
-                }
-                bits = here ? bits : 0u;
-                float sv[4];  // raw scores of the window's keys, -inf elsewhere
-#pragma unroll
-                for (int i = 0; i < 4; ++i) sv[i] = (bits >> i) & 1u ? sc[i] : -INFINITY;
-                float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])) * sl2e;
-                if (__ballot(mx > mref + kRescaleSlack)) {  // some query passes its reference: raise it
-                    mx = fmaxf(mx, __shfl_xor(mx, 16));
-                    mx = fmaxf(mx, __shfl_xor(mx, 32));
-                    if (mx > mref + kRescaleSlack) {
-                        const float alpha = __builtin_amdgcn_exp2f(mref - mx);  // 0 on the first raise
-                        lacc *= alpha;
-#pragma unroll
-                        for (int o = 0; o < kOt; ++o) acc[o] *= alpha;
-                        mref = mx;
-                    }
-                }
-                const float nref = mref == -INFINITY ? 0.f : -mref;  // no key of this query yet: every weight is 0
-                uint32_t ph[4], pl[4];
+            for (int ds = 0; ds < kDs; ++ds) {
+                const bf16x8_t kf = __builtin_bit_cast(
+                    bf16x8_t, *reinterpret_cast<const uint4*>(tk + m * kRowB + 16 * (4 * ds + g4)));
+                sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ds], sc, 0, 0, 0);
+            }
+            // which of the 4 slots lie in query m's window (bit i: slot 16 k + 4 g4 + i)
+            uint32_t bits = 0;
+            if (bx.bw >= 3) {  // the 4 slots span at most two box rows: columns mcl .. mcl + 3 of row, next row
+                const bool ok0 = static_cast<unsigned>(rr) <= static_cast<unsigned>(wrn);
+                const bool ok1 = static_cast<unsigned>(rr + 1) <= static_cast<unsigned>(wrn);
+                bits = __builtin_amdgcn_ubfe((ok0 ? wc : 0u) | (ok1 ? wc2 : 0u), mcl, 4);
+            } else {  // boxes one or two columns wide (grids that narrow): slot by slot
+                int r = rr, cc = mcl;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const float pk = __builtin_amdgcn_exp2f(fmaf(sv[i], sl2e, nref));  // exp2(-inf) = 0
-                    ph[i] = __float_as_uint(pk) & 0xFFFF0000u;
-                    pl[i] = __float_as_uint(pk - __uint_as_float(ph[i]));
+                    const bool ok = static_cast<unsigned>(r) <= static_cast<unsigned>(wrn) && ((wc >> cc) & 1u);
+                    bits |= ok ? 1u << i : 0u;
+                    ++cc;
+                    const bool wrap = cc == bx.bw;
+                    cc = wrap ? 0 : cc;
+                    r += wrap ? 1 : 0;
                 }
-                const bf16x4_t pth =
-                    __builtin_bit_cast(bf16x4_t, make_uint2(hi16_pair(ph[0], ph[1]), hi16_pair(ph[2], ph[3])));
-                const bf16x4_t ptl =
-                    __builtin_bit_cast(bf16x4_t, make_uint2(hi16_pair(pl[0], pl[1]), hi16_pair(pl[2], pl[3])));
-                lacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ones, pth, lacc, 0, 0, 0);
-                lacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ones, ptl, lacc, 0, 0, 0);
-                // V_blk^T operand of tile o: lane holds the value rows 4 g4 + i of the block at channel 16 o + m
-                const uint16_t* const tv16 = reinterpret_cast<const uint16_t*>(tv);
-#pragma unroll
-                for (int o = 0; o < kOt; ++o) {
-                    const uint16_t* const col = tv16 + (4 * g4) * (kRowB / 2) + 16 * o + m;
-                    const uint32_t w0 = col[0] | (static_cast<uint32_t>(col[kRowB / 2]) << 16);
-                    const uint32_t w1 = col[kRowB] | (static_cast<uint32_t>(col[3 * (kRowB / 2)]) << 16);
-                    const bf16x4_t vt = __builtin_bit_cast(bf16x4_t, make_uint2(w0, w1));
-                    acc[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, pth, acc[o], 0, 0, 0);
-                    acc[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, ptl, acc[o], 0, 0, 0);
-                }
-                step16(bx, mr, mcl);
-                wave_lds_sync();  // this block's LDS reads come before the next block's writes
             }
+            float sv[4];  // raw scores of the window's keys, -inf elsewhere
+#pragma unroll
+            for (int i = 0; i < 4; ++i) sv[i] = (bits >> i) & 1u ? sc[i] : -INFINITY;
+            const float mxr = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+            if (__ballot(mxr > thr)) {  // some query may pass its reference: the exact test decides
+                float mx = mxr * sl2e;
+                mx = fmaxf(mx, __shfl_xor(mx, 16));
+                mx = fmaxf(mx, __shfl_xor(mx, 32));
+                if (mx > mref + kRescaleSlack) {
+                    const float alpha = __builtin_amdgcn_exp2f(mref - mx);  // 0 on the first raise
+                    lacc *= alpha;
+#pragma unroll
+                    for (int o = 0; o < kOt; ++o) acc[o] *= alpha;
+                    mref = mx;
+                    nref = -mx;
+                    thr = (mx + (kRescaleSlack - 1.f)) / sl2e;
+                }
+            }
+            uint32_t ph[4], pl[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float pk = __builtin_amdgcn_exp2f(fmaf(sv[i], sl2e, nref));  // exp2(-inf) = 0
+                ph[i] = __float_as_uint(pk) & 0xFFFF0000u;
+                pl[i] = __float_as_uint(pk - __uint_as_float(ph[i]));
+            }
+            const bf16x4_t pth =
+                __builtin_bit_cast(bf16x4_t, make_uint2(hi16_pair(ph[0], ph[1]), hi16_pair(ph[2], ph[3])));
+            const bf16x4_t ptl =
+                __builtin_bit_cast(bf16x4_t, make_uint2(hi16_pair(pl[0], pl[1]), hi16_pair(pl[2], pl[3])));
+            lacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ones, pth, lacc, 0, 0, 0);
+            lacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ones, ptl, lacc, 0, 0, 0);
+#pragma unroll
+            for (int o = 0; o < kOt; ++o) {
+                const bf16x4_t vt = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                    (__attribute__((address_space(3))) bf16x4_t*)(tvt + 32 * o));
+                acc[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, pth, acc[o], 0, 0, 0);
+                acc[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, ptl, acc[o], 0, 0, 0);
+            }
+            if (last) break;
+            if (++k < bx.nb) {
+                step16(bx, rr, mcl);
+            } else {
+                k = 0;
+                bx = box_of(++c);
+                enter();
+            }
+            wave_lds_sync();  // this block's LDS reads come before the next block's writes
         }
     }
     if (!valid) return;
