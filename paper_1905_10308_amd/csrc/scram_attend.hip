@@ -316,9 +316,12 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
     const uint32_t gq = valid ? g : g0;
     uint32_t s, rem;
     divmod(gq, p.div_plane, s, rem);
-    const size_t slice = static_cast<size_t>(s) * p.nkeys;
-    const uint16_t* const Ks = static_cast<const uint16_t*>(p.K) + slice * D;
-    const uint16_t* const Vs = static_cast<const uint16_t*>(p.V) + slice * D;
+    // the slice's key and value rows: every item of a tile lies in one slice, and the caller keeps a
+    // slice's rows below 4 GiB, so a row is a 32-bit byte offset from a wave-uniform base
+    const size_t slice_bytes =
+        static_cast<size_t>(__builtin_amdgcn_readfirstlane(s)) * p.nkeys * static_cast<size_t>(2 * D);
+    const unsigned char* const Kb = static_cast<const unsigned char*>(p.K) + slice_bytes;
+    const unsigned char* const Vb = static_cast<const unsigned char*>(p.V) + slice_bytes;
     int u, v;
     {
         uint32_t uu, vv;
@@ -384,6 +387,7 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
     const bf16x4_t ones = bf16x4_t{static_cast<__bf16>(1.f), static_cast<__bf16>(1.f), static_cast<__bf16>(1.f),
                                    static_cast<__bf16>(1.f)};
     const float sl2e = p.scale_log2e;  // > 0 (the caller routes other scales to the lane-group kernels)
+    const float inv_sl2e = 1.f / sl2e;
     // online softmax state of query m: reference mref (base-2 domain), its negation as the exponent's
     // offset (0 while no key of the window has been seen), and the raw score above which a block may
     // raise the reference (a little below the exact test, which decides)
@@ -406,6 +410,7 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
     struct Box {
         int r0, c0, bw, h, nb, q16, r16;
         float inv;
+        uint32_t kstep, kstep_wrap;  // key index change of a 16-slot step, without and with a column carry
     };
     auto box_of = [&](int cl) {
         Box bx;
@@ -417,6 +422,8 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
         bx.q16 = __builtin_amdgcn_readlane(t_q16, cl);
         bx.r16 = __builtin_amdgcn_readlane(t_r16, cl);
         bx.inv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(t_inv), cl));
+        bx.kstep = static_cast<uint32_t>(bx.q16) * static_cast<uint32_t>(p.Wk) + bx.r16;
+        bx.kstep_wrap = bx.kstep + p.Wk - bx.bw;
         return bx;
     };
     auto step16 = [](const Box& bx, int& r, int& c) {  // slot j -> slot j + 16
@@ -426,26 +433,35 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
         r += bx.q16 + (carry ? 1 : 0);
     };
 
-    // load cursor: block fk of cluster fc, this lane's load slot (lr, lc) in it; one block ahead
-    int fc = 0, fk = 0, lr = 0, lc = 0;
+    // load cursor: block fk of cluster fc; this lane's load slot of that block is box column lc, key fkey
+    // (past the box's last row the slots run on into the rows below it: keys of weight 0, clamped to the
+    // slice)
+    int fc = 0, fk = 0, lc = 0;
+    uint32_t fkey = 0;
     Box fb = box_of(0);
+    auto fetch_first = [&]() {  // this lane's load slot of the first block of cluster fc
+        int lr;
+        box_slot(lslot, fb.bw, fb.inv, lr, lc);
+        fkey = static_cast<uint32_t>(fb.r0 + lr) * static_cast<uint32_t>(p.Wk) + (fb.c0 + lc);
+    };
     uint4 kr0, kr1, vr0, vr1;  // this lane's pieces of the rows in flight
-    auto fetch = [&]() {  // past the box's last row: its first key (weight 0)
-        const uint32_t key0 = static_cast<uint32_t>(fb.r0) * static_cast<uint32_t>(p.Wk) + fb.c0;
-        const uint32_t key = lr < fb.h ? key0 + static_cast<uint32_t>(lr) * static_cast<uint32_t>(p.Wk) + lc : key0;
-        const size_t row = static_cast<size_t>(min(key, p.nkeys - 1u)) * D + 8 * lpiece;  // (the clamp is a guard)
-        kr0 = *reinterpret_cast<const uint4*>(Ks + row);
-        vr0 = *reinterpret_cast<const uint4*>(Vs + row);
+    auto fetch = [&]() {
+        const uint32_t off = min(fkey, p.nkeys - 1u) * (2u * D) + 16u * lpiece;
+        kr0 = *reinterpret_cast<const uint4*>(Kb + off);
+        vr0 = *reinterpret_cast<const uint4*>(Vb + off);
         if constexpr (kPer == 2) {
-            kr1 = *reinterpret_cast<const uint4*>(Ks + row + 32);
-            vr1 = *reinterpret_cast<const uint4*>(Vs + row + 32);
+            kr1 = *reinterpret_cast<const uint4*>(Kb + off + 64);
+            vr1 = *reinterpret_cast<const uint4*>(Vb + off + 64);
         }
         if (++fk < fb.nb) {
-            step16(fb, lr, lc);
+            lc += fb.r16;
+            const bool carry = lc >= fb.bw;
+            lc -= carry ? fb.bw : 0;
+            fkey += carry ? fb.kstep_wrap : fb.kstep;
         } else if (++fc < nclu) {
             fk = 0;
             fb = box_of(fc);
-            box_slot(lslot, fb.bw, fb.inv, lr, lc);
+            fetch_first();
         }
     };
     // compute cursor: block k of cluster c; slot 16 k + 4 g4 of this lane's scores is box row wr0 + rr,
@@ -464,7 +480,7 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
     };
 
     if (nclu > 0) {
-        box_slot(lslot, fb.bw, fb.inv, lr, lc);
+        fetch_first();
         fetch();
         enter();
         for (;;) {
@@ -522,7 +538,7 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
                     for (int o = 0; o < kOt; ++o) acc[o] *= alpha;
                     mref = mx;
                     nref = -mx;
-                    thr = (mx + (kRescaleSlack - 1.f)) / sl2e;
+                    thr = (mx + (kRescaleSlack - 1.f)) * inv_sl2e;
                 }
             }
             uint32_t ph[4], pl[4];
@@ -585,8 +601,8 @@ hipError_t run_attend_m(const AttParams& p, int window, uint64_t blocks, hipStre
 }
 
 // The matrix-core kernel takes bf16 storage with 32 or 64 channels, one
-// window of side 3, 5 or 7 per query, no mask and a positive scale; the
-// lane-group kernels take every other call.
+// window of side 3, 5 or 7 per query, no mask, a positive scale and slices of
+// at most 4 GiB of key rows; the lane-group kernels take every other call.
 #ifndef SCRAM_ATTEND_TILE
 #define SCRAM_ATTEND_TILE 1
 #endif
@@ -599,7 +615,8 @@ hipError_t run_attend(const AttParams& p0, int window, hipStream_t st, hipEvent_
     constexpr int G = Lanes<T, D>::kAttend;
     AttParams p = p0;
     if constexpr (kTileKernel<T, D>) {
-        if (p.kappa == 1 && !p.causal && (window == 3 || window == 5 || window == 7) && p.scale_log2e > 0.f) {
+        if (p.kappa == 1 && !p.causal && (window == 3 || window == 5 || window == 7) && p.scale_log2e > 0.f &&
+            static_cast<uint64_t>(p.nkeys) * (2 * D) <= 0xFFFFFFFFull) {
             p.tq = make_tiling(p.Hq, p.Wq, kBlock / 4);
             p.rc = 6;  // boxes at most 12 + window wide: slots of a box stay below 1024
             const uint64_t tiles = tiling_blocks(p.tq, p.n / p.tq.plane);
