@@ -293,8 +293,9 @@ __device__ __forceinline__ void wave_lds_sync()
 
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 
+// (at most 96 VGPRs: five waves per SIMD hide more of the row loads than four)
 template <int D, int W>
-__global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) void attend_tile_kernel(AttParams p)
 {
     constexpr int B = W / 2;
     constexpr int kDs = D / 32;        // 32-channel contraction steps of S^T
@@ -358,6 +359,7 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
         t_bw = here ? min(vhi + B, p.Wk - 1) - max(vlo - B, 0) + 1 : t_bw;
         ++nclu;
     }
+    if (nclu == 0) return;  // no query of this wave lies inside the grid
     // the rest of each cluster's scalars, once for all clusters: blocks of 16 slots, and the step of 16
     // raster slots as q16 rows and r16 columns
     const float t_inv = __builtin_amdgcn_rcpf(static_cast<float>(t_bw));
@@ -387,11 +389,12 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
     const bf16x4_t ones = bf16x4_t{static_cast<__bf16>(1.f), static_cast<__bf16>(1.f), static_cast<__bf16>(1.f),
                                    static_cast<__bf16>(1.f)};
     const float sl2e = p.scale_log2e;  // > 0 (the caller routes other scales to the lane-group kernels)
-    const float inv_sl2e = 1.f / sl2e;
-    // online softmax state of query m: reference mref (base-2 domain), its negation as the exponent's
-    // offset (0 while no key of the window has been seen), and the raw score above which a block may
-    // raise the reference (a little below the exact test, which decides)
-    float mref = -INFINITY, nref = 0.f, thr = -INFINITY;
+    const float inv_sl2e = __builtin_amdgcn_rcpf(sl2e);
+    // online softmax state of query m: reference mref (base-2 domain) and its negation as the exponent's
+    // offset (0 while no key of the window has been seen); thr is the raw score above which a block may
+    // raise the reference (a little below the exact test, which decides) while the wave is in query m's
+    // cluster, and +inf in the other clusters
+    float mref = -INFINITY, nref = 0.f, thr = INFINITY;
 
     // ---- the clusters' blocks of 16 keys, one at a time; the next block's rows load during this one's
     // products.  Block k of a cluster holds raster slots 16 k .. 16 k + 15 of its box; its 16 key rows and
@@ -408,7 +411,7 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
     const unsigned char* const tvt = tv + (4 * g4 + (m >> 2)) * kRowB + 8 * (m & 3);
     // A cluster's scalars, read from the lanes that hold them
     struct Box {
-        int r0, c0, bw, h, nb, q16, r16;
+        int r0, c0, bw, nb, q16, r16;
         float inv;
         uint32_t kstep, kstep_wrap;  // key index change of a 16-slot step, without and with a column carry
     };
@@ -417,7 +420,6 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
         bx.r0 = __builtin_amdgcn_readlane(t_r0, cl);
         bx.c0 = __builtin_amdgcn_readlane(t_c0, cl);
         bx.bw = __builtin_amdgcn_readlane(t_bw, cl);
-        bx.h = __builtin_amdgcn_readlane(t_h, cl);
         bx.nb = __builtin_amdgcn_readlane(t_nb, cl);
         bx.q16 = __builtin_amdgcn_readlane(t_q16, cl);
         bx.r16 = __builtin_amdgcn_readlane(t_r16, cl);
@@ -426,151 +428,158 @@ __global__ __launch_bounds__(kBlock) void attend_tile_kernel(AttParams p)
         bx.kstep_wrap = bx.kstep + p.Wk - bx.bw;
         return bx;
     };
-    auto step16 = [](const Box& bx, int& r, int& c) {  // slot j -> slot j + 16
-        c += bx.r16;
-        const bool carry = c >= bx.bw;
-        c -= carry ? bx.bw : 0;
-        r += bx.q16 + (carry ? 1 : 0);
-    };
 
-    // load cursor: block fk of cluster fc; this lane's load slot of that block is box column lc, key fkey
-    // (past the box's last row the slots run on into the rows below it: keys of weight 0, clamped to the
-    // slice)
-    int fc = 0, fk = 0, lc = 0;
-    uint32_t fkey = 0;
-    Box fb = box_of(0);
-    auto fetch_first = [&]() {  // this lane's load slot of the first block of cluster fc
-        int lr;
-        box_slot(lslot, fb.bw, fb.inv, lr, lc);
-        fkey = static_cast<uint32_t>(fb.r0 + lr) * static_cast<uint32_t>(p.Wk) + (fb.c0 + lc);
-    };
     uint4 kr0, kr1, vr0, vr1;  // this lane's pieces of the rows in flight
-    auto fetch = [&]() {
-        const uint32_t off = min(fkey, p.nkeys - 1u) * (2u * D) + 16u * lpiece;
+    auto load = [&](uint32_t key) {  // (the clamp is a guard: keys past a box's last row have weight 0)
+        const uint32_t off = min(key, p.nkeys - 1u) * (2u * D) + 16u * lpiece;
         kr0 = *reinterpret_cast<const uint4*>(Kb + off);
         vr0 = *reinterpret_cast<const uint4*>(Vb + off);
         if constexpr (kPer == 2) {
             kr1 = *reinterpret_cast<const uint4*>(Kb + off + 64);
             vr1 = *reinterpret_cast<const uint4*>(Vb + off + 64);
         }
-        if (++fk < fb.nb) {
-            lc += fb.r16;
-            const bool carry = lc >= fb.bw;
-            lc -= carry ? fb.bw : 0;
-            fkey += carry ? fb.kstep_wrap : fb.kstep;
-        } else if (++fc < nclu) {
-            fk = 0;
-            fb = box_of(fc);
-            fetch_first();
+    };
+    auto stage = [&]() {
+        const int off = lslot * kRowB + 16 * lpiece;
+        *reinterpret_cast<uint4*>(tk + off) = kr0;
+        *reinterpret_cast<uint4*>(tv + off) = vr0;
+        if constexpr (kPer == 2) {
+            *reinterpret_cast<uint4*>(tk + off + 64) = kr1;
+            *reinterpret_cast<uint4*>(tv + off + 64) = vr1;
         }
     };
-    // compute cursor: block k of cluster c; slot 16 k + 4 g4 of this lane's scores is box row wr0 + rr,
-    // column mcl; the window's column bits of that row (wc) and of the next one (wc2, shifted past the
-    // row's end), zero outside query m's own cluster
-    int c = 0, k = 0, rr = 0, mcl = 0;
-    uint32_t wc = 0, wc2 = 0;
-    Box bx = fb;
-    auto enter = [&]() {  // the first block of cluster c
-        int mr;
-        box_slot(4 * g4, bx.bw, bx.inv, mr, mcl);
-        rr = mr - wr0;
-        const bool here = c == mine;
-        wc = here ? wcols : 0u;
-        wc2 = here ? wcols << bx.bw : 0u;  // bw <= 19, and only bits below bw + 3 are read
+    // this lane's load slot: box column lc and key index lkey; past the box's last row the slots run on
+    // into the rows below it
+    auto first_slot = [&](const Box& b, int& lc, uint32_t& lkey) {
+        int lr;
+        box_slot(lslot, b.bw, b.inv, lr, lc);
+        lkey = static_cast<uint32_t>(b.r0 + lr) * static_cast<uint32_t>(p.Wk) + (b.c0 + lc);
     };
-
-    if (nclu > 0) {
-        fetch_first();
-        fetch();
-        enter();
-        for (;;) {
-            {
-                const int off = lslot * kRowB + 16 * lpiece;
-                *reinterpret_cast<uint4*>(tk + off) = kr0;
-                *reinterpret_cast<uint4*>(tv + off) = vr0;
-                if constexpr (kPer == 2) {
-                    *reinterpret_cast<uint4*>(tk + off + 64) = kr1;
-                    *reinterpret_cast<uint4*>(tv + off + 64) = vr1;
-                }
-            }
-            const bool last = fc >= nclu;
-            if (!last) fetch();
-            wave_lds_sync();
-
-            // S^T of this block: lane holds keys 4 g4 + i (slots 16 k + 4 g4 + i) for query m
-            f32x4_t sc = zero;
+    auto step_slot = [](const Box& b, int& lc, uint32_t& lkey) {  // 16 slots on
+        lc += b.r16;
+        const bool carry = lc >= b.bw;
+        lc -= carry ? b.bw : 0;
+        lkey += carry ? b.kstep_wrap : b.kstep;
+    };
+    // one block: slot 16 k + 4 g4 of this lane's scores is box row wr0 + rr, column mcl; wc and wc2 are
+    // the window's column bits of that row and of the next one (shifted past the row's end), zero outside
+    // query m's own cluster
+    auto compute = [&](const Box& bx, int rr, int mcl, uint32_t wc, uint32_t wc2) {
+        // S^T of this block: lane holds keys 4 g4 + i (slots 16 k + 4 g4 + i) for query m
+        f32x4_t sc = zero;
 #pragma unroll
-            for (int ds = 0; ds < kDs; ++ds) {
-                const bf16x8_t kf = __builtin_bit_cast(
-                    bf16x8_t, *reinterpret_cast<const uint4*>(tk + m * kRowB + 16 * (4 * ds + g4)));
-                sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ds], sc, 0, 0, 0);
-            }
-            // which of the 4 slots lie in query m's window (bit i: slot 16 k + 4 g4 + i)
-            uint32_t bits = 0;
-            if (bx.bw >= 3) {  // the 4 slots span at most two box rows: columns mcl .. mcl + 3 of row, next row
-                const bool ok0 = static_cast<unsigned>(rr) <= static_cast<unsigned>(wrn);
-                const bool ok1 = static_cast<unsigned>(rr + 1) <= static_cast<unsigned>(wrn);
-                bits = __builtin_amdgcn_ubfe((ok0 ? wc : 0u) | (ok1 ? wc2 : 0u), mcl, 4);
-            } else {  // boxes one or two columns wide (grids that narrow): slot by slot
-                int r = rr, cc = mcl;
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const bool ok = static_cast<unsigned>(r) <= static_cast<unsigned>(wrn) && ((wc >> cc) & 1u);
-                    bits |= ok ? 1u << i : 0u;
-                    ++cc;
-                    const bool wrap = cc == bx.bw;
-                    cc = wrap ? 0 : cc;
-                    r += wrap ? 1 : 0;
-                }
-            }
-            float sv[4];  // raw scores of the window's keys, -inf elsewhere
-#pragma unroll
-            for (int i = 0; i < 4; ++i) sv[i] = (bits >> i) & 1u ? sc[i] : -INFINITY;
-            const float mxr = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
-            if (__ballot(mxr > thr)) {  // some query may pass its reference: the exact test decides
-                float mx = mxr * sl2e;
-                mx = fmaxf(mx, __shfl_xor(mx, 16));
-                mx = fmaxf(mx, __shfl_xor(mx, 32));
-                if (mx > mref + kRescaleSlack) {
-                    const float alpha = __builtin_amdgcn_exp2f(mref - mx);  // 0 on the first raise
-                    lacc *= alpha;
-#pragma unroll
-                    for (int o = 0; o < kOt; ++o) acc[o] *= alpha;
-                    mref = mx;
-                    nref = -mx;
-                    thr = (mx + (kRescaleSlack - 1.f)) * inv_sl2e;
-                }
-            }
-            uint32_t ph[4], pl[4];
+        for (int ds = 0; ds < kDs; ++ds) {
+            const bf16x8_t kf = __builtin_bit_cast(
+                bf16x8_t, *reinterpret_cast<const uint4*>(tk + m * kRowB + 16 * (4 * ds + g4)));
+            sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ds], sc, 0, 0, 0);
+        }
+        // which of the 4 slots lie in query m's window (bit i: slot 16 k + 4 g4 + i)
+        uint32_t bits = 0;
+        if (bx.bw >= 3) {  // the 4 slots span at most two box rows: columns mcl .. mcl + 3 of row, next row
+            const bool ok0 = static_cast<unsigned>(rr) <= static_cast<unsigned>(wrn);
+            const bool ok1 = static_cast<unsigned>(rr + 1) <= static_cast<unsigned>(wrn);
+            bits = __builtin_amdgcn_ubfe((ok0 ? wc : 0u) | (ok1 ? wc2 : 0u), mcl, 4);
+        } else {  // boxes one or two columns wide (grids that narrow): slot by slot
+            int r = rr, cc = mcl;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const float pk = __builtin_amdgcn_exp2f(fmaf(sv[i], sl2e, nref));  // exp2(-inf) = 0
-                ph[i] = __float_as_uint(pk) & 0xFFFF0000u;
-                pl[i] = __float_as_uint(pk - __uint_as_float(ph[i]));
+                const bool ok = static_cast<unsigned>(r) <= static_cast<unsigned>(wrn) && ((wc >> cc) & 1u);
+                bits |= ok ? 1u << i : 0u;
+                ++cc;
+                const bool wrap = cc == bx.bw;
+                cc = wrap ? 0 : cc;
+                r += wrap ? 1 : 0;
             }
-            const bf16x4_t pth =
-                __builtin_bit_cast(bf16x4_t, make_uint2(hi16_pair(ph[0], ph[1]), hi16_pair(ph[2], ph[3])));
-            const bf16x4_t ptl =
-                __builtin_bit_cast(bf16x4_t, make_uint2(hi16_pair(pl[0], pl[1]), hi16_pair(pl[2], pl[3])));
-            lacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ones, pth, lacc, 0, 0, 0);
-            lacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ones, ptl, lacc, 0, 0, 0);
+        }
+        // all ones for the slots of the window, zero elsewhere
+        uint32_t keep[4];
 #pragma unroll
-            for (int o = 0; o < kOt; ++o) {
-                const bf16x4_t vt = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-                    (__attribute__((address_space(3))) bf16x4_t*)(tvt + 32 * o));
-                acc[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, pth, acc[o], 0, 0, 0);
-                acc[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, ptl, acc[o], 0, 0, 0);
+        for (int i = 0; i < 4; ++i) keep[i] = static_cast<uint32_t>(__builtin_amdgcn_sbfe(static_cast<int>(bits), i, 1));
+        // the trigger looks at every slot of the block; the exact test at the window's slots only
+        const float mxr = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
+        if (__ballot(mxr > thr)) {  // some query may pass its reference: the exact test decides
+            float mx = -INFINITY;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) mx = fmaxf(mx, keep[i] ? sc[i] : -INFINITY);
+            mx *= sl2e;
+            mx = fmaxf(mx, __shfl_xor(mx, 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            if (mx > mref + kRescaleSlack) {
+                const float alpha = __builtin_amdgcn_exp2f(mref - mx);  // 0 on the first raise
+                lacc *= alpha;
+#pragma unroll
+                for (int o = 0; o < kOt; ++o) acc[o] *= alpha;
+                mref = mx;
+                nref = -mx;
+                thr = (mx + (kRescaleSlack - 1.f)) * inv_sl2e;
             }
-            if (last) break;
-            if (++k < bx.nb) {
-                step16(bx, rr, mcl);
-            } else {
-                k = 0;
-                bx = box_of(++c);
-                enter();
-            }
+        }
+        uint32_t ph[4], pl[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            // exponent of the window's slots; -inf (a weight of 0) elsewhere
+            const uint32_t x = __float_as_uint(fmaf(sc[i], sl2e, nref));
+            const float pk = __builtin_amdgcn_exp2f(__uint_as_float((x & keep[i]) | (0xFF800000u & ~keep[i])));
+            ph[i] = __float_as_uint(pk) & 0xFFFF0000u;
+            pl[i] = __float_as_uint(pk - __uint_as_float(ph[i]));
+        }
+        const bf16x4_t pth =
+            __builtin_bit_cast(bf16x4_t, make_uint2(hi16_pair(ph[0], ph[1]), hi16_pair(ph[2], ph[3])));
+        const bf16x4_t ptl =
+            __builtin_bit_cast(bf16x4_t, make_uint2(hi16_pair(pl[0], pl[1]), hi16_pair(pl[2], pl[3])));
+        lacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ones, pth, lacc, 0, 0, 0);
+        lacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ones, ptl, lacc, 0, 0, 0);
+#pragma unroll
+        for (int o = 0; o < kOt; ++o) {
+            const bf16x4_t vt = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                (__attribute__((address_space(3))) bf16x4_t*)(tvt + 32 * o));
+            acc[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, pth, acc[o], 0, 0, 0);
+            acc[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, ptl, acc[o], 0, 0, 0);
+        }
+    };
+
+    // The blocks of a cluster are computed in a row; each block's rows load during the previous block's
+    // products, the first block of the next cluster during the last block of this one.
+    Box bx = box_of(0);
+    int lc;
+    uint32_t lkey;
+    first_slot(bx, lc, lkey);
+    load(lkey);
+    for (int c = 0;;) {
+        int mr, mcl;
+        box_slot(4 * g4, bx.bw, bx.inv, mr, mcl);
+        int rr = mr - wr0;
+        const bool here = c == mine;
+        const uint32_t wc = here ? wcols : 0u;
+        const uint32_t wc2 = here ? wcols << bx.bw : 0u;  // bw <= 19, and only bits below bw + 3 are read
+        thr = here ? -INFINITY : INFINITY;  // a query's cluster is visited once, its blocks in a row
+        step_slot(bx, lc, lkey);
+        for (int k = 1; k < bx.nb; ++k) {
+            stage();
+            load(lkey);
+            step_slot(bx, lc, lkey);
+            wave_lds_sync();
+            compute(bx, rr, mcl, wc, wc2);
+            mcl += bx.r16;
+            const bool carry = mcl >= bx.bw;
+            mcl -= carry ? bx.bw : 0;
+            rr += bx.q16 + (carry ? 1 : 0);
             wave_lds_sync();  // this block's LDS reads come before the next block's writes
         }
+        stage();
+        const bool more = c + 1 < nclu;
+        Box nx = bx;
+        if (more) {
+            nx = box_of(c + 1);
+            first_slot(nx, lc, lkey);
+            load(lkey);
+        }
+        wave_lds_sync();
+        compute(bx, rr, mcl, wc, wc2);
+        if (!more) break;
+        bx = nx;
+        ++c;
+        wave_lds_sync();
     }
     if (!valid) return;
     const float lt = lacc[0];  // every row of the ones-block product holds query m's sum of weights
