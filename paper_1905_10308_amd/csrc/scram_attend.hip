@@ -390,6 +390,11 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
                                    static_cast<__bf16>(1.f)};
     const float sl2e = p.scale_log2e;  // > 0 (the caller routes other scales to the lane-group kernels)
     const float inv_sl2e = __builtin_amdgcn_rcpf(sl2e);
+    // bit positions 0..3 as values the compiler cannot see, so that each mask below stays one
+    // bit-field extract instead of a shift pair
+    int bit_at[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) asm volatile("s_mov_b32 %0, %1" : "=s"(bit_at[i]) : "i"(i));
     // online softmax state of query m: reference mref (base-2 domain) and its negation as the exponent's
     // offset (0 while no key of the window has been seen); thr is the raw score above which a block may
     // raise the reference (a little below the exact test, which decides) while the wave is in query m's
@@ -491,13 +496,14 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
                 r += wrap ? 1 : 0;
             }
         }
-        // all ones for the slots of the window, zero elsewhere
+        // all ones for the slots of the window, zero elsewhere (one signed bit-field extract each)
         uint32_t keep[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) keep[i] = static_cast<uint32_t>(__builtin_amdgcn_sbfe(static_cast<int>(bits), i, 1));
+        for (int i = 0; i < 4; ++i)
+            keep[i] = static_cast<uint32_t>(__builtin_amdgcn_sbfe(static_cast<int>(bits), bit_at[i], 1));
         // the trigger looks at every slot of the block; the exact test at the window's slots only
-        const float mxr = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
-        if (__ballot(mxr > thr)) {  // some query may pass its reference: the exact test decides
+        if (__ballot((sc[0] > thr) | (sc[1] > thr) | (sc[2] > thr) | (sc[3] > thr))) {
+            // some query may pass its reference: the exact test decides
             float mx = -INFINITY;
 #pragma unroll
             for (int i = 0; i < 4; ++i) mx = fmaxf(mx, keep[i] ? sc[i] : -INFINITY);
