@@ -292,6 +292,8 @@ __device__ __forceinline__ void wave_lds_sync()
 }
 
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 
 // (at most 96 VGPRs: five waves per SIMD hide more of the row loads than four)
 template <int D, int W>
@@ -589,14 +591,16 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
     }
     if (!valid) return;
     const float lt = lacc[0];  // every row of the ones-block product holds query m's sum of weights
-    const float inv = lt > 0.f ? 1.f / lt : 0.f;
-    // lane holds channels 16 o + 4 g4 + i of query m; bf16 with round to nearest even
+    const float inv = lt > 0.f ? __builtin_amdgcn_rcpf(lt) : 0.f;  // (1 ulp: far below the bf16 rounding)
+    // lane holds channels 16 o + 4 g4 + i of query m; pairs rounded to bf16 (nearest even) together
     uint16_t* const orow = static_cast<uint16_t*>(p.out) + static_cast<size_t>(g) * D;
-    auto bf = [](float x) { return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(x))); };
+    auto bf2 = [](float a, float b) {
+        return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
+    };
 #pragma unroll
     for (int o = 0; o < kOt; ++o) {
-        const uint32_t w0 = bf(acc[o][0] * inv) | (bf(acc[o][1] * inv) << 16);
-        const uint32_t w1 = bf(acc[o][2] * inv) | (bf(acc[o][3] * inv) << 16);
+        const uint32_t w0 = bf2(acc[o][0] * inv, acc[o][1] * inv);
+        const uint32_t w1 = bf2(acc[o][2] * inv, acc[o][3] * inv);
         *reinterpret_cast<uint2*>(orow + 16 * o + 4 * g4) = make_uint2(w0, w1);
     }
 }
