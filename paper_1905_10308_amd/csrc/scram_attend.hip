@@ -421,6 +421,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
         int r0, c0, bw, nb, q16, r16;
         float inv;
         uint32_t kstep, kstep_wrap;  // key index change of a 16-slot step, without and with a column carry
+        uint32_t klast;              // key index of the box's last slot
     };
     auto box_of = [&](int cl) {
         Box bx;
@@ -433,12 +434,15 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
         bx.inv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(t_inv), cl));
         bx.kstep = static_cast<uint32_t>(bx.q16) * static_cast<uint32_t>(p.Wk) + bx.r16;
         bx.kstep_wrap = bx.kstep + p.Wk - bx.bw;
+        const int h = __builtin_amdgcn_readlane(t_h, cl);
+        bx.klast = static_cast<uint32_t>(bx.r0 + h - 1) * static_cast<uint32_t>(p.Wk) + (bx.c0 + bx.bw - 1);
         return bx;
     };
 
     uint4 kr0, kr1, vr0, vr1;  // this lane's pieces of the rows in flight
-    auto load = [&](uint32_t key) {  // (the clamp is a guard: keys past a box's last row have weight 0)
-        const uint32_t off = min(key, p.nkeys - 1u) * (2u * D) + 16u * lpiece;
+    // a slot past the box's last row (weight 0) reads the box's last row, which the block holds anyway
+    auto load = [&](uint32_t key, uint32_t klast) {
+        const uint32_t off = min(key, klast) * (2u * D) + 16u * lpiece;
         kr0 = *reinterpret_cast<const uint4*>(Kb + off);
         vr0 = *reinterpret_cast<const uint4*>(Vb + off);
         if constexpr (kPer == 2) {
@@ -455,8 +459,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
             *reinterpret_cast<uint4*>(tv + off + 64) = vr1;
         }
     };
-    // this lane's load slot: box column lc and key index lkey; past the box's last row the slots run on
-    // into the rows below it
+    // this lane's load slot: box column lc and key index lkey (past the box's last row the slots run on
+    // into the rows below it, and their keys are clamped to the box's last)
     auto first_slot = [&](const Box& b, int& lc, uint32_t& lkey) {
         int lr;
         box_slot(lslot, b.bw, b.inv, lr, lc);
@@ -552,7 +556,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
     int lc;
     uint32_t lkey;
     first_slot(bx, lc, lkey);
-    load(lkey);
+    load(lkey, bx.klast);
     for (int c = 0;;) {
         int mr, mcl;
         box_slot(4 * g4, bx.bw, bx.inv, mr, mcl);
@@ -564,7 +568,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
         step_slot(bx, lc, lkey);
         for (int k = 1; k < bx.nb; ++k) {
             stage();
-            load(lkey);
+            load(lkey, bx.klast);
             step_slot(bx, lc, lkey);
             wave_lds_sync();
             compute(bx, rr, mcl, wc, wc2);
@@ -580,7 +584,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
         if (more) {
             nx = box_of(c + 1);
             first_slot(nx, lc, lkey);
-            load(lkey);
+            load(lkey, nx.klast);
         }
         wave_lds_sync();
         compute(bx, rr, mcl, wc, wc2);
