@@ -58,6 +58,9 @@ def test_headline_line_has_the_contract_fields(capsys):
     assert dense["ms"] == min(b["ms"] for b in dense["backends"].values())
     q = d["map_quality"]
     assert 0.5 < q["recall_vs_exact_argmax"] <= 1 and 0.9 < q["mean_score_ratio"] <= 1 + 1e-12
+    qs = d["map_quality_over_seeds"]  # the workload's own seed first, then the extra seeds
+    assert qs["seeds"] == [12345, 1, 2, 3] and qs["recall"][0] == q["recall_vs_exact_argmax"]
+    assert all(0.5 < r <= 1 for r in qs["recall"]) and 0 <= qs["recall_std"] < 0.05
     assert all(math.isfinite(v) and v > 0 for v in d["kernels_ms"].values())
 
 
