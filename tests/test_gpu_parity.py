@@ -489,3 +489,36 @@ def test_attend_tile_kernel_maps(scram, d, grid):
             worst = max(worst, float(err.max()))
             assert err.max() <= TOL["bf16"], f"{name} window {window}: {err.max():.3e}"
     log(f"tile attend {grid} d={d}: max rel err {worst:.3e}")
+
+
+@pytest.mark.parametrize("Wk", [8191, 8192], ids=["last_slice_under_4GiB", "slice_of_4GiB"])
+def test_attend_key_slice_at_4gib(scram, Wk):
+    """A 4096 x Wk key grid of 64 bf16 channels: 8191 columns make the slice's rows 2^32 - 524288
+    bytes, the largest the matrix-core kernel (32-bit row offsets) takes here; 8192 make exactly 4 GiB,
+    which goes to the lane-group kernels.  The matches sit in the last rows and columns, so the
+    largest offsets are read; the oracle runs on the key rows the windows can reach (the last 16),
+    which gives the same sums as the whole grid."""
+    Hk, d, Hq, Wq, crop = 4096, 64, 16, 16, 16
+    gen = torch.Generator(device="cuda").manual_seed(Wk)
+    K = torch.randn((1, Hk, Wk, d), generator=gen, device="cuda", dtype=torch.bfloat16)
+    V = torch.randn((1, Hk, Wk, d), generator=gen, device="cuda", dtype=torch.bfloat16)
+    rng = np.random.default_rng(Wk)
+    Qn = to_dev(rng.standard_normal((1, Hq, Wq, d)).astype(np.float32), "bf16")
+    # centres in the last 8 rows and 8 columns, the grid's last key among them
+    J = ((Hk - 1 - rng.integers(0, 8, (1, Hq, Wq))) * Wk + (Wk - 1 - rng.integers(0, 8, (1, Hq, Wq)))).astype(np.int32)
+    J[0, 0, 0] = Hk * Wk - 1
+    Kc = K[:, Hk - crop:].float().cpu().numpy()
+    Vc = V[:, Hk - crop:].float().cpu().numpy()
+    Jc = J - (Hk - crop) * Wk
+    Qf = Qn.float().cpu().numpy()
+    try:
+        for window in (5, 7):
+            out = scram.sparse_attend(Qn, K, V, torch.from_numpy(J).cuda(), window, d ** -0.5)
+            ref = oracle.sparse_attend(Qf, Kc, Vc, Jc, window, d ** -0.5)
+            err = row_rel_err(out.float().cpu().numpy(), ref)
+            assert err.max() <= TOL["bf16"], f"window {window}: {err.max():.3e}"
+            log(f"attend on a 4096x{Wk} key slice ({Hk * Wk * d * 2} bytes of rows), window {window}: "
+                f"max rel err {err.max():.3e}")
+    finally:
+        del K, V
+        torch.cuda.empty_cache()
