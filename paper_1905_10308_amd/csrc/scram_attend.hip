@@ -325,19 +325,23 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
         static_cast<size_t>(__builtin_amdgcn_readfirstlane(s)) * p.nkeys * static_cast<size_t>(2 * D);
     const unsigned char* const Kb = static_cast<const unsigned char*>(p.K) + slice_bytes;
     const unsigned char* const Vb = static_cast<const unsigned char*>(p.V) + slice_bytes;
+    const uint32_t centre = static_cast<uint32_t>(clamp_index(p.J[gq], p.nkeys));
     int u, v;
     {
         uint32_t uu, vv;
-        divmod(static_cast<uint32_t>(clamp_index(p.J[gq], p.nkeys)), p.div_wk, uu, vv);
+        divmod(centre, p.div_wk, uu, vv);
         u = static_cast<int>(uu);
         v = static_cast<int>(vv);
     }
-    // B operand of S^T: query m, channels 32 ds + 8 g4 .. + 7
+    // B operand of S^T: query m, channels 32 ds + 8 g4 .. + 7; and the same channels of the match's key
     bf16x8_t qf[kDs];
+    uint4 kc[kDs];
     const uint16_t* const qrow = static_cast<const uint16_t*>(p.Q) + static_cast<size_t>(gq) * D;
 #pragma unroll
-    for (int ds = 0; ds < kDs; ++ds)
+    for (int ds = 0; ds < kDs; ++ds) {
         qf[ds] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(qrow + 32 * ds + 8 * g4));
+        kc[ds] = *reinterpret_cast<const uint4*>(Kb + centre * (2u * D) + 64u * ds + 16u * g4);
+    }
 
     // ---- clusters of the 16 match centres and their key boxes ----
     // Cluster c's box (rows r0 .. r0 + height - 1, columns c0 .. c0 + width - 1, `nb` blocks of 16 raster
@@ -398,10 +402,23 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
 #pragma unroll
     for (int i = 0; i < 4; ++i) asm volatile("s_mov_b32 %0, %1" : "=s"(bit_at[i]) : "i"(i));
     // online softmax state of query m: reference mref (base-2 domain) and its negation as the exponent's
-    // offset (0 while no key of the window has been seen); thr is the raw score above which a block may
-    // raise the reference (a little below the exact test, which decides) while the wave is in query m's
-    // cluster, and +inf in the other clusters
-    float mref = -INFINITY, nref = 0.f, thr = INFINITY;
+    // offset.  The reference starts at the score of the query's match, a key of its window, so that no
+    // block has to set it; thr_q is the raw score above which a block may raise it (a little below the
+    // exact test, which decides), and thr is thr_q while the wave is in query m's cluster, +inf in the
+    // other clusters.
+    float s_centre = 0.f;
+#pragma unroll
+    for (int ds = 0; ds < kDs; ++ds) {
+        const uint4 qa = __builtin_bit_cast(uint4, qf[ds]);
+        s_centre = dot2_bf16(qa.x, kc[ds].x, s_centre);
+        s_centre = dot2_bf16(qa.y, kc[ds].y, s_centre);
+        s_centre = dot2_bf16(qa.z, kc[ds].z, s_centre);
+        s_centre = dot2_bf16(qa.w, kc[ds].w, s_centre);
+    }
+    s_centre += __shfl_xor(s_centre, 16);
+    s_centre += __shfl_xor(s_centre, 32);
+    float mref = s_centre * sl2e, nref = -mref;
+    float thr_q = (mref + (kRescaleSlack - 1.f)) * inv_sl2e, thr = INFINITY;
 
     // ---- the clusters' blocks of 16 keys, one at a time; the next block's rows load during this one's
     // products.  Block k of a cluster holds raster slots 16 k .. 16 k + 15 of its box; its 16 key rows and
@@ -517,7 +534,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
             mx = fmaxf(mx, __shfl_xor(mx, 16));
             mx = fmaxf(mx, __shfl_xor(mx, 32));
             if (mx > mref + kRescaleSlack) {
-                const float alpha = __builtin_amdgcn_exp2f(mref - mx);  // 0 on the first raise
+                const float alpha = __builtin_amdgcn_exp2f(mref - mx);
                 lacc *= alpha;
 #pragma unroll
                 for (int o = 0; o < kOt; ++o) acc[o] *= alpha;
@@ -564,7 +581,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
         const bool here = c == mine;
         const uint32_t wc = here ? wcols : 0u;
         const uint32_t wc2 = here ? wcols << bx.bw : 0u;  // bw <= 19, and only bits below bw + 3 are read
-        thr = here ? -INFINITY : INFINITY;  // a query's cluster is visited once, its blocks in a row
+        thr = here ? thr_q : INFINITY;  // a query's cluster is visited once, its blocks in a row
         step_slot(bx, lc, lkey);
         for (int k = 1; k < bx.nb; ++k) {
             stage();
