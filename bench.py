@@ -25,6 +25,7 @@ import hashlib
 import json
 import os
 import re
+import statistics
 import sys
 import time
 import warnings
@@ -224,8 +225,6 @@ def quality_over_seeds(cfg, Q, K, iters, first, workspace, seeds=EXTRA_PM_SEEDS)
     """Spread of the final map's quality over PatchMatch seeds: extra runs with ``seeds`` (outside the
     timed regions), each scored on the same sampled queries as ``first`` (the run with the workload's
     own seed)."""
-    import statistics
-
     import paper_1905_10308_amd as scram
     import torch
 
@@ -539,10 +538,15 @@ def main(argv=None) -> int:
                    for c in range(kappa)]
     iter_ms = sum(iter_by_run) / kappa
     att_ms = sum(dur(ev, kappa * (T + 1)) for ev in events) / args.steps
+    # per-step durations for the median and minimum over the timed steps (a sweep's: the mean of its run's T)
+    per_step = {"pm_iter": [sum(dur(ev, c * (T + 1) + t) for c in range(kappa) for t in range(1, T + 1)) / (kappa * T)
+                            for ev in events],
+                "attend": [dur(ev, kappa * (T + 1)) for ev in events]}
     bwd = {}
     if args.backward:
         for i, name in enumerate(("backward_scan_fill", "backward_query", "backward_key_side")):
             bwd[name] = sum(dur(ev, kappa * (T + 1) + 1 + i) for ev in events) / args.steps
+            per_step[name] = [dur(ev, kappa * (T + 1) + 1 + i) for ev in events]
 
     nq = cfg.nq
     # the dominant kernel: the sweep, averaged over the runs (run c reads c previous maps)
@@ -590,6 +594,8 @@ def main(argv=None) -> int:
         "pm_init": "fused into the first sweep",
         "pm_iter_ms_by_run": iter_by_run,
         "kernels_ms_source": "dispatch-stamped HIP events, timed region B",
+        "kernels_ms_stats": {k: {"median": statistics.median(v), "min": min(v), "reps": len(v)}
+                             for k, v in per_step.items()},
         "candidate_evals_per_s_nominal": kappa * nq * T * cfg.candidates / (ms_step * 1e-3),
         "step_requested_GBps": (T * kappa * pm_launch_bytes + att_bytes) / (ms_step * 1e-3) / 1e9,
         "hbm_copy_GBps": copy_bandwidth(dev),

@@ -62,6 +62,8 @@ def test_headline_line_has_the_contract_fields(capsys):
     assert qs["seeds"] == [12345, 1, 2, 3] and qs["recall"][0] == q["recall_vs_exact_argmax"]
     assert all(0.5 < r <= 1 for r in qs["recall"]) and 0 <= qs["recall_std"] < 0.05
     assert all(math.isfinite(v) and v > 0 for v in d["kernels_ms"].values())
+    for k, st in d["kernels_ms_stats"].items():  # median and minimum over the timed steps
+        assert st["reps"] == 2 and 0 < st["min"] <= st["median"], k
 
 
 @pytest.mark.parametrize("opts", [("--kappa", "2", "--sep", "2"), ("--causal",), ("--snis", "16"), ("--backward",)])
