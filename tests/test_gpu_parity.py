@@ -441,6 +441,32 @@ def test_stable_marks_leave_the_map_unchanged(scram, work, variant):
     assert int(whole.min()) >= 0 and int(whole.max()) < cfg.Hk * cfg.Wk  # no mark leaks into the result
 
 
+def test_concurrent_calls_on_two_streams(scram, work):
+    """Two calls that run at the same time on two streams, each with its own workspace, give the maps,
+    scores and outputs of the same calls made one after the other: the library keeps no state between
+    calls outside the caller's buffers."""
+    cfg, a, dev = work
+    Q, K, V = dev["Q"], dev["K"], dev["V"]
+    T = cfg.iters
+    ref = [scram.patchmatch(Q, K, T, seed, return_score=True) for seed in (cfg.pm_seed, cfg.pm_seed + 1)]
+    ref_out = [scram.sparse_attend(Q, K, V, J, cfg.window, cfg.scale) for J, _ in ref]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    ws = [torch.empty(scram.patchmatch_workspace_bytes(cfg.S, cfg.Hq, cfg.Wq), dtype=torch.uint8, device="cuda")
+          for _ in streams]
+    res = [None, None]
+    for rep in range(3):
+        for i, (st, seed) in enumerate(zip(streams, (cfg.pm_seed, cfg.pm_seed + 1))):
+            st.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(st):
+                J, s = scram.patchmatch(Q, K, T, seed, return_score=True, workspace=ws[i])
+                res[i] = (J, s, scram.sparse_attend(Q, K, V, J, cfg.window, cfg.scale))
+        torch.cuda.synchronize()
+        for i in range(2):
+            assert torch.equal(res[i][0], ref[i][0]) and torch.equal(res[i][1], ref[i][1]), (rep, i)
+            assert torch.equal(res[i][2], ref_out[i]), (rep, i)
+
+
 # --------------------------------------------------------------------------
 # the matrix-core attend (bf16, 32 or 64 channels, windows 3/5/7, one map, no mask): maps that stress
 # its clusters of match centres and their key boxes
