@@ -157,14 +157,15 @@ __device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_
 {
 #pragma unroll
     for (int i = 0; i < 10; ++i) {
-        const uint32_t a_hi = __umulhi(0xD2511F53u, c0), a_lo = 0xD2511F53u * c0;
-        const uint32_t b_hi = __umulhi(0xCD9E8D57u, c2), b_lo = 0xCD9E8D57u * c2;
-        const uint32_t n0 = b_hi ^ c1 ^ k0;
-        const uint32_t n2 = a_hi ^ c3 ^ k1;
+        // each 64-bit product is one v_mad_u64_u32 (a multiply-high and a multiply-low would be two)
+        const uint64_t a = static_cast<uint64_t>(0xD2511F53u) * c0;
+        const uint64_t b = static_cast<uint64_t>(0xCD9E8D57u) * c2;
+        const uint32_t n0 = static_cast<uint32_t>(b >> 32) ^ c1 ^ k0;
+        const uint32_t n2 = static_cast<uint32_t>(a >> 32) ^ c3 ^ k1;
         c0 = n0;
-        c1 = b_lo;
+        c1 = static_cast<uint32_t>(b);
         c2 = n2;
-        c3 = a_lo;
+        c3 = static_cast<uint32_t>(a);
         k0 += 0x9E3779B9u;
         k1 += 0xBB67AE85u;
     }
