@@ -1,6 +1,6 @@
 // Sparse window attention (Algorithm 2, Equations 8-9).
 
-#include "scram_device.h"
+#include "scram_tile.h"
 
 namespace scram {
 namespace {
@@ -251,50 +251,6 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
 // The other keys of the box enter with weight exactly 0, which leaves the
 // sums unchanged for finite value rows (a non-finite value anywhere in the
 // box would reach every query of the cluster through 0 * inf).
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-
-// bf16 pair (a in the low half, b in the high half) from the high halves of two fp32 patterns
-__device__ __forceinline__ uint32_t hi16_pair(uint32_t a, uint32_t b) { return __builtin_amdgcn_perm(b, a, 0x07060302u); }
-
-template <int CTRL>
-__device__ __forceinline__ int dpp_i(int x)
-{
-    return __builtin_amdgcn_mov_dpp(x, CTRL, 0xF, 0xF, true);
-}
-
-// min and max over the 16 lanes of a DPP row (every lane of the row gets both)
-__device__ __forceinline__ void row_minmax(int& lo, int& hi)
-{
-    lo = min(lo, dpp_i<0xB1>(lo)), hi = max(hi, dpp_i<0xB1>(hi));
-    lo = min(lo, dpp_i<0x4E>(lo)), hi = max(hi, dpp_i<0x4E>(hi));
-    lo = min(lo, dpp_i<0x141>(lo)), hi = max(hi, dpp_i<0x141>(hi));
-    lo = min(lo, dpp_i<0x140>(lo)), hi = max(hi, dpp_i<0x140>(hi));
-}
-
-// (row, column) of raster slot j of a box `bw` wide: exact for j < 1024 and
-// bw <= 31 (the fraction of (j + 1/2) / bw stays 1/(2 bw) away from an
-// integer, far more than the float error of the product)
-__device__ __forceinline__ void box_slot(int j, int bw, float inv_bw, int& r, int& c)
-{
-    r = static_cast<int>((static_cast<float>(j) + 0.5f) * inv_bw);
-    c = j - r * bw;
-}
-
-// LDS written by some lanes of a wave and then read by others: keep the
-// compiler from moving accesses across this point (a wave's LDS instructions
-// execute in order)
-__device__ __forceinline__ void wave_lds_sync()
-{
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
-
 // (at most 96 VGPRs: five waves per SIMD hide more of the row loads than four)
 template <int D, int W>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) void attend_tile_kernel(AttParams p)
@@ -310,9 +266,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int m = lane & 15, g4 = lane >> 4;
     const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
-    // this lane's query m: a 4 x 4 quarter of an 8 x 8 block tile, else 16 consecutive items
-    const uint32_t item = p.tq.lw == 3 ? ((4u * (wave >> 1) + (m >> 2)) << 3) + 4u * (wave & 1) + (m & 3)
-                                       : 16u * wave + m;
+    const uint32_t item = tile_wave_item(p.tq, wave, m);  // this lane's query m
     uint32_t g, g0;
     const bool valid = tile_item<kBlock / 4>(p.tq, blk, item, g);
     tile_item<kBlock / 4>(p.tq, blk, 0, g0);  // item 0 of a tile is always inside the grid
@@ -344,47 +298,10 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
     }
 
     // ---- clusters of the 16 match centres and their key boxes ----
-    // Cluster c's box (rows r0 .. r0 + height - 1, columns c0 .. c0 + width - 1, `nb` blocks of 16 raster
-    // slots) is held by lane c of these registers and read back with readlane.
-    int t_r0 = 0, t_c0 = 0, t_bw = 1, t_h = 0;
-    int nclu = 0, mine = -1;
-    uint32_t todo = static_cast<uint32_t>(__ballot(valid)) & 0xFFFFu;  // bit m: query m (lanes 16.. repeat 0..15)
-    while (todo) {
-        const int a = __builtin_ctz(todo);
-        const int ua = __builtin_amdgcn_readlane(u, a), va = __builtin_amdgcn_readlane(v, a);
-        const bool mem = ((todo >> m) & 1u) && abs(u - ua) <= p.rc && abs(v - va) <= p.rc;
-        todo &= ~(static_cast<uint32_t>(__ballot(mem)) & 0xFFFFu);
-        mine = mem ? nclu : mine;
-        int ulo = mem ? u : ua, uhi = ulo, vlo = mem ? v : va, vhi = vlo;
-        row_minmax(ulo, uhi);
-        row_minmax(vlo, vhi);
-        const bool here = lane == nclu;
-        t_r0 = here ? max(ulo - B, 0) : t_r0;
-        t_c0 = here ? max(vlo - B, 0) : t_c0;
-        t_h = here ? min(uhi + B, p.Hk - 1) - max(ulo - B, 0) + 1 : t_h;
-        t_bw = here ? min(vhi + B, p.Wk - 1) - max(vlo - B, 0) + 1 : t_bw;
-        ++nclu;
-    }
-    if (nclu == 0) return;  // no query of this wave lies inside the grid
-    // the rest of each cluster's scalars, once for all clusters: blocks of 16 slots, and the step of 16
-    // raster slots as q16 rows and r16 columns
-    const float t_inv = __builtin_amdgcn_rcpf(static_cast<float>(t_bw));
-    const int t_nb = (t_h * t_bw + 15) >> 4;
-    int t_q16, t_r16;
-    box_slot(16, t_bw, t_inv, t_q16, t_r16);
-    // the window of query m in its cluster's box: rows wr0 .. wr0 + wrn, and a bit per box column
-    int wr0 = 0, wrn = -1;
-    uint32_t wcols = 0;
-    {
-        const int mc = max(mine, 0);
-        const int r0 = __shfl(t_r0, mc), c0 = __shfl(t_c0, mc), bw = __shfl(t_bw, mc), h = __shfl(t_h, mc);
-        if (mine >= 0) {
-            wr0 = u - B - r0;
-            wrn = min(u + B - r0, h - 1) - wr0;
-            const int lo = max(v - B - c0, 0), hi = min(v + B - c0, bw - 1);  // box columns, bw <= 31
-            wcols = ((2u << hi) - 1u) & ~((1u << lo) - 1u);
-        }
-    }
+    const TileClusters tc = tile_clusters<B>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk);
+    if (tc.nclu == 0) return;  // no query of this wave lies inside the grid
+    const int nclu = tc.nclu, mine = tc.mine, wr0 = tc.wr0, wrn = tc.wrn;
+    const uint32_t wcols = tc.wcols;
 
     const f32x4_t zero = f32x4_t{0.f, 0.f, 0.f, 0.f};
     f32x4_t acc[kOt];
@@ -433,28 +350,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
     // value row 4 g4 + m / 4 at channels 4 (m mod 4) .. + 3 (+ 16 o) and receives rows 4 g4 .. + 3 at
     // channel 16 o + m
     const unsigned char* const tvt = tv + (4 * g4 + (m >> 2)) * kRowB + 8 * (m & 3);
-    // A cluster's scalars, read from the lanes that hold them
-    struct Box {
-        int r0, c0, bw, nb, q16, r16;
-        float inv;
-        uint32_t kstep, kstep_wrap;  // key index change of a 16-slot step, without and with a column carry
-        uint32_t klast;              // key index of the box's last slot
-    };
-    auto box_of = [&](int cl) {
-        Box bx;
-        bx.r0 = __builtin_amdgcn_readlane(t_r0, cl);
-        bx.c0 = __builtin_amdgcn_readlane(t_c0, cl);
-        bx.bw = __builtin_amdgcn_readlane(t_bw, cl);
-        bx.nb = __builtin_amdgcn_readlane(t_nb, cl);
-        bx.q16 = __builtin_amdgcn_readlane(t_q16, cl);
-        bx.r16 = __builtin_amdgcn_readlane(t_r16, cl);
-        bx.inv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(t_inv), cl));
-        bx.kstep = static_cast<uint32_t>(bx.q16) * static_cast<uint32_t>(p.Wk) + bx.r16;
-        bx.kstep_wrap = bx.kstep + p.Wk - bx.bw;
-        const int h = __builtin_amdgcn_readlane(t_h, cl);
-        bx.klast = static_cast<uint32_t>(bx.r0 + h - 1) * static_cast<uint32_t>(p.Wk) + (bx.c0 + bx.bw - 1);
-        return bx;
-    };
+    using Box = TileBox;
+    auto box_of = [&](int cl) { return tile_box(tc, cl, p.Wk); };
 
     uint4 kr0, kr1, vr0, vr1;  // this lane's pieces of the rows in flight
     // a slot past the box's last row (weight 0) reads the box's last row, which the block holds anyway
@@ -502,23 +399,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
             sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ds], sc, 0, 0, 0);
         }
         // which of the 4 slots lie in query m's window (bit i: slot 16 k + 4 g4 + i)
-        uint32_t bits = 0;
-        if (bx.bw >= 3) {  // the 4 slots span at most two box rows: columns mcl .. mcl + 3 of row, next row
-            const bool ok0 = static_cast<unsigned>(rr) <= static_cast<unsigned>(wrn);
-            const bool ok1 = static_cast<unsigned>(rr + 1) <= static_cast<unsigned>(wrn);
-            bits = __builtin_amdgcn_ubfe((ok0 ? wc : 0u) | (ok1 ? wc2 : 0u), mcl, 4);
-        } else {  // boxes one or two columns wide (grids that narrow): slot by slot
-            int r = rr, cc = mcl;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const bool ok = static_cast<unsigned>(r) <= static_cast<unsigned>(wrn) && ((wc >> cc) & 1u);
-                bits |= ok ? 1u << i : 0u;
-                ++cc;
-                const bool wrap = cc == bx.bw;
-                cc = wrap ? 0 : cc;
-                r += wrap ? 1 : 0;
-            }
-        }
+        const uint32_t bits = tile_window_bits(bx, rr, mcl, wrn, wc, wc2);
         // all ones for the slots of the window, zero elsewhere (one signed bit-field extract each)
         uint32_t keep[4];
 #pragma unroll

@@ -1,6 +1,6 @@
 // Backward of the sparse window attention with the maps held fixed.
 
-#include "scram_device.h"
+#include "scram_tile.h"
 
 namespace scram {
 namespace {
@@ -61,6 +61,7 @@ struct BwdParams {
     float scale_log2e;
     int kappa;
     int causal;
+    int rc;                // cluster radius of the matrix-core query kernel
 };
 
 // a[0 .. count) = 0 and, when given, *word = 0
@@ -687,9 +688,6 @@ __global__ __launch_bounds__(kBlock) void bwd_heavy_kernel(BwdParams p)
 // P and dS enter as three bf16 parts that add up to the fp32 values exactly
 // (products of bf16 parts are exact); all sums are fp32.
 // ---------------------------------------------------------------------------
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-
 constexpr int kTileKeys = 64;                          // keys per block, 16 per wave
 constexpr int kTileMaxB = 7;                           // windows up to 15 x 15
 constexpr int kStripMaxRows = 16 + 2 * kTileMaxB;      // halo rows of the tallest strip (16 x 1)
@@ -716,22 +714,6 @@ __device__ __forceinline__ void split3(float x, uint32_t& hi, uint32_t& mid, uin
     const float r1 = x - __uint_as_float(hi);
     mid = __float_as_uint(r1) & 0xFFFF0000u;
     lo = __float_as_uint(r1 - __uint_as_float(mid));
-}
-
-// bf16 pair (a in the low half, b in the high half) from the high halves of two fp32 patterns
-__device__ __forceinline__ uint32_t pack_hi16(uint32_t a, uint32_t b)
-{
-    return __builtin_amdgcn_perm(b, a, 0x07060302u);
-}
-
-// LDS written by some lanes of a wave and then read by others: keep the
-// compiler from moving accesses across this point (a wave's LDS instructions
-// execute in order)
-__device__ __forceinline__ void wave_lds_sync()
-{
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 __device__ __forceinline__ bf16x8_t lds_frag(const unsigned char* p)
@@ -936,8 +918,8 @@ bwd_key_strip_kernel(BwdParams p)
             }
         }
         auto operand = [](const uint32_t (&v)[8]) {
-            return __builtin_bit_cast(bf16x8_t, make_uint4(pack_hi16(v[0], v[1]), pack_hi16(v[2], v[3]),
-                                                           pack_hi16(v[4], v[5]), pack_hi16(v[6], v[7])));
+            return __builtin_bit_cast(bf16x8_t, make_uint4(hi16_pair(v[0], v[1]), hi16_pair(v[2], v[3]),
+                                                           hi16_pair(v[4], v[5]), hi16_pair(v[6], v[7])));
         };
         const bf16x8_t aph = operand(ph), apm = operand(pm), apl = operand(pl);
         const bf16x8_t ash = operand(sh), asm_ = operand(sm), asl = operand(sl);
@@ -953,10 +935,10 @@ bwd_key_strip_kernel(BwdParams p)
             const f32x4_t g1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ag[1][ds], eye[h], zero, 0, 0, 0);
             auto bop = [](const f32x4_t& a, const f32x4_t& b) {
                 return __builtin_bit_cast(
-                    bf16x8_t, make_uint4(pack_hi16(__float_as_uint(a[0]), __float_as_uint(a[1])),
-                                         pack_hi16(__float_as_uint(a[2]), __float_as_uint(a[3])),
-                                         pack_hi16(__float_as_uint(b[0]), __float_as_uint(b[1])),
-                                         pack_hi16(__float_as_uint(b[2]), __float_as_uint(b[3]))));
+                    bf16x8_t, make_uint4(hi16_pair(__float_as_uint(a[0]), __float_as_uint(a[1])),
+                                         hi16_pair(__float_as_uint(a[2]), __float_as_uint(a[3])),
+                                         hi16_pair(__float_as_uint(b[0]), __float_as_uint(b[1])),
+                                         hi16_pair(__float_as_uint(b[2]), __float_as_uint(b[3]))));
             };
             const bf16x8_t bq = bop(q0, q1), bg = bop(g0, g1);
             dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aph, bg, dv[o], 0, 0, 0);
@@ -984,6 +966,307 @@ bwd_key_strip_kernel(BwdParams p)
     }
 }
 
+// ---------------------------------------------------------------------------
+// Query side on the matrix cores (bf16 storage, d 32 or 64, windows 3/5/7,
+// one map, no mask).  The wave's 16 queries, their clusters and key boxes are
+// those of the attend's matrix-core kernel (scram_tile.h); the key and value
+// rows of a box are read a block of 16 keys at a time, staged in LDS, and per
+// block (lane (m, g4): keys 4 g4 + i, query m)
+//   S^T = K_blk Q^T,  dP^T = V_blk dO^T          keys x queries, 16x16x32 bf16
+//   p = 2^(s scale log2e - m_ref) on the query's window, 0 elsewhere; pd = p dp
+//   B^T += K_blk^T P^T,  A^T += K_blk^T PD^T     channels x queries: K_blk^T by
+//                                                the transposing LDS load
+//   l += 1^T P^T,  dn += 1^T PD^T               all-ones blocks
+// with P and PD as three bf16 parts each (they add up to the fp32 values
+// exactly).  With D_i = dn / l and the match's key k_ref,
+//   dQ_i = scale ((A - dn k_ref) - D_i (B - l k_ref)) / l
+//        = scale sum_j p_ij (dp_ij - D_i)(k_j - k_ref) / l
+// the sums of the lane-group kernel, formed from the same rounded weights on
+// both sides, so the subtraction cancels no more than there.  Also writes the
+// per-query statistics and the inverse map's count and slot of the query's
+// match, as the lane-group kernel does.
+template <int D, int W>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) void bwd_query_tile_kernel(BwdParams p)
+{
+    constexpr int B = W / 2;
+    constexpr int kDs = D / 32;        // 32-channel contraction steps of S^T and dP^T
+    constexpr int kOt = D / 16;        // 16-channel tiles of A^T, B^T
+    constexpr int kRowB = 2 * D + 16;  // LDS row stride, bytes (padded)
+    constexpr int kPer = D / 32;       // 16-byte pieces per lane: a row (D / 8 pieces) is read by 4 consecutive lanes
+    constexpr int kWaves = kBlock / 64;
+#ifndef SCRAM_BWD_TILE_PARTS
+#define SCRAM_BWD_TILE_PARTS 3
+#endif
+    constexpr int kParts = SCRAM_BWD_TILE_PARTS;  // bf16 parts of each weight
+    static_assert(kPer == 1 || kPer == 2, "32 or 64 channels");
+    __shared__ __align__(16) unsigned char s_k[kWaves][16 * kRowB], s_v[kWaves][16 * kRowB];
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int m = lane & 15, g4 = lane >> 4;
+    const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+    uint32_t g, g0;
+    const bool valid = tile_item<kBlock / 4>(p.tq, blk, tile_wave_item(p.tq, wave, m), g);
+    tile_item<kBlock / 4>(p.tq, blk, 0, g0);  // item 0 of a tile is always inside the grid
+    const uint32_t gq = valid ? g : g0;
+    uint32_t s, rem;
+    divmod(gq, p.div_plane, s, rem);
+    // the slice's key and value rows as 32-bit byte offsets from a wave-uniform base (the caller keeps
+    // a slice's rows below 4 GiB)
+    const size_t slice_bytes =
+        static_cast<size_t>(__builtin_amdgcn_readfirstlane(s)) * p.nkeys * static_cast<size_t>(2 * D);
+    const unsigned char* const Kb = static_cast<const unsigned char*>(p.K) + slice_bytes;
+    const unsigned char* const Vb = static_cast<const unsigned char*>(p.V) + slice_bytes;
+    const uint32_t centre = static_cast<uint32_t>(clamp_index(p.J[gq], p.nkeys));
+    // the inverse map's count: one entry per query, and its slot among the entries of its match key
+    if (valid && g4 == 0)
+        p.slots[g] = atomicAdd(p.counts + static_cast<size_t>(s) * p.nkeys + centre, 1);
+    int u, v;
+    {
+        uint32_t uu, vv;
+        divmod(centre, p.div_wk, uu, vv);
+        u = static_cast<int>(uu);
+        v = static_cast<int>(vv);
+    }
+    // B operands of S^T and dP^T: query m, channels 32 ds + 8 g4 .. + 7 of q and dO; the same channels
+    // of the match's key
+    bf16x8_t qf[kDs], gf[kDs];
+    uint4 kc[kDs];
+    const uint16_t* const qrow = static_cast<const uint16_t*>(p.Q) + static_cast<size_t>(gq) * D;
+    const uint16_t* const grow = static_cast<const uint16_t*>(p.dO) + static_cast<size_t>(gq) * D;
+#pragma unroll
+    for (int ds = 0; ds < kDs; ++ds) {
+        qf[ds] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(qrow + 32 * ds + 8 * g4));
+        gf[ds] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(grow + 32 * ds + 8 * g4));
+        kc[ds] = *reinterpret_cast<const uint4*>(Kb + centre * (2u * D) + 64u * ds + 16u * g4);
+    }
+
+    const TileClusters tc = tile_clusters<B>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk);
+    if (tc.nclu == 0) return;  // no query of this wave lies inside the grid
+
+    const f32x4_t zero = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    f32x4_t acc_a[kOt], acc_b[kOt];
+#pragma unroll
+    for (int o = 0; o < kOt; ++o) acc_a[o] = acc_b[o] = zero;
+    f32x4_t lacc = zero, dacc = zero;  // every row: sum of p, sum of p dp, of query m
+    const bf16x4_t ones = bf16x4_t{static_cast<__bf16>(1.f), static_cast<__bf16>(1.f), static_cast<__bf16>(1.f),
+                                   static_cast<__bf16>(1.f)};
+    const float sl2e = p.scale_log2e;  // > 0 (the caller routes other scales to the lane-group kernels)
+    const float inv_sl2e = __builtin_amdgcn_rcpf(sl2e);
+    int bit_at[4];  // 0..3 as values the compiler cannot see: one bit-field extract per mask below
+#pragma unroll
+    for (int i = 0; i < 4; ++i) asm volatile("s_mov_b32 %0, %1" : "=s"(bit_at[i]) : "i"(i));
+    // online softmax state of query m, starting at the score of its match (a key of its window), as in
+    // the attend's matrix-core kernel
+    float s_centre = 0.f;
+#pragma unroll
+    for (int ds = 0; ds < kDs; ++ds) {
+        const uint4 qa = __builtin_bit_cast(uint4, qf[ds]);
+        s_centre = dot2_bf16(qa.x, kc[ds].x, s_centre);
+        s_centre = dot2_bf16(qa.y, kc[ds].y, s_centre);
+        s_centre = dot2_bf16(qa.z, kc[ds].z, s_centre);
+        s_centre = dot2_bf16(qa.w, kc[ds].w, s_centre);
+    }
+    s_centre += __shfl_xor(s_centre, 16);
+    s_centre += __shfl_xor(s_centre, 32);
+    float mref = s_centre * sl2e, nref = -mref;
+    const float thr_q = (mref + (kRescaleSlack - 1.f)) * inv_sl2e;
+    float thr = INFINITY;
+
+    const int lslot = lane >> 2, lpiece = lane & 3;  // every lane: one key slot, 16-byte pieces lpiece (+ 4)
+    unsigned char* const tk = s_k[wave];
+    unsigned char* const tv = s_v[wave];
+    // A operand of A^T, B^T for tile o: lane (m, g4) addresses key row 4 g4 + m / 4 at channels
+    // 4 (m mod 4) .. + 3 (+ 16 o) and the transposing load hands it rows 4 g4 .. + 3 at channel 16 o + m
+    const unsigned char* const tkt = tk + (4 * g4 + (m >> 2)) * kRowB + 8 * (m & 3);
+    const uint4 z4 = make_uint4(0u, 0u, 0u, 0u);
+    uint4 kr0 = z4, kr1 = z4, vr0 = z4, vr1 = z4;  // this lane's pieces of the rows in flight
+    auto load = [&](uint32_t key, uint32_t klast) {  // a slot past the box's last row reads its last row
+        const uint32_t off = min(key, klast) * (2u * D) + 16u * lpiece;
+        kr0 = *reinterpret_cast<const uint4*>(Kb + off);
+        vr0 = *reinterpret_cast<const uint4*>(Vb + off);
+        if constexpr (kPer == 2) {
+            kr1 = *reinterpret_cast<const uint4*>(Kb + off + 64);
+            vr1 = *reinterpret_cast<const uint4*>(Vb + off + 64);
+        }
+    };
+    auto stage = [&]() {
+        const int off = lslot * kRowB + 16 * lpiece;
+        *reinterpret_cast<uint4*>(tk + off) = kr0;
+        *reinterpret_cast<uint4*>(tv + off) = vr0;
+        if constexpr (kPer == 2) {
+            *reinterpret_cast<uint4*>(tk + off + 64) = kr1;
+            *reinterpret_cast<uint4*>(tv + off + 64) = vr1;
+        }
+    };
+    auto first_slot = [&](const TileBox& b, int& lc, uint32_t& lkey) {
+        int lr;
+        box_slot(lslot, b.bw, b.inv, lr, lc);
+        lkey = static_cast<uint32_t>(b.r0 + lr) * static_cast<uint32_t>(p.Wk) + (b.c0 + lc);
+    };
+    auto step_slot = [](const TileBox& b, int& lc, uint32_t& lkey) {  // 16 slots on
+        lc += b.r16;
+        const bool carry = lc >= b.bw;
+        lc -= carry ? b.bw : 0;
+        lkey += carry ? b.kstep_wrap : b.kstep;
+    };
+    // the weights as bf16 parts: hi + mid + lo exactly (kParts 3), or hi + the top 8 bits of the rest
+    auto pack3 = [](const uint32_t (&x)[4], bf16x4_t& h, bf16x4_t& md, bf16x4_t& lo) {
+        uint32_t a[4], b[4], c[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if constexpr (kParts == 3) {
+                split3(__uint_as_float(x[i]), a[i], b[i], c[i]);
+            } else {
+                a[i] = x[i] & 0xFFFF0000u;
+                b[i] = __float_as_uint(__uint_as_float(x[i]) - __uint_as_float(a[i]));
+                c[i] = 0u;
+            }
+        }
+        h = __builtin_bit_cast(bf16x4_t, make_uint2(hi16_pair(a[0], a[1]), hi16_pair(a[2], a[3])));
+        md = __builtin_bit_cast(bf16x4_t, make_uint2(hi16_pair(b[0], b[1]), hi16_pair(b[2], b[3])));
+        lo = __builtin_bit_cast(bf16x4_t, make_uint2(hi16_pair(c[0], c[1]), hi16_pair(c[2], c[3])));
+    };
+    auto compute = [&](const TileBox& bx, int rr, int mcl, uint32_t wc, uint32_t wc2) {
+        f32x4_t sc = zero, dp = zero;
+#pragma unroll
+        for (int ds = 0; ds < kDs; ++ds) {
+            const bf16x8_t kf = __builtin_bit_cast(
+                bf16x8_t, *reinterpret_cast<const uint4*>(tk + m * kRowB + 16 * (4 * ds + g4)));
+            const bf16x8_t vf = __builtin_bit_cast(
+                bf16x8_t, *reinterpret_cast<const uint4*>(tv + m * kRowB + 16 * (4 * ds + g4)));
+            sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ds], sc, 0, 0, 0);
+            dp = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, gf[ds], dp, 0, 0, 0);
+        }
+        const uint32_t bits = tile_window_bits(bx, rr, mcl, tc.wrn, wc, wc2);
+        uint32_t keep[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            keep[i] = static_cast<uint32_t>(__builtin_amdgcn_sbfe(static_cast<int>(bits), bit_at[i], 1));
+        if (__ballot((sc[0] > thr) | (sc[1] > thr) | (sc[2] > thr) | (sc[3] > thr))) {
+            float mx = -INFINITY;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) mx = fmaxf(mx, keep[i] ? sc[i] : -INFINITY);
+            mx *= sl2e;
+            mx = fmaxf(mx, __shfl_xor(mx, 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            if (mx > mref + kRescaleSlack) {
+                const float alpha = __builtin_amdgcn_exp2f(mref - mx);
+                lacc *= alpha;
+                dacc *= alpha;
+#pragma unroll
+                for (int o = 0; o < kOt; ++o) {
+                    acc_a[o] *= alpha;
+                    acc_b[o] *= alpha;
+                }
+                mref = mx;
+                nref = -mx;
+                thr = (mx + (kRescaleSlack - 1.f)) * inv_sl2e;
+            }
+        }
+        uint32_t pw[4], pdw[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t x = __float_as_uint(fmaf(sc[i], sl2e, nref));
+            const float pk = __builtin_amdgcn_exp2f(__uint_as_float((x & keep[i]) | (0xFF800000u & ~keep[i])));
+            pw[i] = __float_as_uint(pk);
+            pdw[i] = __float_as_uint(pk * dp[i]);
+        }
+        bf16x4_t ph, pm, pl, dh, dm, dl;
+        pack3(pw, ph, pm, pl);
+        pack3(pdw, dh, dm, dl);
+        lacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ones, ph, lacc, 0, 0, 0);
+        lacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ones, pm, lacc, 0, 0, 0);
+        dacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ones, dh, dacc, 0, 0, 0);
+        dacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ones, dm, dacc, 0, 0, 0);
+        if constexpr (kParts == 3) {
+            lacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ones, pl, lacc, 0, 0, 0);
+            dacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ones, dl, dacc, 0, 0, 0);
+        }
+#pragma unroll
+        for (int o = 0; o < kOt; ++o) {
+            const bf16x4_t kt = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                (__attribute__((address_space(3))) bf16x4_t*)(tkt + 32 * o));
+            acc_b[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(kt, ph, acc_b[o], 0, 0, 0);
+            acc_b[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(kt, pm, acc_b[o], 0, 0, 0);
+            acc_a[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(kt, dh, acc_a[o], 0, 0, 0);
+            acc_a[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(kt, dm, acc_a[o], 0, 0, 0);
+            if constexpr (kParts == 3) {
+                acc_b[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(kt, pl, acc_b[o], 0, 0, 0);
+                acc_a[o] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(kt, dl, acc_a[o], 0, 0, 0);
+            }
+        }
+    };
+
+    // the blocks of each cluster in a row; each block's rows load during the previous block's products
+    TileBox bx = tile_box(tc, 0, p.Wk);
+    int lc;
+    uint32_t lkey;
+    first_slot(bx, lc, lkey);
+    load(lkey, bx.klast);
+    for (int c = 0;;) {
+        int mr, mcl;
+        box_slot(4 * g4, bx.bw, bx.inv, mr, mcl);
+        int rr = mr - tc.wr0;
+        const bool here = c == tc.mine;
+        const uint32_t wc = here ? tc.wcols : 0u;
+        const uint32_t wc2 = here ? tc.wcols << bx.bw : 0u;  // bw <= 19, and only bits below bw + 3 are read
+        thr = here ? thr_q : INFINITY;  // a query's cluster is visited once, its blocks in a row
+        step_slot(bx, lc, lkey);
+        for (int k = 1; k < bx.nb; ++k) {
+            stage();
+            load(lkey, bx.klast);
+            step_slot(bx, lc, lkey);
+            wave_lds_sync();
+            compute(bx, rr, mcl, wc, wc2);
+            mcl += bx.r16;
+            const bool carry = mcl >= bx.bw;
+            mcl -= carry ? bx.bw : 0;
+            rr += bx.q16 + (carry ? 1 : 0);
+            wave_lds_sync();  // this block's LDS reads come before the next block's writes
+        }
+        stage();
+        const bool more = c + 1 < tc.nclu;
+        TileBox nx = bx;
+        if (more) {
+            nx = tile_box(tc, c + 1, p.Wk);
+            first_slot(nx, lc, lkey);
+            load(lkey, nx.klast);
+        }
+        wave_lds_sync();
+        compute(bx, rr, mcl, wc, wc2);
+        if (!more) break;
+        bx = nx;
+        ++c;
+        wave_lds_sync();
+    }
+    if (!valid) return;
+    const float l = lacc[0], dn = dacc[0];
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+    const float Dg = dn * inv;
+    if (g4 == 0) {
+        p.lse2[g] = l > 0.f ? mref + log2f(l) : INFINITY;  // +inf: every weight is 0
+        p.Dq[g] = Dg;
+    }
+    // lane holds channels 16 o + 4 g4 + i of query m
+    const uint16_t* const krow = static_cast<const uint16_t*>(static_cast<const void*>(Kb + centre * (2u * D)));
+    float* const dq = p.dQ + static_cast<size_t>(g) * D;
+#pragma unroll
+    for (int o = 0; o < kOt; ++o) {
+        const uint2 kw = *reinterpret_cast<const uint2*>(krow + 16 * o + 4 * g4);
+        const float kref[4] = {__uint_as_float(kw.x << 16), __uint_as_float(kw.x & 0xFFFF0000u),
+                               __uint_as_float(kw.y << 16), __uint_as_float(kw.y & 0xFFFF0000u)};
+        float r[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            r[i] = ((acc_a[o][i] - dn * kref[i]) - Dg * (acc_b[o][i] - l * kref[i])) * inv * p.scale;
+        *reinterpret_cast<float4*>(dq + 16 * o + 4 * g4) = make_float4(r[0], r[1], r[2], r[3]);
+    }
+}
+
+#ifndef SCRAM_BWD_QUERY_TILE
+#define SCRAM_BWD_QUERY_TILE 1
+#endif
+
 // The query kernel, then the rest of the inverse map (inverse()), then the
 // key side.
 template <typename T, int D, typename Inverse>
@@ -1006,11 +1289,29 @@ hipError_t run_backward(const BwdParams& p0, hipStream_t st, hipEvent_t* ev, Inv
                      : launch(bwd_query_kernel<T, D, G, false, W>, qblocks, st, nullptr, q1, p);
     };
     const int side = 2 * p.b + 1;
-    hipError_t e = side == 1   ? query(std::integral_constant<int, 1>{})
-                   : side == 3 ? query(std::integral_constant<int, 3>{})
-                   : side == 5 ? query(std::integral_constant<int, 5>{})
-                   : side == 7 ? query(std::integral_constant<int, 7>{})
-                               : query(std::integral_constant<int, 0>{});
+    // the matrix-core query kernel takes bf16 storage with 32 or 64 channels, one map, no mask, windows
+    // 3, 5 or 7, a positive scale and slices of at most 4 GiB of key rows
+    hipError_t e = hipSuccess;
+    bool tile = false;
+    if constexpr (SCRAM_BWD_QUERY_TILE && std::is_same<T, uint16_t>::value && (D == 32 || D == 64)) {
+        if (!multi && (side == 3 || side == 5 || side == 7) && p.scale_log2e > 0.f &&
+            static_cast<uint64_t>(p.nkeys) * (2 * D) <= 0xFFFFFFFFull) {
+            BwdParams pq = p;
+            pq.tq = make_tiling(p.Hq, p.Wq, kBlock / 4);
+            pq.rc = 6;  // as in the attend's matrix-core kernel
+            const uint64_t tb = tiling_blocks(pq.tq, p.n / pq.tq.plane);
+            e = side == 3   ? launch(bwd_query_tile_kernel<D, 3>, tb, st, nullptr, q1, pq)
+                : side == 5 ? launch(bwd_query_tile_kernel<D, 5>, tb, st, nullptr, q1, pq)
+                            : launch(bwd_query_tile_kernel<D, 7>, tb, st, nullptr, q1, pq);
+            tile = true;
+        }
+    }
+    if (!tile)
+        e = side == 1   ? query(std::integral_constant<int, 1>{})
+            : side == 3 ? query(std::integral_constant<int, 3>{})
+            : side == 5 ? query(std::integral_constant<int, 5>{})
+            : side == 7 ? query(std::integral_constant<int, 7>{})
+                        : query(std::integral_constant<int, 0>{});
     if (e != hipSuccess) return e;
     if ((e = inverse()) != hipSuccess) return e;
     if constexpr (std::is_same<T, uint16_t>::value) {

@@ -1,0 +1,181 @@
+// Matrix-core pieces shared by the attend (scram_attend.hip) and its backward
+// (scram_backward.hip) for bf16 storage on gfx950.
+//
+// A wave takes 16 queries (a 4 x 4 quarter of an 8 x 8 block tile, or 16
+// consecutive items of narrower tiles); lane l works on query m = l mod 16
+// with lane group g4 = l div 16, so lanes 16.. repeat the queries of 0..15.
+// Neighbouring queries' windows overlap, so the 16 match centres are grouped
+// into clusters -- a query joins the cluster of the first unassigned query
+// whose centre lies within Chebyshev distance rc -- and each cluster's key box
+// (its members' windows, clipped to the grid) is visited in blocks of 16 keys
+// in raster order.  Every query is in exactly one cluster and each key of its
+// window is in that cluster's box exactly once.
+//
+// Everything here lives in an unnamed namespace, like scram_device.h.
+
+#pragma once
+
+#include "scram_device.h"
+
+namespace scram {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// bf16 pair (a in the low half, b in the high half) from the high halves of two fp32 patterns
+__device__ __forceinline__ uint32_t hi16_pair(uint32_t a, uint32_t b) { return __builtin_amdgcn_perm(b, a, 0x07060302u); }
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int x)
+{
+    return __builtin_amdgcn_mov_dpp(x, CTRL, 0xF, 0xF, true);
+}
+
+// min and max over the 16 lanes of a DPP row (every lane of the row gets both)
+__device__ __forceinline__ void row_minmax(int& lo, int& hi)
+{
+    lo = min(lo, dpp_i<0xB1>(lo)), hi = max(hi, dpp_i<0xB1>(hi));
+    lo = min(lo, dpp_i<0x4E>(lo)), hi = max(hi, dpp_i<0x4E>(hi));
+    lo = min(lo, dpp_i<0x141>(lo)), hi = max(hi, dpp_i<0x141>(hi));
+    lo = min(lo, dpp_i<0x140>(lo)), hi = max(hi, dpp_i<0x140>(hi));
+}
+
+// (row, column) of raster slot j of a box `bw` wide: exact for j < 1024 and
+// bw <= 31 (the fraction of (j + 1/2) / bw stays 1/(2 bw) away from an
+// integer, far more than the float error of the product)
+__device__ __forceinline__ void box_slot(int j, int bw, float inv_bw, int& r, int& c)
+{
+    r = static_cast<int>((static_cast<float>(j) + 0.5f) * inv_bw);
+    c = j - r * bw;
+}
+
+// LDS written by some lanes of a wave and then read by others: keep the
+// compiler from moving accesses across this point (a wave's LDS instructions
+// execute in order)
+__device__ __forceinline__ void wave_lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// The item of a block tile that lane (m, wave) works on: a 4 x 4 quarter of an
+// 8 x 8 tile (lw == 3), else 16 consecutive items.
+__device__ __forceinline__ uint32_t tile_wave_item(const Tiling& tq, int wave, int m)
+{
+    return tq.lw == 3 ? ((4u * (wave >> 1) + (m >> 2)) << 3) + 4u * (wave & 1) + (m & 3) : 16u * wave + m;
+}
+
+// A wave's clusters.  Cluster c's box (rows r0 .. r0 + h - 1, columns
+// c0 .. c0 + bw - 1, nb blocks of 16 raster slots, a 16-slot step of q16 rows
+// and r16 columns) is held by lane c of the t_ registers and read back with
+// readlane; query m's window in its own cluster's box is rows wr0 .. wr0 + wrn
+// with a bit per box column in wcols.
+struct TileClusters {
+    int t_r0, t_c0, t_bw, t_h, t_nb, t_q16, t_r16;
+    float t_inv;
+    int nclu, mine;
+    int wr0, wrn;
+    uint32_t wcols;
+};
+
+// Clusters of the 16 centres (u, v) of a wave (windows of half side B, key
+// grid Hk x Wk, cluster radius rc).  nclu == 0 when no query of the wave is
+// valid.
+template <int B>
+__device__ __forceinline__ TileClusters tile_clusters(bool valid, int u, int v, int m, int lane, int rc, int Hk,
+                                                      int Wk)
+{
+    TileClusters tc;
+    int t_r0 = 0, t_c0 = 0, t_bw = 1, t_h = 0;
+    int nclu = 0, mine = -1;
+    uint32_t todo = static_cast<uint32_t>(__ballot(valid)) & 0xFFFFu;  // bit m: query m (lanes 16.. repeat 0..15)
+    while (todo) {
+        const int a = __builtin_ctz(todo);
+        const int ua = __builtin_amdgcn_readlane(u, a), va = __builtin_amdgcn_readlane(v, a);
+        const bool mem = ((todo >> m) & 1u) && abs(u - ua) <= rc && abs(v - va) <= rc;
+        todo &= ~(static_cast<uint32_t>(__ballot(mem)) & 0xFFFFu);
+        mine = mem ? nclu : mine;
+        int ulo = mem ? u : ua, uhi = ulo, vlo = mem ? v : va, vhi = vlo;
+        row_minmax(ulo, uhi);
+        row_minmax(vlo, vhi);
+        const bool here = lane == nclu;
+        t_r0 = here ? max(ulo - B, 0) : t_r0;
+        t_c0 = here ? max(vlo - B, 0) : t_c0;
+        t_h = here ? min(uhi + B, Hk - 1) - max(ulo - B, 0) + 1 : t_h;
+        t_bw = here ? min(vhi + B, Wk - 1) - max(vlo - B, 0) + 1 : t_bw;
+        ++nclu;
+    }
+    tc.t_r0 = t_r0, tc.t_c0 = t_c0, tc.t_bw = t_bw, tc.t_h = t_h, tc.nclu = nclu, tc.mine = mine;
+    // the rest of each cluster's scalars, once for all clusters
+    tc.t_inv = __builtin_amdgcn_rcpf(static_cast<float>(t_bw));
+    tc.t_nb = (t_h * t_bw + 15) >> 4;
+    box_slot(16, t_bw, tc.t_inv, tc.t_q16, tc.t_r16);
+    tc.wr0 = 0, tc.wrn = -1, tc.wcols = 0;
+    const int mc = max(mine, 0);
+    const int r0 = __shfl(t_r0, mc), c0 = __shfl(t_c0, mc), bw = __shfl(t_bw, mc), h = __shfl(t_h, mc);
+    if (mine >= 0) {
+        tc.wr0 = u - B - r0;
+        tc.wrn = min(u + B - r0, h - 1) - tc.wr0;
+        const int lo = max(v - B - c0, 0), hi = min(v + B - c0, bw - 1);  // box columns, bw <= 31
+        tc.wcols = ((2u << hi) - 1u) & ~((1u << lo) - 1u);
+    }
+    return tc;
+}
+
+// A cluster's scalars, read from the lanes that hold them.
+struct TileBox {
+    int r0, c0, bw, nb, q16, r16;
+    float inv;
+    uint32_t kstep, kstep_wrap;  // key index change of a 16-slot step, without and with a column carry
+    uint32_t klast;              // key index of the box's last slot
+};
+
+__device__ __forceinline__ TileBox tile_box(const TileClusters& tc, int cl, int Wk)
+{
+    TileBox bx;
+    bx.r0 = __builtin_amdgcn_readlane(tc.t_r0, cl);
+    bx.c0 = __builtin_amdgcn_readlane(tc.t_c0, cl);
+    bx.bw = __builtin_amdgcn_readlane(tc.t_bw, cl);
+    bx.nb = __builtin_amdgcn_readlane(tc.t_nb, cl);
+    bx.q16 = __builtin_amdgcn_readlane(tc.t_q16, cl);
+    bx.r16 = __builtin_amdgcn_readlane(tc.t_r16, cl);
+    bx.inv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(tc.t_inv), cl));
+    bx.kstep = static_cast<uint32_t>(bx.q16) * static_cast<uint32_t>(Wk) + bx.r16;
+    bx.kstep_wrap = bx.kstep + Wk - bx.bw;
+    const int h = __builtin_amdgcn_readlane(tc.t_h, cl);
+    bx.klast = static_cast<uint32_t>(bx.r0 + h - 1) * static_cast<uint32_t>(Wk) + (bx.c0 + bx.bw - 1);
+    return bx;
+}
+
+// Which of the 4 slots 16 k + 4 g4 + i of a block lie in query m's window (bit i), for the slot
+// 16 k + 4 g4 at box row wr0 + rr, column mcl; wc and wc2 are the window's column bits of that row
+// and of the next one (shifted past the row's end), zero outside query m's own cluster.
+__device__ __forceinline__ uint32_t tile_window_bits(const TileBox& bx, int rr, int mcl, int wrn, uint32_t wc,
+                                                     uint32_t wc2)
+{
+    uint32_t bits = 0;
+    if (bx.bw >= 3) {  // the 4 slots span at most two box rows: columns mcl .. mcl + 3 of row, next row
+        const bool ok0 = static_cast<unsigned>(rr) <= static_cast<unsigned>(wrn);
+        const bool ok1 = static_cast<unsigned>(rr + 1) <= static_cast<unsigned>(wrn);
+        bits = __builtin_amdgcn_ubfe((ok0 ? wc : 0u) | (ok1 ? wc2 : 0u), mcl, 4);
+    } else {  // boxes one or two columns wide (grids that narrow): slot by slot
+        int r = rr, cc = mcl;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const bool ok = static_cast<unsigned>(r) <= static_cast<unsigned>(wrn) && ((wc >> cc) & 1u);
+            bits |= ok ? 1u << i : 0u;
+            ++cc;
+            const bool wrap = cc == bx.bw;
+            cc = wrap ? 0 : cc;
+            r += wrap ? 1 : 0;
+        }
+    }
+    return bits;
+}
+
+}  // namespace
+}  // namespace scram
