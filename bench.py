@@ -41,7 +41,7 @@ CSRC = os.path.join(ROOT, "paper_1905_10308_amd", "csrc")
 # the sources of each timed kernel: its traffic record holds only while they are unchanged
 KERNEL_SRCS = {
     "pm_iter": ("scram_device.h", "scram_pm.hip"),
-    "attend": ("scram_device.h", "scram_attend.hip"),
+    "attend": ("scram_device.h", "scram_tile.h", "scram_attend.hip"),
 }
 # how each timed kernel appears in a rocprofv3 trace (its function name)
 KERNEL_NAMES = {
