@@ -108,3 +108,26 @@ def row_rel_err(got, ref):
 def cheb(a, b, W):
     """Chebyshev distance between flat key indices on a grid of width W."""
     return np.maximum(np.abs(a // W - b // W), np.abs(a % W - b % W))
+
+
+def tile_maps(S, Hq, Wq, Hk, Wk, rng):
+    """Maps that stress the matrix-core kernels' clusters of match centres and their key boxes."""
+    xs, ys = np.meshgrid(np.arange(Hq), np.arange(Wq), indexing="ij")
+    cu = np.clip(xs * Hk // max(Hq, 1), 0, Hk - 1)
+    cv = np.clip(ys * Wk // max(Wq, 1), 0, Wk - 1)
+    coherent = np.broadcast_to(cu * Wk + cv, (S, Hq, Wq))
+    maps = {
+        "random": rng.integers(0, Hk * Wk, (S, Hq, Wq)),
+        "constant": np.full((S, Hq, Wq), (Hk // 2) * Wk + Wk // 2),
+        "corner0": np.zeros((S, Hq, Wq)),
+        "corner_last": np.full((S, Hq, Wq), Hk * Wk - 1),
+        "coherent": coherent,
+        # centres on a lattice 6 and 7 apart: exactly at and just past the cluster radius
+        "lattice6": np.broadcast_to(np.clip(xs * 6, 0, Hk - 1) * Wk + np.clip(ys * 6, 0, Wk - 1), (S, Hq, Wq)),
+        "lattice7": np.broadcast_to(np.clip(xs * 7, 0, Hk - 1) * Wk + np.clip(ys * 7, 0, Wk - 1), (S, Hq, Wq)),
+        # two far-apart keys alternating: two clusters in every wave
+        "two_far": np.where((xs + ys) % 2 == 0, 0, Hk * Wk - 1) + np.zeros((S, 1, 1), np.int64),
+        # coherent with 10 % random outliers
+        "outliers": np.where(rng.random((S, Hq, Wq)) < 0.1, rng.integers(0, Hk * Wk, (S, Hq, Wq)), coherent),
+    }
+    return {k: np.ascontiguousarray(v, dtype=np.int32) for k, v in maps.items()}

@@ -16,7 +16,7 @@ import oracle
 import scram_inputs as si
 
 torch = pytest.importorskip("torch")
-from gpu_util import IDS, SMALL, log, to_dev  # noqa: E402
+from gpu_util import IDS, SMALL, log, tile_maps, to_dev  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -229,3 +229,27 @@ def test_backward_hot_keys(scram, pattern, ci):
     ref = oracle.sparse_attend_backward(a["Q"], a["K"], a["V"], J, 3, cfg.scale, dO.float().cpu().numpy(),
                                         flags=oracle.CAUSAL if causal else 0)
     grads_close(got, ref, pattern)
+
+
+@pytest.mark.parametrize("d", [32, 64])
+@pytest.mark.parametrize("grid", [(2, 37, 45, 37, 45), (1, 1, 50, 1, 50), (1, 50, 1, 50, 1), (3, 5, 3, 5, 3),
+                                  (1, 19, 23, 40, 31)],
+                         ids=lambda g: "x".join(map(str, g)))
+def test_backward_tile_query_maps(scram, d, grid):
+    """The matrix-core query side (bf16, 32 or 64 channels, windows 3/5/7, one map, no mask) on the maps
+    that stress the clusters and key boxes it shares with the forward kernel; every gradient, since the
+    key side reads the query side's statistics."""
+    S, Hq, Wq, Hk, Wk = grid
+    rng = np.random.default_rng(Hq * 53 + Wq * 3 + d)
+    Q, dO = (rng.standard_normal((S, Hq, Wq, d)).astype(np.float32) for _ in range(2))
+    K, V = (rng.standard_normal((S, Hk, Wk, d)).astype(np.float32) for _ in range(2))
+    Q, K, V, dO = (to_dev(x, "bf16").float().cpu().numpy() for x in (Q, K, V, dO))  # the values both sides read
+    dev = [to_dev(x, "bf16") for x in (Q, K, V)]
+    gdev = to_dev(dO, "bf16")
+    worst = 0.0
+    for name, J in tile_maps(S, Hq, Wq, Hk, Wk, rng).items():
+        for window in (3, 5, 7):
+            got = scram.sparse_attend_backward(*dev, torch.from_numpy(J).cuda(), gdev, window, d ** -0.5)
+            ref = oracle.sparse_attend_backward(Q, K, V, J, window, d ** -0.5, dO)
+            worst = max(worst, *grads_close(got, ref, f"{name} window {window}"))
+    log(f"tile backward {grid} d={d}: max rel err {worst:.3e}")

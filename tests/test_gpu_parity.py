@@ -22,7 +22,7 @@ import scram_inputs as si
 
 torch = pytest.importorskip("torch")
 from gpu_util import (IDS, MAX_TIE_FRAC, SCORE_TOL, SMALL, TOL, add_counts, compare_maps, dilate,  # noqa: E402
-                      log, reach_of_ties, row_rel_err, to_dev)
+                      log, reach_of_ties, row_rel_err, tile_maps, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -471,28 +471,6 @@ def test_concurrent_calls_on_two_streams(scram, work):
 # the matrix-core attend (bf16, 32 or 64 channels, windows 3/5/7, one map, no mask): maps that stress
 # its clusters of match centres and their key boxes
 # --------------------------------------------------------------------------
-def _tile_maps(S, Hq, Wq, Hk, Wk, rng):
-    xs, ys = np.meshgrid(np.arange(Hq), np.arange(Wq), indexing="ij")
-    cu = np.clip(xs * Hk // max(Hq, 1), 0, Hk - 1)
-    cv = np.clip(ys * Wk // max(Wq, 1), 0, Wk - 1)
-    coherent = np.broadcast_to(cu * Wk + cv, (S, Hq, Wq))
-    maps = {
-        "random": rng.integers(0, Hk * Wk, (S, Hq, Wq)),
-        "constant": np.full((S, Hq, Wq), (Hk // 2) * Wk + Wk // 2),
-        "corner0": np.zeros((S, Hq, Wq)),
-        "corner_last": np.full((S, Hq, Wq), Hk * Wk - 1),
-        "coherent": coherent,
-        # centres on a lattice 6 and 7 apart: exactly at and just past the cluster radius
-        "lattice6": np.broadcast_to(np.clip(xs * 6, 0, Hk - 1) * Wk + np.clip(ys * 6, 0, Wk - 1), (S, Hq, Wq)),
-        "lattice7": np.broadcast_to(np.clip(xs * 7, 0, Hk - 1) * Wk + np.clip(ys * 7, 0, Wk - 1), (S, Hq, Wq)),
-        # two far-apart keys alternating: two clusters in every wave
-        "two_far": np.where((xs + ys) % 2 == 0, 0, Hk * Wk - 1) + np.zeros((S, 1, 1), np.int64),
-        # coherent with 10 % random outliers
-        "outliers": np.where(rng.random((S, Hq, Wq)) < 0.1, rng.integers(0, Hk * Wk, (S, Hq, Wq)), coherent),
-    }
-    return {k: np.ascontiguousarray(v, dtype=np.int32) for k, v in maps.items()}
-
-
 @pytest.mark.parametrize("d", [32, 64])
 @pytest.mark.parametrize("grid", [(2, 37, 45, 37, 45), (1, 8, 8, 8, 8), (1, 1, 50, 1, 50), (1, 50, 1, 50, 1),
                                   (3, 5, 3, 5, 3), (1, 19, 23, 40, 31), (2, 64, 64, 64, 64)],
@@ -506,7 +484,7 @@ def test_attend_tile_kernel_maps(scram, d, grid):
     Q, K, V = (to_dev(x, "bf16").float().cpu().numpy() for x in (Q, K, V))  # the bf16 values both sides read
     dev = [to_dev(x, "bf16") for x in (Q, K, V)]
     worst = 0.0
-    for name, J in _tile_maps(S, Hq, Wq, Hk, Wk, rng).items():
+    for name, J in tile_maps(S, Hq, Wq, Hk, Wk, rng).items():
         Jd = torch.from_numpy(J).cuda()
         for window in (3, 5, 7):
             out = scram.sparse_attend(*dev, Jd, window, d ** -0.5)
