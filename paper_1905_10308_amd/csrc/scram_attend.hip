@@ -225,8 +225,8 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
 // overlap -- the matches of a coherent region are a shifted copy of it -- so
 // the wave reads each key and value row of the union of its 16 windows once
 // instead of once per query: the queries' match centres are grouped into
-// clusters (a query joins the cluster of the first unassigned query whose
-// centre lies within Chebyshev distance rc), and each cluster's key box (its
+// clusters (scram_tile.h: a query joins the cluster of the first unassigned
+// query whose centre lies within Chebyshev distance rc), and each cluster's key box (its
 // members' windows, clipped to the grid) is visited in blocks of 16 keys in
 // raster order.  A block's rows are gathered a row per 4 consecutive lanes
 // (whole 64-byte spans per load, as in the lane-group kernels), staged in the
@@ -244,8 +244,9 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
 //                            and P enters as two bf16 parts (top 8 significant
 //                            bits, then the top 8 of the rest), so its relative
 //                            error is below 2^-16
-// The softmax reference of a query is raised (and its sums rescaled) only
-// when a score passes it by more than kRescaleSlack, as in the other kernels;
+// The softmax reference of a query starts at the score of its match (a key of
+// its window) and is raised (and its sums rescaled) only when a score passes
+// it by more than kRescaleSlack, as in the other kernels;
 // every query is in exactly one cluster, and each key of its window is in
 // that cluster's box exactly once, so the weights are those of the window.
 // The other keys of the box enter with weight exactly 0, which leaves the
