@@ -252,9 +252,11 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
 // The other keys of the box enter with weight exactly 0, which leaves the
 // sums unchanged for finite value rows (a non-finite value anywhere in the
 // box would reach every query of the cluster through 0 * inf).
-// (at most 96 VGPRs: five waves per SIMD hide more of the row loads than four)
-template <int D, int W>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) void attend_tile_kernel(AttParams p)
+// (at most 96 VGPRs: five waves per SIMD hide more of the row loads than four; the causal mask's
+// registers do not fit there without spills, so its instantiation takes four)
+template <int D, int W, bool CAUSAL>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(CAUSAL ? 4 : 5))) void attend_tile_kernel(
+    AttParams p)
 {
     constexpr int B = W / 2;
     constexpr int kDs = D / 32;        // 32-channel contraction steps of S^T
@@ -299,7 +301,14 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
     }
 
     // ---- clusters of the 16 match centres and their key boxes ----
-    const TileClusters tc = tile_clusters<B>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk);
+    int qx = 0, qy = 0;  // causal: the query's position (queries and keys share the grid)
+    if constexpr (CAUSAL) {
+        uint32_t xx, yy;
+        divmod(rem, p.div_wk, xx, yy);
+        qx = static_cast<int>(xx);
+        qy = static_cast<int>(yy);
+    }
+    const TileClusters tc = tile_clusters<B, CAUSAL>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk, qx, qy);
     if (tc.nclu == 0) return;  // no query of this wave lies inside the grid
     const int nclu = tc.nclu, mine = tc.mine, wr0 = tc.wr0, wrn = tc.wrn;
     const uint32_t wcols = tc.wcols;
@@ -336,6 +345,10 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
     s_centre += __shfl_xor(s_centre, 16);
     s_centre += __shfl_xor(s_centre, 32);
     float mref = s_centre * sl2e, nref = -mref;
+    if (CAUSAL && centre > rem) {  // a match after the query is not in its set: no reference yet
+        mref = -INFINITY;
+        nref = 0.f;
+    }
     float thr_q = (mref + (kRescaleSlack - 1.f)) * inv_sl2e, thr = INFINITY;
 
     // ---- the clusters' blocks of 16 keys, one at a time; the next block's rows load during this one's
@@ -390,7 +403,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
     // one block: slot 16 k + 4 g4 of this lane's scores is box row wr0 + rr, column mcl; wc and wc2 are
     // the window's column bits of that row and of the next one (shifted past the row's end), zero outside
     // query m's own cluster
-    auto compute = [&](const Box& bx, int rr, int mcl, uint32_t wc, uint32_t wc2) {
+    auto compute = [&](const Box& bx, int rr, int mcl, uint32_t wc, uint32_t wc2, uint32_t wk, uint32_t wk2) {
         // S^T of this block: lane holds keys 4 g4 + i (slots 16 k + 4 g4 + i) for query m
         f32x4_t sc = zero;
 #pragma unroll
@@ -400,7 +413,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
             sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ds], sc, 0, 0, 0);
         }
         // which of the 4 slots lie in query m's window (bit i: slot 16 k + 4 g4 + i)
-        const uint32_t bits = tile_window_bits(bx, rr, mcl, wrn, wc, wc2);
+        const uint32_t bits = tile_window_bits<CAUSAL>(bx, rr, mcl, wrn, wc, wc2, tc.rcut, wk, wk2);
         // all ones for the slots of the window, zero elsewhere (one signed bit-field extract each)
         uint32_t keep[4];
 #pragma unroll
@@ -463,6 +476,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
         const bool here = c == mine;
         const uint32_t wc = here ? wcols : 0u;
         const uint32_t wc2 = here ? wcols << bx.bw : 0u;  // bw <= 19, and only bits below bw + 3 are read
+        const uint32_t wk = CAUSAL && here ? tc.wcut : 0u;  // the query's own row (causal)
+        const uint32_t wk2 = CAUSAL && here ? tc.wcut << bx.bw : 0u;
         thr = here ? thr_q : INFINITY;  // a query's cluster is visited once, its blocks in a row
         step_slot(bx, lc, lkey);
         for (int k = 1; k < bx.nb; ++k) {
@@ -470,7 +485,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
             load(lkey, bx.klast);
             step_slot(bx, lc, lkey);
             wave_lds_sync();
-            compute(bx, rr, mcl, wc, wc2);
+            compute(bx, rr, mcl, wc, wc2, wk, wk2);
             mcl += bx.r16;
             const bool carry = mcl >= bx.bw;
             mcl -= carry ? bx.bw : 0;
@@ -486,7 +501,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
             load(lkey, nx.klast);
         }
         wave_lds_sync();
-        compute(bx, rr, mcl, wc, wc2);
+        compute(bx, rr, mcl, wc, wc2, wk, wk2);
         if (!more) break;
         bx = nx;
         ++c;
@@ -523,8 +538,9 @@ hipError_t run_attend_m(const AttParams& p, int window, uint64_t blocks, hipStre
 }
 
 // The matrix-core kernel takes bf16 storage with 32 or 64 channels, one
-// window of side 3, 5 or 7 per query, no mask, a positive scale and slices of
-// at most 4 GiB of key rows; the lane-group kernels take every other call.
+// window of side 3, 5 or 7 per query (with or without the causal mask), a
+// positive scale and slices of at most 4 GiB of key rows; the lane-group
+// kernels take every other call.
 #ifndef SCRAM_ATTEND_TILE
 #define SCRAM_ATTEND_TILE 1
 #endif
@@ -537,16 +553,19 @@ hipError_t run_attend(const AttParams& p0, int window, hipStream_t st, hipEvent_
     constexpr int G = Lanes<T, D>::kAttend;
     AttParams p = p0;
     if constexpr (kTileKernel<T, D>) {
-        if (p.kappa == 1 && !p.causal && (window == 3 || window == 5 || window == 7) && p.scale_log2e > 0.f &&
+        if (p.kappa == 1 && (window == 3 || window == 5 || window == 7) && p.scale_log2e > 0.f &&
             static_cast<uint64_t>(p.nkeys) * (2 * D) <= 0xFFFFFFFFull) {
             p.tq = make_tiling(p.Hq, p.Wq, kBlock / 4);
             p.rc = 6;  // boxes at most 12 + window wide: slots of a box stay below 1024
             const uint64_t tiles = tiling_blocks(p.tq, p.n / p.tq.plane);
-            switch (window) {
-                case 3: return launch(attend_tile_kernel<D, 3>, tiles, st, e0, e1, p);
-                case 5: return launch(attend_tile_kernel<D, 5>, tiles, st, e0, e1, p);
-                default: return launch(attend_tile_kernel<D, 7>, tiles, st, e0, e1, p);
-            }
+            auto go = [&](auto w) {
+                constexpr int Wn = decltype(w)::value;
+                return p.causal ? launch(attend_tile_kernel<D, Wn, true>, tiles, st, e0, e1, p)
+                                : launch(attend_tile_kernel<D, Wn, false>, tiles, st, e0, e1, p);
+            };
+            return window == 3   ? go(std::integral_constant<int, 3>{})
+                   : window == 5 ? go(std::integral_constant<int, 5>{})
+                                 : go(std::integral_constant<int, 7>{});
         }
     }
     p.tq = make_tiling(p.Hq, p.Wq, Row<T, D, G>::kQpb);

@@ -15,6 +15,8 @@
 
 #pragma once
 
+#include <limits.h>
+
 #include "scram_device.h"
 
 namespace scram {
@@ -73,21 +75,25 @@ __device__ __forceinline__ uint32_t tile_wave_item(const Tiling& tq, int wave, i
 // c0 .. c0 + bw - 1, nb blocks of 16 raster slots, a 16-slot step of q16 rows
 // and r16 columns) is held by lane c of the t_ registers and read back with
 // readlane; query m's window in its own cluster's box is rows wr0 .. wr0 + wrn
-// with a bit per box column in wcols.
+// with a bit per box column in wcols.  With the causal mask (keys after the
+// query in raster order dropped; one grid for queries and keys) wrn and wcols
+// cover the window's rows before the query's own row, and the query's row --
+// window row rcut, if the window reaches it -- keeps the columns in wcut (up
+// to the query's column); rcut is INT_MIN otherwise.
 struct TileClusters {
     int t_r0, t_c0, t_bw, t_h, t_nb, t_q16, t_r16;
     float t_inv;
     int nclu, mine;
-    int wr0, wrn;
-    uint32_t wcols;
+    int wr0, wrn, rcut;
+    uint32_t wcols, wcut;
 };
 
 // Clusters of the 16 centres (u, v) of a wave (windows of half side B, key
-// grid Hk x Wk, cluster radius rc).  nclu == 0 when no query of the wave is
-// valid.
-template <int B>
+// grid Hk x Wk, cluster radius rc); CAUSAL: the query sits at (qx, qy) of the
+// same grid.  nclu == 0 when no query of the wave is valid.
+template <int B, bool CAUSAL = false>
 __device__ __forceinline__ TileClusters tile_clusters(bool valid, int u, int v, int m, int lane, int rc, int Hk,
-                                                      int Wk)
+                                                      int Wk, int qx = 0, int qy = 0)
 {
     TileClusters tc;
     int t_r0 = 0, t_c0 = 0, t_bw = 1, t_h = 0;
@@ -114,7 +120,7 @@ __device__ __forceinline__ TileClusters tile_clusters(bool valid, int u, int v, 
     tc.t_inv = __builtin_amdgcn_rcpf(static_cast<float>(t_bw));
     tc.t_nb = (t_h * t_bw + 15) >> 4;
     box_slot(16, t_bw, tc.t_inv, tc.t_q16, tc.t_r16);
-    tc.wr0 = 0, tc.wrn = -1, tc.wcols = 0;
+    tc.wr0 = 0, tc.wrn = -1, tc.wcols = 0, tc.rcut = INT_MIN, tc.wcut = 0;
     const int mc = max(mine, 0);
     const int r0 = __shfl(t_r0, mc), c0 = __shfl(t_c0, mc), bw = __shfl(t_bw, mc), h = __shfl(t_h, mc);
     if (mine >= 0) {
@@ -122,6 +128,16 @@ __device__ __forceinline__ TileClusters tile_clusters(bool valid, int u, int v, 
         tc.wrn = min(u + B - r0, h - 1) - tc.wr0;
         const int lo = max(v - B - c0, 0), hi = min(v + B - c0, bw - 1);  // box columns, bw <= 31
         tc.wcols = ((2u << hi) - 1u) & ~((1u << lo) - 1u);
+        if constexpr (CAUSAL) {
+            const int cut = qx - r0 - tc.wr0;  // the query's row, as a window row
+            if (cut >= 0 && cut <= tc.wrn) {
+                const int qc = qy - c0;  // the query's column in the box
+                tc.rcut = cut;
+                tc.wcut = qc < 0 ? 0u : (qc >= 31 ? tc.wcols : tc.wcols & ((2u << qc) - 1u));
+            }
+            tc.wrn = min(tc.wrn, cut - 1);  // the rows before the query's
+            if (tc.wrn < 0) tc.wcols = 0;   // none: no full row of the window counts
+        }
     }
     return tc;
 }
@@ -152,21 +168,26 @@ __device__ __forceinline__ TileBox tile_box(const TileClusters& tc, int cl, int 
 }
 
 // Which of the 4 slots 16 k + 4 g4 + i of a block lie in query m's window (bit i), for the slot
-// 16 k + 4 g4 at box row wr0 + rr, column mcl; wc and wc2 are the window's column bits of that row
-// and of the next one (shifted past the row's end), zero outside query m's own cluster.
+// 16 k + 4 g4 at window row rr (box row wr0 + rr), column mcl; wc and wc2 are the window's column
+// bits of that row and of the next one (shifted past the row's end), zero outside query m's own
+// cluster; CAUSAL: wk and wk2 likewise for the query's own row, window row rcut.
+template <bool CAUSAL = false>
 __device__ __forceinline__ uint32_t tile_window_bits(const TileBox& bx, int rr, int mcl, int wrn, uint32_t wc,
-                                                     uint32_t wc2)
+                                                     uint32_t wc2, int rcut = 0, uint32_t wk = 0, uint32_t wk2 = 0)
 {
     uint32_t bits = 0;
     if (bx.bw >= 3) {  // the 4 slots span at most two box rows: columns mcl .. mcl + 3 of row, next row
         const bool ok0 = static_cast<unsigned>(rr) <= static_cast<unsigned>(wrn);
         const bool ok1 = static_cast<unsigned>(rr + 1) <= static_cast<unsigned>(wrn);
-        bits = __builtin_amdgcn_ubfe((ok0 ? wc : 0u) | (ok1 ? wc2 : 0u), mcl, 4);
+        uint32_t w = (ok0 ? wc : 0u) | (ok1 ? wc2 : 0u);
+        if constexpr (CAUSAL) w |= (rr == rcut ? wk : 0u) | (rr + 1 == rcut ? wk2 : 0u);
+        bits = __builtin_amdgcn_ubfe(w, mcl, 4);
     } else {  // boxes one or two columns wide (grids that narrow): slot by slot
         int r = rr, cc = mcl;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const bool ok = static_cast<unsigned>(r) <= static_cast<unsigned>(wrn) && ((wc >> cc) & 1u);
+            bool ok = static_cast<unsigned>(r) <= static_cast<unsigned>(wrn) && ((wc >> cc) & 1u);
+            if constexpr (CAUSAL) ok = ok || (r == rcut && ((wk >> cc) & 1u));
             bits |= ok ? 1u << i : 0u;
             ++cc;
             const bool wrap = cc == bx.bw;

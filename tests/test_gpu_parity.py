@@ -9,6 +9,7 @@ sweep).  Attention outputs must be within 1e-5 (fp32 storage) or 1e-2 (bf16
 storage) of the oracle, relative to the row's largest magnitude.
 """
 import dataclasses
+import itertools
 import json
 import math
 import os
@@ -468,8 +469,8 @@ def test_concurrent_calls_on_two_streams(scram, work):
 
 
 # --------------------------------------------------------------------------
-# the matrix-core attend (bf16, 32 or 64 channels, windows 3/5/7, one map, no mask): maps that stress
-# its clusters of match centres and their key boxes
+# the matrix-core attend (bf16, 32 or 64 channels, windows 3/5/7, one map, with and without the causal
+# mask): maps that stress its clusters of match centres and their key boxes
 # --------------------------------------------------------------------------
 @pytest.mark.parametrize("d", [32, 64])
 @pytest.mark.parametrize("grid", [(2, 37, 45, 37, 45), (1, 8, 8, 8, 8), (1, 1, 50, 1, 50), (1, 50, 1, 50, 1),
@@ -484,14 +485,21 @@ def test_attend_tile_kernel_maps(scram, d, grid):
     Q, K, V = (to_dev(x, "bf16").float().cpu().numpy() for x in (Q, K, V))  # the bf16 values both sides read
     dev = [to_dev(x, "bf16") for x in (Q, K, V)]
     worst = 0.0
+    masks = (False, True) if (Hq, Wq) == (Hk, Wk) else (False,)  # the causal mask needs one grid
+    raster = np.arange(Hk * Wk).reshape(Hk, Wk)
     for name, J in tile_maps(S, Hq, Wq, Hk, Wk, rng).items():
         Jd = torch.from_numpy(J).cuda()
-        for window in (3, 5, 7):
-            out = scram.sparse_attend(*dev, Jd, window, d ** -0.5)
-            ref = oracle.sparse_attend(Q, K, V, J, window, d ** -0.5)
-            err = row_rel_err(out.float().cpu().numpy(), ref)
-            worst = max(worst, float(err.max()))
-            assert err.max() <= TOL["bf16"], f"{name} window {window}: {err.max():.3e}"
+        for window, causal in itertools.product((3, 5, 7), masks):
+            out = scram.sparse_attend(*dev, Jd, window, d ** -0.5, causal=causal).float().cpu().numpy()
+            ref = oracle.sparse_attend(Q, K, V, J, window, d ** -0.5, flags=oracle.CAUSAL if causal else 0)
+            keep = np.ones(J.shape, bool)
+            if causal:  # a row is empty iff the window's first key comes after the query: exactly zero
+                b = window // 2
+                keep = np.maximum(J // Wk - b, 0) * Wk + np.maximum(J % Wk - b, 0) <= raster[None]
+                assert (out[~keep] == 0).all() and (ref[~keep] == 0).all(), f"{name} window {window} causal"
+            err = float(row_rel_err(out[keep], ref[keep]).max(initial=0.0))
+            worst = max(worst, err)
+            assert err <= TOL["bf16"], f"{name} window {window} causal {causal}: {err:.3e}"
     log(f"tile attend {grid} d={d}: max rel err {worst:.3e}")
 
 
