@@ -968,7 +968,7 @@ bwd_key_strip_kernel(BwdParams p)
 
 // ---------------------------------------------------------------------------
 // Query side on the matrix cores (bf16 storage, d 32 or 64, windows 3/5/7,
-// one map, no mask).  The wave's 16 queries, their clusters and key boxes are
+// one map, with or without the causal mask).  The wave's 16 queries, their clusters and key boxes are
 // those of the attend's matrix-core kernel (scram_tile.h); the key and value
 // rows of a box are read a block of 16 keys at a time, staged in LDS, and per
 // block (lane (m, g4): keys 4 g4 + i, query m)
@@ -985,7 +985,7 @@ bwd_key_strip_kernel(BwdParams p)
 // both sides, so the subtraction cancels no more than there.  Also writes the
 // per-query statistics and the inverse map's count and slot of the query's
 // match, as the lane-group kernel does.
-template <int D, int W>
+template <int D, int W, bool CAUSAL>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) void bwd_query_tile_kernel(BwdParams p)
 {
     constexpr int B = W / 2;
@@ -1040,7 +1040,14 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
         kc[ds] = *reinterpret_cast<const uint4*>(Kb + centre * (2u * D) + 64u * ds + 16u * g4);
     }
 
-    const TileClusters tc = tile_clusters<B>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk);
+    int qx = 0, qy = 0;  // causal: the query's position (queries and keys share the grid)
+    if constexpr (CAUSAL) {
+        uint32_t xx, yy;
+        divmod(rem, p.div_wk, xx, yy);
+        qx = static_cast<int>(xx);
+        qy = static_cast<int>(yy);
+    }
+    const TileClusters tc = tile_clusters<B, CAUSAL>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk, qx, qy);
     if (tc.nclu == 0) return;  // no query of this wave lies inside the grid
 
     const f32x4_t zero = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -1056,7 +1063,9 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
 #pragma unroll
     for (int i = 0; i < 4; ++i) asm volatile("s_mov_b32 %0, %1" : "=s"(bit_at[i]) : "i"(i));
     // online softmax state of query m, starting at the score of its match (a key of its window), as in
-    // the attend's matrix-core kernel
+    // the attend's matrix-core kernel; under the causal mask a match after the query is not in its set,
+    // and the first kept key sets the reference.  (k_ref stays the match's key: any fixed vector gives
+    // the same dQ, as sum_j p_ij (dp_ij - D_i) is zero.)
     float s_centre = 0.f;
 #pragma unroll
     for (int ds = 0; ds < kDs; ++ds) {
@@ -1069,6 +1078,10 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
     s_centre += __shfl_xor(s_centre, 16);
     s_centre += __shfl_xor(s_centre, 32);
     float mref = s_centre * sl2e, nref = -mref;
+    if (CAUSAL && centre > rem) {
+        mref = -INFINITY;
+        nref = 0.f;
+    }
     const float thr_q = (mref + (kRescaleSlack - 1.f)) * inv_sl2e;
     float thr = INFINITY;
 
@@ -1126,7 +1139,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
         md = __builtin_bit_cast(bf16x4_t, make_uint2(hi16_pair(b[0], b[1]), hi16_pair(b[2], b[3])));
         lo = __builtin_bit_cast(bf16x4_t, make_uint2(hi16_pair(c[0], c[1]), hi16_pair(c[2], c[3])));
     };
-    auto compute = [&](const TileBox& bx, int rr, int mcl, uint32_t wc, uint32_t wc2) {
+    auto compute = [&](const TileBox& bx, int rr, int mcl, uint32_t wc, uint32_t wc2, uint32_t wk, uint32_t wk2) {
         f32x4_t sc = zero, dp = zero;
 #pragma unroll
         for (int ds = 0; ds < kDs; ++ds) {
@@ -1137,7 +1150,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
             sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ds], sc, 0, 0, 0);
             dp = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, gf[ds], dp, 0, 0, 0);
         }
-        const uint32_t bits = tile_window_bits(bx, rr, mcl, tc.wrn, wc, wc2);
+        const uint32_t bits = tile_window_bits<CAUSAL>(bx, rr, mcl, tc.wrn, wc, wc2, tc.rcut, wk, wk2);
         uint32_t keep[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -1210,6 +1223,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
         const bool here = c == tc.mine;
         const uint32_t wc = here ? tc.wcols : 0u;
         const uint32_t wc2 = here ? tc.wcols << bx.bw : 0u;  // bw <= 19, and only bits below bw + 3 are read
+        const uint32_t wk = CAUSAL && here ? tc.wcut : 0u;  // the query's own row (causal)
+        const uint32_t wk2 = CAUSAL && here ? tc.wcut << bx.bw : 0u;
         thr = here ? thr_q : INFINITY;  // a query's cluster is visited once, its blocks in a row
         step_slot(bx, lc, lkey);
         for (int k = 1; k < bx.nb; ++k) {
@@ -1217,7 +1232,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
             load(lkey, bx.klast);
             step_slot(bx, lc, lkey);
             wave_lds_sync();
-            compute(bx, rr, mcl, wc, wc2);
+            compute(bx, rr, mcl, wc, wc2, wk, wk2);
             mcl += bx.r16;
             const bool carry = mcl >= bx.bw;
             mcl -= carry ? bx.bw : 0;
@@ -1233,7 +1248,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
             load(lkey, nx.klast);
         }
         wave_lds_sync();
-        compute(bx, rr, mcl, wc, wc2);
+        compute(bx, rr, mcl, wc, wc2, wk, wk2);
         if (!more) break;
         bx = nx;
         ++c;
@@ -1289,20 +1304,25 @@ hipError_t run_backward(const BwdParams& p0, hipStream_t st, hipEvent_t* ev, Inv
                      : launch(bwd_query_kernel<T, D, G, false, W>, qblocks, st, nullptr, q1, p);
     };
     const int side = 2 * p.b + 1;
-    // the matrix-core query kernel takes bf16 storage with 32 or 64 channels, one map, no mask, windows
-    // 3, 5 or 7, a positive scale and slices of at most 4 GiB of key rows
+    // the matrix-core query kernel takes bf16 storage with 32 or 64 channels, one map (with or without
+    // the causal mask), windows 3, 5 or 7, a positive scale and slices of at most 4 GiB of key rows
     hipError_t e = hipSuccess;
     bool tile = false;
     if constexpr (SCRAM_BWD_QUERY_TILE && std::is_same<T, uint16_t>::value && (D == 32 || D == 64)) {
-        if (!multi && (side == 3 || side == 5 || side == 7) && p.scale_log2e > 0.f &&
+        if (p.kappa == 1 && (side == 3 || side == 5 || side == 7) && p.scale_log2e > 0.f &&
             static_cast<uint64_t>(p.nkeys) * (2 * D) <= 0xFFFFFFFFull) {
             BwdParams pq = p;
             pq.tq = make_tiling(p.Hq, p.Wq, kBlock / 4);
             pq.rc = 6;  // as in the attend's matrix-core kernel
             const uint64_t tb = tiling_blocks(pq.tq, p.n / pq.tq.plane);
-            e = side == 3   ? launch(bwd_query_tile_kernel<D, 3>, tb, st, nullptr, q1, pq)
-                : side == 5 ? launch(bwd_query_tile_kernel<D, 5>, tb, st, nullptr, q1, pq)
-                            : launch(bwd_query_tile_kernel<D, 7>, tb, st, nullptr, q1, pq);
+            auto go = [&](auto w) {
+                constexpr int Wn = decltype(w)::value;
+                return p.causal ? launch(bwd_query_tile_kernel<D, Wn, true>, tb, st, nullptr, q1, pq)
+                                : launch(bwd_query_tile_kernel<D, Wn, false>, tb, st, nullptr, q1, pq);
+            };
+            e = side == 3   ? go(std::integral_constant<int, 3>{})
+                : side == 5 ? go(std::integral_constant<int, 5>{})
+                            : go(std::integral_constant<int, 7>{});
             tile = true;
         }
     }

@@ -7,6 +7,7 @@ a key, gathered through the inverse map in the order it was filled.  Bar: each g
 within 2e-5 of that gradient's largest magnitude (a key gathers at most
 kappa * (2b+1)^2-ish terms of fp32 products, each rounded at ~1e-7).
 """
+import itertools
 import math
 
 import numpy as np
@@ -180,7 +181,7 @@ def test_backward_wide_score_range(scram, dtype, d, scale):
     J = rng.integers(0, H * W, (2, S, H, W)).astype(np.int32)
     dev = [to_dev(x, dtype) for x in (Q, K, V)]
     for window in (3, 5, 9):
-        for maps, causal in ((J[0], False), (J, False), (J, True)):
+        for maps, causal in ((J[0], False), (J, False), (J[0], True), (J, True)):
             got = scram.sparse_attend_backward(*dev, torch.from_numpy(np.ascontiguousarray(maps)).cuda(),
                                                to_dev(dO, dtype), window, scale, causal=causal)
             ref = oracle.sparse_attend_backward(Q, K, V, maps, window, scale, dO,
@@ -236,9 +237,9 @@ def test_backward_hot_keys(scram, pattern, ci):
                                   (1, 19, 23, 40, 31)],
                          ids=lambda g: "x".join(map(str, g)))
 def test_backward_tile_query_maps(scram, d, grid):
-    """The matrix-core query side (bf16, 32 or 64 channels, windows 3/5/7, one map, no mask) on the maps
-    that stress the clusters and key boxes it shares with the forward kernel; every gradient, since the
-    key side reads the query side's statistics."""
+    """The matrix-core query side (bf16, 32 or 64 channels, windows 3/5/7, one map, with and without the
+    causal mask) on the maps that stress the clusters and key boxes it shares with the forward kernel;
+    every gradient, since the key side reads the query side's statistics."""
     S, Hq, Wq, Hk, Wk = grid
     rng = np.random.default_rng(Hq * 53 + Wq * 3 + d)
     Q, dO = (rng.standard_normal((S, Hq, Wq, d)).astype(np.float32) for _ in range(2))
@@ -247,9 +248,12 @@ def test_backward_tile_query_maps(scram, d, grid):
     dev = [to_dev(x, "bf16") for x in (Q, K, V)]
     gdev = to_dev(dO, "bf16")
     worst = 0.0
+    masks = (False, True) if (Hq, Wq) == (Hk, Wk) else (False,)  # the causal mask needs one grid
     for name, J in tile_maps(S, Hq, Wq, Hk, Wk, rng).items():
-        for window in (3, 5, 7):
-            got = scram.sparse_attend_backward(*dev, torch.from_numpy(J).cuda(), gdev, window, d ** -0.5)
-            ref = oracle.sparse_attend_backward(Q, K, V, J, window, d ** -0.5, dO)
-            worst = max(worst, *grads_close(got, ref, f"{name} window {window}"))
+        for window, causal in itertools.product((3, 5, 7), masks):
+            got = scram.sparse_attend_backward(*dev, torch.from_numpy(J).cuda(), gdev, window, d ** -0.5,
+                                               causal=causal)
+            ref = oracle.sparse_attend_backward(Q, K, V, J, window, d ** -0.5, dO,
+                                                flags=oracle.CAUSAL if causal else 0)
+            worst = max(worst, *grads_close(got, ref, f"{name} window {window} causal {causal}"))
     log(f"tile backward {grid} d={d}: max rel err {worst:.3e}")
