@@ -701,8 +701,12 @@ struct KeyStrip {
     static constexpr int kPieces = D / 8;              // 16-byte pieces per row
 };
 
+// The strip kernel's key-set tests: the window only, the window and the causal mask (one map), or
+// several windows (and the causal mask if asked for).
+enum StripMode { kStripPlain = 0, kStripCausal = 1, kStripMulti = 2 };
+
 // waves per SIMD the strip kernel's registers are sized for
-constexpr int strip_waves(int D, bool multi) { return D > 64 || (D == 64 && multi) ? 2 : 3; }
+constexpr int strip_waves(int D, int mode) { return D > 64 || (D == 64 && mode == kStripMulti) ? 2 : 3; }
 
 // x = hi + mid + lo exactly, each part a bf16 value held as an fp32 bit
 // pattern with a zero low half: hi keeps the top 8 significant bits of x
@@ -721,10 +725,12 @@ __device__ __forceinline__ bf16x8_t lds_frag(const unsigned char* p)
     return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(p));
 }
 
-template <int D, bool MULTI>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(strip_waves(D, MULTI)))) void
+template <int D, int MODE>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(strip_waves(D, MODE)))) void
 bwd_key_strip_kernel(BwdParams p)
 {
+    constexpr bool MULTI = MODE == kStripMulti;
+    constexpr bool kQueryIndex = MODE != kStripPlain;  // entries carry their window and query's raster index
     using KS = KeyStrip<D>;
     constexpr int kCE = kStripCE;
     constexpr int kW = kBlock / 64;
@@ -733,7 +739,7 @@ bwd_key_strip_kernel(BwdParams p)
     // halves of the 32 banks, without it the two rows of each pair share banks
     __shared__ __align__(16) unsigned char s_row[kW][2 * kCE * KS::kRowB + 64];
     __shared__ int4 s_meta[kW][kCE];        // match row, match column, lse2 bits, D bits
-    __shared__ int32_t s_el[kW][MULTI ? kCE : 1][2];                 // window index e, query's raster index
+    __shared__ int32_t s_el[kW][kQueryIndex ? kCE : 1][2];           // window index e, query's raster index
     __shared__ int32_t s_prevc[kW][MULTI ? kCE : 1][kMaxKappa - 1];  // centres of windows 0..e-1
     __shared__ int32_t s_lo[kW][kStripMaxRows], s_pre[kW][kStripMaxRows + 1];
 
@@ -852,17 +858,19 @@ bwd_key_strip_kernel(BwdParams p)
             }
             if (hf == 0) {
                 int4 meta = make_int4(-(1 << 30), -(1 << 30), 0, 0);  // no key is near this match
-                if constexpr (MULTI) s_el[wave][t][0] = s_el[wave][t][1] = 0;
+                if constexpr (kQueryIndex) s_el[wave][t][0] = s_el[wave][t][1] = 0;
                 if (code >= 0) {
                     uint32_t mu, mv;
                     divmod(static_cast<uint32_t>(clamp_index(match, p.nkeys)), p.div_wk, mu, mv);
                     meta = make_int4(static_cast<int>(mu), static_cast<int>(mv), __float_as_int(lse),
                                      __float_as_int(dq));
-                    if constexpr (MULTI) {
+                    if constexpr (kQueryIndex) {
                         uint32_t sl, local;
                         divmod(qg, p.div_plane, sl, local);
                         s_el[wave][t][0] = static_cast<int32_t>(qe);
                         s_el[wave][t][1] = static_cast<int32_t>(local);
+                    }
+                    if constexpr (MULTI) {
                         for (int f = 0; f < static_cast<int>(qe); ++f)
                             s_prevc[wave][t][f] = clamp_index(p.J[static_cast<size_t>(f) * p.n + qg], p.nkeys);
                     }
@@ -910,6 +918,8 @@ bwd_key_strip_kernel(BwdParams p)
                             ok = false;  // an earlier window of the query holds this key
                     }
                     if (p.causal) ok = ok && key_local <= static_cast<uint32_t>(s_el[wave][te][1]);
+                } else if constexpr (MODE == kStripCausal) {
+                    ok = ok && key_local <= static_cast<uint32_t>(s_el[wave][te][1]);
                 }
                 const float pr = ok ? __builtin_amdgcn_exp2f(sc[et][r] * p.scale_log2e - __int_as_float(mt.z)) : 0.f;
                 const float dsr = pr * (dp[et][r] - __int_as_float(mt.w));
@@ -1341,8 +1351,9 @@ hipError_t run_backward(const BwdParams& p0, hipStream_t st, hipEvent_t* ev, Inv
             BwdParams pt = p;
             pt.tk = make_tiling(p.Hk, p.Wk, kTileKeys);
             const uint64_t tblocks = tiling_blocks(pt.tk, p.keys_total / p.nkeys);
-            return multi ? launch(bwd_key_strip_kernel<D, true>, tblocks, st, k0, k1, pt)
-                         : launch(bwd_key_strip_kernel<D, false>, tblocks, st, k0, k1, pt);
+            return p.kappa > 1 ? launch(bwd_key_strip_kernel<D, kStripMulti>, tblocks, st, k0, k1, pt)
+                   : p.causal  ? launch(bwd_key_strip_kernel<D, kStripCausal>, tblocks, st, k0, k1, pt)
+                               : launch(bwd_key_strip_kernel<D, kStripPlain>, tblocks, st, k0, k1, pt);
         }
     }
     if ((e = launch(bwd_gather_kernel<T, D, G>, gblocks, st, k0, nullptr, p)) != hipSuccess) return e;
