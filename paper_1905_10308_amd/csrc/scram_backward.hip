@@ -683,8 +683,7 @@ __global__ __launch_bounds__(kBlock) void bwd_heavy_kernel(BwdParams p)
 // entries) is the operand layout of the second, so P and dS never leave
 // registers (the entries' order along the contraction only has to agree
 // between the two operands).  The channel-major operands dO_E, Q_E of the
-// second products are the row-major fragments the first products read,
-// multiplied by identity blocks on the matrix cores (exact for bf16 values).
+// second products come from the staged rows through the transposing LDS load.
 // P and dS enter as three bf16 parts that add up to the fp32 values exactly
 // (products of bf16 parts are exact); all sums are fp32.
 // ---------------------------------------------------------------------------
@@ -706,7 +705,7 @@ struct KeyStrip {
 enum StripMode { kStripPlain = 0, kStripCausal = 1, kStripMulti = 2 };
 
 // waves per SIMD the strip kernel's registers are sized for
-constexpr int strip_waves(int D, int mode) { return D > 64 || (D == 64 && mode == kStripMulti) ? 2 : 3; }
+constexpr int strip_waves(int D, int mode) { return D > 64 ? 2 : D == 64 && mode != kStripPlain ? 3 : 4; }
 
 // x = hi + mid + lo exactly, each part a bf16 value held as an fp32 bit
 // pattern with a zero low half: hi keeps the top 8 significant bits of x
@@ -803,13 +802,6 @@ bwd_key_strip_kernel(BwdParams p)
         vf[ds] = __builtin_bit_cast(bf16x8_t, vw);
     }
     const uint32_t key_local = static_cast<uint32_t>(kx) * p.Wk + ky;  // raster index (causal test)
-    // identity blocks: I_h[k][n] = (k == 16 h + n), lane (n, g4) holding k = 8 g4 .. 8 g4 + 7
-    bf16x8_t eye[2];
-#pragma unroll
-    for (int kk = 0; kk < 8; ++kk) {
-        eye[0][kk] = static_cast<__bf16>(8 * g4 + kk == m ? 1.f : 0.f);
-        eye[1][kk] = static_cast<__bf16>(8 * g4 + kk == 16 + m ? 1.f : 0.f);
-    }
 
     f32x4_t dk[KS::kOt], dv[KS::kOt];
 #pragma unroll
@@ -831,6 +823,17 @@ bwd_key_strip_kernel(BwdParams p)
     };
     unsigned char* const rows_q = s_row[wave];
     unsigned char* const rows_g = s_row[wave] + kCE * KS::kRowB + 64;
+    // B operands of the second products, channel tile o: lane (n, g4) holds entries 4 g4 .. 4 g4 + 3 and
+    // 16 + 4 g4 .. 16 + 4 g4 + 3 at channel 16 o + n.  The transposing LDS load hands lane (n, g4) rows
+    // 4 g4 .. 4 g4 + 3 at channel 16 o + n when it addresses row 4 g4 + n / 4 at channels 4 (n mod 4) .. + 3
+    // (+ 16 o); a second load 16 rows further gives the other four.
+    const int tr_off = (4 * g4 + (m >> 2)) * KS::kRowB + 8 * (m & 3);
+    auto tr_pair = [&](const unsigned char* a) {
+        using lds_v4 = __attribute__((address_space(3))) bf16x4_t*;
+        const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_v4)(a));
+        const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_v4)(a + 16 * KS::kRowB));
+        return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    };
     int code = slot_code(0);
     for (int c0 = 0; c0 < E; c0 += kCE) {
         {
@@ -882,7 +885,6 @@ bwd_key_strip_kernel(BwdParams p)
         wave_lds_sync();
 
         // S^T, dP^T for entries 16 et + (0..15) of the chunk against the strip's 16 keys
-        bf16x8_t aq[2][KS::kDs], ag[2][KS::kDs];
         f32x4_t sc[2], dp[2];
 #pragma unroll
         for (int et = 0; et < 2; ++et) {
@@ -891,13 +893,13 @@ bwd_key_strip_kernel(BwdParams p)
 #pragma unroll
             for (int ds = 0; ds < KS::kDs; ++ds) {
                 const int d = 32 * ds + 8 * g4;
-                aq[et][ds] = ag[et][ds] = __builtin_bit_cast(bf16x8_t, make_uint4(0u, 0u, 0u, 0u));
+                bf16x8_t aq = __builtin_bit_cast(bf16x8_t, make_uint4(0u, 0u, 0u, 0u)), ag = aq;
                 if (d < D) {
-                    aq[et][ds] = lds_frag(rows_q + er * KS::kRowB + d * 2);
-                    ag[et][ds] = lds_frag(rows_g + er * KS::kRowB + d * 2);
+                    aq = lds_frag(rows_q + er * KS::kRowB + d * 2);
+                    ag = lds_frag(rows_g + er * KS::kRowB + d * 2);
                 }
-                sc[et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq[et][ds], kf[ds], sc[et], 0, 0, 0);
-                dp[et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ag[et][ds], vf[ds], dp[et], 0, 0, 0);
+                sc[et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq, kf[ds], sc[et], 0, 0, 0);
+                dp[et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ag, vf[ds], dp[et], 0, 0, 0);
             }
         }
         // P and dS of (key m, entry 16 et + 4 g4 + r): operand slot 4 et + r of this lane, in three parts
@@ -933,24 +935,10 @@ bwd_key_strip_kernel(BwdParams p)
         };
         const bf16x8_t aph = operand(ph), apm = operand(pm), apl = operand(pl);
         const bf16x8_t ash = operand(sh), asm_ = operand(sm), asl = operand(sl);
-        // dV_w += P dO_E, dK_w += dS Q_E per 16-channel tile o: the channel-major operands (lane (n, g4): entries
-        // 4 g4 .. 4 g4 + 3 and 16 + 4 g4 .. 16 + 4 g4 + 3, channel 16 o + n) are the row-major fragments times I_h
-        const f32x4_t zero = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        // dV_w += P dO_E, dK_w += dS Q_E per 16-channel tile o
 #pragma unroll
         for (int o = 0; o < KS::kOt; ++o) {
-            const int ds = o >> 1, h = o & 1;
-            const f32x4_t q0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq[0][ds], eye[h], zero, 0, 0, 0);
-            const f32x4_t q1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq[1][ds], eye[h], zero, 0, 0, 0);
-            const f32x4_t g0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ag[0][ds], eye[h], zero, 0, 0, 0);
-            const f32x4_t g1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ag[1][ds], eye[h], zero, 0, 0, 0);
-            auto bop = [](const f32x4_t& a, const f32x4_t& b) {
-                return __builtin_bit_cast(
-                    bf16x8_t, make_uint4(hi16_pair(__float_as_uint(a[0]), __float_as_uint(a[1])),
-                                         hi16_pair(__float_as_uint(a[2]), __float_as_uint(a[3])),
-                                         hi16_pair(__float_as_uint(b[0]), __float_as_uint(b[1])),
-                                         hi16_pair(__float_as_uint(b[2]), __float_as_uint(b[3]))));
-            };
-            const bf16x8_t bq = bop(q0, q1), bg = bop(g0, g1);
+            const bf16x8_t bq = tr_pair(rows_q + tr_off + 32 * o), bg = tr_pair(rows_g + tr_off + 32 * o);
             dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aph, bg, dv[o], 0, 0, 0);
             dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(apm, bg, dv[o], 0, 0, 0);
             dv[o] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(apl, bg, dv[o], 0, 0, 0);
