@@ -669,8 +669,10 @@ __global__ __launch_bounds__(kBlock) void bwd_heavy_kernel(BwdParams p)
 
 // ---------------------------------------------------------------------------
 // Key side on the matrix cores (bf16 storage).  Each wave takes a strip of 16
-// keys (items 16 w .. 16 w + 15, raster order, of the block's 64-key tile: 2
-// rows of 8 on square grids) and works alone: no block barriers.  The
+// keys (items 16 w .. 16 w + 15, raster order, of a 64-key tile: 2 rows of 8
+// on square grids) and works alone, a block of its own: the number of entries
+// per strip is very uneven, and a wave that finishes releases its LDS at once
+// instead of holding it until the slowest strip of a shared block is done.  The
 // queries whose key sets reach the strip are exactly the entries whose match
 // lies in the strip's halo (the strip widened by b), one contiguous entry
 // range per halo row.  Per chunk of 32 of those entries, staged in the wave's
@@ -705,7 +707,7 @@ struct KeyStrip {
 enum StripMode { kStripPlain = 0, kStripCausal = 1, kStripMulti = 2 };
 
 // waves per SIMD the strip kernel's registers are sized for
-constexpr int strip_waves(int D, int mode) { return D > 64 ? 2 : D == 64 && mode != kStripPlain ? 3 : 4; }
+constexpr int strip_waves(int D) { return D > 64 ? 2 : 4; }
 
 // x = hi + mid + lo exactly, each part a bf16 value held as an fp32 bit
 // pattern with a zero low half: hi keeps the top 8 significant bits of x
@@ -724,15 +726,17 @@ __device__ __forceinline__ bf16x8_t lds_frag(const unsigned char* p)
     return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(p));
 }
 
+constexpr int kStripWaves = kTileKeys / 16;  // strips of a tile, one one-wave block each
+
 template <int D, int MODE>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(strip_waves(D, MODE)))) void
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(strip_waves(D)))) void
 bwd_key_strip_kernel(BwdParams p)
 {
     constexpr bool MULTI = MODE == kStripMulti;
     constexpr bool kQueryIndex = MODE != kStripPlain;  // entries carry their window and query's raster index
     using KS = KeyStrip<D>;
     constexpr int kCE = kStripCE;
-    constexpr int kW = kBlock / 64;
+    constexpr int kW = 1;  // waves per block
     // q rows of the chunk, then 64 bytes of skew, then its dO rows: lanes 2t and 2t + 1 stage row t of
     // each; with the skew the eight lanes of one 128-bit access (rows t .. t + 3 of both) use disjoint
     // halves of the 32 banks, without it the two rows of each pair share banks
@@ -742,17 +746,17 @@ bwd_key_strip_kernel(BwdParams p)
     __shared__ int32_t s_prevc[kW][MULTI ? kCE : 1][kMaxKappa - 1];  // centres of windows 0..e-1
     __shared__ int32_t s_lo[kW][kStripMaxRows], s_pre[kW][kStripMaxRows + 1];
 
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wave = 0;
     const int m = lane & 15, g4 = lane >> 4;
     const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
 
-    // the block's tile (th x tw keys at x0, y0 of slice s) and this wave's strip in it
+    // the tile (th x tw keys at x0, y0 of slice s) and this wave's strip in it
     uint32_t s, k, tr, tc;
-    divmod(blk, p.tk.div_slice, s, k);
+    divmod(blk / kStripWaves, p.tk.div_slice, s, k);
     divmod(k, p.tk.div_w, tr, tc);
     const int tw = 1 << p.tk.lw, th = kTileKeys >> p.tk.lw;
     const int x0 = static_cast<int>(tr) * th, y0 = static_cast<int>(tc) * tw;
-    const int it0 = 16 * wave;
+    const int it0 = 16 * static_cast<int>(blk % kStripWaves);
     const int sr0 = x0 + (it0 >> p.tk.lw), sr1 = x0 + ((it0 + 15) >> p.tk.lw);
     const int sc0 = y0 + (it0 & (tw - 1)), sc1 = sc0 + min(tw, 16) - 1;
     if (sr0 >= p.Hk || sc0 >= p.Wk) return;  // the strip lies past the grid's edge
@@ -1280,6 +1284,18 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
 #define SCRAM_BWD_QUERY_TILE 1
 #endif
 
+// launch() for kernels whose blocks are one wave each
+hipError_t launch_wave(void (*kernel)(BwdParams), uint64_t blocks, hipStream_t st, hipEvent_t start, hipEvent_t stop,
+                       const BwdParams& p)
+{
+    if (blocks == 0 || blocks > 0xFFFFFFFFull / 64) return hipErrorInvalidConfiguration;
+    if (start || stop)
+        hipExtLaunchKernelGGL(kernel, dim3(blocks), dim3(64), 0, st, start, stop, 0, p);
+    else
+        hipLaunchKernelGGL(kernel, dim3(blocks), dim3(64), 0, st, p);
+    return hipGetLastError();
+}
+
 // The query kernel, then the rest of the inverse map (inverse()), then the
 // key side.
 template <typename T, int D, typename Inverse>
@@ -1338,10 +1354,10 @@ hipError_t run_backward(const BwdParams& p0, hipStream_t st, hipEvent_t* ev, Inv
         if (p.b >= 1 && p.b <= kTileMaxB) {
             BwdParams pt = p;
             pt.tk = make_tiling(p.Hk, p.Wk, kTileKeys);
-            const uint64_t tblocks = tiling_blocks(pt.tk, p.keys_total / p.nkeys);
-            return p.kappa > 1 ? launch(bwd_key_strip_kernel<D, kStripMulti>, tblocks, st, k0, k1, pt)
-                   : p.causal  ? launch(bwd_key_strip_kernel<D, kStripCausal>, tblocks, st, k0, k1, pt)
-                               : launch(bwd_key_strip_kernel<D, kStripPlain>, tblocks, st, k0, k1, pt);
+            const uint64_t tblocks = kStripWaves * tiling_blocks(pt.tk, p.keys_total / p.nkeys);
+            return p.kappa > 1 ? launch_wave(bwd_key_strip_kernel<D, kStripMulti>, tblocks, st, k0, k1, pt)
+                   : p.causal  ? launch_wave(bwd_key_strip_kernel<D, kStripCausal>, tblocks, st, k0, k1, pt)
+                               : launch_wave(bwd_key_strip_kernel<D, kStripPlain>, tblocks, st, k0, k1, pt);
         }
     }
     if ((e = launch(bwd_gather_kernel<T, D, G>, gblocks, st, k0, nullptr, p)) != hipSuccess) return e;
