@@ -252,11 +252,17 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
 // The other keys of the box enter with weight exactly 0, which leaves the
 // sums unchanged for finite value rows (a non-finite value anywhere in the
 // box would reach every query of the cluster through 0 * inf).
+// Several maps (kappa <= MK windows per query, attention over their union):
+// one pass per window e, each with the clusters and boxes of the wave's 16
+// window-e centres, into the same online softmax state; a slot of pass e is
+// left out when one of the query's windows 0 .. e-1 holds its key, so every
+// key of the union enters once.
 // (at most 96 VGPRs: five waves per SIMD hide more of the row loads than four; the causal mask's
-// registers do not fit there without spills, so its instantiation takes four)
-template <int D, int W, bool CAUSAL>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(CAUSAL ? 4 : 5))) void attend_tile_kernel(
-    AttParams p)
+// registers and those of up to 4 windows do not fit there without spills, so they take four, and
+// up to 8 windows three)
+template <int D, int W, bool CAUSAL, int MK>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(MK > 4 ? 3 : CAUSAL || MK > 1 ? 4 : 5))) void
+attend_tile_kernel(AttParams p)
 {
     constexpr int B = W / 2;
     constexpr int kDs = D / 32;        // 32-channel contraction steps of S^T
@@ -308,10 +314,18 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(CAUSAL ?
         qx = static_cast<int>(xx);
         qy = static_cast<int>(yy);
     }
-    const TileClusters tc = tile_clusters<B, CAUSAL>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk, qx, qy);
+    TileClusters tc = tile_clusters<B, CAUSAL>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk, qx, qy);
     if (tc.nclu == 0) return;  // no query of this wave lies inside the grid
-    const int nclu = tc.nclu, mine = tc.mine, wr0 = tc.wr0, wrn = tc.wrn;
-    const uint32_t wcols = tc.wcols;
+    int nclu = tc.nclu, mine = tc.mine, wr0 = tc.wr0, wrn = tc.wrn;
+    uint32_t wcols = tc.wcols;
+    // several windows: the centres of windows 0 .. e-1 of query m, as rows relative to window e's first
+    // row (dw) and columns (cv); their columns in the current box (xw; zero for f >= e and outside the
+    // query's own cluster)
+    constexpr int kOther = MK > 1 ? MK - 1 : 1;
+    int cu[kOther], cv[kOther], dw[kOther];
+    uint32_t xw[kOther];
+#pragma unroll
+    for (int f = 0; f < kOther; ++f) cu[f] = cv[f] = 0, dw[f] = 1 << 20, xw[f] = 0u;
 
     const f32x4_t zero = f32x4_t{0.f, 0.f, 0.f, 0.f};
     f32x4_t acc[kOt];
@@ -413,7 +427,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(CAUSAL ?
             sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ds], sc, 0, 0, 0);
         }
         // which of the 4 slots lie in query m's window (bit i: slot 16 k + 4 g4 + i)
-        const uint32_t bits = tile_window_bits<CAUSAL>(bx, rr, mcl, wrn, wc, wc2, tc.rcut, wk, wk2);
+        uint32_t bits = tile_window_bits<CAUSAL>(bx, rr, mcl, wrn, wc, wc2, tc.rcut, wk, wk2);
+        if constexpr (MK > 1) bits &= ~tile_other_bits<kOther, B>(bx, rr, mcl, dw, xw);
         // all ones for the slots of the window, zero elsewhere (one signed bit-field extract each)
         uint32_t keep[4];
 #pragma unroll
@@ -436,6 +451,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(CAUSAL ?
                 mref = mx;
                 nref = -mx;
                 thr = (mx + (kRescaleSlack - 1.f)) * inv_sl2e;
+                if constexpr (MK > 1) thr_q = thr;  // the query's later windows start from here
             }
         }
         uint32_t ph[4], pl[4];
@@ -464,6 +480,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(CAUSAL ?
 
     // The blocks of a cluster are computed in a row; each block's rows load during the previous block's
     // products, the first block of the next cluster during the last block of this one.
+    for (int e = 0;;) {
     Box bx = box_of(0);
     int lc;
     uint32_t lkey;
@@ -478,7 +495,12 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(CAUSAL ?
         const uint32_t wc2 = here ? wcols << bx.bw : 0u;  // bw <= 19, and only bits below bw + 3 are read
         const uint32_t wk = CAUSAL && here ? tc.wcut : 0u;  // the query's own row (causal)
         const uint32_t wk2 = CAUSAL && here ? tc.wcut << bx.bw : 0u;
-        thr = here ? thr_q : INFINITY;  // a query's cluster is visited once, its blocks in a row
+        if constexpr (MK > 1) {
+#pragma unroll
+            for (int f = 0; f < kOther; ++f)
+                xw[f] = here && f < e ? tile_col_bits(cv[f] - B - bx.c0, cv[f] + B - bx.c0, bx.bw) : 0u;
+        }
+        thr = here ? thr_q : INFINITY;  // a query's cluster is visited once per window, its blocks in a row
         step_slot(bx, lc, lkey);
         for (int k = 1; k < bx.nb; ++k) {
             stage();
@@ -506,6 +528,28 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(CAUSAL ?
         bx = nx;
         ++c;
         wave_lds_sync();
+    }
+    if constexpr (MK == 1) {
+        break;
+    } else {
+        if (e + 1 >= p.kappa) break;
+        // the next window: its centres' clusters and boxes; window e joins the earlier ones
+#pragma unroll
+        for (int f = 0; f < kOther; ++f)
+            if (f == e) cu[f] = u, cv[f] = v;
+        ++e;
+        const uint32_t ce = static_cast<uint32_t>(clamp_index(p.J[static_cast<size_t>(e) * p.n + gq], p.nkeys));
+        uint32_t uu, vv;
+        divmod(ce, p.div_wk, uu, vv);
+        u = static_cast<int>(uu);
+        v = static_cast<int>(vv);
+#pragma unroll
+        for (int f = 0; f < kOther; ++f) dw[f] = f < e ? cu[f] - u : 1 << 20;
+        tc = tile_clusters<B, CAUSAL>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk, qx, qy);
+        nclu = tc.nclu, mine = tc.mine, wr0 = tc.wr0, wrn = tc.wrn;
+        wcols = tc.wcols;
+        wave_lds_sync();  // the last block's LDS reads come before the next pass's writes
+    }
     }
     if (!valid) return;
     const float lt = lacc[0];  // every row of the ones-block product holds query m's sum of weights
@@ -537,10 +581,10 @@ hipError_t run_attend_m(const AttParams& p, int window, uint64_t blocks, hipStre
     }
 }
 
-// The matrix-core kernel takes bf16 storage with 32 or 64 channels, one
-// window of side 3, 5 or 7 per query (with or without the causal mask), a
-// positive scale and slices of at most 4 GiB of key rows; the lane-group
-// kernels take every other call.
+// The matrix-core kernel takes bf16 storage with 32 or 64 channels, windows
+// of side 3, 5 or 7 (one per map, up to kMaxKappa maps; with or without the
+// causal mask), a positive scale and slices of at most 4 GiB of key rows; the
+// lane-group kernels take every other call.
 #ifndef SCRAM_ATTEND_TILE
 #define SCRAM_ATTEND_TILE 1
 #endif
@@ -553,15 +597,23 @@ hipError_t run_attend(const AttParams& p0, int window, hipStream_t st, hipEvent_
     constexpr int G = Lanes<T, D>::kAttend;
     AttParams p = p0;
     if constexpr (kTileKernel<T, D>) {
-        if (p.kappa == 1 && (window == 3 || window == 5 || window == 7) && p.scale_log2e > 0.f &&
+        if (p.kappa <= kMaxKappa && (window == 3 || window == 5 || window == 7) && p.scale_log2e > 0.f &&
             static_cast<uint64_t>(p.nkeys) * (2 * D) <= 0xFFFFFFFFull) {
             p.tq = make_tiling(p.Hq, p.Wq, kBlock / 4);
             p.rc = 6;  // boxes at most 12 + window wide: slots of a box stay below 1024
             const uint64_t tiles = tiling_blocks(p.tq, p.n / p.tq.plane);
             auto go = [&](auto w) {
                 constexpr int Wn = decltype(w)::value;
-                return p.causal ? launch(attend_tile_kernel<D, Wn, true>, tiles, st, e0, e1, p)
-                                : launch(attend_tile_kernel<D, Wn, false>, tiles, st, e0, e1, p);
+                // the smallest bound on the windows per query that holds this call's
+                auto with = [&](auto mk) {
+                    constexpr int MK = decltype(mk)::value;
+                    return p.causal ? launch(attend_tile_kernel<D, Wn, true, MK>, tiles, st, e0, e1, p)
+                                    : launch(attend_tile_kernel<D, Wn, false, MK>, tiles, st, e0, e1, p);
+                };
+                return p.kappa == 1   ? with(std::integral_constant<int, 1>{})
+                       : p.kappa == 2 ? with(std::integral_constant<int, 2>{})
+                       : p.kappa <= 4 ? with(std::integral_constant<int, 4>{})
+                                      : with(std::integral_constant<int, kMaxKappa>{});
             };
             return window == 3   ? go(std::integral_constant<int, 3>{})
                    : window == 5 ? go(std::integral_constant<int, 5>{})

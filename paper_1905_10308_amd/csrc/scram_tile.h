@@ -198,5 +198,44 @@ __device__ __forceinline__ uint32_t tile_window_bits(const TileBox& bx, int rr, 
     return bits;
 }
 
+// Box-column bits of the columns lo .. hi of a box `bw` wide (clipped to the box; zero when none is left).
+__device__ __forceinline__ uint32_t tile_col_bits(int lo, int hi, int bw)
+{
+    lo = max(lo, 0), hi = min(hi, bw - 1);
+    return lo <= hi ? ((2u << hi) - 1u) & ~((1u << lo) - 1u) : 0u;
+}
+
+// Which of the 4 slots of tile_window_bits lie in one of N other windows of side 2 B + 1: window f covers
+// window rows d[f] .. d[f] + 2 B (rows of the window the slots are tested against) and the box columns
+// in xw[f] (zero: no window).
+template <int N, int B>
+__device__ __forceinline__ uint32_t tile_other_bits(const TileBox& bx, int rr, int mcl, const int (&d)[N],
+                                                    const uint32_t (&xw)[N])
+{
+    if (bx.bw >= 3) {
+        uint32_t w = 0;
+#pragma unroll
+        for (int f = 0; f < N; ++f) {
+            w |= static_cast<unsigned>(rr - d[f]) <= 2u * B ? xw[f] : 0u;
+            w |= static_cast<unsigned>(rr + 1 - d[f]) <= 2u * B ? xw[f] << bx.bw : 0u;
+        }
+        return __builtin_amdgcn_ubfe(w, mcl, 4);
+    }
+    uint32_t bits = 0;
+    int r = rr, cc = mcl;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        bool in = false;
+#pragma unroll
+        for (int f = 0; f < N; ++f) in = in || (static_cast<unsigned>(r - d[f]) <= 2u * B && ((xw[f] >> cc) & 1u));
+        bits |= in ? 1u << i : 0u;
+        ++cc;
+        const bool wrap = cc == bx.bw;
+        cc = wrap ? 0 : cc;
+        r += wrap ? 1 : 0;
+    }
+    return bits;
+}
+
 }  // namespace
 }  // namespace scram

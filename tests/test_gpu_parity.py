@@ -503,6 +503,47 @@ def test_attend_tile_kernel_maps(scram, d, grid):
     log(f"tile attend {grid} d={d}: max rel err {worst:.3e}")
 
 
+@pytest.mark.parametrize("d", [32, 64])
+@pytest.mark.parametrize("grid", [(2, 37, 45, 37, 45), (1, 1, 50, 1, 50), (1, 50, 1, 50, 1), (3, 5, 3, 5, 3),
+                                  (1, 19, 23, 40, 31)],
+                         ids=lambda g: "x".join(map(str, g)))
+def test_attend_tile_kernel_union_maps(scram, d, grid):
+    """The matrix-core attend over the union of 2, 3 and 8 windows per query (a pass per window, the keys
+    of earlier windows left out): the stress maps combined into windows that repeat, overlap by one key,
+    lie apart or coincide for some queries only, with and without the causal mask."""
+    S, Hq, Wq, Hk, Wk = grid
+    rng = np.random.default_rng(Hq * 17 + Wq * 5 + d)
+    Q = rng.standard_normal((S, Hq, Wq, d)).astype(np.float32)
+    K = rng.standard_normal((S, Hk, Wk, d)).astype(np.float32)
+    V = rng.standard_normal((S, Hk, Wk, d)).astype(np.float32)
+    Q, K, V = (to_dev(x, "bf16").float().cpu().numpy() for x in (Q, K, V))
+    dev = [to_dev(x, "bf16") for x in (Q, K, V)]
+    m = tile_maps(S, Hq, Wq, Hk, Wk, rng)
+    nk = Hk * Wk
+    unions = {
+        "coherent+next_key": (m["coherent"], (m["coherent"] + 1) % nk),
+        "random+random": (m["random"], rng.integers(0, nk, m["random"].shape)),
+        "two_far+constant": (m["two_far"], m["constant"]),
+        "coherent_twice+outliers": (m["coherent"], m["coherent"], m["outliers"]),
+        "eight": tuple(m[k] for k in ("coherent", "outliers", "lattice6", "lattice7", "random", "two_far",
+                                      "corner0", "corner_last")),
+    }
+    masks = (False, True) if (Hq, Wq) == (Hk, Wk) else (False,)
+    worst = 0.0
+    for name, maps in unions.items():
+        J = np.ascontiguousarray(np.stack(maps), dtype=np.int32)
+        Jd = torch.from_numpy(J).cuda()
+        for window, causal in itertools.product((3, 5, 7), masks):
+            out = scram.sparse_attend(*dev, Jd, window, d ** -0.5, causal=causal).float().cpu().numpy()
+            ref = oracle.sparse_attend(Q, K, V, J, window, d ** -0.5, flags=oracle.CAUSAL if causal else 0)
+            empty = ~np.any(ref != 0, axis=-1)  # causal: every key of every window after the query
+            assert (out[empty] == 0).all(), f"{name} window {window} causal {causal}: empty rows"
+            err = float(row_rel_err(out[~empty], ref[~empty]).max(initial=0.0))
+            worst = max(worst, err)
+            assert err <= TOL["bf16"], f"{name} window {window} causal {causal}: {err:.3e}"
+    log(f"tile union attend {grid} d={d}: max rel err {worst:.3e}")
+
+
 @pytest.mark.parametrize("Wk", [8191, 8192], ids=["last_slice_under_4GiB", "slice_of_4GiB"])
 def test_attend_key_slice_at_4gib(scram, Wk):
     """A 4096 x Wk key grid of 64 bf16 channels: 8191 columns make the slice's rows 2^32 - 524288
