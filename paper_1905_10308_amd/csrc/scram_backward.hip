@@ -970,7 +970,9 @@ bwd_key_strip_kernel(BwdParams p)
 
 // ---------------------------------------------------------------------------
 // Query side on the matrix cores (bf16 storage, d 32 or 64, windows 3/5/7,
-// one map, with or without the causal mask).  The wave's 16 queries, their clusters and key boxes are
+// up to MK maps, with or without the causal mask; several maps take a pass
+// per window, with the keys of the query's earlier windows left out, as in the
+// attend's matrix-core kernel).  The wave's 16 queries, their clusters and key boxes are
 // those of the attend's matrix-core kernel (scram_tile.h); the key and value
 // rows of a box are read a block of 16 keys at a time, staged in LDS, and per
 // block (lane (m, g4): keys 4 g4 + i, query m)
@@ -987,7 +989,7 @@ bwd_key_strip_kernel(BwdParams p)
 // both sides, so the subtraction cancels no more than there.  Also writes the
 // per-query statistics and the inverse map's count and slot of the query's
 // match, as the lane-group kernel does.
-template <int D, int W, bool CAUSAL>
+template <int D, int W, bool CAUSAL, int MK>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) void bwd_query_tile_kernel(BwdParams p)
 {
     constexpr int B = W / 2;
@@ -1019,9 +1021,17 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
     const unsigned char* const Kb = static_cast<const unsigned char*>(p.K) + slice_bytes;
     const unsigned char* const Vb = static_cast<const unsigned char*>(p.V) + slice_bytes;
     const uint32_t centre = static_cast<uint32_t>(clamp_index(p.J[gq], p.nkeys));
-    // the inverse map's count: one entry per query, and its slot among the entries of its match key
-    if (valid && g4 == 0)
+    // the inverse map's count: one entry per match of the query, and its slot among the entries of that
+    // match key
+    if (valid && g4 == 0) {
         p.slots[g] = atomicAdd(p.counts + static_cast<size_t>(s) * p.nkeys + centre, 1);
+        if constexpr (MK > 1) {
+            for (int e = 1; e < p.kappa; ++e) {
+                const size_t x = static_cast<size_t>(e) * p.n + g;
+                p.slots[x] = atomicAdd(p.counts + static_cast<size_t>(s) * p.nkeys + clamp_index(p.J[x], p.nkeys), 1);
+            }
+        }
+    }
     int u, v;
     {
         uint32_t uu, vv;
@@ -1049,8 +1059,14 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
         qx = static_cast<int>(xx);
         qy = static_cast<int>(yy);
     }
-    const TileClusters tc = tile_clusters<B, CAUSAL>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk, qx, qy);
+    TileClusters tc = tile_clusters<B, CAUSAL>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk, qx, qy);
     if (tc.nclu == 0) return;  // no query of this wave lies inside the grid
+    // several windows: windows 0 .. e-1 of query m as in the attend's matrix-core kernel
+    constexpr int kOther = MK > 1 ? MK - 1 : 1;
+    int cu[kOther], cv[kOther], dw[kOther];
+    uint32_t xw[kOther];
+#pragma unroll
+    for (int f = 0; f < kOther; ++f) cu[f] = cv[f] = 0, dw[f] = 1 << 20, xw[f] = 0u;
 
     const f32x4_t zero = f32x4_t{0.f, 0.f, 0.f, 0.f};
     f32x4_t acc_a[kOt], acc_b[kOt];
@@ -1084,7 +1100,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
         mref = -INFINITY;
         nref = 0.f;
     }
-    const float thr_q = (mref + (kRescaleSlack - 1.f)) * inv_sl2e;
+    float thr_q = (mref + (kRescaleSlack - 1.f)) * inv_sl2e;
     float thr = INFINITY;
 
     const int lslot = lane >> 2, lpiece = lane & 3;  // every lane: one key slot, 16-byte pieces lpiece (+ 4)
@@ -1152,7 +1168,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
             sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ds], sc, 0, 0, 0);
             dp = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, gf[ds], dp, 0, 0, 0);
         }
-        const uint32_t bits = tile_window_bits<CAUSAL>(bx, rr, mcl, tc.wrn, wc, wc2, tc.rcut, wk, wk2);
+        uint32_t bits = tile_window_bits<CAUSAL>(bx, rr, mcl, tc.wrn, wc, wc2, tc.rcut, wk, wk2);
+        if constexpr (MK > 1) bits &= ~tile_other_bits<kOther, B>(bx, rr, mcl, dw, xw);
         uint32_t keep[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -1176,6 +1193,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
                 mref = mx;
                 nref = -mx;
                 thr = (mx + (kRescaleSlack - 1.f)) * inv_sl2e;
+                if constexpr (MK > 1) thr_q = thr;  // the query's later windows start from here
             }
         }
         uint32_t pw[4], pdw[4];
@@ -1213,6 +1231,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
     };
 
     // the blocks of each cluster in a row; each block's rows load during the previous block's products
+    for (int e = 0;;) {
     TileBox bx = tile_box(tc, 0, p.Wk);
     int lc;
     uint32_t lkey;
@@ -1227,7 +1246,12 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
         const uint32_t wc2 = here ? tc.wcols << bx.bw : 0u;  // bw <= 19, and only bits below bw + 3 are read
         const uint32_t wk = CAUSAL && here ? tc.wcut : 0u;  // the query's own row (causal)
         const uint32_t wk2 = CAUSAL && here ? tc.wcut << bx.bw : 0u;
-        thr = here ? thr_q : INFINITY;  // a query's cluster is visited once, its blocks in a row
+        if constexpr (MK > 1) {
+#pragma unroll
+            for (int f = 0; f < kOther; ++f)
+                xw[f] = here && f < e ? tile_col_bits(cv[f] - B - bx.c0, cv[f] + B - bx.c0, bx.bw) : 0u;
+        }
+        thr = here ? thr_q : INFINITY;  // a query's cluster is visited once per window, its blocks in a row
         step_slot(bx, lc, lkey);
         for (int k = 1; k < bx.nb; ++k) {
             stage();
@@ -1255,6 +1279,26 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
         bx = nx;
         ++c;
         wave_lds_sync();
+    }
+    if constexpr (MK == 1) {
+        break;
+    } else {
+        if (e + 1 >= p.kappa) break;
+        // the next window: its centres' clusters and boxes; window e joins the earlier ones
+#pragma unroll
+        for (int f = 0; f < kOther; ++f)
+            if (f == e) cu[f] = u, cv[f] = v;
+        ++e;
+        const uint32_t ce = static_cast<uint32_t>(clamp_index(p.J[static_cast<size_t>(e) * p.n + gq], p.nkeys));
+        uint32_t uu, vv;
+        divmod(ce, p.div_wk, uu, vv);
+        u = static_cast<int>(uu);
+        v = static_cast<int>(vv);
+#pragma unroll
+        for (int f = 0; f < kOther; ++f) dw[f] = f < e ? cu[f] - u : 1 << 20;
+        tc = tile_clusters<B, CAUSAL>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk, qx, qy);
+        wave_lds_sync();  // the last block's LDS reads come before the next pass's writes
+    }
     }
     if (!valid) return;
     const float l = lacc[0], dn = dacc[0];
@@ -1318,12 +1362,12 @@ hipError_t run_backward(const BwdParams& p0, hipStream_t st, hipEvent_t* ev, Inv
                      : launch(bwd_query_kernel<T, D, G, false, W>, qblocks, st, nullptr, q1, p);
     };
     const int side = 2 * p.b + 1;
-    // the matrix-core query kernel takes bf16 storage with 32 or 64 channels, one map (with or without
-    // the causal mask), windows 3, 5 or 7, a positive scale and slices of at most 4 GiB of key rows
+    // the matrix-core query kernel takes bf16 storage with 32 or 64 channels, up to 4 maps (with or
+    // without the causal mask), windows 3, 5 or 7, a positive scale and slices of at most 4 GiB of key rows
     hipError_t e = hipSuccess;
     bool tile = false;
     if constexpr (SCRAM_BWD_QUERY_TILE && std::is_same<T, uint16_t>::value && (D == 32 || D == 64)) {
-        if (p.kappa == 1 && (side == 3 || side == 5 || side == 7) && p.scale_log2e > 0.f &&
+        if (p.kappa <= 4 && (side == 3 || side == 5 || side == 7) && p.scale_log2e > 0.f &&
             static_cast<uint64_t>(p.nkeys) * (2 * D) <= 0xFFFFFFFFull) {
             BwdParams pq = p;
             pq.tq = make_tiling(p.Hq, p.Wq, kBlock / 4);
@@ -1331,8 +1375,14 @@ hipError_t run_backward(const BwdParams& p0, hipStream_t st, hipEvent_t* ev, Inv
             const uint64_t tb = tiling_blocks(pq.tq, p.n / pq.tq.plane);
             auto go = [&](auto w) {
                 constexpr int Wn = decltype(w)::value;
-                return p.causal ? launch(bwd_query_tile_kernel<D, Wn, true>, tb, st, nullptr, q1, pq)
-                                : launch(bwd_query_tile_kernel<D, Wn, false>, tb, st, nullptr, q1, pq);
+                auto with = [&](auto mk) {  // the smallest bound on the windows per query that holds this call's
+                    constexpr int MK = decltype(mk)::value;
+                    return p.causal ? launch(bwd_query_tile_kernel<D, Wn, true, MK>, tb, st, nullptr, q1, pq)
+                                    : launch(bwd_query_tile_kernel<D, Wn, false, MK>, tb, st, nullptr, q1, pq);
+                };
+                return p.kappa == 1   ? with(std::integral_constant<int, 1>{})
+                       : p.kappa == 2 ? with(std::integral_constant<int, 2>{})
+                                      : with(std::integral_constant<int, 4>{});
             };
             e = side == 3   ? go(std::integral_constant<int, 3>{})
                 : side == 5 ? go(std::integral_constant<int, 5>{})

@@ -168,6 +168,41 @@ def test_backward_many_keys(scram, grid, dtype):
     grads_close(got, ref, f"{grid} {dtype}")
 
 
+@pytest.mark.parametrize("d", [32, 64])
+@pytest.mark.parametrize("grid", [(2, 37, 45, 37, 45), (1, 1, 50, 1, 50), (3, 5, 3, 5, 3), (1, 19, 23, 40, 31)],
+                         ids=lambda g: "x".join(map(str, g)))
+def test_backward_tile_query_union_maps(scram, d, grid):
+    """The matrix-core query side over the union of 2, 3 and 4 windows per query (a pass per window, the
+    keys of earlier windows left out), with and without the causal mask, on combinations of the stress
+    maps: windows that repeat, overlap by one key or lie apart."""
+    S, Hq, Wq, Hk, Wk = grid
+    rng = np.random.default_rng(Hq * 29 + Wq * 11 + d)
+    Q, dO = (rng.standard_normal((S, Hq, Wq, d)).astype(np.float32) for _ in range(2))
+    K, V = (rng.standard_normal((S, Hk, Wk, d)).astype(np.float32) for _ in range(2))
+    Q, K, V, dO = (to_dev(x, "bf16").float().cpu().numpy() for x in (Q, K, V, dO))
+    dev = [to_dev(x, "bf16") for x in (Q, K, V)]
+    gdev = to_dev(dO, "bf16")
+    m = tile_maps(S, Hq, Wq, Hk, Wk, rng)
+    nk = Hk * Wk
+    unions = {
+        "coherent+next_key": (m["coherent"], (m["coherent"] + 1) % nk),
+        "two_far+constant": (m["two_far"], m["constant"]),
+        "coherent_twice+outliers": (m["coherent"], m["coherent"], m["outliers"]),
+        "four": (m["outliers"], m["lattice6"], m["random"], m["corner_last"]),
+    }
+    masks = (False, True) if (Hq, Wq) == (Hk, Wk) else (False,)
+    worst = 0.0
+    for name, maps in unions.items():
+        J = np.ascontiguousarray(np.stack(maps), dtype=np.int32)
+        for window, causal in itertools.product((3, 5, 7), masks):
+            got = scram.sparse_attend_backward(*dev, torch.from_numpy(J).cuda(), gdev, window, d ** -0.5,
+                                               causal=causal)
+            ref = oracle.sparse_attend_backward(Q, K, V, J, window, d ** -0.5, dO,
+                                                flags=oracle.CAUSAL if causal else 0)
+            worst = max(worst, *grads_close(got, ref, f"{name} window {window} causal {causal}"))
+    log(f"tile union backward {grid} d={d}: max rel err {worst:.3e}")
+
+
 @pytest.mark.parametrize("dtype,d,scale", [("f32", 16, 1 / 2), ("bf16", 64, 1 / 4)])
 def test_backward_wide_score_range(scram, dtype, d, scale):
     """Small-integer q, k (exact dot products) with a power-of-two scale near 2/sqrt(d): window scores
