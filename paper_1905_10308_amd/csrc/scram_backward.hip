@@ -707,7 +707,7 @@ struct KeyStrip {
 enum StripMode { kStripPlain = 0, kStripCausal = 1, kStripMulti = 2 };
 
 // waves per SIMD the strip kernel's registers are sized for
-constexpr int strip_waves(int D) { return D > 64 ? 2 : 4; }
+constexpr int strip_waves(int D, int mode) { return D > 64 ? 2 : D == 64 && mode == kStripMulti ? 3 : 4; }
 
 // x = hi + mid + lo exactly, each part a bf16 value held as an fp32 bit
 // pattern with a zero low half: hi keeps the top 8 significant bits of x
@@ -729,7 +729,7 @@ __device__ __forceinline__ bf16x8_t lds_frag(const unsigned char* p)
 constexpr int kStripWaves = kTileKeys / 16;  // strips of a tile, one one-wave block each
 
 template <int D, int MODE>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(strip_waves(D)))) void
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(strip_waves(D, MODE)))) void
 bwd_key_strip_kernel(BwdParams p)
 {
     constexpr bool MULTI = MODE == kStripMulti;
@@ -811,7 +811,7 @@ bwd_key_strip_kernel(BwdParams p)
 #pragma unroll
     for (int o = 0; o < KS::kOt; ++o) dk[o] = dv[o] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    // staging: lane pair (2 t, 2 t + 1) brings entry slot t's q and dO rows; the even lane also its statistics
+    // staging: lane pair (2 t, 2 t + 1) finds entry slot t; the even lane brings its statistics
     const int t = lane >> 1, hf = lane & 1;
     const uint16_t* const Qb = static_cast<const uint16_t*>(p.Q);
     const uint16_t* const Gb = static_cast<const uint16_t*>(p.dO);
@@ -850,19 +850,35 @@ bwd_key_strip_kernel(BwdParams p)
                 lse = p.lse2[qg];
                 dq = p.Dq[qg];
             }
-            const uint4* src = reinterpret_cast<const uint4*>((hf ? Gb : Qb) + static_cast<size_t>(qg) * D);
-            unsigned char* dst = (hf ? rows_g : rows_q) + t * KS::kRowB;
+            // the chunk's q and dO rows, kLR consecutive lanes per row (whole spans per load): lane l
+            // brings pieces l mod kLR (+ kLR ...) of entry slots l / kLR + kRpi j; entry slot e's query
+            // comes from lane 2 e (-1: past the entries, a zero row keeps the operands finite)
+            constexpr int kLR = KS::kPieces < 8 ? KS::kPieces : 8;  // lanes per row
+            constexpr int kRpi = 64 / kLR;                          // rows per load instruction
+            constexpr int kRep = kCE / kRpi;                        // load instructions per row set
+            constexpr int kPpl = KS::kPieces / kLR;                 // pieces per lane and row
+            const int er = lane / kLR, ep = lane % kLR;
+            const int my_q = code >= 0 ? static_cast<int>(qg) : -1;
+            uint4 val[2][kRep][kPpl];
 #pragma unroll
-            for (int i0 = 0; i0 < KS::kPieces; i0 += 8) {
-                uint4 val[8];
+            for (int j = 0; j < kRep; ++j) {
+                const int qj = __shfl(my_q, 2 * (er + kRpi * j), 64);
 #pragma unroll
-                for (int i = 0; i < 8; ++i)
-                    if (i0 + i < KS::kPieces)
-                        val[i] = code >= 0 ? src[i0 + i] : make_uint4(0u, 0u, 0u, 0u);  // zeros: finite operands
+                for (int a = 0; a < 2; ++a) {
+                    const uint4* src = reinterpret_cast<const uint4*>((a ? Gb : Qb) + static_cast<size_t>(max(qj, 0)) * D);
 #pragma unroll
-                for (int i = 0; i < 8; ++i)
-                    if (i0 + i < KS::kPieces) *reinterpret_cast<uint4*>(dst + (i0 + i) * 16) = val[i];
+                    for (int k = 0; k < kPpl; ++k)
+                        val[a][j][k] = qj >= 0 ? src[ep + kLR * k] : make_uint4(0u, 0u, 0u, 0u);
+                }
             }
+#pragma unroll
+            for (int j = 0; j < kRep; ++j)
+#pragma unroll
+                for (int a = 0; a < 2; ++a)
+#pragma unroll
+                    for (int k = 0; k < kPpl; ++k)
+                        *reinterpret_cast<uint4*>((a ? rows_g : rows_q) + (er + kRpi * j) * KS::kRowB +
+                                                  (ep + kLR * k) * 16) = val[a][j][k];
             if (hf == 0) {
                 int4 meta = make_int4(-(1 << 30), -(1 << 30), 0, 0);  // no key is near this match
                 if constexpr (kQueryIndex) s_el[wave][t][0] = s_el[wave][t][1] = 0;
