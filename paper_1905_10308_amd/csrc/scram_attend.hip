@@ -216,9 +216,9 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
     store_row<T, D, G>(p.out, g, lane, acc, l > 0.f ? 1.f / l : 0.f);  // an empty set gives a zero row
 }
 
-
 // ---------------------------------------------------------------------------
-// K4 on the matrix cores (bf16 storage, one window per query, no mask)
+// K4 on the matrix cores (bf16 storage, windows of side 3, 5 or 7, up to 8
+// maps, with or without the causal mask)
 // ---------------------------------------------------------------------------
 // A wave takes a 4 x 4 tile of queries (16 on an 8 x 8 block tile; 16
 // consecutive items of narrower tiles).  Neighbouring queries' windows
