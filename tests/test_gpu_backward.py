@@ -174,7 +174,8 @@ def test_backward_many_keys(scram, grid, dtype):
 def test_backward_tile_query_union_maps(scram, d, grid):
     """The matrix-core query side over the union of 2, 3 and 4 windows per query (a pass per window, the
     keys of earlier windows left out), with and without the causal mask, on combinations of the stress
-    maps: windows that repeat, overlap by one key or lie apart."""
+    maps: windows that repeat, overlap by one key or lie apart; and 8 windows, where the lane-group query
+    side meets the key strips' several-window test at its largest bound."""
     S, Hq, Wq, Hk, Wk = grid
     rng = np.random.default_rng(Hq * 29 + Wq * 11 + d)
     Q, dO = (rng.standard_normal((S, Hq, Wq, d)).astype(np.float32) for _ in range(2))
@@ -189,6 +190,8 @@ def test_backward_tile_query_union_maps(scram, d, grid):
         "two_far+constant": (m["two_far"], m["constant"]),
         "coherent_twice+outliers": (m["coherent"], m["coherent"], m["outliers"]),
         "four": (m["outliers"], m["lattice6"], m["random"], m["corner_last"]),
+        "eight": tuple(m[k] for k in ("coherent", "outliers", "lattice6", "lattice7", "random", "two_far",
+                                      "corner0", "corner_last")),
     }
     masks = (False, True) if (Hq, Wq) == (Hk, Wk) else (False,)
     worst = 0.0
