@@ -206,6 +206,42 @@ def test_backward_tile_query_union_maps(scram, d, grid):
     log(f"tile union backward {grid} d={d}: max rel err {worst:.3e}")
 
 
+def test_backward_tile_random_shapes(scram):
+    """The matrix-core backward (query side up to 4 maps, key strips) on 12 seeded random problems:
+    grid sides 1-24, one grid or two, 1-2 slices, 1, 2 or 3 maps mixing coherent, shifted and random
+    matches, windows 3/5/7, 32 or 64 channels, the causal mask on one-grid problems half of the time."""
+    rng = np.random.default_rng(1202)
+    for case in range(12):
+        S = int(rng.integers(1, 3))
+        Hq, Wq = (int(x) for x in rng.integers(1, 25, 2))
+        same = bool(rng.random() < 0.6)
+        Hk, Wk = (Hq, Wq) if same else tuple(int(x) for x in rng.integers(1, 25, 2))
+        d = int(rng.choice([32, 64]))
+        kappa = int(rng.choice([1, 2, 3]))
+        window = int(rng.choice([3, 5, 7]))
+        causal = same and bool(rng.random() < 0.5)
+        Q, dO = (rng.standard_normal((S, Hq, Wq, d)).astype(np.float32) for _ in range(2))
+        K, V = (rng.standard_normal((S, Hk, Wk, d)).astype(np.float32) for _ in range(2))
+        Q, K, V, dO = (to_dev(x, "bf16").float().cpu().numpy() for x in (Q, K, V, dO))
+        xs, ys = np.meshgrid(np.arange(Hq), np.arange(Wq), indexing="ij")
+        coherent = np.clip(xs * Hk // Hq, 0, Hk - 1) * Wk + np.clip(ys * Wk // Wq, 0, Wk - 1)
+        maps = []
+        for e in range(kappa):
+            shift = rng.integers(-3, 4, 2)
+            u = np.clip(coherent // Wk + shift[0], 0, Hk - 1)
+            v = np.clip(coherent % Wk + shift[1], 0, Wk - 1)
+            m = np.broadcast_to(u * Wk + v, (S, Hq, Wq)).copy()
+            outlier = rng.random((S, Hq, Wq)) < rng.choice([0.0, 0.1, 1.0])
+            m[outlier] = rng.integers(0, Hk * Wk, int(outlier.sum()))
+            maps.append(m)
+        J = np.ascontiguousarray(np.stack(maps) if kappa > 1 else maps[0], dtype=np.int32)
+        got = scram.sparse_attend_backward(*(to_dev(x, "bf16") for x in (Q, K, V)), torch.from_numpy(J).cuda(),
+                                           to_dev(dO, "bf16"), window, d ** -0.5, causal=causal)
+        ref = oracle.sparse_attend_backward(Q, K, V, J, window, d ** -0.5, dO, flags=oracle.CAUSAL if causal else 0)
+        grads_close(got, ref, f"case {case}: S={S} {Hq}x{Wq}->{Hk}x{Wk} d={d} kappa={kappa} window={window} "
+                              f"causal={causal}")
+
+
 @pytest.mark.parametrize("dtype,d,scale", [("f32", 16, 1 / 2), ("bf16", 64, 1 / 4)])
 def test_backward_wide_score_range(scram, dtype, d, scale):
     """Small-integer q, k (exact dot products) with a power-of-two scale near 2/sqrt(d): window scores

@@ -544,6 +544,50 @@ def test_attend_tile_kernel_union_maps(scram, d, grid):
     log(f"tile union attend {grid} d={d}: max rel err {worst:.3e}")
 
 
+def test_attend_tile_kernel_random_shapes(scram):
+    """The matrix-core attend on 24 seeded random problems: grid sides 1-40 (one grid or a query grid
+    resampled onto a key grid of other sides), 1-3 slices, 1, 2, 3 or 5 maps mixing coherent,
+    shifted and uniformly random matches, windows 3/5/7, 32 or 64 channels, the causal mask on one-grid
+    problems half of the time."""
+    rng = np.random.default_rng(20261202)
+    worst = 0.0
+    for case in range(24):
+        S = int(rng.integers(1, 4))
+        Hq, Wq = (int(x) for x in rng.integers(1, 41, 2))
+        same = bool(rng.random() < 0.6)
+        Hk, Wk = (Hq, Wq) if same else tuple(int(x) for x in rng.integers(1, 41, 2))
+        d = int(rng.choice([32, 64]))
+        kappa = int(rng.choice([1, 2, 3, 5]))
+        window = int(rng.choice([3, 5, 7]))
+        causal = same and bool(rng.random() < 0.5)
+        Q = rng.standard_normal((S, Hq, Wq, d)).astype(np.float32)
+        K = rng.standard_normal((S, Hk, Wk, d)).astype(np.float32)
+        V = rng.standard_normal((S, Hk, Wk, d)).astype(np.float32)
+        Q, K, V = (to_dev(x, "bf16").float().cpu().numpy() for x in (Q, K, V))
+        xs, ys = np.meshgrid(np.arange(Hq), np.arange(Wq), indexing="ij")
+        coherent = np.clip(xs * Hk // Hq, 0, Hk - 1) * Wk + np.clip(ys * Wk // Wq, 0, Wk - 1)
+        maps = []
+        for e in range(kappa):
+            shift = rng.integers(-3, 4, 2)
+            u = np.clip(coherent // Wk + shift[0], 0, Hk - 1)
+            v = np.clip(coherent % Wk + shift[1], 0, Wk - 1)
+            m = np.broadcast_to(u * Wk + v, (S, Hq, Wq)).copy()
+            outlier = rng.random((S, Hq, Wq)) < rng.choice([0.0, 0.1, 1.0])
+            m[outlier] = rng.integers(0, Hk * Wk, int(outlier.sum()))
+            maps.append(m)
+        J = np.ascontiguousarray(np.stack(maps) if kappa > 1 else maps[0], dtype=np.int32)
+        out = scram.sparse_attend(*(to_dev(x, "bf16") for x in (Q, K, V)), torch.from_numpy(J).cuda(), window,
+                                  d ** -0.5, causal=causal).float().cpu().numpy()
+        ref = oracle.sparse_attend(Q, K, V, J, window, d ** -0.5, flags=oracle.CAUSAL if causal else 0)
+        tag = f"case {case}: S={S} {Hq}x{Wq}->{Hk}x{Wk} d={d} kappa={kappa} window={window} causal={causal}"
+        empty = ~np.any(ref != 0, axis=-1)
+        assert (out[empty] == 0).all(), f"{tag}: empty rows"
+        err = float(row_rel_err(out[~empty], ref[~empty]).max(initial=0.0))
+        worst = max(worst, err)
+        assert err <= TOL["bf16"], f"{tag}: {err:.3e}"
+    log(f"tile attend, 24 random problems: max rel err {worst:.3e}")
+
+
 @pytest.mark.parametrize("Wk", [8191, 8192], ids=["last_slice_under_4GiB", "slice_of_4GiB"])
 def test_attend_key_slice_at_4gib(scram, Wk):
     """A 4096 x Wk key grid of 64 bf16 channels: 8191 columns make the slice's rows 2^32 - 524288
