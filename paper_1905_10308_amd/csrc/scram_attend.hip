@@ -492,7 +492,7 @@ attend_tile_kernel(AttParams p)
         int rr = mr - wr0;
         const bool here = c == mine;
         const uint32_t wc = here ? wcols : 0u;
-        const uint32_t wc2 = here ? wcols << bx.bw : 0u;  // bw <= 19, and only bits below bw + 3 are read
+        const uint32_t wc2 = here ? wcols << bx.bw : 0u;  // bw <= 27, and only bits below bw + 3 are read
         const uint32_t wk = CAUSAL && here ? tc.wcut : 0u;  // the query's own row (causal)
         const uint32_t wk2 = CAUSAL && here ? tc.wcut << bx.bw : 0u;
         if constexpr (MK > 1) {
@@ -600,7 +600,9 @@ hipError_t run_attend(const AttParams& p0, int window, hipStream_t st, hipEvent_
         if (p.kappa <= kMaxKappa && (window == 3 || window == 5 || window == 7) && p.scale_log2e > 0.f &&
             static_cast<uint64_t>(p.nkeys) * (2 * D) <= 0xFFFFFFFFull) {
             p.tq = make_tiling(p.Hq, p.Wq, kBlock / 4);
-            p.rc = 6;  // boxes at most 12 + window wide: slots of a box stay below 1024
+            // cluster radius: boxes at most 2 rc + window wide (27 for 7 x 7 windows), so a box's slots stay
+            // below 1024 and its two-row column bit fields below 32 bits; 10 measured faster than 4-8 and 11
+            p.rc = 10;
             const uint64_t tiles = tiling_blocks(p.tq, p.n / p.tq.plane);
             auto go = [&](auto w) {
                 constexpr int Wn = decltype(w)::value;

@@ -1259,7 +1259,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
         int rr = mr - tc.wr0;
         const bool here = c == tc.mine;
         const uint32_t wc = here ? tc.wcols : 0u;
-        const uint32_t wc2 = here ? tc.wcols << bx.bw : 0u;  // bw <= 19, and only bits below bw + 3 are read
+        const uint32_t wc2 = here ? tc.wcols << bx.bw : 0u;  // bw <= 27, and only bits below bw + 3 are read
         const uint32_t wk = CAUSAL && here ? tc.wcut : 0u;  // the query's own row (causal)
         const uint32_t wk2 = CAUSAL && here ? tc.wcut << bx.bw : 0u;
         if constexpr (MK > 1) {
@@ -1387,7 +1387,7 @@ hipError_t run_backward(const BwdParams& p0, hipStream_t st, hipEvent_t* ev, Inv
             static_cast<uint64_t>(p.nkeys) * (2 * D) <= 0xFFFFFFFFull) {
             BwdParams pq = p;
             pq.tq = make_tiling(p.Hq, p.Wq, kBlock / 4);
-            pq.rc = 6;  // as in the attend's matrix-core kernel
+            pq.rc = 10;  // as in the attend's matrix-core kernel
             const uint64_t tb = tiling_blocks(pq.tq, p.n / pq.tq.plane);
             auto go = [&](auto w) {
                 constexpr int Wn = decltype(w)::value;

@@ -122,9 +122,11 @@ def tile_maps(S, Hq, Wq, Hk, Wk, rng):
         "corner0": np.zeros((S, Hq, Wq)),
         "corner_last": np.full((S, Hq, Wq), Hk * Wk - 1),
         "coherent": coherent,
-        # centres on a lattice 6 and 7 apart: exactly at and just past the cluster radius
+        # centres on lattices 6, 7, 10 and 11 apart: within, at and just past the cluster radius (10)
         "lattice6": np.broadcast_to(np.clip(xs * 6, 0, Hk - 1) * Wk + np.clip(ys * 6, 0, Wk - 1), (S, Hq, Wq)),
         "lattice7": np.broadcast_to(np.clip(xs * 7, 0, Hk - 1) * Wk + np.clip(ys * 7, 0, Wk - 1), (S, Hq, Wq)),
+        "lattice10": np.broadcast_to(np.clip(xs * 10, 0, Hk - 1) * Wk + np.clip(ys * 10, 0, Wk - 1), (S, Hq, Wq)),
+        "lattice11": np.broadcast_to(np.clip(xs * 11, 0, Hk - 1) * Wk + np.clip(ys * 11, 0, Wk - 1), (S, Hq, Wq)),
         # two far-apart keys alternating: two clusters in every wave
         "two_far": np.where((xs + ys) % 2 == 0, 0, Hk * Wk - 1) + np.zeros((S, 1, 1), np.int64),
         # coherent with 10 % random outliers
