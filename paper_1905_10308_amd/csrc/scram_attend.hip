@@ -481,75 +481,75 @@ attend_tile_kernel(AttParams p)
     // The blocks of a cluster are computed in a row; each block's rows load during the previous block's
     // products, the first block of the next cluster during the last block of this one.
     for (int e = 0;;) {
-    Box bx = box_of(0);
-    int lc;
-    uint32_t lkey;
-    first_slot(bx, lc, lkey);
-    load(lkey, bx.klast);
-    for (int c = 0;;) {
-        int mr, mcl;
-        box_slot(4 * g4, bx.bw, bx.inv, mr, mcl);
-        int rr = mr - wr0;
-        const bool here = c == mine;
-        const uint32_t wc = here ? wcols : 0u;
-        const uint32_t wc2 = here ? wcols << bx.bw : 0u;  // bw <= 27, and only bits below bw + 3 are read
-        const uint32_t wk = CAUSAL && here ? tc.wcut : 0u;  // the query's own row (causal)
-        const uint32_t wk2 = CAUSAL && here ? tc.wcut << bx.bw : 0u;
-        if constexpr (MK > 1) {
+        Box bx = box_of(0);
+        int lc;
+        uint32_t lkey;
+        first_slot(bx, lc, lkey);
+        load(lkey, bx.klast);
+        for (int c = 0;;) {
+            int mr, mcl;
+            box_slot(4 * g4, bx.bw, bx.inv, mr, mcl);
+            int rr = mr - wr0;
+            const bool here = c == mine;
+            const uint32_t wc = here ? wcols : 0u;
+            const uint32_t wc2 = here ? wcols << bx.bw : 0u;  // bw <= 27, and only bits below bw + 3 are read
+            const uint32_t wk = CAUSAL && here ? tc.wcut : 0u;  // the query's own row (causal)
+            const uint32_t wk2 = CAUSAL && here ? tc.wcut << bx.bw : 0u;
+            if constexpr (MK > 1) {
 #pragma unroll
-            for (int f = 0; f < kOther; ++f)
-                xw[f] = here && f < e ? tile_col_bits(cv[f] - B - bx.c0, cv[f] + B - bx.c0, bx.bw) : 0u;
-        }
-        thr = here ? thr_q : INFINITY;  // a query's cluster is visited once per window, its blocks in a row
-        step_slot(bx, lc, lkey);
-        for (int k = 1; k < bx.nb; ++k) {
-            stage();
-            load(lkey, bx.klast);
+                for (int f = 0; f < kOther; ++f)
+                    xw[f] = here && f < e ? tile_col_bits(cv[f] - B - bx.c0, cv[f] + B - bx.c0, bx.bw) : 0u;
+            }
+            thr = here ? thr_q : INFINITY;  // a query's cluster is visited once per window, its blocks in a row
             step_slot(bx, lc, lkey);
+            for (int k = 1; k < bx.nb; ++k) {
+                stage();
+                load(lkey, bx.klast);
+                step_slot(bx, lc, lkey);
+                wave_lds_sync();
+                compute(bx, rr, mcl, wc, wc2, wk, wk2);
+                mcl += bx.r16;
+                const bool carry = mcl >= bx.bw;
+                mcl -= carry ? bx.bw : 0;
+                rr += bx.q16 + (carry ? 1 : 0);
+                wave_lds_sync();  // this block's LDS reads come before the next block's writes
+            }
+            stage();
+            const bool more = c + 1 < nclu;
+            Box nx = bx;
+            if (more) {
+                nx = box_of(c + 1);
+                first_slot(nx, lc, lkey);
+                load(lkey, nx.klast);
+            }
             wave_lds_sync();
             compute(bx, rr, mcl, wc, wc2, wk, wk2);
-            mcl += bx.r16;
-            const bool carry = mcl >= bx.bw;
-            mcl -= carry ? bx.bw : 0;
-            rr += bx.q16 + (carry ? 1 : 0);
-            wave_lds_sync();  // this block's LDS reads come before the next block's writes
+            if (!more) break;
+            bx = nx;
+            ++c;
+            wave_lds_sync();
         }
-        stage();
-        const bool more = c + 1 < nclu;
-        Box nx = bx;
-        if (more) {
-            nx = box_of(c + 1);
-            first_slot(nx, lc, lkey);
-            load(lkey, nx.klast);
+        if constexpr (MK == 1) {
+            break;
+        } else {
+            if (e + 1 >= p.kappa) break;
+            // the next window: its centres' clusters and boxes; window e joins the earlier ones
+#pragma unroll
+            for (int f = 0; f < kOther; ++f)
+                if (f == e) cu[f] = u, cv[f] = v;
+            ++e;
+            const uint32_t ce = static_cast<uint32_t>(clamp_index(p.J[static_cast<size_t>(e) * p.n + gq], p.nkeys));
+            uint32_t uu, vv;
+            divmod(ce, p.div_wk, uu, vv);
+            u = static_cast<int>(uu);
+            v = static_cast<int>(vv);
+#pragma unroll
+            for (int f = 0; f < kOther; ++f) dw[f] = f < e ? cu[f] - u : 1 << 20;
+            tc = tile_clusters<B, CAUSAL>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk, qx, qy);
+            nclu = tc.nclu, mine = tc.mine, wr0 = tc.wr0, wrn = tc.wrn;
+            wcols = tc.wcols;
+            wave_lds_sync();  // the last block's LDS reads come before the next pass's writes
         }
-        wave_lds_sync();
-        compute(bx, rr, mcl, wc, wc2, wk, wk2);
-        if (!more) break;
-        bx = nx;
-        ++c;
-        wave_lds_sync();
-    }
-    if constexpr (MK == 1) {
-        break;
-    } else {
-        if (e + 1 >= p.kappa) break;
-        // the next window: its centres' clusters and boxes; window e joins the earlier ones
-#pragma unroll
-        for (int f = 0; f < kOther; ++f)
-            if (f == e) cu[f] = u, cv[f] = v;
-        ++e;
-        const uint32_t ce = static_cast<uint32_t>(clamp_index(p.J[static_cast<size_t>(e) * p.n + gq], p.nkeys));
-        uint32_t uu, vv;
-        divmod(ce, p.div_wk, uu, vv);
-        u = static_cast<int>(uu);
-        v = static_cast<int>(vv);
-#pragma unroll
-        for (int f = 0; f < kOther; ++f) dw[f] = f < e ? cu[f] - u : 1 << 20;
-        tc = tile_clusters<B, CAUSAL>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk, qx, qy);
-        nclu = tc.nclu, mine = tc.mine, wr0 = tc.wr0, wrn = tc.wrn;
-        wcols = tc.wcols;
-        wave_lds_sync();  // the last block's LDS reads come before the next pass's writes
-    }
     }
     if (!valid) return;
     const float lt = lacc[0];  // every row of the ones-block product holds query m's sum of weights

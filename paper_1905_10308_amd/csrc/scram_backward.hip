@@ -109,7 +109,8 @@ __device__ int32_t block_exclusive_scan(const int32_t* in, int32_t* out, size_t 
 // Exclusive scan, step 1: each block scans a tile of kScanTile counts into
 // out (tile-local prefixes; out may be in) and writes the tile's total to
 // sums[tile].
-__global__ __launch_bounds__(kBlock) void scan_tiles_kernel(const int32_t* in, int32_t* out, int32_t* sums, size_t count)
+__global__ __launch_bounds__(kBlock) void scan_tiles_kernel(const int32_t* in, int32_t* out, int32_t* sums,
+                                                            size_t count)
 {
     __shared__ int32_t wave_tot[kBlock / 64];
     const size_t base = static_cast<size_t>(blockIdx.x) * kScanTile;
@@ -865,7 +866,8 @@ bwd_key_strip_kernel(BwdParams p)
                 const int qj = __shfl(my_q, 2 * (er + kRpi * j), 64);
 #pragma unroll
                 for (int a = 0; a < 2; ++a) {
-                    const uint4* src = reinterpret_cast<const uint4*>((a ? Gb : Qb) + static_cast<size_t>(max(qj, 0)) * D);
+                    const uint16_t* const row = (a ? Gb : Qb) + static_cast<size_t>(max(qj, 0)) * D;
+                    const uint4* src = reinterpret_cast<const uint4*>(row);
 #pragma unroll
                     for (int k = 0; k < kPpl; ++k)
                         val[a][j][k] = qj >= 0 ? src[ep + kLR * k] : make_uint4(0u, 0u, 0u, 0u);
@@ -1248,73 +1250,73 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
 
     // the blocks of each cluster in a row; each block's rows load during the previous block's products
     for (int e = 0;;) {
-    TileBox bx = tile_box(tc, 0, p.Wk);
-    int lc;
-    uint32_t lkey;
-    first_slot(bx, lc, lkey);
-    load(lkey, bx.klast);
-    for (int c = 0;;) {
-        int mr, mcl;
-        box_slot(4 * g4, bx.bw, bx.inv, mr, mcl);
-        int rr = mr - tc.wr0;
-        const bool here = c == tc.mine;
-        const uint32_t wc = here ? tc.wcols : 0u;
-        const uint32_t wc2 = here ? tc.wcols << bx.bw : 0u;  // bw <= 27, and only bits below bw + 3 are read
-        const uint32_t wk = CAUSAL && here ? tc.wcut : 0u;  // the query's own row (causal)
-        const uint32_t wk2 = CAUSAL && here ? tc.wcut << bx.bw : 0u;
-        if constexpr (MK > 1) {
+        TileBox bx = tile_box(tc, 0, p.Wk);
+        int lc;
+        uint32_t lkey;
+        first_slot(bx, lc, lkey);
+        load(lkey, bx.klast);
+        for (int c = 0;;) {
+            int mr, mcl;
+            box_slot(4 * g4, bx.bw, bx.inv, mr, mcl);
+            int rr = mr - tc.wr0;
+            const bool here = c == tc.mine;
+            const uint32_t wc = here ? tc.wcols : 0u;
+            const uint32_t wc2 = here ? tc.wcols << bx.bw : 0u;  // bw <= 27, and only bits below bw + 3 are read
+            const uint32_t wk = CAUSAL && here ? tc.wcut : 0u;  // the query's own row (causal)
+            const uint32_t wk2 = CAUSAL && here ? tc.wcut << bx.bw : 0u;
+            if constexpr (MK > 1) {
 #pragma unroll
-            for (int f = 0; f < kOther; ++f)
-                xw[f] = here && f < e ? tile_col_bits(cv[f] - B - bx.c0, cv[f] + B - bx.c0, bx.bw) : 0u;
-        }
-        thr = here ? thr_q : INFINITY;  // a query's cluster is visited once per window, its blocks in a row
-        step_slot(bx, lc, lkey);
-        for (int k = 1; k < bx.nb; ++k) {
-            stage();
-            load(lkey, bx.klast);
+                for (int f = 0; f < kOther; ++f)
+                    xw[f] = here && f < e ? tile_col_bits(cv[f] - B - bx.c0, cv[f] + B - bx.c0, bx.bw) : 0u;
+            }
+            thr = here ? thr_q : INFINITY;  // a query's cluster is visited once per window, its blocks in a row
             step_slot(bx, lc, lkey);
+            for (int k = 1; k < bx.nb; ++k) {
+                stage();
+                load(lkey, bx.klast);
+                step_slot(bx, lc, lkey);
+                wave_lds_sync();
+                compute(bx, rr, mcl, wc, wc2, wk, wk2);
+                mcl += bx.r16;
+                const bool carry = mcl >= bx.bw;
+                mcl -= carry ? bx.bw : 0;
+                rr += bx.q16 + (carry ? 1 : 0);
+                wave_lds_sync();  // this block's LDS reads come before the next block's writes
+            }
+            stage();
+            const bool more = c + 1 < tc.nclu;
+            TileBox nx = bx;
+            if (more) {
+                nx = tile_box(tc, c + 1, p.Wk);
+                first_slot(nx, lc, lkey);
+                load(lkey, nx.klast);
+            }
             wave_lds_sync();
             compute(bx, rr, mcl, wc, wc2, wk, wk2);
-            mcl += bx.r16;
-            const bool carry = mcl >= bx.bw;
-            mcl -= carry ? bx.bw : 0;
-            rr += bx.q16 + (carry ? 1 : 0);
-            wave_lds_sync();  // this block's LDS reads come before the next block's writes
+            if (!more) break;
+            bx = nx;
+            ++c;
+            wave_lds_sync();
         }
-        stage();
-        const bool more = c + 1 < tc.nclu;
-        TileBox nx = bx;
-        if (more) {
-            nx = tile_box(tc, c + 1, p.Wk);
-            first_slot(nx, lc, lkey);
-            load(lkey, nx.klast);
+        if constexpr (MK == 1) {
+            break;
+        } else {
+            if (e + 1 >= p.kappa) break;
+            // the next window: its centres' clusters and boxes; window e joins the earlier ones
+#pragma unroll
+            for (int f = 0; f < kOther; ++f)
+                if (f == e) cu[f] = u, cv[f] = v;
+            ++e;
+            const uint32_t ce = static_cast<uint32_t>(clamp_index(p.J[static_cast<size_t>(e) * p.n + gq], p.nkeys));
+            uint32_t uu, vv;
+            divmod(ce, p.div_wk, uu, vv);
+            u = static_cast<int>(uu);
+            v = static_cast<int>(vv);
+#pragma unroll
+            for (int f = 0; f < kOther; ++f) dw[f] = f < e ? cu[f] - u : 1 << 20;
+            tc = tile_clusters<B, CAUSAL>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk, qx, qy);
+            wave_lds_sync();  // the last block's LDS reads come before the next pass's writes
         }
-        wave_lds_sync();
-        compute(bx, rr, mcl, wc, wc2, wk, wk2);
-        if (!more) break;
-        bx = nx;
-        ++c;
-        wave_lds_sync();
-    }
-    if constexpr (MK == 1) {
-        break;
-    } else {
-        if (e + 1 >= p.kappa) break;
-        // the next window: its centres' clusters and boxes; window e joins the earlier ones
-#pragma unroll
-        for (int f = 0; f < kOther; ++f)
-            if (f == e) cu[f] = u, cv[f] = v;
-        ++e;
-        const uint32_t ce = static_cast<uint32_t>(clamp_index(p.J[static_cast<size_t>(e) * p.n + gq], p.nkeys));
-        uint32_t uu, vv;
-        divmod(ce, p.div_wk, uu, vv);
-        u = static_cast<int>(uu);
-        v = static_cast<int>(vv);
-#pragma unroll
-        for (int f = 0; f < kOther; ++f) dw[f] = f < e ? cu[f] - u : 1 << 20;
-        tc = tile_clusters<B, CAUSAL>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk, qx, qy);
-        wave_lds_sync();  // the last block's LDS reads come before the next pass's writes
-    }
     }
     if (!valid) return;
     const float l = lacc[0], dn = dacc[0];

@@ -28,7 +28,10 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 
 // bf16 pair (a in the low half, b in the high half) from the high halves of two fp32 patterns
-__device__ __forceinline__ uint32_t hi16_pair(uint32_t a, uint32_t b) { return __builtin_amdgcn_perm(b, a, 0x07060302u); }
+__device__ __forceinline__ uint32_t hi16_pair(uint32_t a, uint32_t b)
+{
+    return __builtin_amdgcn_perm(b, a, 0x07060302u);
+}
 
 template <int CTRL>
 __device__ __forceinline__ int dpp_i(int x)
