@@ -260,8 +260,9 @@ int scram_sparse_attend(const void* Q, const void* K, const void* V, int dtype, 
  * weights are recomputed from Q, K, V (the forward output is not needed).
  * Key j lies in W_i exactly when a match of query i lies in the
  * (2b+1) x (2b+1) neighbourhood of j, so dK_j and dV_j gather over the
- * queries found through the inverse of the maps (kept in the workspace,
- * with copies of those queries' q, dO rows in the inverse map's order).
+ * queries found through the inverse of the maps (kept in the workspace; for
+ * fp32 storage and for windows of side 1 or above 15 the key side also copies
+ * those queries' q, dO rows there in the inverse map's order).
  * Every gradient row has a single writer; the order in which the queries of
  * one match key are summed is the order the inverse map was filled in,
  * which may differ between calls (dK, dV may differ in the last bits; dQ is
