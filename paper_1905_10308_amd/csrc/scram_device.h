@@ -94,15 +94,28 @@ __device__ __forceinline__ uint32_t xcd_remap(uint32_t b, uint32_t nb)
 
 // Block tiles.  The lane groups of a block cover a tile of `items` positions
 // (a power of two; raster order inside the tile) of one slice's 2-D grid;
-// blocks take the tiles of slice 0 in raster order, then those of slice 1,
-// ...  Neighbouring positions have nearby matches, so a squarish tile shares
-// more of the rows its lane groups read in L1 than a row segment of the same
-// size.  Grids narrower than the squarish tile get a flatter one, so that
-// 1-D grids keep every lane group busy.
+// blocks take the tiles of slice 0, then those of slice 1, ...  Within a
+// slice the tiles go in raster order; on grids more than kBandMax tiles wide,
+// in bands of kBandTiles tile columns instead (top to bottom, left to right
+// within a band's tile row), so that the blocks in flight on an XCD cover a
+// compact patch of the grid rather than part of one long tile row, and a
+// tile's neighbours below are dispatched soon after it.  Neighbouring
+// positions have nearby matches, so a squarish tile shares more of the rows
+// its lane groups read in L1 than a row segment of the same size.  Grids
+// narrower than the squarish tile get a flatter one, so that 1-D grids keep
+// every lane group busy.
+#ifndef SCRAM_BAND_TILES
+#define SCRAM_BAND_TILES 16
+#endif
+constexpr uint32_t kBandTiles = SCRAM_BAND_TILES;
+constexpr uint32_t kBandMax = 64;
+
 struct Tiling {
     uint32_t H, W, plane;  // one slice's grid
     uint32_t lw;           // log2 of the tile width
+    uint32_t nw, bw;       // tiles per grid row, tile columns per band (nw: one band, raster order)
     Div div_w, div_slice;  // tiles per grid row, tiles per slice
+    Div div_band, div_bw;  // tiles per band, bw
 };
 
 // Host: the tiling of one slice's H x W grid by blocks of `items` positions.
@@ -127,8 +140,9 @@ inline Tiling make_tiling(int H, int W, uint32_t items)
     lw = 0;
     while ((1u << lw) < tw) ++lw;
     const uint32_t nw = (static_cast<uint32_t>(W) + tw - 1) / tw, nh = (static_cast<uint32_t>(H) + th - 1) / th;
-    return Tiling{static_cast<uint32_t>(H), static_cast<uint32_t>(W), static_cast<uint32_t>(H) * W, lw,
-                  make_div(nw), make_div(nw * nh)};
+    const uint32_t bw = nw > kBandMax ? kBandTiles : nw;
+    return Tiling{static_cast<uint32_t>(H), static_cast<uint32_t>(W), static_cast<uint32_t>(H) * W, lw, nw, bw,
+                  make_div(nw), make_div(nw * nh), make_div(bw * nh), make_div(bw)};
 }
 
 inline uint64_t tiling_blocks(const Tiling& t, uint32_t slices) { return uint64_t(slices) * t.div_slice.d; }
@@ -140,9 +154,17 @@ template <uint32_t kItems>
 __device__ __forceinline__ bool tile_item(const Tiling& t, uint32_t blk, uint32_t i, uint32_t& g)
 {
     static_assert((kItems & (kItems - 1)) == 0, "tiles of a power-of-two size");
-    uint32_t s, k, tr, tc;
+    uint32_t s, k, band, rem, tr, tc;
     divmod(blk, t.div_slice, s, k);
-    divmod(k, t.div_w, tr, tc);
+    divmod(k, t.div_band, band, rem);
+    const uint32_t c0 = band * t.bw, wb = min(t.bw, t.nw - c0);  // the last band may be narrower
+    if (wb == t.bw) {
+        divmod(rem, t.div_bw, tr, tc);
+    } else {
+        tr = rem / wb;
+        tc = rem - tr * wb;
+    }
+    tc += c0;
     const uint32_t th = kItems >> t.lw;
     const uint32_t x = tr * th + (i >> t.lw), y = (tc << t.lw) + (i & ((1u << t.lw) - 1u));
     g = s * t.plane + x * t.W + y;

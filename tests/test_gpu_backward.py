@@ -206,6 +206,25 @@ def test_backward_tile_query_union_maps(scram, d, grid):
     log(f"tile union backward {grid} d={d}: max rel err {worst:.3e}")
 
 
+@pytest.mark.parametrize("causal", [False, True])
+def test_backward_wide_grid(scram, causal):
+    """A 9 x 1100 grid (138 tiles per row: blocks take the tiles in bands, the last one narrower), bf16,
+    64 channels, 5 x 5 windows, coherent matches with 10 % random ones."""
+    rng = np.random.default_rng(1100)
+    S, H, W, d = 1, 9, 1100, 64
+    Q, K, V, dO = (rng.standard_normal((S, H, W, d)).astype(np.float32) for _ in range(4))
+    Q, K, V, dO = (to_dev(x, "bf16").float().cpu().numpy() for x in (Q, K, V, dO))
+    xs, ys = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    J = np.broadcast_to(np.clip(xs + 1, 0, H - 1) * W + np.clip(ys - 2, 0, W - 1), (S, H, W)).copy()
+    out = rng.random(J.shape) < 0.1
+    J[out] = rng.integers(0, H * W, int(out.sum()))
+    J = J.astype(np.int32)
+    got = scram.sparse_attend_backward(*(to_dev(x, "bf16") for x in (Q, K, V)), torch.from_numpy(J).cuda(),
+                                       to_dev(dO, "bf16"), 5, d ** -0.5, causal=causal)
+    ref = oracle.sparse_attend_backward(Q, K, V, J, 5, d ** -0.5, dO, flags=oracle.CAUSAL if causal else 0)
+    grads_close(got, ref, f"wide grid causal {causal}")
+
+
 def test_backward_tile_random_shapes(scram):
     """The matrix-core backward (query side up to 4 maps, key strips) on 12 seeded random problems:
     grid sides 1-24, one grid or two, 1-2 slices, 1, 2 or 3 maps mixing coherent, shifted and random

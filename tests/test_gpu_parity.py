@@ -317,6 +317,9 @@ SHAPES = [
     (2, 17, 13, 17, 13, 16, "bf16"),
     (1, 33, 31, 20, 50, 64, "bf16"),
     (5, 7, 9, 7, 9, 32, "f32"),
+    # wide grids: more than 64 tiles per row, so blocks take the tiles in bands, the last one narrower
+    (1, 9, 1100, 9, 1100, 64, "bf16"),
+    (2, 12, 700, 12, 700, 32, "f32"),
 ]
 
 
