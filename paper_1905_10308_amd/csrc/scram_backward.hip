@@ -670,8 +670,9 @@ __global__ __launch_bounds__(kBlock) void bwd_heavy_kernel(BwdParams p)
 
 // ---------------------------------------------------------------------------
 // Key side on the matrix cores (bf16 storage).  Each wave takes a strip of 16
-// keys (items 16 w .. 16 w + 15, raster order, of a 64-key tile: 2 rows of 8
-// on square grids) and works alone, a block of its own: the number of entries
+// keys of a 64-key tile (a 4 x 4 quarter of an 8 x 8 tile; items 16 w .. 16 w
+// + 15 in raster order of flatter or taller tiles) and works alone, a block
+// of its own: the number of entries
 // per strip is very uneven, and a wave that finishes releases its LDS at once
 // instead of holding it until the slowest strip of a shared block is done.  The
 // queries whose key sets reach the strip are exactly the entries whose match
@@ -757,9 +758,19 @@ bwd_key_strip_kernel(BwdParams p)
     divmod(k, p.tk.div_w, tr, tc);
     const int tw = 1 << p.tk.lw, th = kTileKeys >> p.tk.lw;
     const int x0 = static_cast<int>(tr) * th, y0 = static_cast<int>(tc) * tw;
-    const int it0 = 16 * static_cast<int>(blk % kStripWaves);
-    const int sr0 = x0 + (it0 >> p.tk.lw), sr1 = x0 + ((it0 + 15) >> p.tk.lw);
-    const int sc0 = y0 + (it0 & (tw - 1)), sc1 = sc0 + min(tw, 16) - 1;
+    const int w4 = static_cast<int>(blk % kStripWaves);
+    // the strip: a 4 x 4 quarter of an 8 x 8 tile (its halo holds 11 % fewer match positions than that
+    // of 2 rows of 8), else items 16 w4 .. 16 w4 + 15 of the tile in raster order; key i of the strip
+    const bool quad = p.tk.lw == 3 && th == 8;
+    const int it0 = 16 * w4;
+    const int sr0 = quad ? x0 + 4 * (w4 >> 1) : x0 + (it0 >> p.tk.lw);
+    const int sr1 = quad ? sr0 + 3 : x0 + ((it0 + 15) >> p.tk.lw);
+    const int sc0 = quad ? y0 + 4 * (w4 & 1) : y0 + (it0 & (tw - 1));
+    const int sc1 = quad ? sc0 + 3 : sc0 + min(tw, 16) - 1;
+    auto strip_key = [&](int i, int& x, int& y) {
+        x = quad ? sr0 + (i >> 2) : x0 + ((it0 + i) >> p.tk.lw);
+        y = quad ? sc0 + (i & 3) : y0 + ((it0 + i) & (tw - 1));
+    };
     if (sr0 >= p.Hk || sc0 >= p.Wk) return;  // the strip lies past the grid's edge
     const int hr0 = max(sr0 - p.b, 0), hr1 = min(sr1 + p.b, p.Hk - 1);
     const int hc0 = max(sc0 - p.b, 0), hc1 = min(sc1 + p.b, p.Wk - 1);
@@ -789,8 +800,9 @@ bwd_key_strip_kernel(BwdParams p)
     }
     wave_lds_sync();
 
-    // this lane's key (column of the first products): item it0 + m of the tile
-    const int kx = x0 + ((it0 + m) >> p.tk.lw), ky = y0 + ((it0 + m) & (tw - 1));
+    // this lane's key (column of the first products): key m of the strip
+    int kx, ky;
+    strip_key(m, kx, ky);
     const bool key_ok = kx < p.Hk && ky < p.Wk;
     const size_t kslice = static_cast<size_t>(s) * p.nkeys;
     const size_t krow = kslice + (key_ok ? static_cast<size_t>(kx) * p.Wk + ky : static_cast<size_t>(sr0) * p.Wk + sc0);
@@ -974,8 +986,8 @@ bwd_key_strip_kernel(BwdParams p)
     // lane holds keys 4 g4 + r of the strip, channel 16 o + m
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-        const int it = it0 + 4 * g4 + r;
-        const int ox = x0 + (it >> p.tk.lw), oy = y0 + (it & (tw - 1));
+        int ox, oy;
+        strip_key(4 * g4 + r, ox, oy);
         if (ox >= p.Hk || oy >= p.Wk) continue;
         const size_t row = (kslice + static_cast<size_t>(ox) * p.Wk + oy) * D;
 #pragma unroll
