@@ -755,7 +755,7 @@ bwd_key_strip_kernel(BwdParams p)
     // the tile (th x tw keys at x0, y0 of slice s) and this wave's strip in it
     uint32_t s, k, tr, tc;
     divmod(blk / kStripWaves, p.tk.div_slice, s, k);
-    divmod(k, p.tk.div_w, tr, tc);
+    tile_coords(p.tk, k, tr, tc);
     const int tw = 1 << p.tk.lw, th = kTileKeys >> p.tk.lw;
     const int x0 = static_cast<int>(tr) * th, y0 = static_cast<int>(tc) * tw;
     const int w4 = static_cast<int>(blk % kStripWaves);

@@ -114,7 +114,7 @@ struct Tiling {
     uint32_t H, W, plane;  // one slice's grid
     uint32_t lw;           // log2 of the tile width
     uint32_t nw, bw;       // tiles per grid row, tile columns per band (nw: one band, raster order)
-    Div div_w, div_slice;  // tiles per grid row, tiles per slice
+    Div div_slice;         // tiles per slice
     Div div_band, div_bw;  // tiles per band, bw
 };
 
@@ -142,20 +142,15 @@ inline Tiling make_tiling(int H, int W, uint32_t items)
     const uint32_t nw = (static_cast<uint32_t>(W) + tw - 1) / tw, nh = (static_cast<uint32_t>(H) + th - 1) / th;
     const uint32_t bw = nw > kBandMax ? kBandTiles : nw;
     return Tiling{static_cast<uint32_t>(H), static_cast<uint32_t>(W), static_cast<uint32_t>(H) * W, lw, nw, bw,
-                  make_div(nw), make_div(nw * nh), make_div(bw * nh), make_div(bw)};
+                  make_div(nw * nh), make_div(bw * nh), make_div(bw)};
 }
 
 inline uint64_t tiling_blocks(const Tiling& t, uint32_t slices) { return uint64_t(slices) * t.div_slice.d; }
 
-// Flat position g = s * H * W + x * W + y of item i (< kItems) of (remapped)
-// block blk; false past the grid's right or bottom edge (g is then not
-// meaningful).
-template <uint32_t kItems>
-__device__ __forceinline__ bool tile_item(const Tiling& t, uint32_t blk, uint32_t i, uint32_t& g)
+// Tile row and column of the k-th tile of a slice, in the order above.
+__device__ __forceinline__ void tile_coords(const Tiling& t, uint32_t k, uint32_t& tr, uint32_t& tc)
 {
-    static_assert((kItems & (kItems - 1)) == 0, "tiles of a power-of-two size");
-    uint32_t s, k, band, rem, tr, tc;
-    divmod(blk, t.div_slice, s, k);
+    uint32_t band, rem;
     divmod(k, t.div_band, band, rem);
     const uint32_t c0 = band * t.bw, wb = min(t.bw, t.nw - c0);  // the last band may be narrower
     if (wb == t.bw) {
@@ -165,6 +160,18 @@ __device__ __forceinline__ bool tile_item(const Tiling& t, uint32_t blk, uint32_
         tc = rem - tr * wb;
     }
     tc += c0;
+}
+
+// Flat position g = s * H * W + x * W + y of item i (< kItems) of (remapped)
+// block blk; false past the grid's right or bottom edge (g is then not
+// meaningful).
+template <uint32_t kItems>
+__device__ __forceinline__ bool tile_item(const Tiling& t, uint32_t blk, uint32_t i, uint32_t& g)
+{
+    static_assert((kItems & (kItems - 1)) == 0, "tiles of a power-of-two size");
+    uint32_t s, k, tr, tc;
+    divmod(blk, t.div_slice, s, k);
+    tile_coords(t, k, tr, tc);
     const uint32_t th = kItems >> t.lw;
     const uint32_t x = tr * th + (i >> t.lw), y = (tc << t.lw) + (i & ((1u << t.lw) - 1u));
     g = s * t.plane + x * t.W + y;
