@@ -15,6 +15,8 @@ import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "_lib", "libscram.so")
+#: the same kernels built with other tile shapes and dispatch orders (for the race checks)
+ORDER_LIB_PATH = os.path.join(_HERE, "_lib", "libscram_order.so")
 
 SCRAM_F32 = 0
 SCRAM_BF16 = 1
@@ -51,12 +53,18 @@ class ScramError(RuntimeError):
 def lib() -> ctypes.CDLL:
     """The loaded library (raises if it has not been built)."""
     global _lib
-    if _lib is not None:
-        return _lib
-    if not os.path.exists(LIB_PATH):
-        raise RuntimeError(f"SCRAM HIP library not found at {LIB_PATH}; build it with "
+    if _lib is None:
+        _lib = load(LIB_PATH)
+    return _lib
+
+
+def load(path: str) -> ctypes.CDLL:
+    """Load a build of the library at ``path`` and declare its entry points (raises if it is missing).
+    ``lib()`` is ``load(LIB_PATH)``, loaded once."""
+    if not os.path.exists(path):
+        raise RuntimeError(f"SCRAM HIP library not found at {path}; build it with "
                            "`python -m paper_1905_10308_amd.build` (or __graft_entry__.build())")
-    L = ctypes.CDLL(LIB_PATH)
+    L = ctypes.CDLL(path)
     P, I, U32, U64, SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_size_t
     L.scram_patchmatch_workspace_bytes.argtypes = [I, I, I]
     L.scram_patchmatch_workspace_bytes.restype = SZ
@@ -78,7 +86,6 @@ def lib() -> ctypes.CDLL:
     L.scram_status_string.restype = ctypes.c_char_p
     L.scram_abi_version.argtypes = []
     L.scram_abi_version.restype = I
-    _lib = L
     return L
 
 

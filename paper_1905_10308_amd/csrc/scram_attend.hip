@@ -622,7 +622,7 @@ hipError_t run_attend(const AttParams& p0, int window, hipStream_t st, hipEvent_
                                  : go(std::integral_constant<int, 7>{});
         }
     }
-    p.tq = make_tiling(p.Hq, p.Wq, Row<T, D, G>::kQpb);
+    p.tq = make_tiling(p.Hq, p.Wq, Row<T, D, G>::kQpb, kLaneSkew);
     const uint64_t blocks = tiling_blocks(p.tq, p.n / p.tq.plane);
     // the smallest register budget that holds this call's window centres
     if (p.kappa == 1) {
@@ -668,7 +668,7 @@ uint64_t attend_max_blocks(int dtype, const Grid& g)
     return dispatch_value(dtype, g.d, uint64_t(0), [&](auto t, auto d) {
         using T = decltype(t);
         constexpr int D = decltype(d)::value;
-        const uint64_t lanes = tiling_blocks(make_tiling(g.Hq, g.Wq, Row<T, D, Lanes<T, D>::kAttend>::kQpb), g.S);
+        const uint64_t lanes = tiling_blocks(make_tiling(g.Hq, g.Wq, Row<T, D, Lanes<T, D>::kAttend>::kQpb, kLaneSkew), g.S);
         const uint64_t tiles = kTileKernel<T, D> ? tiling_blocks(make_tiling(g.Hq, g.Wq, kBlock / 4), g.S) : 0;
         return lanes > tiles ? lanes : tiles;
     });

@@ -1378,8 +1378,8 @@ hipError_t run_backward(const BwdParams& p0, hipStream_t st, hipEvent_t* ev, Inv
     constexpr int G = Lanes<T, D>::kAttend;
     constexpr uint32_t kQpb = Row<T, D, G>::kQpb;
     BwdParams p = p0;
-    p.tq = make_tiling(p.Hq, p.Wq, kQpb);
-    p.tk = make_tiling(p.Hk, p.Wk, kQpb);
+    p.tq = make_tiling(p.Hq, p.Wq, kQpb, kLaneSkew);
+    p.tk = make_tiling(p.Hk, p.Wk, kQpb, kLaneSkew);
     const uint64_t qblocks = tiling_blocks(p.tq, p.n / p.tq.plane);
     const uint64_t gblocks = (static_cast<uint64_t>(p.kappa) * p.n + kQpb - 1) / kQpb;
     const uint64_t kblocks = tiling_blocks(p.tk, p.keys_total / p.nkeys);
@@ -1565,9 +1565,9 @@ uint64_t attend_backward_max_blocks(int dtype, const Grid& g, int kappa)
         const uint64_t n = uint64_t(g.S) * g.Hq * g.Wq, keys = uint64_t(g.S) * g.Hk * g.Wk;
         uint64_t most = 4096;  // the grid-stride kernels of the inverse map
         auto keep = [&](uint64_t b) { most = b > most ? b : most; };
-        keep(tiling_blocks(make_tiling(g.Hq, g.Wq, kQpb), g.S));    // query kernel
+        keep(tiling_blocks(make_tiling(g.Hq, g.Wq, kQpb, kLaneSkew), g.S));    // query kernel
         keep((uint64_t(kappa) * n + kQpb - 1) / kQpb);              // entry-order copies
-        keep(tiling_blocks(make_tiling(g.Hk, g.Wk, kQpb), g.S));    // key kernel
+        keep(tiling_blocks(make_tiling(g.Hk, g.Wk, kQpb, kLaneSkew), g.S));    // key kernel
         keep(tiling_blocks(make_tiling(g.Hk, g.Wk, kTileKeys), g.S));  // key tiles on the matrix cores
         keep((keys + kScanTile - 1) / kScanTile);                   // scan tiles
         return most;

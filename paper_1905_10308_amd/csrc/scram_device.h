@@ -83,9 +83,14 @@ __device__ __forceinline__ int32_t clamp_index(int32_t j, uint32_t nkeys)
 
 // Block b of nb runs on XCD b % 8.  Give XCD x the contiguous logical range
 // [start(x), start(x) + count(x)) so that neighbouring queries -- which read
-// neighbouring keys -- share one L2.  A bijection for every nb.
+// neighbouring keys -- share one L2.  A bijection for every nb.  Built with
+// SCRAM_XCD_REMAP=0, blocks take their tiles in dispatch order instead.
+#ifndef SCRAM_XCD_REMAP
+#define SCRAM_XCD_REMAP 1
+#endif
 __device__ __forceinline__ uint32_t xcd_remap(uint32_t b, uint32_t nb)
 {
+    if (!SCRAM_XCD_REMAP) return b;
     const uint32_t x = b % kXcds, local = b / kXcds;
     const uint32_t q = nb / kXcds, r = nb % kXcds;
     const uint32_t start = x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q;
@@ -104,11 +109,26 @@ __device__ __forceinline__ uint32_t xcd_remap(uint32_t b, uint32_t nb)
 // its lane groups read in L1 than a row segment of the same size.  Grids
 // narrower than the squarish tile get a flatter one, so that 1-D grids keep
 // every lane group busy.
+//
+// The kernels that give an item the same result whatever else its tile holds
+// (a lane group per query or key) take their tiles through make_tiling's
+// skew, kLaneSkew: the tile's width is doubled (halved for a negative skew)
+// that many times over the squarish one.  Every one of these is a build
+// setting (0, 16 and 64 here); a build with other values -- other tile
+// shapes and dispatch orders, same results -- is what the race checks of the
+// sweep compare this one against.
 #ifndef SCRAM_BAND_TILES
 #define SCRAM_BAND_TILES 16
 #endif
+#ifndef SCRAM_BAND_MAX
+#define SCRAM_BAND_MAX 64
+#endif
+#ifndef SCRAM_LANE_TILE_SKEW
+#define SCRAM_LANE_TILE_SKEW 0
+#endif
 constexpr uint32_t kBandTiles = SCRAM_BAND_TILES;
-constexpr uint32_t kBandMax = 64;
+constexpr uint32_t kBandMax = SCRAM_BAND_MAX;
+constexpr int kLaneSkew = SCRAM_LANE_TILE_SKEW;
 
 struct Tiling {
     uint32_t H, W, plane;  // one slice's grid
@@ -119,7 +139,7 @@ struct Tiling {
 };
 
 // Host: the tiling of one slice's H x W grid by blocks of `items` positions.
-inline Tiling make_tiling(int H, int W, uint32_t items)
+inline Tiling make_tiling(int H, int W, uint32_t items, int skew = 0)
 {
     auto pow2_at_least = [](uint32_t v) {
         uint32_t p = 1;
@@ -128,6 +148,8 @@ inline Tiling make_tiling(int H, int W, uint32_t items)
     };
     uint32_t lw = 0;
     while ((1u << (2 * (lw + 1))) <= items) ++lw;  // squarish: width = sqrt(items) rounded down to a power of two
+    for (; skew > 0 && (2u << lw) <= items; --skew) ++lw;
+    for (; skew < 0 && lw > 0; ++skew) --lw;
     uint32_t tw = 1u << lw, th = items / tw;
     if (th > pow2_at_least(static_cast<uint32_t>(H))) {  // short grid: wider tiles
         th = pow2_at_least(static_cast<uint32_t>(H));

@@ -456,7 +456,7 @@ hipError_t run_iter(const PmParams& p0, uint32_t flags, hipStream_t st, hipEvent
 {
     constexpr int G = Lanes<T, D>::kPm;
     PmParams p = p0;
-    p.tq = make_tiling(p.Hq, p.Wq, Row<T, D, G>::kQpb * SCRAM_PM_QPG);
+    p.tq = make_tiling(p.Hq, p.Wq, Row<T, D, G>::kQpb * SCRAM_PM_QPG, kLaneSkew);
     const uint64_t blocks = tiling_blocks(p.tq, p.n / p.plane_q);
     // the smallest register budget that holds this run's previous matches
     if (p.n_prev == 0) {
@@ -517,7 +517,7 @@ uint64_t patchmatch_max_blocks(int dtype, const Grid& g)
         constexpr int D = decltype(d)::value;
         constexpr uint32_t kQpb = Row<T, D, Lanes<T, D>::kPm>::kQpb;
         const uint64_t init = (uint64_t(g.S) * g.Hq * g.Wq + kQpb - 1) / kQpb;
-        const uint64_t iter = tiling_blocks(make_tiling(g.Hq, g.Wq, kQpb * SCRAM_PM_QPG), g.S);
+        const uint64_t iter = tiling_blocks(make_tiling(g.Hq, g.Wq, kQpb * SCRAM_PM_QPG, kLaneSkew), g.S);
         return init > iter ? init : iter;
     });
 }

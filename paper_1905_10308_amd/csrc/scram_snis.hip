@@ -301,7 +301,7 @@ hipError_t run_snis(const SnisParams& p0, hipStream_t st, hipEvent_t e0, hipEven
 {
     constexpr int G = Lanes<T, D>::kAttend;
     SnisParams p = p0;
-    p.tq = make_tiling(p.Hq, p.Wq, Row<T, D, G>::kQpb);
+    p.tq = make_tiling(p.Hq, p.Wq, Row<T, D, G>::kQpb, kLaneSkew);
     const uint64_t blocks = tiling_blocks(p.tq, p.n / p.tq.plane);
     // the smallest register budget that holds the query's modes
     auto go = [&](auto mk) {
@@ -363,7 +363,7 @@ uint64_t snis_max_blocks(int dtype, const Grid& g)
     return dispatch_value(dtype, g.d, uint64_t(0), [&](auto t, auto d) {
         using T = decltype(t);
         constexpr int D = decltype(d)::value;
-        return tiling_blocks(make_tiling(g.Hq, g.Wq, Row<T, D, Lanes<T, D>::kAttend>::kQpb), g.S);
+        return tiling_blocks(make_tiling(g.Hq, g.Wq, Row<T, D, Lanes<T, D>::kAttend>::kQpb, kLaneSkew), g.S);
     });
 }
 

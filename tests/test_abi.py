@@ -55,6 +55,27 @@ def test_abi_version(L):
     assert L.scram_abi_version() == (2 << 16) | 6
 
 
+def test_launch_order_variant_library():
+    """The build with other tile shapes and dispatch orders (the race checks' second library) exports the
+    same entry points, and binds its own calls to its own definitions (-Bsymbolic), so that loaded beside
+    the product it runs its own kernels."""
+    import subprocess
+
+    from paper_1905_10308_amd import binding
+
+    if not os.path.exists(binding.ORDER_LIB_PATH):
+        from paper_1905_10308_amd import build
+
+        build.build()
+    V = binding.load(binding.ORDER_LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(V, name), f"{name} declared in scram.h but not exported by the variant"
+    assert V.scram_abi_version() == (2 << 16) | 6
+    for path in (binding.LIB_PATH, binding.ORDER_LIB_PATH):
+        dyn = subprocess.run(["readelf", "-d", path], capture_output=True, text=True, check=True).stdout
+        assert "SYMBOLIC" in dyn, path
+
+
 def test_status_strings(L):
     seen = set()
     for code in (OK, ENULL, ESHAPE, EUNSUP, EALIGN, EALIAS, EHIP, EWS, ESCRATCH):
