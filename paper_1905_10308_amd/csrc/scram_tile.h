@@ -145,6 +145,45 @@ __device__ __forceinline__ TileClusters tile_clusters(bool valid, int u, int v, 
     return tc;
 }
 
+// Clusters of the 32 centres of a wave's two windows per query: lane i < 32 holds centre i (window
+// i / 16 of query i mod 16), lanes 32 .. 63 repeat lanes 0 .. 31; mine is the cluster of the lane's
+// centre.  Only the clusters' scalars are set (the caller places each window in its own box).
+template <int B>
+__device__ __forceinline__ TileClusters tile_clusters_pair(bool valid, int u, int v, int lane, int rc, int Hk,
+                                                           int Wk)
+{
+    TileClusters tc;
+    int t_r0 = 0, t_c0 = 0, t_bw = 1, t_h = 0;
+    int nclu = 0, mine = -1;
+    const int it = lane & 31;
+    uint32_t todo = static_cast<uint32_t>(__ballot(valid));  // bit i: centre i (a query's two centres share its validity)
+    while (todo) {
+        const int a = __builtin_ctz(todo);
+        const int ua = __builtin_amdgcn_readlane(u, a), va = __builtin_amdgcn_readlane(v, a);
+        const bool mem = ((todo >> it) & 1u) && abs(u - ua) <= rc && abs(v - va) <= rc;
+        todo &= ~static_cast<uint32_t>(__ballot(mem));
+        mine = mem ? nclu : mine;
+        int ulo = mem ? u : ua, uhi = ulo, vlo = mem ? v : va, vhi = vlo;
+        row_minmax(ulo, uhi);
+        row_minmax(vlo, vhi);
+        // and across the two 16-lane rows that hold the 32 centres
+        ulo = min(ulo, __shfl_xor(ulo, 16)), uhi = max(uhi, __shfl_xor(uhi, 16));
+        vlo = min(vlo, __shfl_xor(vlo, 16)), vhi = max(vhi, __shfl_xor(vhi, 16));
+        const bool here = lane == nclu;
+        t_r0 = here ? max(ulo - B, 0) : t_r0;
+        t_c0 = here ? max(vlo - B, 0) : t_c0;
+        t_h = here ? min(uhi + B, Hk - 1) - max(ulo - B, 0) + 1 : t_h;
+        t_bw = here ? min(vhi + B, Wk - 1) - max(vlo - B, 0) + 1 : t_bw;
+        ++nclu;
+    }
+    tc.t_r0 = t_r0, tc.t_c0 = t_c0, tc.t_bw = t_bw, tc.t_h = t_h, tc.nclu = nclu, tc.mine = mine;
+    tc.t_inv = __builtin_amdgcn_rcpf(static_cast<float>(t_bw));
+    tc.t_nb = (t_h * t_bw + 15) >> 4;
+    box_slot(16, t_bw, tc.t_inv, tc.t_q16, tc.t_r16);
+    tc.wr0 = 0, tc.wrn = -1, tc.wcols = 0, tc.rcut = INT_MIN, tc.wcut = 0;
+    return tc;
+}
+
 // A cluster's scalars, read from the lanes that hold them.
 struct TileBox {
     int r0, c0, bw, nb, q16, r16;
