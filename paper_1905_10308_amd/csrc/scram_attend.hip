@@ -256,7 +256,10 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
 // one pass per window e, each with the clusters and boxes of the wave's 16
 // window-e centres, into the same online softmax state; a slot of pass e is
 // left out when one of the query's windows 0 .. e-1 holds its key, so every
-// key of the union enters once.
+// key of the union enters once.  Two maps without the causal mask take a
+// single pass over the clusters of all 32 centres instead: each window is
+// kept in the box of its own centre's cluster, window 1 less the keys of
+// window 0.
 // (at most 96 VGPRs: five waves per SIMD hide more of the row loads than four; the causal mask's
 // registers and those of up to 4 windows do not fit there without spills, so they take four, and
 // up to 8 windows three)
