@@ -1089,7 +1089,25 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
         qx = static_cast<int>(xx);
         qy = static_cast<int>(yy);
     }
-    TileClusters tc = tile_clusters<B, CAUSAL>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk, qx, qy);
+    // two windows without the causal mask: one pass over the clusters of all 32 centres, as in the
+    // attend's matrix-core kernel
+    constexpr bool JOINT = MK == 2 && !CAUSAL;
+    int u1 = 0, v1 = 0, mine1 = -1, wrn1 = -1;
+    TileClusters tc;
+    if constexpr (JOINT) {
+        uint32_t uu, vv;
+        divmod(static_cast<uint32_t>(clamp_index(p.J[static_cast<size_t>(p.n) + gq], p.nkeys)), p.div_wk, uu, vv);
+        u1 = static_cast<int>(uu);
+        v1 = static_cast<int>(vv);
+        const bool w1 = (g4 & 1) != 0;  // lanes 16 .. 31 and 48 .. 63 cluster window 1's centres
+        tc = tile_clusters_pair<B>(valid, w1 ? u1 : u, w1 ? v1 : v, lane, p.rc, p.Hk, p.Wk);
+        mine1 = __shfl(tc.mine, m + 16);
+        tc.mine = __shfl(tc.mine, m);
+        tc.wrn = min(u + B, p.Hk - 1) - (u - B);
+        wrn1 = min(u1 + B, p.Hk - 1) - (u1 - B);
+    } else {
+        tc = tile_clusters<B, CAUSAL>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk, qx, qy);
+    }
     if (tc.nclu == 0) return;  // no query of this wave lies inside the grid
     // several windows: windows 0 .. e-1 of query m as in the attend's matrix-core kernel
     constexpr int kOther = MK > 1 ? MK - 1 : 1;
@@ -1097,6 +1115,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
     uint32_t xw[kOther];
 #pragma unroll
     for (int f = 0; f < kOther; ++f) cu[f] = cv[f] = 0, dw[f] = 1 << 20, xw[f] = 0u;
+    if constexpr (JOINT) dw[0] = u - u1;  // window 0's first row, as a row of window 1
+    const int du = u1 - u;                // JOINT: window 0's row of a slot is window 1's row + du
 
     const f32x4_t zero = f32x4_t{0.f, 0.f, 0.f, 0.f};
     f32x4_t acc_a[kOt], acc_b[kOt];
@@ -1198,8 +1218,16 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
             sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ds], sc, 0, 0, 0);
             dp = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, gf[ds], dp, 0, 0, 0);
         }
-        uint32_t bits = tile_window_bits<CAUSAL>(bx, rr, mcl, tc.wrn, wc, wc2, tc.rcut, wk, wk2);
-        if constexpr (MK > 1) bits &= ~tile_other_bits<kOther, B>(bx, rr, mcl, dw, xw);
+        uint32_t bits;
+        if constexpr (JOINT) {
+            // window 0 (wc, wc2), and window 1 (wk, wk2; rows from rr) less the keys of window 0
+            bits = tile_window_bits<false>(bx, rr + du, mcl, tc.wrn, wc, wc2) |
+                   (tile_window_bits<false>(bx, rr, mcl, wrn1, wk, wk2) &
+                    ~tile_other_bits<kOther, B>(bx, rr, mcl, dw, xw));
+        } else {
+            bits = tile_window_bits<CAUSAL>(bx, rr, mcl, tc.wrn, wc, wc2, tc.rcut, wk, wk2);
+            if constexpr (MK > 1) bits &= ~tile_other_bits<kOther, B>(bx, rr, mcl, dw, xw);
+        }
         uint32_t keep[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -1272,16 +1300,29 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
             box_slot(4 * g4, bx.bw, bx.inv, mr, mcl);
             int rr = mr - tc.wr0;
             const bool here = c == tc.mine;
-            const uint32_t wc = here ? tc.wcols : 0u;
-            const uint32_t wc2 = here ? tc.wcols << bx.bw : 0u;  // bw <= 27, and only bits below bw + 3 are read
-            const uint32_t wk = CAUSAL && here ? tc.wcut : 0u;  // the query's own row (causal)
-            const uint32_t wk2 = CAUSAL && here ? tc.wcut << bx.bw : 0u;
-            if constexpr (MK > 1) {
+            uint32_t wcl = tc.wcols;
+            if constexpr (JOINT) {
+                rr = mr + bx.r0 - (u1 - B);  // window 1's row
+                wcl = tile_col_bits(v - B - bx.c0, v + B - bx.c0, bx.bw);  // window 0's columns in this box
+            }
+            const uint32_t wc = here ? wcl : 0u;
+            const uint32_t wc2 = here ? wcl << bx.bw : 0u;  // bw <= 27, and only bits below bw + 3 are read
+            uint32_t wk = CAUSAL && here ? tc.wcut : 0u;  // the query's own row (causal)
+            uint32_t wk2 = CAUSAL && here ? tc.wcut << bx.bw : 0u;
+            bool in = here;
+            if constexpr (JOINT) {
+                // window 1 when this is its cluster; window 0's columns then mask its keys
+                const bool here1 = c == mine1;
+                wk = here1 ? tile_col_bits(v1 - B - bx.c0, v1 + B - bx.c0, bx.bw) : 0u;
+                wk2 = wk << bx.bw;
+                xw[0] = here1 ? wcl : 0u;
+                in = here || here1;
+            } else if constexpr (MK > 1) {
 #pragma unroll
                 for (int f = 0; f < kOther; ++f)
                     xw[f] = here && f < e ? tile_col_bits(cv[f] - B - bx.c0, cv[f] + B - bx.c0, bx.bw) : 0u;
             }
-            thr = here ? thr_q : INFINITY;  // a query's cluster is visited once per window, its blocks in a row
+            thr = in ? thr_q : INFINITY;  // a query's cluster is visited once per window, its blocks in a row
             step_slot(bx, lc, lkey);
             for (int k = 1; k < bx.nb; ++k) {
                 stage();
@@ -1310,7 +1351,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
             ++c;
             wave_lds_sync();
         }
-        if constexpr (MK == 1) {
+        if constexpr (MK == 1 || JOINT) {
             break;
         } else {
             if (e + 1 >= p.kappa) break;
