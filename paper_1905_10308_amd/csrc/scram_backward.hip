@@ -1089,22 +1089,29 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
         qx = static_cast<int>(xx);
         qy = static_cast<int>(yy);
     }
-    // two windows without the causal mask: one pass over the clusters of all 32 centres, as in the
-    // attend's matrix-core kernel
-    constexpr bool JOINT = MK == 2 && !CAUSAL;
-    int u1 = 0, v1 = 0, mine1 = -1, wrn1 = -1;
+    // up to four windows without the causal mask: one pass over the clusters of all their centres, as
+    // in the attend's matrix-core kernel
+    constexpr bool JOINT = (MK == 2 || MK == 4) && !CAUSAL;
+    constexpr int NJ = JOINT ? MK : 1;
+    int ju[NJ], jv[NJ], jmine[NJ];  // window e's centre and the cluster that holds it (-1: no window e)
     TileClusters tc;
     if constexpr (JOINT) {
-        uint32_t uu, vv;
-        divmod(static_cast<uint32_t>(clamp_index(p.J[static_cast<size_t>(p.n) + gq], p.nkeys)), p.div_wk, uu, vv);
-        u1 = static_cast<int>(uu);
-        v1 = static_cast<int>(vv);
-        const bool w1 = (g4 & 1) != 0;  // lanes 16 .. 31 and 48 .. 63 cluster window 1's centres
-        tc = tile_clusters_pair<B>(valid, w1 ? u1 : u, w1 ? v1 : v, lane, p.rc, p.Hk, p.Wk);
-        mine1 = __shfl(tc.mine, m + 16);
-        tc.mine = __shfl(tc.mine, m);
-        tc.wrn = min(u + B, p.Hk - 1) - (u - B);
-        wrn1 = min(u1 + B, p.Hk - 1) - (u1 - B);
+        const int ew = g4 & (NJ - 1);  // the window whose centre this lane clusters
+        int iu = u, iv = v;
+#pragma unroll
+        for (int e = 0; e < NJ; ++e) {
+            ju[e] = u, jv[e] = v;  // window 0; a window past kappa repeats it and is not clustered
+            if (e > 0 && e < p.kappa) {
+                uint32_t uu, vv;
+                divmod(static_cast<uint32_t>(clamp_index(p.J[static_cast<size_t>(e) * p.n + gq], p.nkeys)),
+                       p.div_wk, uu, vv);
+                ju[e] = static_cast<int>(uu), jv[e] = static_cast<int>(vv);
+            }
+            iu = ew == e ? ju[e] : iu, iv = ew == e ? jv[e] : iv;
+        }
+        tc = tile_clusters_joint<B, NJ>(valid && ew < p.kappa, iu, iv, lane, p.rc, p.Hk, p.Wk);
+#pragma unroll
+        for (int e = 0; e < NJ; ++e) jmine[e] = __shfl(tc.mine, m + 16 * e);
     } else {
         tc = tile_clusters<B, CAUSAL>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk, qx, qy);
     }
@@ -1115,8 +1122,12 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
     uint32_t xw[kOther];
 #pragma unroll
     for (int f = 0; f < kOther; ++f) cu[f] = cv[f] = 0, dw[f] = 1 << 20, xw[f] = 0u;
-    if constexpr (JOINT) dw[0] = u - u1;  // window 0's first row, as a row of window 1
-    const int du = u1 - u;                // JOINT: window 0's row of a slot is window 1's row + du
+    // joint pass, per cluster: window e's first row as a box row (jd), its rows less one, cut at the
+    // box's last (jn), its columns in the box (jx); bit e of hm: the cluster holds window e's centre
+    int jd[NJ], jn[NJ];
+    uint32_t jx[NJ], hm = 0u;
+#pragma unroll
+    for (int e = 0; e < NJ; ++e) jd[e] = jn[e] = 0, jx[e] = 0u;
 
     const f32x4_t zero = f32x4_t{0.f, 0.f, 0.f, 0.f};
     f32x4_t acc_a[kOt], acc_b[kOt];
@@ -1220,10 +1231,16 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
         }
         uint32_t bits;
         if constexpr (JOINT) {
-            // window 0 (wc, wc2), and window 1 (wk, wk2; rows from rr) less the keys of window 0
-            bits = tile_window_bits<false>(bx, rr + du, mcl, tc.wrn, wc, wc2) |
-                   (tile_window_bits<false>(bx, rr, mcl, wrn1, wk, wk2) &
-                    ~tile_other_bits<kOther, B>(bx, rr, mcl, dw, xw));
+            // rr is the slot's box row: window e's slots when this cluster holds its centre, less those of
+            // the query's earlier windows
+            bits = 0u;
+            uint32_t held = 0u;
+#pragma unroll
+            for (int e = 0; e < NJ; ++e) {
+                const uint32_t w = tile_window_bits<false>(bx, rr - jd[e], mcl, jn[e], jx[e], jx[e] << bx.bw);
+                bits |= ((hm >> e) & 1u) ? w & ~held : 0u;
+                held |= w;
+            }
         } else {
             bits = tile_window_bits<CAUSAL>(bx, rr, mcl, tc.wrn, wc, wc2, tc.rcut, wk, wk2);
             if constexpr (MK > 1) bits &= ~tile_other_bits<kOther, B>(bx, rr, mcl, dw, xw);
@@ -1300,23 +1317,23 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
             box_slot(4 * g4, bx.bw, bx.inv, mr, mcl);
             int rr = mr - tc.wr0;
             const bool here = c == tc.mine;
-            uint32_t wcl = tc.wcols;
-            if constexpr (JOINT) {
-                rr = mr + bx.r0 - (u1 - B);  // window 1's row
-                wcl = tile_col_bits(v - B - bx.c0, v + B - bx.c0, bx.bw);  // window 0's columns in this box
-            }
-            const uint32_t wc = here ? wcl : 0u;
-            const uint32_t wc2 = here ? wcl << bx.bw : 0u;  // bw <= 27, and only bits below bw + 3 are read
-            uint32_t wk = CAUSAL && here ? tc.wcut : 0u;  // the query's own row (causal)
-            uint32_t wk2 = CAUSAL && here ? tc.wcut << bx.bw : 0u;
+            const uint32_t wc = here ? tc.wcols : 0u;
+            const uint32_t wc2 = here ? tc.wcols << bx.bw : 0u;  // bw <= 27, and only bits below bw + 3 are read
+            const uint32_t wk = CAUSAL && here ? tc.wcut : 0u;  // the query's own row (causal)
+            const uint32_t wk2 = CAUSAL && here ? tc.wcut << bx.bw : 0u;
             bool in = here;
             if constexpr (JOINT) {
-                // window 1 when this is its cluster; window 0's columns then mask its keys
-                const bool here1 = c == mine1;
-                wk = here1 ? tile_col_bits(v1 - B - bx.c0, v1 + B - bx.c0, bx.bw) : 0u;
-                wk2 = wk << bx.bw;
-                xw[0] = here1 ? wcl : 0u;
-                in = here || here1;
+                rr = mr;
+                hm = 0u;
+#pragma unroll
+                for (int e = 0; e < NJ; ++e) {
+                    jd[e] = ju[e] - B - bx.r0;
+                    jn[e] = min(2 * B, bx.h - 1 - jd[e]);
+                    // no columns for a window wholly below the box (its row count would be negative)
+                    jx[e] = jn[e] >= 0 ? tile_col_bits(jv[e] - B - bx.c0, jv[e] + B - bx.c0, bx.bw) : 0u;
+                    hm |= c == jmine[e] ? 1u << e : 0u;
+                }
+                in = hm != 0u;
             } else if constexpr (MK > 1) {
 #pragma unroll
                 for (int f = 0; f < kOther; ++f)

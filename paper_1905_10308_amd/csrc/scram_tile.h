@@ -145,30 +145,37 @@ __device__ __forceinline__ TileClusters tile_clusters(bool valid, int u, int v, 
     return tc;
 }
 
-// Clusters of the 32 centres of a wave's two windows per query: lane i < 32 holds centre i (window
-// i / 16 of query i mod 16), lanes 32 .. 63 repeat lanes 0 .. 31; mine is the cluster of the lane's
-// centre.  Only the clusters' scalars are set (the caller places each window in its own box).
-template <int B>
-__device__ __forceinline__ TileClusters tile_clusters_pair(bool valid, int u, int v, int lane, int rc, int Hk,
-                                                           int Wk)
+// Clusters of the centres of a wave's NJ (2 or 4) windows per query: lane i < 16 NJ holds centre i
+// (window i / 16 of query i mod 16), the other lanes repeat them; valid is false for a centre that
+// does not exist; mine is the cluster of the lane's centre.  Only the clusters' scalars are set (the
+// caller places each window in its own box).
+template <int B, int NJ>
+__device__ __forceinline__ TileClusters tile_clusters_joint(bool valid, int u, int v, int lane, int rc, int Hk,
+                                                            int Wk)
 {
+    static_assert(NJ == 2 || NJ == 4, "16 NJ centres in the lanes of a wave");
+    constexpr uint64_t kItems = NJ == 4 ? ~0ull : 0xFFFFFFFFull;
     TileClusters tc;
     int t_r0 = 0, t_c0 = 0, t_bw = 1, t_h = 0;
     int nclu = 0, mine = -1;
-    const int it = lane & 31;
-    uint32_t todo = static_cast<uint32_t>(__ballot(valid));  // bit i: centre i (a query's two centres share its validity)
+    const int it = lane & (16 * NJ - 1);
+    uint64_t todo = static_cast<uint64_t>(__ballot(valid)) & kItems;  // bit i: centre i
     while (todo) {
-        const int a = __builtin_ctz(todo);
+        const int a = __builtin_ctzll(todo);
         const int ua = __builtin_amdgcn_readlane(u, a), va = __builtin_amdgcn_readlane(v, a);
         const bool mem = ((todo >> it) & 1u) && abs(u - ua) <= rc && abs(v - va) <= rc;
-        todo &= ~static_cast<uint32_t>(__ballot(mem));
+        todo &= ~(static_cast<uint64_t>(__ballot(mem)) & kItems);
         mine = mem ? nclu : mine;
         int ulo = mem ? u : ua, uhi = ulo, vlo = mem ? v : va, vhi = vlo;
         row_minmax(ulo, uhi);
         row_minmax(vlo, vhi);
-        // and across the two 16-lane rows that hold the 32 centres
+        // and across the 16-lane rows that hold the centres
         ulo = min(ulo, __shfl_xor(ulo, 16)), uhi = max(uhi, __shfl_xor(uhi, 16));
         vlo = min(vlo, __shfl_xor(vlo, 16)), vhi = max(vhi, __shfl_xor(vhi, 16));
+        if constexpr (NJ == 4) {
+            ulo = min(ulo, __shfl_xor(ulo, 32)), uhi = max(uhi, __shfl_xor(uhi, 32));
+            vlo = min(vlo, __shfl_xor(vlo, 32)), vhi = max(vhi, __shfl_xor(vhi, 32));
+        }
         const bool here = lane == nclu;
         t_r0 = here ? max(ulo - B, 0) : t_r0;
         t_c0 = here ? max(vlo - B, 0) : t_c0;
@@ -186,7 +193,7 @@ __device__ __forceinline__ TileClusters tile_clusters_pair(bool valid, int u, in
 
 // A cluster's scalars, read from the lanes that hold them.
 struct TileBox {
-    int r0, c0, bw, nb, q16, r16;
+    int r0, c0, bw, h, nb, q16, r16;
     float inv;
     uint32_t kstep, kstep_wrap;  // key index change of a 16-slot step, without and with a column carry
     uint32_t klast;              // key index of the box's last slot
@@ -204,8 +211,8 @@ __device__ __forceinline__ TileBox tile_box(const TileClusters& tc, int cl, int 
     bx.inv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(tc.t_inv), cl));
     bx.kstep = static_cast<uint32_t>(bx.q16) * static_cast<uint32_t>(Wk) + bx.r16;
     bx.kstep_wrap = bx.kstep + Wk - bx.bw;
-    const int h = __builtin_amdgcn_readlane(tc.t_h, cl);
-    bx.klast = static_cast<uint32_t>(bx.r0 + h - 1) * static_cast<uint32_t>(Wk) + (bx.c0 + bx.bw - 1);
+    bx.h = __builtin_amdgcn_readlane(tc.t_h, cl);
+    bx.klast = static_cast<uint32_t>(bx.r0 + bx.h - 1) * static_cast<uint32_t>(Wk) + (bx.c0 + bx.bw - 1);
     return bx;
 }
 
