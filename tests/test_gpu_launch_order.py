@@ -137,15 +137,16 @@ def test_resumed_and_noalloc_sweeps(scram, variant, case):
 
 def test_attend_outputs(scram, variant, case):
     """The attend on one map (windows 1-9; bf16 with 32 or 64 channels takes the matrix-core kernel for
-    3, 5, 7), causal, and over the union of two maps' windows."""
+    3, 5, 7), causal, and over the union of two and of three maps' windows."""
     Q, K, V = case["Q"], case["K"], case["V"]
     log(case["name"], "attend", tuple(Q.shape), Q.dtype)
-    J = scram.patchmatch_kappa(Q, K, 2, case["iters"], case["seed"])
+    J = scram.patchmatch_kappa(Q, K, 3, case["iters"], case["seed"])
     for window in sorted({1, 3, 5, 7, 9, case["window"]}):
         ref, runs = both(variant, lambda: scram.sparse_attend(Q, K, V, J[0], window))
         same(ref, runs, f"attend {window}")
-    ref, runs = both(variant, lambda: scram.sparse_attend(Q, K, V, J, case["window"]))
-    same(ref, runs, "union attend")
+    for kappa in (2, 3):
+        ref, runs = both(variant, lambda: scram.sparse_attend(Q, K, V, J[:kappa], case["window"]))
+        same(ref, runs, f"union attend {kappa}")
     if case["self_grid"]:
         Jc = scram.patchmatch(Q, K, case["iters"], case["seed"], causal=True)
         ref, runs = both(variant, lambda: scram.sparse_attend(Q, K, V, Jc, case["window"], causal=True))
@@ -169,7 +170,8 @@ def test_backward(scram, variant, case):
     J = scram.patchmatch_kappa(Q, K, 2, case["iters"], case["seed"])
     g = torch.Generator(device="cpu").manual_seed(3)
     dO = torch.randn(tuple(Q.shape[:3]) + (V.shape[3],), generator=g).to(device=Q.device, dtype=Q.dtype)
-    calls = [(J[0], case["window"], False), (J, case["window"], False)]
+    J3 = scram.patchmatch_kappa(Q, K, 3, case["iters"], case["seed"])
+    calls = [(J[0], case["window"], False), (J, case["window"], False), (J3, case["window"], False)]
     if case["self_grid"]:
         calls.append((scram.patchmatch(Q, K, case["iters"], case["seed"], causal=True), case["window"], True))
     for maps, window, causal in calls:
