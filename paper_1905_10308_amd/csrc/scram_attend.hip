@@ -256,10 +256,10 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
 // one pass per window e, each with the clusters and boxes of the wave's 16
 // window-e centres, into the same online softmax state; a slot of pass e is
 // left out when one of the query's windows 0 .. e-1 holds its key, so every
-// key of the union enters once.  Up to four maps without the causal mask
+// key of the union enters once.  Up to four maps (two with the causal mask)
 // take a single pass over the clusters of all their centres instead: each
 // window is kept in the box of its own centre's cluster, less the keys of
-// the query's earlier windows.
+// the query's earlier windows (and of those after the query).
 // (at most 96 VGPRs: five waves per SIMD hide more of the row loads than four; the causal mask's
 // registers and those of up to 4 windows do not fit there without spills, so they take four, and
 // up to 8 windows three)
@@ -317,12 +317,13 @@ attend_tile_kernel(AttParams p)
         qx = static_cast<int>(xx);
         qy = static_cast<int>(yy);
     }
-    // up to four windows without the causal mask: one pass over the clusters of all their centres
-    // instead of a pass per window (lanes 16 e .. 16 e + 15 cluster window e's centres).  A query keeps
-    // the slots of window e in the cluster of that window's centre, less the keys of its windows
-    // 0 .. e-1, so every key of the union enters once; coherent maps walk a third (two windows) to a
-    // half (three) fewer blocks
-    constexpr bool JOINT = (MK == 2 || MK == 4) && !CAUSAL;
+    // up to four windows (two with the causal mask): one pass over the clusters of all their centres
+    // instead of a pass per window
+    // (lanes 16 e .. 16 e + 15 cluster window e's centres).  A query keeps the slots of window e in the
+    // cluster of that window's centre, less the keys of its windows 0 .. e-1 (and with the causal mask
+    // those after the query), so every key of the union enters once; coherent maps walk a third (two
+    // windows) to a half (three) fewer blocks
+    constexpr bool JOINT = MK == 2 || (MK == 4 && !CAUSAL);  // four windows and the causal cut would spill
     constexpr int NJ = JOINT ? MK : 1;
     int ju[NJ], jv[NJ], jmine[NJ];  // window e's centre and the cluster that holds it (-1: no window e)
     TileClusters tc;
@@ -363,6 +364,8 @@ attend_tile_kernel(AttParams p)
     uint32_t jx[NJ], hm = 0u;
 #pragma unroll
     for (int e = 0; e < NJ; ++e) jd[e] = jn[e] = 0, jx[e] = 0u;
+    int jqr = 0;        // causal: the query's row as a box row
+    uint32_t jqc = 0u;  // and the box columns up to the query's
 
     const f32x4_t zero = f32x4_t{0.f, 0.f, 0.f, 0.f};
     f32x4_t acc[kOt];
@@ -476,6 +479,7 @@ attend_tile_kernel(AttParams p)
                 bits |= ((hm >> e) & 1u) ? w & ~held : 0u;
                 held |= w;
             }
+            if constexpr (CAUSAL) bits &= tile_causal_bits(bx, rr, mcl, jqr, jqc);
         } else {
             bits = tile_window_bits<CAUSAL>(bx, rr, mcl, wrn, wc, wc2, tc.rcut, wk, wk2);
             if constexpr (MK > 1) bits &= ~tile_other_bits<kOther, B>(bx, rr, mcl, dw, xw);
@@ -559,6 +563,11 @@ attend_tile_kernel(AttParams p)
                     hm |= c == jmine[e] ? 1u << e : 0u;
                 }
                 in = hm != 0u;
+                if constexpr (CAUSAL) {
+                    jqr = qx - bx.r0;
+                    const int qc = qy - bx.c0;
+                    jqc = qc < 0 ? 0u : (qc >= bx.bw - 1 ? (1u << bx.bw) - 1u : (2u << qc) - 1u);
+                }
             } else if constexpr (MK > 1) {
 #pragma unroll
                 for (int f = 0; f < kOther; ++f)

@@ -1089,9 +1089,9 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
         qx = static_cast<int>(xx);
         qy = static_cast<int>(yy);
     }
-    // up to four windows without the causal mask: one pass over the clusters of all their centres, as
-    // in the attend's matrix-core kernel
-    constexpr bool JOINT = (MK == 2 || MK == 4) && !CAUSAL;
+    // up to four windows (two with the causal mask): one pass over the clusters of all their centres,
+    // as in the attend's matrix-core kernel
+    constexpr bool JOINT = MK == 2 || (MK == 4 && !CAUSAL);  // four windows and the causal cut would spill
     constexpr int NJ = JOINT ? MK : 1;
     int ju[NJ], jv[NJ], jmine[NJ];  // window e's centre and the cluster that holds it (-1: no window e)
     TileClusters tc;
@@ -1128,6 +1128,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
     uint32_t jx[NJ], hm = 0u;
 #pragma unroll
     for (int e = 0; e < NJ; ++e) jd[e] = jn[e] = 0, jx[e] = 0u;
+    int jqr = 0;        // causal: the query's row as a box row
+    uint32_t jqc = 0u;  // and the box columns up to the query's
 
     const f32x4_t zero = f32x4_t{0.f, 0.f, 0.f, 0.f};
     f32x4_t acc_a[kOt], acc_b[kOt];
@@ -1241,6 +1243,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
                 bits |= ((hm >> e) & 1u) ? w & ~held : 0u;
                 held |= w;
             }
+            if constexpr (CAUSAL) bits &= tile_causal_bits(bx, rr, mcl, jqr, jqc);
         } else {
             bits = tile_window_bits<CAUSAL>(bx, rr, mcl, tc.wrn, wc, wc2, tc.rcut, wk, wk2);
             if constexpr (MK > 1) bits &= ~tile_other_bits<kOther, B>(bx, rr, mcl, dw, xw);
@@ -1334,6 +1337,11 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
                     hm |= c == jmine[e] ? 1u << e : 0u;
                 }
                 in = hm != 0u;
+                if constexpr (CAUSAL) {
+                    jqr = qx - bx.r0;
+                    const int qc = qy - bx.c0;
+                    jqc = qc < 0 ? 0u : (qc >= bx.bw - 1 ? (1u << bx.bw) - 1u : (2u << qc) - 1u);
+                }
             } else if constexpr (MK > 1) {
 #pragma unroll
                 for (int f = 0; f < kOther; ++f)

@@ -247,6 +247,29 @@ __device__ __forceinline__ uint32_t tile_window_bits(const TileBox& bx, int rr, 
     return bits;
 }
 
+// Which of the 4 slots of tile_window_bits lie at or before the query in raster order, for the slot
+// 16 k + 4 g4 at box row rr, column mcl: the box rows before qr, and in row qr the box columns in qc.
+__device__ __forceinline__ uint32_t tile_causal_bits(const TileBox& bx, int rr, int mcl, int qr, uint32_t qc)
+{
+    if (bx.bw >= 3) {  // the 4 slots span at most two box rows (bw <= 27: only bits below bw + 3 are read)
+        const uint32_t full = (1u << bx.bw) - 1u;
+        const uint32_t w0 = rr < qr ? full : (rr == qr ? qc : 0u);
+        const uint32_t w1 = rr + 1 < qr ? full : (rr + 1 == qr ? qc : 0u);
+        return __builtin_amdgcn_ubfe(w0 | (w1 << bx.bw), mcl, 4);
+    }
+    uint32_t bits = 0;
+    int r = rr, cc = mcl;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        bits |= r < qr || (r == qr && ((qc >> cc) & 1u)) ? 1u << i : 0u;
+        ++cc;
+        const bool wrap = cc == bx.bw;
+        cc = wrap ? 0 : cc;
+        r += wrap ? 1 : 0;
+    }
+    return bits;
+}
+
 // Box-column bits of the columns lo .. hi of a box `bw` wide (clipped to the box; zero when none is left).
 __device__ __forceinline__ uint32_t tile_col_bits(int lo, int hi, int bw)
 {

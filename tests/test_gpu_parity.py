@@ -511,9 +511,10 @@ def test_attend_tile_kernel_maps(scram, d, grid):
                                   (1, 19, 23, 40, 31)],
                          ids=lambda g: "x".join(map(str, g)))
 def test_attend_tile_kernel_union_maps(scram, d, grid):
-    """The matrix-core attend over the union of 2, 3 and 8 windows per query (a pass per window, the keys
-    of earlier windows left out): the stress maps combined into windows that repeat, overlap by one key,
-    lie apart or coincide for some queries only, with and without the causal mask."""
+    """The matrix-core attend over the union of 2, 3 and 8 windows per query (one pass over the joint
+    clusters of up to 4 windows' centres, 2 with the causal mask, else a pass per window; the keys of a
+    query's earlier windows left out): the stress maps combined into windows that repeat, overlap by one
+    key, lie apart or coincide for some queries only, with and without the causal mask."""
     S, Hq, Wq, Hk, Wk = grid
     rng = np.random.default_rng(Hq * 17 + Wq * 5 + d)
     Q = rng.standard_normal((S, Hq, Wq, d)).astype(np.float32)
