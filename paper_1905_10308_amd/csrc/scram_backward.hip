@@ -709,7 +709,7 @@ struct KeyStrip {
 enum StripMode { kStripPlain = 0, kStripCausal = 1, kStripMulti = 2 };
 
 // waves per SIMD the strip kernel's registers are sized for
-constexpr int strip_waves(int D, int mode) { return D > 64 ? 2 : D == 64 && mode == kStripMulti ? 3 : 4; }
+constexpr int strip_waves(int D) { return D > 64 ? 2 : 4; }
 
 // x = hi + mid + lo exactly, each part a bf16 value held as an fp32 bit
 // pattern with a zero low half: hi keeps the top 8 significant bits of x
@@ -731,7 +731,7 @@ __device__ __forceinline__ bf16x8_t lds_frag(const unsigned char* p)
 constexpr int kStripWaves = kTileKeys / 16;  // strips of a tile, one one-wave block each
 
 template <int D, int MODE>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(strip_waves(D, MODE)))) void
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(strip_waves(D)))) void
 bwd_key_strip_kernel(BwdParams p)
 {
     constexpr bool MULTI = MODE == kStripMulti;
@@ -744,8 +744,9 @@ bwd_key_strip_kernel(BwdParams p)
     // halves of the 32 banks, without it the two rows of each pair share banks
     __shared__ __align__(16) unsigned char s_row[kW][2 * kCE * KS::kRowB + 64];
     __shared__ int4 s_meta[kW][kCE];        // match row, match column, lse2 bits, D bits
-    __shared__ int32_t s_el[kW][kQueryIndex ? kCE : 1][2];           // window index e, query's raster index
-    __shared__ int32_t s_prevc[kW][MULTI ? kCE : 1][kMaxKappa - 1];  // centres of windows 0..e-1
+    // several windows: the strip's keys that one of the entry query's earlier windows holds (bit k: key
+    // k); causal: the query's raster index
+    __shared__ int32_t s_el[kW][kQueryIndex ? kCE : 1][2];
     __shared__ int32_t s_lo[kW][kStripMaxRows], s_pre[kW][kStripMaxRows + 1];
 
     const int lane = threadIdx.x & 63, wave = 0;
@@ -770,6 +771,18 @@ bwd_key_strip_kernel(BwdParams p)
     auto strip_key = [&](int i, int& x, int& y) {
         x = quad ? sr0 + (i >> 2) : x0 + ((it0 + i) >> p.tk.lw);
         y = quad ? sc0 + (i & 3) : y0 + ((it0 + i) & (tw - 1));
+    };
+    // the strip is a rectangle: key i at row sr0 + i / sC, column sc0 + i mod sC.  Bits of the keys in
+    // rows rlo .. rhi, columns clo .. chi (relative to the strip's first row and column)
+    const int sC = sc1 - sc0 + 1, sR = 16 / sC;
+    auto strip_bits = [&](int rlo, int rhi, int clo, int chi) {
+        rlo = max(rlo, 0), rhi = min(rhi, sR - 1), clo = max(clo, 0), chi = min(chi, sC - 1);
+        uint32_t bits = 0u;
+        if (clo <= chi) {
+            const uint32_t cb = ((2u << chi) - 1u) & ~((1u << clo) - 1u);
+            for (int r = rlo; r <= rhi; ++r) bits |= cb << (sC * r);
+        }
+        return bits;
     };
     if (sr0 >= p.Hk || sc0 >= p.Wk) return;  // the strip lies past the grid's edge
     const int hr0 = max(sr0 - p.b, 0), hr1 = min(sr1 + p.b, p.Hk - 1);
@@ -904,12 +917,26 @@ bwd_key_strip_kernel(BwdParams p)
                     if constexpr (kQueryIndex) {
                         uint32_t sl, local;
                         divmod(qg, p.div_plane, sl, local);
-                        s_el[wave][t][0] = static_cast<int32_t>(qe);
                         s_el[wave][t][1] = static_cast<int32_t>(local);
                     }
                     if constexpr (MULTI) {
-                        for (int f = 0; f < static_cast<int>(qe); ++f)
-                            s_prevc[wave][t][f] = clamp_index(p.J[static_cast<size_t>(f) * p.n + qg], p.nkeys);
+                        // the centres of the query's windows 0 .. e-1 (loaded together), then the strip's
+                        // keys their (2 b + 1)^2 neighbourhoods hold
+                        int32_t pc[kMaxKappa - 1];
+#pragma unroll
+                        for (int f = 0; f < kMaxKappa - 1; ++f)
+                            pc[f] = f < static_cast<int>(qe) ? p.J[static_cast<size_t>(f) * p.n + qg] : 0;
+                        uint32_t held = 0u;
+#pragma unroll
+                        for (int f = 0; f < kMaxKappa - 1; ++f) {
+                            if (f < static_cast<int>(qe)) {
+                                uint32_t fu, fv;
+                                divmod(static_cast<uint32_t>(clamp_index(pc[f], p.nkeys)), p.div_wk, fu, fv);
+                                const int ru = static_cast<int>(fu) - sr0, cv = static_cast<int>(fv) - sc0;
+                                held |= strip_bits(ru - p.b, ru + p.b, cv - p.b, cv + p.b);
+                            }
+                        }
+                        s_el[wave][t][0] = static_cast<int32_t>(held);
                     }
                 }
                 s_meta[wave][t] = meta;
@@ -946,13 +973,8 @@ bwd_key_strip_kernel(BwdParams p)
                 const int4 mt = s_meta[wave][te];
                 bool ok = key_ok && abs(mt.x - kx) <= p.b && abs(mt.y - ky) <= p.b;
                 if constexpr (MULTI) {
-                    const int e = s_el[wave][te][0];
-                    for (int f = 0; f < e && ok; ++f) {
-                        uint32_t fu, fv;
-                        divmod(static_cast<uint32_t>(s_prevc[wave][te][f]), p.div_wk, fu, fv);
-                        if (abs(static_cast<int>(fu) - kx) <= p.b && abs(static_cast<int>(fv) - ky) <= p.b)
-                            ok = false;  // an earlier window of the query holds this key
-                    }
+                    // not when an earlier window of the query holds this key (key m of the strip)
+                    ok = ok && !((static_cast<uint32_t>(s_el[wave][te][0]) >> m) & 1u);
                     if (p.causal) ok = ok && key_local <= static_cast<uint32_t>(s_el[wave][te][1]);
                 } else if constexpr (MODE == kStripCausal) {
                     ok = ok && key_local <= static_cast<uint32_t>(s_el[wave][te][1]);
