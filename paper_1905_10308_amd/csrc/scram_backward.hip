@@ -1022,9 +1022,10 @@ bwd_key_strip_kernel(BwdParams p)
 
 // ---------------------------------------------------------------------------
 // Query side on the matrix cores (bf16 storage, d 32 or 64, windows 3/5/7,
-// up to MK maps, with or without the causal mask; several maps take a pass
-// per window, with the keys of the query's earlier windows left out, as in the
-// attend's matrix-core kernel).  The wave's 16 queries, their clusters and key boxes are
+// up to MK maps, with or without the causal mask; several maps as in the
+// attend's matrix-core kernel: one pass over the joint clusters of up to four
+// windows' centres, two with the causal mask, else a pass per window, with the
+// keys of the query's earlier windows left out).  The wave's 16 queries, their clusters and key boxes are
 // those of the attend's matrix-core kernel (scram_tile.h); the key and value
 // rows of a box are read a block of 16 keys at a time, staged in LDS, and per
 // block (lane (m, g4): keys 4 g4 + i, query m)

@@ -172,8 +172,9 @@ def test_backward_many_keys(scram, grid, dtype):
 @pytest.mark.parametrize("grid", [(2, 37, 45, 37, 45), (1, 1, 50, 1, 50), (3, 5, 3, 5, 3), (1, 19, 23, 40, 31)],
                          ids=lambda g: "x".join(map(str, g)))
 def test_backward_tile_query_union_maps(scram, d, grid):
-    """The matrix-core query side over the union of 2, 3 and 4 windows per query (a pass per window, the
-    keys of earlier windows left out), with and without the causal mask, on combinations of the stress
+    """The matrix-core query side over the union of 2, 3 and 4 windows per query (one pass over the joint
+    clusters of their centres, a pass per window for 3-4 with the causal mask; the keys of earlier windows
+    left out), with and without the causal mask, on combinations of the stress
     maps: windows that repeat, overlap by one key or lie apart; and 8 windows, where the lane-group query
     side meets the key strips' several-window test at its largest bound."""
     S, Hq, Wq, Hk, Wk = grid
