@@ -256,15 +256,15 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
 // one pass per window e, each with the clusters and boxes of the wave's 16
 // window-e centres, into the same online softmax state; a slot of pass e is
 // left out when one of the query's windows 0 .. e-1 holds its key, so every
-// key of the union enters once.  Up to four maps (two with the causal mask)
-// take a single pass over the clusters of all their centres instead: each
+// key of the union enters once.  Up to four maps take a single pass over the
+// clusters of all their centres instead: each
 // window is kept in the box of its own centre's cluster, less the keys of
 // the query's earlier windows (and of those after the query).
 // (at most 96 VGPRs: five waves per SIMD hide more of the row loads than four; the causal mask's
 // registers and those of up to 4 windows do not fit there without spills, so they take four, and
-// up to 8 windows three)
+// up to 8 windows, or 4 with the causal mask, three)
 template <int D, int W, bool CAUSAL, int MK>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(MK > 4 ? 3 : CAUSAL || MK > 1 ? 4 : 5))) void
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(MK > 4 || (MK == 4 && CAUSAL) ? 3 : CAUSAL || MK > 1 ? 4 : 5))) void
 attend_tile_kernel(AttParams p)
 {
     constexpr int B = W / 2;
@@ -317,13 +317,12 @@ attend_tile_kernel(AttParams p)
         qx = static_cast<int>(xx);
         qy = static_cast<int>(yy);
     }
-    // up to four windows (two with the causal mask): one pass over the clusters of all their centres
-    // instead of a pass per window
+    // up to four windows: one pass over the clusters of all their centres instead of a pass per window
     // (lanes 16 e .. 16 e + 15 cluster window e's centres).  A query keeps the slots of window e in the
     // cluster of that window's centre, less the keys of its windows 0 .. e-1 (and with the causal mask
     // those after the query), so every key of the union enters once; coherent maps walk a third (two
     // windows) to a half (three) fewer blocks
-    constexpr bool JOINT = MK == 2 || (MK == 4 && !CAUSAL);  // four windows and the causal cut would spill
+    constexpr bool JOINT = MK == 2 || MK == 4;
     constexpr int NJ = JOINT ? MK : 1;
     int ju[NJ], jv[NJ], jmine[NJ];  // window e's centre and the cluster that holds it (-1: no window e)
     TileClusters tc;
