@@ -1024,8 +1024,8 @@ bwd_key_strip_kernel(BwdParams p)
 // Query side on the matrix cores (bf16 storage, d 32 or 64, windows 3/5/7,
 // up to MK maps, with or without the causal mask; several maps as in the
 // attend's matrix-core kernel: one pass over the joint clusters of up to four
-// windows' centres, two with the causal mask, else a pass per window, with the
-// keys of the query's earlier windows left out).  The wave's 16 queries, their clusters and key boxes are
+// windows' centres, else a pass per window, with the keys of the query's
+// earlier windows left out).  The wave's 16 queries, their clusters and key boxes are
 // those of the attend's matrix-core kernel (scram_tile.h); the key and value
 // rows of a box are read a block of 16 keys at a time, staged in LDS, and per
 // block (lane (m, g4): keys 4 g4 + i, query m)
@@ -1112,9 +1112,10 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
         qx = static_cast<int>(xx);
         qy = static_cast<int>(yy);
     }
-    // up to four windows (two with the causal mask): one pass over the clusters of all their centres,
-    // as in the attend's matrix-core kernel
-    constexpr bool JOINT = MK == 2 || (MK == 4 && !CAUSAL);  // four windows and the causal cut would spill
+    // up to four windows: one pass over the clusters of all their centres, as in the attend's
+    // matrix-core kernel (with four windows and the causal mask a few registers spill; the halved
+    // block count still pays)
+    constexpr bool JOINT = MK == 2 || MK == 4;
     constexpr int NJ = JOINT ? MK : 1;
     int ju[NJ], jv[NJ], jmine[NJ];  // window e's centre and the cluster that holds it (-1: no window e)
     TileClusters tc;

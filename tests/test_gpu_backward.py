@@ -173,8 +173,7 @@ def test_backward_many_keys(scram, grid, dtype):
                          ids=lambda g: "x".join(map(str, g)))
 def test_backward_tile_query_union_maps(scram, d, grid):
     """The matrix-core query side over the union of 2, 3 and 4 windows per query (one pass over the joint
-    clusters of their centres, a pass per window for 3-4 with the causal mask; the keys of earlier windows
-    left out), with and without the causal mask, on combinations of the stress
+    clusters of their centres; the keys of earlier windows left out), with and without the causal mask, on combinations of the stress
     maps: windows that repeat, overlap by one key or lie apart; and 8 windows, where the lane-group query
     side meets the key strips' several-window test at its largest bound."""
     S, Hq, Wq, Hk, Wk = grid
