@@ -511,7 +511,7 @@ def test_attend_tile_kernel_maps(scram, d, grid):
                                   (1, 19, 23, 40, 31)],
                          ids=lambda g: "x".join(map(str, g)))
 def test_attend_tile_kernel_union_maps(scram, d, grid):
-    """The matrix-core attend over the union of 2, 3 and 8 windows per query (one pass over the joint
+    """The matrix-core attend over the union of 2, 3, 4 and 8 windows per query (one pass over the joint
     clusters of up to 4 windows' centres, else a pass per window; the keys of a
     query's earlier windows left out): the stress maps combined into windows that repeat, overlap by one
     key, lie apart or coincide for some queries only, with and without the causal mask."""
@@ -529,6 +529,7 @@ def test_attend_tile_kernel_union_maps(scram, d, grid):
         "random+random": (m["random"], rng.integers(0, nk, m["random"].shape)),
         "two_far+constant": (m["two_far"], m["constant"]),
         "coherent_twice+outliers": (m["coherent"], m["coherent"], m["outliers"]),
+        "four": (m["coherent"], m["outliers"], m["lattice6"], (m["coherent"] + 1) % nk),
         "eight": tuple(m[k] for k in ("coherent", "outliers", "lattice6", "lattice7", "random", "two_far",
                                       "corner0", "corner_last")),
     }
