@@ -257,7 +257,8 @@ __global__ __launch_bounds__(kBlock) void attend_kernel(AttParams p)
 // window-e centres, into the same online softmax state; a slot of pass e is
 // left out when one of the query's windows 0 .. e-1 holds its key, so every
 // key of the union enters once.  Up to four maps take a single pass over the
-// clusters of all their centres instead: each
+// clusters of all their centres instead, five to eight two such passes (the
+// second holding back the keys of the first's windows): each
 // window is kept in the box of its own centre's cluster, less the keys of
 // the query's earlier windows (and of those after the query).
 // (at most 96 VGPRs: five waves per SIMD hide more of the row loads than four; the causal mask's
@@ -317,20 +318,33 @@ attend_tile_kernel(AttParams p)
         qx = static_cast<int>(xx);
         qy = static_cast<int>(yy);
     }
-    // up to four windows: one pass over the clusters of all their centres instead of a pass per window
+    // up to four windows: one pass over the clusters of all their centres instead of a pass per window;
+    // five to eight: two such rounds, the second holding back the keys of the first round's windows
     // (lanes 16 e .. 16 e + 15 cluster window e's centres).  A query keeps the slots of window e in the
     // cluster of that window's centre, less the keys of its windows 0 .. e-1 (and with the causal mask
     // those after the query), so every key of the union enters once; coherent maps walk a third (two
     // windows) to a half (three) fewer blocks
-    constexpr bool JOINT = MK == 2 || MK == 4;
-    constexpr int NJ = JOINT ? MK : 1;
-    int ju[NJ], jv[NJ], jmine[NJ];  // window e's centre and the cluster that holds it (-1: no window e)
+    constexpr bool JOINT = MK == 2 || MK == 4 || MK == 8;
+    constexpr int NJ = JOINT ? (MK < 4 ? MK : 4) : 1;  // windows clustered together: a round
+    constexpr int NW = JOINT ? MK : 1;                 // windows in all (eight: two rounds of four)
+    int ju[NW], jv[NW], jmine[NJ];  // window e's centre; the cluster that holds the round's window e
+    int round = 0;
     TileClusters tc;
-    if constexpr (JOINT) {
-        const int ew = g4 & (NJ - 1);  // the window whose centre this lane clusters
-        int iu = u, iv = v;
+    // the clusters of round r's centres (windows NJ r .. NJ r + NJ - 1)
+    auto joint_round = [&](int r) {
+        if constexpr (JOINT) {
+            const int ew = NJ * r + (g4 & (NJ - 1));  // the window whose centre this lane clusters
+            int iu = u, iv = v;
 #pragma unroll
-        for (int e = 0; e < NJ; ++e) {
+            for (int e = 0; e < NW; ++e) iu = ew == e ? ju[e] : iu, iv = ew == e ? jv[e] : iv;
+            tc = tile_clusters_joint<B, NJ>(valid && ew < p.kappa, iu, iv, lane, p.rc, p.Hk, p.Wk);
+#pragma unroll
+            for (int e = 0; e < NJ; ++e) jmine[e] = __shfl(tc.mine, m + 16 * e);
+        }
+    };
+    if constexpr (JOINT) {
+#pragma unroll
+        for (int e = 0; e < NW; ++e) {
             ju[e] = u, jv[e] = v;  // window 0; a window past kappa repeats it and is not clustered
             if (e > 0 && e < p.kappa) {
                 uint32_t uu, vv;
@@ -338,11 +352,8 @@ attend_tile_kernel(AttParams p)
                        p.div_wk, uu, vv);
                 ju[e] = static_cast<int>(uu), jv[e] = static_cast<int>(vv);
             }
-            iu = ew == e ? ju[e] : iu, iv = ew == e ? jv[e] : iv;
         }
-        tc = tile_clusters_joint<B, NJ>(valid && ew < p.kappa, iu, iv, lane, p.rc, p.Hk, p.Wk);
-#pragma unroll
-        for (int e = 0; e < NJ; ++e) jmine[e] = __shfl(tc.mine, m + 16 * e);
+        joint_round(0);
     } else {
         tc = tile_clusters<B, CAUSAL>(valid, u, v, m, lane, p.rc, p.Hk, p.Wk, qx, qy);
     }
@@ -359,10 +370,10 @@ attend_tile_kernel(AttParams p)
     for (int f = 0; f < kOther; ++f) cu[f] = cv[f] = 0, dw[f] = 1 << 20, xw[f] = 0u;
     // joint pass, per cluster: window e's first row as a box row (jd), its rows less one, cut at the
     // box's last (jn), its columns in the box (jx); bit e of hm: the cluster holds window e's centre
-    int jd[NJ], jn[NJ];
-    uint32_t jx[NJ], hm = 0u;
+    int jd[NW], jn[NW];
+    uint32_t jx[NW], hm = 0u;
 #pragma unroll
-    for (int e = 0; e < NJ; ++e) jd[e] = jn[e] = 0, jx[e] = 0u;
+    for (int e = 0; e < NW; ++e) jd[e] = jn[e] = 0, jx[e] = 0u;
     int jqr = 0;        // causal: the query's row as a box row
     uint32_t jqc = 0u;  // and the box columns up to the query's
 
@@ -473,7 +484,8 @@ attend_tile_kernel(AttParams p)
             bits = 0u;
             uint32_t held = 0u;
 #pragma unroll
-            for (int e = 0; e < NJ; ++e) {
+            for (int e = 0; e < NW; ++e) {
+                if (NW > NJ && e / NJ > round) break;  // the windows of later rounds come later
                 const uint32_t w = tile_window_bits<false>(bx, rr - jd[e], mcl, jn[e], jx[e], jx[e] << bx.bw);
                 bits |= ((hm >> e) & 1u) ? w & ~held : 0u;
                 held |= w;
@@ -554,12 +566,14 @@ attend_tile_kernel(AttParams p)
                 rr = mr;
                 hm = 0u;
 #pragma unroll
-                for (int e = 0; e < NJ; ++e) {
+                for (int e = 0; e < NW; ++e) {
+                    if (NW > NJ && e / NJ > round) break;
                     jd[e] = ju[e] - B - bx.r0;
                     jn[e] = min(2 * B, bx.h - 1 - jd[e]);
                     // no columns for a window wholly below the box (its row count would be negative)
                     jx[e] = jn[e] >= 0 ? tile_col_bits(jv[e] - B - bx.c0, jv[e] + B - bx.c0, bx.bw) : 0u;
-                    hm |= c == jmine[e] ? 1u << e : 0u;
+                    // this round's windows whose centre the cluster holds (earlier rounds' hold back keys)
+                    hm |= (NW == NJ || e / NJ == round) && c == jmine[e % NJ] ? 1u << e : 0u;
                 }
                 in = hm != 0u;
                 if constexpr (CAUSAL) {
@@ -601,8 +615,15 @@ attend_tile_kernel(AttParams p)
             ++c;
             wave_lds_sync();
         }
-        if constexpr (MK == 1 || JOINT) {
+        if constexpr (MK == 1 || (JOINT && NW == NJ)) {
             break;
+        } else if constexpr (JOINT) {
+            // the next round: its centres' clusters; the earlier rounds' windows hold back their keys
+            if (NJ * (round + 1) >= p.kappa) break;
+            ++round;
+            joint_round(round);
+            nclu = tc.nclu, mine = tc.mine;
+            wave_lds_sync();  // the last block's LDS reads come before the next round's writes
         } else {
             if (e + 1 >= p.kappa) break;
             // the next window: its centres' clusters and boxes; window e joins the earlier ones

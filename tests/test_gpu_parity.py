@@ -512,7 +512,7 @@ def test_attend_tile_kernel_maps(scram, d, grid):
                          ids=lambda g: "x".join(map(str, g)))
 def test_attend_tile_kernel_union_maps(scram, d, grid):
     """The matrix-core attend over the union of 2, 3, 4 and 8 windows per query (one pass over the joint
-    clusters of up to 4 windows' centres, else a pass per window; the keys of a
+    clusters of up to 4 windows' centres, two such passes for 5-8; the keys of a
     query's earlier windows left out): the stress maps combined into windows that repeat, overlap by one
     key, lie apart or coincide for some queries only, with and without the causal mask."""
     S, Hq, Wq, Hk, Wk = grid
