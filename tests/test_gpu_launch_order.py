@@ -137,7 +137,7 @@ def test_resumed_and_noalloc_sweeps(scram, variant, case):
 
 def test_attend_outputs(scram, variant, case):
     """The attend on one map (windows 1-9; bf16 with 32 or 64 channels takes the matrix-core kernel for
-    3, 5, 7), causal, and over the union of two and of three maps' windows."""
+    3, 5, 7), causal, and over the union of two, three and eight maps' windows."""
     Q, K, V = case["Q"], case["K"], case["V"]
     log(case["name"], "attend", tuple(Q.shape), Q.dtype)
     J = scram.patchmatch_kappa(Q, K, 3, case["iters"], case["seed"])
@@ -147,6 +147,10 @@ def test_attend_outputs(scram, variant, case):
     for kappa in (2, 3):
         ref, runs = both(variant, lambda: scram.sparse_attend(Q, K, V, J[:kappa], case["window"]))
         same(ref, runs, f"union attend {kappa}")
+    nk = K.shape[1] * K.shape[2]
+    J8 = torch.cat([J, J[:, :, :, torch.arange(Q.shape[2] - 1, -1, -1, device=J.device)], (J[:2] + 1) % nk])
+    ref, runs = both(variant, lambda: scram.sparse_attend(Q, K, V, J8, case["window"]))
+    same(ref, runs, "union attend 8")
     if case["self_grid"]:
         Jc = scram.patchmatch(Q, K, case["iters"], case["seed"], causal=True)
         ref, runs = both(variant, lambda: scram.sparse_attend(Q, K, V, Jc, case["window"], causal=True))
